@@ -1,0 +1,199 @@
+"""Benchmark: the CanonicalMerge render of a LatentFragmentSet on one MI355X.
+
+One step = the whole path over one batch of deliveries: Id of every delivery
+(hash), scores, dedupe + canonical order + offsets, one small device-to-host
+plan copy, output allocation, rotate-and-concatenate render. Inputs are
+resident in HBM before timing starts.
+
+value = merged-cache bytes read + written per step (2 x the bytes of the
+distinct fragments) / step time, in GB/s; merges_per_s = 1 / step time.
+
+Prints one JSON line. `roofline` is for the kernel with the largest share of
+the step (per-kernel HIP events on the launch stream, measured over the timed
+steps); `roofline_render` adds the render kernel against HBM bandwidth.
+`cpu_baseline` times the CPU oracle on a bounded sample of the same workload.
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0                 # MI355X HBM3E
+VALU_PEAK_TOPS = 256 * 64 * 2.4e9 / 1e12  # 256 CUs x 64 lanes x 2.4 GHz, non-packed 32-bit ops
+B2S_OPS_PER_BLOCK = 960                # 10 rounds x 8 G x 12 VALU ops (add3, add, xor, alignbit)
+
+
+def _kernel_source_hash(name: str) -> str:
+    path = os.path.join(ROOT, "paper_2607_01308_amd", "csrc", name)
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def _traffic(kernel: str, source: str, workload: str):
+    """HBM bytes per launch from a committed rocprofv3 counter summary, if it was
+    taken on the current kernel source; otherwise None."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        t = json.load(f)
+    if t.get("source_sha256_16") != _kernel_source_hash(source):
+        return None
+    return t.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(w, frags):
+    """The oracle, unchanged, over the three shortest distinct fragments."""
+    import oracle
+    import synth
+    idx = sorted(range(w.n_distinct), key=lambda i: w.lengths[i])[:3]
+    sample = [oracle.Fragment(*synth.to_numpy_cache(frags[i])) for i in idx]
+    t0 = time.perf_counter()
+    oracle.render_deliveries(sample, w.routing_layer, w.rope_base)
+    dt = time.perf_counter() - t0
+    nbytes = 2 * sum(w.fragment_bytes(i) for i in idx)
+    return {
+        "value": round(nbytes / dt / 1e9, 4),
+        "unit": "GB/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": f"full path (hash, score, order, render) over the 3 shortest distinct fragments "
+                  f"(T={[w.lengths[i] for i in idx]}, {nbytes / 1e9:.2f} GB read+write), "
+                  f"{dt:.1f} s, single-threaded numpy/hashlib",
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="qwen3-4b-large")
+    ap.add_argument("--seed", type=int, default=42)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print(f"bench.py runs on one GPU only (asked for {args.gpus}); the render is a "
+              "single-GPU path and no multi-GPU figure is produced", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import synth
+    import paper_2607_01308_amd as cm
+
+    dev = torch.device("cuda:0")
+    w = synth.workload(args.workload, args.seed)
+    print(f"[bench] generating {w.name}: {w.n_deliveries} deliveries, {w.n_distinct} distinct, "
+          f"{w.merged_tokens} merged tokens", file=sys.stderr, flush=True)
+    frags = synth.make_fragments(w, device=dev)
+    deliveries = synth.make_deliveries(w, frags)
+    batch = cm.FragmentBatch(deliveries)
+    torch.cuda.synchronize()
+
+    def step():
+        return cm.render_deliveries(batch, w.routing_layer, w.rope_base)
+
+    for _ in range(args.warmup):
+        r = step()
+        del r
+    torch.cuda.synchronize()
+    print("[bench] warmup done", file=sys.stderr, flush=True)
+
+    cm.timing_reset()
+    cm.timing_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        r = step()
+        del r
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    cm.timing_enable(False)
+    per_kernel = {}
+    for k in cm.KERNELS:
+        ms, n = cm.timing_query(k)
+        if n:
+            per_kernel[k] = {"total_ms": ms, "launches": n, "avg_ms": ms / n}
+    cm.timing_reset()
+
+    # steps 2-5 on the ingested set (ids already computed at Ingest, Alg. 2)
+    S = cm.LatentFragmentSet()
+    S.ingest_many(deliveries)
+    for _ in range(2):
+        S.render(w.routing_layer, w.rope_base)
+    torch.cuda.synchronize()
+    t2 = time.perf_counter()
+    for _ in range(args.steps):
+        r = S.render(w.routing_layer, w.rope_base)
+        del r
+    torch.cuda.synchronize()
+    t3 = time.perf_counter()
+
+    ms_step = (t1 - t0) / args.steps * 1e3
+    ms_render_set = (t3 - t2) / args.steps * 1e3
+    render_bytes = w.render_bytes
+    value = render_bytes / (ms_step / 1e3) / 1e9
+
+    # dominant kernel and its roofline
+    dom = max(per_kernel, key=lambda k: per_kernel[k]["total_ms"] / args.steps)
+    delivered = w.delivery_bytes
+    hash_blocks = delivered // 64
+    rooflines = {}
+    if "hash_leaf" in per_kernel:
+        avg = per_kernel["hash_leaf"]["total_ms"] / args.steps / 1e3
+        ach = B2S_OPS_PER_BLOCK * hash_blocks / avg / 1e12
+        rooflines["hash_leaf"] = {"bound": "alu", "achieved": round(ach, 3),
+                                  "peak": round(VALU_PEAK_TOPS, 3), "unit": "Tops/s",
+                                  "frac": round(ach / VALU_PEAK_TOPS, 4),
+                                  "traffic": _traffic("hash_leaf", "hash.hip", w.name),
+                                  "input_GBps": round(delivered / avg / 1e9, 1)}
+    if "render" in per_kernel:
+        avg = per_kernel["render"]["total_ms"] / args.steps / 1e3
+        ach = render_bytes / avg / 1e9
+        rooflines["render"] = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBPS,
+                               "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBPS, 4),
+                               "traffic": _traffic("render", "render.hip", w.name)}
+    out = {
+        "metric": "merged-cache render GB/s (read+write) and % of MI355X HBM peak; merges/s",
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if w.dtype == "bfloat16" else "f32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "deliveries": w.n_deliveries, "distinct": w.n_distinct,
+                   "merged_tokens": w.merged_tokens, "layers": w.L, "kv_heads": w.H,
+                   "head_dim": w.d, "routing_layer": w.routing_layer, "rope_base": w.rope_base,
+                   "render_bytes": render_bytes, "delivery_bytes": delivered,
+                   "parallelism": "single GPU"},
+        "pct_hbm_peak": round(100 * value / HBM_PEAK_GBPS, 2),
+        "merges_per_s": round(1e3 / ms_step, 3),
+        "roofline": dict(rooflines.get(dom, {}), kernel=dom) if dom in rooflines else None,
+        "roofline_render": rooflines.get("render"),
+        "kernels_ms_per_step": {k: round(v["total_ms"] / args.steps, 4) for k, v in per_kernel.items()},
+        "render_set_ms": round(ms_render_set, 4),
+        "render_set_GBps": round(render_bytes / (ms_render_set / 1e3) / 1e9, 1),
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(w, frags)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,195 @@
+/*
+ * cmerge.h — C ABI of libcmerge: the CanonicalMerge render of a LatentFragmentSet
+ * on AMD Instinct MI355X (gfx950).
+ *
+ * Paper: "Cache Merging as a Convergent Replicated State for Multi-Agent Latent
+ * Reasoning" (arXiv 2607.01308). The four calls below are the steps of Alg. 1
+ * (CanonicalMerge) run inside Render of Alg. 2 (LatentFragmentSet):
+ *   cm_fragment_hash    Id of Alg. 2 / the hash tiebreak h_i of §4.3
+ *   cm_fragment_knorm   the mean K-norm score rho_i of Eq. (3)
+ *   cm_canonical_order  Ingest dedupe (Eq. (5)) + argsort(-rho, -h) of Alg. 1
+ *                       + the offsets s of §4.2
+ *   cm_render_merge     Eq. (1)-(2): K of slot i rotated by R(s_i), V copied,
+ *                       both concatenated along the sequence axis
+ *
+ * Conventions
+ *   - Every function returns int32_t: CM_OK (0) or a negative cm_status. No
+ *     exception crosses the ABI. cm_last_error() returns a thread-local message
+ *     for the last failing call on the calling thread.
+ *   - Device work is enqueued on `stream` (a hipStream_t passed as void*; NULL is
+ *     the null stream) and the call returns without waiting for it. Argument
+ *     checks happen on the host before anything is enqueued; a call that returns
+ *     an error has enqueued nothing.
+ *   - All buffers are owned by the caller. The library allocates no device
+ *     memory: calls that need scratch take a workspace of at least
+ *     cm_workspace_size() bytes (device memory, 256-byte aligned). Buffers must
+ *     stay valid until the enqueued work has finished. Calls that share a
+ *     workspace must be ordered (same stream, or synchronised).
+ *   - Tensors: a fragment is a HuggingFace legacy KV cache: per layer l a K and a
+ *     V tensor of shape [1, H, T, d], contiguous, row-major, dtype bf16 or fp32.
+ *     K is stored post-RoPE at local positions 0..T-1 (§4.1). Every tensor
+ *     address must be 16-byte aligned.
+ *   - Supported shapes: d a power of two with d * element_bytes in [64, 1024];
+ *     1 <= n <= CM_MAX_FRAGMENTS; L, H >= 1; T >= 1.
+ */
+#ifndef CMERGE_H
+#define CMERGE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define CM_ABI_VERSION 1
+#define CM_MAX_FRAGMENTS 1024
+
+typedef enum {
+  CM_OK = 0,
+  CM_EINVAL = -1,      /* NULL pointer, count or index out of range, misaligned buffer */
+  CM_ESHAPE = -2,      /* unsupported or inconsistent shape; T_out != sum of slot lengths */
+  CM_EDTYPE = -3,      /* unsupported dtype */
+  CM_ENONFINITE = -4,  /* a score is NaN or infinite (reported through the plan) */
+  CM_EHIP = -5,        /* a HIP runtime call failed; the message carries hipGetErrorString */
+  CM_EWORKSPACE = -6,  /* workspace NULL, misaligned or smaller than cm_workspace_size() */
+} cm_status;
+
+typedef enum { CM_F32 = 0, CM_BF16 = 1 } cm_dtype;
+
+/* RoPE pairing (§4.1 leaves it open): CM_ROPE_HALF pairs (j, j + d/2), the
+ * HuggingFace Qwen3 layout and the default. CM_ROPE_INTERLEAVED pairs (2j, 2j+1). */
+typedef enum { CM_ROPE_HALF = 0, CM_ROPE_INTERLEAVED = 1 } cm_rope_style;
+
+/* A set of n fragments (deliveries; byte-identical duplicates allowed) sharing
+ * L, H, d and dtype.
+ * table_host: host memory, n rows of (1 + 2L) int64:
+ *     row i = { T_i, addr(K_i^0), addr(V_i^0), ..., addr(K_i^{L-1}), addr(V_i^{L-1}) }
+ *     with device addresses of the [1, H, T_i, d] tensors.
+ * table_dev: device memory holding the same n * (1 + 2L) values (the kernels read
+ *     it; the host validates table_host). The caller keeps the two identical. */
+typedef struct {
+  int32_t n;
+  int32_t L;
+  int32_t H;
+  int32_t d;
+  int32_t dtype;     /* cm_dtype */
+  int32_t reserved;  /* must be 0 */
+  const int64_t* table_host;
+  const int64_t* table_dev;
+} cm_fragset;
+
+/* RoPE of the model: theta_j = base^(-2j/d) (§4.1). */
+typedef struct {
+  double base;
+  int32_t style;     /* cm_rope_style */
+  int32_t reserved;  /* must be 0 */
+} cm_rope;
+
+/* ---------------------------------------------------------------- plan layout
+ * A plan is an int64 array of cm_plan_elems(n) entries, written on the device by
+ * cm_canonical_order and read by cm_render_merge:
+ *   [0]                 status: CM_OK, or CM_ENONFINITE if a score is not finite
+ *   [1]                 n (deliveries)
+ *   [2]                 n_unique: distinct fragments = slots of the merged cache
+ *   [3]                 T_out: merged length, the sum of the slot lengths
+ *   [4 + s]             delivery index rendered in slot s (s < n_unique)
+ *   [4 + n + s]         offset s_pi(s) of slot s (§4.2)
+ *   [4 + 2n + s]        length of slot s
+ *   [4 + 3n + i]        slot holding the content of delivery i (duplicates point
+ *                       at the slot of their first arrival)
+ * Entries for s >= n_unique are -1. */
+#define CM_PLAN_STATUS 0
+#define CM_PLAN_N 1
+#define CM_PLAN_NUNIQUE 2
+#define CM_PLAN_TOUT 3
+#define CM_PLAN_HEADER 4
+
+/* ---------------------------------------------------------------- utilities */
+
+int32_t cm_version(void);                    /* CM_ABI_VERSION */
+const char* cm_last_error(void);             /* "" when the last call succeeded */
+const char* cm_status_string(int32_t status);
+size_t cm_plan_elems(int32_t n);             /* 4 + 4n */
+
+/* Workspace bytes that every call below needs for this set (the maximum over
+ * the calls). The set is validated (host table only). */
+int32_t cm_workspace_size(const cm_fragset* set, size_t* bytes_out);
+
+/* ---------------------------------------------------------------- step 1
+ * Id of Alg. 2 (content address; also the hash tiebreak of §4.3): for every
+ * fragment, a 32-byte digest of its shapes, dtype and the raw bytes of
+ * K^0, V^0, ..., K^{L-1}, V^{L-1} in that order. Function: per tensor a BLAKE2s-256
+ * (RFC 7693) binary tree over 4 KiB leaves (fanout 2, depth 255, leaf 4096,
+ * inner 32; leaf k: node_offset k, depth 0; parent j at level v: node_offset j,
+ * depth v, children 2j and 2j+1; last_node on the last node of each level; an
+ * unpaired last node is carried up unchanged); then a sequential BLAKE2s-256 of
+ * a 64-byte header (magic "CMFRAG01", u32 dtype code 0=fp32 1=bf16, u32 element
+ * bytes, u32 L, u32 batch=1, u32 H, u64 T, u32 d, zero pad; little-endian)
+ * followed by the 2L tensor roots.
+ * digests_dev: device, n * 32 bytes, written in delivery order. */
+int32_t cm_fragment_hash(const cm_fragset* set, uint8_t* digests_dev,
+                         void* workspace, size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------- step 2
+ * Score of Eq. (3) / Alg. 1: for every fragment i,
+ *   keys_dev[i] = S_i = sum over heads h and rows r in [T_i - tail_len, T_i) of
+ *                 || K_i^{(routing_layer)}[0, h, r, :] ||_2
+ * and rho_i = S_i / (H * tail_len). tail_len is T* = min_j T_j of the set.
+ * Arithmetic (identical on every device and in the CPU oracle): fp64; squares
+ * exact; each row sum by a level-wise adjacent-pair tree over d; correctly
+ * rounded sqrt; the H * tail_len row norms, flattened (h, r) row-major and
+ * zero-padded to a power of two, summed by the same kind of tree.
+ * routing_layer: 0-based, in [0, L). tail_len in [1, min_i T_i].
+ * keys_dev: device, n doubles. Non-finite inputs give non-finite keys (reported
+ * by cm_canonical_order). */
+int32_t cm_fragment_knorm(const cm_fragset* set, int32_t routing_layer, int64_t tail_len,
+                          double* keys_dev, void* workspace, size_t workspace_bytes,
+                          void* stream);
+
+/* ---------------------------------------------------------------- step 3
+ * Ingest dedupe (Alg. 2; Eq. (5)) and canonical order (Alg. 1): deliveries with
+ * equal digests are one fragment (the first arrival is kept); the distinct
+ * fragments are sorted by descending key, equal keys by descending digest read
+ * as a 256-bit big-endian unsigned integer; offsets are the exclusive prefix sum
+ * of the lengths in that order (§4.2). Runs on the device in one workgroup.
+ * keys_dev, digests_dev: outputs of steps 1-2 (device). plan_dev: device,
+ * cm_plan_elems(n) int64 (layout above). A non-finite key sets plan status
+ * CM_ENONFINITE; the call itself still returns CM_OK. */
+int32_t cm_canonical_order(const cm_fragset* set, const double* keys_dev,
+                           const uint8_t* digests_dev, int64_t* plan_dev, void* stream);
+
+/* ---------------------------------------------------------------- steps 4-5
+ * Eq. (1)-(2) with pi = the plan's slot order: for every layer l and head h,
+ *   out K rows [s, s + T) = R(s) K_slot  (rotation in fp64, rounded to nearest
+ *                                          even in the storage dtype; s = 0 is a
+ *                                          byte copy)
+ *   out V rows [s, s + T) = V_slot       (byte copy)
+ * R(s) rotates pair (x1, x2) by s * theta_j: (x1 c - x2 sn, x2 c + x1 sn).
+ * plan_dev: the plan on the device; plan_host: the same plan copied to the host
+ * (the host validates it and sizes the launch from it).
+ * out_dev: device, 16-byte aligned, 2 * L * H * T_out * d elements laid out as
+ * [L][2][1][H][T_out][d]: layer l's K is the contiguous [1, H, T_out, d] block at
+ * element offset (2l) * H * T_out * d and its V the block after it.
+ * T_out must equal the plan's T_out. The plan status must be CM_OK. */
+int32_t cm_render_merge(const cm_fragset* set, const int64_t* plan_dev,
+                        const int64_t* plan_host, const cm_rope* rope, void* out_dev,
+                        int64_t T_out, void* workspace, size_t workspace_bytes,
+                        void* stream);
+
+/* ---------------------------------------------------------------- timing
+ * Optional per-kernel timing with HIP events recorded on the launch stream
+ * around every kernel this library enqueues (off by default; a process-wide
+ * switch). cm_timing_query waits for the recorded events, adds their durations
+ * to the per-kernel totals and returns the total milliseconds and launch count
+ * for one kernel name ("hash_leaf", "hash_parent", "hash_final", "knorm_rows",
+ * "knorm_tree", "order", "render_prep", "render"). */
+int32_t cm_timing_enable(int32_t on);
+int32_t cm_timing_reset(void);
+int32_t cm_timing_query(const char* kernel, double* total_ms, int64_t* launches);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CMERGE_H */

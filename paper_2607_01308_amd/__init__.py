@@ -1,0 +1,25 @@
+"""MI355X-native CanonicalMerge render of a LatentFragmentSet (arXiv 2607.01308,
+§4.3-§4.5, Alg. 1-2): HIP kernels for gfx950 behind the C ABI of
+include/cmerge.h, with a thin torch binding."""
+
+from ._cabi import CmError, LIB_PATH  # noqa: F401
+from .binding import (  # noqa: F401
+    KERNELS,
+    FragmentBatch,
+    canonical_order,
+    fragment_hash,
+    fragment_knorm,
+    plan_elems,
+    render_merge,
+    timing_enable,
+    timing_query,
+    timing_reset,
+    workspace_size,
+)
+from .fragset import (  # noqa: F401
+    LatentFragmentSet,
+    RenderResult,
+    fragment_ids,
+    release_workspace,
+    render_deliveries,
+)

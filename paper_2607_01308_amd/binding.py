@@ -1,0 +1,145 @@
+"""Python binding of the C ABI (include/cmerge.h), one function per entry point
+with the same name. Argument marshalling only: every step runs in the HIP
+kernels of libcmerge.so; torch provides device memory and streams."""
+
+from __future__ import annotations
+
+import ctypes
+from typing import Sequence
+
+import numpy as np
+import torch
+
+from . import _cabi as C
+
+_DTYPES = {torch.bfloat16: C.CM_BF16, torch.float32: C.CM_F32}
+_STYLES = {"half": C.CM_ROPE_HALF, "interleaved": C.CM_ROPE_INTERLEAVED}
+
+
+def _ptr(t: torch.Tensor) -> ctypes.c_void_p:
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream, device) -> ctypes.c_void_p:
+    s = stream if stream is not None else torch.cuda.current_stream(device)
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+class FragmentBatch:
+    """A list of fragments (legacy KV caches on one GPU) described for the C ABI:
+    host and device copies of the table {T_i, addr(K_i^0), addr(V_i^0), ...}.
+    Holds references to the tensors so their addresses stay valid."""
+
+    def __init__(self, caches: Sequence, device=None):
+        if len(caches) == 0:
+            raise ValueError("a fragment set needs at least one fragment")
+        first_k = caches[0][0][0]
+        self.L = len(caches[0])
+        _, self.H, _, self.d = first_k.shape
+        self.torch_dtype = first_k.dtype
+        if self.torch_dtype not in _DTYPES:
+            raise TypeError(f"unsupported dtype {self.torch_dtype} (bfloat16 or float32)")
+        self.device = torch.device(device) if device is not None else first_k.device
+        if self.device.type != "cuda":
+            raise ValueError("fragments must live on a GPU")
+        rows = []
+        for i, cache in enumerate(caches):
+            if len(cache) != self.L:
+                raise ValueError(f"fragment {i} has {len(cache)} layers, expected {self.L}")
+            T = cache[0][0].shape[2]
+            row = [T]
+            for l, (K, V) in enumerate(cache):
+                for x in (K, V):
+                    if (x.dim() != 4 or x.shape[0] != 1 or x.shape[1] != self.H or x.shape[2] != T
+                            or x.shape[3] != self.d):
+                        raise ValueError(f"fragment {i} layer {l}: shape {tuple(x.shape)} is not "
+                                         f"[1, {self.H}, {T}, {self.d}]")
+                    if x.dtype != self.torch_dtype or x.device != self.device:
+                        raise ValueError(f"fragment {i} layer {l}: dtype/device differ from the set")
+                    if not x.is_contiguous():
+                        raise ValueError(f"fragment {i} layer {l}: tensor is not contiguous")
+                    row.append(x.data_ptr())
+            rows.append(row)
+        self.caches = list(caches)
+        self.table_host = np.ascontiguousarray(np.array(rows, dtype=np.int64))
+        self.table_dev = torch.from_numpy(self.table_host).to(self.device)
+        self.lengths = [int(r[0]) for r in rows]
+        self.struct = C.CmFragset(
+            n=len(caches), L=self.L, H=self.H, d=self.d, dtype=_DTYPES[self.torch_dtype],
+            reserved=0, table_host=self.table_host.ctypes.data, table_dev=self.table_dev.data_ptr())
+
+    @property
+    def n(self) -> int:
+        return len(self.caches)
+
+    @property
+    def elem_bytes(self) -> int:
+        return 2 if self.torch_dtype == torch.bfloat16 else 4
+
+    def fragment_bytes(self, i: int) -> int:
+        return 2 * self.L * self.H * self.lengths[i] * self.d * self.elem_bytes
+
+
+def workspace_size(batch: FragmentBatch) -> int:
+    out = ctypes.c_size_t(0)
+    C.check(C.lib().cm_workspace_size(ctypes.byref(batch.struct), ctypes.byref(out)),
+            "cm_workspace_size")
+    return int(out.value)
+
+
+def fragment_hash(batch: FragmentBatch, digests: torch.Tensor, workspace: torch.Tensor,
+                  stream=None) -> None:
+    C.check(C.lib().cm_fragment_hash(ctypes.byref(batch.struct), _ptr(digests), _ptr(workspace),
+                                     workspace.numel() * workspace.element_size(),
+                                     _stream(stream, batch.device)), "cm_fragment_hash")
+
+
+def fragment_knorm(batch: FragmentBatch, routing_layer: int, tail_len: int, keys: torch.Tensor,
+                   workspace: torch.Tensor, stream=None) -> None:
+    C.check(C.lib().cm_fragment_knorm(ctypes.byref(batch.struct), routing_layer, tail_len,
+                                      _ptr(keys), _ptr(workspace),
+                                      workspace.numel() * workspace.element_size(),
+                                      _stream(stream, batch.device)), "cm_fragment_knorm")
+
+
+def canonical_order(batch: FragmentBatch, keys: torch.Tensor, digests: torch.Tensor,
+                    plan: torch.Tensor, stream=None) -> None:
+    C.check(C.lib().cm_canonical_order(ctypes.byref(batch.struct), _ptr(keys), _ptr(digests),
+                                       _ptr(plan), _stream(stream, batch.device)),
+            "cm_canonical_order")
+
+
+def render_merge(batch: FragmentBatch, plan_dev: torch.Tensor, plan_host: np.ndarray,
+                 rope_base: float, style: str, out: torch.Tensor, T_out: int,
+                 workspace: torch.Tensor, stream=None) -> None:
+    plan_host = np.ascontiguousarray(plan_host, dtype=np.int64)
+    rope = C.CmRope(base=float(rope_base), style=_STYLES[style], reserved=0)
+    C.check(C.lib().cm_render_merge(ctypes.byref(batch.struct), _ptr(plan_dev),
+                                    plan_host.ctypes.data_as(ctypes.c_void_p), ctypes.byref(rope),
+                                    _ptr(out), T_out, _ptr(workspace),
+                                    workspace.numel() * workspace.element_size(),
+                                    _stream(stream, batch.device)), "cm_render_merge")
+
+
+def plan_elems(n: int) -> int:
+    return int(C.lib().cm_plan_elems(n))
+
+
+def timing_enable(on: bool) -> None:
+    C.check(C.lib().cm_timing_enable(1 if on else 0), "cm_timing_enable")
+
+
+def timing_reset() -> None:
+    C.check(C.lib().cm_timing_reset(), "cm_timing_reset")
+
+
+def timing_query(kernel: str):
+    ms = ctypes.c_double(0.0)
+    cnt = ctypes.c_int64(0)
+    C.check(C.lib().cm_timing_query(kernel.encode(), ctypes.byref(ms), ctypes.byref(cnt)),
+            "cm_timing_query")
+    return float(ms.value), int(cnt.value)
+
+
+KERNELS = ("hash_prep", "hash_leaf", "hash_parent", "hash_final", "knorm_rows", "knorm_tree",
+           "order", "render_prep", "render")

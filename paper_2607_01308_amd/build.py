@@ -1,0 +1,70 @@
+"""Build libcmerge.so (the HIP kernels + C ABI) in-tree for gfx950 with hipcc.
+
+Also builds tests/native/libcm_hostcheck.so, a CPU-side harness the tests use
+to run the library's BLAKE2s code on the host."""
+
+from __future__ import annotations
+
+import concurrent.futures as cf
+import os
+import shutil
+import subprocess
+import sys
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(PKG)
+CSRC = os.path.join(PKG, "csrc")
+INCLUDE = os.path.join(ROOT, "include")
+BUILD = os.path.join(ROOT, "_build")
+LIB = os.path.join(PKG, "libcmerge.so")
+HOSTCHECK_SRC = os.path.join(ROOT, "tests", "native", "hostcheck.hip")
+HOSTCHECK_LIB = os.path.join(ROOT, "tests", "native", "libcm_hostcheck.so")
+
+ARCH = "gfx950"
+SOURCES = ["api.cpp", "hash.hip", "knorm.hip", "order.hip", "render.hip"]
+COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function",
+          f"-I{INCLUDE}", f"-I{CSRC}"]
+DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+
+
+def _hipcc() -> str:
+    for c in (os.environ.get("HIPCC"), "/opt/rocm/bin/hipcc", shutil.which("hipcc")):
+        if c and os.path.exists(c):
+            return c
+    raise RuntimeError("hipcc not found (ROCm is required to build libcmerge)")
+
+
+def _run(cmd, verbose):
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    out = "\n".join(l for l in (r.stdout + r.stderr).splitlines()
+                    if "packed-fp32-ops" not in l)
+    if r.returncode != 0:
+        raise RuntimeError(f"build step failed: {' '.join(cmd)}\n{out}")
+    if verbose and out.strip():
+        print(out, flush=True)
+
+
+def build(verbose: bool = False) -> str:
+    hipcc = _hipcc()
+    os.makedirs(BUILD, exist_ok=True)
+    objs, jobs = [], []
+    for src in SOURCES:
+        obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
+        objs.append(obj)
+        lang = ["-x", "hip"] + DEVICE if src.endswith(".hip") else []
+        jobs.append([hipcc, *COMMON, *lang, "-c", os.path.join(CSRC, src), "-o", obj])
+    jobs.append([hipcc, *COMMON, "-x", "hip", *DEVICE, "-shared", HOSTCHECK_SRC,
+                 "-o", HOSTCHECK_LIB + ".tmp"])
+    with cf.ThreadPoolExecutor(max_workers=min(len(jobs), os.cpu_count() or 4)) as ex:
+        list(ex.map(lambda c: _run(c, verbose), jobs))
+    tmp = LIB + ".tmp"
+    _run([hipcc, *DEVICE, "-shared", "-fPIC", *objs, "-o", tmp], verbose)
+    os.replace(tmp, LIB)
+    os.replace(HOSTCHECK_LIB + ".tmp", HOSTCHECK_LIB)
+    return LIB
+
+
+if __name__ == "__main__":
+    print(build(verbose="-v" in sys.argv))

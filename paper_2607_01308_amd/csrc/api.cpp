@@ -1,0 +1,325 @@
+// C ABI of libcmerge (include/cmerge.h): argument validation on the host, workspace
+// sizing, error reporting and the optional per-kernel event timing. Every check
+// runs before anything is enqueued, so a failing call leaves the stream untouched.
+#include <atomic>
+#include <cmath>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "cmerge.h"
+#include "internal.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+int32_t fail(int32_t code, const std::string& msg) {
+  g_err = msg;
+  return code;
+}
+
+int32_t fail_hip(hipError_t e, const char* where) {
+  return fail(CM_EHIP, std::string(where) + ": " + hipGetErrorName(e) + ": " + hipGetErrorString(e));
+}
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+bool is_pow2(int64_t x) { return x > 0 && (x & (x - 1)) == 0; }
+
+int32_t check_set(const cm_fragset* set, cm::SetDesc* out) {
+  if (!set) return fail(CM_EINVAL, "set is NULL");
+  if (set->n < 1 || set->n > CM_MAX_FRAGMENTS)
+    return fail(CM_EINVAL, "n must be in [1, " + std::to_string(CM_MAX_FRAGMENTS) + "], got " +
+                               std::to_string(set->n));
+  if (set->L < 1 || set->H < 1) return fail(CM_EINVAL, "L and H must be >= 1");
+  if ((int64_t)2 * set->L * set->H > 65535)
+    return fail(CM_ESHAPE, "2 * L * H must be <= 65535");
+  int esize = 0;
+  if (set->dtype == CM_F32) esize = 4;
+  else if (set->dtype == CM_BF16) esize = 2;
+  else return fail(CM_EDTYPE, "dtype must be CM_F32 or CM_BF16, got " + std::to_string(set->dtype));
+  const int64_t row_bytes = (int64_t)set->d * esize;
+  if (!is_pow2(set->d) || row_bytes < 64 || row_bytes > 1024)
+    return fail(CM_ESHAPE, "d must be a power of two with d * element_bytes in [64, 1024], got d=" +
+                               std::to_string(set->d));
+  if (set->reserved != 0) return fail(CM_EINVAL, "reserved field must be 0");
+  if (!set->table_host || !set->table_dev) return fail(CM_EINVAL, "fragment tables are NULL");
+  if (!aligned(set->table_dev, 8)) return fail(CM_EINVAL, "table_dev must be 8-byte aligned");
+  const int64_t stride = 1 + 2 * (int64_t)set->L;
+  for (int i = 0; i < set->n; ++i) {
+    const int64_t* row = set->table_host + (int64_t)i * stride;
+    const int64_t T = row[0];
+    if (T < 1) return fail(CM_EINVAL, "fragment " + std::to_string(i) + " has T < 1");
+    if (T > ((int64_t)1 << 40) / ((int64_t)set->H * row_bytes))
+      return fail(CM_ESHAPE, "fragment " + std::to_string(i) + " tensor exceeds 1 TiB");
+    for (int64_t t = 1; t < stride; ++t) {
+      const uintptr_t a = (uintptr_t)row[t];
+      if (a == 0 || (a & 15) != 0)
+        return fail(CM_EINVAL, "fragment " + std::to_string(i) + " tensor " + std::to_string(t - 1) +
+                                   " address is NULL or not 16-byte aligned");
+    }
+  }
+  out->n = set->n;
+  out->L = set->L;
+  out->H = set->H;
+  out->d = set->d;
+  out->dtype = set->dtype;
+  out->esize = esize;
+  out->stride = stride;
+  out->row_bytes = row_bytes;
+  out->table_dev = set->table_dev;
+  out->table_host = set->table_host;
+  return CM_OK;
+}
+
+int32_t check_ws(void* ws, size_t ws_bytes, size_t need) {
+  if (need == 0) return CM_OK;
+  if (!ws) return fail(CM_EWORKSPACE, "workspace is NULL");
+  if (!aligned(ws, cm::kWsAlign)) return fail(CM_EWORKSPACE, "workspace must be 256-byte aligned");
+  if (ws_bytes < need)
+    return fail(CM_EWORKSPACE, "workspace too small: need " + std::to_string(need) + " bytes, got " +
+                                   std::to_string(ws_bytes));
+  return CM_OK;
+}
+
+int64_t min_T(const cm::SetDesc& s) {
+  int64_t m = s.T(0);
+  for (int i = 1; i < s.n; ++i) m = s.T(i) < m ? s.T(i) : m;
+  return m;
+}
+
+// ------------------------------------------------------------------ timing registry
+const char* const kKernelNames[cm::K_COUNT] = {"hash_prep",  "hash_leaf",  "hash_parent",
+                                               "hash_final", "knorm_rows", "knorm_tree",
+                                               "order",      "render_prep", "render"};
+std::atomic<bool> g_timing{false};
+std::mutex g_tmu;
+struct Pending {
+  int id;
+  hipEvent_t a, b;
+};
+std::vector<Pending> g_pending;
+std::vector<hipEvent_t> g_pool;
+double g_total_ms[cm::K_COUNT];
+int64_t g_count[cm::K_COUNT];
+
+hipEvent_t take_event() {
+  {
+    std::lock_guard<std::mutex> lk(g_tmu);
+    if (!g_pool.empty()) {
+      hipEvent_t e = g_pool.back();
+      g_pool.pop_back();
+      return e;
+    }
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+hipError_t drain_pending() {
+  std::lock_guard<std::mutex> lk(g_tmu);
+  hipError_t first = hipSuccess;
+  for (const Pending& p : g_pending) {
+    float ms = 0.f;
+    hipError_t e = hipEventSynchronize(p.b);
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, p.a, p.b);
+    if (e == hipSuccess) {
+      g_total_ms[p.id] += ms;
+      g_count[p.id] += 1;
+    } else if (first == hipSuccess) {
+      first = e;
+    }
+    g_pool.push_back(p.a);
+    g_pool.push_back(p.b);
+  }
+  g_pending.clear();
+  return first;
+}
+
+}  // namespace
+
+namespace cm {
+
+ScopedTiming::ScopedTiming(int kernel_id, hipStream_t stream) : id_(kernel_id), stream_(stream) {
+  if (!g_timing.load(std::memory_order_relaxed)) return;
+  start_ = take_event();
+  if (start_ && hipEventRecord(start_, stream_) != hipSuccess) start_ = nullptr;
+}
+
+ScopedTiming::~ScopedTiming() {
+  if (!start_) return;
+  hipEvent_t end = take_event();
+  if (!end || hipEventRecord(end, stream_) != hipSuccess) return;
+  std::lock_guard<std::mutex> lk(g_tmu);
+  g_pending.push_back({id_, start_, end});
+}
+
+}  // namespace cm
+
+extern "C" {
+
+int32_t cm_version(void) { return CM_ABI_VERSION; }
+
+const char* cm_last_error(void) { return g_err.c_str(); }
+
+const char* cm_status_string(int32_t status) {
+  switch (status) {
+    case CM_OK: return "CM_OK";
+    case CM_EINVAL: return "CM_EINVAL";
+    case CM_ESHAPE: return "CM_ESHAPE";
+    case CM_EDTYPE: return "CM_EDTYPE";
+    case CM_ENONFINITE: return "CM_ENONFINITE";
+    case CM_EHIP: return "CM_EHIP";
+    case CM_EWORKSPACE: return "CM_EWORKSPACE";
+    default: return "CM_UNKNOWN";
+  }
+}
+
+size_t cm_plan_elems(int32_t n) { return n < 0 ? 0 : (size_t)CM_PLAN_HEADER + 4 * (size_t)n; }
+
+int32_t cm_workspace_size(const cm_fragset* set, size_t* bytes_out) {
+  g_err.clear();
+  cm::SetDesc s;
+  int32_t st = check_set(set, &s);
+  if (st != CM_OK) return st;
+  if (!bytes_out) return fail(CM_EINVAL, "bytes_out is NULL");
+  size_t need = cm::hash_layout(s).bytes;
+  const size_t kn = cm::knorm_max_bytes(s);
+  const size_t rn = cm::render_layout(s).bytes;
+  need = kn > need ? kn : need;
+  need = rn > need ? rn : need;
+  *bytes_out = need;
+  return CM_OK;
+}
+
+int32_t cm_fragment_hash(const cm_fragset* set, uint8_t* digests_dev, void* workspace,
+                         size_t workspace_bytes, void* stream) {
+  g_err.clear();
+  cm::SetDesc s;
+  int32_t st = check_set(set, &s);
+  if (st != CM_OK) return st;
+  if (!digests_dev || !aligned(digests_dev, 16))
+    return fail(CM_EINVAL, "digests_dev is NULL or not 16-byte aligned");
+  const cm::HashLayout lay = cm::hash_layout(s);
+  if ((st = check_ws(workspace, workspace_bytes, lay.bytes)) != CM_OK) return st;
+  hipError_t e = cm::launch_hash(s, lay, digests_dev, static_cast<uint8_t*>(workspace),
+                                 static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? CM_OK : fail_hip(e, "cm_fragment_hash");
+}
+
+int32_t cm_fragment_knorm(const cm_fragset* set, int32_t routing_layer, int64_t tail_len,
+                          double* keys_dev, void* workspace, size_t workspace_bytes,
+                          void* stream) {
+  g_err.clear();
+  cm::SetDesc s;
+  int32_t st = check_set(set, &s);
+  if (st != CM_OK) return st;
+  if (routing_layer < 0 || routing_layer >= s.L)
+    return fail(CM_EINVAL, "routing_layer must be in [0, L), got " + std::to_string(routing_layer));
+  const int64_t tmin = min_T(s);
+  if (tail_len < 1 || tail_len > tmin)
+    return fail(CM_EINVAL, "tail_len must be in [1, min T] = [1, " + std::to_string(tmin) + "], got " +
+                               std::to_string(tail_len));
+  if (!keys_dev || !aligned(keys_dev, 8))
+    return fail(CM_EINVAL, "keys_dev is NULL or not 8-byte aligned");
+  const cm::KnormLayout lay = cm::knorm_layout(s, tail_len);
+  if ((st = check_ws(workspace, workspace_bytes, lay.bytes)) != CM_OK) return st;
+  hipError_t e = cm::launch_knorm(s, lay, routing_layer, tail_len, keys_dev,
+                                  static_cast<uint8_t*>(workspace), static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? CM_OK : fail_hip(e, "cm_fragment_knorm");
+}
+
+int32_t cm_canonical_order(const cm_fragset* set, const double* keys_dev,
+                           const uint8_t* digests_dev, int64_t* plan_dev, void* stream) {
+  g_err.clear();
+  cm::SetDesc s;
+  int32_t st = check_set(set, &s);
+  if (st != CM_OK) return st;
+  if (!keys_dev || !aligned(keys_dev, 8)) return fail(CM_EINVAL, "keys_dev is NULL or misaligned");
+  if (!digests_dev || !aligned(digests_dev, 4))
+    return fail(CM_EINVAL, "digests_dev is NULL or misaligned");
+  if (!plan_dev || !aligned(plan_dev, 8)) return fail(CM_EINVAL, "plan_dev is NULL or misaligned");
+  hipError_t e = cm::launch_order(s, keys_dev, digests_dev, plan_dev, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? CM_OK : fail_hip(e, "cm_canonical_order");
+}
+
+int32_t cm_render_merge(const cm_fragset* set, const int64_t* plan_dev, const int64_t* plan_host,
+                        const cm_rope* rope, void* out_dev, int64_t T_out, void* workspace,
+                        size_t workspace_bytes, void* stream) {
+  g_err.clear();
+  cm::SetDesc s;
+  int32_t st = check_set(set, &s);
+  if (st != CM_OK) return st;
+  if (!rope) return fail(CM_EINVAL, "rope is NULL");
+  if (!std::isfinite(rope->base) || rope->base <= 0.0)
+    return fail(CM_EINVAL, "rope base must be finite and > 0");
+  if (rope->style != CM_ROPE_HALF && rope->style != CM_ROPE_INTERLEAVED)
+    return fail(CM_EINVAL, "rope style must be CM_ROPE_HALF or CM_ROPE_INTERLEAVED");
+  if (rope->reserved != 0) return fail(CM_EINVAL, "rope reserved field must be 0");
+  if (!plan_dev || !aligned(plan_dev, 8) || !plan_host)
+    return fail(CM_EINVAL, "plan_dev / plan_host is NULL or misaligned");
+  if (!out_dev || !aligned(out_dev, 16)) return fail(CM_EINVAL, "out_dev is NULL or not 16-byte aligned");
+  if (plan_host[CM_PLAN_STATUS] == CM_ENONFINITE)
+    return fail(CM_ENONFINITE, "the plan reports a non-finite score");
+  if (plan_host[CM_PLAN_STATUS] != CM_OK) return fail(CM_EINVAL, "plan status is not CM_OK");
+  if (plan_host[CM_PLAN_N] != s.n) return fail(CM_EINVAL, "plan was built for another n");
+  const int64_t nu = plan_host[CM_PLAN_NUNIQUE];
+  if (nu < 1 || nu > s.n) return fail(CM_EINVAL, "plan n_unique out of range");
+  if (T_out < 1 || plan_host[CM_PLAN_TOUT] != T_out)
+    return fail(CM_ESHAPE, "T_out does not match the plan");
+  const cm::RenderLayout lay = cm::render_layout(s);
+  int64_t off = 0, tiles = 0;
+  for (int64_t k = 0; k < nu; ++k) {
+    const int64_t src = plan_host[CM_PLAN_HEADER + k];
+    const int64_t o = plan_host[CM_PLAN_HEADER + s.n + k];
+    const int64_t len = plan_host[CM_PLAN_HEADER + 2 * (int64_t)s.n + k];
+    if (src < 0 || src >= s.n) return fail(CM_EINVAL, "plan slot refers to no delivery");
+    if (len != s.T((int)src)) return fail(CM_ESHAPE, "plan slot length differs from the fragment's T");
+    if (o != off) return fail(CM_ESHAPE, "plan offsets are not the prefix sum of slot lengths");
+    off += len;
+    tiles += (len + lay.tile_rows - 1) / lay.tile_rows;
+  }
+  if (off != T_out) return fail(CM_ESHAPE, "T_out differs from the sum of slot lengths");
+  if (tiles >= ((int64_t)1 << 31)) return fail(CM_ESHAPE, "merged cache too long for one launch");
+  if ((st = check_ws(workspace, workspace_bytes, lay.bytes)) != CM_OK) return st;
+  hipError_t e = cm::launch_render(s, lay, plan_dev, (int32_t)nu, tiles, T_out, rope->base,
+                                   rope->style, out_dev, static_cast<uint8_t*>(workspace),
+                                   static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? CM_OK : fail_hip(e, "cm_render_merge");
+}
+
+int32_t cm_timing_enable(int32_t on) {
+  g_err.clear();
+  g_timing.store(on != 0);
+  return CM_OK;
+}
+
+int32_t cm_timing_reset(void) {
+  g_err.clear();
+  hipError_t e = drain_pending();
+  std::lock_guard<std::mutex> lk(g_tmu);
+  for (int k = 0; k < cm::K_COUNT; ++k) {
+    g_total_ms[k] = 0.0;
+    g_count[k] = 0;
+  }
+  return e == hipSuccess ? CM_OK : fail_hip(e, "cm_timing_reset");
+}
+
+int32_t cm_timing_query(const char* kernel, double* total_ms, int64_t* launches) {
+  g_err.clear();
+  if (!kernel || !total_ms || !launches) return fail(CM_EINVAL, "NULL argument");
+  int id = -1;
+  for (int k = 0; k < cm::K_COUNT; ++k)
+    if (std::strcmp(kernel, kKernelNames[k]) == 0) id = k;
+  if (id < 0) return fail(CM_EINVAL, std::string("unknown kernel name ") + kernel);
+  hipError_t e = drain_pending();
+  std::lock_guard<std::mutex> lk(g_tmu);
+  *total_ms = g_total_ms[id];
+  *launches = g_count[id];
+  return e == hipSuccess ? CM_OK : fail_hip(e, "cm_timing_query");
+}
+
+}  // extern "C"

@@ -1,0 +1,98 @@
+// Internal interface between the C-ABI layer (api.cpp) and the kernel files.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "cmerge.h"
+
+namespace cm {
+
+// Validated description of a fragment set (see cm_fragset in cmerge.h).
+struct SetDesc {
+  int32_t n, L, H, d, dtype;
+  int32_t esize;              // bytes per element
+  int64_t stride;             // int64 entries per table row = 1 + 2L
+  int64_t row_bytes;          // bytes of one [d] row = d * esize
+  const int64_t* table_dev;   // device table (kernels)
+  const int64_t* table_host;  // host table (sizing)
+  int64_t T(int i) const { return table_host[(int64_t)i * stride]; }
+};
+
+constexpr int kLeafBytes = 4096;
+constexpr size_t kWsAlign = 256;
+
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// Tree-hash geometry of a set: leaves per tensor of fragment i at level 0 is
+// m0(i) = ceil(H*T_i*d*esize / 4096); level v has ceil(m0 / 2^v) nodes.
+struct HashLayout {
+  int32_t levels;         // parent levels above the leaves (0 if every tensor is one leaf)
+  int64_t total0;         // nodes at level 0 over all tensors
+  int64_t total1;         // nodes at level 1 over all tensors (0 if levels == 0)
+  size_t off_tables;      // int64 [levels+1][n+1] per-level node bases
+  size_t off_buf0;        // level-0 (and even levels) node digests
+  size_t off_buf1;        // odd levels
+  size_t bytes;           // total workspace bytes
+};
+HashLayout hash_layout(const SetDesc& s);
+
+struct KnormLayout {
+  int64_t rows;           // H * tail_len
+  int64_t padded;         // next power of two >= rows
+  int32_t rows_per_block; // min(256, padded)
+  int64_t count0;         // partial sums per fragment after the row pass
+  size_t off_a, off_b;    // ping-pong partial buffers (doubles)
+  size_t bytes;
+};
+KnormLayout knorm_layout(const SetDesc& s, int64_t tail_len);
+size_t knorm_max_bytes(const SetDesc& s);  // over every legal tail_len
+
+struct RenderLayout {
+  int32_t tile_rows;      // rows per render tile
+  size_t off_tiles;       // int64 [n+1] tile bases per slot
+  size_t off_angles;      // double [n][d/2][2] cos, sin per slot
+  size_t bytes;
+};
+RenderLayout render_layout(const SetDesc& s);
+
+// Launchers (enqueue on `stream`, return the first HIP error).
+hipError_t launch_hash(const SetDesc& s, const HashLayout& lay, uint8_t* digests, uint8_t* ws,
+                       hipStream_t stream);
+hipError_t launch_knorm(const SetDesc& s, const KnormLayout& lay, int32_t layer, int64_t tail_len,
+                        double* keys, uint8_t* ws, hipStream_t stream);
+hipError_t launch_order(const SetDesc& s, const double* keys, const uint8_t* digests,
+                        int64_t* plan, hipStream_t stream);
+hipError_t launch_render(const SetDesc& s, const RenderLayout& lay, const int64_t* plan_dev,
+                         int32_t n_unique, int64_t total_tiles, int64_t T_out, double base,
+                         int32_t style, void* out, uint8_t* ws, hipStream_t stream);
+
+// Per-kernel event timing (no-op unless cm_timing_enable(1)).
+class ScopedTiming {
+ public:
+  ScopedTiming(int kernel_id, hipStream_t stream);
+  ~ScopedTiming();
+  ScopedTiming(const ScopedTiming&) = delete;
+  ScopedTiming& operator=(const ScopedTiming&) = delete;
+
+ private:
+  int id_;
+  hipStream_t stream_;
+  hipEvent_t start_ = nullptr;
+};
+
+enum KernelId {
+  K_HASH_PREP = 0,
+  K_HASH_LEAF,
+  K_HASH_PARENT,
+  K_HASH_FINAL,
+  K_KNORM_ROWS,
+  K_KNORM_TREE,
+  K_ORDER,
+  K_RENDER_PREP,
+  K_RENDER,
+  K_COUNT
+};
+
+}  // namespace cm

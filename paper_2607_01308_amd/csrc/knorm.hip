@@ -1,0 +1,174 @@
+// Step 2 — score of Eq. (3) / Alg. 1: S_i = sum over heads and the last T* rows
+// of the routing layer's K of the row L2 norms (rho_i = S_i / (H T*)).
+//
+// The summation order is fixed so that the key is bit-identical on any device
+// and in the CPU oracle: squares in fp64 (exact for bf16 and fp32 inputs), each
+// row summed by a level-wise adjacent-pair tree over d, correctly rounded sqrt,
+// and the H*T* row norms (flattened (h, r), zero-padded to a power of two)
+// summed by the same kind of tree. A row is spread over d*e/16 consecutive
+// lanes (one 16-byte load each): the lane's own elements form the bottom levels
+// of the row tree in registers and an xor-butterfly over those lanes forms the
+// upper levels (fp addition is commutative, so both partners hold the same
+// node). An aligned block of up to 256 row norms is one subtree, reduced in LDS;
+// further levels run as small tree launches. Reads only the H*T*d*e tail bytes
+// of one layer per fragment.
+#include "internal.h"
+
+namespace cm {
+
+namespace {
+
+template <int ESIZE>
+__device__ __forceinline__ double row_chunk_sumsq(const uint4 v) {
+  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+  if constexpr (ESIZE == 2) {
+    double e[8];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const double lo = (double)__uint_as_float(w[k] << 16);
+      const double hi = (double)__uint_as_float(w[k] & 0xFFFF0000u);
+      e[2 * k] = lo * lo;
+      e[2 * k + 1] = hi * hi;
+    }
+    return ((e[0] + e[1]) + (e[2] + e[3])) + ((e[4] + e[5]) + (e[6] + e[7]));
+  } else {
+    double e[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const double x = (double)__uint_as_float(w[k]);
+      e[k] = x * x;
+    }
+    return (e[0] + e[1]) + (e[2] + e[3]);
+  }
+}
+
+// In-place level-wise adjacent-pair tree over sh[0..count), count a power of two.
+__device__ __forceinline__ double lds_tree(double* sh, int count) {
+  const int tid = threadIdx.x;
+  for (int w = count >> 1; w >= 1; w >>= 1) {
+    double t = 0.0;
+    if (tid < w) t = sh[2 * tid] + sh[2 * tid + 1];
+    __syncthreads();
+    if (tid < w) sh[tid] = t;
+    __syncthreads();
+  }
+  return sh[0];
+}
+
+// grid (count0, n), 256 threads: block b of fragment i sums rows
+// [b*rpb, (b+1)*rpb) of the padded (h, r) row space.
+template <int ESIZE>
+__global__ __launch_bounds__(256) void knorm_rows_kernel(const int64_t* __restrict__ table,
+                                                         int64_t stride, int32_t layer,
+                                                         int64_t tail, int32_t d, int64_t rows,
+                                                         int32_t rpb, int64_t count0,
+                                                         double* __restrict__ out) {
+#pragma clang fp contract(off)
+  __shared__ double sh[256];
+  const int i = blockIdx.y;
+  const int64_t blk = blockIdx.x;
+  const int64_t T = table[(int64_t)i * stride];
+  const uint8_t* K = reinterpret_cast<const uint8_t*>(table[(int64_t)i * stride + 1 + 2 * layer]);
+  const int row_bytes = d * ESIZE;
+  const int lpr = row_bytes >> 4;  // lanes per row: a power of two in [4, 64]
+  const int rpp = 256 / lpr;       // rows per pass
+  const int tid = threadIdx.x;
+  const int q = tid & (lpr - 1);
+  for (int p0 = 0; p0 < rpb; p0 += rpp) {
+    const int fl = p0 + tid / lpr;
+    const int64_t f = blk * rpb + fl;
+    const bool valid = fl < rpb && f < rows;
+    double acc = 0.0;
+    if (valid) {
+      const int64_t h = f / tail;
+      const int64_t r = f - h * tail;
+      const uint8_t* src = K + (h * T + (T - tail + r)) * row_bytes + q * 16;
+      acc = row_chunk_sumsq<ESIZE>(*reinterpret_cast<const uint4*>(src));
+    }
+    for (int o = 1; o < lpr; o <<= 1) acc = acc + __shfl_xor(acc, o, 64);
+    if (fl < rpb && q == 0) sh[fl] = valid ? sqrt(acc) : 0.0;
+  }
+  __syncthreads();
+  const double s = lds_tree(sh, rpb);
+  if (tid == 0) out[(int64_t)i * count0 + blk] = s;
+}
+
+// grid (cout, n), g threads: out[i][b] = tree of in[i][b*g .. b*g+g).
+__global__ __launch_bounds__(256) void knorm_tree_kernel(const double* __restrict__ in,
+                                                         int64_t cin, double* __restrict__ out,
+                                                         int64_t cout) {
+#pragma clang fp contract(off)
+  __shared__ double sh[256];
+  const int i = blockIdx.y;
+  const int g = blockDim.x;
+  sh[threadIdx.x] = in[(int64_t)i * cin + (int64_t)blockIdx.x * g + threadIdx.x];
+  __syncthreads();
+  const double s = lds_tree(sh, g);
+  if (threadIdx.x == 0) out[(int64_t)i * cout + blockIdx.x] = s;
+}
+
+int64_t next_pow2(int64_t x) {
+  int64_t p = 1;
+  while (p < x) p <<= 1;
+  return p;
+}
+
+}  // namespace
+
+KnormLayout knorm_layout(const SetDesc& s, int64_t tail_len) {
+  KnormLayout lay{};
+  lay.rows = (int64_t)s.H * tail_len;
+  lay.padded = next_pow2(lay.rows);
+  lay.rows_per_block = (int32_t)(lay.padded < 256 ? lay.padded : 256);
+  lay.count0 = lay.padded / lay.rows_per_block;
+  const size_t a = sizeof(double) * (size_t)s.n * (size_t)lay.count0;
+  const size_t b = sizeof(double) * (size_t)s.n * (size_t)((lay.count0 + 255) / 256);
+  lay.off_a = 0;
+  lay.off_b = align_up(a, kWsAlign);
+  lay.bytes = align_up(lay.off_b + b, kWsAlign);
+  return lay;
+}
+
+size_t knorm_max_bytes(const SetDesc& s) {
+  int64_t tmin = s.T(0);
+  for (int i = 1; i < s.n; ++i)
+    if (s.T(i) < tmin) tmin = s.T(i);
+  return knorm_layout(s, tmin).bytes;  // grows with tail_len, which is at most min T
+}
+
+hipError_t launch_knorm(const SetDesc& s, const KnormLayout& lay, int32_t layer, int64_t tail_len,
+                        double* keys, uint8_t* ws, hipStream_t stream) {
+  double* bufs[2] = {reinterpret_cast<double*>(ws + lay.off_a),
+                     reinterpret_cast<double*>(ws + lay.off_b)};
+  {
+    ScopedTiming tm(K_KNORM_ROWS, stream);
+    double* out = lay.count0 == 1 ? keys : bufs[0];
+    const dim3 grid((uint32_t)lay.count0, (uint32_t)s.n);
+    if (s.esize == 2)
+      hipLaunchKernelGGL(knorm_rows_kernel<2>, grid, dim3(256), 0, stream, s.table_dev,
+                         s.stride, layer, tail_len, s.d, lay.rows, lay.rows_per_block,
+                         lay.count0, out);
+    else
+      hipLaunchKernelGGL(knorm_rows_kernel<4>, grid, dim3(256), 0, stream, s.table_dev,
+                         s.stride, layer, tail_len, s.d, lay.rows, lay.rows_per_block,
+                         lay.count0, out);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  int64_t c = lay.count0;
+  int cur = 0;
+  while (c > 1) {
+    const int64_t g = c < 256 ? c : 256;
+    const int64_t cout = c / g;
+    double* out = cout == 1 ? keys : bufs[cur ^ 1];
+    ScopedTiming tm(K_KNORM_TREE, stream);
+    hipLaunchKernelGGL(knorm_tree_kernel, dim3((uint32_t)cout, (uint32_t)s.n), dim3((uint32_t)g),
+                       0, stream, bufs[cur], c, out, cout);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    cur ^= 1;
+    c = cout;
+  }
+  return hipSuccess;
+}
+
+}  // namespace cm

@@ -1,0 +1,140 @@
+// Step 3 — Ingest dedupe (Alg. 2, Eq. (5)) and canonical order (Alg. 1):
+// pi* = argsort(-S, -h) over the distinct fragments, offsets by exclusive prefix
+// sum of the lengths in that order (§4.2).
+//
+// n <= 1024 deliveries fit one workgroup (one lane per delivery), so the order
+// is built by exact counting, with no sort network and no host round trip: a
+// delivery is absorbed if an earlier one has the same digest; the slot of a
+// distinct fragment is the number of distinct fragments that precede it (larger
+// key, or equal key and larger big-endian digest). Keys are compared as IEEE
+// doubles and only bitwise-equal keys tie. Everything is integer or comparison
+// work, so the plan is exact and independent of thread timing.
+#include "internal.h"
+
+namespace cm {
+
+namespace {
+
+__device__ __forceinline__ uint32_t bswap32(uint32_t x) {
+  return __builtin_bswap32(x);
+}
+
+// Digest words in big-endian significance order (byte 0 most significant).
+__device__ __forceinline__ void load_digest_be(const uint8_t* __restrict__ digests, int i,
+                                               uint32_t (&w)[8]) {
+  const uint32_t* p = reinterpret_cast<const uint32_t*>(digests + (int64_t)i * 32);
+#pragma unroll
+  for (int k = 0; k < 8; ++k) w[k] = bswap32(p[k]);
+}
+
+// -1, 0, +1 for a <, ==, > b as 256-bit big-endian unsigned integers.
+__device__ __forceinline__ int cmp_digest(const uint32_t (&a)[8], const uint32_t (&b)[8]) {
+#pragma unroll
+  for (int k = 0; k < 8; ++k)
+    if (a[k] != b[k]) return a[k] > b[k] ? 1 : -1;
+  return 0;
+}
+
+__global__ __launch_bounds__(1024) void order_kernel(const int64_t* __restrict__ table,
+                                                     int64_t stride, int32_t n,
+                                                     const double* __restrict__ keys,
+                                                     const uint8_t* __restrict__ digests,
+                                                     int64_t* __restrict__ plan) {
+  __shared__ double s_key[1024];
+  __shared__ int64_t s_len[1024];     // by delivery, then by slot
+  __shared__ int32_t s_first[1024];   // first delivery with the same digest
+  __shared__ int32_t s_rank[1024];    // slot of each distinct delivery
+  __shared__ int32_t s_src[1024];     // delivery of each slot
+  __shared__ int64_t s_slot_len[1024];
+  const int tid = threadIdx.x;
+  const bool live = tid < n;
+  uint32_t mine[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  double key = 0.0;
+  int64_t len = 0;
+  s_src[tid] = -1;
+  s_slot_len[tid] = 0;
+  s_rank[tid] = 0;
+  if (live) {
+    key = keys[tid];
+    len = table[(int64_t)tid * stride];
+    load_digest_be(digests, tid, mine);
+    s_key[tid] = key;
+    s_len[tid] = len;
+  }
+  const int bad = __syncthreads_or(live && !isfinite(key));
+
+  // Absorption: the first arrival of each digest is kept.
+  int first = tid;
+  if (live) {
+    for (int j = 0; j < tid; ++j) {
+      uint32_t other[8];
+      load_digest_be(digests, j, other);
+      if (cmp_digest(other, mine) == 0) { first = j; break; }
+    }
+    s_first[tid] = first;
+  }
+  __syncthreads();
+  const bool distinct = live && first == tid;
+  const int n_unique = __syncthreads_count(distinct);
+
+  // Slot = number of distinct fragments ordered before this one.
+  if (distinct) {
+    int rank = 0;
+    for (int j = 0; j < n; ++j) {
+      if (j == tid || s_first[j] != j) continue;
+      const double kj = s_key[j];
+      bool before = kj > key;
+      if (!before && kj == key) {
+        uint32_t other[8];
+        load_digest_be(digests, j, other);
+        before = cmp_digest(other, mine) > 0;
+      }
+      rank += before ? 1 : 0;
+    }
+    s_rank[tid] = rank;
+    if (rank < 1024) {
+      s_src[rank] = tid;
+      s_slot_len[rank] = len;
+    }
+  }
+  __syncthreads();
+
+  // Offsets: exclusive prefix sum of slot lengths (exact integers).
+  int64_t off = 0;
+  if (tid < n_unique) {
+    for (int s2 = 0; s2 < tid; ++s2) off += s_slot_len[s2];
+  }
+  if (tid < n) {
+    const int64_t nn = n;
+    if (tid < n_unique) {
+      plan[CM_PLAN_HEADER + tid] = s_src[tid];
+      plan[CM_PLAN_HEADER + nn + tid] = off;
+      plan[CM_PLAN_HEADER + 2 * nn + tid] = s_slot_len[tid];
+    } else {
+      plan[CM_PLAN_HEADER + tid] = -1;
+      plan[CM_PLAN_HEADER + nn + tid] = -1;
+      plan[CM_PLAN_HEADER + 2 * nn + tid] = -1;
+    }
+    plan[CM_PLAN_HEADER + 3 * nn + tid] = s_rank[s_first[tid]];
+  }
+  if (tid == n_unique - 1) {
+    plan[CM_PLAN_STATUS] = bad ? CM_ENONFINITE : CM_OK;
+    plan[CM_PLAN_N] = n;
+    plan[CM_PLAN_NUNIQUE] = n_unique;
+    plan[CM_PLAN_TOUT] = off + s_slot_len[tid];
+  }
+}
+
+}  // namespace
+
+hipError_t launch_order(const SetDesc& s, const double* keys, const uint8_t* digests,
+                        int64_t* plan, hipStream_t stream) {
+  int threads = 64;
+  while (threads < s.n) threads <<= 1;
+  ScopedTiming tm(K_ORDER, stream);
+  hipLaunchKernelGGL(order_kernel, dim3(1), dim3(threads), 0, stream, s.table_dev, s.stride,
+                     s.n, keys, digests, plan);
+  return hipGetLastError();
+}
+
+}  // namespace cm

@@ -1,0 +1,176 @@
+"""LatentFragmentSet (Alg. 2) and the render path on one GPU.
+
+render_deliveries runs the whole path over a list of deliveries: Id of every
+delivery (cm_fragment_hash), scores (cm_fragment_knorm), dedupe + canonical
+order + offsets (cm_canonical_order), one device-to-host copy of the small plan
+so the caller can size the output, then the rotate-and-concatenate render
+(cm_render_merge). LatentFragmentSet keeps the state of Alg. 2 (a set keyed by
+Id) and renders it with the ids computed at Ingest."""
+
+from __future__ import annotations
+
+from dataclasses import dataclass
+from typing import Dict, List, Optional, Sequence, Union
+
+import numpy as np
+import torch
+
+from . import _cabi as C
+from .binding import (FragmentBatch, canonical_order, fragment_hash, fragment_knorm, plan_elems,
+                      render_merge, workspace_size)
+
+_WS: Dict[torch.device, torch.Tensor] = {}
+
+
+def _workspace(batch: FragmentBatch) -> torch.Tensor:
+    need = max(workspace_size(batch), 256)
+    ws = _WS.get(batch.device)
+    if ws is None or ws.numel() < need:
+        ws = torch.empty(need, dtype=torch.uint8, device=batch.device)
+        _WS[batch.device] = ws
+    return ws
+
+
+def release_workspace() -> None:
+    _WS.clear()
+
+
+@dataclass
+class RenderResult:
+    cache: tuple                 # per layer (K, V), each [1, H, T_out, d]
+    merged: torch.Tensor         # the single [L, 2, 1, H, T_out, d] buffer behind `cache`
+    digests_dev: torch.Tensor    # [n, 32] uint8, per delivery
+    keys_dev: torch.Tensor       # [n] float64 S_i, per delivery
+    plan: np.ndarray             # host copy of the plan (layout in include/cmerge.h)
+    tail_len: int
+
+    @property
+    def n_unique(self) -> int:
+        return int(self.plan[C.PLAN_NUNIQUE])
+
+    @property
+    def T_out(self) -> int:
+        return int(self.plan[C.PLAN_TOUT])
+
+    @property
+    def order(self) -> List[int]:
+        n = int(self.plan[C.PLAN_N])
+        return [int(x) for x in self.plan[C.PLAN_HEADER:C.PLAN_HEADER + self.n_unique]][:n]
+
+    @property
+    def offsets(self) -> List[int]:
+        n = int(self.plan[C.PLAN_N])
+        b = C.PLAN_HEADER + n
+        return [int(x) for x in self.plan[b:b + self.n_unique]]
+
+    @property
+    def lengths(self) -> List[int]:
+        n = int(self.plan[C.PLAN_N])
+        b = C.PLAN_HEADER + 2 * n
+        return [int(x) for x in self.plan[b:b + self.n_unique]]
+
+    @property
+    def slot_of_delivery(self) -> List[int]:
+        n = int(self.plan[C.PLAN_N])
+        b = C.PLAN_HEADER + 3 * n
+        return [int(x) for x in self.plan[b:b + n]]
+
+    @property
+    def digests(self) -> List[bytes]:
+        return [bytes(r) for r in self.digests_dev.cpu().numpy()]
+
+    @property
+    def keys(self) -> np.ndarray:
+        return self.keys_dev.cpu().numpy()
+
+
+def _render_plan(batch: FragmentBatch, plan_dev: torch.Tensor, plan_host: np.ndarray,
+                 rope_base: float, style: str, ws: torch.Tensor, stream):
+    status = int(plan_host[C.PLAN_STATUS])
+    if status != C.CM_OK:
+        raise C.CmError(status, "cm_canonical_order", "plan status is not CM_OK "
+                        "(a score is NaN or infinite)" if status == C.CM_ENONFINITE else "")
+    T_out = int(plan_host[C.PLAN_TOUT])
+    merged = torch.empty((batch.L, 2, 1, batch.H, T_out, batch.d), dtype=batch.torch_dtype,
+                         device=batch.device)
+    render_merge(batch, plan_dev, plan_host, rope_base, style, merged, T_out, ws, stream)
+    cache = tuple((merged[l, 0], merged[l, 1]) for l in range(batch.L))
+    return merged, cache
+
+
+def render_deliveries(deliveries: Union[FragmentBatch, Sequence], routing_layer: int,
+                      rope_base: float, style: str = "half", stream=None) -> RenderResult:
+    """The whole path over a list of deliveries (duplicates allowed)."""
+    batch = deliveries if isinstance(deliveries, FragmentBatch) else FragmentBatch(deliveries)
+    dev = batch.device
+    ws = _workspace(batch)
+    digests = torch.empty((batch.n, 32), dtype=torch.uint8, device=dev)
+    keys = torch.empty(batch.n, dtype=torch.float64, device=dev)
+    plan_dev = torch.empty(plan_elems(batch.n), dtype=torch.int64, device=dev)
+    tail = min(batch.lengths)
+    fragment_hash(batch, digests, ws, stream)
+    fragment_knorm(batch, routing_layer, tail, keys, ws, stream)
+    canonical_order(batch, keys, digests, plan_dev, stream)
+    plan_host = plan_dev.to("cpu").numpy()
+    merged, cache = _render_plan(batch, plan_dev, plan_host, rope_base, style, ws, stream)
+    return RenderResult(cache=cache, merged=merged, digests_dev=digests, keys_dev=keys,
+                        plan=plan_host, tail_len=tail)
+
+
+def fragment_ids(caches: Sequence, stream=None) -> List[bytes]:
+    """Id of Alg. 2 for each cache (one batched launch)."""
+    batch = FragmentBatch(caches)
+    ws = _workspace(batch)
+    digests = torch.empty((batch.n, 32), dtype=torch.uint8, device=batch.device)
+    fragment_hash(batch, digests, ws, stream)
+    return [bytes(r) for r in digests.cpu().numpy()]
+
+
+class LatentFragmentSet:
+    """State of Alg. 2: fragments keyed by their content address. Ingest and
+    Merge are set union (a byte-identical re-delivery is absorbed); Render is
+    CanonicalMerge over the set, a pure function of the set."""
+
+    def __init__(self, items: Optional[Dict[bytes, tuple]] = None):
+        self._items: Dict[bytes, tuple] = dict(items or {})
+
+    def ingest(self, cache) -> bytes:
+        return self.ingest_many([cache])[0]
+
+    def ingest_many(self, caches: Sequence) -> List[bytes]:
+        ids = fragment_ids(caches)
+        for fid, cache in zip(ids, caches):
+            self._items.setdefault(fid, cache)
+        return ids
+
+    def merge(self, other: "LatentFragmentSet") -> "LatentFragmentSet":
+        out = dict(self._items)
+        for k, v in other._items.items():
+            out.setdefault(k, v)
+        return LatentFragmentSet(out)
+
+    def ids(self) -> frozenset:
+        return frozenset(self._items)
+
+    def __len__(self) -> int:
+        return len(self._items)
+
+    def render(self, routing_layer: int, rope_base: float, style: str = "half",
+               stream=None) -> RenderResult:
+        if not self._items:
+            raise ValueError("cannot render an empty set")
+        ids = list(self._items.keys())
+        batch = FragmentBatch([self._items[k] for k in ids])
+        dev = batch.device
+        ws = _workspace(batch)
+        digests = torch.tensor(np.frombuffer(b"".join(ids), dtype=np.uint8).reshape(-1, 32),
+                               device=dev)
+        keys = torch.empty(batch.n, dtype=torch.float64, device=dev)
+        plan_dev = torch.empty(plan_elems(batch.n), dtype=torch.int64, device=dev)
+        tail = min(batch.lengths)
+        fragment_knorm(batch, routing_layer, tail, keys, ws, stream)
+        canonical_order(batch, keys, digests, plan_dev, stream)
+        plan_host = plan_dev.to("cpu").numpy()
+        merged, cache = _render_plan(batch, plan_dev, plan_host, rope_base, style, ws, stream)
+        return RenderResult(cache=cache, merged=merged, digests_dev=digests, keys_dev=keys,
+                            plan=plan_host, tail_len=tail)

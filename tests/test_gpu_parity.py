@@ -1,0 +1,244 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Digests, scores, dedupe, order, offsets and V are compared bit for bit; K
+element by element within 2^-7 (bf16) or 1e-5 (fp32) relative to
+max(|ref|, smallest normal), and the bit-identical fraction is asserted too.
+Inputs come from the seeded generator, never from the HIP path."""
+
+import itertools
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+import paper_2607_01308_amd as cm
+from gpu_util import (check_render, gpu_deliveries, k_close, log, oracle_ids, oracle_keys,
+                      oracle_plan)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("needs a GPU")
+    yield
+    torch.cuda.synchronize()
+
+
+def _run(w, deliveries, style="half"):
+    log(f"[render] {w.name} n={len(deliveries)} L={w.L} H={w.H} d={w.d} {w.dtype}")
+    res = cm.render_deliveries(deliveries, w.routing_layer, w.rope_base, style=style)
+    torch.cuda.synchronize()
+    return res
+
+
+def test_tiny_workload():
+    w = synth.tiny()
+    _, dl = gpu_deliveries(w)
+    res = _run(w, dl)
+    frac = check_render(res, dl, w.dtype, w.routing_layer, w.rope_base)
+    assert res.T_out == 40 and res.n_unique == 2
+    log(f"tiny: K bit-identical fraction {frac:.6f}")
+
+
+SHAPES = [
+    dict(name="bf16-d128-ragged", dtype="bfloat16", d=128, H=2, L=3, lengths=(300, 517, 1000),
+         deliveries=(0, 1, 2, 1, 0)),
+    dict(name="fp32-d64", dtype="float32", d=64, H=3, L=2, lengths=(129, 64, 7), deliveries=(2, 0, 1)),
+    dict(name="bf16-d32-row64B", dtype="bfloat16", d=32, H=4, L=2, lengths=(33, 100)),
+    dict(name="bf16-d512-row1KiB", dtype="bfloat16", d=512, H=1, L=2, lengths=(40, 77, 5)),
+    dict(name="fp32-d16-row64B", dtype="float32", d=16, H=2, L=2, lengths=(5, 3, 11)),
+    dict(name="fp32-d256-row1KiB", dtype="float32", d=256, H=2, L=2, lengths=(70, 31)),
+    dict(name="bf16-T1", dtype="bfloat16", d=128, H=8, L=2, lengths=(1, 1, 2)),
+]
+
+
+@pytest.mark.parametrize("spec", SHAPES, ids=[s["name"] for s in SHAPES])
+def test_shapes_tiles_and_ragged_tails(spec):
+    spec = dict(spec)
+    name = spec.pop("name")
+    w = synth.custom(name, routing_layer=1, rope_base=1e6, **spec)
+    _, dl = gpu_deliveries(w)
+    res = _run(w, dl)
+    frac = check_render(res, dl, w.dtype, w.routing_layer, w.rope_base)
+    log(f"{name}: unique={res.n_unique} T_out={res.T_out} K identical {frac:.6f}")
+
+
+def test_interleaved_rope_style():
+    w = synth.custom("interleaved", dtype="bfloat16", d=64, H=2, L=2, lengths=(200, 90),
+                     routing_layer=0, rope_base=1e4)
+    _, dl = gpu_deliveries(w)
+    res = _run(w, dl, style="interleaved")
+    check_render(res, dl, w.dtype, w.routing_layer, w.rope_base, style="interleaved")
+
+
+def test_multi_level_hash_trees():
+    # 125 and 251 leaves per tensor: odd counts carried up at several levels
+    w = synth.custom("tree", dtype="bfloat16", d=128, H=2, L=2, lengths=(1000, 2008, 16))
+    _, dl = gpu_deliveries(w)
+    res = _run(w, dl)
+    assert res.digests == oracle_ids(dl, w.dtype)
+
+
+def test_single_fragment_and_all_duplicates():
+    w = synth.custom("one", dtype="bfloat16", d=128, H=2, L=2, lengths=(77,), deliveries=(0, 0, 0, 0))
+    frags, dl = gpu_deliveries(w)
+    res = _run(w, dl)
+    assert res.n_unique == 1 and res.T_out == 77 and res.slot_of_delivery == [0, 0, 0, 0]
+    assert res.order == [0]
+    for l in range(w.L):
+        assert torch.equal(res.cache[l][0], frags[0][l][0])
+        assert torch.equal(res.cache[l][1], frags[0][l][1])
+    assert len(set(res.digests)) == 1
+
+
+def test_equal_scores_fall_to_digest():
+    w = synth.custom("tie", dtype="bfloat16", d=128, H=2, L=2, lengths=(64, 64, 40),
+                     shared_k=((0, 1),), routing_layer=0)
+    _, dl = gpu_deliveries(w)
+    res = _run(w, dl)
+    k = res.keys
+    assert k[0] == k[1]
+    check_render(res, dl, w.dtype, w.routing_layer, w.rope_base)
+    d0, d1 = res.digests[0], res.digests[1]
+    s0, s1 = res.slot_of_delivery[0], res.slot_of_delivery[1]
+    assert (s0 < s1) == (d0 > d1)
+
+
+def test_rerun_and_permutations_byte_identical():
+    w = synth.custom("perm", dtype="bfloat16", d=128, H=2, L=2, lengths=(90, 130, 40, 75))
+    frags, _ = gpu_deliveries(w)
+    ref = cm.render_deliveries(frags, w.routing_layer, w.rope_base)
+    again = cm.render_deliveries(frags, w.routing_layer, w.rope_base)
+    assert torch.equal(ref.merged, again.merged)
+    count = 0
+    for perm in itertools.permutations(range(4)):
+        out = cm.render_deliveries([frags[p] for p in perm], w.routing_layer, w.rope_base)
+        assert torch.equal(out.merged, ref.merged)
+        count += 1
+    assert count == 24
+
+
+def test_nonfinite_score_is_an_error():
+    w = synth.custom("nan", dtype="bfloat16", d=128, H=2, L=2, lengths=(20, 30), routing_layer=1)
+    frags, _ = gpu_deliveries(w)
+    frags[1][1][0][0, 1, 25, 3] = float("nan")       # inside the routing layer's tail
+    with pytest.raises(cm.CmError) as e:
+        cm.render_deliveries(frags, w.routing_layer, w.rope_base)
+    assert e.value.status == -4
+    frags2, _ = gpu_deliveries(w)
+    frags2[1][1][0][0, 1, 3, 3] = float("inf")        # before the tail (T* = 20 -> rows 10..29)
+    frags2[0][0][0][0, 0, 5, 7] = float("nan")        # another layer
+    res = cm.render_deliveries(frags2, w.routing_layer, w.rope_base)
+    check_render(res, frags2, w.dtype, w.routing_layer, w.rope_base)
+
+
+def test_render_equals_one_long_sequence():
+    """Fragments keyed at local positions (rotation done here by complex
+    multiplication in fp64) render into one long sequence's keys (§4.2)."""
+    rng = np.random.default_rng(0)
+    H, d, base = 2, 64, 1e4
+    theta = base ** (-np.arange(0, d, 2) / d)
+
+    def rot(raw, pos):
+        z = (raw[..., : d // 2] + 1j * raw[..., d // 2:]) * np.exp(1j * pos[None, :, None] * theta)
+        return np.concatenate([z.real, z.imag], axis=-1)
+
+    raws, caches = [], []
+    for T, s in ((300, 1.0), (170, 2.0), (45, 1.4)):
+        raw = rng.standard_normal((H, T, d)) * s
+        K = torch.from_numpy(rot(raw, np.arange(T)).astype(np.float32))[None].cuda()
+        raws.append(raw)
+        caches.append(((K, torch.zeros_like(K)),))
+    res = cm.render_deliveries(caches, 0, base)
+    out = res.cache[0][0][0].cpu().numpy().astype(np.float64)
+    for i, off in zip(res.order, res.offsets):
+        T = raws[i].shape[1]
+        want = rot(raws[i], off + np.arange(T))
+        assert np.allclose(out[:, off:off + T], want, rtol=0, atol=4e-7 * np.abs(want).max())
+
+
+def test_latent_fragment_set_matches_delivery_render():
+    w = synth.custom("set", dtype="bfloat16", d=128, H=2, L=2, lengths=(50, 80, 33),
+                     deliveries=(1, 0, 1, 2, 2))
+    frags, dl = gpu_deliveries(w)
+    S = cm.LatentFragmentSet()
+    S.ingest_many(dl[:2])
+    T = cm.LatentFragmentSet()
+    T.ingest_many(dl[2:])
+    U = S.merge(T)
+    assert len(U) == 3 and U.ids() == T.merge(S).ids()
+    assert U.merge(U).ids() == U.ids()
+    a = U.render(w.routing_layer, w.rope_base)
+    b = cm.render_deliveries(dl, w.routing_layer, w.rope_base)
+    assert torch.equal(a.merged, b.merged)
+    assert set(U.ids()) == set(oracle_ids([frags[i] for i in range(3)], w.dtype))
+
+
+def test_timing_api_counts_launches():
+    w = synth.custom("timing", lengths=(64, 32))
+    _, dl = gpu_deliveries(w)
+    cm.timing_reset()
+    cm.timing_enable(True)
+    try:
+        cm.render_deliveries(dl, w.routing_layer, w.rope_base)
+        torch.cuda.synchronize()
+        for k in ("hash_leaf", "hash_final", "knorm_rows", "order", "render_prep", "render"):
+            ms, n = cm.timing_query(k)
+            assert n >= 1 and ms > 0.0, k
+    finally:
+        cm.timing_enable(False)
+        cm.timing_reset()
+
+
+def test_binding_rejects_bad_tensors():
+    K = torch.zeros((1, 2, 8, 64), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(ValueError):
+        cm.FragmentBatch([((K.transpose(2, 3).contiguous().transpose(2, 3), K),)])
+    with pytest.raises(ValueError):
+        cm.FragmentBatch([((K, K),), ((K, K), (K, K))])
+    with pytest.raises(TypeError):
+        cm.FragmentBatch([((K.half(), K.half()),)])
+
+
+# ---------------------------------------------------------------- workload sizes
+
+def test_qwen3_17b_n2_full():
+    w = synth.qwen3_17b_n2()
+    _, dl = gpu_deliveries(w)
+    res = _run(w, dl)
+    frac = check_render(res, dl, w.dtype, w.routing_layer, w.rope_base)
+    log(f"qwen3-1.7b-n2: K bit-identical fraction {frac:.7f}")
+
+
+def test_qwen3_17b_n5_all_permutations_and_redelivery():
+    w = synth.qwen3_17b_n5()
+    frags, dl = gpu_deliveries(w)
+    res = _run(w, dl)
+    frac = check_render(res, dl, w.dtype, w.routing_layer, w.rope_base, layers=(0, 14, 27))
+    log(f"qwen3-1.7b-n5: oracle parity on layers 0/14/27, K identical {frac:.7f}")
+    assert res.n_unique == 5 and res.T_out == sum(w.lengths)
+    copies = {i: tuple((K.clone(), V.clone()) for K, V in frags[i]) for i in range(5)}
+    redelivered = [i for i in range(5) for _ in range(w.deliveries.count(i) - 1)]
+    rng = np.random.default_rng(11)
+    count = 0
+    for perm in itertools.permutations(range(5)):
+        lst = [frags[p] for p in perm]
+        for i in redelivered:                               # re-deliveries at random places
+            lst.insert(int(rng.integers(0, len(lst) + 1)), copies[i])
+        out = cm.render_deliveries(lst, w.routing_layer, w.rope_base)
+        assert out.n_unique == 5 and torch.equal(out.merged, res.merged)
+        count += 1
+    assert count == 120
+    log("qwen3-1.7b-n5: 120 permutations with shuffled re-deliveries byte-identical")
+
+
+def test_qwen3_4b_n4_sampled_layers():
+    w = synth.qwen3_4b_n4()
+    _, dl = gpu_deliveries(w)
+    res = _run(w, dl)
+    frac = check_render(res, dl, w.dtype, w.routing_layer, w.rope_base, layers=(0, 18, 35))
+    log(f"qwen3-4b-n4: K identical {frac:.7f}")
