@@ -80,6 +80,9 @@ def main():
     ap.add_argument("--workload", default="qwen3-4b-large")
     ap.add_argument("--seed", type=int, default=42)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="first run a plain streaming kernel (torch.neg over 2 GiB of bf16), whose "
+                         "known read/write bytes scale rocprofv3's FETCH_SIZE/WRITE_SIZE counters")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -92,6 +95,15 @@ def main():
     import paper_2607_01308_amd as cm
 
     dev = torch.device("cuda:0")
+    if args.copy_calibration:
+        src = torch.ones(1 << 30, dtype=torch.bfloat16, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+        print("[bench] calibration copy: 3 x torch.neg over 2 GiB in, 2 GiB out",
+              file=sys.stderr, flush=True)
+        del src, dst
     w = synth.workload(args.workload, args.seed)
     print(f"[bench] generating {w.name}: {w.n_deliveries} deliveries, {w.n_distinct} distinct, "
           f"{w.merged_tokens} merged tokens", file=sys.stderr, flush=True)
