@@ -131,6 +131,14 @@ int32_t cm_workspace_size(const cm_fragset* set, size_t* bytes_out);
 int32_t cm_fragment_hash(const cm_fragset* set, uint8_t* digests_dev,
                          void* workspace, size_t workspace_bytes, void* stream);
 
+/* Same Id, computed only for the fragments i with select_dev[i] == select_value
+ * (select_dev: device, n bytes; select_value in [0, 255]); the other digests are
+ * left untouched. Two calls with complementary selections may run concurrently
+ * on different streams if each has a workspace of its own. */
+int32_t cm_fragment_hash_select(const cm_fragset* set, const uint8_t* select_dev,
+                                int32_t select_value, uint8_t* digests_dev, void* workspace,
+                                size_t workspace_bytes, void* stream);
+
 /* ---------------------------------------------------------------- step 2
  * Score of Eq. (3) / Alg. 1: for every fragment i,
  *   keys_dev[i] = S_i = sum over heads h and rows r in [T_i - tail_len, T_i) of
@@ -148,14 +156,23 @@ int32_t cm_fragment_knorm(const cm_fragset* set, int32_t routing_layer, int64_t 
                           void* stream);
 
 /* ---------------------------------------------------------------- step 3
- * Ingest dedupe (Alg. 2; Eq. (5)) and canonical order (Alg. 1): deliveries with
+ * Which digests the order needs (for running the rest of step 1 concurrently
+ * with steps 4-5): mask_dev[i] = 1 if another fragment has a bitwise-equal key
+ * and the same T, else 0. Byte-identical copies always share key and T, and
+ * ties need equal keys, so cm_canonical_order reads exactly these digests.
+ * keys_dev: output of cm_fragment_knorm (device); mask_dev: device, n bytes. */
+int32_t cm_equal_key_mask(const cm_fragset* set, const double* keys_dev, uint8_t* mask_dev,
+                          void* stream);
+
+/* Ingest dedupe (Alg. 2; Eq. (5)) and canonical order (Alg. 1): deliveries with
  * equal digests are one fragment (the first arrival is kept); the distinct
  * fragments are sorted by descending key, equal keys by descending digest read
  * as a 256-bit big-endian unsigned integer; offsets are the exclusive prefix sum
  * of the lengths in that order (§4.2). Runs on the device in one workgroup.
- * keys_dev, digests_dev: outputs of steps 1-2 (device). plan_dev: device,
- * cm_plan_elems(n) int64 (layout above). A non-finite key sets plan status
- * CM_ENONFINITE; the call itself still returns CM_OK. */
+ * keys_dev, digests_dev: outputs of steps 1-2 (device); only the digests of
+ * fragments marked by cm_equal_key_mask are read, the others may still be in
+ * flight. plan_dev: device, cm_plan_elems(n) int64 (layout above). A non-finite
+ * key sets plan status CM_ENONFINITE; the call itself still returns CM_OK. */
 int32_t cm_canonical_order(const cm_fragset* set, const double* keys_dev,
                            const uint8_t* digests_dev, int64_t* plan_dev, void* stream);
 
@@ -182,8 +199,8 @@ int32_t cm_render_merge(const cm_fragset* set, const int64_t* plan_dev,
  * around every kernel this library enqueues (off by default; a process-wide
  * switch). cm_timing_query waits for the recorded events, adds their durations
  * to the per-kernel totals and returns the total milliseconds and launch count
- * for one kernel name ("hash_leaf", "hash_parent", "hash_final", "knorm_rows",
- * "knorm_tree", "order", "render_prep", "render"). */
+ * for one kernel name ("hash_prep", "hash_leaf", "hash_parent", "hash_final",
+ * "knorm_rows", "knorm_tree", "order", "key_mask", "render_prep", "render"). */
 int32_t cm_timing_enable(int32_t on);
 int32_t cm_timing_reset(void);
 int32_t cm_timing_query(const char* kernel, double* total_ms, int64_t* launches);

@@ -7,7 +7,9 @@ from .binding import (  # noqa: F401
     KERNELS,
     FragmentBatch,
     canonical_order,
+    equal_key_mask,
     fragment_hash,
+    fragment_hash_select,
     fragment_knorm,
     plan_elems,
     render_merge,

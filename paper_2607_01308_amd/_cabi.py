@@ -28,7 +28,8 @@ PLAN_STATUS, PLAN_N, PLAN_NUNIQUE, PLAN_TOUT, PLAN_HEADER = 0, 1, 2, 3, 4
 # every symbol include/cmerge.h declares
 EXPORTS = (
     "cm_version", "cm_last_error", "cm_status_string", "cm_plan_elems", "cm_workspace_size",
-    "cm_fragment_hash", "cm_fragment_knorm", "cm_canonical_order", "cm_render_merge",
+    "cm_fragment_hash", "cm_fragment_hash_select", "cm_fragment_knorm", "cm_equal_key_mask",
+    "cm_canonical_order", "cm_render_merge",
     "cm_timing_enable", "cm_timing_reset", "cm_timing_query",
 )
 
@@ -76,6 +77,8 @@ def lib() -> ctypes.CDLL:
             "cm_plan_elems": (SZ, [I32]),
             "cm_workspace_size": (I32, [FS, ctypes.POINTER(SZ)]),
             "cm_fragment_hash": (I32, [FS, P, P, SZ, P]),
+            "cm_fragment_hash_select": (I32, [FS, P, I32, P, P, SZ, P]),
+            "cm_equal_key_mask": (I32, [FS, P, P, P]),
             "cm_fragment_knorm": (I32, [FS, I32, I64, P, P, SZ, P]),
             "cm_canonical_order": (I32, [FS, P, P, P, P]),
             "cm_render_merge": (I32, [FS, P, P, ctypes.POINTER(CmRope), P, I64, P, SZ, P]),

@@ -94,6 +94,19 @@ def fragment_hash(batch: FragmentBatch, digests: torch.Tensor, workspace: torch.
                                      _stream(stream, batch.device)), "cm_fragment_hash")
 
 
+def fragment_hash_select(batch: FragmentBatch, select: torch.Tensor, value: int,
+                         digests: torch.Tensor, workspace: torch.Tensor, stream=None) -> None:
+    C.check(C.lib().cm_fragment_hash_select(ctypes.byref(batch.struct), _ptr(select), int(value),
+                                            _ptr(digests), _ptr(workspace),
+                                            workspace.numel() * workspace.element_size(),
+                                            _stream(stream, batch.device)), "cm_fragment_hash_select")
+
+
+def equal_key_mask(batch: FragmentBatch, keys: torch.Tensor, mask: torch.Tensor, stream=None) -> None:
+    C.check(C.lib().cm_equal_key_mask(ctypes.byref(batch.struct), _ptr(keys), _ptr(mask),
+                                      _stream(stream, batch.device)), "cm_equal_key_mask")
+
+
 def fragment_knorm(batch: FragmentBatch, routing_layer: int, tail_len: int, keys: torch.Tensor,
                    workspace: torch.Tensor, stream=None) -> None:
     C.check(C.lib().cm_fragment_knorm(ctypes.byref(batch.struct), routing_layer, tail_len,
@@ -142,4 +155,4 @@ def timing_query(kernel: str):
 
 
 KERNELS = ("hash_prep", "hash_leaf", "hash_parent", "hash_final", "knorm_rows", "knorm_tree",
-           "order", "render_prep", "render")
+           "order", "key_mask", "render_prep", "render")

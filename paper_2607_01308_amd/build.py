@@ -53,7 +53,7 @@ def build(verbose: bool = False) -> str:
     for src in SOURCES:
         obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
         objs.append(obj)
-        lang = ["-x", "hip"] + DEVICE if src.endswith(".hip") else []
+        lang = ["-x", "hip"] + DEVICE  # hipcc compiles .cpp as HIP too; give it the target
         jobs.append([hipcc, *COMMON, *lang, "-c", os.path.join(CSRC, src), "-o", obj])
     jobs.append([hipcc, *COMMON, "-x", "hip", *DEVICE, "-shared", HOSTCHECK_SRC,
                  "-o", HOSTCHECK_LIB + ".tmp"])

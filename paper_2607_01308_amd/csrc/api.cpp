@@ -91,9 +91,9 @@ int64_t min_T(const cm::SetDesc& s) {
 }
 
 // ------------------------------------------------------------------ timing registry
-const char* const kKernelNames[cm::K_COUNT] = {"hash_prep",  "hash_leaf",  "hash_parent",
-                                               "hash_final", "knorm_rows", "knorm_tree",
-                                               "order",      "render_prep", "render"};
+const char* const kKernelNames[cm::K_COUNT] = {
+    "hash_prep", "hash_leaf", "hash_parent", "hash_final", "knorm_rows", "knorm_tree",
+    "order",     "key_mask",  "render_prep", "render"};
 std::atomic<bool> g_timing{false};
 std::mutex g_tmu;
 struct Pending {
@@ -195,19 +195,54 @@ int32_t cm_workspace_size(const cm_fragset* set, size_t* bytes_out) {
   return CM_OK;
 }
 
-int32_t cm_fragment_hash(const cm_fragset* set, uint8_t* digests_dev, void* workspace,
-                         size_t workspace_bytes, void* stream) {
+static int32_t hash_common(const cm_fragset* set, const uint8_t* select, uint32_t want,
+                           uint8_t* digests_dev, void* workspace, size_t workspace_bytes,
+                           void* stream, const char* where) {
   g_err.clear();
   cm::SetDesc s;
   int32_t st = check_set(set, &s);
   if (st != CM_OK) return st;
   if (!digests_dev || !aligned(digests_dev, 16))
     return fail(CM_EINVAL, "digests_dev is NULL or not 16-byte aligned");
+  if (want > 255) return fail(CM_EINVAL, "select_value must be in [0, 255]");
   const cm::HashLayout lay = cm::hash_layout(s);
   if ((st = check_ws(workspace, workspace_bytes, lay.bytes)) != CM_OK) return st;
-  hipError_t e = cm::launch_hash(s, lay, digests_dev, static_cast<uint8_t*>(workspace),
-                                 static_cast<hipStream_t>(stream));
-  return e == hipSuccess ? CM_OK : fail_hip(e, "cm_fragment_hash");
+  hipError_t e = cm::launch_hash(s, lay, select, want, digests_dev,
+                                 static_cast<uint8_t*>(workspace), static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? CM_OK : fail_hip(e, where);
+}
+
+int32_t cm_fragment_hash(const cm_fragset* set, uint8_t* digests_dev, void* workspace,
+                         size_t workspace_bytes, void* stream) {
+  return hash_common(set, nullptr, 0, digests_dev, workspace, workspace_bytes, stream,
+                     "cm_fragment_hash");
+}
+
+int32_t cm_fragment_hash_select(const cm_fragset* set, const uint8_t* select_dev,
+                                int32_t select_value, uint8_t* digests_dev, void* workspace,
+                                size_t workspace_bytes, void* stream) {
+  if (!select_dev) {
+    g_err.clear();
+    return fail(CM_EINVAL, "select_dev is NULL");
+  }
+  if (select_value < 0) {
+    g_err.clear();
+    return fail(CM_EINVAL, "select_value must be in [0, 255]");
+  }
+  return hash_common(set, select_dev, (uint32_t)select_value, digests_dev, workspace,
+                     workspace_bytes, stream, "cm_fragment_hash_select");
+}
+
+int32_t cm_equal_key_mask(const cm_fragset* set, const double* keys_dev, uint8_t* mask_dev,
+                          void* stream) {
+  g_err.clear();
+  cm::SetDesc s;
+  int32_t st = check_set(set, &s);
+  if (st != CM_OK) return st;
+  if (!keys_dev || !aligned(keys_dev, 8)) return fail(CM_EINVAL, "keys_dev is NULL or misaligned");
+  if (!mask_dev) return fail(CM_EINVAL, "mask_dev is NULL");
+  hipError_t e = cm::launch_equal_key_mask(s, keys_dev, mask_dev, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? CM_OK : fail_hip(e, "cm_equal_key_mask");
 }
 
 int32_t cm_fragment_knorm(const cm_fragset* set, int32_t routing_layer, int64_t tail_len,

@@ -119,21 +119,27 @@ __host__ __device__ __forceinline__ void b2s_compress(B2sState& s, const uint32_
 #undef CM_B2S_ROUND
 #undef CM_B2S_G
 
-// Hash one node of the tree whose bytes are 16-byte aligned and a multiple of
-// 64 bytes long (len >= 64), read with the given 128-bit loader.
-template <class Load16>
+// Hash one node whose bytes are 16-byte aligned and a multiple of 64 bytes long
+// (len >= 64), read with the given 64-byte loader. Blocks are fetched two at a
+// time (one 128-byte cache line) one line ahead of the compression, with two
+// alternating line buffers so no registers are copied between iterations.
+template <class Load64>
 __host__ __device__ __forceinline__ void b2s_node_aligned(B2sState& s, const uint8_t* p,
                                                           uint64_t len, bool last_node,
-                                                          Load16 load16) {
+                                                          Load64 load64) {
   const uint64_t nb = len >> 6;
-  uint32_t cur[16], nxt[16];
-  load16(p, cur);
-  for (uint64_t b = 0; b < nb; ++b) {
-    if (b + 1 < nb) load16(p + ((b + 1) << 6), nxt);
-    const bool last = (b + 1 == nb);
-    b2s_compress(s, cur, (b + 1) << 6, last, last && last_node);
-#pragma unroll
-    for (int w = 0; w < 16; ++w) cur[w] = nxt[w];
+  uint32_t x0[16], x1[16], y0[16], y1[16];
+  load64(p, x0);
+  if (nb > 1) load64(p + 64, x1);
+  for (uint64_t b = 0; b < nb; b += 4) {
+    if (b + 2 < nb) load64(p + ((b + 2) << 6), y0);
+    if (b + 3 < nb) load64(p + ((b + 3) << 6), y1);
+    b2s_compress(s, x0, (b + 1) << 6, b + 1 == nb, b + 1 == nb && last_node);
+    if (b + 1 < nb) b2s_compress(s, x1, (b + 2) << 6, b + 2 == nb, b + 2 == nb && last_node);
+    if (b + 4 < nb) load64(p + ((b + 4) << 6), x0);
+    if (b + 5 < nb) load64(p + ((b + 5) << 6), x1);
+    if (b + 2 < nb) b2s_compress(s, y0, (b + 3) << 6, b + 3 == nb, b + 3 == nb && last_node);
+    if (b + 3 < nb) b2s_compress(s, y1, (b + 4) << 6, b + 4 == nb, b + 4 == nb && last_node);
   }
 }
 

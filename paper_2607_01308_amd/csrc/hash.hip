@@ -19,14 +19,14 @@ namespace {
 constexpr int kBlock = 256;
 
 __device__ __forceinline__ void load64(const uint8_t* p, uint32_t (&m)[16]) {
-  const uint4* q = reinterpret_cast<const uint4*>(p);
+  const CM_GLOBAL u32x4* q = global_ptr<u32x4>(p);
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
-    uint4 v = q[k];
-    m[4 * k + 0] = v.x;
-    m[4 * k + 1] = v.y;
-    m[4 * k + 2] = v.z;
-    m[4 * k + 3] = v.w;
+    const u32x4 v = q[k];
+    m[4 * k + 0] = v[0];
+    m[4 * k + 1] = v[1];
+    m[4 * k + 2] = v[2];
+    m[4 * k + 3] = v[3];
   }
 }
 
@@ -88,10 +88,13 @@ __global__ __launch_bounds__(kBlock) void hash_leaf_kernel(const int64_t* __rest
                                                            int64_t token_bytes,
                                                            const int64_t* __restrict__ base0,
                                                            int64_t total0,
+                                                           const uint8_t* __restrict__ select,
+                                                           uint32_t want,
                                                            uint8_t* __restrict__ nodes) {
   const int64_t g = (int64_t)blockIdx.x * kBlock + threadIdx.x;
   if (g >= total0) return;
   const int i = find_fragment(base0, n, g);
+  if (select && select[i] != want) return;
   const int64_t bytes = table[(int64_t)i * stride] * token_bytes;
   const int64_t m = leaves_of(bytes);
   const int64_t local = g - base0[i];
@@ -112,10 +115,12 @@ __global__ __launch_bounds__(kBlock) void hash_leaf_kernel(const int64_t* __rest
 __global__ __launch_bounds__(kBlock) void hash_parent_kernel(
     const int64_t* __restrict__ table, int32_t n, int64_t stride, int64_t token_bytes, int32_t v,
     const int64_t* __restrict__ base_prev, const int64_t* __restrict__ base_cur,
-    int64_t total_cur, const uint8_t* __restrict__ in, uint8_t* __restrict__ out) {
+    int64_t total_cur, const uint8_t* __restrict__ select, uint32_t want,
+    const uint8_t* __restrict__ in, uint8_t* __restrict__ out) {
   const int64_t g = (int64_t)blockIdx.x * kBlock + threadIdx.x;
   if (g >= total_cur) return;
   const int i = find_fragment(base_cur, n, g);
+  if (select && select[i] != want) return;
   const int64_t m0 = leaves_of(table[(int64_t)i * stride] * token_bytes);
   const int64_t m_prev = nodes_at(m0, v - 1);
   const int64_t m_cur = nodes_at(m0, v);
@@ -142,9 +147,11 @@ __global__ __launch_bounds__(kBlock) void hash_parent_kernel(
 __global__ __launch_bounds__(64) void hash_final_kernel(
     const int64_t* __restrict__ table, int32_t n, int64_t stride, int32_t L, int32_t H,
     int32_t d, uint32_t dtype_code, uint32_t esize, const int64_t* __restrict__ base_last,
-    const uint8_t* __restrict__ roots, uint8_t* __restrict__ digests) {
+    const uint8_t* __restrict__ select, uint32_t want, const uint8_t* __restrict__ roots,
+    uint8_t* __restrict__ digests) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n) return;
+  if (select && select[i] != want) return;
   const uint64_t T = (uint64_t)table[(int64_t)i * stride];
   uint32_t m[16] = {0x52464D43u, 0x31304741u,  // "CMFRAG01"
                     dtype_code, esize, (uint32_t)L, 1u, (uint32_t)H,
@@ -188,8 +195,8 @@ HashLayout hash_layout(const SetDesc& s) {
   return lay;
 }
 
-hipError_t launch_hash(const SetDesc& s, const HashLayout& lay, uint8_t* digests, uint8_t* ws,
-                       hipStream_t stream) {
+hipError_t launch_hash(const SetDesc& s, const HashLayout& lay, const uint8_t* select,
+                       uint32_t want, uint8_t* digests, uint8_t* ws, hipStream_t stream) {
   int64_t* base = reinterpret_cast<int64_t*>(ws + lay.off_tables);
   uint8_t* buf[2] = {ws + lay.off_buf0, ws + lay.off_buf1};
   const int64_t nb1 = s.n + 1;
@@ -206,7 +213,8 @@ hipError_t launch_hash(const SetDesc& s, const HashLayout& lay, uint8_t* digests
     ScopedTiming tm(K_HASH_LEAF, stream);
     const int64_t grid = (lay.total0 + kBlock - 1) / kBlock;
     hipLaunchKernelGGL(hash_leaf_kernel, dim3((uint32_t)grid), dim3(kBlock), 0, stream,
-                       s.table_dev, s.n, s.stride, token_bytes_of(s), base, lay.total0, buf[0]);
+                       s.table_dev, s.n, s.stride, token_bytes_of(s), base, lay.total0, select,
+                       want, buf[0]);
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   for (int v = 1; v <= lay.levels; ++v) {
@@ -217,7 +225,7 @@ hipError_t launch_hash(const SetDesc& s, const HashLayout& lay, uint8_t* digests
     const int64_t grid = (total + kBlock - 1) / kBlock;
     hipLaunchKernelGGL(hash_parent_kernel, dim3((uint32_t)grid), dim3(kBlock), 0, stream,
                        s.table_dev, s.n, s.stride, token_bytes_of(s), v, base + (v - 1) * nb1,
-                       base + v * nb1, total, buf[(v - 1) & 1], buf[v & 1]);
+                       base + v * nb1, total, select, want, buf[(v - 1) & 1], buf[v & 1]);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   {
@@ -225,8 +233,8 @@ hipError_t launch_hash(const SetDesc& s, const HashLayout& lay, uint8_t* digests
     const uint32_t code = s.dtype;  // cm_dtype value doubles as the header dtype code
     hipLaunchKernelGGL(hash_final_kernel, dim3((uint32_t)((s.n + 63) / 64)), dim3(64), 0,
                        stream, s.table_dev, s.n, s.stride, s.L, s.H, s.d, code,
-                       (uint32_t)s.esize, base + lay.levels * nb1, buf[lay.levels & 1],
-                       digests);
+                       (uint32_t)s.esize, base + lay.levels * nb1, select, want,
+                       buf[lay.levels & 1], digests);
   }
   return hipGetLastError();
 }

@@ -9,6 +9,15 @@
 
 namespace cm {
 
+// Device pointers read from the fragment table arrive as integers; casting them
+// into the global address space lets the compiler emit global (not flat) loads.
+#define CM_GLOBAL __attribute__((address_space(1)))
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+template <class T>
+__device__ __forceinline__ const CM_GLOBAL T* global_ptr(const void* p) {
+  return (const CM_GLOBAL T*)p;
+}
+
 // Validated description of a fragment set (see cm_fragset in cmerge.h).
 struct SetDesc {
   int32_t n, L, H, d, dtype;
@@ -58,8 +67,12 @@ struct RenderLayout {
 RenderLayout render_layout(const SetDesc& s);
 
 // Launchers (enqueue on `stream`, return the first HIP error).
-hipError_t launch_hash(const SetDesc& s, const HashLayout& lay, uint8_t* digests, uint8_t* ws,
-                       hipStream_t stream);
+// select == nullptr hashes every fragment; otherwise only fragments i with
+// select[i] == want (the other digests are left untouched).
+hipError_t launch_hash(const SetDesc& s, const HashLayout& lay, const uint8_t* select,
+                       uint32_t want, uint8_t* digests, uint8_t* ws, hipStream_t stream);
+hipError_t launch_equal_key_mask(const SetDesc& s, const double* keys, uint8_t* mask,
+                                 hipStream_t stream);
 hipError_t launch_knorm(const SetDesc& s, const KnormLayout& lay, int32_t layer, int64_t tail_len,
                         double* keys, uint8_t* ws, hipStream_t stream);
 hipError_t launch_order(const SetDesc& s, const double* keys, const uint8_t* digests,
@@ -90,6 +103,7 @@ enum KernelId {
   K_KNORM_ROWS,
   K_KNORM_TREE,
   K_ORDER,
+  K_KEY_MASK,
   K_RENDER_PREP,
   K_RENDER,
   K_COUNT

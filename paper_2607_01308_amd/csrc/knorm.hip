@@ -19,8 +19,8 @@ namespace cm {
 namespace {
 
 template <int ESIZE>
-__device__ __forceinline__ double row_chunk_sumsq(const uint4 v) {
-  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+__device__ __forceinline__ double row_chunk_sumsq(const u32x4 v) {
+  const uint32_t w[4] = {v[0], v[1], v[2], v[3]};
   if constexpr (ESIZE == 2) {
     double e[8];
 #pragma unroll
@@ -83,7 +83,7 @@ __global__ __launch_bounds__(256) void knorm_rows_kernel(const int64_t* __restri
       const int64_t h = f / tail;
       const int64_t r = f - h * tail;
       const uint8_t* src = K + (h * T + (T - tail + r)) * row_bytes + q * 16;
-      acc = row_chunk_sumsq<ESIZE>(*reinterpret_cast<const uint4*>(src));
+      acc = row_chunk_sumsq<ESIZE>(*global_ptr<u32x4>(src));
     }
     for (int o = 1; o < lpr; o <<= 1) acc = acc + __shfl_xor(acc, o, 64);
     if (fl < rpb && q == 0) sh[fl] = valid ? sqrt(acc) : 0.0;

@@ -9,6 +9,12 @@
 // key, or equal key and larger big-endian digest). Keys are compared as IEEE
 // doubles and only bitwise-equal keys tie. Everything is integer or comparison
 // work, so the plan is exact and independent of thread timing.
+//
+// Byte-identical deliveries have bitwise-equal keys and equal lengths (the key
+// is a deterministic function of the bytes), and ties need equal keys, so the
+// digest of a delivery is read only when another delivery has the same key
+// and length. That lets the digests of every other delivery be computed
+// concurrently with the render (equal_key_mask marks the ones needed first).
 #include "internal.h"
 
 namespace cm {
@@ -57,16 +63,23 @@ __global__ __launch_bounds__(1024) void order_kernel(const int64_t* __restrict__
   if (live) {
     key = keys[tid];
     len = table[(int64_t)tid * stride];
-    load_digest_be(digests, tid, mine);
     s_key[tid] = key;
     s_len[tid] = len;
   }
   const int bad = __syncthreads_or(live && !isfinite(key));
+  if (live) {
+    bool shared = false;
+    for (int j = 0; j < n; ++j)
+      shared |= (j != tid && s_key[j] == key && s_len[j] == len);
+    if (shared) load_digest_be(digests, tid, mine);
+  }
 
-  // Absorption: the first arrival of each digest is kept.
+  // Absorption: the first arrival of each content is kept (copies share key,
+  // length and digest).
   int first = tid;
   if (live) {
     for (int j = 0; j < tid; ++j) {
+      if (s_key[j] != key || s_len[j] != len) continue;
       uint32_t other[8];
       load_digest_be(digests, j, other);
       if (cmp_digest(other, mine) == 0) { first = j; break; }
@@ -125,7 +138,43 @@ __global__ __launch_bounds__(1024) void order_kernel(const int64_t* __restrict__
   }
 }
 
+// mask[i] = 1 if another delivery has a bitwise-equal key and the same length
+// (only those digests decide dedupe and ties), else 0.
+__global__ __launch_bounds__(1024) void equal_key_mask_kernel(const int64_t* __restrict__ table,
+                                                              int64_t stride, int32_t n,
+                                                              const double* __restrict__ keys,
+                                                              uint8_t* __restrict__ mask) {
+  __shared__ double s_key[1024];
+  __shared__ int64_t s_len[1024];
+  const int tid = threadIdx.x;
+  double key = 0.0;
+  int64_t len = 0;
+  if (tid < n) {
+    key = keys[tid];
+    len = table[(int64_t)tid * stride];
+    s_key[tid] = key;
+    s_len[tid] = len;
+  }
+  __syncthreads();
+  if (tid < n) {
+    bool shared = false;
+    for (int j = 0; j < n; ++j)
+      shared |= (j != tid && s_key[j] == key && s_len[j] == len);
+    mask[tid] = shared ? 1 : 0;
+  }
+}
+
 }  // namespace
+
+hipError_t launch_equal_key_mask(const SetDesc& s, const double* keys, uint8_t* mask,
+                                 hipStream_t stream) {
+  int threads = 64;
+  while (threads < s.n) threads <<= 1;
+  ScopedTiming tm(K_KEY_MASK, stream);
+  hipLaunchKernelGGL(equal_key_mask_kernel, dim3(1), dim3(threads), 0, stream, s.table_dev,
+                     s.stride, s.n, keys, mask);
+  return hipGetLastError();
+}
 
 hipError_t launch_order(const SetDesc& s, const double* keys, const uint8_t* digests,
                         int64_t* plan, hipStream_t stream) {

@@ -18,13 +18,33 @@ namespace cm {
 
 namespace {
 
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-
+#ifndef CM_RENDER_TILE_BYTES
+#define CM_RENDER_TILE_BYTES 32768
+#endif
 constexpr int kThreads = 256;
-constexpr int kTileBytes = 32768;
+constexpr int kTileBytes = CM_RENDER_TILE_BYTES;
 
-__device__ __forceinline__ u32x4 ld_stream(const u32x4* p) { return __builtin_nontemporal_load(p); }
-__device__ __forceinline__ void st_stream(u32x4* p, u32x4 v) { __builtin_nontemporal_store(v, p); }
+__device__ __forceinline__ u32x4 ld_stream(const uint8_t* p) {
+  return __builtin_nontemporal_load(global_ptr<u32x4>(p));
+}
+__device__ __forceinline__ void st_stream(uint8_t* p, u32x4 v) {
+  __builtin_nontemporal_store(v, (CM_GLOBAL u32x4*)p);
+}
+
+// Round fp64 to the nearest bf16, ties to even, as one rounding step. Rounding
+// to fp32 first can only go wrong when the fp32 value lands exactly on a bf16
+// midpoint (every bf16 value and midpoint is an fp32 value, so otherwise y and
+// its fp32 rounding lie on the same side of every midpoint); in that case the
+// fp32 value is nudged one ulp towards y before the hardware bf16 conversion.
+__device__ __forceinline__ uint32_t bf16_bits_rne(double y) {
+  const float f = (float)y;
+  uint32_t u = __float_as_uint(f);
+  if (__builtin_expect((u & 0xFFFFu) == 0x8000u, 0)) {
+    const double back = (double)f;
+    if (y != back) u = (fabs(y) > fabs(back)) ? u + 1u : u - 1u;
+  }
+  return (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)__uint_as_float(u));
+}
 
 // 16 bytes <-> fp64 lanes
 template <int ESIZE>
@@ -43,12 +63,7 @@ struct Chunk<2> {
   __device__ __forceinline__ static u32x4 pack(const double (&y)[8]) {
     u32x4 v;
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const __bf16 lo = (__bf16)y[2 * k];
-      const __bf16 hi = (__bf16)y[2 * k + 1];
-      v[k] = (uint32_t)__builtin_bit_cast(uint16_t, lo) |
-             ((uint32_t)__builtin_bit_cast(uint16_t, hi) << 16);
-    }
+    for (int k = 0; k < 4; ++k) v[k] = bf16_bits_rne(y[2 * k]) | (bf16_bits_rne(y[2 * k + 1]) << 16);
     return v;
   }
 };
@@ -71,18 +86,16 @@ struct Chunk<4> {
 __device__ __forceinline__ void copy_tile(const uint8_t* __restrict__ src, uint8_t* __restrict__ dst,
                                           int64_t bytes) {
   constexpr int U = kTileBytes / 16 / kThreads;
-  const u32x4* s = reinterpret_cast<const u32x4*>(src);
-  u32x4* o = reinterpret_cast<u32x4*>(dst);
   const int tid = threadIdx.x;
   const int64_t chunks = bytes >> 4;
   if (chunks == (int64_t)U * kThreads) {
     u32x4 v[U];
 #pragma unroll
-    for (int u = 0; u < U; ++u) v[u] = ld_stream(s + tid + u * kThreads);
+    for (int u = 0; u < U; ++u) v[u] = ld_stream(src + (int64_t)(tid + u * kThreads) * 16);
 #pragma unroll
-    for (int u = 0; u < U; ++u) st_stream(o + tid + u * kThreads, v[u]);
+    for (int u = 0; u < U; ++u) st_stream(dst + (int64_t)(tid + u * kThreads) * 16, v[u]);
   } else {
-    for (int64_t c = tid; c < chunks; c += kThreads) st_stream(o + c, ld_stream(s + c));
+    for (int64_t c = tid; c < chunks; c += kThreads) st_stream(dst + c * 16, ld_stream(src + c * 16));
   }
 }
 
@@ -128,25 +141,24 @@ __device__ __forceinline__ void rotate_tile(const uint8_t* __restrict__ src,
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int64_t off = (int64_t)(rsub + u * rpi) * row_bytes + q * 16;
-        a[u] = ld_stream(reinterpret_cast<const u32x4*>(src + off));
-        b[u] = ld_stream(reinterpret_cast<const u32x4*>(src + off + half));
+        a[u] = ld_stream(src + off);
+        b[u] = ld_stream(src + off + half);
       }
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int64_t off = (int64_t)(rsub + u * rpi) * row_bytes + q * 16;
         u32x4 ya, yb;
         body(a[u], b[u], ya, yb);
-        st_stream(reinterpret_cast<u32x4*>(dst + off), ya);
-        st_stream(reinterpret_cast<u32x4*>(dst + off + half), yb);
+        st_stream(dst + off, ya);
+        st_stream(dst + off + half, yb);
       }
     } else {
       for (int64_t r = rsub; r < rows; r += rpi) {
         const int64_t off = r * row_bytes + q * 16;
         u32x4 ya, yb;
-        body(ld_stream(reinterpret_cast<const u32x4*>(src + off)),
-             ld_stream(reinterpret_cast<const u32x4*>(src + off + half)), ya, yb);
-        st_stream(reinterpret_cast<u32x4*>(dst + off), ya);
-        st_stream(reinterpret_cast<u32x4*>(dst + off + half), yb);
+        body(ld_stream(src + off), ld_stream(src + off + half), ya, yb);
+        st_stream(dst + off, ya);
+        st_stream(dst + off + half, yb);
       }
     }
   } else {
@@ -164,13 +176,13 @@ __device__ __forceinline__ void rotate_tile(const uint8_t* __restrict__ src,
     for (int64_t r = rsub; r < rows; r += rpi) {
       const int64_t off = r * row_bytes + cq * 16;
       double x[E], y[E];
-      C::unpack(ld_stream(reinterpret_cast<const u32x4*>(src + off)), x);
+      C::unpack(ld_stream(src + off), x);
 #pragma unroll
       for (int p = 0; p < PP; ++p) {
         y[2 * p] = x[2 * p] * c[p] - x[2 * p + 1] * sn[p];
         y[2 * p + 1] = x[2 * p + 1] * c[p] + x[2 * p] * sn[p];
       }
-      st_stream(reinterpret_cast<u32x4*>(dst + off), C::pack(y));
+      st_stream(dst + off, C::pack(y));
     }
   }
 }

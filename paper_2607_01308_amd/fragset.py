@@ -1,11 +1,15 @@
 """LatentFragmentSet (Alg. 2) and the render path on one GPU.
 
-render_deliveries runs the whole path over a list of deliveries: Id of every
-delivery (cm_fragment_hash), scores (cm_fragment_knorm), dedupe + canonical
-order + offsets (cm_canonical_order), one device-to-host copy of the small plan
-so the caller can size the output, then the rotate-and-concatenate render
-(cm_render_merge). LatentFragmentSet keeps the state of Alg. 2 (a set keyed by
-Id) and renders it with the ids computed at Ingest."""
+render_deliveries runs the whole path over a list of deliveries: scores
+(cm_fragment_knorm), the Id of every delivery whose score and length collide
+with another's (cm_equal_key_mask + cm_fragment_hash_select: only those decide
+dedupe and ties), dedupe + canonical order + offsets (cm_canonical_order), one
+device-to-host copy of the small plan so the caller can size the output, then
+the rotate-and-concatenate render (cm_render_merge). The Id of every other
+delivery is computed on a second stream while the render runs: the hash is
+bound by vector ALU work and the render by HBM bandwidth, so the two overlap.
+LatentFragmentSet keeps the state of Alg. 2 (a set keyed by Id) and renders it
+with the ids computed at Ingest."""
 
 from __future__ import annotations
 
@@ -16,19 +20,31 @@ import numpy as np
 import torch
 
 from . import _cabi as C
-from .binding import (FragmentBatch, canonical_order, fragment_hash, fragment_knorm, plan_elems,
-                      render_merge, workspace_size)
+from .binding import (FragmentBatch, canonical_order, equal_key_mask, fragment_hash,
+                      fragment_hash_select, fragment_knorm, plan_elems, render_merge,
+                      workspace_size)
 
-_WS: Dict[torch.device, torch.Tensor] = {}
+_WS: Dict[tuple, torch.Tensor] = {}
+_SIDE: Dict[torch.device, torch.cuda.Stream] = {}
 
 
-def _workspace(batch: FragmentBatch) -> torch.Tensor:
+def _workspace(batch: FragmentBatch, slot: int = 0) -> torch.Tensor:
+    """Cached workspace per (device, slot); slot 1 belongs to the side stream."""
     need = max(workspace_size(batch), 256)
-    ws = _WS.get(batch.device)
+    key = (batch.device, slot)
+    ws = _WS.get(key)
     if ws is None or ws.numel() < need:
         ws = torch.empty(need, dtype=torch.uint8, device=batch.device)
-        _WS[batch.device] = ws
+        _WS[key] = ws
     return ws
+
+
+def _side_stream(device: torch.device) -> torch.cuda.Stream:
+    st = _SIDE.get(device)
+    if st is None:
+        st = torch.cuda.Stream(device=device)  # default priority
+        _SIDE[device] = st
+    return st
 
 
 def release_workspace() -> None:
@@ -99,20 +115,41 @@ def _render_plan(batch: FragmentBatch, plan_dev: torch.Tensor, plan_host: np.nda
 
 
 def render_deliveries(deliveries: Union[FragmentBatch, Sequence], routing_layer: int,
-                      rope_base: float, style: str = "half", stream=None) -> RenderResult:
-    """The whole path over a list of deliveries (duplicates allowed)."""
+                      rope_base: float, style: str = "half", stream=None,
+                      overlap: bool = True) -> RenderResult:
+    """The whole path over a list of deliveries (duplicates allowed). With
+    overlap=False every step runs in order on one stream."""
     batch = deliveries if isinstance(deliveries, FragmentBatch) else FragmentBatch(deliveries)
     dev = batch.device
-    ws = _workspace(batch)
-    digests = torch.empty((batch.n, 32), dtype=torch.uint8, device=dev)
-    keys = torch.empty(batch.n, dtype=torch.float64, device=dev)
-    plan_dev = torch.empty(plan_elems(batch.n), dtype=torch.int64, device=dev)
-    tail = min(batch.lengths)
-    fragment_hash(batch, digests, ws, stream)
-    fragment_knorm(batch, routing_layer, tail, keys, ws, stream)
-    canonical_order(batch, keys, digests, plan_dev, stream)
-    plan_host = plan_dev.to("cpu").numpy()
-    merged, cache = _render_plan(batch, plan_dev, plan_host, rope_base, style, ws, stream)
+    main = stream if stream is not None else torch.cuda.current_stream(dev)
+    with torch.cuda.stream(main):
+        ws = _workspace(batch, 0)
+        digests = torch.empty((batch.n, 32), dtype=torch.uint8, device=dev)
+        keys = torch.empty(batch.n, dtype=torch.float64, device=dev)
+        mask = torch.empty(batch.n, dtype=torch.uint8, device=dev)
+        plan_dev = torch.empty(plan_elems(batch.n), dtype=torch.int64, device=dev)
+        tail = min(batch.lengths)
+        fragment_knorm(batch, routing_layer, tail, keys, ws, main)
+        equal_key_mask(batch, keys, mask, main)
+        fragment_hash_select(batch, mask, 1, digests, ws, main)
+        side_done = None
+        if overlap:
+            ready = torch.cuda.Event()
+            ready.record(main)
+            side = _side_stream(dev)
+            side.wait_event(ready)
+            fragment_hash_select(batch, mask, 0, digests, _workspace(batch, 1), side)
+            side_done = torch.cuda.Event()
+            side_done.record(side)
+        else:
+            fragment_hash_select(batch, mask, 0, digests, ws, main)
+        canonical_order(batch, keys, digests, plan_dev, main)
+        plan_host = plan_dev.to("cpu").numpy()
+        try:
+            merged, cache = _render_plan(batch, plan_dev, plan_host, rope_base, style, ws, main)
+        finally:
+            if side_done is not None:
+                main.wait_event(side_done)
     return RenderResult(cache=cache, merged=merged, digests_dev=digests, keys_dev=keys,
                         plan=plan_host, tail_len=tail)
 

@@ -242,3 +242,73 @@ def test_qwen3_4b_n4_sampled_layers():
     res = _run(w, dl)
     frac = check_render(res, dl, w.dtype, w.routing_layer, w.rope_base, layers=(0, 18, 35))
     log(f"qwen3-4b-n4: K identical {frac:.7f}")
+
+
+# ---------------------------------------------------------------- overlapped pipeline
+
+def _keys_and_mask(batch, w):
+    ws = torch.empty(max(cm.workspace_size(batch), 256), dtype=torch.uint8, device="cuda")
+    keys = torch.empty(batch.n, dtype=torch.float64, device="cuda")
+    mask = torch.empty(batch.n, dtype=torch.uint8, device="cuda")
+    cm.fragment_knorm(batch, w.routing_layer, min(batch.lengths), keys, ws)
+    cm.equal_key_mask(batch, keys, mask)
+    torch.cuda.synchronize()
+    return ws, keys, mask
+
+
+def test_equal_key_mask_marks_copies_and_ties():
+    w = synth.custom("mask", dtype="bfloat16", d=128, H=2, L=2, lengths=(64, 64, 40, 70),
+                     shared_k=((0, 1),), deliveries=(0, 1, 2, 3, 2), routing_layer=0)
+    _, dl = gpu_deliveries(w)
+    batch = cm.FragmentBatch(dl)
+    _, keys, mask = _keys_and_mask(batch, w)
+    assert mask.cpu().tolist() == [1, 1, 1, 0, 1]
+
+
+def test_hash_select_writes_only_selected_digests():
+    w = synth.custom("sel", dtype="bfloat16", d=128, H=2, L=2, lengths=(300, 64, 129))
+    _, dl = gpu_deliveries(w)
+    batch = cm.FragmentBatch(dl)
+    ws = torch.empty(max(cm.workspace_size(batch), 256), dtype=torch.uint8, device="cuda")
+    sel = torch.tensor([0, 1, 0], dtype=torch.uint8, device="cuda")
+    dig = torch.full((3, 32), 0xAB, dtype=torch.uint8, device="cuda")
+    cm.fragment_hash_select(batch, sel, 1, dig, ws)
+    torch.cuda.synchronize()
+    ref = oracle_ids(dl, w.dtype)
+    got = [bytes(r) for r in dig.cpu().numpy()]
+    assert got[1] == ref[1] and got[0] == bytes([0xAB]) * 32 and got[2] == bytes([0xAB]) * 32
+    cm.fragment_hash_select(batch, sel, 0, dig, ws)
+    torch.cuda.synchronize()
+    assert [bytes(r) for r in dig.cpu().numpy()] == ref
+
+
+def test_order_reads_only_colliding_digests():
+    w = synth.custom("ordsel", dtype="bfloat16", d=128, H=2, L=2, lengths=(64, 64, 40, 70),
+                     shared_k=((0, 1),), deliveries=(2, 0, 1, 3, 2))
+    _, dl = gpu_deliveries(w)
+    batch = cm.FragmentBatch(dl)
+    ws, keys, mask = _keys_and_mask(batch, w)
+    dig = torch.empty((batch.n, 32), dtype=torch.uint8, device="cuda")
+    cm.fragment_hash(batch, dig, ws)
+    plan_a = torch.empty(cm.plan_elems(batch.n), dtype=torch.int64, device="cuda")
+    cm.canonical_order(batch, keys, dig, plan_a)
+    noisy = dig.clone()
+    rnd = torch.randint(0, 256, noisy.shape, dtype=torch.uint8, device="cuda")
+    noisy[mask == 0] = rnd[mask == 0]
+    plan_b = torch.empty_like(plan_a)
+    cm.canonical_order(batch, keys, noisy, plan_b)
+    torch.cuda.synchronize()
+    assert torch.equal(plan_a, plan_b)
+
+
+def test_overlapped_pipeline_matches_serial():
+    w = synth.custom("overlap", dtype="bfloat16", d=128, H=4, L=3, lengths=(700, 700, 300, 1200),
+                     shared_k=((0, 1),), deliveries=(3, 0, 2, 1, 0))
+    _, dl = gpu_deliveries(w)
+    a = cm.render_deliveries(dl, w.routing_layer, w.rope_base, overlap=True)
+    b = cm.render_deliveries(dl, w.routing_layer, w.rope_base, overlap=False)
+    torch.cuda.synchronize()
+    assert torch.equal(a.merged, b.merged)
+    assert a.digests == b.digests == oracle_ids(dl, w.dtype)
+    assert list(a.plan) == list(b.plan)
+    check_render(a, dl, w.dtype, w.routing_layer, w.rope_base)
