@@ -120,13 +120,16 @@ int32_t cm_workspace_size(const cm_fragset* set, size_t* bytes_out);
  * Id of Alg. 2 (content address; also the hash tiebreak of §4.3): for every
  * fragment, a 32-byte digest of its shapes, dtype and the raw bytes of
  * K^0, V^0, ..., K^{L-1}, V^{L-1} in that order. Function: per tensor a BLAKE2s-256
- * (RFC 7693) binary tree over 4 KiB leaves (fanout 2, depth 255, leaf 4096,
- * inner 32; leaf k: node_offset k, depth 0; parent j at level v: node_offset j,
- * depth v, children 2j and 2j+1; last_node on the last node of each level; an
- * unpaired last node is carried up unchanged); then a sequential BLAKE2s-256 of
- * a 64-byte header (magic "CMFRAG01", u32 dtype code 0=fp32 1=bf16, u32 element
- * bytes, u32 L, u32 batch=1, u32 H, u64 T, u32 d, zero pad; little-endian)
- * followed by the 2L tensor roots.
+ * (RFC 7693) binary tree (fanout 2, depth 255, leaf 4096, inner 32) over striped
+ * leaves: the tensor's 64-byte blocks are grouped in stripes of 4096 blocks
+ * (256 KiB, the last may be shorter) and leaf 64*s + k is blocks k, k+64, k+128,
+ * ... of stripe s (k < min(64, blocks in the stripe)); leaf j is hashed with
+ * node_offset j, depth 0; parent j at level v with node_offset j, depth v,
+ * children 2j and 2j+1; last_node on the last node of each level; an unpaired
+ * last node is carried up unchanged. Then a sequential BLAKE2s-256 of a 64-byte
+ * header (magic "CMFRAG01", u32 dtype code 0=fp32 1=bf16, u32 element bytes,
+ * u32 L, u32 batch=1, u32 H, u64 T, u32 d, zero pad; little-endian) followed by
+ * the 2L tensor roots.
  * digests_dev: device, n * 32 bytes, written in delivery order. */
 int32_t cm_fragment_hash(const cm_fragset* set, uint8_t* digests_dev,
                          void* workspace, size_t workspace_bytes, void* stream);

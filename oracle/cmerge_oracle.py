@@ -8,8 +8,9 @@ What each function follows:
     Alg. 2 (§4.5) and the hash tiebreak of §4.3 ("shapes, dtypes and raw bytes
     of every layer's K and V", order K1,V1,...,KL,VL, unshifted). The paper names
     no hash function; the reading used here is BLAKE2s-256 (RFC 7693) in tree
-    mode over 4 KiB leaves per tensor, then a sequential BLAKE2s over a 64-byte
-    shape/dtype header followed by the tensor roots.
+    mode over striped leaves of at most 4 KiB per tensor (see tensor_leaves),
+    then a sequential BLAKE2s over a 64-byte shape/dtype header followed by the
+    tensor roots.
   * FragmentSet: Ingest and Merge of Alg. 2 — set union keyed by Id, Eq. (5).
   * fragment_key / mean_knorm: Eq. (3) (§4.3) and Alg. 1 — mean L2 norm of the
     routing layer's K rows over the last T* = min_j T_j positions, averaged over
@@ -37,7 +38,10 @@ from typing import Dict, Iterable, List, Sequence, Tuple
 
 import numpy as np
 
-LEAF_BYTES = 4096          # tree-hash leaf size (bytes)
+LEAF_BYTES = 4096          # tree-hash leaf size (bytes), the maximum
+BLOCK_BYTES = 64           # BLAKE2s message block
+STRIPE_LEAVES = 64         # leaves interleaved in one stripe
+STRIPE_BYTES = STRIPE_LEAVES * LEAF_BYTES   # 256 KiB
 _DIGEST = 32               # BLAKE2s-256
 # dtype -> (header code, element bytes)
 _DTYPE_INFO = {"float32": (0, 4), "bfloat16": (1, 2)}
@@ -92,19 +96,40 @@ def _blake2s_node(data, node_offset: int, node_depth: int, last_node: bool) -> b
                            last_node=last_node).digest()
 
 
-def tensor_root(buf) -> bytes:
-    """Root of the binary tree over one tensor's raw bytes.
+def tensor_leaves(buf) -> List[bytes]:
+    """Leaf messages of one tensor, in leaf order.
 
-    Level 0: 4 KiB leaves (the last may be short), leaf k hashed with
-    node_offset=k, node_depth=0, last_node on the last leaf. Level l >= 1: node j
-    hashes the concatenated digests of children 2j and 2j+1 (node_offset=j,
-    node_depth=l, last_node on the last node of the level); an unpaired last
-    child is carried up unchanged. The single node left is the root."""
-    mv = memoryview(buf).cast("B")
-    n = len(mv)
-    nleaves = max(1, -(-n // LEAF_BYTES))
-    level = [_blake2s_node(mv[k * LEAF_BYTES:(k + 1) * LEAF_BYTES], k, 0, k == nleaves - 1)
-             for k in range(nleaves)]
+    The raw bytes (a multiple of 64) are cut into 64-byte blocks and the blocks
+    into stripes of 4096 blocks (256 KiB; the last stripe may be shorter). In a
+    stripe with B blocks, leaf k (k < min(64, B)) is the concatenation of blocks
+    k, k + 64, k + 128, ... of that stripe, so a full leaf is 4 KiB. Leaves are
+    numbered stripe by stripe: leaf index = 64 * stripe + k."""
+    raw = np.frombuffer(memoryview(buf).cast("B"), dtype=np.uint8)
+    n = raw.size
+    if n == 0:
+        return [b""]
+    if n % BLOCK_BYTES:
+        raise ValueError("tensor bytes must be a multiple of 64")
+    blocks = raw.reshape(-1, BLOCK_BYTES)
+    leaves = []
+    for s0 in range(0, blocks.shape[0], STRIPE_BYTES // BLOCK_BYTES):
+        stripe = blocks[s0:s0 + STRIPE_BYTES // BLOCK_BYTES]
+        for k in range(min(STRIPE_LEAVES, stripe.shape[0])):
+            leaves.append(stripe[k::STRIPE_LEAVES].tobytes())
+    return leaves
+
+
+def tensor_root(buf) -> bytes:
+    """Root of the binary tree over one tensor's leaves (tensor_leaves).
+
+    Level 0: leaf k hashed with node_offset=k, node_depth=0, last_node on the
+    last leaf. Level l >= 1: node j hashes the concatenated digests of children
+    2j and 2j+1 (node_offset=j, node_depth=l, last_node on the last node of the
+    level); an unpaired last child is carried up unchanged. The single node left
+    is the root."""
+    leaves = tensor_leaves(buf)
+    nleaves = len(leaves)
+    level = [_blake2s_node(leaf, k, 0, k == nleaves - 1) for k, leaf in enumerate(leaves)]
     depth = 0
     while len(level) > 1:
         depth += 1

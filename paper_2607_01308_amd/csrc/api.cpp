@@ -143,6 +143,21 @@ hipError_t drain_pending() {
 
 namespace cm {
 
+int device_cu_count() {
+  static std::mutex mu;
+  static int counts[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  std::lock_guard<std::mutex> lk(mu);
+  if (counts[dev] == 0) {
+    int cu = 0;
+    if (hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cu <= 0)
+      cu = 256;
+    counts[dev] = cu;
+  }
+  return counts[dev];
+}
+
 ScopedTiming::ScopedTiming(int kernel_id, hipStream_t stream) : id_(kernel_id), stream_(stream) {
   if (!g_timing.load(std::memory_order_relaxed)) return;
   start_ = take_event();

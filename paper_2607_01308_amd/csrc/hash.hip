@@ -1,14 +1,15 @@
 // Step 1 — content address Id of Alg. 2 (also the hash tiebreak of §4.3).
 //
-// Per tensor, a BLAKE2s-256 binary tree over 4 KiB leaves; per fragment, a
+// Per tensor, a BLAKE2s-256 binary tree over striped leaves; per fragment, a
 // sequential BLAKE2s-256 of a 64-byte shape/dtype header followed by the 2L
-// tensor roots (K^0, V^0, ..., K^{L-1}, V^{L-1}). The work is VALU-bound
-// (12 VALU ops per G step, 960 per 64-byte block), so the layout aims at keeping
-// every SIMD busy: one lane hashes one whole 4 KiB leaf (64 dependent
-// compressions with the next block's loads in flight), every tensor of every
-// fragment is flattened into one leaf grid, and each upper tree level is one
-// launch over all tensors at full lane occupancy (the parents add 1/64 of the
-// leaf work).
+// tensor roots (K^0, V^0, ..., K^{L-1}, V^{L-1}). A tensor's 64-byte blocks are
+// grouped in stripes of 4096 blocks (256 KiB); leaf k of a stripe is blocks
+// k, k+64, k+128, ... of it. That layout is chosen for 64-wide wavefronts: one
+// wave takes one stripe, lane k hashes leaf k (64 dependent compressions with
+// the next blocks in flight), and at every step the wave reads 4 KiB of
+// contiguous memory. The work is VALU-bound (12 VALU ops per G step, 960 per
+// block); each upper tree level is one launch over all tensors at full lane
+// occupancy (the parents add 1/64 of the leaf work).
 #include "blake2s.h"
 #include "internal.h"
 
@@ -17,6 +18,10 @@ namespace cm {
 namespace {
 
 constexpr int kBlock = 256;
+#ifndef CM_HASH_BLOCKS_PER_CU
+#define CM_HASH_BLOCKS_PER_CU 2
+#endif
+constexpr int kLeafBlocksPerCu = CM_HASH_BLOCKS_PER_CU;
 
 __device__ __forceinline__ void load64(const uint8_t* p, uint32_t (&m)[16]) {
   const CM_GLOBAL u32x4* q = global_ptr<u32x4>(p);
@@ -36,8 +41,18 @@ __device__ __forceinline__ void store_digest(uint8_t* out, const B2sState& s) {
   q[1] = make_uint4(s.h[4], s.h[5], s.h[6], s.h[7]);
 }
 
+constexpr int64_t kStripeBlocks = 4096;  // 64 leaves x 64 blocks = 256 KiB
+constexpr int kStripeLeaves = 64;
+
+// Leaves per tensor of `bytes` (a positive multiple of 64).
 __host__ __device__ __forceinline__ int64_t leaves_of(int64_t bytes) {
-  return (bytes + kLeafBytes - 1) / kLeafBytes;
+  const int64_t blocks = bytes >> 6;
+  const int64_t rest = blocks % kStripeBlocks;
+  return kStripeLeaves * (blocks / kStripeBlocks) + (rest < kStripeLeaves ? rest : kStripeLeaves);
+}
+
+__host__ __device__ __forceinline__ int64_t stripes_of(int64_t bytes) {
+  return ((bytes >> 6) + kStripeBlocks - 1) / kStripeBlocks;
 }
 
 // Nodes per tensor at tree level v: ceil(m0 / 2^v).
@@ -56,7 +71,9 @@ __device__ __forceinline__ int find_fragment(const int64_t* __restrict__ base, i
 }
 
 // base[v][i] = number of level-v nodes of fragments 0..i-1 (all 2L tensors each);
-// base[v][n] = total nodes at level v. One workgroup, block-wide inclusive scan.
+// base[v][n] = total nodes at level v; row levels+1 holds the same prefix sums
+// of the (tensor, stripe) tasks of the leaf kernel. One workgroup, block-wide
+// inclusive scans.
 __global__ __launch_bounds__(1024) void hash_prep_kernel(const int64_t* __restrict__ table,
                                                          int32_t n, int64_t stride,
                                                          int64_t token_bytes, int32_t L,
@@ -64,9 +81,11 @@ __global__ __launch_bounds__(1024) void hash_prep_kernel(const int64_t* __restri
                                                          int64_t* __restrict__ base) {
   __shared__ int64_t sc[1024];
   const int tid = threadIdx.x;
-  const int64_t m0 = tid < n ? leaves_of(table[(int64_t)tid * stride] * token_bytes) : 0;
-  for (int v = 0; v <= levels; ++v) {
-    const int64_t x = tid < n ? 2 * (int64_t)L * nodes_at(m0, v) : 0;
+  const int64_t bytes = tid < n ? table[(int64_t)tid * stride] * token_bytes : 0;
+  const int64_t m0 = tid < n ? leaves_of(bytes) : 0;
+  for (int v = 0; v <= levels + 1; ++v) {
+    const int64_t per = v <= levels ? nodes_at(m0, v) : stripes_of(bytes);
+    const int64_t x = tid < n ? 2 * (int64_t)L * per : 0;
     sc[tid] = x;
     __syncthreads();
     for (int off = 1; off < (int)blockDim.x; off <<= 1) {
@@ -82,32 +101,45 @@ __global__ __launch_bounds__(1024) void hash_prep_kernel(const int64_t* __restri
   }
 }
 
-// One lane = one 4 KiB leaf (the last leaf of a tensor may be shorter).
+// One wave = one (tensor, stripe) task at a time; lane k hashes leaf k of the
+// stripe, whose blocks lie 4 KiB apart. The grid is bounded (a few workgroups
+// per CU) and strides over all tasks: a VALU-bound kernel saturates the SIMDs
+// with a couple of waves each, and the wave slots left free let an HBM-bound
+// kernel on another stream run on the same CUs.
 __global__ __launch_bounds__(kBlock) void hash_leaf_kernel(const int64_t* __restrict__ table,
                                                            int32_t n, int64_t stride,
                                                            int64_t token_bytes,
                                                            const int64_t* __restrict__ base0,
-                                                           int64_t total0,
+                                                           const int64_t* __restrict__ task_base,
+                                                           int64_t total_tasks,
                                                            const uint8_t* __restrict__ select,
                                                            uint32_t want,
                                                            uint8_t* __restrict__ nodes) {
-  const int64_t g = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-  if (g >= total0) return;
-  const int i = find_fragment(base0, n, g);
-  if (select && select[i] != want) return;
-  const int64_t bytes = table[(int64_t)i * stride] * token_bytes;
-  const int64_t m = leaves_of(bytes);
-  const int64_t local = g - base0[i];
-  const int64_t t = local / m;
-  const int64_t k = local - t * m;
-  const uint8_t* p = reinterpret_cast<const uint8_t*>(table[(int64_t)i * stride + 1 + t]) +
-                     (k << 12);
-  const int64_t len = bytes - (k << 12) < kLeafBytes ? bytes - (k << 12) : kLeafBytes;
-  B2sState s;
-  b2s_init_tree(s, (uint64_t)k, 0);
-  b2s_node_aligned(s, p, (uint64_t)len, k == m - 1,
-                   [](const uint8_t* q, uint32_t (&w)[16]) { load64(q, w); });
-  store_digest(nodes + g * 32, s);
+  const int lane = threadIdx.x & 63;
+  const int64_t waves = (int64_t)gridDim.x * (kBlock / 64);
+  for (int64_t task = (int64_t)blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6); task < total_tasks;
+       task += waves) {
+    const int i = find_fragment(task_base, n, task);
+    if (select && select[i] != want) continue;
+    const int64_t bytes = table[(int64_t)i * stride] * token_bytes;
+    const int64_t stripes = stripes_of(bytes);
+    const int64_t m = leaves_of(bytes);
+    const int64_t local = task - task_base[i];
+    const int64_t t = local / stripes;
+    const int64_t sidx = local - t * stripes;
+    const int64_t in_stripe = (bytes >> 6) - sidx * kStripeBlocks;
+    const int64_t blocks_here = in_stripe < kStripeBlocks ? in_stripe : kStripeBlocks;
+    if (lane >= blocks_here) continue;
+    const int64_t nb = (blocks_here - lane + kStripeLeaves - 1) / kStripeLeaves;
+    const int64_t leaf = sidx * kStripeLeaves + lane;
+    const uint8_t* p = reinterpret_cast<const uint8_t*>(table[(int64_t)i * stride + 1 + t]) +
+                       ((sidx * kStripeBlocks + lane) << 6);
+    B2sState s;
+    b2s_init_tree(s, (uint64_t)leaf, 0);
+    b2s_node_blocks(s, p, (uint64_t)nb, (uint64_t)kStripeLeaves * 64, leaf == m - 1,
+                    [](const uint8_t* q, uint32_t (&w)[16]) { load64(q, w); });
+    store_digest(nodes + (base0[i] + t * m + leaf) * 32, s);
+  }
 }
 
 // Level v >= 1: node j of a tensor hashes children 2j, 2j+1 of level v-1;
@@ -177,6 +209,7 @@ HashLayout hash_layout(const SetDesc& s) {
   HashLayout lay{};
   int64_t max_m0 = 1;
   for (int i = 0; i < s.n; ++i) {
+    lay.tasks += 2 * (int64_t)s.L * stripes_of(s.T(i) * token_bytes_of(s));
     const int64_t m0 = leaves_of(s.T(i) * token_bytes_of(s));
     if (m0 > max_m0) max_m0 = m0;
     lay.total0 += 2 * (int64_t)s.L * m0;
@@ -186,7 +219,7 @@ HashLayout hash_layout(const SetDesc& s) {
   if (lay.levels == 0) lay.total1 = 0;
   size_t off = 0;
   lay.off_tables = off;
-  off = align_up(off + sizeof(int64_t) * (size_t)(lay.levels + 1) * (size_t)(s.n + 1), kWsAlign);
+  off = align_up(off + sizeof(int64_t) * (size_t)(lay.levels + 2) * (size_t)(s.n + 1), kWsAlign);
   lay.off_buf0 = off;
   off = align_up(off + 32 * (size_t)lay.total0, kWsAlign);
   lay.off_buf1 = off;
@@ -211,10 +244,12 @@ hipError_t launch_hash(const SetDesc& s, const HashLayout& lay, const uint8_t* s
   if (e != hipSuccess) return e;
   {
     ScopedTiming tm(K_HASH_LEAF, stream);
-    const int64_t grid = (lay.total0 + kBlock - 1) / kBlock;
+    const int64_t full = (lay.tasks + (kBlock / 64) - 1) / (kBlock / 64);
+    const int64_t cap = (int64_t)device_cu_count() * kLeafBlocksPerCu;
+    const int64_t grid = full < cap ? full : cap;
     hipLaunchKernelGGL(hash_leaf_kernel, dim3((uint32_t)grid), dim3(kBlock), 0, stream,
-                       s.table_dev, s.n, s.stride, token_bytes_of(s), base, lay.total0, select,
-                       want, buf[0]);
+                       s.table_dev, s.n, s.stride, token_bytes_of(s), base,
+                       base + (int64_t)(lay.levels + 1) * nb1, lay.tasks, select, want, buf[0]);
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   for (int v = 1; v <= lay.levels; ++v) {

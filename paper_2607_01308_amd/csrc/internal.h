@@ -34,13 +34,18 @@ constexpr size_t kWsAlign = 256;
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
-// Tree-hash geometry of a set: leaves per tensor of fragment i at level 0 is
-// m0(i) = ceil(H*T_i*d*esize / 4096); level v has ceil(m0 / 2^v) nodes.
+// Compute units of the current device (cached per device).
+int device_cu_count();
+
+// Tree-hash geometry of a set: a tensor of B bytes has B/64 blocks in stripes
+// of 4096 and m0 = 64 * full stripes + min(64, blocks of the last stripe)
+// leaves; level v has ceil(m0 / 2^v) nodes.
 struct HashLayout {
   int32_t levels;         // parent levels above the leaves (0 if every tensor is one leaf)
+  int64_t tasks;          // (tensor, stripe) work items of the leaf kernel
   int64_t total0;         // nodes at level 0 over all tensors
   int64_t total1;         // nodes at level 1 over all tensors (0 if levels == 0)
-  size_t off_tables;      // int64 [levels+1][n+1] per-level node bases
+  size_t off_tables;      // int64 [levels+2][n+1]: per-level node bases, then task bases
   size_t off_buf0;        // level-0 (and even levels) node digests
   size_t off_buf1;        // odd levels
   size_t bytes;           // total workspace bytes

@@ -55,10 +55,12 @@ def test_sequential_matches_hashlib(hc):
 
 def test_tensor_root_from_library_nodes(hc):
     """Rebuild the oracle's per-tensor tree with the library's node function."""
+    from oracle import cmerge_oracle as om
     rng = np.random.default_rng(3)
-    buf = rng.integers(0, 256, size=5 * 4096 + 1024, dtype=np.uint8).tobytes()
-    m = -(-len(buf) // 4096)
-    level = [_node(hc, buf[k * 4096:(k + 1) * 4096], k, 0, k == m - 1) for k in range(m)]
+    buf = rng.integers(0, 256, size=262144 + 5 * 4096 + 1024, dtype=np.uint8).tobytes()
+    leaves = om.tensor_leaves(buf)
+    m = len(leaves)
+    level = [_node(hc, leaf, k, 0, k == m - 1) for k, leaf in enumerate(leaves)]
     depth = 0
     while len(level) > 1:
         depth += 1

@@ -33,8 +33,33 @@ def test_tree_parameters_take_effect():
     assert om._blake2s_node(data, 0, 0, False) != node     # last-node flag
 
 
-@pytest.mark.parametrize("m", [1, 2, 3, 5, 8, 13])
-def test_tree_schedule_closed_form(monkeypatch, m):
+def _expected_leaves(nbytes):
+    blocks = nbytes // 64
+    full, rest = divmod(blocks, 4096)
+    return 64 * full + min(64, rest)
+
+
+@pytest.mark.parametrize("nblocks", [1, 5, 64, 65, 4096, 4096 + 1, 4096 * 2 + 70, 4096 * 3])
+def test_striped_leaves_closed_form(nblocks):
+    """Leaf k of a stripe holds blocks k, k+64, ... of that stripe: the leaves are
+    a permutation of the 64-byte blocks, at most 4 KiB each."""
+    ids = np.arange(nblocks * 16, dtype=np.uint32)          # 16 words per block
+    buf = ids.view(np.uint8)
+    leaves = om.tensor_leaves(buf)
+    assert len(leaves) == _expected_leaves(buf.nbytes)
+    seen = []
+    for idx, leaf in enumerate(leaves):
+        assert 0 < len(leaf) <= 4096 and len(leaf) % 64 == 0
+        words = np.frombuffer(leaf, np.uint32).reshape(-1, 16)
+        blocks = (words[:, 0] // 16).tolist()
+        s, k = divmod(idx, 64)
+        assert blocks == list(range(s * 4096 + k, min((s + 1) * 4096, nblocks), 64))
+        seen += blocks
+    assert sorted(seen) == list(range(nblocks))
+
+
+@pytest.mark.parametrize("nblocks", [1, 2, 64, 65, 130, 4096 + 3, 3 * 4096])
+def test_tree_schedule_closed_form(monkeypatch, nblocks):
     """A binary tree with m leaves and carried-up odd nodes hashes exactly m
     leaves (offsets 0..m-1, depth 0, last flag on leaf m-1) and m-1 parents,
     with depth = ceil(log2 m) at the root."""
@@ -46,7 +71,8 @@ def test_tree_schedule_closed_form(monkeypatch, m):
         return real(data, off, depth, last)
 
     monkeypatch.setattr(om, "_blake2s_node", spy)
-    buf = np.arange(m * 4096 - 100, dtype=np.uint8) if m > 1 else np.arange(37, dtype=np.uint8)
+    buf = np.arange(nblocks * 64, dtype=np.uint8)
+    m = _expected_leaves(buf.nbytes)
     om.tensor_root(buf)
     leaves = [c for c in calls if c[2] == 0]
     parents = [c for c in calls if c[2] > 0]
@@ -63,9 +89,9 @@ def test_tree_schedule_closed_form(monkeypatch, m):
 
 def test_root_changes_on_every_single_byte_flip():
     rng = np.random.default_rng(0)
-    buf = rng.integers(0, 256, size=3 * 4096 + 1000, dtype=np.uint8)
+    buf = rng.integers(0, 256, size=3 * 4096 + 1024, dtype=np.uint8)
     base = om.tensor_root(buf)
-    positions = [0, 1, 4095, 4096, 8191, 8192, 12287, 12288, buf.size - 1]
+    positions = [0, 1, 63, 64, 4095, 4096, 8191, 8192, 12287, 12288, buf.size - 1]
     positions += list(rng.integers(0, buf.size, size=40))
     seen = {base}
     for p in positions:
@@ -84,7 +110,11 @@ def test_root_is_order_and_length_sensitive():
     swapped = np.concatenate([buf[4096:8192], buf[:4096], buf[8192:]])
     assert om.tensor_root(swapped) != base
     assert om.tensor_root(np.concatenate([buf, np.zeros(4096, np.uint8)])) != base
-    assert om.tensor_root(buf[:-2]) != base
+    assert om.tensor_root(buf[:-64]) != base
+    big = rng.integers(0, 256, size=2 * 262144, dtype=np.uint8)       # two full stripes
+    sw = big.copy()
+    sw[:64], sw[64:128] = big[64:128], big[:64]                      # swap blocks of two leaves
+    assert om.tensor_root(sw) != om.tensor_root(big)
 
 
 def test_header_layout():

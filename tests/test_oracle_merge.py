@@ -51,17 +51,20 @@ def test_descending_score_places_densest_first():
 
 def test_equal_scores_fall_to_descending_digest():
     rng = np.random.default_rng(2)
-    a = rand_fragment(rng, T=9)
-    b = copy_fragment(a)
-    for l in range(b.L):                                  # same K, fresh V: equal score, new Id
-        b.layers[l] = (b.layers[l][0], rng.standard_normal(b.layers[l][1].shape).astype(np.float32))
-    ida, idb = oracle.fragment_id(a), oracle.fragment_id(b)
-    assert ida != idb
-    res = oracle.canonical_merge([a, b], 0, 1e4)
-    assert res["keys"][0] == res["keys"][1]
-    first = 0 if ida > idb else 1                         # bytes compare as big-endian unsigned
-    assert res["order"][0] == first
-    assert cache_bytes(oracle.canonical_merge([b, a], 0, 1e4)["cache"]) == cache_bytes(res["cache"])
+    for trial in range(12):                               # independent pairs: no lucky agreement
+        a = rand_fragment(rng, T=9)
+        b = copy_fragment(a)
+        for l in range(b.L):                              # same K, fresh V: equal score, new Id
+            b.layers[l] = (b.layers[l][0],
+                           rng.standard_normal(b.layers[l][1].shape).astype(np.float32))
+        ida, idb = oracle.fragment_id(a), oracle.fragment_id(b)
+        assert ida != idb
+        res = oracle.canonical_merge([a, b], 0, 1e4)
+        assert res["keys"][0] == res["keys"][1]
+        first = 0 if ida > idb else 1                     # bytes compare as big-endian unsigned
+        assert res["order"][0] == first
+        assert cache_bytes(oracle.canonical_merge([b, a], 0, 1e4)["cache"]) == \
+            cache_bytes(res["cache"])
 
 
 def test_two_input_reduction():
