@@ -197,13 +197,28 @@ int32_t cm_render_merge(const cm_fragset* set, const int64_t* plan_dev,
                         int64_t T_out, void* workspace, size_t workspace_bytes,
                         void* stream);
 
+/* Steps 1 and 4-5 in one pass: the render of cm_render_merge and, for every
+ * slot delivery i with select_dev[i] == 0, its Id (as cm_fragment_hash) written
+ * to digests_dev[i]; the Id's leaf level is computed from the same loads that
+ * feed the render, so each fragment byte is read once. The digests of all
+ * other deliveries are left untouched (give them select 1 and compute them
+ * before, e.g. with cm_fragment_hash_select: with select = the output of
+ * cm_equal_key_mask, every delivery not rendered in a slot is among them).
+ * select_dev: device, n bytes. Workspace: cm_workspace_size() bytes. */
+int32_t cm_render_merge_hash(const cm_fragset* set, const int64_t* plan_dev,
+                             const int64_t* plan_host, const cm_rope* rope,
+                             const uint8_t* select_dev, uint8_t* digests_dev, void* out_dev,
+                             int64_t T_out, void* workspace, size_t workspace_bytes,
+                             void* stream);
+
 /* ---------------------------------------------------------------- timing
  * Optional per-kernel timing with HIP events recorded on the launch stream
  * around every kernel this library enqueues (off by default; a process-wide
  * switch). cm_timing_query waits for the recorded events, adds their durations
  * to the per-kernel totals and returns the total milliseconds and launch count
  * for one kernel name ("hash_prep", "hash_leaf", "hash_parent", "hash_final",
- * "knorm_rows", "knorm_tree", "order", "key_mask", "render_prep", "render"). */
+ * "knorm_rows", "knorm_tree", "order", "key_mask", "render_prep", "render",
+ * "render_hash"). */
 int32_t cm_timing_enable(int32_t on);
 int32_t cm_timing_reset(void);
 int32_t cm_timing_query(const char* kernel, double* total_ms, int64_t* launches);

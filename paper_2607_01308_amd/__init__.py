@@ -13,6 +13,7 @@ from .binding import (  # noqa: F401
     fragment_knorm,
     plan_elems,
     render_merge,
+    render_merge_hash,
     timing_enable,
     timing_query,
     timing_reset,
@@ -20,6 +21,7 @@ from .binding import (  # noqa: F401
 )
 from .fragset import (  # noqa: F401
     LatentFragmentSet,
+    PIPELINES,
     RenderResult,
     fragment_ids,
     release_workspace,

@@ -134,6 +134,19 @@ def render_merge(batch: FragmentBatch, plan_dev: torch.Tensor, plan_host: np.nda
                                     _stream(stream, batch.device)), "cm_render_merge")
 
 
+def render_merge_hash(batch: FragmentBatch, plan_dev: torch.Tensor, plan_host: np.ndarray,
+                      rope_base: float, style: str, select: torch.Tensor, digests: torch.Tensor,
+                      out: torch.Tensor, T_out: int, workspace: torch.Tensor, stream=None) -> None:
+    plan_host = np.ascontiguousarray(plan_host, dtype=np.int64)
+    rope = C.CmRope(base=float(rope_base), style=_STYLES[style], reserved=0)
+    C.check(C.lib().cm_render_merge_hash(ctypes.byref(batch.struct), _ptr(plan_dev),
+                                         plan_host.ctypes.data_as(ctypes.c_void_p),
+                                         ctypes.byref(rope), _ptr(select), _ptr(digests),
+                                         _ptr(out), T_out, _ptr(workspace),
+                                         workspace.numel() * workspace.element_size(),
+                                         _stream(stream, batch.device)), "cm_render_merge_hash")
+
+
 def plan_elems(n: int) -> int:
     return int(C.lib().cm_plan_elems(n))
 
@@ -155,4 +168,4 @@ def timing_query(kernel: str):
 
 
 KERNELS = ("hash_prep", "hash_leaf", "hash_parent", "hash_final", "knorm_rows", "knorm_tree",
-           "order", "key_mask", "render_prep", "render")
+           "order", "key_mask", "render_prep", "render", "render_hash")

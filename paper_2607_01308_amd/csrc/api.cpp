@@ -84,6 +84,16 @@ int32_t check_ws(void* ws, size_t ws_bytes, size_t need) {
   return CM_OK;
 }
 
+// Every call fits in this many bytes; the fused render+hash needs the hash
+// workspace followed by the render workspace.
+size_t workspace_need(const cm::SetDesc& s) {
+  const size_t hb = cm::align_up(cm::hash_layout(s).bytes, cm::kWsAlign);
+  const size_t rb = cm::render_layout(s).bytes;
+  size_t need = hb + rb;
+  const size_t kn = cm::knorm_max_bytes(s);
+  return kn > need ? kn : need;
+}
+
 int64_t min_T(const cm::SetDesc& s) {
   int64_t m = s.T(0);
   for (int i = 1; i < s.n; ++i) m = s.T(i) < m ? s.T(i) : m;
@@ -93,7 +103,7 @@ int64_t min_T(const cm::SetDesc& s) {
 // ------------------------------------------------------------------ timing registry
 const char* const kKernelNames[cm::K_COUNT] = {
     "hash_prep", "hash_leaf", "hash_parent", "hash_final", "knorm_rows", "knorm_tree",
-    "order",     "key_mask",  "render_prep", "render"};
+    "order",     "key_mask",  "render_prep", "render",     "render_hash"};
 std::atomic<bool> g_timing{false};
 std::mutex g_tmu;
 struct Pending {
@@ -201,12 +211,7 @@ int32_t cm_workspace_size(const cm_fragset* set, size_t* bytes_out) {
   int32_t st = check_set(set, &s);
   if (st != CM_OK) return st;
   if (!bytes_out) return fail(CM_EINVAL, "bytes_out is NULL");
-  size_t need = cm::hash_layout(s).bytes;
-  const size_t kn = cm::knorm_max_bytes(s);
-  const size_t rn = cm::render_layout(s).bytes;
-  need = kn > need ? kn : need;
-  need = rn > need ? rn : need;
-  *bytes_out = need;
+  *bytes_out = workspace_need(s);
   return CM_OK;
 }
 
@@ -296,13 +301,15 @@ int32_t cm_canonical_order(const cm_fragset* set, const double* keys_dev,
   return e == hipSuccess ? CM_OK : fail_hip(e, "cm_canonical_order");
 }
 
-int32_t cm_render_merge(const cm_fragset* set, const int64_t* plan_dev, const int64_t* plan_host,
-                        const cm_rope* rope, void* out_dev, int64_t T_out, void* workspace,
-                        size_t workspace_bytes, void* stream) {
-  g_err.clear();
-  cm::SetDesc s;
-  int32_t st = check_set(set, &s);
-  if (st != CM_OK) return st;
+}  // extern "C"
+
+namespace {
+
+// Checks shared by the render entry points; returns the slot count and the
+// tile count of the tiled render.
+int32_t check_render_args(const cm::SetDesc& s, const int64_t* plan_dev, const int64_t* plan_host,
+                          const cm_rope* rope, void* out_dev, int64_t T_out, int64_t* nu_out,
+                          int64_t* tiles_out) {
   if (!rope) return fail(CM_EINVAL, "rope is NULL");
   if (!std::isfinite(rope->base) || rope->base <= 0.0)
     return fail(CM_EINVAL, "rope base must be finite and > 0");
@@ -334,11 +341,58 @@ int32_t cm_render_merge(const cm_fragset* set, const int64_t* plan_dev, const in
   }
   if (off != T_out) return fail(CM_ESHAPE, "T_out differs from the sum of slot lengths");
   if (tiles >= ((int64_t)1 << 31)) return fail(CM_ESHAPE, "merged cache too long for one launch");
+  *nu_out = nu;
+  *tiles_out = tiles;
+  return CM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t cm_render_merge(const cm_fragset* set, const int64_t* plan_dev, const int64_t* plan_host,
+                        const cm_rope* rope, void* out_dev, int64_t T_out, void* workspace,
+                        size_t workspace_bytes, void* stream) {
+  g_err.clear();
+  cm::SetDesc s;
+  int32_t st = check_set(set, &s);
+  if (st != CM_OK) return st;
+  int64_t nu = 0, tiles = 0;
+  if ((st = check_render_args(s, plan_dev, plan_host, rope, out_dev, T_out, &nu, &tiles)) != CM_OK)
+    return st;
+  const cm::RenderLayout lay = cm::render_layout(s);
   if ((st = check_ws(workspace, workspace_bytes, lay.bytes)) != CM_OK) return st;
   hipError_t e = cm::launch_render(s, lay, plan_dev, (int32_t)nu, tiles, T_out, rope->base,
                                    rope->style, out_dev, static_cast<uint8_t*>(workspace),
                                    static_cast<hipStream_t>(stream));
   return e == hipSuccess ? CM_OK : fail_hip(e, "cm_render_merge");
+}
+
+int32_t cm_render_merge_hash(const cm_fragset* set, const int64_t* plan_dev,
+                             const int64_t* plan_host, const cm_rope* rope,
+                             const uint8_t* select_dev, uint8_t* digests_dev, void* out_dev,
+                             int64_t T_out, void* workspace, size_t workspace_bytes,
+                             void* stream) {
+  g_err.clear();
+  cm::SetDesc s;
+  int32_t st = check_set(set, &s);
+  if (st != CM_OK) return st;
+  int64_t nu = 0, tiles = 0;
+  if ((st = check_render_args(s, plan_dev, plan_host, rope, out_dev, T_out, &nu, &tiles)) != CM_OK)
+    return st;
+  if (!select_dev) return fail(CM_EINVAL, "select_dev is NULL");
+  if (!digests_dev || !aligned(digests_dev, 16))
+    return fail(CM_EINVAL, "digests_dev is NULL or not 16-byte aligned");
+  const cm::HashLayout hlay = cm::hash_layout(s);
+  const cm::RenderLayout rlay = cm::render_layout(s);
+  const size_t need = cm::align_up(hlay.bytes, cm::kWsAlign) + rlay.bytes;
+  if ((st = check_ws(workspace, workspace_bytes, need)) != CM_OK) return st;
+  const int64_t tasks = cm::render_hash_tasks(s, plan_host);
+  hipError_t e = cm::launch_render_hash(s, hlay, rlay, plan_dev, (int32_t)nu, tasks, T_out,
+                                        rope->base, rope->style, select_dev, digests_dev, out_dev,
+                                        static_cast<uint8_t*>(workspace),
+                                        static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? CM_OK : fail_hip(e, "cm_render_merge_hash");
 }
 
 int32_t cm_timing_enable(int32_t on) {

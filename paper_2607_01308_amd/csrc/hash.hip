@@ -41,25 +41,6 @@ __device__ __forceinline__ void store_digest(uint8_t* out, const B2sState& s) {
   q[1] = make_uint4(s.h[4], s.h[5], s.h[6], s.h[7]);
 }
 
-constexpr int64_t kStripeBlocks = 4096;  // 64 leaves x 64 blocks = 256 KiB
-constexpr int kStripeLeaves = 64;
-
-// Leaves per tensor of `bytes` (a positive multiple of 64).
-__host__ __device__ __forceinline__ int64_t leaves_of(int64_t bytes) {
-  const int64_t blocks = bytes >> 6;
-  const int64_t rest = blocks % kStripeBlocks;
-  return kStripeLeaves * (blocks / kStripeBlocks) + (rest < kStripeLeaves ? rest : kStripeLeaves);
-}
-
-__host__ __device__ __forceinline__ int64_t stripes_of(int64_t bytes) {
-  return ((bytes >> 6) + kStripeBlocks - 1) / kStripeBlocks;
-}
-
-// Nodes per tensor at tree level v: ceil(m0 / 2^v).
-__host__ __device__ __forceinline__ int64_t nodes_at(int64_t m0, int v) {
-  return (m0 + (((int64_t)1 << v) - 1)) >> v;
-}
-
 // Largest i in [0, n) with base[i] <= g (bases strictly increase).
 __device__ __forceinline__ int find_fragment(const int64_t* __restrict__ base, int n, int64_t g) {
   int lo = 0, hi = n - 1;
@@ -202,9 +183,6 @@ __global__ __launch_bounds__(64) void hash_final_kernel(
 
 }  // namespace
 
-// Bytes of one token of one tensor: H rows of d elements.
-static int64_t token_bytes_of(const SetDesc& s) { return (int64_t)s.H * s.row_bytes; }
-
 HashLayout hash_layout(const SetDesc& s) {
   HashLayout lay{};
   int64_t max_m0 = 1;
@@ -228,30 +206,23 @@ HashLayout hash_layout(const SetDesc& s) {
   return lay;
 }
 
-hipError_t launch_hash(const SetDesc& s, const HashLayout& lay, const uint8_t* select,
-                       uint32_t want, uint8_t* digests, uint8_t* ws, hipStream_t stream) {
+hipError_t launch_hash_prep(const SetDesc& s, const HashLayout& lay, uint8_t* ws,
+                            hipStream_t stream) {
+  ScopedTiming tm(K_HASH_PREP, stream);
+  int threads = 64;
+  while (threads < s.n) threads <<= 1;
+  hipLaunchKernelGGL(hash_prep_kernel, dim3(1), dim3(threads), 0, stream, s.table_dev, s.n,
+                     s.stride, token_bytes_of(s), s.L, lay.levels,
+                     reinterpret_cast<int64_t*>(ws + lay.off_tables));
+  return hipGetLastError();
+}
+
+hipError_t launch_hash_tree(const SetDesc& s, const HashLayout& lay, const uint8_t* select,
+                            uint32_t want, uint8_t* digests, uint8_t* ws, hipStream_t stream) {
   int64_t* base = reinterpret_cast<int64_t*>(ws + lay.off_tables);
   uint8_t* buf[2] = {ws + lay.off_buf0, ws + lay.off_buf1};
   const int64_t nb1 = s.n + 1;
-  {
-    ScopedTiming tm(K_HASH_PREP, stream);
-    int threads = 64;
-    while (threads < s.n) threads <<= 1;
-    hipLaunchKernelGGL(hash_prep_kernel, dim3(1), dim3(threads), 0, stream, s.table_dev, s.n,
-                       s.stride, token_bytes_of(s), s.L, lay.levels, base);
-  }
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  {
-    ScopedTiming tm(K_HASH_LEAF, stream);
-    const int64_t full = (lay.tasks + (kBlock / 64) - 1) / (kBlock / 64);
-    const int64_t cap = (int64_t)device_cu_count() * kLeafBlocksPerCu;
-    const int64_t grid = full < cap ? full : cap;
-    hipLaunchKernelGGL(hash_leaf_kernel, dim3((uint32_t)grid), dim3(kBlock), 0, stream,
-                       s.table_dev, s.n, s.stride, token_bytes_of(s), base,
-                       base + (int64_t)(lay.levels + 1) * nb1, lay.tasks, select, want, buf[0]);
-  }
-  if ((e = hipGetLastError()) != hipSuccess) return e;
+  hipError_t e = hipSuccess;
   for (int v = 1; v <= lay.levels; ++v) {
     int64_t total = 0;
     for (int i = 0; i < s.n; ++i)
@@ -272,6 +243,26 @@ hipError_t launch_hash(const SetDesc& s, const HashLayout& lay, const uint8_t* s
                        buf[lay.levels & 1], digests);
   }
   return hipGetLastError();
+}
+
+hipError_t launch_hash(const SetDesc& s, const HashLayout& lay, const uint8_t* select,
+                       uint32_t want, uint8_t* digests, uint8_t* ws, hipStream_t stream) {
+  hipError_t e = launch_hash_prep(s, lay, ws, stream);
+  if (e != hipSuccess) return e;
+  {
+    int64_t* base = reinterpret_cast<int64_t*>(ws + lay.off_tables);
+    const int64_t nb1 = s.n + 1;
+    ScopedTiming tm(K_HASH_LEAF, stream);
+    const int64_t full = (lay.tasks + (kBlock / 64) - 1) / (kBlock / 64);
+    const int64_t cap = (int64_t)device_cu_count() * kLeafBlocksPerCu;
+    const int64_t grid = full < cap ? full : cap;
+    hipLaunchKernelGGL(hash_leaf_kernel, dim3((uint32_t)grid), dim3(kBlock), 0, stream,
+                       s.table_dev, s.n, s.stride, token_bytes_of(s), base,
+                       base + (int64_t)(lay.levels + 1) * nb1, lay.tasks, select, want,
+                       ws + lay.off_buf0);
+  }
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  return launch_hash_tree(s, lay, select, want, digests, ws, stream);
 }
 
 }  // namespace cm

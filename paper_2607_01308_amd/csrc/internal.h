@@ -29,8 +29,31 @@ struct SetDesc {
   int64_t T(int i) const { return table_host[(int64_t)i * stride]; }
 };
 
-constexpr int kLeafBytes = 4096;
+// Bytes of one token of one tensor: H rows of d elements.
+inline int64_t token_bytes_of(const SetDesc& s) { return (int64_t)s.H * s.row_bytes; }
+
 constexpr size_t kWsAlign = 256;
+
+// Hash-tree geometry (see cm_fragment_hash): 64-byte blocks, stripes of 4096
+// blocks (256 KiB) holding 64 leaves each.
+constexpr int64_t kStripeBlocks = 4096;
+constexpr int kStripeLeaves = 64;
+
+// Leaves per tensor of `bytes` (a positive multiple of 64).
+__host__ __device__ __forceinline__ int64_t leaves_of(int64_t bytes) {
+  const int64_t blocks = bytes >> 6;
+  const int64_t rest = blocks % kStripeBlocks;
+  return kStripeLeaves * (blocks / kStripeBlocks) + (rest < kStripeLeaves ? rest : kStripeLeaves);
+}
+
+__host__ __device__ __forceinline__ int64_t stripes_of(int64_t bytes) {
+  return ((bytes >> 6) + kStripeBlocks - 1) / kStripeBlocks;
+}
+
+// Nodes per tensor at tree level v: ceil(m0 / 2^v).
+__host__ __device__ __forceinline__ int64_t nodes_at(int64_t m0, int v) {
+  return (m0 + (((int64_t)1 << v) - 1)) >> v;
+}
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
@@ -65,8 +88,9 @@ size_t knorm_max_bytes(const SetDesc& s);  // over every legal tail_len
 
 struct RenderLayout {
   int32_t tile_rows;      // rows per render tile
-  size_t off_tiles;       // int64 [n+1] tile bases per slot
+  size_t off_tiles;       // int64 [n+1] work-unit bases per slot (tiles or stripe tasks)
   size_t off_angles;      // double [n][d/2][2] cos, sin per slot
+  size_t off_hsel;        // uint8 [n]: 0 = slot delivery hashed by the fused kernel
   size_t bytes;
 };
 RenderLayout render_layout(const SetDesc& s);
@@ -76,12 +100,29 @@ RenderLayout render_layout(const SetDesc& s);
 // select[i] == want (the other digests are left untouched).
 hipError_t launch_hash(const SetDesc& s, const HashLayout& lay, const uint8_t* select,
                        uint32_t want, uint8_t* digests, uint8_t* ws, hipStream_t stream);
+// The stages of launch_hash: node-base tables, then (after the leaves) the
+// parent levels and the final Id.
+hipError_t launch_hash_prep(const SetDesc& s, const HashLayout& lay, uint8_t* ws,
+                            hipStream_t stream);
+hipError_t launch_hash_tree(const SetDesc& s, const HashLayout& lay, const uint8_t* select,
+                            uint32_t want, uint8_t* digests, uint8_t* ws, hipStream_t stream);
 hipError_t launch_equal_key_mask(const SetDesc& s, const double* keys, uint8_t* mask,
                                  hipStream_t stream);
 hipError_t launch_knorm(const SetDesc& s, const KnormLayout& lay, int32_t layer, int64_t tail_len,
                         double* keys, uint8_t* ws, hipStream_t stream);
 hipError_t launch_order(const SetDesc& s, const double* keys, const uint8_t* digests,
                         int64_t* plan, hipStream_t stream);
+hipError_t launch_render_prep(const SetDesc& s, const RenderLayout& lay, const int64_t* plan_dev,
+                              int32_t n_unique, double base, bool stripe_tasks,
+                              const uint8_t* select, uint8_t* ws, hipStream_t stream);
+// Work items of the fused hash+render: 2L * stripes per slot.
+int64_t render_hash_tasks(const SetDesc& s, const int64_t* plan_host);
+// Render plus, for every slot delivery i with select[i] == 0, its Id (leaf level
+// fused into the render, then the tree). ws = hash workspace, then render's.
+hipError_t launch_render_hash(const SetDesc& s, const HashLayout& hlay, const RenderLayout& rlay,
+                              const int64_t* plan_dev, int32_t n_unique, int64_t total_tasks,
+                              int64_t T_out, double base, int32_t style, const uint8_t* select,
+                              uint8_t* digests, void* out, uint8_t* ws, hipStream_t stream);
 hipError_t launch_render(const SetDesc& s, const RenderLayout& lay, const int64_t* plan_dev,
                          int32_t n_unique, int64_t total_tiles, int64_t T_out, double base,
                          int32_t style, void* out, uint8_t* ws, hipStream_t stream);
@@ -111,6 +152,7 @@ enum KernelId {
   K_KEY_MASK,
   K_RENDER_PREP,
   K_RENDER,
+  K_RENDER_HASH,
   K_COUNT
 };
 

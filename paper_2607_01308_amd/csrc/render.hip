@@ -13,6 +13,7 @@
 // add/subtract rounded separately, then rounds once to the storage dtype
 // (round-to-nearest-even; bf16 via the compiler's single-step conversion).
 #include "internal.h"
+#include "stream_ops.h"
 
 namespace cm {
 
@@ -23,28 +24,6 @@ namespace {
 #endif
 constexpr int kThreads = 256;
 constexpr int kTileBytes = CM_RENDER_TILE_BYTES;
-
-__device__ __forceinline__ u32x4 ld_stream(const uint8_t* p) {
-  return __builtin_nontemporal_load(global_ptr<u32x4>(p));
-}
-__device__ __forceinline__ void st_stream(uint8_t* p, u32x4 v) {
-  __builtin_nontemporal_store(v, (CM_GLOBAL u32x4*)p);
-}
-
-// Round fp64 to the nearest bf16, ties to even, as one rounding step. Rounding
-// to fp32 first can only go wrong when the fp32 value lands exactly on a bf16
-// midpoint (every bf16 value and midpoint is an fp32 value, so otherwise y and
-// its fp32 rounding lie on the same side of every midpoint); in that case the
-// fp32 value is nudged one ulp towards y before the hardware bf16 conversion.
-__device__ __forceinline__ uint32_t bf16_bits_rne(double y) {
-  const float f = (float)y;
-  uint32_t u = __float_as_uint(f);
-  if (__builtin_expect((u & 0xFFFFu) == 0x8000u, 0)) {
-    const double back = (double)f;
-    if (y != back) u = (fabs(y) > fabs(back)) ? u + 1u : u - 1u;
-  }
-  return (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)__uint_as_float(u));
-}
 
 // 16 bytes <-> fp64 lanes
 template <int ESIZE>
@@ -222,19 +201,26 @@ __global__ __launch_bounds__(kThreads) void render_kernel(
     rotate_tile<ESIZE, STYLE>(src, dst, rows, d, angles + (int64_t)s * d);
 }
 
-// One workgroup: tile bases per slot (exclusive scan of ceil(len/tile_rows)) and
-// cos/sin(off_s * theta_j), theta_j = base^(-2j/d), in fp64.
-__global__ __launch_bounds__(1024) void render_prep_kernel(const int64_t* __restrict__ plan,
-                                                           int32_t n, int32_t d, double base,
-                                                           int32_t tile_rows,
-                                                           int64_t* __restrict__ tile_base,
-                                                           double* __restrict__ angles) {
+// One workgroup: per-slot work-unit bases (exclusive scan of the units of each
+// slot: ceil(len / tile_rows) tiles, or 2L * stripes for the fused hash+render)
+// and cos/sin(off_s * theta_j), theta_j = base^(-2j/d), in fp64. With a select
+// mask it also writes hsel[i] = 0 for the slot deliveries whose Id the fused
+// kernel computes (select[i] == 0), 1 for every other delivery.
+__global__ __launch_bounds__(1024) void render_prep_kernel(
+    const int64_t* __restrict__ plan, int32_t n, int32_t d, double base, int32_t tile_rows,
+    int32_t stripe_mode, int64_t tensor_pairs, int64_t token_bytes,
+    const uint8_t* __restrict__ select, uint8_t* __restrict__ hsel,
+    int64_t* __restrict__ unit_base, double* __restrict__ angles) {
   __shared__ int64_t sc[1024];
   const int tid = threadIdx.x;
   const int n_u = (int)plan[CM_PLAN_NUNIQUE];
   const int64_t len = tid < n_u ? plan[CM_PLAN_HEADER + 2 * (int64_t)n + tid] : 0;
-  const int64_t x = (len + tile_rows - 1) / tile_rows;
+  int64_t x = 0;
+  if (tid < n_u)
+    x = stripe_mode ? 2 * tensor_pairs * stripes_of(len * token_bytes)
+                    : (len + tile_rows - 1) / tile_rows;
   sc[tid] = x;
+  if (hsel && tid < n) hsel[tid] = 1;
   __syncthreads();
   for (int o = 1; o < (int)blockDim.x; o <<= 1) {
     const int64_t t = tid >= o ? sc[tid - o] : 0;
@@ -242,8 +228,12 @@ __global__ __launch_bounds__(1024) void render_prep_kernel(const int64_t* __rest
     sc[tid] += t;
     __syncthreads();
   }
-  if (tid < n_u) tile_base[tid] = sc[tid] - x;
-  if (tid == (int)blockDim.x - 1) tile_base[n_u] = sc[tid];
+  if (tid < n_u) unit_base[tid] = sc[tid] - x;
+  if (tid == (int)blockDim.x - 1) unit_base[n_u] = sc[tid];
+  if (hsel && tid < n_u) {
+    const int64_t i = plan[CM_PLAN_HEADER + tid];
+    if (select[i] == 0) hsel[i] = 0;
+  }
   const int halfd = d >> 1;
   for (int idx = tid; idx < n_u * halfd; idx += blockDim.x) {
     const int s = idx / halfd;
@@ -281,22 +271,30 @@ RenderLayout render_layout(const SetDesc& s) {
   lay.tile_rows = (int32_t)(kTileBytes / s.row_bytes);
   lay.off_tiles = 0;
   lay.off_angles = align_up(sizeof(int64_t) * (size_t)(s.n + 1), kWsAlign);
-  lay.bytes = align_up(lay.off_angles + sizeof(double) * (size_t)s.n * (size_t)s.d, kWsAlign);
+  lay.off_hsel = align_up(lay.off_angles + sizeof(double) * (size_t)s.n * (size_t)s.d, kWsAlign);
+  lay.bytes = align_up(lay.off_hsel + (size_t)s.n, kWsAlign);
   return lay;
+}
+
+hipError_t launch_render_prep(const SetDesc& s, const RenderLayout& lay, const int64_t* plan_dev,
+                              int32_t n_unique, double base, bool stripe_tasks,
+                              const uint8_t* select, uint8_t* ws, hipStream_t stream) {
+  ScopedTiming tm(K_RENDER_PREP, stream);
+  int threads = 64;
+  const int need = n_unique > s.n ? n_unique : s.n;
+  while (threads < need) threads <<= 1;
+  hipLaunchKernelGGL(render_prep_kernel, dim3(1), dim3(threads), 0, stream, plan_dev, s.n, s.d,
+                     base, lay.tile_rows, stripe_tasks ? 1 : 0, (int64_t)s.L, token_bytes_of(s),
+                     select, select ? ws + lay.off_hsel : nullptr,
+                     reinterpret_cast<int64_t*>(ws + lay.off_tiles),
+                     reinterpret_cast<double*>(ws + lay.off_angles));
+  return hipGetLastError();
 }
 
 hipError_t launch_render(const SetDesc& s, const RenderLayout& lay, const int64_t* plan_dev,
                          int32_t n_unique, int64_t total_tiles, int64_t T_out, double base,
                          int32_t style, void* out, uint8_t* ws, hipStream_t stream) {
-  {
-    ScopedTiming tm(K_RENDER_PREP, stream);
-    int threads = 64;
-    while (threads < n_unique) threads <<= 1;
-    hipLaunchKernelGGL(render_prep_kernel, dim3(1), dim3(threads), 0, stream, plan_dev, s.n, s.d,
-                       base, lay.tile_rows, reinterpret_cast<int64_t*>(ws + lay.off_tiles),
-                       reinterpret_cast<double*>(ws + lay.off_angles));
-  }
-  hipError_t e = hipGetLastError();
+  hipError_t e = launch_render_prep(s, lay, plan_dev, n_unique, base, false, nullptr, ws, stream);
   if (e != hipSuccess) return e;
   if (s.esize == 2)
     return launch_render_t<2>(s, lay, plan_dev, n_unique, total_tiles, T_out, style, out, ws, stream);

@@ -5,9 +5,10 @@ render_deliveries runs the whole path over a list of deliveries: scores
 with another's (cm_equal_key_mask + cm_fragment_hash_select: only those decide
 dedupe and ties), dedupe + canonical order + offsets (cm_canonical_order), one
 device-to-host copy of the small plan so the caller can size the output, then
-the rotate-and-concatenate render (cm_render_merge). The Id of every other
-delivery is computed on a second stream while the render runs: the hash is
-bound by vector ALU work and the render by HBM bandwidth, so the two overlap.
+the rotate-and-concatenate render. By default the render also computes the Id
+of every other delivery from the same loads (cm_render_merge_hash), so each
+byte is read once; pipeline="overlap" instead hashes them on a second stream
+next to cm_render_merge, and pipeline="serial" runs every step in order.
 LatentFragmentSet keeps the state of Alg. 2 (a set keyed by Id) and renders it
 with the ids computed at Ingest."""
 
@@ -22,7 +23,7 @@ import torch
 from . import _cabi as C
 from .binding import (FragmentBatch, canonical_order, equal_key_mask, fragment_hash,
                       fragment_hash_select, fragment_knorm, plan_elems, render_merge,
-                      workspace_size)
+                      render_merge_hash, workspace_size)
 
 _WS: Dict[tuple, torch.Tensor] = {}
 _SIDE: Dict[torch.device, torch.cuda.Stream] = {}
@@ -101,7 +102,8 @@ class RenderResult:
 
 
 def _render_plan(batch: FragmentBatch, plan_dev: torch.Tensor, plan_host: np.ndarray,
-                 rope_base: float, style: str, ws: torch.Tensor, stream):
+                 rope_base: float, style: str, ws: torch.Tensor, stream, hash_select=None,
+                 digests=None):
     status = int(plan_host[C.PLAN_STATUS])
     if status != C.CM_OK:
         raise C.CmError(status, "cm_canonical_order", "plan status is not CM_OK "
@@ -109,16 +111,24 @@ def _render_plan(batch: FragmentBatch, plan_dev: torch.Tensor, plan_host: np.nda
     T_out = int(plan_host[C.PLAN_TOUT])
     merged = torch.empty((batch.L, 2, 1, batch.H, T_out, batch.d), dtype=batch.torch_dtype,
                          device=batch.device)
-    render_merge(batch, plan_dev, plan_host, rope_base, style, merged, T_out, ws, stream)
+    if hash_select is None:
+        render_merge(batch, plan_dev, plan_host, rope_base, style, merged, T_out, ws, stream)
+    else:
+        render_merge_hash(batch, plan_dev, plan_host, rope_base, style, hash_select, digests,
+                          merged, T_out, ws, stream)
     cache = tuple((merged[l, 0], merged[l, 1]) for l in range(batch.L))
     return merged, cache
 
 
+PIPELINES = ("fused", "overlap", "serial")
+
+
 def render_deliveries(deliveries: Union[FragmentBatch, Sequence], routing_layer: int,
                       rope_base: float, style: str = "half", stream=None,
-                      overlap: bool = True) -> RenderResult:
-    """The whole path over a list of deliveries (duplicates allowed). With
-    overlap=False every step runs in order on one stream."""
+                      pipeline: str = "fused") -> RenderResult:
+    """The whole path over a list of deliveries (duplicates allowed)."""
+    if pipeline not in PIPELINES:
+        raise ValueError(f"pipeline must be one of {PIPELINES}")
     batch = deliveries if isinstance(deliveries, FragmentBatch) else FragmentBatch(deliveries)
     dev = batch.device
     main = stream if stream is not None else torch.cuda.current_stream(dev)
@@ -131,9 +141,9 @@ def render_deliveries(deliveries: Union[FragmentBatch, Sequence], routing_layer:
         tail = min(batch.lengths)
         fragment_knorm(batch, routing_layer, tail, keys, ws, main)
         equal_key_mask(batch, keys, mask, main)
-        fragment_hash_select(batch, mask, 1, digests, ws, main)
+        fragment_hash_select(batch, mask, 1, digests, ws, main)   # the digests the order reads
         side_done = None
-        if overlap:
+        if pipeline == "overlap":
             ready = torch.cuda.Event()
             ready.record(main)
             side = _side_stream(dev)
@@ -141,12 +151,16 @@ def render_deliveries(deliveries: Union[FragmentBatch, Sequence], routing_layer:
             fragment_hash_select(batch, mask, 0, digests, _workspace(batch, 1), side)
             side_done = torch.cuda.Event()
             side_done.record(side)
-        else:
+        elif pipeline == "serial":
             fragment_hash_select(batch, mask, 0, digests, ws, main)
         canonical_order(batch, keys, digests, plan_dev, main)
         plan_host = plan_dev.to("cpu").numpy()
         try:
-            merged, cache = _render_plan(batch, plan_dev, plan_host, rope_base, style, ws, main)
+            if pipeline == "fused":
+                merged, cache = _render_plan(batch, plan_dev, plan_host, rope_base, style, ws, main,
+                                             hash_select=mask, digests=digests)
+            else:
+                merged, cache = _render_plan(batch, plan_dev, plan_host, rope_base, style, ws, main)
         finally:
             if side_done is not None:
                 main.wait_event(side_done)

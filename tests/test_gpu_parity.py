@@ -301,14 +301,38 @@ def test_order_reads_only_colliding_digests():
     assert torch.equal(plan_a, plan_b)
 
 
-def test_overlapped_pipeline_matches_serial():
-    w = synth.custom("overlap", dtype="bfloat16", d=128, H=4, L=3, lengths=(700, 700, 300, 1200),
-                     shared_k=((0, 1),), deliveries=(3, 0, 2, 1, 0))
+PIPE_SHAPES = [
+    dict(dtype="bfloat16", d=128, H=4, L=3, lengths=(700, 700, 300, 1200), shared_k=((0, 1),),
+         deliveries=(3, 0, 2, 1, 0)),
+    dict(dtype="bfloat16", d=64, H=3, L=2, lengths=(3000, 77, 1)),       # multi-stripe, tiny T
+    dict(dtype="float32", d=64, H=2, L=2, lengths=(130, 4100, 9)),
+    dict(dtype="bfloat16", d=32, H=4, L=2, lengths=(513, 40), deliveries=(1, 0, 1)),  # 64 B rows
+    dict(dtype="bfloat16", d=512, H=1, L=2, lengths=(300, 257)),         # 1 KiB rows
+    dict(dtype="float32", d=16, H=2, L=2, lengths=(70, 33)),             # 64 B rows, fp32
+]
+
+
+@pytest.mark.parametrize("spec", PIPE_SHAPES, ids=[f"pipe{i}" for i in range(len(PIPE_SHAPES))])
+def test_pipelines_agree_and_match_oracle(spec):
+    w = synth.custom("pipes", routing_layer=1, **spec)
     _, dl = gpu_deliveries(w)
-    a = cm.render_deliveries(dl, w.routing_layer, w.rope_base, overlap=True)
-    b = cm.render_deliveries(dl, w.routing_layer, w.rope_base, overlap=False)
+    outs = {p: cm.render_deliveries(dl, w.routing_layer, w.rope_base, pipeline=p)
+            for p in cm.PIPELINES}
     torch.cuda.synchronize()
-    assert torch.equal(a.merged, b.merged)
-    assert a.digests == b.digests == oracle_ids(dl, w.dtype)
-    assert list(a.plan) == list(b.plan)
-    check_render(a, dl, w.dtype, w.routing_layer, w.rope_base)
+    ref = outs["serial"]
+    for p, r in outs.items():
+        assert torch.equal(r.merged, ref.merged), p
+        assert r.digests == ref.digests, p
+        assert list(r.plan) == list(ref.plan), p
+    check_render(outs["fused"], dl, w.dtype, w.routing_layer, w.rope_base)
+
+
+def test_fused_interleaved_style():
+    w = synth.custom("fused-il", dtype="bfloat16", d=128, H=2, L=2, lengths=(600, 333),
+                     routing_layer=0, rope_base=1e4)
+    _, dl = gpu_deliveries(w)
+    a = cm.render_deliveries(dl, w.routing_layer, w.rope_base, style="interleaved", pipeline="fused")
+    b = cm.render_deliveries(dl, w.routing_layer, w.rope_base, style="interleaved", pipeline="serial")
+    torch.cuda.synchronize()
+    assert torch.equal(a.merged, b.merged) and a.digests == b.digests
+    check_render(a, dl, w.dtype, w.routing_layer, w.rope_base, style="interleaved")
