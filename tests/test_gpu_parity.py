@@ -184,9 +184,11 @@ def test_timing_api_counts_launches():
     cm.timing_reset()
     cm.timing_enable(True)
     try:
-        cm.render_deliveries(dl, w.routing_layer, w.rope_base)
+        cm.render_deliveries(dl, w.routing_layer, w.rope_base, pipeline="fused")
+        cm.render_deliveries(dl, w.routing_layer, w.rope_base, pipeline="serial")
         torch.cuda.synchronize()
-        for k in ("hash_leaf", "hash_final", "knorm_rows", "order", "render_prep", "render"):
+        for k in ("hash_leaf", "hash_final", "knorm_rows", "order", "key_mask", "render_prep",
+                  "render", "render_hash"):
             ms, n = cm.timing_query(k)
             assert n >= 1 and ms > 0.0, k
     finally:
