@@ -121,9 +121,11 @@ int32_t cm_workspace_size(const cm_fragset* set, size_t* bytes_out);
  * fragment, a 32-byte digest of its shapes, dtype and the raw bytes of
  * K^0, V^0, ..., K^{L-1}, V^{L-1} in that order. Function: per tensor a BLAKE2s-256
  * (RFC 7693) binary tree (fanout 2, depth 255, leaf 4096, inner 32) over striped
- * leaves: the tensor's 64-byte blocks are grouped in stripes of 4096 blocks
- * (256 KiB, the last may be shorter) and leaf 64*s + k is blocks k, k+64, k+128,
- * ... of stripe s (k < min(64, blocks in the stripe)); leaf j is hashed with
+ * leaves: the tensor is cut into stripes of 256 KiB and each stripe into steps of
+ * 4 KiB (the last of each may be shorter); stripe s has min(64, its 64-byte
+ * blocks) leaves, and in every step leaf 64*s + k takes one 64-byte message
+ * block: the 16-byte pieces k, k+64, k+128, k+192 of a full step, or block k of
+ * a shorter final step; leaf j is hashed with
  * node_offset j, depth 0; parent j at level v with node_offset j, depth v,
  * children 2j and 2j+1; last_node on the last node of each level; an unpaired
  * last node is carried up unchanged. Then a sequential BLAKE2s-256 of a 64-byte

@@ -40,7 +40,9 @@ import numpy as np
 
 LEAF_BYTES = 4096          # tree-hash leaf size (bytes), the maximum
 BLOCK_BYTES = 64           # BLAKE2s message block
+PIECE_BYTES = 16           # interleave granularity inside a step
 STRIPE_LEAVES = 64         # leaves interleaved in one stripe
+STEP_BYTES = STRIPE_LEAVES * BLOCK_BYTES    # 4 KiB: one block of every leaf
 STRIPE_BYTES = STRIPE_LEAVES * LEAF_BYTES   # 256 KiB
 _DIGEST = 32               # BLAKE2s-256
 # dtype -> (header code, element bytes)
@@ -99,23 +101,34 @@ def _blake2s_node(data, node_offset: int, node_depth: int, last_node: bool) -> b
 def tensor_leaves(buf) -> List[bytes]:
     """Leaf messages of one tensor, in leaf order.
 
-    The raw bytes (a multiple of 64) are cut into 64-byte blocks and the blocks
-    into stripes of 4096 blocks (256 KiB; the last stripe may be shorter). In a
-    stripe with B blocks, leaf k (k < min(64, B)) is the concatenation of blocks
-    k, k + 64, k + 128, ... of that stripe, so a full leaf is 4 KiB. Leaves are
-    numbered stripe by stripe: leaf index = 64 * stripe + k."""
+    The raw bytes (a multiple of 64) are cut into stripes of 256 KiB (the last
+    may be shorter) and each stripe into steps of 4 KiB (the last may be
+    shorter). A stripe has min(64, its 64-byte blocks) leaves; in every step each
+    leaf k takes one 64-byte message block:
+      * full 4 KiB step: the 16-byte pieces k, k+64, k+128, k+192 of the step,
+        in that order;
+      * shorter final step of m blocks: block k of the step (k < m), unchanged.
+    Leaf k's message is its blocks in step order; leaves are numbered stripe by
+    stripe: leaf index = 64 * stripe + k."""
     raw = np.frombuffer(memoryview(buf).cast("B"), dtype=np.uint8)
     n = raw.size
     if n == 0:
         return [b""]
     if n % BLOCK_BYTES:
         raise ValueError("tensor bytes must be a multiple of 64")
-    blocks = raw.reshape(-1, BLOCK_BYTES)
     leaves = []
-    for s0 in range(0, blocks.shape[0], STRIPE_BYTES // BLOCK_BYTES):
-        stripe = blocks[s0:s0 + STRIPE_BYTES // BLOCK_BYTES]
-        for k in range(min(STRIPE_LEAVES, stripe.shape[0])):
-            leaves.append(stripe[k::STRIPE_LEAVES].tobytes())
+    for s0 in range(0, n, STRIPE_BYTES):
+        stripe = raw[s0:s0 + STRIPE_BYTES]
+        parts = [[] for _ in range(min(STRIPE_LEAVES, stripe.size // BLOCK_BYTES))]
+        for t0 in range(0, stripe.size, STEP_BYTES):
+            step = stripe[t0:t0 + STEP_BYTES]
+            if step.size == STEP_BYTES:
+                blocks = step.reshape(4, STRIPE_LEAVES, PIECE_BYTES).transpose(1, 0, 2)
+            else:
+                blocks = step.reshape(-1, BLOCK_BYTES)
+            for k in range(blocks.shape[0]):
+                parts[k].append(blocks[k].tobytes())
+        leaves.extend(b"".join(p) for p in parts)
     return leaves
 
 

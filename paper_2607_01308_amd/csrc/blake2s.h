@@ -119,35 +119,35 @@ __host__ __device__ __forceinline__ void b2s_compress(B2sState& s, const uint32_
 #undef CM_B2S_ROUND
 #undef CM_B2S_G
 
-// Hash one node made of nb >= 1 64-byte blocks, block b at p + b * stride
-// (16-byte aligned), read with the given 64-byte loader. The next two blocks are
-// in flight while two are compressed, with alternating buffers so no registers
-// are copied between iterations.
-template <class Load64>
-__host__ __device__ __forceinline__ void b2s_node_blocks(B2sState& s, const uint8_t* p,
-                                                         uint64_t nb, uint64_t stride,
-                                                         bool last_node, Load64 load64) {
+// Hash one node made of nb >= 1 64-byte message blocks; load_block(b, w) reads
+// block b into w[16]. Two blocks are in flight while two are compressed, with
+// alternating buffers so no registers are copied between iterations.
+template <class LoadBlock>
+__host__ __device__ __forceinline__ void b2s_node(B2sState& s, uint64_t nb, bool last_node,
+                                                  LoadBlock load_block) {
   uint32_t x0[16], x1[16], y0[16], y1[16];
-  load64(p, x0);
-  if (nb > 1) load64(p + stride, x1);
+  load_block(0, x0);
+  if (nb > 1) load_block(1, x1);
   for (uint64_t b = 0; b < nb; b += 4) {
-    if (b + 2 < nb) load64(p + (b + 2) * stride, y0);
-    if (b + 3 < nb) load64(p + (b + 3) * stride, y1);
+    if (b + 2 < nb) load_block(b + 2, y0);
+    if (b + 3 < nb) load_block(b + 3, y1);
     b2s_compress(s, x0, (b + 1) << 6, b + 1 == nb, b + 1 == nb && last_node);
     if (b + 1 < nb) b2s_compress(s, x1, (b + 2) << 6, b + 2 == nb, b + 2 == nb && last_node);
-    if (b + 4 < nb) load64(p + (b + 4) * stride, x0);
-    if (b + 5 < nb) load64(p + (b + 5) * stride, x1);
+    if (b + 4 < nb) load_block(b + 4, x0);
+    if (b + 5 < nb) load_block(b + 5, x1);
     if (b + 2 < nb) b2s_compress(s, y0, (b + 3) << 6, b + 3 == nb, b + 3 == nb && last_node);
     if (b + 3 < nb) b2s_compress(s, y1, (b + 4) << 6, b + 4 == nb, b + 4 == nb && last_node);
   }
 }
 
-// A node whose len bytes (a positive multiple of 64) are contiguous.
+// A node whose len bytes (a positive multiple of 64) are contiguous, read with
+// the 64-byte loader load64(p, w).
 template <class Load64>
 __host__ __device__ __forceinline__ void b2s_node_aligned(B2sState& s, const uint8_t* p,
                                                           uint64_t len, bool last_node,
                                                           Load64 load64) {
-  b2s_node_blocks(s, p, len >> 6, 64, last_node, load64);
+  b2s_node(s, len >> 6, last_node,
+           [&](uint64_t b, uint32_t (&w)[16]) { load64(p + (b << 6), w); });
 }
 
 }  // namespace cm

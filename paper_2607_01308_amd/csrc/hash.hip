@@ -2,14 +2,16 @@
 //
 // Per tensor, a BLAKE2s-256 binary tree over striped leaves; per fragment, a
 // sequential BLAKE2s-256 of a 64-byte shape/dtype header followed by the 2L
-// tensor roots (K^0, V^0, ..., K^{L-1}, V^{L-1}). A tensor's 64-byte blocks are
-// grouped in stripes of 4096 blocks (256 KiB); leaf k of a stripe is blocks
-// k, k+64, k+128, ... of it. That layout is chosen for 64-wide wavefronts: one
-// wave takes one stripe, lane k hashes leaf k (64 dependent compressions with
-// the next blocks in flight), and at every step the wave reads 4 KiB of
-// contiguous memory. The work is VALU-bound (12 VALU ops per G step, 960 per
-// block); each upper tree level is one launch over all tensors at full lane
-// occupancy (the parents add 1/64 of the leaf work).
+// tensor roots (K^0, V^0, ..., K^{L-1}, V^{L-1}). A tensor is cut into stripes
+// of 256 KiB and steps of 4 KiB; in every step each of the stripe's 64 leaves
+// takes one 64-byte block: leaf k the 16-byte pieces k, k+64, k+128, k+192 (a
+// shorter final step keeps block k whole). That layout is chosen for 64-wide
+// wavefronts: one wave takes one stripe, lane k hashes leaf k (64 dependent
+// compressions with the next blocks in flight), and each of the four 16-byte
+// loads of a step reads 1 KiB of contiguous memory across the wave. The work is
+// VALU-bound (12 VALU ops per G step, 960 per block); each upper tree level is
+// one launch over all tensors at full lane occupancy (the parents add 1/64 of
+// the leaf work).
 #include "blake2s.h"
 #include "internal.h"
 
@@ -32,6 +34,26 @@ __device__ __forceinline__ void load64(const uint8_t* p, uint32_t (&m)[16]) {
     m[4 * k + 1] = v[1];
     m[4 * k + 2] = v[2];
     m[4 * k + 3] = v[3];
+  }
+}
+
+// Block of leaf `lane` in step j of a stripe starting at p: the 16-byte pieces
+// lane, lane+64, lane+128, lane+192 of a full step; block `lane` of the final
+// short step (j == full_steps).
+__device__ __forceinline__ void load_leaf_block(const uint8_t* p, int lane, int64_t j,
+                                               int64_t full_steps, uint32_t (&m)[16]) {
+  if (j < full_steps) {
+    const CM_GLOBAL u32x4* q = global_ptr<u32x4>(p + (j << 12) + lane * 16);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const u32x4 v = q[k * 64];
+      m[4 * k + 0] = v[0];
+      m[4 * k + 1] = v[1];
+      m[4 * k + 2] = v[2];
+      m[4 * k + 3] = v[3];
+    }
+  } else {
+    load64(p + (j << 12) + lane * 64, m);
   }
 }
 
@@ -112,13 +134,15 @@ __global__ __launch_bounds__(kBlock) void hash_leaf_kernel(const int64_t* __rest
     const int64_t blocks_here = in_stripe < kStripeBlocks ? in_stripe : kStripeBlocks;
     if (lane >= blocks_here) continue;
     const int64_t nb = (blocks_here - lane + kStripeLeaves - 1) / kStripeLeaves;
+    const int64_t full_steps = blocks_here / kStripeLeaves;
     const int64_t leaf = sidx * kStripeLeaves + lane;
     const uint8_t* p = reinterpret_cast<const uint8_t*>(table[(int64_t)i * stride + 1 + t]) +
-                       ((sidx * kStripeBlocks + lane) << 6);
+                       ((sidx * kStripeBlocks) << 6);
     B2sState s;
     b2s_init_tree(s, (uint64_t)leaf, 0);
-    b2s_node_blocks(s, p, (uint64_t)nb, (uint64_t)kStripeLeaves * 64, leaf == m - 1,
-                    [](const uint8_t* q, uint32_t (&w)[16]) { load64(q, w); });
+    b2s_node(s, (uint64_t)nb, leaf == m - 1, [&](uint64_t b, uint32_t (&w)[16]) {
+      load_leaf_block(p, lane, (int64_t)b, full_steps, w);
+    });
     store_digest(nodes + (base0[i] + t * m + leaf) * 32, s);
   }
 }

@@ -4,14 +4,17 @@
 //
 // Hashing is VALU-bound (960 VALU ops per 64-byte block) and the render is
 // HBM-bound; done separately they read every byte twice. Here one wave takes
-// one (slot, tensor, stripe) task: at step j every lane loads one 64-byte block
-// (block 64j + lane of the 256 KiB stripe, so the wave reads 4 KiB of
-// contiguous memory), compresses it into its leaf (leaf = lane of the stripe,
-// exactly the striped leaf layout of the tree) and writes it to its place in
-// the merged cache: V and offset-0 K unchanged, other K rotated by R(off).
-// A row is row_bytes / 64 consecutive lanes, so the other half of a lane's
-// pairs sits in lane ^ (blocks per row / 2) and one xor shuffle brings it in.
-// The slot's cos/sin table lives in LDS, one copy per wave. HBM traffic is the
+// one (slot, tensor, stripe) task. At full step j of the 256 KiB stripe every
+// lane loads the 16-byte pieces lane, lane+64, lane+128, lane+192 of the 4 KiB
+// step (four loads, each 1 KiB contiguous across the wave), compresses them as
+// one 64-byte block into its leaf (exactly the leaf layout of the tree) and
+// writes each piece to its place in the merged cache: V and offset-0 K
+// unchanged, other K rotated by R(off). A row holds row_bytes / 16 pieces and
+// 64 is a multiple of that, so all four pieces of a lane sit in the same column
+// of their rows: the lane's cos/sin pairs are fixed for the task (registers),
+// and the other half of its pairs is in lane ^ (pieces per row / 2) (one xor
+// shuffle). The short final step of a stripe, if any, keeps whole 64-byte
+// blocks per lane and reads its angles from memory. HBM traffic is the
 // algorithmic minimum (each byte read once, written once); the kernel is bound
 // by the VALU work of the hash plus the fp64 rotation.
 #include "blake2s.h"
@@ -24,37 +27,27 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
-constexpr int kMaxD = 512;  // largest head dimension (d * element bytes <= 1024)
 #ifndef CM_FUSED_BLOCKS_PER_CU
 #define CM_FUSED_BLOCKS_PER_CU 2
 #endif
 
-__device__ __forceinline__ void load64(const uint8_t* p, uint32_t (&m)[16]) {
-  const CM_GLOBAL u32x4* q = global_ptr<u32x4>(p);
-#pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    const u32x4 v = __builtin_nontemporal_load(q + k);
-    m[4 * k + 0] = v[0];
-    m[4 * k + 1] = v[1];
-    m[4 * k + 2] = v[2];
-    m[4 * k + 3] = v[3];
-  }
+__device__ __forceinline__ u32x4 ld16(const uint8_t* p) {
+  return __builtin_nontemporal_load(global_ptr<u32x4>(p));
 }
 
-__device__ __forceinline__ void store64(uint8_t* p, const uint32_t (&y)[16]) {
-#pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    u32x4 v;
-    v[0] = y[4 * k + 0];
-    v[1] = y[4 * k + 1];
-    v[2] = y[4 * k + 2];
-    v[3] = y[4 * k + 3];
-    st_stream(p + 16 * k, v);
+// Element e of a 16-byte piece as fp64.
+template <int ESIZE>
+__device__ __forceinline__ double piece_elem(const u32x4 v, int e) {
+  if constexpr (ESIZE == 2) {
+    const uint32_t x = v[e >> 1];
+    return (double)__uint_as_float((e & 1) ? (x & 0xFFFF0000u) : (x << 16));
+  } else {
+    return (double)__uint_as_float(v[e]);
   }
 }
 
 template <int ESIZE>
-__device__ __forceinline__ void put_bits(uint32_t (&y)[16], int e, uint32_t bits) {
+__device__ __forceinline__ void piece_put(u32x4& y, int e, uint32_t bits) {
   if constexpr (ESIZE == 2) {
     if (e & 1) y[e >> 1] |= bits << 16;
     else y[e >> 1] = bits;
@@ -63,48 +56,102 @@ __device__ __forceinline__ void put_bits(uint32_t (&y)[16], int e, uint32_t bits
   }
 }
 
-// Rotate the block x (lane's chunk c of a row; bpr blocks per row) into y.
-// ang holds (cos, sin) of pair j at [2j], [2j+1]. Must be reached by every lane
-// of the wave (the half-row partner comes from a cross-lane shuffle).
-template <int ESIZE, int STYLE>
-__device__ __forceinline__ void rotate_block(const uint32_t (&x)[16], int c, int bpr,
-                                             const double* ang, uint32_t (&y)[16]) {
+// Rotate one 16-byte piece whose pairs are (x, partner) with the lane's fixed
+// angles; first half: y = x c - p s, second half: y = x c + p s = x c - (-p) s.
+template <int ESIZE>
+__device__ __forceinline__ u32x4 rotate_piece_half(const u32x4 x, const u32x4 p, bool second,
+                                                   const double* cs, const double* sn) {
 #pragma clang fp contract(off)
-  constexpr int E = 64 / ESIZE;  // elements per block
-  if constexpr (STYLE == CM_ROPE_INTERLEAVED) {
-    const int j0 = c * (E / 2);
+  constexpr int EP = 16 / ESIZE;
+  u32x4 y;
 #pragma unroll
-    for (int p = 0; p < E / 2; ++p) {
-      const double x1 = elem_f64<ESIZE>(x, 2 * p), x2 = elem_f64<ESIZE>(x, 2 * p + 1);
-      const double cs = ang[2 * (j0 + p)], sn = ang[2 * (j0 + p) + 1];
-      put_bits<ESIZE>(y, 2 * p, round_bits<ESIZE>(x1 * cs - x2 * sn));
-      put_bits<ESIZE>(y, 2 * p + 1, round_bits<ESIZE>(x2 * cs + x1 * sn));
+  for (int e = 0; e < EP; ++e) {
+    const double xv = piece_elem<ESIZE>(x, e);
+    const double pv = second ? -piece_elem<ESIZE>(p, e) : piece_elem<ESIZE>(p, e);
+    piece_put<ESIZE>(y, e, round_bits<ESIZE>(xv * cs[e] - pv * sn[e]));
+  }
+  return y;
+}
+
+// Interleaved pairs (2j, 2j+1) inside the piece.
+template <int ESIZE>
+__device__ __forceinline__ u32x4 rotate_piece_il(const u32x4 x, const double* cs,
+                                                 const double* sn) {
+#pragma clang fp contract(off)
+  constexpr int EP = 16 / ESIZE;
+  u32x4 y;
+#pragma unroll
+  for (int q = 0; q < EP / 2; ++q) {
+    const double x1 = piece_elem<ESIZE>(x, 2 * q), x2 = piece_elem<ESIZE>(x, 2 * q + 1);
+    piece_put<ESIZE>(y, 2 * q, round_bits<ESIZE>(x1 * cs[q] - x2 * sn[q]));
+    piece_put<ESIZE>(y, 2 * q + 1, round_bits<ESIZE>(x2 * cs[q] + x1 * sn[q]));
+  }
+  return y;
+}
+
+// Short final step: lane owns block c (of bpr per row) of its row as 4 pieces
+// with consecutive columns; ang = the slot's (cos, sin) table in global memory.
+// Reached by every lane of the wave (cross-lane shuffle for the half row).
+template <int ESIZE, int STYLE>
+__device__ __forceinline__ void rotate_block_tail(u32x4 (&x)[4], int c, int bpr,
+                                                  const double* __restrict__ ang) {
+#pragma clang fp contract(off)
+  constexpr int EP = 16 / ESIZE;
+  if constexpr (STYLE == CM_ROPE_INTERLEAVED) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int j0 = (c * 4 + k) * (EP / 2);
+      double cs[EP / 2], sn[EP / 2];
+#pragma unroll
+      for (int q = 0; q < EP / 2; ++q) {
+        cs[q] = ang[2 * (j0 + q)];
+        sn[q] = ang[2 * (j0 + q) + 1];
+      }
+      x[k] = rotate_piece_il<ESIZE>(x[k], cs, sn);
     }
   } else if (bpr == 1) {
-    // the whole row is this block: pairs (e, e + E/2)
+    // the whole row is this block: pieces 0-1 pair with pieces 2-3
+    u32x4 y[4];
 #pragma unroll
-    for (int e = 0; e < E / 2; ++e) {
-      const double x1 = elem_f64<ESIZE>(x, e), x2 = elem_f64<ESIZE>(x, e + E / 2);
-      const double cs = ang[2 * e], sn = ang[2 * e + 1];
-      put_bits<ESIZE>(y, e, round_bits<ESIZE>(x1 * cs - x2 * sn));
-      put_bits<ESIZE>(y, e + E / 2, round_bits<ESIZE>(x2 * cs + x1 * sn));
+    for (int k = 0; k < 2; ++k) {
+      double cs[EP], sn[EP];
+#pragma unroll
+      for (int e = 0; e < EP; ++e) {
+        cs[e] = ang[2 * (k * EP + e)];
+        sn[e] = ang[2 * (k * EP + e) + 1];
+      }
+      y[k] = rotate_piece_half<ESIZE>(x[k], x[k + 2], false, cs, sn);
+      y[k + 2] = rotate_piece_half<ESIZE>(x[k + 2], x[k], true, cs, sn);
     }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) x[k] = y[k];
   } else {
     const int hb = bpr >> 1;
-    uint32_t p[16];
-#pragma unroll
-    for (int w = 0; w < 16; ++w) p[w] = __shfl_xor(x[w], hb, 64);
     const bool second = c >= hb;
-    const int j0 = (second ? c - hb : c) * E;
-    // first half: y = x c - p s; second half: y = x c + p s = x c - (-p) s
-    const double sg = second ? -1.0 : 1.0;
+    const int cb = second ? c - hb : c;
 #pragma unroll
-    for (int e = 0; e < E; ++e) {
-      const double xv = elem_f64<ESIZE>(x, e);
-      const double pv = sg * elem_f64<ESIZE>(p, e);
-      const double cs = ang[2 * (j0 + e)], sn = ang[2 * (j0 + e) + 1];
-      put_bits<ESIZE>(y, e, round_bits<ESIZE>(xv * cs - pv * sn));
+    for (int k = 0; k < 4; ++k) {
+      u32x4 p;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) p[w] = __shfl_xor(x[k][w], hb, 64);
+      const int j0 = (cb * 4 + k) * EP;
+      double cs[EP], sn[EP];
+#pragma unroll
+      for (int e = 0; e < EP; ++e) {
+        cs[e] = ang[2 * (j0 + e)];
+        sn[e] = ang[2 * (j0 + e) + 1];
+      }
+      x[k] = rotate_piece_half<ESIZE>(x[k], p, second, cs, sn);
     }
+  }
+}
+
+// (head, row) of a tensor row index r advanced by `by` rows (T rows per head).
+__device__ __forceinline__ void advance_row(int64_t& hh, int64_t& tt, int64_t by, int64_t T) {
+  tt += by;
+  while (tt >= T) {
+    tt -= T;
+    ++hh;
   }
 }
 
@@ -115,15 +162,18 @@ __global__ __launch_bounds__(kThreads) void render_hash_kernel(
     const double* __restrict__ angles, int32_t H, int32_t d, int64_t T_out,
     const uint8_t* __restrict__ select, const int64_t* __restrict__ base0,
     uint8_t* __restrict__ nodes, uint8_t* __restrict__ out) {
-  __shared__ double sh_ang[kWaves][kMaxD];
+  constexpr int EP = 16 / ESIZE;                   // elements per 16-byte piece
+  constexpr int NA = STYLE == CM_ROPE_HALF ? EP : EP / 2;  // angle pairs per lane
   const int wave = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
   const int64_t row_bytes = (int64_t)d * ESIZE;
-  const int bpr = (int)(row_bytes >> 6);  // 64-byte blocks per row: 1, 2, 4, 8 or 16
-  const int c = lane & (bpr - 1);         // this lane's block within its row
-  const int rows_step = 64 / bpr;         // rows covered by one wave step
+  const int ppr = (int)(row_bytes >> 4);           // 16-byte pieces per row: 4 .. 64
+  const int bpr = ppr >> 2;                        // 64-byte blocks per row
+  const int cp = lane & (ppr - 1);                 // column piece of this lane (full steps)
+  const bool second = STYLE == CM_ROPE_HALF && cp >= (ppr >> 1);
+  const int rows_q = 64 / ppr;                     // rows between a lane's pieces q and q+1
+  const int rows_step = 256 / ppr;                 // rows per 4 KiB step
   const int64_t waves = (int64_t)gridDim.x * kWaves;
-  double* ang = sh_ang[wave];
   for (int64_t task = (int64_t)blockIdx.x * kWaves + wave; task < total_tasks; task += waves) {
     int lo = 0, hi = n_u - 1;
     while (lo < hi) {
@@ -138,52 +188,104 @@ __global__ __launch_bounds__(kThreads) void render_hash_kernel(
     const int64_t bytes = (int64_t)H * T * row_bytes;
     const int64_t stripes = stripes_of(bytes);
     const int64_t local = task - task_base[s];
-    const int64_t t = local / stripes;            // tensor: 2l + kv
+    const int64_t t = local / stripes;             // tensor: 2l + kv
     const int64_t sidx = local - t * stripes;
     const bool rotate = (t & 1) == 0 && off != 0;
+    const double* ang = angles + (int64_t)s * d;
+    double cs[NA], sn[NA];
     if (rotate) {
-      for (int q = lane; q < d; q += 64) ang[q] = angles[(int64_t)s * d + q];
-      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-      __builtin_amdgcn_wave_barrier();
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      const int j0 = STYLE == CM_ROPE_HALF ? (second ? cp - (ppr >> 1) : cp) * EP : cp * (EP / 2);
+#pragma unroll
+      for (int e = 0; e < NA; ++e) {
+        cs[e] = ang[2 * (j0 + e)];
+        sn[e] = ang[2 * (j0 + e) + 1];
+      }
     }
     const int64_t in_stripe = (bytes >> 6) - sidx * kStripeBlocks;
     const int bh = (int)(in_stripe < kStripeBlocks ? in_stripe : kStripeBlocks);
-    const int steps = (bh + kStripeLeaves - 1) / kStripeLeaves;
-    const int nb = lane < bh ? (bh - lane + kStripeLeaves - 1) / kStripeLeaves : 0;
-    const int64_t first_block = sidx * kStripeBlocks + lane;
+    const int full_steps = bh / kStripeLeaves;
+    const int rem = bh - full_steps * kStripeLeaves;
+    const int nb = full_steps + (lane < rem ? 1 : 0);
     const uint8_t* src = reinterpret_cast<const uint8_t*>(table[i * stride + 1 + t]) +
-                         (first_block << 6);
+                         ((sidx * kStripeBlocks) << 6);
     uint8_t* out_t = out + t * (int64_t)H * T_out * row_bytes;
     const int64_t leaf = sidx * kStripeLeaves + lane;
     const int64_t m = leaves_of(bytes);
-    int64_t row = first_block / bpr;
-    int64_t hh = row / T;
-    int64_t tt = row - hh * T;
     B2sState st;
     b2s_init_tree(st, (uint64_t)leaf, 0);
-    uint32_t cur[16], nxt[16];
-    if (nb > 0) load64(src, cur);
-    for (int j = 0; j < steps; ++j) {
-      const bool active = j < nb;
-      if (j + 1 < nb) load64(src + (int64_t)(j + 1) * (kStripeLeaves * 64), nxt);
-      if (hashing && active)
-        b2s_compress(st, cur, (uint64_t)(j + 1) << 6, j + 1 == nb, j + 1 == nb && leaf == m - 1);
-      uint32_t y[16];
-      if (rotate) {
-        rotate_block<ESIZE, STYLE>(cur, c, bpr, ang, y);
-      } else {
+    // row of piece 0 of this lane in step 0
+    int64_t hh, tt;
+    {
+      const int64_t r0 = ((sidx * kStripeBlocks) << 6) / row_bytes + lane / ppr;
+      hh = r0 / T;
+      tt = r0 - hh * T;
+    }
+    u32x4 cur[4], nxt[4];
+    if (full_steps > 0) {
 #pragma unroll
-        for (int w = 0; w < 16; ++w) y[w] = cur[w];
-      }
-      if (active) store64(out_t + ((hh * T_out + off + tt) * row_bytes + c * 64), y);
-      tt += rows_step;
-      while (tt >= T) {
-        tt -= T;
-        ++hh;
-      }
+      for (int k = 0; k < 4; ++k) cur[k] = ld16(src + lane * 16 + k * 1024);
+    }
+    for (int j = 0; j < full_steps; ++j) {
+      if (j + 1 < full_steps) {
 #pragma unroll
-      for (int w = 0; w < 16; ++w) cur[w] = nxt[w];
+        for (int k = 0; k < 4; ++k) nxt[k] = ld16(src + ((int64_t)(j + 1) << 12) + lane * 16 + k * 1024);
+      }
+      if (hashing) {
+        uint32_t w[16];
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) w[4 * k + q] = cur[k][q];
+        b2s_compress(st, w, (uint64_t)(j + 1) << 6, j + 1 == nb, j + 1 == nb && leaf == m - 1);
+      }
+      int64_t h2 = hh, t2 = tt;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        u32x4 y = cur[k];
+        if (rotate) {
+          if constexpr (STYLE == CM_ROPE_HALF) {
+            u32x4 p;
+#pragma unroll
+            for (int w = 0; w < 4; ++w) p[w] = __shfl_xor(cur[k][w], ppr >> 1, 64);
+            y = rotate_piece_half<ESIZE>(cur[k], p, second, cs, sn);
+          } else {
+            y = rotate_piece_il<ESIZE>(cur[k], cs, sn);
+          }
+        }
+        st_stream(out_t + (h2 * T_out + off + t2) * row_bytes + cp * 16, y);
+        if (k < 3) advance_row(h2, t2, rows_q, T);
+      }
+      advance_row(hh, tt, rows_step, T);
+#pragma unroll
+      for (int k = 0; k < 4; ++k) cur[k] = nxt[k];
+    }
+    if (rem > 0) {
+      // short final step: lane < rem owns block `lane` whole (4 consecutive pieces)
+      const uint8_t* sp = src + ((int64_t)full_steps << 12) + lane * 64;
+      u32x4 x[4] = {};
+      if (lane < rem) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) x[k] = ld16(sp + 16 * k);
+        if (hashing) {
+          uint32_t w[16];
+#pragma unroll
+          for (int k = 0; k < 4; ++k)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) w[4 * k + q] = x[k][q];
+          b2s_compress(st, w, (uint64_t)nb << 6, true, leaf == m - 1);
+        }
+      }
+      const int64_t step_byte = ((sidx * kStripeBlocks + (int64_t)full_steps * 64) << 6) + lane * 64;
+      const int64_t r = step_byte / row_bytes;
+      const int cb = (int)((step_byte % row_bytes) >> 6);   // block of the row
+      if (rotate) rotate_block_tail<ESIZE, STYLE>(x, cb, bpr, ang);
+      if (lane < rem) {
+        const int64_t h3 = r / T;
+        const int64_t t3 = r - h3 * T;
+        uint8_t* dp = out_t + (h3 * T_out + off + t3) * row_bytes + cb * 64;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) st_stream(dp + 16 * k, x[k]);
+      }
     }
     if (hashing && nb > 0) {
       uint4* q = reinterpret_cast<uint4*>(nodes + (base0[i] + t * m + leaf) * 32);

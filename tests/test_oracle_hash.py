@@ -39,23 +39,33 @@ def _expected_leaves(nbytes):
     return 64 * full + min(64, rest)
 
 
-@pytest.mark.parametrize("nblocks", [1, 5, 64, 65, 4096, 4096 + 1, 4096 * 2 + 70, 4096 * 3])
+@pytest.mark.parametrize("nblocks", [1, 5, 64, 65, 130, 4096, 4096 + 1, 4096 * 2 + 70, 4096 * 3])
 def test_striped_leaves_closed_form(nblocks):
-    """Leaf k of a stripe holds blocks k, k+64, ... of that stripe: the leaves are
-    a permutation of the 64-byte blocks, at most 4 KiB each."""
-    ids = np.arange(nblocks * 16, dtype=np.uint32)          # 16 words per block
+    """Closed form of the leaf layout: in a full 4 KiB step leaf k takes the
+    16-byte pieces k, k+64, k+128, k+192; in a shorter final step it takes
+    block k whole. The leaves are a permutation of the 16-byte pieces."""
+    npieces = nblocks * 4
+    ids = np.arange(npieces * 4, dtype=np.uint32)           # 4 words per 16-byte piece
     buf = ids.view(np.uint8)
     leaves = om.tensor_leaves(buf)
     assert len(leaves) == _expected_leaves(buf.nbytes)
     seen = []
     for idx, leaf in enumerate(leaves):
         assert 0 < len(leaf) <= 4096 and len(leaf) % 64 == 0
-        words = np.frombuffer(leaf, np.uint32).reshape(-1, 16)
-        blocks = (words[:, 0] // 16).tolist()
+        pieces = (np.frombuffer(leaf, np.uint32).reshape(-1, 4)[:, 0] // 4).tolist()
         s, k = divmod(idx, 64)
-        assert blocks == list(range(s * 4096 + k, min((s + 1) * 4096, nblocks), 64))
-        seen += blocks
-    assert sorted(seen) == list(range(nblocks))
+        want = []
+        stripe_pieces = min(16384, npieces - s * 16384)
+        for t0 in range(0, stripe_pieces, 256):
+            base = s * 16384 + t0
+            step = min(256, stripe_pieces - t0)
+            if step == 256:
+                want += [base + k + 64 * q for q in range(4)]
+            elif 4 * k < step:
+                want += [base + 4 * k + q for q in range(4)]
+        assert pieces == want
+        seen += pieces
+    assert sorted(seen) == list(range(npieces))
 
 
 @pytest.mark.parametrize("nblocks", [1, 2, 64, 65, 130, 4096 + 3, 3 * 4096])
