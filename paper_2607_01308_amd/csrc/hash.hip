@@ -119,8 +119,9 @@ __global__ __launch_bounds__(kBlock) void hash_leaf_kernel(const int64_t* __rest
                                                            uint32_t want,
                                                            uint8_t* __restrict__ nodes) {
   const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform per wave
   const int64_t waves = (int64_t)gridDim.x * (kBlock / 64);
-  for (int64_t task = (int64_t)blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6); task < total_tasks;
+  for (int64_t task = (int64_t)blockIdx.x * (kBlock / 64) + wave; task < total_tasks;
        task += waves) {
     const int i = find_fragment(task_base, n, task);
     if (select && select[i] != want) continue;

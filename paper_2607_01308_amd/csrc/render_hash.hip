@@ -12,9 +12,12 @@
 // unchanged, other K rotated by R(off). A row holds row_bytes / 16 pieces and
 // 64 is a multiple of that, so all four pieces of a lane sit in the same column
 // of their rows: the lane's cos/sin pairs are fixed for the task (registers),
-// and the other half of its pairs is in lane ^ (pieces per row / 2) (one xor
-// shuffle). The short final step of a stripe, if any, keeps whole 64-byte
-// blocks per lane and reads its angles from memory. HBM traffic is the
+// and the other half of its pairs is in lane ^ (pieces per row / 2) (one
+// cross-lane move, chosen at compile time). A step covers whole rows; unless it
+// straddles two heads its rows are consecutive in the merged cache too, so its
+// stores take the same wave-uniform base plus lane offsets as its loads. The
+// short final step of a stripe, if any, keeps whole 64-byte blocks per lane and
+// reads its angles from memory. HBM traffic is the
 // algorithmic minimum (each byte read once, written once); the kernel is bound
 // by the VALU work of the hash plus the fp64 rotation.
 #include "blake2s.h"
@@ -27,9 +30,21 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
+// Persistent grid of CUs x CM_FUSED_BLOCKS_PER_CU blocks; the register budget
+// is capped so that CM_FUSED_WAVES_PER_EU waves fit on each SIMD (3 waves:
+// 168 VGPRs, enough for the hash state, two 4 KiB step buffers and the angles).
 #ifndef CM_FUSED_BLOCKS_PER_CU
-#define CM_FUSED_BLOCKS_PER_CU 2
+#define CM_FUSED_BLOCKS_PER_CU 4
 #endif
+#ifndef CM_FUSED_WAVES_PER_EU
+#define CM_FUSED_WAVES_PER_EU 3
+#endif
+#define CM_FUSED_OCCUPANCY __attribute__((amdgpu_waves_per_eu(CM_FUSED_WAVES_PER_EU)))
+
+template <int S, int B>
+struct Tag {
+  static constexpr int style = S, hb = B;
+};
 
 __device__ __forceinline__ u32x4 ld16(const uint8_t* p) {
   return __builtin_nontemporal_load(global_ptr<u32x4>(p));
@@ -56,21 +71,58 @@ __device__ __forceinline__ void piece_put(u32x4& y, int e, uint32_t bits) {
   }
 }
 
-// Rotate one 16-byte piece whose pairs are (x, partner) with the lane's fixed
-// angles; first half: y = x c - p s, second half: y = x c + p s = x c - (-p) s.
+// Round EP fp64 values into a 16-byte piece. bf16: fp32 rounding first is exact
+// unless an fp32 result sits on a bf16 midpoint (see bf16_bits_rne); that rare
+// case is tested once for the whole piece and settled element by element.
 template <int ESIZE>
-__device__ __forceinline__ u32x4 rotate_piece_half(const u32x4 x, const u32x4 p, bool second,
-                                                   const double* cs, const double* sn) {
+__device__ __forceinline__ u32x4 round_piece(const double (&y)[16 / ESIZE]) {
+  constexpr int EP = 16 / ESIZE;
+  u32x4 out;
+  if constexpr (ESIZE == 2) {
+    float f[EP];
+    bool mid = false;
+#pragma unroll
+    for (int e = 0; e < EP; ++e) {
+      f[e] = (float)y[e];
+      mid |= (__float_as_uint(f[e]) & 0xFFFFu) == 0x8000u;
+    }
+    if (__builtin_expect(mid, 0)) {
+#pragma unroll
+      for (int e = 0; e < EP; ++e) {
+        uint32_t u = __float_as_uint(f[e]);
+        if ((u & 0xFFFFu) == 0x8000u) {
+          const double back = (double)f[e];
+          if (y[e] != back) u = (fabs(y[e]) > fabs(back)) ? u + 1u : u - 1u;
+        }
+        f[e] = __uint_as_float(u);
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const uint32_t lo = __builtin_bit_cast(uint16_t, (__bf16)f[2 * k]);
+      const uint32_t hi = __builtin_bit_cast(uint16_t, (__bf16)f[2 * k + 1]);
+      out[k] = lo | (hi << 16);
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < EP; ++e) out[e] = __float_as_uint((float)y[e]);
+  }
+  return out;
+}
+
+// Rotate one 16-byte piece whose pairs are (x, partner p) with the lane's fixed
+// angles: y = x c - p s', where s' = s in the first half of the row and -s in
+// the second (x c - p (-s) = x c + p s, bit for bit).
+template <int ESIZE>
+__device__ __forceinline__ u32x4 rotate_piece_half(const u32x4 x, const u32x4 p, const double* cs,
+                                                   const double* sn) {
 #pragma clang fp contract(off)
   constexpr int EP = 16 / ESIZE;
-  u32x4 y;
+  double y[EP];
 #pragma unroll
-  for (int e = 0; e < EP; ++e) {
-    const double xv = piece_elem<ESIZE>(x, e);
-    const double pv = second ? -piece_elem<ESIZE>(p, e) : piece_elem<ESIZE>(p, e);
-    piece_put<ESIZE>(y, e, round_bits<ESIZE>(xv * cs[e] - pv * sn[e]));
-  }
-  return y;
+  for (int e = 0; e < EP; ++e)
+    y[e] = piece_elem<ESIZE>(x, e) * cs[e] - piece_elem<ESIZE>(p, e) * sn[e];
+  return round_piece<ESIZE>(y);
 }
 
 // Interleaved pairs (2j, 2j+1) inside the piece.
@@ -79,21 +131,35 @@ __device__ __forceinline__ u32x4 rotate_piece_il(const u32x4 x, const double* cs
                                                  const double* sn) {
 #pragma clang fp contract(off)
   constexpr int EP = 16 / ESIZE;
-  u32x4 y;
+  double y[EP];
 #pragma unroll
   for (int q = 0; q < EP / 2; ++q) {
     const double x1 = piece_elem<ESIZE>(x, 2 * q), x2 = piece_elem<ESIZE>(x, 2 * q + 1);
-    piece_put<ESIZE>(y, 2 * q, round_bits<ESIZE>(x1 * cs[q] - x2 * sn[q]));
-    piece_put<ESIZE>(y, 2 * q + 1, round_bits<ESIZE>(x2 * cs[q] + x1 * sn[q]));
+    y[2 * q] = x1 * cs[q] - x2 * sn[q];
+    y[2 * q + 1] = x2 * cs[q] + x1 * sn[q];
   }
-  return y;
+  return round_piece<ESIZE>(y);
 }
 
-// Short final step: lane owns block c (of bpr per row) of its row as 4 pieces
-// with consecutive columns; ang = the slot's (cos, sin) table in global memory.
-// Reached by every lane of the wave (cross-lane shuffle for the half row).
-template <int ESIZE, int STYLE>
-__device__ __forceinline__ void rotate_block_tail(u32x4 (&x)[4], int c, int bpr,
+// Word of the lane HB away (lane ^ HB) in the wave, without LDS traffic where
+// the hardware allows: HB = 1 and 2 are quad permutations, HB = 8 a DPP rotate by 8
+// within each 16-lane row, HB = 4 and 16 a ds_swizzle xor inside 32 lanes, and
+// HB = 32 a ds_bpermute.
+template <int HB>
+__device__ __forceinline__ uint32_t lane_xor(uint32_t v) {
+  if constexpr (HB == 1) return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0xB1, 0xF, 0xF, false);
+  else if constexpr (HB == 2) return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x4E, 0xF, 0xF, false);
+  else if constexpr (HB == 8) return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x128, 0xF, 0xF, false);
+  else if constexpr (HB == 4 || HB == 16) return (uint32_t)__builtin_amdgcn_ds_swizzle((int)v, (HB << 10) | 0x1F);
+  else return (uint32_t)__shfl_xor((int)v, HB, 64);
+}
+
+// Short final step: lane owns block c of its row as 4 pieces with consecutive
+// columns; ang = the slot's (cos, sin) table in global memory. A row holds
+// HB / 2 blocks (half-split pairs: the partner block c ^ (HB / 4) sits HB / 4
+// lanes away). Reached by every lane of the wave (cross-lane exchange).
+template <int ESIZE, int STYLE, int HB>
+__device__ __forceinline__ void rotate_block_tail(u32x4 (&x)[4], int c,
                                                   const double* __restrict__ ang) {
 #pragma clang fp contract(off)
   constexpr int EP = 16 / ESIZE;
@@ -109,54 +175,72 @@ __device__ __forceinline__ void rotate_block_tail(u32x4 (&x)[4], int c, int bpr,
       }
       x[k] = rotate_piece_il<ESIZE>(x[k], cs, sn);
     }
-  } else if (bpr == 1) {
+  } else if constexpr (HB == 2) {
     // the whole row is this block: pieces 0-1 pair with pieces 2-3
     u32x4 y[4];
 #pragma unroll
     for (int k = 0; k < 2; ++k) {
-      double cs[EP], sn[EP];
+      double cs[EP], sn[EP], nsn[EP];
 #pragma unroll
       for (int e = 0; e < EP; ++e) {
         cs[e] = ang[2 * (k * EP + e)];
         sn[e] = ang[2 * (k * EP + e) + 1];
+        nsn[e] = -sn[e];
       }
-      y[k] = rotate_piece_half<ESIZE>(x[k], x[k + 2], false, cs, sn);
-      y[k + 2] = rotate_piece_half<ESIZE>(x[k + 2], x[k], true, cs, sn);
+      y[k] = rotate_piece_half<ESIZE>(x[k], x[k + 2], cs, sn);
+      y[k + 2] = rotate_piece_half<ESIZE>(x[k + 2], x[k], cs, nsn);
     }
 #pragma unroll
     for (int k = 0; k < 4; ++k) x[k] = y[k];
   } else {
-    const int hb = bpr >> 1;
+    constexpr int hb = HB / 4;
     const bool second = c >= hb;
     const int cb = second ? c - hb : c;
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
       u32x4 p;
 #pragma unroll
-      for (int w = 0; w < 4; ++w) p[w] = __shfl_xor(x[k][w], hb, 64);
+      for (int w = 0; w < 4; ++w) p[w] = lane_xor<hb>(x[k][w]);
       const int j0 = (cb * 4 + k) * EP;
       double cs[EP], sn[EP];
 #pragma unroll
       for (int e = 0; e < EP; ++e) {
         cs[e] = ang[2 * (j0 + e)];
-        sn[e] = ang[2 * (j0 + e) + 1];
+        sn[e] = second ? -ang[2 * (j0 + e) + 1] : ang[2 * (j0 + e) + 1];
       }
-      x[k] = rotate_piece_half<ESIZE>(x[k], p, second, cs, sn);
+      x[k] = rotate_piece_half<ESIZE>(x[k], p, cs, sn);
     }
   }
 }
 
-// (head, row) of a tensor row index r advanced by `by` rows (T rows per head).
-__device__ __forceinline__ void advance_row(int64_t& hh, int64_t& tt, int64_t by, int64_t T) {
-  tt += by;
-  while (tt >= T) {
-    tt -= T;
-    ++hh;
-  }
+__device__ __forceinline__ void compress_pieces(B2sState& st, const u32x4 (&x)[4], uint64_t count,
+                                                bool last, bool last_node) {
+  uint32_t w[16];
+#pragma unroll
+  for (int k = 0; k < 4; ++k)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) w[4 * k + q] = x[k][q];
+  b2s_compress(st, w, count, last, last_node);
 }
 
-template <int ESIZE, int STYLE>
-__global__ __launch_bounds__(kThreads) void render_hash_kernel(
+// Destination of byte `rel` (0 <= rel < 4096) of a step whose first row is row
+// tt of head hh of the fragment: rows past the head's end continue in the next
+// head of the merged cache (only reached when a step straddles heads).
+__device__ __forceinline__ uint8_t* dest_wrapped(uint8_t* out_t, int64_t hh, int64_t tt, int rel,
+                                                 int rb_shift, int64_t T, int64_t T_out,
+                                                 int64_t off) {
+  int64_t rr = tt + (rel >> rb_shift);
+  while (rr >= T) {
+    rr -= T;
+    ++hh;
+  }
+  return out_t + ((hh * T_out + off + rr) << rb_shift) + (rel & ((1 << rb_shift) - 1));
+}
+
+// HB: for half-split pairs, the lane distance between a piece and its partner
+// piece in full steps (16-byte pieces per row / 2); 0 for interleaved pairs.
+template <int ESIZE, int STYLE, int HB>
+__global__ __launch_bounds__(kThreads) CM_FUSED_OCCUPANCY void render_hash_kernel(
     const int64_t* __restrict__ table, int64_t stride, int32_t n, const int64_t* __restrict__ plan,
     const int64_t* __restrict__ task_base, int32_t n_u, int64_t total_tasks,
     const double* __restrict__ angles, int32_t H, int32_t d, int64_t T_out,
@@ -164,15 +248,17 @@ __global__ __launch_bounds__(kThreads) void render_hash_kernel(
     uint8_t* __restrict__ nodes, uint8_t* __restrict__ out) {
   constexpr int EP = 16 / ESIZE;                   // elements per 16-byte piece
   constexpr int NA = STYLE == CM_ROPE_HALF ? EP : EP / 2;  // angle pairs per lane
-  const int wave = threadIdx.x >> 6;
+  // the wave index is the same on every lane: say so, so that everything derived
+  // from the task (slot, lengths, offsets, step positions, branches) stays in
+  // scalar registers
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
-  const int64_t row_bytes = (int64_t)d * ESIZE;
+  const int rb_shift = __builtin_ctz((unsigned)(d * ESIZE));   // log2 of the row bytes
+  const int64_t row_bytes = (int64_t)1 << rb_shift;
   const int ppr = (int)(row_bytes >> 4);           // 16-byte pieces per row: 4 .. 64
-  const int bpr = ppr >> 2;                        // 64-byte blocks per row
+  const int rps = 4096 >> rb_shift;                // rows per full step
   const int cp = lane & (ppr - 1);                 // column piece of this lane (full steps)
   const bool second = STYLE == CM_ROPE_HALF && cp >= (ppr >> 1);
-  const int rows_q = 64 / ppr;                     // rows between a lane's pieces q and q+1
-  const int rows_step = 256 / ppr;                 // rows per 4 KiB step
   const int64_t waves = (int64_t)gridDim.x * kWaves;
   for (int64_t task = (int64_t)blockIdx.x * kWaves + wave; task < total_tasks; task += waves) {
     int lo = 0, hi = n_u - 1;
@@ -198,7 +284,7 @@ __global__ __launch_bounds__(kThreads) void render_hash_kernel(
 #pragma unroll
       for (int e = 0; e < NA; ++e) {
         cs[e] = ang[2 * (j0 + e)];
-        sn[e] = ang[2 * (j0 + e) + 1];
+        sn[e] = second ? -ang[2 * (j0 + e) + 1] : ang[2 * (j0 + e) + 1];
       }
     }
     const int64_t in_stripe = (bytes >> 6) - sidx * kStripeBlocks;
@@ -213,51 +299,62 @@ __global__ __launch_bounds__(kThreads) void render_hash_kernel(
     const int64_t m = leaves_of(bytes);
     B2sState st;
     b2s_init_tree(st, (uint64_t)leaf, 0);
-    // row of piece 0 of this lane in step 0
+    // first row of the current step: head hh, row tt of that head (scalars)
     int64_t hh, tt;
     {
-      const int64_t r0 = ((sidx * kStripeBlocks) << 6) / row_bytes + lane / ppr;
+      const int64_t r0 = ((sidx * kStripeBlocks) << 6) >> rb_shift;
       hh = r0 / T;
       tt = r0 - hh * T;
     }
-    u32x4 cur[4], nxt[4];
-    if (full_steps > 0) {
-#pragma unroll
-      for (int k = 0; k < 4; ++k) cur[k] = ld16(src + lane * 16 + k * 1024);
-    }
-    for (int j = 0; j < full_steps; ++j) {
+    auto step = [&](const u32x4 (&x)[4], u32x4 (&nx)[4], int j) {
       if (j + 1 < full_steps) {
 #pragma unroll
-        for (int k = 0; k < 4; ++k) nxt[k] = ld16(src + ((int64_t)(j + 1) << 12) + lane * 16 + k * 1024);
-      }
-      if (hashing) {
-        uint32_t w[16];
-#pragma unroll
         for (int k = 0; k < 4; ++k)
-#pragma unroll
-          for (int q = 0; q < 4; ++q) w[4 * k + q] = cur[k][q];
-        b2s_compress(st, w, (uint64_t)(j + 1) << 6, j + 1 == nb, j + 1 == nb && leaf == m - 1);
+          nx[k] = ld16(src + ((int64_t)(j + 1) << 12) + lane * 16 + k * 1024);
       }
-      int64_t h2 = hh, t2 = tt;
+      if (hashing) compress_pieces(st, x, (uint64_t)(j + 1) << 6, j + 1 == nb,
+                                   j + 1 == nb && leaf == m - 1);
+      u32x4 y[4];
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
-        u32x4 y = cur[k];
+        y[k] = x[k];
         if (rotate) {
           if constexpr (STYLE == CM_ROPE_HALF) {
             u32x4 p;
 #pragma unroll
-            for (int w = 0; w < 4; ++w) p[w] = __shfl_xor(cur[k][w], ppr >> 1, 64);
-            y = rotate_piece_half<ESIZE>(cur[k], p, second, cs, sn);
+            for (int w = 0; w < 4; ++w) p[w] = lane_xor<HB>(x[k][w]);
+            y[k] = rotate_piece_half<ESIZE>(x[k], p, cs, sn);
           } else {
-            y = rotate_piece_il<ESIZE>(cur[k], cs, sn);
+            y[k] = rotate_piece_il<ESIZE>(x[k], cs, sn);
           }
         }
-        st_stream(out_t + (h2 * T_out + off + t2) * row_bytes + cp * 16, y);
-        if (k < 3) advance_row(h2, t2, rows_q, T);
       }
-      advance_row(hh, tt, rows_step, T);
+      if (tt + rps <= T) {
+        // the step's rows are consecutive rows of one head, in the source and in
+        // the merged cache alike
+        uint8_t* dp = out_t + ((hh * T_out + off + tt) << rb_shift) + lane * 16;
 #pragma unroll
-      for (int k = 0; k < 4; ++k) cur[k] = nxt[k];
+        for (int k = 0; k < 4; ++k) st_stream(dp + k * 1024, y[k]);
+      } else {
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+          st_stream(dest_wrapped(out_t, hh, tt, lane * 16 + k * 1024, rb_shift, T, T_out, off),
+                    y[k]);
+      }
+      tt += rps;
+      while (tt >= T) {
+        tt -= T;
+        ++hh;
+      }
+    };
+    u32x4 bufa[4], bufb[4];
+    if (full_steps > 0) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) bufa[k] = ld16(src + lane * 16 + k * 1024);
+    }
+    for (int j = 0; j < full_steps; j += 2) {
+      step(bufa, bufb, j);
+      if (j + 1 < full_steps) step(bufb, bufa, j + 1);
     }
     if (rem > 0) {
       // short final step: lane < rem owns block `lane` whole (4 consecutive pieces)
@@ -266,23 +363,12 @@ __global__ __launch_bounds__(kThreads) void render_hash_kernel(
       if (lane < rem) {
 #pragma unroll
         for (int k = 0; k < 4; ++k) x[k] = ld16(sp + 16 * k);
-        if (hashing) {
-          uint32_t w[16];
-#pragma unroll
-          for (int k = 0; k < 4; ++k)
-#pragma unroll
-            for (int q = 0; q < 4; ++q) w[4 * k + q] = x[k][q];
-          b2s_compress(st, w, (uint64_t)nb << 6, true, leaf == m - 1);
-        }
+        if (hashing) compress_pieces(st, x, (uint64_t)nb << 6, true, leaf == m - 1);
       }
-      const int64_t step_byte = ((sidx * kStripeBlocks + (int64_t)full_steps * 64) << 6) + lane * 64;
-      const int64_t r = step_byte / row_bytes;
-      const int cb = (int)((step_byte % row_bytes) >> 6);   // block of the row
-      if (rotate) rotate_block_tail<ESIZE, STYLE>(x, cb, bpr, ang);
+      const int cb = (int)(((lane * 64) & (row_bytes - 1)) >> 6);   // block of the row
+      if (rotate) rotate_block_tail<ESIZE, STYLE, HB>(x, cb, ang);
       if (lane < rem) {
-        const int64_t h3 = r / T;
-        const int64_t t3 = r - h3 * T;
-        uint8_t* dp = out_t + (h3 * T_out + off + t3) * row_bytes + cb * 64;
+        uint8_t* dp = dest_wrapped(out_t, hh, tt, lane * 64, rb_shift, T, T_out, off);
 #pragma unroll
         for (int k = 0; k < 4; ++k) st_stream(dp + 16 * k, x[k]);
       }
@@ -292,6 +378,36 @@ __global__ __launch_bounds__(kThreads) void render_hash_kernel(
       q[0] = make_uint4(st.h[0], st.h[1], st.h[2], st.h[3]);
       q[1] = make_uint4(st.h[4], st.h[5], st.h[6], st.h[7]);
     }
+  }
+}
+
+template <int ESIZE, int STYLE, int HB>
+void launch_fused(dim3 grid, hipStream_t stream, const SetDesc& s, const int64_t* plan_dev,
+                  const int64_t* tasks, int32_t n_unique, int64_t total_tasks,
+                  const double* angles, int64_t T_out, const uint8_t* hsel,
+                  const int64_t* base_tab, uint8_t* nodes, uint8_t* o) {
+  hipLaunchKernelGGL((render_hash_kernel<ESIZE, STYLE, HB>), grid, dim3(kThreads), 0, stream,
+                     s.table_dev, s.stride, s.n, plan_dev, tasks, n_unique, total_tasks, angles,
+                     s.H, s.d, T_out, hsel, base_tab, nodes, o);
+}
+
+template <int ESIZE>
+void launch_fused_es(int32_t style, dim3 grid, hipStream_t stream, const SetDesc& s,
+                     const int64_t* plan_dev, const int64_t* tasks, int32_t n_unique,
+                     int64_t total_tasks, const double* angles, int64_t T_out,
+                     const uint8_t* hsel, const int64_t* base_tab, uint8_t* nodes, uint8_t* o) {
+  auto go = [&](auto kernel_tag) {
+    constexpr int STYLE = decltype(kernel_tag)::style, HB = decltype(kernel_tag)::hb;
+    launch_fused<ESIZE, STYLE, HB>(grid, stream, s, plan_dev, tasks, n_unique, total_tasks,
+                                   angles, T_out, hsel, base_tab, nodes, o);
+  };
+  if (style == CM_ROPE_INTERLEAVED) return go(Tag<CM_ROPE_INTERLEAVED, 0>{});
+  switch ((int)(s.d * s.esize / 32)) {   // pieces per row / 2
+    case 2: return go(Tag<CM_ROPE_HALF, 2>{});
+    case 4: return go(Tag<CM_ROPE_HALF, 4>{});
+    case 8: return go(Tag<CM_ROPE_HALF, 8>{});
+    case 16: return go(Tag<CM_ROPE_HALF, 16>{});
+    default: return go(Tag<CM_ROPE_HALF, 32>{});
   }
 }
 
@@ -329,25 +445,12 @@ hipError_t launch_render_hash(const SetDesc& s, const HashLayout& hlay, const Re
     ScopedTiming tm(K_RENDER_HASH, stream);
     uint8_t* nodes = hws + hlay.off_buf0;
     uint8_t* o = reinterpret_cast<uint8_t*>(out);
-    if (s.esize == 2) {
-      if (style == CM_ROPE_HALF)
-        hipLaunchKernelGGL((render_hash_kernel<2, CM_ROPE_HALF>), grid, dim3(kThreads), 0, stream,
-                           s.table_dev, s.stride, s.n, plan_dev, tasks, n_unique, total_tasks,
-                           angles, s.H, s.d, T_out, hsel, base_tab, nodes, o);
-      else
-        hipLaunchKernelGGL((render_hash_kernel<2, CM_ROPE_INTERLEAVED>), grid, dim3(kThreads), 0,
-                           stream, s.table_dev, s.stride, s.n, plan_dev, tasks, n_unique,
-                           total_tasks, angles, s.H, s.d, T_out, hsel, base_tab, nodes, o);
-    } else {
-      if (style == CM_ROPE_HALF)
-        hipLaunchKernelGGL((render_hash_kernel<4, CM_ROPE_HALF>), grid, dim3(kThreads), 0, stream,
-                           s.table_dev, s.stride, s.n, plan_dev, tasks, n_unique, total_tasks,
-                           angles, s.H, s.d, T_out, hsel, base_tab, nodes, o);
-      else
-        hipLaunchKernelGGL((render_hash_kernel<4, CM_ROPE_INTERLEAVED>), grid, dim3(kThreads), 0,
-                           stream, s.table_dev, s.stride, s.n, plan_dev, tasks, n_unique,
-                           total_tasks, angles, s.H, s.d, T_out, hsel, base_tab, nodes, o);
-    }
+    if (s.esize == 2)
+      launch_fused_es<2>(style, grid, stream, s, plan_dev, tasks, n_unique, total_tasks, angles,
+                         T_out, hsel, base_tab, nodes, o);
+    else
+      launch_fused_es<4>(style, grid, stream, s, plan_dev, tasks, n_unique, total_tasks, angles,
+                         T_out, hsel, base_tab, nodes, o);
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   return launch_hash_tree(s, hlay, hsel, 0, digests, hws, stream);

@@ -311,6 +311,9 @@ PIPE_SHAPES = [
     dict(dtype="bfloat16", d=32, H=4, L=2, lengths=(513, 40), deliveries=(1, 0, 1)),  # 64 B rows
     dict(dtype="bfloat16", d=512, H=1, L=2, lengths=(300, 257)),         # 1 KiB rows
     dict(dtype="float32", d=16, H=2, L=2, lengths=(70, 33)),             # 64 B rows, fp32
+    dict(dtype="bfloat16", d=256, H=2, L=2, lengths=(520, 61, 3)),       # partner 16 lanes away
+    dict(dtype="float32", d=32, H=3, L=2, lengths=(300, 17)),            # partner 4 lanes away
+    dict(dtype="float32", d=128, H=2, L=2, lengths=(140, 1025)),         # partner 16 lanes away
 ]
 
 
@@ -329,8 +332,9 @@ def test_pipelines_agree_and_match_oracle(spec):
     check_render(outs["fused"], dl, w.dtype, w.routing_layer, w.rope_base)
 
 
-def test_fused_interleaved_style():
-    w = synth.custom("fused-il", dtype="bfloat16", d=128, H=2, L=2, lengths=(600, 333),
+@pytest.mark.parametrize("dtype", ["bfloat16", "float32"])
+def test_fused_interleaved_style(dtype):
+    w = synth.custom("fused-il", dtype=dtype, d=128, H=2, L=2, lengths=(600, 333),
                      routing_layer=0, rope_base=1e4)
     _, dl = gpu_deliveries(w)
     a = cm.render_deliveries(dl, w.routing_layer, w.rope_base, style="interleaved", pipeline="fused")
