@@ -20,6 +20,8 @@
 // reads its angles from memory. HBM traffic is the
 // algorithmic minimum (each byte read once, written once); the kernel is bound
 // by the VALU work of the hash plus the fp64 rotation.
+#include <type_traits>
+
 #include "blake2s.h"
 #include "internal.h"
 #include "stream_ops.h"
@@ -306,12 +308,17 @@ __global__ __launch_bounds__(kThreads) CM_FUSED_OCCUPANCY void render_hash_kerne
       hh = r0 / T;
       tt = r0 - hh * T;
     }
-    auto step = [&](const u32x4 (&x)[4], u32x4 (&nx)[4], int j) {
-      if (j + 1 < full_steps) {
+    const int64_t gap = (T_out - T) << rb_shift;   // end of a head's rows -> next head
+    // One full step: prefetch the next one, hash this one into the lane's leaf,
+    // rotate it if needed, store it. WRAPS: the fragment is shorter than a step
+    // (T < rows per step), so a step may span several heads.
+    auto step = [&](auto wraps, const u32x4 (&x)[4], u32x4 (&nx)[4], int j) {
+      // the last step loads itself again: the loads stay unconditional, which
+      // keeps the count of memory operations the same on every path
+      const int jn = j + 1 < full_steps ? j + 1 : j;
+      const uint8_t* sb = src + ((int64_t)jn << 12);     // wave-uniform base
 #pragma unroll
-        for (int k = 0; k < 4; ++k)
-          nx[k] = ld16(src + ((int64_t)(j + 1) << 12) + lane * 16 + k * 1024);
-      }
+      for (int k = 0; k < 4; ++k) nx[k] = ld16(sb + (uint32_t)(lane * 16 + k * 1024));
       if (hashing) compress_pieces(st, x, (uint64_t)(j + 1) << 6, j + 1 == nb,
                                    j + 1 == nb && leaf == m - 1);
       u32x4 y[4];
@@ -329,32 +336,53 @@ __global__ __launch_bounds__(kThreads) CM_FUSED_OCCUPANCY void render_hash_kerne
           }
         }
       }
-      if (tt + rps <= T) {
-        // the step's rows are consecutive rows of one head, in the source and in
-        // the merged cache alike
-        uint8_t* dp = out_t + ((hh * T_out + off + tt) << rb_shift) + lane * 16;
+      if constexpr (!decltype(wraps)::value) {
+        // the step's rows are consecutive rows of the source and, up to one head
+        // change (branch-free: the rows from `left` on move on by `gap`), of the
+        // merged cache
+        uint8_t* db = out_t + ((hh * T_out + off + tt) << rb_shift);   // wave-uniform base
+        const int64_t left = T - tt;
 #pragma unroll
-        for (int k = 0; k < 4; ++k) st_stream(dp + k * 1024, y[k]);
+        for (int k = 0; k < 4; ++k) {
+          const uint32_t rel = (uint32_t)(lane * 16 + k * 1024);
+          st_stream(db + rel + ((int64_t)(rel >> rb_shift) >= left ? gap : 0), y[k]);
+        }
+        tt += rps;
+        const bool next_head = tt >= T;
+        tt = next_head ? tt - T : tt;
+        hh += next_head ? 1 : 0;
       } else {
 #pragma unroll
         for (int k = 0; k < 4; ++k)
           st_stream(dest_wrapped(out_t, hh, tt, lane * 16 + k * 1024, rb_shift, T, T_out, off),
                     y[k]);
-      }
-      tt += rps;
-      while (tt >= T) {
-        tt -= T;
-        ++hh;
+        tt += rps;
+        while (tt >= T) {
+          tt -= T;
+          ++hh;
+        }
       }
     };
-    u32x4 bufa[4], bufb[4];
-    if (full_steps > 0) {
+    // Software pipeline over the full steps, two buffers. The first step is
+    // peeled so that the loop is entered with the same operations in flight as
+    // on its back edge (this step's loads, the previous stores): the wait for
+    // a step's data then never covers the stores just issued.
+    auto run = [&](auto wraps) {
+      u32x4 bufa[4], bufb[4];
 #pragma unroll
-      for (int k = 0; k < 4; ++k) bufa[k] = ld16(src + lane * 16 + k * 1024);
-    }
-    for (int j = 0; j < full_steps; j += 2) {
-      step(bufa, bufb, j);
-      if (j + 1 < full_steps) step(bufb, bufa, j + 1);
+      for (int k = 0; k < 4; ++k) bufa[k] = ld16(src + (uint32_t)(lane * 16 + k * 1024));
+      step(wraps, bufa, bufb, 0);
+      int j = 1;
+      while (j + 1 < full_steps) {
+        step(wraps, bufb, bufa, j);
+        step(wraps, bufa, bufb, j + 1);
+        j += 2;
+      }
+      if (j < full_steps) step(wraps, bufb, bufa, j);
+    };
+    if (full_steps > 0) {
+      if (T >= rps) run(std::false_type{});
+      else run(std::true_type{});
     }
     if (rem > 0) {
       // short final step: lane < rem owns block `lane` whole (4 consecutive pieces)
