@@ -305,11 +305,9 @@ int32_t cm_canonical_order(const cm_fragset* set, const double* keys_dev,
 
 namespace {
 
-// Checks shared by the render entry points; returns the slot count and the
-// tile count of the tiled render.
+// Checks shared by the render entry points; returns the slot count.
 int32_t check_render_args(const cm::SetDesc& s, const int64_t* plan_dev, const int64_t* plan_host,
-                          const cm_rope* rope, void* out_dev, int64_t T_out, int64_t* nu_out,
-                          int64_t* tiles_out) {
+                          const cm_rope* rope, void* out_dev, int64_t T_out, int64_t* nu_out) {
   if (!rope) return fail(CM_EINVAL, "rope is NULL");
   if (!std::isfinite(rope->base) || rope->base <= 0.0)
     return fail(CM_EINVAL, "rope base must be finite and > 0");
@@ -327,8 +325,7 @@ int32_t check_render_args(const cm::SetDesc& s, const int64_t* plan_dev, const i
   if (nu < 1 || nu > s.n) return fail(CM_EINVAL, "plan n_unique out of range");
   if (T_out < 1 || plan_host[CM_PLAN_TOUT] != T_out)
     return fail(CM_ESHAPE, "T_out does not match the plan");
-  const cm::RenderLayout lay = cm::render_layout(s);
-  int64_t off = 0, tiles = 0;
+  int64_t off = 0;
   for (int64_t k = 0; k < nu; ++k) {
     const int64_t src = plan_host[CM_PLAN_HEADER + k];
     const int64_t o = plan_host[CM_PLAN_HEADER + s.n + k];
@@ -337,12 +334,11 @@ int32_t check_render_args(const cm::SetDesc& s, const int64_t* plan_dev, const i
     if (len != s.T((int)src)) return fail(CM_ESHAPE, "plan slot length differs from the fragment's T");
     if (o != off) return fail(CM_ESHAPE, "plan offsets are not the prefix sum of slot lengths");
     off += len;
-    tiles += (len + lay.tile_rows - 1) / lay.tile_rows;
   }
   if (off != T_out) return fail(CM_ESHAPE, "T_out differs from the sum of slot lengths");
-  if (tiles >= ((int64_t)1 << 31)) return fail(CM_ESHAPE, "merged cache too long for one launch");
+  if (cm::render_units(s, T_out) >= ((int64_t)1 << 31))
+    return fail(CM_ESHAPE, "merged cache too long for one launch");
   *nu_out = nu;
-  *tiles_out = tiles;
   return CM_OK;
 }
 
@@ -357,13 +353,13 @@ int32_t cm_render_merge(const cm_fragset* set, const int64_t* plan_dev, const in
   cm::SetDesc s;
   int32_t st = check_set(set, &s);
   if (st != CM_OK) return st;
-  int64_t nu = 0, tiles = 0;
-  if ((st = check_render_args(s, plan_dev, plan_host, rope, out_dev, T_out, &nu, &tiles)) != CM_OK)
+  int64_t nu = 0;
+  if ((st = check_render_args(s, plan_dev, plan_host, rope, out_dev, T_out, &nu)) != CM_OK)
     return st;
   const cm::RenderLayout lay = cm::render_layout(s);
   if ((st = check_ws(workspace, workspace_bytes, lay.bytes)) != CM_OK) return st;
-  hipError_t e = cm::launch_render(s, lay, plan_dev, (int32_t)nu, tiles, T_out, rope->base,
-                                   rope->style, out_dev, static_cast<uint8_t*>(workspace),
+  hipError_t e = cm::launch_render(s, lay, plan_dev, (int32_t)nu, T_out, rope->base, rope->style,
+                                   out_dev, static_cast<uint8_t*>(workspace),
                                    static_cast<hipStream_t>(stream));
   return e == hipSuccess ? CM_OK : fail_hip(e, "cm_render_merge");
 }
@@ -377,8 +373,8 @@ int32_t cm_render_merge_hash(const cm_fragset* set, const int64_t* plan_dev,
   cm::SetDesc s;
   int32_t st = check_set(set, &s);
   if (st != CM_OK) return st;
-  int64_t nu = 0, tiles = 0;
-  if ((st = check_render_args(s, plan_dev, plan_host, rope, out_dev, T_out, &nu, &tiles)) != CM_OK)
+  int64_t nu = 0;
+  if ((st = check_render_args(s, plan_dev, plan_host, rope, out_dev, T_out, &nu)) != CM_OK)
     return st;
   if (!select_dev) return fail(CM_EINVAL, "select_dev is NULL");
   if (!digests_dev || !aligned(digests_dev, 16))
@@ -387,7 +383,7 @@ int32_t cm_render_merge_hash(const cm_fragset* set, const int64_t* plan_dev,
   const cm::RenderLayout rlay = cm::render_layout(s);
   const size_t need = cm::align_up(hlay.bytes, cm::kWsAlign) + rlay.bytes;
   if ((st = check_ws(workspace, workspace_bytes, need)) != CM_OK) return st;
-  const int64_t tasks = cm::render_hash_tasks(s, plan_host);
+  const int64_t tasks = cm::stripe_tasks(s, plan_host, (int32_t)cm::kStripeBlocks);
   hipError_t e = cm::launch_render_hash(s, hlay, rlay, plan_dev, (int32_t)nu, tasks, T_out,
                                         rope->base, rope->style, select_dev, digests_dev, out_dev,
                                         static_cast<uint8_t*>(workspace),

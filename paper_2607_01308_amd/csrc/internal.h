@@ -87,13 +87,16 @@ KnormLayout knorm_layout(const SetDesc& s, int64_t tail_len);
 size_t knorm_max_bytes(const SetDesc& s);  // over every legal tail_len
 
 struct RenderLayout {
-  int32_t tile_rows;      // rows per render tile
-  size_t off_tiles;       // int64 [n+1] work-unit bases per slot (tiles or stripe tasks)
-  size_t off_angles;      // double [n][d/2][2] cos, sin per slot
+  size_t off_tiles;       // int64 [n+1] work-unit bases per slot (fused hash+render tasks)
+  size_t off_angles;      // double [n][d/2][2] cos, sin per slot (piece-ordered, rotate.h)
   size_t off_hsel;        // uint8 [n]: 0 = slot delivery hashed by the fused kernel
+  size_t off_src_base;    // int64 [n][2LH]: per slot and row block, the source base of row 0
+  size_t off_unit_slot;   // int32 [render units]: slot of each unit of a row block
   size_t bytes;
 };
 RenderLayout render_layout(const SetDesc& s);
+// Units of one merged row block (the render grid's x extent).
+int64_t render_units(const SetDesc& s, int64_t T_out);
 
 // Launchers (enqueue on `stream`, return the first HIP error).
 // select == nullptr hashes every fragment; otherwise only fragments i with
@@ -112,11 +115,13 @@ hipError_t launch_knorm(const SetDesc& s, const KnormLayout& lay, int32_t layer,
                         double* keys, uint8_t* ws, hipStream_t stream);
 hipError_t launch_order(const SetDesc& s, const double* keys, const uint8_t* digests,
                         int64_t* plan, hipStream_t stream);
+// Per-slot angle tables; with stripe_blocks > 0 also the per-slot task bases of
+// 2L * stripes of that many 64-byte blocks (and hsel when select is given).
 hipError_t launch_render_prep(const SetDesc& s, const RenderLayout& lay, const int64_t* plan_dev,
-                              int32_t n_unique, double base, bool stripe_tasks,
+                              int32_t n_unique, double base, int32_t style, int32_t stripe_blocks,
                               const uint8_t* select, uint8_t* ws, hipStream_t stream);
-// Work items of the fused hash+render: 2L * stripes per slot.
-int64_t render_hash_tasks(const SetDesc& s, const int64_t* plan_host);
+// Work items of the fused kernel: 2L * stripes of stripe_blocks per slot.
+int64_t stripe_tasks(const SetDesc& s, const int64_t* plan_host, int32_t stripe_blocks);
 // Render plus, for every slot delivery i with select[i] == 0, its Id (leaf level
 // fused into the render, then the tree). ws = hash workspace, then render's.
 hipError_t launch_render_hash(const SetDesc& s, const HashLayout& hlay, const RenderLayout& rlay,
@@ -124,8 +129,8 @@ hipError_t launch_render_hash(const SetDesc& s, const HashLayout& hlay, const Re
                               int64_t T_out, double base, int32_t style, const uint8_t* select,
                               uint8_t* digests, void* out, uint8_t* ws, hipStream_t stream);
 hipError_t launch_render(const SetDesc& s, const RenderLayout& lay, const int64_t* plan_dev,
-                         int32_t n_unique, int64_t total_tiles, int64_t T_out, double base,
-                         int32_t style, void* out, uint8_t* ws, hipStream_t stream);
+                         int32_t n_unique, int64_t T_out, double base, int32_t style, void* out,
+                         uint8_t* ws, hipStream_t stream);
 
 // Per-kernel event timing (no-op unless cm_timing_enable(1)).
 class ScopedTiming {

@@ -2,289 +2,207 @@
 // [T_out, d] block is the concatenation over slots s of the fragment rows, K
 // multiplied by R(off_s) (byte copy when off_s = 0), V copied.
 //
-// HBM-bound streaming (about 0.4 flop per byte moved), so the design is about
-// bytes in flight: each (l, kv, h, slot) segment is contiguous in both source
-// and destination and is cut into 32 KiB tiles; one 256-lane workgroup moves
-// one tile with all of its 16-byte nontemporal loads issued before the first
-// store. A K lane owns the same 16-byte column chunk of both halves of a row
-// (pairs j and j + d/2, or the adjacent pairs of an interleaved chunk), so its
-// cos/sin values are loaded once per tile from the per-slot angle table and
-// kept in registers. The rotation runs in fp64 with the products and the
-// add/subtract rounded separately, then rounds once to the storage dtype
-// (round-to-nearest-even; bf16 via the compiler's single-step conversion).
-#include "internal.h"
-#include "stream_ops.h"
+// HBM-bound streaming (about 0.4 flop per byte moved). On this chip a copy
+// reaches its highest bandwidth when the grid walks memory in address order in
+// small units, so the render is a one-shot grid of one-wave workgroups, each
+// writing one 4 KiB unit of the merged cache in output order: block (x, y)
+// writes bytes [4096 x, 4096 x + 4096) of row block y = (l*2 + kv)*H + h, lane
+// pieces lane + 64 k (each load and store 1 KiB contiguous across the wave, all
+// pieces of a lane in one column). The lookups are precomputed by a prep pass so
+// that a wave's data load waits on two scalar loads only: the slot of its unit
+// (every row block has the same row -> slot map) and the source base of that
+// slot in its row block. A unit crossing a slot boundary resolves the slot per
+// lane. K at a non-zero offset is rotated with the partner piece fetched from
+// the lane P pieces away.
+#include "rotate.h"
 
 namespace cm {
 
 namespace {
 
-#ifndef CM_RENDER_TILE_BYTES
-#define CM_RENDER_TILE_BYTES 32768
+#ifndef CM_RENDER_UNIT_PIECES
+#define CM_RENDER_UNIT_PIECES 4
 #endif
-constexpr int kThreads = 256;
-constexpr int kTileBytes = CM_RENDER_TILE_BYTES;
+constexpr int kUnitPieces = CM_RENDER_UNIT_PIECES;   // 16-byte pieces per lane
+constexpr int kUnitBytes = 1024 * kUnitPieces;
+constexpr int32_t kUnitCrosses = 1 << 16;            // unit_slot flag: slot boundary inside
 
-// 16 bytes <-> fp64 lanes
-template <int ESIZE>
-struct Chunk;
-
-template <>
-struct Chunk<2> {
-  static constexpr int E = 8;
-  __device__ __forceinline__ static void unpack(const u32x4 v, double (&x)[8]) {
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      x[2 * k] = (double)__uint_as_float(v[k] << 16);
-      x[2 * k + 1] = (double)__uint_as_float(v[k] & 0xFFFF0000u);
-    }
-  }
-  __device__ __forceinline__ static u32x4 pack(const double (&y)[8]) {
-    u32x4 v;
-#pragma unroll
-    for (int k = 0; k < 4; ++k) v[k] = bf16_bits_rne(y[2 * k]) | (bf16_bits_rne(y[2 * k + 1]) << 16);
-    return v;
-  }
-};
-
-template <>
-struct Chunk<4> {
-  static constexpr int E = 4;
-  __device__ __forceinline__ static void unpack(const u32x4 v, double (&x)[4]) {
-#pragma unroll
-    for (int k = 0; k < 4; ++k) x[k] = (double)__uint_as_float(v[k]);
-  }
-  __device__ __forceinline__ static u32x4 pack(const double (&y)[4]) {
-    u32x4 v;
-#pragma unroll
-    for (int k = 0; k < 4; ++k) v[k] = __float_as_uint((float)y[k]);
-    return v;
-  }
-};
-
-__device__ __forceinline__ void copy_tile(const uint8_t* __restrict__ src, uint8_t* __restrict__ dst,
-                                          int64_t bytes) {
-  constexpr int U = kTileBytes / 16 / kThreads;
-  const int tid = threadIdx.x;
-  const int64_t chunks = bytes >> 4;
-  if (chunks == (int64_t)U * kThreads) {
-    u32x4 v[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) v[u] = ld_stream(src + (int64_t)(tid + u * kThreads) * 16);
-#pragma unroll
-    for (int u = 0; u < U; ++u) st_stream(dst + (int64_t)(tid + u * kThreads) * 16, v[u]);
-  } else {
-    for (int64_t c = tid; c < chunks; c += kThreads) st_stream(dst + c * 16, ld_stream(src + c * 16));
-  }
-}
-
-// Rotate rows of one slot. HALF: lane pairs column chunk q of the first half with
-// chunk q of the second half (P = chunks per half row). INTERLEAVED: lane owns
-// chunk c of the row, whose EPC elements are EPC/2 adjacent pairs.
-template <int ESIZE, int STYLE>
-__device__ __forceinline__ void rotate_tile(const uint8_t* __restrict__ src,
-                                            uint8_t* __restrict__ dst, int64_t rows, int d,
-                                            const double* __restrict__ cs) {
-#pragma clang fp contract(off)
-  using C = Chunk<ESIZE>;
-  constexpr int E = C::E;
-  const int row_bytes = d * ESIZE;
-  const int tid = threadIdx.x;
-  if constexpr (STYLE == CM_ROPE_HALF) {
-    const int P = row_bytes >> 5;          // 16-byte chunks per half row
-    const int rpi = kThreads / P;          // rows per iteration
-    const int q = tid % P;
-    const int rsub = tid / P;
-    const int half = row_bytes >> 1;
-    double c[E], sn[E];
-#pragma unroll
-    for (int e = 0; e < E; ++e) {
-      c[e] = cs[2 * (q * E + e)];
-      sn[e] = cs[2 * (q * E + e) + 1];
-    }
-    constexpr int U = kTileBytes / 32 / kThreads;  // iterations of a full tile
-    auto body = [&](const u32x4 a, const u32x4 b, u32x4& ya, u32x4& yb) {
-      double x1[E], x2[E], y1[E], y2[E];
-      C::unpack(a, x1);
-      C::unpack(b, x2);
-#pragma unroll
-      for (int e = 0; e < E; ++e) {
-        y1[e] = x1[e] * c[e] - x2[e] * sn[e];
-        y2[e] = x2[e] * c[e] + x1[e] * sn[e];
-      }
-      ya = C::pack(y1);
-      yb = C::pack(y2);
-    };
-    if (rows == (int64_t)U * rpi) {
-      u32x4 a[U], b[U];
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int64_t off = (int64_t)(rsub + u * rpi) * row_bytes + q * 16;
-        a[u] = ld_stream(src + off);
-        b[u] = ld_stream(src + off + half);
-      }
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int64_t off = (int64_t)(rsub + u * rpi) * row_bytes + q * 16;
-        u32x4 ya, yb;
-        body(a[u], b[u], ya, yb);
-        st_stream(dst + off, ya);
-        st_stream(dst + off + half, yb);
+template <int ESIZE, int STYLE, int HB>
+__global__ __launch_bounds__(64) void render_unit_kernel(
+    const int32_t* __restrict__ unit_slot, const int64_t* __restrict__ src_base,
+    const int64_t* __restrict__ plan, int32_t n, int32_t n_u, const double* __restrict__ angles,
+    int32_t H, int32_t d, int64_t T_out, uint8_t* __restrict__ out) {
+  constexpr int EP = 16 / ESIZE;
+  constexpr int NA = STYLE == CM_ROPE_HALF ? EP : EP / 2;
+  const int lane = threadIdx.x;
+  const int rb_shift = __builtin_ctz((unsigned)(d * ESIZE));
+  const int64_t row_mask = ((int64_t)1 << rb_shift) - 1;
+  const int ppr = (d * ESIZE) >> 4;                    // 16-byte pieces per row
+  const int lkh = blockIdx.y;                          // (l * 2 + kv) * H + h
+  const bool is_k = ((lkh / H) & 1) == 0;
+  const int64_t R = T_out << rb_shift;                 // bytes of one row block
+  const int64_t lb = (int64_t)blockIdx.x * kUnitBytes + lane * 16;   // piece k: lb + 1024 k
+  const int cp = (int)((lb & row_mask) >> 4);          // column piece of this lane
+  const int64_t* offs = plan + CM_PLAN_HEADER + n;
+  const int64_t n_lkh = gridDim.y;
+  // piece k from slot s: load, rotate (K at a non-zero offset), store
+  auto piece = [&](int k, int s, const double* cs, const double* sn) {
+    const int64_t b = lb + 1024 * k;
+    const bool valid = b < R;
+    const uint8_t* src = reinterpret_cast<const uint8_t*>(src_base[s * n_lkh + lkh]);
+    u32x4 x = {0u, 0u, 0u, 0u};
+    if (valid) x = ld16(src + b);                      // row b >> rb_shift, same column
+    const bool rotate = is_k && offs[s] != 0;
+    u32x4 y = x;
+    double cl[NA], sl[NA];
+    if constexpr (STYLE == CM_ROPE_HALF) {
+      const u32x4 p = lane_xor4<HB>(x);              // every lane takes part
+      if (rotate) {
+        if (!cs) piece_angles<ESIZE, STYLE>(angles + (int64_t)s * d, cp, ppr, cl, sl);
+        y = rotate_piece_half<ESIZE>(x, p, cs ? cs : cl, cs ? sn : sl);
       }
     } else {
-      for (int64_t r = rsub; r < rows; r += rpi) {
-        const int64_t off = r * row_bytes + q * 16;
-        u32x4 ya, yb;
-        body(ld_stream(src + off), ld_stream(src + off + half), ya, yb);
-        st_stream(dst + off, ya);
-        st_stream(dst + off + half, yb);
+      if (rotate) {
+        if (!cs) piece_angles<ESIZE, STYLE>(angles + (int64_t)s * d, cp, ppr, cl, sl);
+        y = rotate_piece_il<ESIZE>(x, cs ? cs : cl, cs ? sn : sl);
       }
     }
+    if (valid) st_stream(out + lkh * R + b, y);
+  };
+  const int32_t us = unit_slot[blockIdx.x];
+  const int s0 = us & (kUnitCrosses - 1);
+  if (!(us & kUnitCrosses)) {
+    // one slot for the whole unit: angles once, every piece
+    double cs[NA], sn[NA];
+    if (is_k && offs[s0] != 0) piece_angles<ESIZE, STYLE>(angles + (int64_t)s0 * d, cp, ppr, cs, sn);
+#pragma unroll
+    for (int k = 0; k < kUnitPieces; ++k) piece(k, s0, cs, sn);
   } else {
-    const int CPR = row_bytes >> 4;        // chunks per row
-    const int rpi = kThreads / CPR;
-    const int cq = tid % CPR;
-    const int rsub = tid / CPR;
-    constexpr int PP = E / 2;              // pairs per chunk
-    double c[PP], sn[PP];
+    // the unit crosses a slot boundary: slot per lane and piece
 #pragma unroll
-    for (int p = 0; p < PP; ++p) {
-      c[p] = cs[2 * (cq * PP + p)];
-      sn[p] = cs[2 * (cq * PP + p) + 1];
-    }
-    for (int64_t r = rsub; r < rows; r += rpi) {
-      const int64_t off = r * row_bytes + cq * 16;
-      double x[E], y[E];
-      C::unpack(ld_stream(src + off), x);
-#pragma unroll
-      for (int p = 0; p < PP; ++p) {
-        y[2 * p] = x[2 * p] * c[p] - x[2 * p + 1] * sn[p];
-        y[2 * p + 1] = x[2 * p + 1] * c[p] + x[2 * p] * sn[p];
-      }
-      st_stream(dst + off, C::pack(y));
+    for (int k = 0; k < kUnitPieces; ++k) {
+      const int64_t r = (lb + 1024 * k) >> rb_shift;
+      int s = s0;
+      while (s + 1 < n_u && offs[s + 1] <= r) ++s;
+      piece(k, s, nullptr, nullptr);
     }
   }
 }
 
-// grid (tiles per (l, kv, h), 2*L*H); block (x, y) moves tile x of row block
-// y = (l*2 + kv)*H + h of the output.
-template <int ESIZE, int STYLE>
-__global__ __launch_bounds__(kThreads) void render_kernel(
-    const int64_t* __restrict__ table, int64_t stride, int32_t n, const int64_t* __restrict__ plan,
-    const int64_t* __restrict__ tile_base, int32_t n_unique, const double* __restrict__ angles,
-    int32_t H, int32_t d, int64_t T_out, int32_t tile_rows, uint8_t* __restrict__ out) {
-  const int64_t k = blockIdx.x;
-  const int32_t lkh = blockIdx.y;
-  int lo = 0, hi = n_unique - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (tile_base[mid] <= k) lo = mid; else hi = mid - 1;
+// The lookups of the unit render: unit_slot[x] = slot of the first row of unit
+// x (| kUnitCrosses if a later row of the unit lies in another slot), and
+// src_base[s][lkh] = address that row r of slot s in row block lkh is read from
+// when offset by r * row_bytes: fragment tensor base + (h * T_s - off_s) rows.
+__global__ __launch_bounds__(256) void render_unit_prep_kernel(
+    const int64_t* __restrict__ table, int64_t stride, const int64_t* __restrict__ plan,
+    int32_t n, int32_t H, int32_t n_lkh, int32_t rb_shift, int64_t units, int32_t* unit_slot,
+    int64_t* src_base) {
+  const int n_u = (int)plan[CM_PLAN_NUNIQUE];
+  const int64_t* offs = plan + CM_PLAN_HEADER + n;
+  const int64_t T_out = plan[CM_PLAN_TOUT];
+  const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t nthreads = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t x = tid; x < units; x += nthreads) {
+    const int64_t r0 = (x * kUnitBytes) >> rb_shift;
+    int64_t r1 = ((x + 1) * kUnitBytes - 1) >> rb_shift;
+    r1 = r1 < T_out ? r1 : T_out - 1;
+    int lo = 0, hi = n_u - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (offs[mid] <= r0) lo = mid; else hi = mid - 1;
+    }
+    const bool crosses = lo + 1 < n_u && offs[lo + 1] <= r1;
+    unit_slot[x] = lo | (crosses ? kUnitCrosses : 0);
   }
-  const int s = lo;
-  const int64_t src_i = plan[CM_PLAN_HEADER + s];
-  const int64_t off = plan[CM_PLAN_HEADER + n + s];
-  const int64_t len = plan[CM_PLAN_HEADER + 2 * (int64_t)n + s];
-  const int64_t r0 = (k - tile_base[s]) * tile_rows;
-  const int64_t rows = len - r0 < tile_rows ? len - r0 : tile_rows;
-  if (rows <= 0) return;
-  const int h = lkh % H;
-  const int lk = lkh / H;
-  const int kv = lk & 1;
-  const int l = lk >> 1;
-  const int64_t row_bytes = (int64_t)d * ESIZE;
-  const uint8_t* src = reinterpret_cast<const uint8_t*>(table[src_i * stride + 1 + 2 * l + kv]) +
-                       ((int64_t)h * len + r0) * row_bytes;
-  uint8_t* dst = out + ((int64_t)lkh * T_out + off + r0) * row_bytes;
-  if (kv == 1 || off == 0)
-    copy_tile(src, dst, rows * row_bytes);
-  else
-    rotate_tile<ESIZE, STYLE>(src, dst, rows, d, angles + (int64_t)s * d);
+  for (int64_t e = tid; e < (int64_t)n_u * n_lkh; e += nthreads) {
+    const int s = (int)(e / n_lkh);
+    const int lkh = (int)(e - (int64_t)s * n_lkh);
+    const int64_t i = plan[CM_PLAN_HEADER + s];
+    const int64_t T = plan[CM_PLAN_HEADER + 2 * (int64_t)n + s];
+    const int64_t base = table[i * stride + 1 + lkh / H];
+    src_base[e] = base + (((int64_t)(lkh % H) * T - offs[s]) << rb_shift);
+  }
 }
 
-// One workgroup: per-slot work-unit bases (exclusive scan of the units of each
-// slot: ceil(len / tile_rows) tiles, or 2L * stripes for the fused hash+render)
-// and cos/sin(off_s * theta_j), theta_j = base^(-2j/d), in fp64. With a select
-// mask it also writes hsel[i] = 0 for the slot deliveries whose Id the fused
-// kernel computes (select[i] == 0), 1 for every other delivery.
+// One workgroup: per-slot cos/sin(off_s * theta_j), theta_j = base^(-2j/d), in
+// fp64, in the piece-ordered layout of rotate.h. With stripe_blocks > 0 also the
+// per-slot work-unit bases of the fused hash+render (2L * stripes of that many
+// 64-byte blocks per slot, exclusive scan) and, with a select mask, hsel[i] = 0
+// for the slot deliveries whose Id the fused kernel computes (select[i] == 0),
+// 1 for every other delivery.
 __global__ __launch_bounds__(1024) void render_prep_kernel(
-    const int64_t* __restrict__ plan, int32_t n, int32_t d, double base, int32_t tile_rows,
-    int32_t stripe_mode, int64_t tensor_pairs, int64_t token_bytes,
+    const int64_t* __restrict__ plan, int32_t n, int32_t d, int32_t ep, int32_t style,
+    double base, int32_t stripe_blocks, int64_t tensor_pairs, int64_t token_bytes,
     const uint8_t* __restrict__ select, uint8_t* __restrict__ hsel,
     int64_t* __restrict__ unit_base, double* __restrict__ angles) {
   __shared__ int64_t sc[1024];
   const int tid = threadIdx.x;
   const int n_u = (int)plan[CM_PLAN_NUNIQUE];
-  const int64_t len = tid < n_u ? plan[CM_PLAN_HEADER + 2 * (int64_t)n + tid] : 0;
-  int64_t x = 0;
-  if (tid < n_u)
-    x = stripe_mode ? 2 * tensor_pairs * stripes_of(len * token_bytes)
-                    : (len + tile_rows - 1) / tile_rows;
-  sc[tid] = x;
-  if (hsel && tid < n) hsel[tid] = 1;
-  __syncthreads();
-  for (int o = 1; o < (int)blockDim.x; o <<= 1) {
-    const int64_t t = tid >= o ? sc[tid - o] : 0;
+  if (stripe_blocks > 0) {
+    const int64_t len = tid < n_u ? plan[CM_PLAN_HEADER + 2 * (int64_t)n + tid] : 0;
+    int64_t x = 0;
+    if (tid < n_u)
+      x = 2 * tensor_pairs * ((((len * token_bytes) >> 6) + stripe_blocks - 1) / stripe_blocks);
+    sc[tid] = x;
+    if (hsel && tid < n) hsel[tid] = 1;
     __syncthreads();
-    sc[tid] += t;
-    __syncthreads();
-  }
-  if (tid < n_u) unit_base[tid] = sc[tid] - x;
-  if (tid == (int)blockDim.x - 1) unit_base[n_u] = sc[tid];
-  if (hsel && tid < n_u) {
-    const int64_t i = plan[CM_PLAN_HEADER + tid];
-    if (select[i] == 0) hsel[i] = 0;
+    for (int o = 1; o < (int)blockDim.x; o <<= 1) {
+      const int64_t t = tid >= o ? sc[tid - o] : 0;
+      __syncthreads();
+      sc[tid] += t;
+      __syncthreads();
+    }
+    if (tid < n_u) unit_base[tid] = sc[tid] - x;
+    if (tid == (int)blockDim.x - 1) unit_base[n_u] = sc[tid];
+    if (hsel && tid < n_u) {
+      const int64_t i = plan[CM_PLAN_HEADER + tid];
+      if (select[i] == 0) hsel[i] = 0;
+    }
   }
   const int halfd = d >> 1;
+  const int ppr = d / ep;                    // pieces per row
   for (int idx = tid; idx < n_u * halfd; idx += blockDim.x) {
     const int s = idx / halfd;
     const int j = idx - s * halfd;
     const double theta = pow(base, -(double)(2 * j) / (double)d);
     const double phi = (double)plan[CM_PLAN_HEADER + n + s] * theta;
-    angles[2 * idx] = cos(phi);
-    angles[2 * idx + 1] = sin(phi);
+    const int k = style == CM_ROPE_HALF ? angle_slot_half(j / ep, j % ep, ppr >> 1)
+                                        : angle_slot_il(j / (ep >> 1), j % (ep >> 1), ppr);
+    angles[2 * ((int64_t)s * halfd + k)] = cos(phi);
+    angles[2 * ((int64_t)s * halfd + k) + 1] = sin(phi);
   }
-}
-
-template <int ESIZE>
-hipError_t launch_render_t(const SetDesc& s, const RenderLayout& lay, const int64_t* plan,
-                           int32_t n_unique, int64_t total_tiles, int64_t T_out, int32_t style,
-                           void* out, uint8_t* ws, hipStream_t stream) {
-  const int64_t* tiles = reinterpret_cast<const int64_t*>(ws + lay.off_tiles);
-  const double* angles = reinterpret_cast<const double*>(ws + lay.off_angles);
-  const dim3 grid((uint32_t)total_tiles, (uint32_t)(2 * s.L * s.H));
-  ScopedTiming tm(K_RENDER, stream);
-  if (style == CM_ROPE_HALF)
-    hipLaunchKernelGGL((render_kernel<ESIZE, CM_ROPE_HALF>), grid, dim3(kThreads), 0, stream,
-                       s.table_dev, s.stride, s.n, plan, tiles, n_unique, angles, s.H, s.d, T_out,
-                       lay.tile_rows, reinterpret_cast<uint8_t*>(out));
-  else
-    hipLaunchKernelGGL((render_kernel<ESIZE, CM_ROPE_INTERLEAVED>), grid, dim3(kThreads), 0,
-                       stream, s.table_dev, s.stride, s.n, plan, tiles, n_unique, angles, s.H, s.d,
-                       T_out, lay.tile_rows, reinterpret_cast<uint8_t*>(out));
-  return hipGetLastError();
 }
 
 }  // namespace
 
+int64_t render_units(const SetDesc& s, int64_t T_out) {
+  return (T_out * s.row_bytes + kUnitBytes - 1) / kUnitBytes;
+}
+
 RenderLayout render_layout(const SetDesc& s) {
+  int64_t T_all = 0;                      // T_out never exceeds the sum over all deliveries
+  for (int i = 0; i < s.n; ++i) T_all += s.T(i);
   RenderLayout lay{};
-  lay.tile_rows = (int32_t)(kTileBytes / s.row_bytes);
   lay.off_tiles = 0;
   lay.off_angles = align_up(sizeof(int64_t) * (size_t)(s.n + 1), kWsAlign);
   lay.off_hsel = align_up(lay.off_angles + sizeof(double) * (size_t)s.n * (size_t)s.d, kWsAlign);
-  lay.bytes = align_up(lay.off_hsel + (size_t)s.n, kWsAlign);
+  lay.off_src_base = align_up(lay.off_hsel + (size_t)s.n, kWsAlign);
+  lay.off_unit_slot = align_up(lay.off_src_base + sizeof(int64_t) * (size_t)s.n * 2 * s.L * s.H,
+                               kWsAlign);
+  lay.bytes = align_up(lay.off_unit_slot + sizeof(int32_t) * (size_t)render_units(s, T_all),
+                       kWsAlign);
   return lay;
 }
 
 hipError_t launch_render_prep(const SetDesc& s, const RenderLayout& lay, const int64_t* plan_dev,
-                              int32_t n_unique, double base, bool stripe_tasks,
+                              int32_t n_unique, double base, int32_t style, int32_t stripe_blocks,
                               const uint8_t* select, uint8_t* ws, hipStream_t stream) {
   ScopedTiming tm(K_RENDER_PREP, stream);
   int threads = 64;
   const int need = n_unique > s.n ? n_unique : s.n;
   while (threads < need) threads <<= 1;
   hipLaunchKernelGGL(render_prep_kernel, dim3(1), dim3(threads), 0, stream, plan_dev, s.n, s.d,
-                     base, lay.tile_rows, stripe_tasks ? 1 : 0, (int64_t)s.L, token_bytes_of(s),
+                     16 / s.esize, style, base, stripe_blocks, (int64_t)s.L, token_bytes_of(s),
                      select, select ? ws + lay.off_hsel : nullptr,
                      reinterpret_cast<int64_t*>(ws + lay.off_tiles),
                      reinterpret_cast<double*>(ws + lay.off_angles));
@@ -292,13 +210,39 @@ hipError_t launch_render_prep(const SetDesc& s, const RenderLayout& lay, const i
 }
 
 hipError_t launch_render(const SetDesc& s, const RenderLayout& lay, const int64_t* plan_dev,
-                         int32_t n_unique, int64_t total_tiles, int64_t T_out, double base,
-                         int32_t style, void* out, uint8_t* ws, hipStream_t stream) {
-  hipError_t e = launch_render_prep(s, lay, plan_dev, n_unique, base, false, nullptr, ws, stream);
+                         int32_t n_unique, int64_t T_out, double base, int32_t style, void* out,
+                         uint8_t* ws, hipStream_t stream) {
+  hipError_t e = launch_render_prep(s, lay, plan_dev, n_unique, base, style, 0, nullptr, ws, stream);
   if (e != hipSuccess) return e;
-  if (s.esize == 2)
-    return launch_render_t<2>(s, lay, plan_dev, n_unique, total_tiles, T_out, style, out, ws, stream);
-  return launch_render_t<4>(s, lay, plan_dev, n_unique, total_tiles, T_out, style, out, ws, stream);
+  const int64_t units = render_units(s, T_out);
+  const int32_t n_lkh = 2 * s.L * s.H;
+  const int rb_shift = __builtin_ctzll((unsigned long long)s.row_bytes);
+  int32_t* unit_slot = reinterpret_cast<int32_t*>(ws + lay.off_unit_slot);
+  int64_t* src_base = reinterpret_cast<int64_t*>(ws + lay.off_src_base);
+  {
+    ScopedTiming tm(K_RENDER_PREP, stream);
+    const int64_t work = units > (int64_t)n_unique * n_lkh ? units : (int64_t)n_unique * n_lkh;
+    const int64_t blocks = (work + 255) / 256;
+    hipLaunchKernelGGL(render_unit_prep_kernel, dim3((uint32_t)(blocks < 1024 ? blocks : 1024)),
+                       dim3(256), 0, stream, s.table_dev, s.stride, plan_dev, s.n, s.H, n_lkh,
+                       rb_shift, units, unit_slot, src_base);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  const double* angles = reinterpret_cast<const double*>(ws + lay.off_angles);
+  const dim3 grid((uint32_t)units, (uint32_t)n_lkh);
+  uint8_t* o = reinterpret_cast<uint8_t*>(out);
+  ScopedTiming tm(K_RENDER, stream);
+  auto go = [&](auto tag) {
+    constexpr int STYLE = decltype(tag)::style, HB = decltype(tag)::hb;
+    if (s.esize == 2)
+      hipLaunchKernelGGL((render_unit_kernel<2, STYLE, HB>), grid, dim3(64), 0, stream, unit_slot,
+                         src_base, plan_dev, s.n, n_unique, angles, s.H, s.d, T_out, o);
+    else
+      hipLaunchKernelGGL((render_unit_kernel<4, STYLE, HB>), grid, dim3(64), 0, stream, unit_slot,
+                         src_base, plan_dev, s.n, n_unique, angles, s.H, s.d, T_out, o);
+  };
+  dispatch_style(style, s.row_bytes, go);
+  return hipGetLastError();
 }
 
 }  // namespace cm

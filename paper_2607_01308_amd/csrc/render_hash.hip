@@ -23,8 +23,7 @@
 #include <type_traits>
 
 #include "blake2s.h"
-#include "internal.h"
-#include "stream_ops.h"
+#include "rotate.h"
 
 namespace cm {
 
@@ -43,176 +42,31 @@ constexpr int kWaves = kThreads / 64;
 #endif
 #define CM_FUSED_OCCUPANCY __attribute__((amdgpu_waves_per_eu(CM_FUSED_WAVES_PER_EU)))
 
-template <int S, int B>
-struct Tag {
-  static constexpr int style = S, hb = B;
-};
-
-__device__ __forceinline__ u32x4 ld16(const uint8_t* p) {
-  return __builtin_nontemporal_load(global_ptr<u32x4>(p));
-}
-
-// Element e of a 16-byte piece as fp64.
-template <int ESIZE>
-__device__ __forceinline__ double piece_elem(const u32x4 v, int e) {
-  if constexpr (ESIZE == 2) {
-    const uint32_t x = v[e >> 1];
-    return (double)__uint_as_float((e & 1) ? (x & 0xFFFF0000u) : (x << 16));
-  } else {
-    return (double)__uint_as_float(v[e]);
-  }
-}
-
-template <int ESIZE>
-__device__ __forceinline__ void piece_put(u32x4& y, int e, uint32_t bits) {
-  if constexpr (ESIZE == 2) {
-    if (e & 1) y[e >> 1] |= bits << 16;
-    else y[e >> 1] = bits;
-  } else {
-    y[e] = bits;
-  }
-}
-
-// Round EP fp64 values into a 16-byte piece. bf16: fp32 rounding first is exact
-// unless an fp32 result sits on a bf16 midpoint (see bf16_bits_rne); that rare
-// case is tested once for the whole piece and settled element by element.
-template <int ESIZE>
-__device__ __forceinline__ u32x4 round_piece(const double (&y)[16 / ESIZE]) {
-  constexpr int EP = 16 / ESIZE;
-  u32x4 out;
-  if constexpr (ESIZE == 2) {
-    float f[EP];
-    bool mid = false;
-#pragma unroll
-    for (int e = 0; e < EP; ++e) {
-      f[e] = (float)y[e];
-      mid |= (__float_as_uint(f[e]) & 0xFFFFu) == 0x8000u;
-    }
-    if (__builtin_expect(mid, 0)) {
-#pragma unroll
-      for (int e = 0; e < EP; ++e) {
-        uint32_t u = __float_as_uint(f[e]);
-        if ((u & 0xFFFFu) == 0x8000u) {
-          const double back = (double)f[e];
-          if (y[e] != back) u = (fabs(y[e]) > fabs(back)) ? u + 1u : u - 1u;
-        }
-        f[e] = __uint_as_float(u);
-      }
-    }
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const uint32_t lo = __builtin_bit_cast(uint16_t, (__bf16)f[2 * k]);
-      const uint32_t hi = __builtin_bit_cast(uint16_t, (__bf16)f[2 * k + 1]);
-      out[k] = lo | (hi << 16);
-    }
-  } else {
-#pragma unroll
-    for (int e = 0; e < EP; ++e) out[e] = __float_as_uint((float)y[e]);
-  }
-  return out;
-}
-
-// Rotate one 16-byte piece whose pairs are (x, partner p) with the lane's fixed
-// angles: y = x c - p s', where s' = s in the first half of the row and -s in
-// the second (x c - p (-s) = x c + p s, bit for bit).
-template <int ESIZE>
-__device__ __forceinline__ u32x4 rotate_piece_half(const u32x4 x, const u32x4 p, const double* cs,
-                                                   const double* sn) {
-#pragma clang fp contract(off)
-  constexpr int EP = 16 / ESIZE;
-  double y[EP];
-#pragma unroll
-  for (int e = 0; e < EP; ++e)
-    y[e] = piece_elem<ESIZE>(x, e) * cs[e] - piece_elem<ESIZE>(p, e) * sn[e];
-  return round_piece<ESIZE>(y);
-}
-
-// Interleaved pairs (2j, 2j+1) inside the piece.
-template <int ESIZE>
-__device__ __forceinline__ u32x4 rotate_piece_il(const u32x4 x, const double* cs,
-                                                 const double* sn) {
-#pragma clang fp contract(off)
-  constexpr int EP = 16 / ESIZE;
-  double y[EP];
-#pragma unroll
-  for (int q = 0; q < EP / 2; ++q) {
-    const double x1 = piece_elem<ESIZE>(x, 2 * q), x2 = piece_elem<ESIZE>(x, 2 * q + 1);
-    y[2 * q] = x1 * cs[q] - x2 * sn[q];
-    y[2 * q + 1] = x2 * cs[q] + x1 * sn[q];
-  }
-  return round_piece<ESIZE>(y);
-}
-
-// Word of the lane HB away (lane ^ HB) in the wave, without LDS traffic where
-// the hardware allows: HB = 1 and 2 are quad permutations, HB = 8 a DPP rotate by 8
-// within each 16-lane row, HB = 4 and 16 a ds_swizzle xor inside 32 lanes, and
-// HB = 32 a ds_bpermute.
-template <int HB>
-__device__ __forceinline__ uint32_t lane_xor(uint32_t v) {
-  if constexpr (HB == 1) return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0xB1, 0xF, 0xF, false);
-  else if constexpr (HB == 2) return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x4E, 0xF, 0xF, false);
-  else if constexpr (HB == 8) return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x128, 0xF, 0xF, false);
-  else if constexpr (HB == 4 || HB == 16) return (uint32_t)__builtin_amdgcn_ds_swizzle((int)v, (HB << 10) | 0x1F);
-  else return (uint32_t)__shfl_xor((int)v, HB, 64);
-}
-
 // Short final step: lane owns block c of its row as 4 pieces with consecutive
-// columns; ang = the slot's (cos, sin) table in global memory. A row holds
-// HB / 2 blocks (half-split pairs: the partner block c ^ (HB / 4) sits HB / 4
-// lanes away). Reached by every lane of the wave (cross-lane exchange).
+// columns c*4 .. c*4+3 of a row of ppr pieces; ang = the slot's (cos, sin)
+// table. Half-split: a row holds HB / 2 blocks and the partner block sits HB / 4
+// lanes away (HB = 2: the row is this one block, pieces 0-1 pair with 2-3).
+// Reached by every lane of the wave (cross-lane exchange).
 template <int ESIZE, int STYLE, int HB>
-__device__ __forceinline__ void rotate_block_tail(u32x4 (&x)[4], int c,
+__device__ __forceinline__ void rotate_block_tail(u32x4 (&x)[4], int c, int ppr,
                                                   const double* __restrict__ ang) {
-#pragma clang fp contract(off)
   constexpr int EP = 16 / ESIZE;
-  if constexpr (STYLE == CM_ROPE_INTERLEAVED) {
+  constexpr int NA = STYLE == CM_ROPE_HALF ? EP : EP / 2;
+  u32x4 y[4];
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const int j0 = (c * 4 + k) * (EP / 2);
-      double cs[EP / 2], sn[EP / 2];
-#pragma unroll
-      for (int q = 0; q < EP / 2; ++q) {
-        cs[q] = ang[2 * (j0 + q)];
-        sn[q] = ang[2 * (j0 + q) + 1];
-      }
-      x[k] = rotate_piece_il<ESIZE>(x[k], cs, sn);
-    }
-  } else if constexpr (HB == 2) {
-    // the whole row is this block: pieces 0-1 pair with pieces 2-3
-    u32x4 y[4];
-#pragma unroll
-    for (int k = 0; k < 2; ++k) {
-      double cs[EP], sn[EP], nsn[EP];
-#pragma unroll
-      for (int e = 0; e < EP; ++e) {
-        cs[e] = ang[2 * (k * EP + e)];
-        sn[e] = ang[2 * (k * EP + e) + 1];
-        nsn[e] = -sn[e];
-      }
-      y[k] = rotate_piece_half<ESIZE>(x[k], x[k + 2], cs, sn);
-      y[k + 2] = rotate_piece_half<ESIZE>(x[k + 2], x[k], cs, nsn);
-    }
-#pragma unroll
-    for (int k = 0; k < 4; ++k) x[k] = y[k];
-  } else {
-    constexpr int hb = HB / 4;
-    const bool second = c >= hb;
-    const int cb = second ? c - hb : c;
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      u32x4 p;
-#pragma unroll
-      for (int w = 0; w < 4; ++w) p[w] = lane_xor<hb>(x[k][w]);
-      const int j0 = (cb * 4 + k) * EP;
-      double cs[EP], sn[EP];
-#pragma unroll
-      for (int e = 0; e < EP; ++e) {
-        cs[e] = ang[2 * (j0 + e)];
-        sn[e] = second ? -ang[2 * (j0 + e) + 1] : ang[2 * (j0 + e) + 1];
-      }
-      x[k] = rotate_piece_half<ESIZE>(x[k], p, cs, sn);
+  for (int k = 0; k < 4; ++k) {
+    double cs[NA], sn[NA];
+    piece_angles<ESIZE, STYLE>(ang, c * 4 + k, ppr, cs, sn);
+    if constexpr (STYLE == CM_ROPE_INTERLEAVED) {
+      y[k] = rotate_piece_il<ESIZE>(x[k], cs, sn);
+    } else if constexpr (HB == 2) {
+      y[k] = rotate_piece_half<ESIZE>(x[k], x[k ^ 2], cs, sn);
+    } else {
+      y[k] = rotate_piece_half<ESIZE>(x[k], lane_xor4<HB / 4>(x[k]), cs, sn);
     }
   }
+#pragma unroll
+  for (int k = 0; k < 4; ++k) x[k] = y[k];
 }
 
 __device__ __forceinline__ void compress_pieces(B2sState& st, const u32x4 (&x)[4], uint64_t count,
@@ -260,7 +114,6 @@ __global__ __launch_bounds__(kThreads) CM_FUSED_OCCUPANCY void render_hash_kerne
   const int ppr = (int)(row_bytes >> 4);           // 16-byte pieces per row: 4 .. 64
   const int rps = 4096 >> rb_shift;                // rows per full step
   const int cp = lane & (ppr - 1);                 // column piece of this lane (full steps)
-  const bool second = STYLE == CM_ROPE_HALF && cp >= (ppr >> 1);
   const int64_t waves = (int64_t)gridDim.x * kWaves;
   for (int64_t task = (int64_t)blockIdx.x * kWaves + wave; task < total_tasks; task += waves) {
     int lo = 0, hi = n_u - 1;
@@ -281,14 +134,7 @@ __global__ __launch_bounds__(kThreads) CM_FUSED_OCCUPANCY void render_hash_kerne
     const bool rotate = (t & 1) == 0 && off != 0;
     const double* ang = angles + (int64_t)s * d;
     double cs[NA], sn[NA];
-    if (rotate) {
-      const int j0 = STYLE == CM_ROPE_HALF ? (second ? cp - (ppr >> 1) : cp) * EP : cp * (EP / 2);
-#pragma unroll
-      for (int e = 0; e < NA; ++e) {
-        cs[e] = ang[2 * (j0 + e)];
-        sn[e] = second ? -ang[2 * (j0 + e) + 1] : ang[2 * (j0 + e) + 1];
-      }
-    }
+    if (rotate) piece_angles<ESIZE, STYLE>(ang, cp, ppr, cs, sn);
     const int64_t in_stripe = (bytes >> 6) - sidx * kStripeBlocks;
     const int bh = (int)(in_stripe < kStripeBlocks ? in_stripe : kStripeBlocks);
     const int full_steps = bh / kStripeLeaves;
@@ -326,14 +172,10 @@ __global__ __launch_bounds__(kThreads) CM_FUSED_OCCUPANCY void render_hash_kerne
       for (int k = 0; k < 4; ++k) {
         y[k] = x[k];
         if (rotate) {
-          if constexpr (STYLE == CM_ROPE_HALF) {
-            u32x4 p;
-#pragma unroll
-            for (int w = 0; w < 4; ++w) p[w] = lane_xor<HB>(x[k][w]);
-            y[k] = rotate_piece_half<ESIZE>(x[k], p, cs, sn);
-          } else {
+          if constexpr (STYLE == CM_ROPE_HALF)
+            y[k] = rotate_piece_half<ESIZE>(x[k], lane_xor4<HB>(x[k]), cs, sn);
+          else
             y[k] = rotate_piece_il<ESIZE>(x[k], cs, sn);
-          }
         }
       }
       if constexpr (!decltype(wraps)::value) {
@@ -394,7 +236,7 @@ __global__ __launch_bounds__(kThreads) CM_FUSED_OCCUPANCY void render_hash_kerne
         if (hashing) compress_pieces(st, x, (uint64_t)nb << 6, true, leaf == m - 1);
       }
       const int cb = (int)(((lane * 64) & (row_bytes - 1)) >> 6);   // block of the row
-      if (rotate) rotate_block_tail<ESIZE, STYLE, HB>(x, cb, ang);
+      if (rotate) rotate_block_tail<ESIZE, STYLE, HB>(x, cb, ppr, ang);
       if (lane < rem) {
         uint8_t* dp = dest_wrapped(out_t, hh, tt, lane * 64, rb_shift, T, T_out, off);
 #pragma unroll
@@ -409,44 +251,14 @@ __global__ __launch_bounds__(kThreads) CM_FUSED_OCCUPANCY void render_hash_kerne
   }
 }
 
-template <int ESIZE, int STYLE, int HB>
-void launch_fused(dim3 grid, hipStream_t stream, const SetDesc& s, const int64_t* plan_dev,
-                  const int64_t* tasks, int32_t n_unique, int64_t total_tasks,
-                  const double* angles, int64_t T_out, const uint8_t* hsel,
-                  const int64_t* base_tab, uint8_t* nodes, uint8_t* o) {
-  hipLaunchKernelGGL((render_hash_kernel<ESIZE, STYLE, HB>), grid, dim3(kThreads), 0, stream,
-                     s.table_dev, s.stride, s.n, plan_dev, tasks, n_unique, total_tasks, angles,
-                     s.H, s.d, T_out, hsel, base_tab, nodes, o);
-}
-
-template <int ESIZE>
-void launch_fused_es(int32_t style, dim3 grid, hipStream_t stream, const SetDesc& s,
-                     const int64_t* plan_dev, const int64_t* tasks, int32_t n_unique,
-                     int64_t total_tasks, const double* angles, int64_t T_out,
-                     const uint8_t* hsel, const int64_t* base_tab, uint8_t* nodes, uint8_t* o) {
-  auto go = [&](auto kernel_tag) {
-    constexpr int STYLE = decltype(kernel_tag)::style, HB = decltype(kernel_tag)::hb;
-    launch_fused<ESIZE, STYLE, HB>(grid, stream, s, plan_dev, tasks, n_unique, total_tasks,
-                                   angles, T_out, hsel, base_tab, nodes, o);
-  };
-  if (style == CM_ROPE_INTERLEAVED) return go(Tag<CM_ROPE_INTERLEAVED, 0>{});
-  switch ((int)(s.d * s.esize / 32)) {   // pieces per row / 2
-    case 2: return go(Tag<CM_ROPE_HALF, 2>{});
-    case 4: return go(Tag<CM_ROPE_HALF, 4>{});
-    case 8: return go(Tag<CM_ROPE_HALF, 8>{});
-    case 16: return go(Tag<CM_ROPE_HALF, 16>{});
-    default: return go(Tag<CM_ROPE_HALF, 32>{});
-  }
-}
-
 }  // namespace
 
-int64_t render_hash_tasks(const SetDesc& s, const int64_t* plan_host) {
+int64_t stripe_tasks(const SetDesc& s, const int64_t* plan_host, int32_t stripe_blocks) {
   const int64_t nu = plan_host[CM_PLAN_NUNIQUE];
   int64_t tasks = 0;
   for (int64_t k = 0; k < nu; ++k) {
-    const int64_t len = plan_host[CM_PLAN_HEADER + 2 * (int64_t)s.n + k];
-    tasks += 2 * (int64_t)s.L * stripes_of(len * token_bytes_of(s));
+    const int64_t blocks = (plan_host[CM_PLAN_HEADER + 2 * (int64_t)s.n + k] * token_bytes_of(s)) >> 6;
+    tasks += 2 * (int64_t)s.L * ((blocks + stripe_blocks - 1) / stripe_blocks);
   }
   return tasks;
 }
@@ -459,8 +271,8 @@ hipError_t launch_render_hash(const SetDesc& s, const HashLayout& hlay, const Re
   uint8_t* rws = ws + align_up(hlay.bytes, kWsAlign);
   hipError_t e = launch_hash_prep(s, hlay, hws, stream);
   if (e != hipSuccess) return e;
-  if ((e = launch_render_prep(s, rlay, plan_dev, n_unique, base, /*stripe_tasks=*/true, select,
-                              rws, stream)) != hipSuccess)
+  if ((e = launch_render_prep(s, rlay, plan_dev, n_unique, base, style, (int32_t)kStripeBlocks,
+                              select, rws, stream)) != hipSuccess)
     return e;
   const uint8_t* hsel = rws + rlay.off_hsel;  // 0: slot delivery whose Id is computed here
   {
@@ -473,12 +285,18 @@ hipError_t launch_render_hash(const SetDesc& s, const HashLayout& hlay, const Re
     ScopedTiming tm(K_RENDER_HASH, stream);
     uint8_t* nodes = hws + hlay.off_buf0;
     uint8_t* o = reinterpret_cast<uint8_t*>(out);
-    if (s.esize == 2)
-      launch_fused_es<2>(style, grid, stream, s, plan_dev, tasks, n_unique, total_tasks, angles,
-                         T_out, hsel, base_tab, nodes, o);
-    else
-      launch_fused_es<4>(style, grid, stream, s, plan_dev, tasks, n_unique, total_tasks, angles,
-                         T_out, hsel, base_tab, nodes, o);
+    auto go = [&](auto tag) {
+      constexpr int STYLE = decltype(tag)::style, HB = decltype(tag)::hb;
+      if (s.esize == 2)
+        hipLaunchKernelGGL((render_hash_kernel<2, STYLE, HB>), grid, dim3(kThreads), 0, stream,
+                           s.table_dev, s.stride, s.n, plan_dev, tasks, n_unique, total_tasks,
+                           angles, s.H, s.d, T_out, hsel, base_tab, nodes, o);
+      else
+        hipLaunchKernelGGL((render_hash_kernel<4, STYLE, HB>), grid, dim3(kThreads), 0, stream,
+                           s.table_dev, s.stride, s.n, plan_dev, tasks, n_unique, total_tasks,
+                           angles, s.H, s.d, T_out, hsel, base_tab, nodes, o);
+    };
+    dispatch_style(style, s.row_bytes, go);
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   return launch_hash_tree(s, hlay, hsel, 0, digests, hws, stream);

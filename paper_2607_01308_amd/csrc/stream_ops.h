@@ -1,14 +1,10 @@
 // Device helpers shared by the render kernels: 16-byte nontemporal global
-// loads/stores and the single-step fp64 -> bf16 rounding.
+// stores and the single-step fp64 -> bf16 rounding.
 #pragma once
 
 #include "internal.h"
 
 namespace cm {
-
-__device__ __forceinline__ u32x4 ld_stream(const uint8_t* p) {
-  return __builtin_nontemporal_load(global_ptr<u32x4>(p));
-}
 
 __device__ __forceinline__ void st_stream(uint8_t* p, u32x4 v) {
   __builtin_nontemporal_store(v, (CM_GLOBAL u32x4*)p);
