@@ -1,17 +1,24 @@
 """Benchmark: the CanonicalMerge render of a LatentFragmentSet on one MI355X.
 
-One step = the whole path over one batch of deliveries: Id of every delivery
-(hash), scores, dedupe + canonical order + offsets, one small device-to-host
-plan copy, output allocation, rotate-and-concatenate render. Inputs are
-resident in HBM before timing starts.
+One step = the whole path over one batch of deliveries (steps 1-5): scores,
+the Id of every delivery whose score and length collide with another's, dedupe
++ canonical order + offsets, one small device-to-host plan copy, output
+allocation, then the fused kernel that renders the merged cache and computes
+the remaining Ids from the same loads. Inputs are resident in HBM before timing
+starts.
 
 value = merged-cache bytes read + written per step (2 x the bytes of the
 distinct fragments) / step time, in GB/s; merges_per_s = 1 / step time.
+`render_set` is the same render over the already-ingested set (steps 2-5, Ids
+computed at ingest), the path whose bytes are all HBM streaming.
 
 Prints one JSON line. `roofline` is for the kernel with the largest share of
-the step (per-kernel HIP events on the launch stream, measured over the timed
-steps); `roofline_render` adds the render kernel against HBM bandwidth.
-`cpu_baseline` times the CPU oracle on a bounded sample of the same workload.
+the step, measured with per-kernel HIP events on the launch stream over the
+timed steps: the fused hash+render kernel against the VALU issue rate (its
+algorithmic operations: 960 per hashed 64-byte block, 5 per rotated K
+element). `roofline_render` gives the render kernel of `render_set` against
+HBM bandwidth. `cpu_baseline` times the CPU oracle on a bounded sample of the
+same workload.
 """
 
 from __future__ import annotations
@@ -28,34 +35,56 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0                 # MI355X HBM3E
-VALU_PEAK_TOPS = 256 * 64 * 2.4e9 / 1e12  # 256 CUs x 64 lanes x 2.4 GHz, non-packed 32-bit ops
+VALU_PEAK_TOPS = 256 * 64 * 2.4e9 / 1e12  # 256 CUs x 64 lanes x 2.4 GHz: one 32-bit or fp64 op
 B2S_OPS_PER_BLOCK = 960                # 10 rounds x 8 G x 12 VALU ops (add3, add, xor, alignbit)
+ROT_OPS_PER_ELEM = 5                   # widen, 2 fp64 products, 1 fp64 add/sub, narrow
+
+# source files each timed kernel is built from: a traffic summary is only used
+# while these are unchanged
+KERNEL_SOURCES = {
+    "render_hash": ["render_hash.hip", "rotate.h", "blake2s.h", "stream_ops.h", "internal.h"],
+    "render": ["render.hip", "rotate.h", "stream_ops.h", "internal.h"],
+}
 
 
-def _kernel_source_hash(name: str) -> str:
-    path = os.path.join(ROOT, "paper_2607_01308_amd", "csrc", name)
-    with open(path, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+def kernel_source_hash(kernel: str) -> str:
+    h = hashlib.sha256()
+    for name in KERNEL_SOURCES[kernel]:
+        with open(os.path.join(ROOT, "paper_2607_01308_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
-def _traffic(kernel: str, source: str, workload: str):
+def _traffic(kernel: str, workload: str):
     """HBM bytes per launch from a committed rocprofv3 counter summary, if it was
-    taken on the current kernel source; otherwise None."""
+    taken on the current kernel sources; otherwise None."""
     path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_traffic.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
         t = json.load(f)
-    if t.get("source_sha256_16") != _kernel_source_hash(source):
+    if t.get("source_sha256_16") != kernel_source_hash(kernel):
         return None
     return t.get("hbm_bytes_per_launch")
 
 
+def fused_work(w, r, mask):
+    """Algorithmic work of one fused launch: VALU ops (hash of every slot whose
+    Id it computes, rotation of every K element at a non-zero offset) and the
+    bytes it must move."""
+    tok = w.L * w.H * w.d                       # elements per token per tensor kind
+    esize = 2 if w.dtype == "bfloat16" else 4
+    hashed_blocks = sum(2 * tok * T * esize // 64 for i, T in zip(r.order, r.lengths)
+                        if int(mask[i]) == 0)
+    rotated = sum(tok * T for off, T in zip(r.offsets, r.lengths) if off != 0)
+    return B2S_OPS_PER_BLOCK * hashed_blocks + ROT_OPS_PER_ELEM * rotated, hashed_blocks * 64, rotated
+
+
 def cpu_baseline(w, frags):
-    """The oracle, unchanged, over the three shortest distinct fragments."""
+    """The oracle, unchanged, over the five shortest distinct fragments."""
     import oracle
     import synth
-    idx = sorted(range(w.n_distinct), key=lambda i: w.lengths[i])[:3]
+    idx = sorted(range(w.n_distinct), key=lambda i: w.lengths[i])[:5]
     sample = [oracle.Fragment(*synth.to_numpy_cache(frags[i])) for i in idx]
     t0 = time.perf_counter()
     oracle.render_deliveries(sample, w.routing_layer, w.rope_base)
@@ -66,7 +95,7 @@ def cpu_baseline(w, frags):
         "unit": "GB/s",
         "cores": 1,
         "kind": "oracle",
-        "sample": f"full path (hash, score, order, render) over the 3 shortest distinct fragments "
+        "sample": f"full path (hash, score, order, render) over the 5 shortest distinct fragments "
                   f"(T={[w.lengths[i] for i in idx]}, {nbytes / 1e9:.2f} GB read+write), "
                   f"{dt:.1f} s, single-threaded numpy/hashlib",
     }
@@ -144,37 +173,57 @@ def main():
     for _ in range(2):
         S.render(w.routing_layer, w.rope_base)
     torch.cuda.synchronize()
+    cm.timing_reset()
+    cm.timing_enable(True)
     t2 = time.perf_counter()
     for _ in range(args.steps):
         r = S.render(w.routing_layer, w.rope_base)
         del r
     torch.cuda.synchronize()
     t3 = time.perf_counter()
+    cm.timing_enable(False)
+    set_kernels = {}
+    for k in cm.KERNELS:
+        ms, n = cm.timing_query(k)
+        if n:
+            set_kernels[k] = {"total_ms": ms, "launches": n}
+    cm.timing_reset()
 
     ms_step = (t1 - t0) / args.steps * 1e3
     ms_render_set = (t3 - t2) / args.steps * 1e3
     render_bytes = w.render_bytes
     value = render_bytes / (ms_step / 1e3) / 1e9
 
-    # dominant kernel and its roofline
-    dom = max(per_kernel, key=lambda k: per_kernel[k]["total_ms"] / args.steps)
+    # dominant kernel of the step and its roofline
+    dom = max(per_kernel, key=lambda k: per_kernel[k]["total_ms"])
     delivered = w.delivery_bytes
-    hash_blocks = delivered // 64
     rooflines = {}
-    if "hash_leaf" in per_kernel:
-        avg = per_kernel["hash_leaf"]["total_ms"] / args.steps / 1e3
-        ach = B2S_OPS_PER_BLOCK * hash_blocks / avg / 1e12
-        rooflines["hash_leaf"] = {"bound": "alu", "achieved": round(ach, 3),
-                                  "peak": round(VALU_PEAK_TOPS, 3), "unit": "Tops/s",
-                                  "frac": round(ach / VALU_PEAK_TOPS, 4),
-                                  "traffic": _traffic("hash_leaf", "hash.hip", w.name),
-                                  "input_GBps": round(delivered / avg / 1e9, 1)}
-    if "render" in per_kernel:
-        avg = per_kernel["render"]["total_ms"] / args.steps / 1e3
+    if "render_hash" in per_kernel:
+        r = step()
+        keys = torch.empty(batch.n, dtype=torch.float64, device=dev)
+        mask = torch.empty(batch.n, dtype=torch.uint8, device=dev)
+        ws = torch.empty(cm.workspace_size(batch), dtype=torch.uint8, device=dev)
+        cm.fragment_knorm(batch, w.routing_layer, r.tail_len, keys, ws)
+        cm.equal_key_mask(batch, keys, mask)
+        ops, hashed_bytes, rotated = fused_work(w, r, mask.cpu().numpy())
+        del r, ws
+        pk = per_kernel["render_hash"]
+        avg = pk["total_ms"] / pk["launches"] / 1e3
+        ach = ops / avg / 1e12
+        rooflines["render_hash"] = {
+            "bound": "alu", "achieved": round(ach, 3), "peak": round(VALU_PEAK_TOPS, 3),
+            "unit": "Tops/s", "frac": round(ach / VALU_PEAK_TOPS, 4),
+            "traffic": _traffic("render_hash", w.name),
+            "ops_per_launch": ops, "hashed_bytes": hashed_bytes, "rotated_elements": rotated,
+            "avg_ms": round(avg * 1e3, 4), "hbm_GBps": round(render_bytes / avg / 1e9, 1)}
+    if "render" in set_kernels:
+        pk = set_kernels["render"]
+        avg = pk["total_ms"] / pk["launches"] / 1e3
         ach = render_bytes / avg / 1e9
         rooflines["render"] = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBPS,
                                "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBPS, 4),
-                               "traffic": _traffic("render", "render.hip", w.name)}
+                               "traffic": _traffic("render", w.name),
+                               "bytes_per_launch": render_bytes, "avg_ms": round(avg * 1e3, 4)}
     out = {
         "metric": "merged-cache render GB/s (read+write) and % of MI355X HBM peak; merges/s",
         "value": round(value, 2),
@@ -198,8 +247,13 @@ def main():
         "roofline": dict(rooflines.get(dom, {}), kernel=dom) if dom in rooflines else None,
         "roofline_render": rooflines.get("render"),
         "kernels_ms_per_step": {k: round(v["total_ms"] / args.steps, 4) for k, v in per_kernel.items()},
-        "render_set_ms": round(ms_render_set, 4),
-        "render_set_GBps": round(render_bytes / (ms_render_set / 1e3) / 1e9, 1),
+        "render_set": {"ms": round(ms_render_set, 4),
+                       "GBps": round(render_bytes / (ms_render_set / 1e3) / 1e9, 1),
+                       "pct_hbm_peak": round(100 * render_bytes / (ms_render_set / 1e3) / 1e9
+                                             / HBM_PEAK_GBPS, 2),
+                       "merges_per_s": round(1e3 / ms_render_set, 3),
+                       "kernels_ms": {k: round(v["total_ms"] / args.steps, 4)
+                                      for k, v in set_kernels.items()}},
     }
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
