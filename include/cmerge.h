@@ -3,14 +3,18 @@
  * on AMD Instinct MI355X (gfx950).
  *
  * Paper: "Cache Merging as a Convergent Replicated State for Multi-Agent Latent
- * Reasoning" (arXiv 2607.01308). The four calls below are the steps of Alg. 1
+ * Reasoning" (arXiv 2607.01308). The calls below are the steps of Alg. 1
  * (CanonicalMerge) run inside Render of Alg. 2 (LatentFragmentSet):
- *   cm_fragment_hash    Id of Alg. 2 / the hash tiebreak h_i of §4.3
- *   cm_fragment_knorm   the mean K-norm score rho_i of Eq. (3)
- *   cm_canonical_order  Ingest dedupe (Eq. (5)) + argsort(-rho, -h) of Alg. 1
- *                       + the offsets s of §4.2
- *   cm_render_merge     Eq. (1)-(2): K of slot i rotated by R(s_i), V copied,
- *                       both concatenated along the sequence axis
+ *   cm_fragment_hash        Id of Alg. 2 / the hash tiebreak h_i of §4.3
+ *   cm_fragment_knorm       the mean K-norm score rho_i of Eq. (3)
+ *   cm_canonical_order      Ingest dedupe (Eq. (5)) + argsort(-rho, -h) of Alg. 1
+ *                           + the offsets s of §4.2
+ *   cm_render_merge         Eq. (1)-(2): K of slot i rotated by R(s_i), V copied,
+ *                           both concatenated along the sequence axis
+ * and, to run step 1 without a second read of the fragments:
+ *   cm_equal_key_mask       the deliveries whose digest the order needs
+ *   cm_fragment_hash_select the Id of a subset of the deliveries
+ *   cm_render_merge_hash    the render plus the remaining Ids from its loads
  *
  * Conventions
  *   - Every function returns int32_t: CM_OK (0) or a negative cm_status. No
