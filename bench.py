@@ -1,7 +1,7 @@
 """Benchmark: the CanonicalMerge render of a LatentFragmentSet on one MI355X.
 
 One step = the whole path over one batch of deliveries (steps 1-5): scores,
-the Id of every delivery whose score and length collide with another's, dedupe
+the Id of every delivery whose score collides with another's, dedupe
 + canonical order + offsets, one small device-to-host plan copy, output
 allocation, then the fused kernel that renders the merged cache and computes
 the remaining Ids from the same loads. Inputs are resident in HBM before timing

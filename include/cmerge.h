@@ -11,6 +11,9 @@
  *                           + the offsets s of §4.2
  *   cm_render_merge         Eq. (1)-(2): K of slot i rotated by R(s_i), V copied,
  *                           both concatenated along the sequence axis
+ * the paper's baselines over the same render:
+ *   cm_multiset_order       the naive re-render order of §5.9 (no dedupe)
+ *   cm_bag_plan             BagMerge with a caller-supplied order (§4.2)
  * and, to run step 1 without a second read of the fragments:
  *   cm_equal_key_mask       the deliveries whose digest the order needs
  *   cm_fragment_hash_select the Id of a subset of the deliveries
@@ -92,7 +95,8 @@ typedef struct {
 
 /* ---------------------------------------------------------------- plan layout
  * A plan is an int64 array of cm_plan_elems(n) entries, written on the device by
- * cm_canonical_order and read by cm_render_merge:
+ * cm_canonical_order (or cm_multiset_order; on the host by cm_bag_plan) and read
+ * by cm_render_merge:
  *   [0]                 status: CM_OK, or CM_ENONFINITE if a score is not finite
  *   [1]                 n (deliveries)
  *   [2]                 n_unique: distinct fragments = slots of the merged cache
@@ -166,9 +170,9 @@ int32_t cm_fragment_knorm(const cm_fragset* set, int32_t routing_layer, int64_t 
 
 /* ---------------------------------------------------------------- step 3
  * Which digests the order needs (for running the rest of step 1 concurrently
- * with steps 4-5): mask_dev[i] = 1 if another fragment has a bitwise-equal key
- * and the same T, else 0. Byte-identical copies always share key and T, and
- * ties need equal keys, so cm_canonical_order reads exactly these digests.
+ * with steps 4-5): mask_dev[i] = 1 if another fragment has a bitwise-equal key,
+ * else 0. Byte-identical copies always share their key, and ties need equal
+ * keys, so cm_canonical_order and cm_multiset_order read exactly these digests.
  * keys_dev: output of cm_fragment_knorm (device); mask_dev: device, n bytes. */
 int32_t cm_equal_key_mask(const cm_fragset* set, const double* keys_dev, uint8_t* mask_dev,
                           void* stream);
@@ -185,6 +189,22 @@ int32_t cm_equal_key_mask(const cm_fragset* set, const double* keys_dev, uint8_t
 int32_t cm_canonical_order(const cm_fragset* set, const double* keys_dev,
                            const uint8_t* digests_dev, int64_t* plan_dev, void* stream);
 
+/* The naive re-render of §5.9 (Table 10's foil): the order of
+ * cm_canonical_order over every delivery, without Ingest's dedupe. Each
+ * delivery gets a slot; byte-identical copies tie on key and digest and keep
+ * their delivery order. Same arguments and plan layout as cm_canonical_order
+ * (n_unique = n, slot_of_delivery[i] = the slot of delivery i). */
+int32_t cm_multiset_order(const cm_fragset* set, const double* keys_dev,
+                          const uint8_t* digests_dev, int64_t* plan_dev, void* stream);
+/* BagMerge of Eq. (1)-(2) with a caller-supplied order pi (the paper's fixed
+ * orders, e.g. default and swap, §4.2): slot k renders delivery order_host[k]
+ * at the offset of the lengths before it; no dedupe, no scores. Host only: writes
+ * the cm_plan_elems(n) int64 plan to plan_host (the caller copies it to the
+ * device for cm_render_merge). order_host: host, count indices in [0, n), each
+ * one delivery (a delivery may appear more than once); 1 <= count <= n.
+ * slot_of_delivery[i] is the first slot rendering delivery i, or -1. */
+int32_t cm_bag_plan(const cm_fragset* set, const int32_t* order_host, int32_t count,
+                    int64_t* plan_host);
 /* ---------------------------------------------------------------- steps 4-5
  * Eq. (1)-(2) with pi = the plan's slot order: for every layer l and head h,
  *   out K rows [s, s + T) = R(s) K_slot  (rotation in fp64, rounded to nearest

@@ -6,11 +6,13 @@ from ._cabi import CmError, LIB_PATH  # noqa: F401
 from .binding import (  # noqa: F401
     KERNELS,
     FragmentBatch,
+    bag_plan,
     canonical_order,
     equal_key_mask,
     fragment_hash,
     fragment_hash_select,
     fragment_knorm,
+    multiset_order,
     plan_elems,
     render_merge,
     render_merge_hash,
@@ -23,7 +25,9 @@ from .fragset import (  # noqa: F401
     LatentFragmentSet,
     PIPELINES,
     RenderResult,
+    bag_merge,
     fragment_ids,
     release_workspace,
     render_deliveries,
+    render_multiset,
 )

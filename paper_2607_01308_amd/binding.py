@@ -122,6 +122,23 @@ def canonical_order(batch: FragmentBatch, keys: torch.Tensor, digests: torch.Ten
             "cm_canonical_order")
 
 
+def multiset_order(batch: FragmentBatch, keys: torch.Tensor, digests: torch.Tensor,
+                   plan: torch.Tensor, stream=None) -> None:
+    C.check(C.lib().cm_multiset_order(ctypes.byref(batch.struct), _ptr(keys), _ptr(digests),
+                                      _ptr(plan), _stream(stream, batch.device)),
+            "cm_multiset_order")
+
+
+def bag_plan(batch: FragmentBatch, order) -> np.ndarray:
+    """Host plan of BagMerge with the given order (delivery indices per slot)."""
+    order = np.ascontiguousarray(np.asarray(order, dtype=np.int32))
+    plan = np.empty(plan_elems(batch.n), dtype=np.int64)
+    C.check(C.lib().cm_bag_plan(ctypes.byref(batch.struct),
+                                order.ctypes.data_as(ctypes.c_void_p), int(order.size),
+                                plan.ctypes.data_as(ctypes.c_void_p)), "cm_bag_plan")
+    return plan
+
+
 def render_merge(batch: FragmentBatch, plan_dev: torch.Tensor, plan_host: np.ndarray,
                  rope_base: float, style: str, out: torch.Tensor, T_out: int,
                  workspace: torch.Tensor, stream=None) -> None:

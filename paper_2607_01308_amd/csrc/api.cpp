@@ -297,8 +297,55 @@ int32_t cm_canonical_order(const cm_fragset* set, const double* keys_dev,
   if (!digests_dev || !aligned(digests_dev, 4))
     return fail(CM_EINVAL, "digests_dev is NULL or misaligned");
   if (!plan_dev || !aligned(plan_dev, 8)) return fail(CM_EINVAL, "plan_dev is NULL or misaligned");
-  hipError_t e = cm::launch_order(s, keys_dev, digests_dev, plan_dev, static_cast<hipStream_t>(stream));
+  hipError_t e =
+      cm::launch_order(s, keys_dev, digests_dev, true, plan_dev, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? CM_OK : fail_hip(e, "cm_canonical_order");
+}
+
+int32_t cm_multiset_order(const cm_fragset* set, const double* keys_dev,
+                          const uint8_t* digests_dev, int64_t* plan_dev, void* stream) {
+  g_err.clear();
+  cm::SetDesc s;
+  int32_t st = check_set(set, &s);
+  if (st != CM_OK) return st;
+  if (!keys_dev || !aligned(keys_dev, 8)) return fail(CM_EINVAL, "keys_dev is NULL or misaligned");
+  if (!digests_dev || !aligned(digests_dev, 4))
+    return fail(CM_EINVAL, "digests_dev is NULL or misaligned");
+  if (!plan_dev || !aligned(plan_dev, 8)) return fail(CM_EINVAL, "plan_dev is NULL or misaligned");
+  hipError_t e =
+      cm::launch_order(s, keys_dev, digests_dev, false, plan_dev, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? CM_OK : fail_hip(e, "cm_multiset_order");
+}
+
+int32_t cm_bag_plan(const cm_fragset* set, const int32_t* order_host, int32_t count,
+                    int64_t* plan_host) {
+  g_err.clear();
+  cm::SetDesc s;
+  int32_t st = check_set(set, &s);
+  if (st != CM_OK) return st;
+  if (!order_host || !plan_host) return fail(CM_EINVAL, "order_host / plan_host is NULL");
+  if (count < 1 || count > s.n)
+    return fail(CM_EINVAL, "count must be in [1, n] = [1, " + std::to_string(s.n) + "], got " +
+                               std::to_string(count));
+  const int64_t n = s.n;
+  for (int64_t k = 0; k < 4 + 4 * n; ++k) plan_host[k] = -1;
+  int64_t off = 0;
+  for (int32_t k = 0; k < count; ++k) {
+    const int32_t i = order_host[k];
+    if (i < 0 || i >= s.n)
+      return fail(CM_EINVAL, "order entry " + std::to_string(k) + " = " + std::to_string(i) +
+                                 " is not a delivery index");
+    plan_host[CM_PLAN_HEADER + k] = i;
+    plan_host[CM_PLAN_HEADER + n + k] = off;
+    plan_host[CM_PLAN_HEADER + 2 * n + k] = s.T(i);
+    if (plan_host[CM_PLAN_HEADER + 3 * n + i] < 0) plan_host[CM_PLAN_HEADER + 3 * n + i] = k;
+    off += s.T(i);
+  }
+  plan_host[CM_PLAN_STATUS] = CM_OK;
+  plan_host[CM_PLAN_N] = n;
+  plan_host[CM_PLAN_NUNIQUE] = count;
+  plan_host[CM_PLAN_TOUT] = off;
+  return CM_OK;
 }
 
 }  // extern "C"

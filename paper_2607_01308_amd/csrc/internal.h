@@ -113,8 +113,9 @@ hipError_t launch_equal_key_mask(const SetDesc& s, const double* keys, uint8_t* 
                                  hipStream_t stream);
 hipError_t launch_knorm(const SetDesc& s, const KnormLayout& lay, int32_t layer, int64_t tail_len,
                         double* keys, uint8_t* ws, hipStream_t stream);
+// dedupe = false: every delivery gets a slot (naive multiset order).
 hipError_t launch_order(const SetDesc& s, const double* keys, const uint8_t* digests,
-                        int64_t* plan, hipStream_t stream);
+                        bool dedupe, int64_t* plan, hipStream_t stream);
 // Per-slot angle tables; with stripe_blocks > 0 also the per-slot task bases of
 // 2L * stripes of that many 64-byte blocks (and hsel when select is given).
 hipError_t launch_render_prep(const SetDesc& s, const RenderLayout& lay, const int64_t* plan_dev,

@@ -1,20 +1,23 @@
 // Step 3 — Ingest dedupe (Alg. 2, Eq. (5)) and canonical order (Alg. 1):
 // pi* = argsort(-S, -h) over the distinct fragments, offsets by exclusive prefix
-// sum of the lengths in that order (§4.2).
+// sum of the lengths in that order (§4.2). Without dedupe the same order over
+// every delivery is the naive re-render of §5.9: byte-identical copies tie on
+// key and digest and keep their delivery order.
 //
 // n <= 1024 deliveries fit one workgroup (one lane per delivery), so the order
 // is built by exact counting, with no sort network and no host round trip: a
 // delivery is absorbed if an earlier one has the same digest; the slot of a
-// distinct fragment is the number of distinct fragments that precede it (larger
-// key, or equal key and larger big-endian digest). Keys are compared as IEEE
-// doubles and only bitwise-equal keys tie. Everything is integer or comparison
-// work, so the plan is exact and independent of thread timing.
+// kept delivery is the number of kept deliveries that precede it (larger key,
+// or equal key and larger big-endian digest, or equal both and earlier).
+// Keys are compared as IEEE doubles and only bitwise-equal keys tie.
+// Everything is integer or comparison work, so the plan is exact and
+// independent of thread timing.
 //
-// Byte-identical deliveries have bitwise-equal keys and equal lengths (the key
-// is a deterministic function of the bytes), and ties need equal keys, so the
-// digest of a delivery is read only when another delivery has the same key
-// and length. That lets the digests of every other delivery be computed
-// concurrently with the render (equal_key_mask marks the ones needed first).
+// Byte-identical deliveries have bitwise-equal keys (the key is a
+// deterministic function of the bytes), and ties need equal keys, so the
+// digest of a delivery is read only when another delivery has the same key.
+// That lets the digests of every other delivery be computed concurrently with
+// the render (equal_key_mask marks the ones needed first).
 #include "internal.h"
 
 namespace cm {
@@ -45,7 +48,7 @@ __global__ __launch_bounds__(1024) void order_kernel(const int64_t* __restrict__
                                                      int64_t stride, int32_t n,
                                                      const double* __restrict__ keys,
                                                      const uint8_t* __restrict__ digests,
-                                                     int64_t* __restrict__ plan) {
+                                                     int32_t dedupe, int64_t* __restrict__ plan) {
   __shared__ double s_key[1024];
   __shared__ int64_t s_len[1024];     // by delivery, then by slot
   __shared__ int32_t s_first[1024];   // first delivery with the same digest
@@ -69,8 +72,7 @@ __global__ __launch_bounds__(1024) void order_kernel(const int64_t* __restrict__
   const int bad = __syncthreads_or(live && !isfinite(key));
   if (live) {
     bool shared = false;
-    for (int j = 0; j < n; ++j)
-      shared |= (j != tid && s_key[j] == key && s_len[j] == len);
+    for (int j = 0; j < n; ++j) shared |= (j != tid && s_key[j] == key);
     if (shared) load_digest_be(digests, tid, mine);
   }
 
@@ -78,7 +80,7 @@ __global__ __launch_bounds__(1024) void order_kernel(const int64_t* __restrict__
   // length and digest).
   int first = tid;
   if (live) {
-    for (int j = 0; j < tid; ++j) {
+    for (int j = 0; dedupe && j < tid; ++j) {
       if (s_key[j] != key || s_len[j] != len) continue;
       uint32_t other[8];
       load_digest_be(digests, j, other);
@@ -90,7 +92,7 @@ __global__ __launch_bounds__(1024) void order_kernel(const int64_t* __restrict__
   const bool distinct = live && first == tid;
   const int n_unique = __syncthreads_count(distinct);
 
-  // Slot = number of distinct fragments ordered before this one.
+  // Slot = number of kept deliveries ordered before this one.
   if (distinct) {
     int rank = 0;
     for (int j = 0; j < n; ++j) {
@@ -100,7 +102,8 @@ __global__ __launch_bounds__(1024) void order_kernel(const int64_t* __restrict__
       if (!before && kj == key) {
         uint32_t other[8];
         load_digest_be(digests, j, other);
-        before = cmp_digest(other, mine) > 0;
+        const int c = cmp_digest(other, mine);
+        before = c > 0 || (c == 0 && j < tid);   // equal content (no dedupe): delivery order
       }
       rank += before ? 1 : 0;
     }
@@ -138,28 +141,23 @@ __global__ __launch_bounds__(1024) void order_kernel(const int64_t* __restrict__
   }
 }
 
-// mask[i] = 1 if another delivery has a bitwise-equal key and the same length
-// (only those digests decide dedupe and ties), else 0.
+// mask[i] = 1 if another delivery has a bitwise-equal key (only those digests
+// decide dedupe and ties), else 0.
 __global__ __launch_bounds__(1024) void equal_key_mask_kernel(const int64_t* __restrict__ table,
                                                               int64_t stride, int32_t n,
                                                               const double* __restrict__ keys,
                                                               uint8_t* __restrict__ mask) {
   __shared__ double s_key[1024];
-  __shared__ int64_t s_len[1024];
   const int tid = threadIdx.x;
   double key = 0.0;
-  int64_t len = 0;
   if (tid < n) {
     key = keys[tid];
-    len = table[(int64_t)tid * stride];
     s_key[tid] = key;
-    s_len[tid] = len;
   }
   __syncthreads();
   if (tid < n) {
     bool shared = false;
-    for (int j = 0; j < n; ++j)
-      shared |= (j != tid && s_key[j] == key && s_len[j] == len);
+    for (int j = 0; j < n; ++j) shared |= (j != tid && s_key[j] == key);
     mask[tid] = shared ? 1 : 0;
   }
 }
@@ -177,12 +175,12 @@ hipError_t launch_equal_key_mask(const SetDesc& s, const double* keys, uint8_t* 
 }
 
 hipError_t launch_order(const SetDesc& s, const double* keys, const uint8_t* digests,
-                        int64_t* plan, hipStream_t stream) {
+                        bool dedupe, int64_t* plan, hipStream_t stream) {
   int threads = 64;
   while (threads < s.n) threads <<= 1;
   ScopedTiming tm(K_ORDER, stream);
   hipLaunchKernelGGL(order_kernel, dim3(1), dim3(threads), 0, stream, s.table_dev, s.stride,
-                     s.n, keys, digests, plan);
+                     s.n, keys, digests, dedupe ? 1 : 0, plan);
   return hipGetLastError();
 }
 

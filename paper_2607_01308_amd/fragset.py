@@ -1,7 +1,7 @@
 """LatentFragmentSet (Alg. 2) and the render path on one GPU.
 
 render_deliveries runs the whole path over a list of deliveries: scores
-(cm_fragment_knorm), the Id of every delivery whose score and length collide
+(cm_fragment_knorm), the Id of every delivery whose score collides
 with another's (cm_equal_key_mask + cm_fragment_hash_select: only those decide
 dedupe and ties), dedupe + canonical order + offsets (cm_canonical_order), one
 device-to-host copy of the small plan so the caller can size the output, then
@@ -21,9 +21,9 @@ import numpy as np
 import torch
 
 from . import _cabi as C
-from .binding import (FragmentBatch, canonical_order, equal_key_mask, fragment_hash,
-                      fragment_hash_select, fragment_knorm, plan_elems, render_merge,
-                      render_merge_hash, workspace_size)
+from .binding import (FragmentBatch, bag_plan, canonical_order, equal_key_mask, fragment_hash,
+                      fragment_hash_select, fragment_knorm, multiset_order, plan_elems,
+                      render_merge, render_merge_hash, workspace_size)
 
 _WS: Dict[tuple, torch.Tensor] = {}
 _SIDE: Dict[torch.device, torch.cuda.Stream] = {}
@@ -166,6 +166,52 @@ def render_deliveries(deliveries: Union[FragmentBatch, Sequence], routing_layer:
                 main.wait_event(side_done)
     return RenderResult(cache=cache, merged=merged, digests_dev=digests, keys_dev=keys,
                         plan=plan_host, tail_len=tail)
+
+
+def render_multiset(deliveries: Union[FragmentBatch, Sequence], routing_layer: int,
+                    rope_base: float, style: str = "half", stream=None) -> RenderResult:
+    """The naive re-render of §5.9: every delivery is its own operand (no
+    Ingest dedupe), in canonical order; copies sit next to each other, so R
+    deliveries of each fragment give a cache R times as long (Table 10's
+    foil). Digests as in render_deliveries (fused into the render)."""
+    batch = deliveries if isinstance(deliveries, FragmentBatch) else FragmentBatch(deliveries)
+    dev = batch.device
+    main = stream if stream is not None else torch.cuda.current_stream(dev)
+    with torch.cuda.stream(main):
+        ws = _workspace(batch, 0)
+        digests = torch.empty((batch.n, 32), dtype=torch.uint8, device=dev)
+        keys = torch.empty(batch.n, dtype=torch.float64, device=dev)
+        mask = torch.empty(batch.n, dtype=torch.uint8, device=dev)
+        plan_dev = torch.empty(plan_elems(batch.n), dtype=torch.int64, device=dev)
+        tail = min(batch.lengths)
+        fragment_knorm(batch, routing_layer, tail, keys, ws, main)
+        equal_key_mask(batch, keys, mask, main)
+        fragment_hash_select(batch, mask, 1, digests, ws, main)   # the digests the order reads
+        multiset_order(batch, keys, digests, plan_dev, main)
+        plan_host = plan_dev.to("cpu").numpy()
+        merged, cache = _render_plan(batch, plan_dev, plan_host, rope_base, style, ws, main,
+                                     hash_select=mask, digests=digests)
+    return RenderResult(cache=cache, merged=merged, digests_dev=digests, keys_dev=keys,
+                        plan=plan_host, tail_len=tail)
+
+
+def bag_merge(deliveries: Union[FragmentBatch, Sequence], order: Sequence[int],
+              rope_base: float, style: str = "half", stream=None) -> RenderResult:
+    """BagMerge (Eq. (1)-(2)) with a caller-supplied order, e.g. the paper's
+    default (delivery order) and swap baselines: slot k renders delivery
+    order[k]; no scores, no Ids, no dedupe (digests and keys stay empty)."""
+    batch = deliveries if isinstance(deliveries, FragmentBatch) else FragmentBatch(deliveries)
+    dev = batch.device
+    main = stream if stream is not None else torch.cuda.current_stream(dev)
+    plan_host = bag_plan(batch, order)
+    with torch.cuda.stream(main):
+        ws = _workspace(batch, 0)
+        plan_dev = torch.from_numpy(plan_host).to(dev, non_blocking=False)
+        merged, cache = _render_plan(batch, plan_dev, plan_host, rope_base, style, ws, main)
+    empty = torch.empty(0, dtype=torch.uint8, device=dev)
+    return RenderResult(cache=cache, merged=merged, digests_dev=empty,
+                        keys_dev=torch.empty(0, dtype=torch.float64, device=dev),
+                        plan=plan_host, tail_len=0)
 
 
 def fragment_ids(caches: Sequence, stream=None) -> List[bytes]:

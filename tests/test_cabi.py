@@ -175,3 +175,55 @@ def test_render_plan_checks(lib):
     nu0 = good.copy()
     nu0[2] = 0
     assert call(nu0, 14) == C.CM_EINVAL
+
+
+def test_multiset_order_argument_checks(lib):
+    fs = FakeSet()
+    p = ctypes.c_void_p(0x20000)
+    assert lib.cm_multiset_order(fs.ref, None, p, p, None) == C.CM_EINVAL
+    assert lib.cm_multiset_order(fs.ref, p, None, p, None) == C.CM_EINVAL
+    assert lib.cm_multiset_order(fs.ref, p, p, ctypes.c_void_p(0x20004), None) == C.CM_EINVAL
+
+
+def _bag(lib, fs, order):
+    order = np.asarray(order, dtype=np.int32)
+    plan = np.zeros(4 + 4 * fs.s.n, dtype=np.int64)
+    st = lib.cm_bag_plan(fs.ref, order.ctypes.data_as(ctypes.c_void_p), int(order.size),
+                         plan.ctypes.data_as(ctypes.c_void_p))
+    return st, plan
+
+
+def test_bag_plan_layout(lib):
+    """BagMerge plan (§4.2): slot k renders order[k] at the sum of the lengths
+    before it; the plan passes the render's own checks."""
+    fs = FakeSet(lengths=(5, 9, 4))
+    st, plan = _bag(lib, fs, [2, 0, 1])
+    assert st == C.CM_OK
+    assert list(plan[:4]) == [C.CM_OK, 3, 3, 18]
+    assert list(plan[4:7]) == [2, 0, 1]
+    assert list(plan[7:10]) == [0, 4, 9]
+    assert list(plan[10:13]) == [4, 5, 9]
+    assert list(plan[13:16]) == [1, 2, 0]                # slot of each delivery
+    assert np.array_equal(plan[:13], _plan(3, [2, 0, 1], [4, 5, 9])[:13])
+    _, need = _ws(lib, fs)
+    rope = C.CmRope(base=1e4, style=0, reserved=0)
+    st = lib.cm_render_merge(fs.ref, ctypes.c_void_p(0x30000), plan.ctypes.data_as(ctypes.c_void_p),
+                             ctypes.byref(rope), ctypes.c_void_p(0x80000), 18,
+                             ctypes.c_void_p(0x40000), 0, None)
+    assert st == C.CM_EWORKSPACE                         # every plan check passed
+
+
+def test_bag_plan_repeats_and_partial(lib):
+    fs = FakeSet(lengths=(5, 9, 4))
+    st, plan = _bag(lib, fs, [1, 1])                     # a delivery rendered twice
+    assert st == C.CM_OK
+    assert list(plan[:4]) == [C.CM_OK, 3, 2, 18]
+    assert list(plan[4:7]) == [1, 1, -1] and list(plan[7:10]) == [0, 9, -1]
+    assert list(plan[13:16]) == [-1, 0, -1]              # first slot per delivery, -1 if absent
+
+
+@pytest.mark.parametrize("order", [[], [0, 1, 2, 0], [3], [-1]])
+def test_bag_plan_rejects(lib, order):
+    fs = FakeSet(lengths=(5, 9, 4))
+    st, _ = _bag(lib, fs, order)
+    assert st == C.CM_EINVAL
