@@ -11,6 +11,7 @@
  *                           + the offsets s of §4.2
  *   cm_render_merge         Eq. (1)-(2): K of slot i rotated by R(s_i), V copied,
  *                           both concatenated along the sequence axis
+ *   cm_render_merge_devplan the same with the plan left on the device
  * the paper's baselines over the same render:
  *   cm_multiset_order       the naive re-render order of §5.9 (no dedupe)
  *   cm_bag_plan             BagMerge with a caller-supplied order (§4.2)
@@ -223,6 +224,18 @@ int32_t cm_render_merge(const cm_fragset* set, const int64_t* plan_dev,
                         int64_t T_out, void* workspace, size_t workspace_bytes,
                         void* stream);
 
+/* As cm_render_merge for a plan that is only on the device (e.g. just written by
+ * cm_canonical_order on the same stream): nothing waits for the plan. The caller
+ * gives T_out (for a set of distinct fragments, the sum of their lengths;
+ * 1 <= T_out <= the sum of all lengths). Before any byte moves, the device checks
+ * the plan against the set and T_out (status CM_OK, n, n_unique, each slot's
+ * delivery and length, offsets as prefix sums, T_out); a plan that fails is not
+ * rendered (out_dev is left untouched) and CM_ESHAPE is written into its status
+ * entry plan_dev[0], which the caller reads after the stream has finished. The
+ * call itself returns CM_OK for such a plan. */
+int32_t cm_render_merge_devplan(const cm_fragset* set, int64_t* plan_dev, const cm_rope* rope,
+                                void* out_dev, int64_t T_out, void* workspace,
+                                size_t workspace_bytes, void* stream);
 /* Steps 1 and 4-5 in one pass: the render of cm_render_merge and, for every
  * slot delivery i with select_dev[i] == 0, its Id (as cm_fragment_hash) written
  * to digests_dev[i]; the Id's leaf level is computed from the same loads that

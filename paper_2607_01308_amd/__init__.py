@@ -15,6 +15,7 @@ from .binding import (  # noqa: F401
     multiset_order,
     plan_elems,
     render_merge,
+    render_merge_devplan,
     render_merge_hash,
     timing_enable,
     timing_query,

@@ -151,6 +151,17 @@ def render_merge(batch: FragmentBatch, plan_dev: torch.Tensor, plan_host: np.nda
                                     _stream(stream, batch.device)), "cm_render_merge")
 
 
+def render_merge_devplan(batch: FragmentBatch, plan_dev: torch.Tensor, rope_base: float,
+                         style: str, out: torch.Tensor, T_out: int, workspace: torch.Tensor,
+                         stream=None) -> None:
+    rope = C.CmRope(base=float(rope_base), style=_STYLES[style], reserved=0)
+    C.check(C.lib().cm_render_merge_devplan(ctypes.byref(batch.struct), _ptr(plan_dev),
+                                            ctypes.byref(rope), _ptr(out), T_out, _ptr(workspace),
+                                            workspace.numel() * workspace.element_size(),
+                                            _stream(stream, batch.device)),
+            "cm_render_merge_devplan")
+
+
 def render_merge_hash(batch: FragmentBatch, plan_dev: torch.Tensor, plan_host: np.ndarray,
                       rope_base: float, style: str, select: torch.Tensor, digests: torch.Tensor,
                       out: torch.Tensor, T_out: int, workspace: torch.Tensor, stream=None) -> None:

@@ -353,14 +353,20 @@ int32_t cm_bag_plan(const cm_fragset* set, const int32_t* order_host, int32_t co
 namespace {
 
 // Checks shared by the render entry points; returns the slot count.
-int32_t check_render_args(const cm::SetDesc& s, const int64_t* plan_dev, const int64_t* plan_host,
-                          const cm_rope* rope, void* out_dev, int64_t T_out, int64_t* nu_out) {
+int32_t check_rope(const cm_rope* rope) {
   if (!rope) return fail(CM_EINVAL, "rope is NULL");
   if (!std::isfinite(rope->base) || rope->base <= 0.0)
     return fail(CM_EINVAL, "rope base must be finite and > 0");
   if (rope->style != CM_ROPE_HALF && rope->style != CM_ROPE_INTERLEAVED)
     return fail(CM_EINVAL, "rope style must be CM_ROPE_HALF or CM_ROPE_INTERLEAVED");
   if (rope->reserved != 0) return fail(CM_EINVAL, "rope reserved field must be 0");
+  return CM_OK;
+}
+
+int32_t check_render_args(const cm::SetDesc& s, const int64_t* plan_dev, const int64_t* plan_host,
+                          const cm_rope* rope, void* out_dev, int64_t T_out, int64_t* nu_out) {
+  int32_t st = check_rope(rope);
+  if (st != CM_OK) return st;
   if (!plan_dev || !aligned(plan_dev, 8) || !plan_host)
     return fail(CM_EINVAL, "plan_dev / plan_host is NULL or misaligned");
   if (!out_dev || !aligned(out_dev, 16)) return fail(CM_EINVAL, "out_dev is NULL or not 16-byte aligned");
@@ -405,10 +411,34 @@ int32_t cm_render_merge(const cm_fragset* set, const int64_t* plan_dev, const in
     return st;
   const cm::RenderLayout lay = cm::render_layout(s);
   if ((st = check_ws(workspace, workspace_bytes, lay.bytes)) != CM_OK) return st;
-  hipError_t e = cm::launch_render(s, lay, plan_dev, (int32_t)nu, T_out, rope->base, rope->style,
+  hipError_t e = cm::launch_render(s, lay, plan_dev, T_out, rope->base, rope->style, false,
                                    out_dev, static_cast<uint8_t*>(workspace),
                                    static_cast<hipStream_t>(stream));
   return e == hipSuccess ? CM_OK : fail_hip(e, "cm_render_merge");
+}
+
+int32_t cm_render_merge_devplan(const cm_fragset* set, int64_t* plan_dev, const cm_rope* rope,
+                                void* out_dev, int64_t T_out, void* workspace,
+                                size_t workspace_bytes, void* stream) {
+  g_err.clear();
+  cm::SetDesc s;
+  int32_t st = check_set(set, &s);
+  if (st != CM_OK) return st;
+  if ((st = check_rope(rope)) != CM_OK) return st;
+  if (!plan_dev || !aligned(plan_dev, 8)) return fail(CM_EINVAL, "plan_dev is NULL or misaligned");
+  if (!out_dev || !aligned(out_dev, 16)) return fail(CM_EINVAL, "out_dev is NULL or not 16-byte aligned");
+  int64_t T_all = 0;
+  for (int i = 0; i < s.n; ++i) T_all += s.T(i);
+  if (T_out < 1 || T_out > T_all)
+    return fail(CM_ESHAPE, "T_out must be in [1, sum of the fragment lengths]");
+  if (cm::render_units(s, T_out) >= ((int64_t)1 << 31))
+    return fail(CM_ESHAPE, "merged cache too long for one launch");
+  const cm::RenderLayout lay = cm::render_layout(s);
+  if ((st = check_ws(workspace, workspace_bytes, lay.bytes)) != CM_OK) return st;
+  hipError_t e = cm::launch_render(s, lay, plan_dev, T_out, rope->base, rope->style, true,
+                                   out_dev, static_cast<uint8_t*>(workspace),
+                                   static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? CM_OK : fail_hip(e, "cm_render_merge_devplan");
 }
 
 int32_t cm_render_merge_hash(const cm_fragset* set, const int64_t* plan_dev,

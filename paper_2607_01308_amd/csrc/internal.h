@@ -92,6 +92,7 @@ struct RenderLayout {
   size_t off_hsel;        // uint8 [n]: 0 = slot delivery hashed by the fused kernel
   size_t off_src_base;    // int64 [n][2LH]: per slot and row block, the source base of row 0
   size_t off_unit_slot;   // int32 [render units]: slot of each unit of a row block
+  size_t off_flag;        // int32: 1 if the plan passed its device check
   size_t bytes;
 };
 RenderLayout render_layout(const SetDesc& s);
@@ -129,9 +130,12 @@ hipError_t launch_render_hash(const SetDesc& s, const HashLayout& hlay, const Re
                               const int64_t* plan_dev, int32_t n_unique, int64_t total_tasks,
                               int64_t T_out, double base, int32_t style, const uint8_t* select,
                               uint8_t* digests, void* out, uint8_t* ws, hipStream_t stream);
+// check_on_device: the plan was not validated on the host; the prep kernel checks
+// it against the set and T_out and, if it fails, skips the render and writes
+// CM_ESHAPE into the plan's status.
 hipError_t launch_render(const SetDesc& s, const RenderLayout& lay, const int64_t* plan_dev,
-                         int32_t n_unique, int64_t T_out, double base, int32_t style, void* out,
-                         uint8_t* ws, hipStream_t stream);
+                         int64_t T_out, double base, int32_t style, bool check_on_device,
+                         void* out, uint8_t* ws, hipStream_t stream);
 
 // Per-kernel event timing (no-op unless cm_timing_enable(1)).
 class ScopedTiming {

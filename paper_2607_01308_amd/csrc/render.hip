@@ -30,7 +30,7 @@ constexpr int32_t kUnitCrosses = 1 << 16;            // unit_slot flag: slot bou
 template <int ESIZE, int STYLE, int HB>
 __global__ __launch_bounds__(64) void render_unit_kernel(
     const int32_t* __restrict__ unit_slot, const int64_t* __restrict__ src_base,
-    const int64_t* __restrict__ plan, int32_t n, int32_t n_u, const double* __restrict__ angles,
+    const int64_t* __restrict__ plan, int32_t n, const double* __restrict__ angles,
     int32_t H, int32_t d, int64_t T_out, uint8_t* __restrict__ out) {
   constexpr int EP = 16 / ESIZE;
   constexpr int NA = STYLE == CM_ROPE_HALF ? EP : EP / 2;
@@ -70,6 +70,8 @@ __global__ __launch_bounds__(64) void render_unit_kernel(
     if (valid) st_stream(out + lkh * R + b, y);
   };
   const int32_t us = unit_slot[blockIdx.x];
+  if (us < 0) return;                                  // the plan failed its device check
+  const int n_u = (int)plan[CM_PLAN_NUNIQUE];
   const int s0 = us & (kUnitCrosses - 1);
   if (!(us & kUnitCrosses)) {
     // one slot for the whole unit: angles once, every piece
@@ -95,13 +97,17 @@ __global__ __launch_bounds__(64) void render_unit_kernel(
 // when offset by r * row_bytes: fragment tensor base + (h * T_s - off_s) rows.
 __global__ __launch_bounds__(256) void render_unit_prep_kernel(
     const int64_t* __restrict__ table, int64_t stride, const int64_t* __restrict__ plan,
-    int32_t n, int32_t H, int32_t n_lkh, int32_t rb_shift, int64_t units, int32_t* unit_slot,
-    int64_t* src_base) {
+    int32_t n, int32_t H, int32_t n_lkh, int32_t rb_shift, int64_t units,
+    const int32_t* __restrict__ plan_ok, int32_t* unit_slot, int64_t* src_base) {
+  const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t nthreads = (int64_t)gridDim.x * blockDim.x;
+  if (plan_ok && *plan_ok == 0) {                      // rejected plan: every unit is skipped
+    for (int64_t x = tid; x < units; x += nthreads) unit_slot[x] = -1;
+    return;
+  }
   const int n_u = (int)plan[CM_PLAN_NUNIQUE];
   const int64_t* offs = plan + CM_PLAN_HEADER + n;
   const int64_t T_out = plan[CM_PLAN_TOUT];
-  const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t nthreads = (int64_t)gridDim.x * blockDim.x;
   for (int64_t x = tid; x < units; x += nthreads) {
     const int64_t r0 = (x * kUnitBytes) >> rb_shift;
     int64_t r1 = ((x + 1) * kUnitBytes - 1) >> rb_shift;
@@ -134,10 +140,42 @@ __global__ __launch_bounds__(1024) void render_prep_kernel(
     const int64_t* __restrict__ plan, int32_t n, int32_t d, int32_t ep, int32_t style,
     double base, int32_t stripe_blocks, int64_t tensor_pairs, int64_t token_bytes,
     const uint8_t* __restrict__ select, uint8_t* __restrict__ hsel,
-    int64_t* __restrict__ unit_base, double* __restrict__ angles) {
+    int64_t* __restrict__ unit_base, double* __restrict__ angles,
+    const int64_t* __restrict__ table, int64_t stride, int64_t T_out, int32_t* plan_ok,
+    int64_t* plan_status) {
   __shared__ int64_t sc[1024];
   const int tid = threadIdx.x;
-  const int n_u = (int)plan[CM_PLAN_NUNIQUE];
+  int n_u = (int)plan[CM_PLAN_NUNIQUE];
+  if (plan_ok) {
+    // A plan the host has not seen: status, n, n_unique, T_out, every slot's
+    // delivery and length, and the offsets as exclusive prefix sums. The block
+    // holds at least n threads, one per slot.
+    const bool head = plan[CM_PLAN_STATUS] == CM_OK && plan[CM_PLAN_N] == n && n_u >= 1 &&
+                      n_u <= n && plan[CM_PLAN_TOUT] == T_out;
+    bool ok = true;
+    int64_t len = 0;
+    if (head && tid < n_u) {
+      const int64_t src = plan[CM_PLAN_HEADER + tid];
+      len = plan[CM_PLAN_HEADER + 2 * (int64_t)n + tid];
+      ok = src >= 0 && src < n && len >= 1 && len == table[src * stride];
+    }
+    sc[tid] = ok ? len : 0;
+    __syncthreads();
+    for (int o = 1; o < (int)blockDim.x; o <<= 1) {
+      const int64_t t = tid >= o ? sc[tid - o] : 0;
+      __syncthreads();
+      sc[tid] += t;
+      __syncthreads();
+    }
+    if (head && tid < n_u) ok = ok && plan[CM_PLAN_HEADER + n + tid] == sc[tid] - len;
+    const bool all = __syncthreads_and(ok) && head && sc[blockDim.x - 1] == T_out;
+    if (tid == 0) {
+      *plan_ok = all ? 1 : 0;
+      if (!all) *plan_status = CM_ESHAPE;
+    }
+    if (!all) return;
+    __syncthreads();
+  }
   if (stripe_blocks > 0) {
     const int64_t len = tid < n_u ? plan[CM_PLAN_HEADER + 2 * (int64_t)n + tid] : 0;
     int64_t x = 0;
@@ -189,8 +227,9 @@ RenderLayout render_layout(const SetDesc& s) {
   lay.off_src_base = align_up(lay.off_hsel + (size_t)s.n, kWsAlign);
   lay.off_unit_slot = align_up(lay.off_src_base + sizeof(int64_t) * (size_t)s.n * 2 * s.L * s.H,
                                kWsAlign);
-  lay.bytes = align_up(lay.off_unit_slot + sizeof(int32_t) * (size_t)render_units(s, T_all),
-                       kWsAlign);
+  lay.off_flag = align_up(lay.off_unit_slot + sizeof(int32_t) * (size_t)render_units(s, T_all),
+                          kWsAlign);
+  lay.bytes = align_up(lay.off_flag + sizeof(int32_t), kWsAlign);
   return lay;
 }
 
@@ -205,14 +244,26 @@ hipError_t launch_render_prep(const SetDesc& s, const RenderLayout& lay, const i
                      16 / s.esize, style, base, stripe_blocks, (int64_t)s.L, token_bytes_of(s),
                      select, select ? ws + lay.off_hsel : nullptr,
                      reinterpret_cast<int64_t*>(ws + lay.off_tiles),
-                     reinterpret_cast<double*>(ws + lay.off_angles));
+                     reinterpret_cast<double*>(ws + lay.off_angles), s.table_dev, s.stride,
+                     (int64_t)0, nullptr, nullptr);
   return hipGetLastError();
 }
 
 hipError_t launch_render(const SetDesc& s, const RenderLayout& lay, const int64_t* plan_dev,
-                         int32_t n_unique, int64_t T_out, double base, int32_t style, void* out,
-                         uint8_t* ws, hipStream_t stream) {
-  hipError_t e = launch_render_prep(s, lay, plan_dev, n_unique, base, style, 0, nullptr, ws, stream);
+                         int64_t T_out, double base, int32_t style, bool check_on_device,
+                         void* out, uint8_t* ws, hipStream_t stream) {
+  int32_t* plan_ok = check_on_device ? reinterpret_cast<int32_t*>(ws + lay.off_flag) : nullptr;
+  {
+    ScopedTiming tm(K_RENDER_PREP, stream);
+    int threads = 64;
+    while (threads < s.n) threads <<= 1;
+    hipLaunchKernelGGL(render_prep_kernel, dim3(1), dim3(threads), 0, stream, plan_dev, s.n, s.d,
+                       16 / s.esize, style, base, 0, (int64_t)s.L, token_bytes_of(s), nullptr,
+                       nullptr, reinterpret_cast<int64_t*>(ws + lay.off_tiles),
+                       reinterpret_cast<double*>(ws + lay.off_angles), s.table_dev, s.stride,
+                       T_out, plan_ok, const_cast<int64_t*>(plan_dev));
+  }
+  hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int64_t units = render_units(s, T_out);
   const int32_t n_lkh = 2 * s.L * s.H;
@@ -221,11 +272,11 @@ hipError_t launch_render(const SetDesc& s, const RenderLayout& lay, const int64_
   int64_t* src_base = reinterpret_cast<int64_t*>(ws + lay.off_src_base);
   {
     ScopedTiming tm(K_RENDER_PREP, stream);
-    const int64_t work = units > (int64_t)n_unique * n_lkh ? units : (int64_t)n_unique * n_lkh;
+    const int64_t work = units > (int64_t)s.n * n_lkh ? units : (int64_t)s.n * n_lkh;
     const int64_t blocks = (work + 255) / 256;
     hipLaunchKernelGGL(render_unit_prep_kernel, dim3((uint32_t)(blocks < 1024 ? blocks : 1024)),
                        dim3(256), 0, stream, s.table_dev, s.stride, plan_dev, s.n, s.H, n_lkh,
-                       rb_shift, units, unit_slot, src_base);
+                       rb_shift, units, plan_ok, unit_slot, src_base);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   const double* angles = reinterpret_cast<const double*>(ws + lay.off_angles);
@@ -236,10 +287,10 @@ hipError_t launch_render(const SetDesc& s, const RenderLayout& lay, const int64_
     constexpr int STYLE = decltype(tag)::style, HB = decltype(tag)::hb;
     if (s.esize == 2)
       hipLaunchKernelGGL((render_unit_kernel<2, STYLE, HB>), grid, dim3(64), 0, stream, unit_slot,
-                         src_base, plan_dev, s.n, n_unique, angles, s.H, s.d, T_out, o);
+                         src_base, plan_dev, s.n, angles, s.H, s.d, T_out, o);
     else
       hipLaunchKernelGGL((render_unit_kernel<4, STYLE, HB>), grid, dim3(64), 0, stream, unit_slot,
-                         src_base, plan_dev, s.n, n_unique, angles, s.H, s.d, T_out, o);
+                         src_base, plan_dev, s.n, angles, s.H, s.d, T_out, o);
   };
   dispatch_style(style, s.row_bytes, go);
   return hipGetLastError();

@@ -23,7 +23,7 @@ import torch
 from . import _cabi as C
 from .binding import (FragmentBatch, bag_plan, canonical_order, equal_key_mask, fragment_hash,
                       fragment_hash_select, fragment_knorm, multiset_order, plan_elems,
-                      render_merge, render_merge_hash, workspace_size)
+                      render_merge, render_merge_devplan, render_merge_hash, workspace_size)
 
 _WS: Dict[tuple, torch.Tensor] = {}
 _SIDE: Dict[torch.device, torch.cuda.Stream] = {}
@@ -48,8 +48,27 @@ def _side_stream(device: torch.device) -> torch.cuda.Stream:
     return st
 
 
+_PINNED: Dict[tuple, torch.Tensor] = {}
+
+
 def release_workspace() -> None:
     _WS.clear()
+    _PINNED.clear()
+
+
+def _plan_to_host(plan_dev: torch.Tensor, stream) -> np.ndarray:
+    """Host copy of a plan through a cached pinned buffer (an asynchronous copy
+    on the stream, then a wait for that stream only)."""
+    key = (plan_dev.device, plan_dev.numel())
+    buf = _PINNED.get(key)
+    if buf is None:
+        buf = torch.empty(plan_dev.numel(), dtype=torch.int64, pin_memory=True)
+        _PINNED[key] = buf
+    st = stream if stream is not None else torch.cuda.current_stream(plan_dev.device)
+    with torch.cuda.stream(st):
+        buf.copy_(plan_dev, non_blocking=True)
+    st.synchronize()
+    return buf.numpy().copy()
 
 
 @dataclass
@@ -58,8 +77,20 @@ class RenderResult:
     merged: torch.Tensor         # the single [L, 2, 1, H, T_out, d] buffer behind `cache`
     digests_dev: torch.Tensor    # [n, 32] uint8, per delivery
     keys_dev: torch.Tensor       # [n] float64 S_i, per delivery
-    plan: np.ndarray             # host copy of the plan (layout in include/cmerge.h)
+    plan_host: Optional[np.ndarray]   # host copy of the plan (layout in include/cmerge.h)
     tail_len: int
+    plan_dev: Optional[torch.Tensor] = None
+
+    @property
+    def plan(self) -> np.ndarray:
+        """The plan on the host (copied from the device on first use when the
+        render did not need it; a rejected plan raises)."""
+        if self.plan_host is None:
+            self.plan_host = self.plan_dev.to("cpu").numpy()
+            status = int(self.plan_host[C.PLAN_STATUS])
+            if status != C.CM_OK:
+                raise C.CmError(status, "cm_render_merge_devplan", "the plan failed its device check")
+        return self.plan_host
 
     @property
     def n_unique(self) -> int:
@@ -154,7 +185,7 @@ def render_deliveries(deliveries: Union[FragmentBatch, Sequence], routing_layer:
         elif pipeline == "serial":
             fragment_hash_select(batch, mask, 0, digests, ws, main)
         canonical_order(batch, keys, digests, plan_dev, main)
-        plan_host = plan_dev.to("cpu").numpy()
+        plan_host = _plan_to_host(plan_dev, main)
         try:
             if pipeline == "fused":
                 merged, cache = _render_plan(batch, plan_dev, plan_host, rope_base, style, ws, main,
@@ -165,7 +196,7 @@ def render_deliveries(deliveries: Union[FragmentBatch, Sequence], routing_layer:
             if side_done is not None:
                 main.wait_event(side_done)
     return RenderResult(cache=cache, merged=merged, digests_dev=digests, keys_dev=keys,
-                        plan=plan_host, tail_len=tail)
+                        plan_host=plan_host, tail_len=tail, plan_dev=plan_dev)
 
 
 def render_multiset(deliveries: Union[FragmentBatch, Sequence], routing_layer: int,
@@ -188,11 +219,11 @@ def render_multiset(deliveries: Union[FragmentBatch, Sequence], routing_layer: i
         equal_key_mask(batch, keys, mask, main)
         fragment_hash_select(batch, mask, 1, digests, ws, main)   # the digests the order reads
         multiset_order(batch, keys, digests, plan_dev, main)
-        plan_host = plan_dev.to("cpu").numpy()
+        plan_host = _plan_to_host(plan_dev, main)
         merged, cache = _render_plan(batch, plan_dev, plan_host, rope_base, style, ws, main,
                                      hash_select=mask, digests=digests)
     return RenderResult(cache=cache, merged=merged, digests_dev=digests, keys_dev=keys,
-                        plan=plan_host, tail_len=tail)
+                        plan_host=plan_host, tail_len=tail, plan_dev=plan_dev)
 
 
 def bag_merge(deliveries: Union[FragmentBatch, Sequence], order: Sequence[int],
@@ -211,7 +242,7 @@ def bag_merge(deliveries: Union[FragmentBatch, Sequence], order: Sequence[int],
     empty = torch.empty(0, dtype=torch.uint8, device=dev)
     return RenderResult(cache=cache, merged=merged, digests_dev=empty,
                         keys_dev=torch.empty(0, dtype=torch.float64, device=dev),
-                        plan=plan_host, tail_len=0)
+                        plan_host=plan_host, tail_len=0, plan_dev=plan_dev)
 
 
 def fragment_ids(caches: Sequence, stream=None) -> List[bytes]:
@@ -230,6 +261,7 @@ class LatentFragmentSet:
 
     def __init__(self, items: Optional[Dict[bytes, tuple]] = None):
         self._items: Dict[bytes, tuple] = dict(items or {})
+        self._desc = None          # (FragmentBatch, device Id array) of the current members
 
     def ingest(self, cache) -> bytes:
         return self.ingest_many([cache])[0]
@@ -237,8 +269,21 @@ class LatentFragmentSet:
     def ingest_many(self, caches: Sequence) -> List[bytes]:
         ids = fragment_ids(caches)
         for fid, cache in zip(ids, caches):
-            self._items.setdefault(fid, cache)
+            if fid not in self._items:
+                self._items[fid] = cache
+                self._desc = None
         return ids
+
+    def _description(self):
+        """The members as the C ABI sees them: fragment table and their Ids on the
+        device; rebuilt only when the membership changes."""
+        if self._desc is None:
+            ids = list(self._items.keys())
+            batch = FragmentBatch([self._items[k] for k in ids])
+            digests = torch.tensor(np.frombuffer(b"".join(ids), dtype=np.uint8).reshape(-1, 32),
+                                   device=batch.device)
+            self._desc = (batch, digests)
+        return self._desc
 
     def merge(self, other: "LatentFragmentSet") -> "LatentFragmentSet":
         out = dict(self._items)
@@ -256,18 +301,21 @@ class LatentFragmentSet:
                stream=None) -> RenderResult:
         if not self._items:
             raise ValueError("cannot render an empty set")
-        ids = list(self._items.keys())
-        batch = FragmentBatch([self._items[k] for k in ids])
+        batch, digests = self._description()
         dev = batch.device
         ws = _workspace(batch)
-        digests = torch.tensor(np.frombuffer(b"".join(ids), dtype=np.uint8).reshape(-1, 32),
-                               device=dev)
         keys = torch.empty(batch.n, dtype=torch.float64, device=dev)
         plan_dev = torch.empty(plan_elems(batch.n), dtype=torch.int64, device=dev)
         tail = min(batch.lengths)
         fragment_knorm(batch, routing_layer, tail, keys, ws, stream)
         canonical_order(batch, keys, digests, plan_dev, stream)
-        plan_host = plan_dev.to("cpu").numpy()
-        merged, cache = _render_plan(batch, plan_dev, plan_host, rope_base, style, ws, stream)
+        # the members are distinct, so T_out is the sum of their lengths and the
+        # plan can stay on the device (checked there before the render)
+        T_out = int(sum(batch.lengths))
+        merged = torch.empty((batch.L, 2, 1, batch.H, T_out, batch.d), dtype=batch.torch_dtype,
+                             device=dev)
+        render_merge_devplan(batch, plan_dev, rope_base, style, merged, T_out, ws, stream)
+        cache = tuple((merged[l, 0], merged[l, 1]) for l in range(batch.L))
+        plan_host = None
         return RenderResult(cache=cache, merged=merged, digests_dev=digests, keys_dev=keys,
-                            plan=plan_host, tail_len=tail)
+                            plan_host=plan_host, tail_len=tail, plan_dev=plan_dev)

@@ -227,3 +227,22 @@ def test_bag_plan_rejects(lib, order):
     fs = FakeSet(lengths=(5, 9, 4))
     st, _ = _bag(lib, fs, order)
     assert st == C.CM_EINVAL
+
+
+def test_render_devplan_argument_checks(lib):
+    fs = FakeSet(lengths=(5, 9))
+    _, need = _ws(lib, fs)
+    rope = C.CmRope(base=1e4, style=0, reserved=0)
+    plan, out, ws = ctypes.c_void_p(0x30000), ctypes.c_void_p(0x80000), ctypes.c_void_p(0x40000)
+
+    def call(T_out, plan=plan, out=out, rope=rope, ws_bytes=need):
+        return lib.cm_render_merge_devplan(fs.ref, plan, ctypes.byref(rope), out, T_out, ws,
+                                           ws_bytes, None)
+
+    assert call(14, ws_bytes=0) == C.CM_EWORKSPACE          # every other check passed
+    assert call(15) == C.CM_ESHAPE                          # longer than all fragments together
+    assert call(0) == C.CM_ESHAPE
+    assert call(14, plan=None) == C.CM_EINVAL
+    assert call(14, plan=ctypes.c_void_p(0x30004)) == C.CM_EINVAL
+    assert call(14, out=ctypes.c_void_p(0x80008)) == C.CM_EINVAL
+    assert call(14, rope=C.CmRope(base=0.0, style=0, reserved=0)) == C.CM_EINVAL

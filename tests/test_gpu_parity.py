@@ -342,3 +342,43 @@ def test_fused_interleaved_style(dtype):
     torch.cuda.synchronize()
     assert torch.equal(a.merged, b.merged) and a.digests == b.digests
     check_render(a, dl, w.dtype, w.routing_layer, w.rope_base, style="interleaved")
+
+
+def test_devplan_render_equals_host_checked_render_and_rejects_bad_plans():
+    """cm_render_merge_devplan renders the device plan exactly like
+    cm_render_merge; a plan that fails the device check moves no byte and
+    reports CM_ESHAPE in its status entry."""
+    w = synth.custom("devplan", dtype="bfloat16", d=128, H=2, L=2, lengths=(300, 129, 77),
+                     routing_layer=1)
+    _, dl = gpu_deliveries(w)
+    ref = cm.render_deliveries(dl, w.routing_layer, w.rope_base, pipeline="serial")
+    torch.cuda.synchronize()
+    batch = cm.FragmentBatch(dl)
+    ws = torch.empty(max(cm.workspace_size(batch), 256), dtype=torch.uint8, device="cuda")
+    plan = torch.from_numpy(ref.plan.copy()).to("cuda")
+    out = torch.zeros_like(ref.merged)
+    cm.render_merge_devplan(batch, plan, w.rope_base, "half", out, ref.T_out, ws)
+    torch.cuda.synchronize()
+    assert torch.equal(out, ref.merged)
+    assert int(plan[0]) == 0
+    n = batch.n
+    for what, mutate in (("offset", lambda p: p.__setitem__(4 + n + 1, p[4 + n + 1] + 1)),
+                         ("length", lambda p: p.__setitem__(4 + 2 * n, p[4 + 2 * n] - 1)),
+                         ("delivery", lambda p: p.__setitem__(4, 7)),
+                         ("status", lambda p: p.__setitem__(0, -4))):
+        bad = ref.plan.copy()
+        mutate(bad)
+        log(f"[devplan] corrupted {what}")
+        plan = torch.from_numpy(bad).to("cuda")
+        out = torch.full_like(ref.merged, 3)
+        cm.render_merge_devplan(batch, plan, w.rope_base, "half", out, ref.T_out, ws)
+        torch.cuda.synchronize()
+        assert int(plan[0]) == -2, what
+        assert bool((out == 3).all()), what
+    plan = torch.from_numpy(ref.plan.copy()).to("cuda")
+    shape = list(ref.merged.shape)
+    shape[4] -= 1                                                  # T_out one short
+    out = torch.full(shape, 3, dtype=ref.merged.dtype, device="cuda")
+    cm.render_merge_devplan(batch, plan, w.rope_base, "half", out, ref.T_out - 1, ws)
+    torch.cuda.synchronize()
+    assert int(plan[0]) == -2 and bool((out == 3).all())
