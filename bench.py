@@ -80,6 +80,11 @@ def fused_work(w, r, mask):
     return B2S_OPS_PER_BLOCK * hashed_blocks + ROT_OPS_PER_ELEM * rotated, hashed_blocks * 64, rotated
 
 
+def delivered_bytes(w):
+    """Bytes of every delivery (duplicates counted): what the naive render moves each way."""
+    return w.delivery_bytes
+
+
 def cpu_baseline(w, frags):
     """The oracle, unchanged, over the five shortest distinct fragments."""
     import oracle
@@ -189,6 +194,37 @@ def main():
             set_kernels[k] = {"total_ms": ms, "launches": n}
     cm.timing_reset()
 
+    # the paper's baselines over the same render: the naive multiset re-render
+    # (§5.9, every delivery its own operand) and BagMerge in delivery order (§4.2)
+    def timed(fn):
+        for _ in range(2):
+            r = fn()
+            del r
+        torch.cuda.synchronize()
+        ta = time.perf_counter()
+        for _ in range(args.steps):
+            r = fn()
+            T = r.T_out
+            del r
+        torch.cuda.synchronize()
+        return (time.perf_counter() - ta) / args.steps * 1e3, T
+
+    multiset_bytes = 2 * delivered_bytes(w)
+    ms_naive, T_naive = timed(lambda: cm.render_multiset(batch, w.routing_layer, w.rope_base))
+    order = list(range(batch.n))
+    ms_bag, T_bag = timed(lambda: cm.bag_merge(batch, order, w.rope_base))
+    baselines = {
+        "naive_multiset": {"ms": round(ms_naive, 4), "T_out": T_naive,
+                           "GBps": round(multiset_bytes / (ms_naive / 1e3) / 1e9, 1),
+                           "what": "steps 1-5 without dedupe: hash, score, multiset order, render "
+                                   "of every delivery (fused)"},
+        "bag_merge_default": {"ms": round(ms_bag, 4), "T_out": T_bag,
+                              "GBps": round(multiset_bytes / (ms_bag / 1e3) / 1e9, 1),
+                              "pct_hbm_peak": round(100 * multiset_bytes / (ms_bag / 1e3) / 1e9
+                                                    / HBM_PEAK_GBPS, 2),
+                              "what": "render of every delivery in delivery order (plan on the host)"},
+    }
+
     ms_step = (t1 - t0) / args.steps * 1e3
     ms_render_set = (t3 - t2) / args.steps * 1e3
     render_bytes = w.render_bytes
@@ -254,6 +290,7 @@ def main():
                        "merges_per_s": round(1e3 / ms_render_set, 3),
                        "kernels_ms": {k: round(v["total_ms"] / args.steps, 4)
                                       for k, v in set_kernels.items()}},
+        "baselines": baselines,
     }
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
