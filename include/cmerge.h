@@ -12,6 +12,7 @@
  *   cm_render_merge         Eq. (1)-(2): K of slot i rotated by R(s_i), V copied,
  *                           both concatenated along the sequence axis
  *   cm_render_merge_devplan the same with the plan left on the device
+ *   cm_render_merge_range   the slots from a given rank on (incremental render)
  * the paper's baselines over the same render:
  *   cm_multiset_order       the naive re-render order of §5.9 (no dedupe)
  *   cm_bag_plan             BagMerge with a caller-supplied order (§4.2)
@@ -224,6 +225,21 @@ int32_t cm_render_merge(const cm_fragset* set, const int64_t* plan_dev,
                         int64_t T_out, void* workspace, size_t workspace_bytes,
                         void* stream);
 
+/* Incremental render (the lazy Render of Alg. 2 without re-rendering the whole
+ * set): renders only slots [first_slot, n_unique) of the plan, i.e. rows
+ * [offset of first_slot, T_out) of every row block, into a merged cache whose row
+ * blocks are T_cap >= T_out rows long: out_dev laid out [L][2][1][H][T_cap][d]
+ * (layer l's K is the block at element offset (2l) * H * T_cap * d, rows
+ * [0, T_out) of each head in use). Rows before the first slot's offset are not
+ * touched. After a fragment is inserted into a set at rank r, the slots before r
+ * keep their fragments and offsets, so rendering the new plan from slot r into
+ * the cache rendered for the old plan (same T_cap) gives exactly the full render.
+ * plan_dev / plan_host as in cm_render_merge (T_out is the plan's);
+ * 0 <= first_slot < n_unique. */
+int32_t cm_render_merge_range(const cm_fragset* set, const int64_t* plan_dev,
+                              const int64_t* plan_host, const cm_rope* rope, int32_t first_slot,
+                              void* out_dev, int64_t T_cap, void* workspace,
+                              size_t workspace_bytes, void* stream);
 /* As cm_render_merge for a plan that is only on the device (e.g. just written by
  * cm_canonical_order on the same stream): nothing waits for the plan. The caller
  * gives T_out (for a set of distinct fragments, the sum of their lengths;

@@ -16,6 +16,7 @@ from .binding import (  # noqa: F401
     plan_elems,
     render_merge,
     render_merge_devplan,
+    render_merge_range,
     render_merge_hash,
     timing_enable,
     timing_query,
@@ -24,6 +25,7 @@ from .binding import (  # noqa: F401
 )
 from .fragset import (  # noqa: F401
     LatentFragmentSet,
+    MergedCache,
     PIPELINES,
     RenderResult,
     bag_merge,

@@ -30,7 +30,7 @@ EXPORTS = (
     "cm_version", "cm_last_error", "cm_status_string", "cm_plan_elems", "cm_workspace_size",
     "cm_fragment_hash", "cm_fragment_hash_select", "cm_fragment_knorm", "cm_equal_key_mask",
     "cm_canonical_order", "cm_multiset_order", "cm_bag_plan", "cm_render_merge",
-    "cm_render_merge_devplan", "cm_render_merge_hash",
+    "cm_render_merge_devplan", "cm_render_merge_range", "cm_render_merge_hash",
     "cm_timing_enable", "cm_timing_reset", "cm_timing_query",
 )
 
@@ -86,6 +86,8 @@ def lib() -> ctypes.CDLL:
             "cm_bag_plan": (I32, [FS, P, I32, P]),
             "cm_render_merge": (I32, [FS, P, P, ctypes.POINTER(CmRope), P, I64, P, SZ, P]),
             "cm_render_merge_devplan": (I32, [FS, P, ctypes.POINTER(CmRope), P, I64, P, SZ, P]),
+            "cm_render_merge_range": (I32, [FS, P, P, ctypes.POINTER(CmRope), I32, P, I64, P, SZ,
+                                            P]),
             "cm_render_merge_hash": (I32, [FS, P, P, ctypes.POINTER(CmRope), P, P, P, I64, P, SZ,
                                            P]),
             "cm_timing_enable": (I32, [I32]),

@@ -151,6 +151,19 @@ def render_merge(batch: FragmentBatch, plan_dev: torch.Tensor, plan_host: np.nda
                                     _stream(stream, batch.device)), "cm_render_merge")
 
 
+def render_merge_range(batch: FragmentBatch, plan_dev: torch.Tensor, plan_host: np.ndarray,
+                       rope_base: float, style: str, first_slot: int, out: torch.Tensor,
+                       T_cap: int, workspace: torch.Tensor, stream=None) -> None:
+    plan_host = np.ascontiguousarray(plan_host, dtype=np.int64)
+    rope = C.CmRope(base=float(rope_base), style=_STYLES[style], reserved=0)
+    C.check(C.lib().cm_render_merge_range(ctypes.byref(batch.struct), _ptr(plan_dev),
+                                          plan_host.ctypes.data_as(ctypes.c_void_p),
+                                          ctypes.byref(rope), int(first_slot), _ptr(out), T_cap,
+                                          _ptr(workspace),
+                                          workspace.numel() * workspace.element_size(),
+                                          _stream(stream, batch.device)), "cm_render_merge_range")
+
+
 def render_merge_devplan(batch: FragmentBatch, plan_dev: torch.Tensor, rope_base: float,
                          style: str, out: torch.Tensor, T_out: int, workspace: torch.Tensor,
                          stream=None) -> None:

@@ -411,10 +411,35 @@ int32_t cm_render_merge(const cm_fragset* set, const int64_t* plan_dev, const in
     return st;
   const cm::RenderLayout lay = cm::render_layout(s);
   if ((st = check_ws(workspace, workspace_bytes, lay.bytes)) != CM_OK) return st;
-  hipError_t e = cm::launch_render(s, lay, plan_dev, T_out, rope->base, rope->style, false,
-                                   out_dev, static_cast<uint8_t*>(workspace),
+  hipError_t e = cm::launch_render(s, lay, plan_dev, {0, T_out, T_out}, rope->base, rope->style,
+                                   false, out_dev, static_cast<uint8_t*>(workspace),
                                    static_cast<hipStream_t>(stream));
   return e == hipSuccess ? CM_OK : fail_hip(e, "cm_render_merge");
+}
+
+int32_t cm_render_merge_range(const cm_fragset* set, const int64_t* plan_dev,
+                              const int64_t* plan_host, const cm_rope* rope, int32_t first_slot,
+                              void* out_dev, int64_t T_cap, void* workspace,
+                              size_t workspace_bytes, void* stream) {
+  g_err.clear();
+  cm::SetDesc s;
+  int32_t st = check_set(set, &s);
+  if (st != CM_OK) return st;
+  if (!plan_host) return fail(CM_EINVAL, "plan_host is NULL");
+  const int64_t T_out = plan_host[CM_PLAN_TOUT];
+  int64_t nu = 0;
+  if ((st = check_render_args(s, plan_dev, plan_host, rope, out_dev, T_out, &nu)) != CM_OK)
+    return st;
+  if (first_slot < 0 || first_slot >= nu)
+    return fail(CM_EINVAL, "first_slot must be in [0, n_unique)");
+  if (T_cap < T_out) return fail(CM_ESHAPE, "T_cap must be >= the plan's T_out");
+  const cm::RenderLayout lay = cm::render_layout(s);
+  if ((st = check_ws(workspace, workspace_bytes, lay.bytes)) != CM_OK) return st;
+  const int64_t row0 = plan_host[CM_PLAN_HEADER + s.n + first_slot];
+  hipError_t e = cm::launch_render(s, lay, plan_dev, {row0, T_out, T_cap}, rope->base,
+                                   rope->style, false, out_dev, static_cast<uint8_t*>(workspace),
+                                   static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? CM_OK : fail_hip(e, "cm_render_merge_range");
 }
 
 int32_t cm_render_merge_devplan(const cm_fragset* set, int64_t* plan_dev, const cm_rope* rope,
@@ -435,8 +460,8 @@ int32_t cm_render_merge_devplan(const cm_fragset* set, int64_t* plan_dev, const 
     return fail(CM_ESHAPE, "merged cache too long for one launch");
   const cm::RenderLayout lay = cm::render_layout(s);
   if ((st = check_ws(workspace, workspace_bytes, lay.bytes)) != CM_OK) return st;
-  hipError_t e = cm::launch_render(s, lay, plan_dev, T_out, rope->base, rope->style, true,
-                                   out_dev, static_cast<uint8_t*>(workspace),
+  hipError_t e = cm::launch_render(s, lay, plan_dev, {0, T_out, T_out}, rope->base, rope->style,
+                                   true, out_dev, static_cast<uint8_t*>(workspace),
                                    static_cast<hipStream_t>(stream));
   return e == hipSuccess ? CM_OK : fail_hip(e, "cm_render_merge_devplan");
 }

@@ -130,11 +130,16 @@ hipError_t launch_render_hash(const SetDesc& s, const HashLayout& hlay, const Re
                               const int64_t* plan_dev, int32_t n_unique, int64_t total_tasks,
                               int64_t T_out, double base, int32_t style, const uint8_t* select,
                               uint8_t* digests, void* out, uint8_t* ws, hipStream_t stream);
+// Rows [row0, T_out) of every row block are rendered into `out`, whose row
+// blocks are T_cap rows long (row0 = 0, T_cap = T_out: the whole merged cache).
+struct RenderRange {
+  int64_t row0, T_out, T_cap;
+};
 // check_on_device: the plan was not validated on the host; the prep kernel checks
 // it against the set and T_out and, if it fails, skips the render and writes
 // CM_ESHAPE into the plan's status.
 hipError_t launch_render(const SetDesc& s, const RenderLayout& lay, const int64_t* plan_dev,
-                         int64_t T_out, double base, int32_t style, bool check_on_device,
+                         const RenderRange& rr, double base, int32_t style, bool check_on_device,
                          void* out, uint8_t* ws, hipStream_t stream);
 
 // Per-kernel event timing (no-op unless cm_timing_enable(1)).

@@ -31,7 +31,7 @@ template <int ESIZE, int STYLE, int HB>
 __global__ __launch_bounds__(64) void render_unit_kernel(
     const int32_t* __restrict__ unit_slot, const int64_t* __restrict__ src_base,
     const int64_t* __restrict__ plan, int32_t n, const double* __restrict__ angles,
-    int32_t H, int32_t d, int64_t T_out, uint8_t* __restrict__ out) {
+    int32_t H, int32_t d, int64_t row0, int64_t T_out, int64_t T_cap, uint8_t* __restrict__ out) {
   constexpr int EP = 16 / ESIZE;
   constexpr int NA = STYLE == CM_ROPE_HALF ? EP : EP / 2;
   const int lane = threadIdx.x;
@@ -40,15 +40,18 @@ __global__ __launch_bounds__(64) void render_unit_kernel(
   const int ppr = (d * ESIZE) >> 4;                    // 16-byte pieces per row
   const int lkh = blockIdx.y;                          // (l * 2 + kv) * H + h
   const bool is_k = ((lkh / H) & 1) == 0;
-  const int64_t R = T_out << rb_shift;                 // bytes of one row block
-  const int64_t lb = (int64_t)blockIdx.x * kUnitBytes + lane * 16;   // piece k: lb + 1024 k
+  const int64_t end = T_out << rb_shift;               // rendered bytes of a row block end here
+  const int64_t R = T_cap << rb_shift;                 // bytes of one row block of `out`
+  // units tile rows [row0, T_out) of every row block; piece k of the lane is
+  // byte lb + 1024 k of the row block
+  const int64_t lb = (row0 << rb_shift) + (int64_t)blockIdx.x * kUnitBytes + lane * 16;
   const int cp = (int)((lb & row_mask) >> 4);          // column piece of this lane
   const int64_t* offs = plan + CM_PLAN_HEADER + n;
   const int64_t n_lkh = gridDim.y;
   // piece k from slot s: load, rotate (K at a non-zero offset), store
   auto piece = [&](int k, int s, const double* cs, const double* sn) {
     const int64_t b = lb + 1024 * k;
-    const bool valid = b < R;
+    const bool valid = b < end;
     const uint8_t* src = reinterpret_cast<const uint8_t*>(src_base[s * n_lkh + lkh]);
     u32x4 x = {0u, 0u, 0u, 0u};
     if (valid) x = ld16(src + b);                      // row b >> rb_shift, same column
@@ -97,7 +100,7 @@ __global__ __launch_bounds__(64) void render_unit_kernel(
 // when offset by r * row_bytes: fragment tensor base + (h * T_s - off_s) rows.
 __global__ __launch_bounds__(256) void render_unit_prep_kernel(
     const int64_t* __restrict__ table, int64_t stride, const int64_t* __restrict__ plan,
-    int32_t n, int32_t H, int32_t n_lkh, int32_t rb_shift, int64_t units,
+    int32_t n, int32_t H, int32_t n_lkh, int32_t rb_shift, int64_t row0, int64_t units,
     const int32_t* __restrict__ plan_ok, int32_t* unit_slot, int64_t* src_base) {
   const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t nthreads = (int64_t)gridDim.x * blockDim.x;
@@ -109,8 +112,9 @@ __global__ __launch_bounds__(256) void render_unit_prep_kernel(
   const int64_t* offs = plan + CM_PLAN_HEADER + n;
   const int64_t T_out = plan[CM_PLAN_TOUT];
   for (int64_t x = tid; x < units; x += nthreads) {
-    const int64_t r0 = (x * kUnitBytes) >> rb_shift;
-    int64_t r1 = ((x + 1) * kUnitBytes - 1) >> rb_shift;
+    const int64_t b0 = (row0 << rb_shift) + x * kUnitBytes;
+    const int64_t r0 = b0 >> rb_shift;
+    int64_t r1 = (b0 + kUnitBytes - 1) >> rb_shift;
     r1 = r1 < T_out ? r1 : T_out - 1;
     int lo = 0, hi = n_u - 1;
     while (lo < hi) {
@@ -250,7 +254,7 @@ hipError_t launch_render_prep(const SetDesc& s, const RenderLayout& lay, const i
 }
 
 hipError_t launch_render(const SetDesc& s, const RenderLayout& lay, const int64_t* plan_dev,
-                         int64_t T_out, double base, int32_t style, bool check_on_device,
+                         const RenderRange& rr, double base, int32_t style, bool check_on_device,
                          void* out, uint8_t* ws, hipStream_t stream) {
   int32_t* plan_ok = check_on_device ? reinterpret_cast<int32_t*>(ws + lay.off_flag) : nullptr;
   {
@@ -261,11 +265,11 @@ hipError_t launch_render(const SetDesc& s, const RenderLayout& lay, const int64_
                        16 / s.esize, style, base, 0, (int64_t)s.L, token_bytes_of(s), nullptr,
                        nullptr, reinterpret_cast<int64_t*>(ws + lay.off_tiles),
                        reinterpret_cast<double*>(ws + lay.off_angles), s.table_dev, s.stride,
-                       T_out, plan_ok, const_cast<int64_t*>(plan_dev));
+                       rr.T_out, plan_ok, const_cast<int64_t*>(plan_dev));
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const int64_t units = render_units(s, T_out);
+  const int64_t units = render_units(s, rr.T_out - rr.row0);
   const int32_t n_lkh = 2 * s.L * s.H;
   const int rb_shift = __builtin_ctzll((unsigned long long)s.row_bytes);
   int32_t* unit_slot = reinterpret_cast<int32_t*>(ws + lay.off_unit_slot);
@@ -276,7 +280,7 @@ hipError_t launch_render(const SetDesc& s, const RenderLayout& lay, const int64_
     const int64_t blocks = (work + 255) / 256;
     hipLaunchKernelGGL(render_unit_prep_kernel, dim3((uint32_t)(blocks < 1024 ? blocks : 1024)),
                        dim3(256), 0, stream, s.table_dev, s.stride, plan_dev, s.n, s.H, n_lkh,
-                       rb_shift, units, plan_ok, unit_slot, src_base);
+                       rb_shift, rr.row0, units, plan_ok, unit_slot, src_base);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   const double* angles = reinterpret_cast<const double*>(ws + lay.off_angles);
@@ -287,10 +291,10 @@ hipError_t launch_render(const SetDesc& s, const RenderLayout& lay, const int64_
     constexpr int STYLE = decltype(tag)::style, HB = decltype(tag)::hb;
     if (s.esize == 2)
       hipLaunchKernelGGL((render_unit_kernel<2, STYLE, HB>), grid, dim3(64), 0, stream, unit_slot,
-                         src_base, plan_dev, s.n, angles, s.H, s.d, T_out, o);
+                         src_base, plan_dev, s.n, angles, s.H, s.d, rr.row0, rr.T_out, rr.T_cap, o);
     else
       hipLaunchKernelGGL((render_unit_kernel<4, STYLE, HB>), grid, dim3(64), 0, stream, unit_slot,
-                         src_base, plan_dev, s.n, angles, s.H, s.d, T_out, o);
+                         src_base, plan_dev, s.n, angles, s.H, s.d, rr.row0, rr.T_out, rr.T_cap, o);
   };
   dispatch_style(style, s.row_bytes, go);
   return hipGetLastError();

@@ -23,7 +23,8 @@ import torch
 from . import _cabi as C
 from .binding import (FragmentBatch, bag_plan, canonical_order, equal_key_mask, fragment_hash,
                       fragment_hash_select, fragment_knorm, multiset_order, plan_elems,
-                      render_merge, render_merge_devplan, render_merge_hash, workspace_size)
+                      render_merge, render_merge_devplan, render_merge_hash,
+                      render_merge_range, workspace_size)
 
 _WS: Dict[tuple, torch.Tensor] = {}
 _SIDE: Dict[torch.device, torch.cuda.Stream] = {}
@@ -319,3 +320,66 @@ class LatentFragmentSet:
         plan_host = None
         return RenderResult(cache=cache, merged=merged, digests_dev=digests, keys_dev=keys,
                             plan_host=plan_host, tail_len=tail, plan_dev=plan_dev)
+
+
+class MergedCache:
+    """The render of a LatentFragmentSet kept up to date as the set grows
+    (Render of Alg. 2 without re-rendering every fragment each time).
+
+    The merged cache lives in one buffer [L][2][1][H][T_cap][d]; `cache` are
+    the [1, H, T_out, d] views of its first T_out rows. update() computes the
+    set's plan and re-renders only the slots from the first one whose fragment
+    differs from the previous render: inserting a fragment at rank r leaves the
+    slots before r with the same fragments and offsets, hence the same bytes,
+    so the result equals the full render of the set bit for bit. When T_out
+    outgrows T_cap the buffer grows by `growth` and everything is rendered."""
+
+    def __init__(self, fset: LatentFragmentSet, routing_layer: int, rope_base: float,
+                 style: str = "half", capacity: int = 0, growth: float = 1.5):
+        self.fset = fset
+        self.routing_layer, self.rope_base, self.style = routing_layer, rope_base, style
+        self.capacity, self.growth = int(capacity), float(growth)
+        self.buffer: Optional[torch.Tensor] = None
+        self.slot_ids: List[bytes] = []
+        self.T_out = 0
+        self.last_first_slot = 0        # first slot rendered by the last update
+        self.last_rows = 0              # rows per row block rendered by the last update
+
+    @property
+    def T_cap(self) -> int:
+        return 0 if self.buffer is None else int(self.buffer.shape[4])
+
+    @property
+    def cache(self) -> tuple:
+        b = self.buffer
+        return tuple((b[l, 0, :, :, :self.T_out], b[l, 1, :, :, :self.T_out])
+                     for l in range(b.shape[0]))
+
+    def update(self, stream=None) -> tuple:
+        batch, digests = self.fset._description()
+        ids = list(self.fset._items.keys())
+        dev = batch.device
+        ws = _workspace(batch)
+        keys = torch.empty(batch.n, dtype=torch.float64, device=dev)
+        plan_dev = torch.empty(plan_elems(batch.n), dtype=torch.int64, device=dev)
+        fragment_knorm(batch, self.routing_layer, min(batch.lengths), keys, ws, stream)
+        canonical_order(batch, keys, digests, plan_dev, stream)
+        plan = _plan_to_host(plan_dev, stream)
+        n, n_u, T_out = int(plan[C.PLAN_N]), int(plan[C.PLAN_NUNIQUE]), int(plan[C.PLAN_TOUT])
+        slot_ids = [ids[int(plan[C.PLAN_HEADER + s])] for s in range(n_u)]
+        if self.buffer is None or T_out > self.T_cap:
+            T_cap = max(T_out, self.capacity, int(self.T_cap * self.growth))
+            self.buffer = torch.empty((batch.L, 2, 1, batch.H, T_cap, batch.d),
+                                      dtype=batch.torch_dtype, device=dev)
+            first = 0
+        else:
+            first = 0
+            while first < min(n_u, len(self.slot_ids)) and slot_ids[first] == self.slot_ids[first]:
+                first += 1
+        if first < n_u:
+            render_merge_range(batch, plan_dev, plan, self.rope_base, self.style, first,
+                               self.buffer, self.T_cap, ws, stream)
+        self.last_first_slot = first
+        self.last_rows = T_out - (int(plan[C.PLAN_HEADER + n + first]) if first < n_u else T_out)
+        self.slot_ids, self.T_out = slot_ids, T_out
+        return self.cache

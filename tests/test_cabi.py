@@ -246,3 +246,23 @@ def test_render_devplan_argument_checks(lib):
     assert call(14, plan=ctypes.c_void_p(0x30004)) == C.CM_EINVAL
     assert call(14, out=ctypes.c_void_p(0x80008)) == C.CM_EINVAL
     assert call(14, rope=C.CmRope(base=0.0, style=0, reserved=0)) == C.CM_EINVAL
+
+
+def test_render_range_argument_checks(lib):
+    fs = FakeSet(lengths=(5, 9))
+    _, need = _ws(lib, fs)
+    rope = C.CmRope(base=1e4, style=0, reserved=0)
+    good = _plan(2, [1, 0], [9, 5])
+
+    def call(first, T_cap, plan=good, ws_bytes=need):
+        return lib.cm_render_merge_range(fs.ref, ctypes.c_void_p(0x30000),
+                                         plan.ctypes.data_as(ctypes.c_void_p), ctypes.byref(rope),
+                                         first, ctypes.c_void_p(0x80000), T_cap,
+                                         ctypes.c_void_p(0x40000), ws_bytes, None)
+
+    assert call(1, 20, ws_bytes=0) == C.CM_EWORKSPACE       # every other check passed
+    assert call(0, 14, ws_bytes=0) == C.CM_EWORKSPACE
+    assert call(2, 20) == C.CM_EINVAL                       # no such slot
+    assert call(-1, 20) == C.CM_EINVAL
+    assert call(0, 13) == C.CM_ESHAPE                       # capacity below T_out
+    assert call(0, 20, plan=_plan(2, [1, 0], [9, 6])) == C.CM_ESHAPE
