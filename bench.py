@@ -225,6 +225,41 @@ def main():
                               "what": "render of every delivery in delivery order (plan on the host)"},
     }
 
+    # incremental render: a set missing one fragment X of middle rank is
+    # rendered into a buffer with room for all; ingesting X then re-renders only
+    # the slots from X's rank on (timed), and is compared with the full render
+    full = S.render(w.routing_layer, w.rope_base)
+    torch.cuda.synchronize()
+    distinct = list(S._items.values())
+    mid = full.order[len(full.order) // 2]
+    x_cache = distinct[mid]
+    S_without = cm.LatentFragmentSet()
+    S_without.ingest_many([c for k, c in enumerate(distinct) if k != mid])
+    S_with = S_without.merge(cm.LatentFragmentSet())
+    S_with.ingest(x_cache)
+    mc = cm.MergedCache(S_without, w.routing_layer, w.rope_base, capacity=full.T_out)
+    mc.update()
+    incr_ms = []
+    for _ in range(args.steps):
+        mc.fset = S_with
+        torch.cuda.synchronize()
+        ta = time.perf_counter()
+        mc.update()
+        torch.cuda.synchronize()
+        incr_ms.append((time.perf_counter() - ta) * 1e3)
+        rows, first = mc.last_rows, mc.last_first_slot
+        mc.fset = S_without
+        mc.update()
+    mc.fset = S_with
+    mc.update()
+    torch.cuda.synchronize()
+    incr_equal = all(torch.equal(a, b) and torch.equal(c, e)
+                     for (a, c), (b, e) in zip(mc.cache, full.cache))
+    token_bytes = 2 * w.L * w.H * w.d * (2 if w.dtype == "bfloat16" else 4)
+    incr_bytes = 2 * rows * token_bytes
+    ms_incr = sorted(incr_ms)[len(incr_ms) // 2]
+    del mc, full
+
     ms_step = (t1 - t0) / args.steps * 1e3
     ms_render_set = (t3 - t2) / args.steps * 1e3
     render_bytes = w.render_bytes
@@ -291,6 +326,13 @@ def main():
                        "kernels_ms": {k: round(v["total_ms"] / args.steps, 4)
                                       for k, v in set_kernels.items()}},
         "baselines": baselines,
+        "incremental": {"ms": round(ms_incr, 4), "first_slot": first, "slots": len(distinct),
+                        "rows_rendered": rows, "T_out": w.merged_tokens,
+                        "bytes": incr_bytes, "GBps": round(incr_bytes / (ms_incr / 1e3) / 1e9, 1),
+                        "equals_full_render": incr_equal,
+                        "what": "ingest one fragment of middle rank into a rendered set: knorm, "
+                                "order, plan copy, render of the slots from its rank (median of "
+                                "the timed steps)"},
     }
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
