@@ -13,6 +13,7 @@
  *                           both concatenated along the sequence axis
  *   cm_render_merge_devplan the same with the plan left on the device
  *   cm_render_merge_range   the slots from a given rank on (incremental render)
+ *   cm_paged_tables / cm_paged_render  the same render over paged storage
  * the paper's baselines over the same render:
  *   cm_multiset_order       the naive re-render order of §5.9 (no dedupe)
  *   cm_bag_plan             BagMerge with a caller-supplied order (§4.2)
@@ -265,6 +266,63 @@ int32_t cm_render_merge_hash(const cm_fragset* set, const int64_t* plan_dev,
                              const uint8_t* select_dev, uint8_t* digests_dev, void* out_dev,
                              int64_t T_out, void* workspace, size_t workspace_bytes,
                              void* stream);
+
+/* ---------------------------------------------------------------- paged render
+ * Paged KV storage (the merge as a permutation of already-allocated blocks plus
+ * the RoPE rotation, §4.5): one page pool holds, for every layer and K/V, P pages
+ * of B tokens of all H heads: pool laid out [L][2][P][H][B][d] (page p of layer
+ * l's K is the [H][B][d] block at element offset (2l * P + p) * H * B * d; its V
+ * at ((2l + 1) * P + p) * H * B * d). Fragment i is its length T_i and
+ * ceil(T_i / B) page ids, the same for every layer and K/V: its row t lives in
+ * row t % B of page blocks[first_i + t / B].
+ * table_host / table_dev: n rows of 2 int64 {T_i, first_i}; blocks_host /
+ * blocks_dev: n_blocks int32 page ids in [0, P). B is a power of two with
+ * B * d * element_bytes in [1 KiB, 16 KiB]. The pool address is 16-byte aligned.
+ */
+typedef struct {
+  int32_t n;
+  int32_t L;
+  int32_t H;
+  int32_t d;
+  int32_t dtype;     /* cm_dtype */
+  int32_t block;     /* B, tokens per page */
+  int64_t pages;     /* P */
+  void* pool_dev;
+  const int64_t* table_host;
+  const int64_t* table_dev;
+  const int32_t* blocks_host;
+  const int32_t* blocks_dev;
+  int64_t n_blocks;
+} cm_pagedset;
+
+/* Block tables of the merged cache for a plan over the paged fragments (any plan
+ * of this file's layout whose slots index the paged set's fragments, e.g. from
+ * cm_canonical_order over the same fragments or cm_bag_plan). Merged block j
+ * holds rows [jB, min(jB + B, T_out)). It reuses a fragment page, with no copy,
+ * when all its rows come from one slot s, start at a page boundary of that
+ * fragment (jB - offset_s a multiple of B) and, for K, offset_s = 0 (R(0) = I);
+ * otherwise it gets the next page of free_host, to be written by
+ * cm_paged_render. Outputs (host, ceil(T_out / B) entries each): k_table_host,
+ * v_table_host (page ids); fresh_host: the fresh pages to write as codes
+ * 2j + kv (at most 2 ceil(T_out / B) entries), their count in *n_fresh.
+ * Host only. CM_EINVAL if free_host has fewer than the pages needed (*n_fresh
+ * then holds the number needed). */
+int32_t cm_paged_tables(const cm_pagedset* set, const int64_t* plan_host, const int32_t* free_host,
+                        int64_t n_free, int32_t* k_table_host, int32_t* v_table_host,
+                        int32_t* fresh_host, int64_t* n_fresh);
+/* Writes the fresh pages of cm_paged_tables: for each code 2j + kv of fresh_dev
+ * (device, n_fresh int32), every layer and head, rows [jB, min(jB + B, T_out)) of
+ * the merged cache into page (kv ? v_table : k_table)[j] — K of a slot at offset
+ * s rotated by R(s) as in cm_render_merge, V copied; rows past T_out in the last
+ * page are left untouched. Pages not listed are neither read as destinations
+ * nor written. k_table_dev, v_table_dev: device copies of the tables.
+ * plan_dev / plan_host as in cm_render_merge. Workspace: cm_paged_workspace_size()
+ * bytes. */
+int32_t cm_paged_render(const cm_pagedset* set, const int64_t* plan_dev, const int64_t* plan_host,
+                        const cm_rope* rope, const int32_t* k_table_dev,
+                        const int32_t* v_table_dev, const int32_t* fresh_dev, int64_t n_fresh,
+                        void* workspace, size_t workspace_bytes, void* stream);
+int32_t cm_paged_workspace_size(const cm_pagedset* set, size_t* bytes_out);
 
 /* ---------------------------------------------------------------- timing
  * Optional per-kernel timing with HIP events recorded on the launch stream

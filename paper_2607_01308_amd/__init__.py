@@ -6,6 +6,7 @@ from ._cabi import CmError, LIB_PATH  # noqa: F401
 from .binding import (  # noqa: F401
     KERNELS,
     FragmentBatch,
+    PagedSet,
     bag_plan,
     canonical_order,
     equal_key_mask,
@@ -13,6 +14,9 @@ from .binding import (  # noqa: F401
     fragment_hash_select,
     fragment_knorm,
     multiset_order,
+    paged_render,
+    paged_tables,
+    paged_workspace_size,
     plan_elems,
     render_merge,
     render_merge_devplan,
@@ -26,6 +30,7 @@ from .binding import (  # noqa: F401
 from .fragset import (  # noqa: F401
     LatentFragmentSet,
     MergedCache,
+    PagedRender,
     PIPELINES,
     RenderResult,
     bag_merge,
@@ -33,4 +38,5 @@ from .fragset import (  # noqa: F401
     release_workspace,
     render_deliveries,
     render_multiset,
+    render_paged,
 )

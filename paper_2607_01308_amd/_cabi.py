@@ -31,6 +31,7 @@ EXPORTS = (
     "cm_fragment_hash", "cm_fragment_hash_select", "cm_fragment_knorm", "cm_equal_key_mask",
     "cm_canonical_order", "cm_multiset_order", "cm_bag_plan", "cm_render_merge",
     "cm_render_merge_devplan", "cm_render_merge_range", "cm_render_merge_hash",
+    "cm_paged_workspace_size", "cm_paged_tables", "cm_paged_render",
     "cm_timing_enable", "cm_timing_reset", "cm_timing_query",
 )
 
@@ -45,6 +46,24 @@ class CmFragset(ctypes.Structure):
         ("reserved", ctypes.c_int32),
         ("table_host", ctypes.c_void_p),
         ("table_dev", ctypes.c_void_p),
+    ]
+
+
+class CmPagedset(ctypes.Structure):
+    _fields_ = [
+        ("n", ctypes.c_int32),
+        ("L", ctypes.c_int32),
+        ("H", ctypes.c_int32),
+        ("d", ctypes.c_int32),
+        ("dtype", ctypes.c_int32),
+        ("block", ctypes.c_int32),
+        ("pages", ctypes.c_int64),
+        ("pool_dev", ctypes.c_void_p),
+        ("table_host", ctypes.c_void_p),
+        ("table_dev", ctypes.c_void_p),
+        ("blocks_host", ctypes.c_void_p),
+        ("blocks_dev", ctypes.c_void_p),
+        ("n_blocks", ctypes.c_int64),
     ]
 
 
@@ -71,6 +90,7 @@ def lib() -> ctypes.CDLL:
         L = ctypes.CDLL(LIB_PATH)
         P, I32, I64, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
         FS = ctypes.POINTER(CmFragset)
+        PS = ctypes.POINTER(CmPagedset)
         sig = {
             "cm_version": (I32, []),
             "cm_last_error": (ctypes.c_char_p, []),
@@ -90,6 +110,9 @@ def lib() -> ctypes.CDLL:
                                             P]),
             "cm_render_merge_hash": (I32, [FS, P, P, ctypes.POINTER(CmRope), P, P, P, I64, P, SZ,
                                            P]),
+            "cm_paged_workspace_size": (I32, [PS, ctypes.POINTER(SZ)]),
+            "cm_paged_tables": (I32, [PS, P, P, I64, P, P, P, ctypes.POINTER(I64)]),
+            "cm_paged_render": (I32, [PS, P, P, ctypes.POINTER(CmRope), P, P, P, I64, P, SZ, P]),
             "cm_timing_enable": (I32, [I32]),
             "cm_timing_reset": (I32, []),
             "cm_timing_query": (I32, [ctypes.c_char_p, ctypes.POINTER(ctypes.c_double),

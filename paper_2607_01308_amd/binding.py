@@ -209,4 +209,76 @@ def timing_query(kernel: str):
 
 
 KERNELS = ("hash_prep", "hash_leaf", "hash_parent", "hash_final", "knorm_rows", "knorm_tree",
-           "order", "key_mask", "render_prep", "render", "render_hash")
+           "order", "key_mask", "render_prep", "render", "render_hash", "paged")
+
+
+class PagedSet:
+    """Fragments in a paged pool (see cm_pagedset): pool [L, 2, P, H, B, d],
+    fragment i = its length and its ceil(T_i / B) page ids."""
+
+    def __init__(self, pool: torch.Tensor, lengths: Sequence[int], page_lists: Sequence):
+        if pool.dim() != 6 or pool.shape[1] != 2 or not pool.is_contiguous():
+            raise ValueError("pool must be a contiguous [L, 2, P, H, B, d] tensor")
+        if pool.dtype not in _DTYPES:
+            raise TypeError(f"unsupported dtype {pool.dtype}")
+        self.pool = pool
+        self.L, _, self.P, self.H, self.B, self.d = pool.shape
+        self.torch_dtype = pool.dtype
+        self.device = pool.device
+        self.lengths = [int(t) for t in lengths]
+        rows, blocks = [], []
+        for T, pages in zip(self.lengths, page_lists):
+            rows.append([T, len(blocks)])
+            blocks.extend(int(q) for q in pages)
+        self.table_host = np.ascontiguousarray(np.array(rows, dtype=np.int64))
+        self.blocks_host = np.ascontiguousarray(np.array(blocks, dtype=np.int32))
+        self.table_dev = torch.from_numpy(self.table_host).to(self.device)
+        self.blocks_dev = torch.from_numpy(self.blocks_host).to(self.device)
+        self.struct = C.CmPagedset(
+            n=len(self.lengths), L=self.L, H=self.H, d=self.d, dtype=_DTYPES[self.torch_dtype],
+            block=self.B, pages=self.P, pool_dev=pool.data_ptr(),
+            table_host=self.table_host.ctypes.data, table_dev=self.table_dev.data_ptr(),
+            blocks_host=self.blocks_host.ctypes.data, blocks_dev=self.blocks_dev.data_ptr(),
+            n_blocks=len(blocks))
+
+    @property
+    def n(self) -> int:
+        return len(self.lengths)
+
+
+def paged_workspace_size(pset: PagedSet) -> int:
+    out = ctypes.c_size_t(0)
+    C.check(C.lib().cm_paged_workspace_size(ctypes.byref(pset.struct), ctypes.byref(out)),
+            "cm_paged_workspace_size")
+    return int(out.value)
+
+
+def paged_tables(pset: PagedSet, plan_host: np.ndarray, free_pages):
+    """Block tables of the merged cache (host): K table, V table, fresh codes 2j + kv."""
+    plan_host = np.ascontiguousarray(plan_host, dtype=np.int64)
+    free = np.ascontiguousarray(np.asarray(free_pages, dtype=np.int32))
+    nbo = (int(plan_host[C.PLAN_TOUT]) + pset.B - 1) // pset.B
+    kt = np.empty(nbo, dtype=np.int32)
+    vt = np.empty(nbo, dtype=np.int32)
+    fresh = np.empty(2 * nbo, dtype=np.int32)
+    count = ctypes.c_int64(0)
+    C.check(C.lib().cm_paged_tables(ctypes.byref(pset.struct),
+                                    plan_host.ctypes.data_as(ctypes.c_void_p),
+                                    free.ctypes.data_as(ctypes.c_void_p), int(free.size),
+                                    kt.ctypes.data_as(ctypes.c_void_p),
+                                    vt.ctypes.data_as(ctypes.c_void_p),
+                                    fresh.ctypes.data_as(ctypes.c_void_p), ctypes.byref(count)),
+            "cm_paged_tables")
+    return kt, vt, fresh[:count.value].copy()
+
+
+def paged_render(pset: PagedSet, plan_dev: torch.Tensor, plan_host: np.ndarray, rope_base: float,
+                 style: str, k_table: torch.Tensor, v_table: torch.Tensor, fresh: torch.Tensor,
+                 workspace: torch.Tensor, stream=None) -> None:
+    plan_host = np.ascontiguousarray(plan_host, dtype=np.int64)
+    rope = C.CmRope(base=float(rope_base), style=_STYLES[style], reserved=0)
+    C.check(C.lib().cm_paged_render(ctypes.byref(pset.struct), _ptr(plan_dev),
+                                    plan_host.ctypes.data_as(ctypes.c_void_p), ctypes.byref(rope),
+                                    _ptr(k_table), _ptr(v_table), _ptr(fresh), int(fresh.numel()),
+                                    _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                    _stream(stream, pset.device)), "cm_paged_render")

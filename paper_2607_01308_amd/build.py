@@ -21,7 +21,8 @@ HOSTCHECK_SRC = os.path.join(ROOT, "tests", "native", "hostcheck.hip")
 HOSTCHECK_LIB = os.path.join(ROOT, "tests", "native", "libcm_hostcheck.so")
 
 ARCH = "gfx950"
-SOURCES = ["api.cpp", "hash.hip", "knorm.hip", "order.hip", "render.hip", "render_hash.hip"]
+SOURCES = ["api.cpp", "hash.hip", "knorm.hip", "order.hip", "paged.hip", "render.hip",
+           "render_hash.hip"]
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function",
           f"-I{INCLUDE}", f"-I{CSRC}"]
 DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]

@@ -1,6 +1,7 @@
 // C ABI of libcmerge (include/cmerge.h): argument validation on the host, workspace
 // sizing, error reporting and the optional per-kernel event timing. Every check
 // runs before anything is enqueued, so a failing call leaves the stream untouched.
+#include <algorithm>
 #include <atomic>
 #include <cmath>
 #include <cstring>
@@ -103,7 +104,7 @@ int64_t min_T(const cm::SetDesc& s) {
 // ------------------------------------------------------------------ timing registry
 const char* const kKernelNames[cm::K_COUNT] = {
     "hash_prep", "hash_leaf", "hash_parent", "hash_final", "knorm_rows", "knorm_tree",
-    "order",     "key_mask",  "render_prep", "render",     "render_hash"};
+    "order",     "key_mask",  "render_prep", "render",     "render_hash", "paged"};
 std::atomic<bool> g_timing{false};
 std::mutex g_tmu;
 struct Pending {
@@ -491,6 +492,180 @@ int32_t cm_render_merge_hash(const cm_fragset* set, const int64_t* plan_dev,
                                         static_cast<uint8_t*>(workspace),
                                         static_cast<hipStream_t>(stream));
   return e == hipSuccess ? CM_OK : fail_hip(e, "cm_render_merge_hash");
+}
+
+}  // extern "C"
+
+namespace {
+
+int32_t check_pagedset(const cm_pagedset* set, cm::PagedDesc* out) {
+  if (!set) return fail(CM_EINVAL, "set is NULL");
+  if (set->n < 1 || set->n > CM_MAX_FRAGMENTS)
+    return fail(CM_EINVAL, "n must be in [1, " + std::to_string(CM_MAX_FRAGMENTS) + "]");
+  if (set->L < 1 || set->H < 1) return fail(CM_EINVAL, "L and H must be >= 1");
+  if ((int64_t)2 * set->L * set->H > 65535) return fail(CM_ESHAPE, "2 * L * H must be <= 65535");
+  int esize = 0;
+  if (set->dtype == CM_F32) esize = 4;
+  else if (set->dtype == CM_BF16) esize = 2;
+  else return fail(CM_EDTYPE, "dtype must be CM_F32 or CM_BF16");
+  const int64_t row_bytes = (int64_t)set->d * esize;
+  if (!is_pow2(set->d) || row_bytes < 64 || row_bytes > 1024)
+    return fail(CM_ESHAPE, "d must be a power of two with d * element_bytes in [64, 1024]");
+  if (set->block < 1 || !is_pow2(set->block) || set->block * row_bytes < 1024 ||
+      set->block * row_bytes > 16384)
+    return fail(CM_ESHAPE, "block must be a power of two with block * d * element_bytes in "
+                           "[1024, 16384]");
+  if (set->pages < 1 || set->pages > ((int64_t)1 << 31) - 1)
+    return fail(CM_EINVAL, "pages must be in [1, 2^31)");
+  if (!set->pool_dev || !aligned(set->pool_dev, 16))
+    return fail(CM_EINVAL, "pool_dev is NULL or not 16-byte aligned");
+  if (!set->table_host || !set->table_dev || !set->blocks_host || !set->blocks_dev)
+    return fail(CM_EINVAL, "paged tables are NULL");
+  if (!aligned(set->table_dev, 8) || !aligned(set->blocks_dev, 4))
+    return fail(CM_EINVAL, "table_dev / blocks_dev misaligned");
+  if (set->n_blocks < 1) return fail(CM_EINVAL, "n_blocks must be >= 1");
+  for (int64_t k = 0; k < set->n_blocks; ++k)
+    if (set->blocks_host[k] < 0 || set->blocks_host[k] >= set->pages)
+      return fail(CM_EINVAL, "page id " + std::to_string(k) + " outside the pool");
+  for (int i = 0; i < set->n; ++i) {
+    const int64_t T = set->table_host[2 * (int64_t)i], first = set->table_host[2 * (int64_t)i + 1];
+    if (T < 1) return fail(CM_EINVAL, "fragment " + std::to_string(i) + " has T < 1");
+    const int64_t nb = (T + set->block - 1) / set->block;
+    if (first < 0 || first > set->n_blocks - nb)
+      return fail(CM_EINVAL, "fragment " + std::to_string(i) + " page list outside blocks");
+  }
+  cm::SetDesc& s = out->s;
+  s.n = set->n;
+  s.L = set->L;
+  s.H = set->H;
+  s.d = set->d;
+  s.dtype = set->dtype;
+  s.esize = esize;
+  s.stride = 2;
+  s.row_bytes = row_bytes;
+  s.table_dev = set->table_dev;
+  s.table_host = set->table_host;
+  out->block = set->block;
+  out->b_shift = __builtin_ctz((unsigned)set->block);
+  out->pages = set->pages;
+  out->pool = set->pool_dev;
+  out->blocks_dev = set->blocks_dev;
+  return CM_OK;
+}
+
+// Plan checks against the fragments' lengths (slots, lengths, prefix offsets).
+int32_t check_plan_host(const cm::SetDesc& s, const int64_t* plan_host, int64_t* nu_out) {
+  if (!plan_host) return fail(CM_EINVAL, "plan_host is NULL");
+  if (plan_host[CM_PLAN_STATUS] != CM_OK) return fail(CM_EINVAL, "plan status is not CM_OK");
+  if (plan_host[CM_PLAN_N] != s.n) return fail(CM_EINVAL, "plan was built for another n");
+  const int64_t nu = plan_host[CM_PLAN_NUNIQUE];
+  if (nu < 1 || nu > s.n) return fail(CM_EINVAL, "plan n_unique out of range");
+  int64_t off = 0;
+  for (int64_t k = 0; k < nu; ++k) {
+    const int64_t src = plan_host[CM_PLAN_HEADER + k];
+    if (src < 0 || src >= s.n) return fail(CM_EINVAL, "plan slot refers to no fragment");
+    if (plan_host[CM_PLAN_HEADER + 2 * (int64_t)s.n + k] != s.T((int)src))
+      return fail(CM_ESHAPE, "plan slot length differs from the fragment's T");
+    if (plan_host[CM_PLAN_HEADER + s.n + k] != off)
+      return fail(CM_ESHAPE, "plan offsets are not the prefix sum of slot lengths");
+    off += s.T((int)src);
+  }
+  if (plan_host[CM_PLAN_TOUT] != off) return fail(CM_ESHAPE, "plan T_out is not the sum of lengths");
+  *nu_out = nu;
+  return CM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t cm_paged_workspace_size(const cm_pagedset* set, size_t* bytes_out) {
+  g_err.clear();
+  cm::PagedDesc p;
+  int32_t st = check_pagedset(set, &p);
+  if (st != CM_OK) return st;
+  if (!bytes_out) return fail(CM_EINVAL, "bytes_out is NULL");
+  *bytes_out = cm::align_up(sizeof(double) * (size_t)p.s.n * p.s.d, cm::kWsAlign);
+  return CM_OK;
+}
+
+int32_t cm_paged_tables(const cm_pagedset* set, const int64_t* plan_host, const int32_t* free_host,
+                        int64_t n_free, int32_t* k_table_host, int32_t* v_table_host,
+                        int32_t* fresh_host, int64_t* n_fresh) {
+  g_err.clear();
+  cm::PagedDesc p;
+  int32_t st = check_pagedset(set, &p);
+  if (st != CM_OK) return st;
+  int64_t nu = 0;
+  if ((st = check_plan_host(p.s, plan_host, &nu)) != CM_OK) return st;
+  if (!k_table_host || !v_table_host || !fresh_host || !n_fresh)
+    return fail(CM_EINVAL, "output pointer is NULL");
+  if (n_free < 0 || (n_free > 0 && !free_host)) return fail(CM_EINVAL, "free_host is NULL");
+  // free pages: inside the pool, distinct, used by no fragment
+  std::vector<uint8_t> used((size_t)p.pages, 0);
+  for (int64_t k = 0; k < set->n_blocks; ++k) used[(size_t)set->blocks_host[k]] = 1;
+  for (int64_t k = 0; k < n_free; ++k) {
+    const int32_t q = free_host[k];
+    if (q < 0 || q >= p.pages || used[(size_t)q])
+      return fail(CM_EINVAL, "free page " + std::to_string(k) +
+                                 " is outside the pool, repeated or holds a fragment page");
+    used[(size_t)q] = 2;
+  }
+  const int64_t n = p.s.n, B = p.block;
+  const int64_t T_out = plan_host[CM_PLAN_TOUT];
+  const int64_t nbo = (T_out + B - 1) / B;
+  int64_t taken = 0, count = 0;
+  int64_t s = 0;                                   // slot holding row j * B
+  for (int64_t j = 0; j < nbo; ++j) {
+    const int64_t r0 = j * B, e = std::min(r0 + B, T_out);
+    while (s + 1 < nu && plan_host[CM_PLAN_HEADER + n + s + 1] <= r0) ++s;
+    const int64_t i = plan_host[CM_PLAN_HEADER + s];
+    const int64_t off = plan_host[CM_PLAN_HEADER + n + s];
+    const int64_t T = plan_host[CM_PLAN_HEADER + 2 * n + s];
+    const bool whole_page = e <= off + T && (r0 - off) % B == 0;
+    const int32_t page = whole_page ? set->blocks_host[set->table_host[2 * i + 1] + (r0 - off) / B]
+                                    : -1;
+    for (int kv = 0; kv < 2; ++kv) {
+      int32_t* tab = kv ? v_table_host : k_table_host;
+      if (whole_page && (kv == 1 || off == 0)) {
+        tab[j] = page;
+      } else {
+        tab[j] = taken < n_free ? free_host[taken] : -1;
+        ++taken;
+        fresh_host[count++] = (int32_t)(2 * j + kv);
+      }
+    }
+  }
+  *n_fresh = count;
+  if (taken > n_free)
+    return fail(CM_EINVAL, "need " + std::to_string(taken) + " free pages, got " +
+                               std::to_string(n_free));
+  return CM_OK;
+}
+
+int32_t cm_paged_render(const cm_pagedset* set, const int64_t* plan_dev, const int64_t* plan_host,
+                        const cm_rope* rope, const int32_t* k_table_dev,
+                        const int32_t* v_table_dev, const int32_t* fresh_dev, int64_t n_fresh,
+                        void* workspace, size_t workspace_bytes, void* stream) {
+  g_err.clear();
+  cm::PagedDesc p;
+  int32_t st = check_pagedset(set, &p);
+  if (st != CM_OK) return st;
+  if ((st = check_rope(rope)) != CM_OK) return st;
+  int64_t nu = 0;
+  if ((st = check_plan_host(p.s, plan_host, &nu)) != CM_OK) return st;
+  if (!plan_dev || !aligned(plan_dev, 8)) return fail(CM_EINVAL, "plan_dev is NULL or misaligned");
+  const int64_t nbo = (plan_host[CM_PLAN_TOUT] + p.block - 1) / p.block;
+  if (n_fresh < 0 || n_fresh > 2 * nbo) return fail(CM_EINVAL, "n_fresh out of range");
+  if (n_fresh > 0 && (!fresh_dev || !k_table_dev || !v_table_dev))
+    return fail(CM_EINVAL, "fresh_dev / tables are NULL");
+  const size_t need = cm::align_up(sizeof(double) * (size_t)p.s.n * p.s.d, cm::kWsAlign);
+  if ((st = check_ws(workspace, workspace_bytes, need)) != CM_OK) return st;
+  hipError_t e = cm::launch_paged_render(p, plan_dev, (int32_t)nu, rope->base, rope->style,
+                                         k_table_dev, v_table_dev, fresh_dev, n_fresh,
+                                         static_cast<uint8_t*>(workspace),
+                                         static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? CM_OK : fail_hip(e, "cm_paged_render");
 }
 
 int32_t cm_timing_enable(int32_t on) {

@@ -142,6 +142,20 @@ hipError_t launch_render(const SetDesc& s, const RenderLayout& lay, const int64_
                          const RenderRange& rr, double base, int32_t style, bool check_on_device,
                          void* out, uint8_t* ws, hipStream_t stream);
 
+// Validated paged set (see cm_pagedset): s describes the fragments with a table
+// of 2 int64 per fragment {T, first page index}.
+struct PagedDesc {
+  SetDesc s;
+  int32_t block, b_shift;
+  int64_t pages;
+  void* pool;
+  const int32_t* blocks_dev;
+};
+hipError_t launch_paged_render(const PagedDesc& p, const int64_t* plan_dev, int32_t n_unique,
+                               double base, int32_t style, const int32_t* k_table,
+                               const int32_t* v_table, const int32_t* fresh, int64_t n_fresh,
+                               uint8_t* ws, hipStream_t stream);
+
 // Per-kernel event timing (no-op unless cm_timing_enable(1)).
 class ScopedTiming {
  public:
@@ -168,6 +182,7 @@ enum KernelId {
   K_RENDER_PREP,
   K_RENDER,
   K_RENDER_HASH,
+  K_PAGED,
   K_COUNT
 };
 

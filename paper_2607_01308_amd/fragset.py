@@ -23,8 +23,9 @@ import torch
 from . import _cabi as C
 from .binding import (FragmentBatch, bag_plan, canonical_order, equal_key_mask, fragment_hash,
                       fragment_hash_select, fragment_knorm, multiset_order, plan_elems,
-                      render_merge, render_merge_devplan, render_merge_hash,
-                      render_merge_range, workspace_size)
+                      paged_render, paged_tables, paged_workspace_size, render_merge,
+                      render_merge_devplan, render_merge_hash, render_merge_range, workspace_size)
+from .binding import PagedSet
 
 _WS: Dict[tuple, torch.Tensor] = {}
 _SIDE: Dict[torch.device, torch.cuda.Stream] = {}
@@ -383,3 +384,35 @@ class MergedCache:
         self.last_rows = T_out - (int(plan[C.PLAN_HEADER + n + first]) if first < n_u else T_out)
         self.slot_ids, self.T_out = slot_ids, T_out
         return self.cache
+
+
+@dataclass
+class PagedRender:
+    k_table: np.ndarray          # page id of each merged block of K (B rows)
+    v_table: np.ndarray          # the same for V
+    fresh: np.ndarray            # pages written by the render, as codes 2j + kv
+    T_out: int
+
+    @property
+    def reused_pages(self) -> int:
+        return 2 * len(self.k_table) - len(self.fresh)
+
+
+def render_paged(pset: PagedSet, plan_host: np.ndarray, free_pages, rope_base: float,
+                 style: str = "half", stream=None) -> PagedRender:
+    """Steps 4-5 over paged storage (§4.5): block tables that reuse every
+    fragment page a merged block equals (V of page-aligned slots, K only at
+    offset 0), and a render of the other pages into free_pages. plan_host: a
+    plan whose slots index pset's fragments (e.g. RenderResult.plan of the same
+    fragments in dense form, or bag_plan)."""
+    kt, vt, fresh = paged_tables(pset, plan_host, free_pages)
+    dev = pset.device
+    main = stream if stream is not None else torch.cuda.current_stream(dev)
+    with torch.cuda.stream(main):
+        ws = torch.empty(max(paged_workspace_size(pset), 256), dtype=torch.uint8, device=dev)
+        plan_dev = torch.from_numpy(np.ascontiguousarray(plan_host, dtype=np.int64)).to(dev)
+        kd, vd = torch.from_numpy(kt).to(dev), torch.from_numpy(vt).to(dev)
+        fd = torch.from_numpy(fresh).to(dev)
+        paged_render(pset, plan_dev, plan_host, rope_base, style, kd, vd, fd, ws, main)
+    return PagedRender(k_table=kt, v_table=vt, fresh=fresh,
+                       T_out=int(plan_host[C.PLAN_TOUT]))

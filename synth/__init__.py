@@ -20,8 +20,10 @@ from .configs import (  # noqa: F401
 from .generate import (  # noqa: F401
     TORCH_DTYPES,
     draw_tensor,
+    gather_paged,
     make_deliveries,
     make_fragments,
+    make_paged,
     tensor_to_numpy,
     to_numpy_cache,
 )

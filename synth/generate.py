@@ -81,3 +81,41 @@ def to_numpy_cache(cache) -> Tuple[str, list]:
     """Host copy of a legacy cache: (dtype name, [(K, V) numpy arrays])."""
     dtype = {torch.bfloat16: "bfloat16", torch.float32: "float32"}[cache[0][0].dtype]
     return dtype, [(tensor_to_numpy(K), tensor_to_numpy(V)) for K, V in cache]
+
+
+def make_paged(caches: Sequence, block: int, spare_pages: int, seed: int = 0, device=None):
+    """The same fragments stored in a page pool [L, 2, P, H, B, d] (pages of B
+    tokens of every head), each fragment on ceil(T / B) pages drawn at random from
+    the pool, plus `spare_pages` pages left free. Returns (pool, lengths,
+    page_lists, free_pages). Unused rows of a fragment's last page are zero."""
+    K0 = caches[0][0][0]
+    L, (_, H, _, d) = len(caches[0]), K0.shape
+    device = device if device is not None else K0.device
+    lengths = [int(c[0][0].shape[2]) for c in caches]
+    need = [(T + block - 1) // block for T in lengths]
+    P = sum(need) + spare_pages
+    perm = np.random.default_rng(seed).permutation(P)
+    pool = torch.zeros((L, 2, P, H, block, d), dtype=K0.dtype, device=device)
+    page_lists, k = [], 0
+    for c, T, nb in zip(caches, lengths, need):
+        pages = perm[k:k + nb].tolist()
+        k += nb
+        page_lists.append(pages)
+        idx = torch.tensor(pages, dtype=torch.long, device=device)
+        for l, (K, V) in enumerate(c):
+            for kv, x in enumerate((K, V)):
+                padded = torch.zeros((H, nb * block, d), dtype=x.dtype, device=device)
+                padded[:, :T] = x[0]
+                pool[l, kv, idx] = padded.reshape(H, nb, block, d).permute(1, 0, 2, 3)
+    free = perm[k:].tolist()
+    return pool, lengths, page_lists, free
+
+
+def gather_paged(pool: torch.Tensor, table, T: int) -> torch.Tensor:
+    """Dense [L, 2, 1, H, T, d] view-copy of a sequence stored on pages `table`
+    (one page id per B rows)."""
+    L, _, _, H, B, d = pool.shape
+    idx = torch.as_tensor(np.asarray(table, dtype=np.int64), device=pool.device)
+    pages = pool[:, :, idx]                                  # [L, 2, nb, H, B, d]
+    dense = pages.permute(0, 1, 3, 2, 4, 5).reshape(L, 2, H, -1, d)[:, :, :, :T]
+    return dense.unsqueeze(2).contiguous()

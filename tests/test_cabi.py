@@ -266,3 +266,95 @@ def test_render_range_argument_checks(lib):
     assert call(-1, 20) == C.CM_EINVAL
     assert call(0, 13) == C.CM_ESHAPE                       # capacity below T_out
     assert call(0, 20, plan=_plan(2, [1, 0], [9, 6])) == C.CM_ESHAPE
+
+
+class FakePaged:
+    """A cm_pagedset with dummy device addresses (host checks only)."""
+
+    def __init__(self, lengths, B=16, L=2, H=2, d=64, dtype=C.CM_BF16, spare=8, seed=0):
+        rng = np.random.default_rng(seed)
+        need = [(T + B - 1) // B for T in lengths]
+        self.P = sum(need) + spare
+        perm = rng.permutation(self.P).astype(np.int32)
+        self.pages, k = [], 0
+        for nb in need:
+            self.pages.append(perm[k:k + nb].tolist())
+            k += nb
+        self.free = perm[k:].astype(np.int32)
+        self.lengths = list(lengths)
+        self.B = B
+        self.table = np.array([[T, sum(need[:i])] for i, T in enumerate(lengths)], dtype=np.int64)
+        self.blocks = np.concatenate([np.array(p, dtype=np.int32) for p in self.pages])
+        self.s = C.CmPagedset(n=len(lengths), L=L, H=H, d=d, dtype=dtype, block=B, pages=self.P,
+                              pool_dev=0x100000, table_host=self.table.ctypes.data,
+                              table_dev=0x10000, blocks_host=self.blocks.ctypes.data,
+                              blocks_dev=0x20000, n_blocks=len(self.blocks))
+
+    @property
+    def ref(self):
+        return ctypes.byref(self.s)
+
+
+def _paged_tables(lib, fp, plan, free=None):
+    free = fp.free if free is None else np.asarray(free, dtype=np.int32)
+    nbo = (int(plan[3]) + fp.B - 1) // fp.B
+    kt, vt = np.full(nbo, -7, np.int32), np.full(nbo, -7, np.int32)
+    fresh = np.full(2 * nbo, -7, np.int32)
+    cnt = ctypes.c_int64(0)
+    st = lib.cm_paged_tables(fp.ref, plan.ctypes.data_as(ctypes.c_void_p),
+                             free.ctypes.data_as(ctypes.c_void_p), int(free.size),
+                             kt.ctypes.data_as(ctypes.c_void_p), vt.ctypes.data_as(ctypes.c_void_p),
+                             fresh.ctypes.data_as(ctypes.c_void_p), ctypes.byref(cnt))
+    return st, kt, vt, fresh[:cnt.value]
+
+
+@pytest.mark.parametrize("lengths,order", [((32, 48, 16), [1, 0, 2]),        # page-aligned slots
+                                           ((30, 50, 7, 64), [2, 0, 3, 1]),  # ragged
+                                           ((5,), [0])])
+def test_paged_tables_reuse_whole_pages(lib, lengths, order):
+    """Merged block j reuses fragment page blocks[(jB - off) / B] iff all its rows
+    come from one slot starting on one of that fragment's page boundaries (V),
+    and additionally the slot's offset is 0 (K, R(0) = I); every other block gets
+    a distinct free page, listed once in fresh as 2j + kv."""
+    fp = FakePaged(lengths, spare=64)
+    plan = _plan(len(lengths), order, [lengths[i] for i in order])
+    st, kt, vt, fresh = _paged_tables(lib, fp, plan)
+    assert st == C.CM_OK
+    B, T_out = fp.B, int(plan[3])
+    offs = [int(plan[4 + len(lengths) + s]) for s in range(len(order))]
+    expect_fresh = []
+    for j in range(len(kt)):
+        r0, e = j * B, min(j * B + B, T_out)
+        s = max(k for k in range(len(order)) if offs[k] <= r0)
+        i = order[s]
+        whole = e <= offs[s] + lengths[i] and (r0 - offs[s]) % B == 0
+        page = fp.pages[i][(r0 - offs[s]) // B] if whole else None
+        for kv, tab in ((0, kt), (1, vt)):
+            if whole and (kv == 1 or offs[s] == 0):
+                assert tab[j] == page
+            else:
+                assert tab[j] in set(fp.free.tolist())
+                expect_fresh.append(2 * j + kv)
+    assert fresh.tolist() == expect_fresh
+    used = [t for j, t in enumerate(kt) if 2 * j in expect_fresh] + \
+           [t for j, t in enumerate(vt) if 2 * j + 1 in expect_fresh]
+    assert len(set(used)) == len(used) == len(expect_fresh)
+
+
+def test_paged_tables_rejects(lib):
+    fp = FakePaged((30, 50), spare=64)
+    plan = _plan(2, [1, 0], [50, 30])
+    st, *_ = _paged_tables(lib, fp, plan, free=fp.free[:2])            # too few free pages
+    assert st == C.CM_EINVAL
+    st, *_ = _paged_tables(lib, fp, plan, free=[fp.pages[0][0]])        # a fragment's page
+    assert st == C.CM_EINVAL
+    st, *_ = _paged_tables(lib, fp, plan, free=[fp.free[0], fp.free[0]])
+    assert st == C.CM_EINVAL
+    st, *_ = _paged_tables(lib, fp, _plan(2, [1, 0], [50, 31]))         # wrong length
+    assert st == C.CM_ESHAPE
+    bad = FakePaged((30, 50), B=8, d=32)                                # 8 * 64 B < 1 KiB page
+    st, *_ = _paged_tables(lib, bad, plan)
+    assert st == C.CM_ESHAPE
+    fp.blocks[0] = fp.P                                                 # page outside the pool
+    st, *_ = _paged_tables(lib, fp, plan)
+    assert st == C.CM_EINVAL
