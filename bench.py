@@ -260,6 +260,42 @@ def main():
     ms_incr = sorted(incr_ms)[len(incr_ms) // 2]
     del mc, full
 
+    # paged render (§4.5): the distinct fragments on pages of 16 tokens; block
+    # tables reuse every whole fragment page they can, the kernel writes the rest
+    del S_with, S_without
+    torch.cuda.empty_cache()
+    res_set = S.render(w.routing_layer, w.rope_base)
+    set_plan = res_set.plan.copy()
+    del res_set
+    torch.cuda.empty_cache()
+    B = 16
+    pool, lengths, page_lists, free = synth.make_paged(distinct, B, spare_pages=2 * (
+        (w.merged_tokens + B - 1) // B + len(distinct)), seed=args.seed)
+    pset = cm.PagedSet(pool, lengths, page_lists)
+    for _ in range(2):
+        pr = cm.render_paged(pset, set_plan, free, w.rope_base)
+    torch.cuda.synchronize()
+    cm.timing_reset()
+    cm.timing_enable(True)
+    tp = time.perf_counter()
+    for _ in range(args.steps):
+        pr = cm.render_paged(pset, set_plan, free, w.rope_base)
+    torch.cuda.synchronize()
+    ms_paged = (time.perf_counter() - tp) / args.steps * 1e3
+    cm.timing_enable(False)
+    k_ms, k_n = cm.timing_query("paged")
+    cm.timing_reset()
+    page_bytes = w.L * w.H * B * w.d * (2 if w.dtype == "bfloat16" else 4)
+    paged_bytes = 2 * len(pr.fresh) * page_bytes
+    paged = {"ms": round(ms_paged, 4), "kernel_ms": round(k_ms / max(k_n, 1), 4),
+             "block_tokens": B, "merged_blocks": len(pr.k_table), "pages_written": len(pr.fresh),
+             "pages_reused": pr.reused_pages, "bytes": paged_bytes,
+             "bytes_vs_dense": round(paged_bytes / w.render_bytes, 4),
+             "kernel_GBps": round(paged_bytes / (k_ms / max(k_n, 1) / 1e3) / 1e9, 1),
+             "what": "block tables (host) + table upload + paged render kernel per step"}
+    del pool, pset, pr
+    torch.cuda.empty_cache()
+
     ms_step = (t1 - t0) / args.steps * 1e3
     ms_render_set = (t3 - t2) / args.steps * 1e3
     render_bytes = w.render_bytes
@@ -326,6 +362,7 @@ def main():
                        "kernels_ms": {k: round(v["total_ms"] / args.steps, 4)
                                       for k, v in set_kernels.items()}},
         "baselines": baselines,
+        "paged": paged,
         "incremental": {"ms": round(ms_incr, 4), "first_slot": first, "slots": len(distinct),
                         "rows_rendered": rows, "T_out": w.merged_tokens,
                         "bytes": incr_bytes, "GBps": round(incr_bytes / (ms_incr / 1e3) / 1e9, 1),

@@ -304,7 +304,8 @@ typedef struct {
  * otherwise it gets the next page of free_host, to be written by
  * cm_paged_render. Outputs (host, ceil(T_out / B) entries each): k_table_host,
  * v_table_host (page ids); fresh_host: the fresh pages to write as codes
- * 2j + kv (at most 2 ceil(T_out / B) entries), their count in *n_fresh.
+ * 2j + kv (at most 2 ceil(T_out / B) entries; K pages first, each kind in
+ * ascending page id), their count in *n_fresh.
  * Host only. CM_EINVAL if free_host has fewer than the pages needed (*n_fresh
  * then holds the number needed). */
 int32_t cm_paged_tables(const cm_pagedset* set, const int64_t* plan_host, const int32_t* free_host,

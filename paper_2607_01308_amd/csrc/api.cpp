@@ -553,6 +553,16 @@ int32_t check_pagedset(const cm_pagedset* set, cm::PagedDesc* out) {
   return CM_OK;
 }
 
+// Workspace of the paged render: angles, then 32 bytes per fresh page (at most
+// two per merged block of B rows, T_out at most the sum of the lengths).
+size_t paged_ws(const cm::PagedDesc& p) {
+  int64_t T_all = 0;
+  for (int i = 0; i < p.s.n; ++i) T_all += p.s.T(i);
+  const int64_t blocks = (T_all + p.block - 1) / p.block;
+  return cm::align_up(sizeof(double) * (size_t)p.s.n * p.s.d, cm::kWsAlign) +
+         cm::align_up(32 * 2 * (size_t)blocks, cm::kWsAlign);
+}
+
 // Plan checks against the fragments' lengths (slots, lengths, prefix offsets).
 int32_t check_plan_host(const cm::SetDesc& s, const int64_t* plan_host, int64_t* nu_out) {
   if (!plan_host) return fail(CM_EINVAL, "plan_host is NULL");
@@ -585,7 +595,7 @@ int32_t cm_paged_workspace_size(const cm_pagedset* set, size_t* bytes_out) {
   int32_t st = check_pagedset(set, &p);
   if (st != CM_OK) return st;
   if (!bytes_out) return fail(CM_EINVAL, "bytes_out is NULL");
-  *bytes_out = cm::align_up(sizeof(double) * (size_t)p.s.n * p.s.d, cm::kWsAlign);
+  *bytes_out = paged_ws(p);
   return CM_OK;
 }
 
@@ -637,6 +647,13 @@ int32_t cm_paged_tables(const cm_pagedset* set, const int64_t* plan_host, const 
     }
   }
   *n_fresh = count;
+  if (taken <= n_free) {
+    std::sort(fresh_host, fresh_host + count, [&](int32_t a, int32_t b) {
+      const int32_t pa = (a & 1 ? v_table_host : k_table_host)[a >> 1];
+      const int32_t pb = (b & 1 ? v_table_host : k_table_host)[b >> 1];
+      return (a & 1) != (b & 1) ? (a & 1) < (b & 1) : pa < pb;
+    });
+  }
   if (taken > n_free)
     return fail(CM_EINVAL, "need " + std::to_string(taken) + " free pages, got " +
                                std::to_string(n_free));
@@ -659,8 +676,7 @@ int32_t cm_paged_render(const cm_pagedset* set, const int64_t* plan_dev, const i
   if (n_fresh < 0 || n_fresh > 2 * nbo) return fail(CM_EINVAL, "n_fresh out of range");
   if (n_fresh > 0 && (!fresh_dev || !k_table_dev || !v_table_dev))
     return fail(CM_EINVAL, "fresh_dev / tables are NULL");
-  const size_t need = cm::align_up(sizeof(double) * (size_t)p.s.n * p.s.d, cm::kWsAlign);
-  if ((st = check_ws(workspace, workspace_bytes, need)) != CM_OK) return st;
+  if ((st = check_ws(workspace, workspace_bytes, paged_ws(p))) != CM_OK) return st;
   hipError_t e = cm::launch_paged_render(p, plan_dev, (int32_t)nu, rope->base, rope->style,
                                          k_table_dev, v_table_dev, fresh_dev, n_fresh,
                                          static_cast<uint8_t*>(workspace),

@@ -335,7 +335,9 @@ def test_paged_tables_reuse_whole_pages(lib, lengths, order):
             else:
                 assert tab[j] in set(fp.free.tolist())
                 expect_fresh.append(2 * j + kv)
-    assert fresh.tolist() == expect_fresh
+    assert sorted(fresh.tolist()) == sorted(expect_fresh)
+    page_of = [(c & 1, int((vt if c & 1 else kt)[c >> 1])) for c in fresh.tolist()]
+    assert page_of == sorted(page_of)                     # K pages first, ascending page ids
     used = [t for j, t in enumerate(kt) if 2 * j in expect_fresh] + \
            [t for j, t in enumerate(vt) if 2 * j + 1 in expect_fresh]
     assert len(set(used)) == len(used) == len(expect_fresh)
