@@ -119,16 +119,17 @@ def tensor_leaves(buf) -> List[bytes]:
     leaves = []
     for s0 in range(0, n, STRIPE_BYTES):
         stripe = raw[s0:s0 + STRIPE_BYTES]
-        parts = [[] for _ in range(min(STRIPE_LEAVES, stripe.size // BLOCK_BYTES))]
-        for t0 in range(0, stripe.size, STEP_BYTES):
-            step = stripe[t0:t0 + STEP_BYTES]
-            if step.size == STEP_BYTES:
-                blocks = step.reshape(4, STRIPE_LEAVES, PIECE_BYTES).transpose(1, 0, 2)
-            else:
-                blocks = step.reshape(-1, BLOCK_BYTES)
-            for k in range(blocks.shape[0]):
-                parts[k].append(blocks[k].tobytes())
-        leaves.extend(b"".join(p) for p in parts)
+        n_full = stripe.size // STEP_BYTES
+        # full steps as [step][piece group j][leaf k][16 bytes]; leaf k's blocks
+        # are the pieces k + 64 j of each step, so [k][step][j] is its message
+        full = stripe[:n_full * STEP_BYTES].reshape(n_full, 4, STRIPE_LEAVES, PIECE_BYTES)
+        by_leaf = full.transpose(2, 0, 1, 3)
+        last = stripe[n_full * STEP_BYTES:].reshape(-1, BLOCK_BYTES)   # shorter final step
+        for k in range(min(STRIPE_LEAVES, stripe.size // BLOCK_BYTES)):
+            msg = by_leaf[k].tobytes() if n_full else b""
+            if k < last.shape[0]:
+                msg += last[k].tobytes()
+            leaves.append(msg)
     return leaves
 
 
