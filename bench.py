@@ -5,7 +5,10 @@ the Id of every delivery whose score collides with another's, dedupe
 + canonical order + offsets, one small device-to-host plan copy, output
 allocation, then the fused kernel that renders the merged cache and computes
 the remaining Ids from the same loads. Inputs are resident in HBM before timing
-starts.
+starts. A workload smaller than 1 GiB of deliveries (four times the 256 MiB
+Infinity Cache) is replicated and successive steps take successive copies, so
+its reads come from HBM; `step_ms_p10_p50_p90` gives the spread of the timed
+steps (HIP events between steps).
 
 value = merged-cache bytes read + written per step (2 x the bytes of the
 distinct fragments) / step time, in GB/s; merges_per_s = 1 / step time.
@@ -38,6 +41,8 @@ HBM_PEAK_GBPS = 8000.0                 # MI355X HBM3E
 VALU_PEAK_TOPS = 256 * 64 * 2.4e9 / 1e12  # 256 CUs x 64 lanes x 2.4 GHz: one 32-bit or fp64 op
 B2S_OPS_PER_BLOCK = 960                # 10 rounds x 8 G x 12 VALU ops (add3, add, xor, alignbit)
 ROT_OPS_PER_ELEM = 5                   # widen, 2 fp64 products, 1 fp64 add/sub, narrow
+MALL_BYTES = 256 << 20                 # MI355X Infinity Cache: inputs smaller than 4x this are
+ROTATE_TARGET = 4 * MALL_BYTES         # replicated and the steps cycle through the copies
 
 # source files each timed kernel is built from: a traffic summary is only used
 # while these are unchanged
@@ -83,6 +88,12 @@ def fused_work(w, r, mask):
 def delivered_bytes(w):
     """Bytes of every delivery (duplicates counted): what the naive render moves each way."""
     return w.delivery_bytes
+
+
+def percentiles(ms):
+    """p10, p50, p90 of per-step times (nearest rank)."""
+    v = sorted(ms)
+    return [round(v[min(len(v) - 1, int(q * len(v)))], 4) for q in (0.1, 0.5, 0.9)]
 
 
 def cpu_baseline(w, frags):
@@ -144,10 +155,19 @@ def main():
     frags = synth.make_fragments(w, device=dev)
     deliveries = synth.make_deliveries(w, frags)
     batch = cm.FragmentBatch(deliveries)
+    # a workload that would sit in the Infinity Cache is replicated, each step
+    # taking the next copy, so every step reads its inputs from HBM
+    n_copies = max(1, min(32, -(-ROTATE_TARGET // w.delivery_bytes)))
+    copies = [deliveries] + [[tuple((K.clone(), V.clone()) for K, V in c) for c in deliveries]
+                             for _ in range(n_copies - 1)]
+    batches = [batch] + [cm.FragmentBatch(c) for c in copies[1:]]
     torch.cuda.synchronize()
+    k_step = [0]
 
     def step():
-        return cm.render_deliveries(batch, w.routing_layer, w.rope_base)
+        b = batches[k_step[0] % n_copies]
+        k_step[0] += 1
+        return cm.render_deliveries(b, w.routing_layer, w.rope_base)
 
     for _ in range(args.warmup):
         r = step()
@@ -155,15 +175,22 @@ def main():
     torch.cuda.synchronize()
     print("[bench] warmup done", file=sys.stderr, flush=True)
 
+    def events(n):
+        return [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
+
     cm.timing_reset()
     cm.timing_enable(True)
+    ev = events(args.steps)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(args.steps):
+    ev[0].record()
+    for i in range(args.steps):
         r = step()
+        ev[i + 1].record()
         del r
     torch.cuda.synchronize()
     t1 = time.perf_counter()
+    step_pct = percentiles([ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps)])
     cm.timing_enable(False)
     per_kernel = {}
     for k in cm.KERNELS:
@@ -173,19 +200,26 @@ def main():
     cm.timing_reset()
 
     # steps 2-5 on the ingested set (ids already computed at Ingest, Alg. 2)
-    S = cm.LatentFragmentSet()
-    S.ingest_many(deliveries)
-    for _ in range(2):
-        S.render(w.routing_layer, w.rope_base)
+    sets = []
+    for c in copies:
+        sets.append(cm.LatentFragmentSet())
+        sets[-1].ingest_many(c)
+    S = sets[0]
+    for i in range(2):
+        sets[i % n_copies].render(w.routing_layer, w.rope_base)
     torch.cuda.synchronize()
     cm.timing_reset()
     cm.timing_enable(True)
+    ev = events(args.steps)
     t2 = time.perf_counter()
-    for _ in range(args.steps):
-        r = S.render(w.routing_layer, w.rope_base)
+    ev[0].record()
+    for i in range(args.steps):
+        r = sets[i % n_copies].render(w.routing_layer, w.rope_base)
+        ev[i + 1].record()
         del r
     torch.cuda.synchronize()
     t3 = time.perf_counter()
+    set_pct = percentiles([ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps)])
     cm.timing_enable(False)
     set_kernels = {}
     for k in cm.KERNELS:
@@ -197,22 +231,22 @@ def main():
     # the paper's baselines over the same render: the naive multiset re-render
     # (§5.9, every delivery its own operand) and BagMerge in delivery order (§4.2)
     def timed(fn):
-        for _ in range(2):
-            r = fn()
+        for i in range(2):
+            r = fn(batches[i % n_copies])
             del r
         torch.cuda.synchronize()
         ta = time.perf_counter()
-        for _ in range(args.steps):
-            r = fn()
+        for i in range(args.steps):
+            r = fn(batches[i % n_copies])
             T = r.T_out
             del r
         torch.cuda.synchronize()
         return (time.perf_counter() - ta) / args.steps * 1e3, T
 
     multiset_bytes = 2 * delivered_bytes(w)
-    ms_naive, T_naive = timed(lambda: cm.render_multiset(batch, w.routing_layer, w.rope_base))
+    ms_naive, T_naive = timed(lambda b: cm.render_multiset(b, w.routing_layer, w.rope_base))
     order = list(range(batch.n))
-    ms_bag, T_bag = timed(lambda: cm.bag_merge(batch, order, w.rope_base))
+    ms_bag, T_bag = timed(lambda b: cm.bag_merge(b, order, w.rope_base))
     baselines = {
         "naive_multiset": {"ms": round(ms_naive, 4), "T_out": T_naive,
                            "GBps": round(multiset_bytes / (ms_naive / 1e3) / 1e9, 1),
@@ -262,7 +296,7 @@ def main():
 
     # paged render (§4.5): the distinct fragments on pages of 16 tokens; block
     # tables reuse every whole fragment page they can, the kernel writes the rest
-    del S_with, S_without
+    del S_with, S_without, sets[1:], batches[1:], copies[1:]
     torch.cuda.empty_cache()
     res_set = S.render(w.routing_layer, w.rope_base)
     set_plan = res_set.plan.copy()
@@ -306,7 +340,7 @@ def main():
     delivered = w.delivery_bytes
     rooflines = {}
     if "render_hash" in per_kernel:
-        r = step()
+        r = cm.render_deliveries(batch, w.routing_layer, w.rope_base)
         keys = torch.empty(batch.n, dtype=torch.float64, device=dev)
         mask = torch.empty(batch.n, dtype=torch.uint8, device=dev)
         ws = torch.empty(cm.workspace_size(batch), dtype=torch.uint8, device=dev)
@@ -339,6 +373,7 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms_step, 4),
+        "step_ms_p10_p50_p90": step_pct,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -348,13 +383,13 @@ def main():
                    "merged_tokens": w.merged_tokens, "layers": w.L, "kv_heads": w.H,
                    "head_dim": w.d, "routing_layer": w.routing_layer, "rope_base": w.rope_base,
                    "render_bytes": render_bytes, "delivery_bytes": delivered,
-                   "parallelism": "single GPU"},
+                   "input_copies": n_copies, "parallelism": "single GPU"},
         "pct_hbm_peak": round(100 * value / HBM_PEAK_GBPS, 2),
         "merges_per_s": round(1e3 / ms_step, 3),
         "roofline": dict(rooflines.get(dom, {}), kernel=dom) if dom in rooflines else None,
         "roofline_render": rooflines.get("render"),
         "kernels_ms_per_step": {k: round(v["total_ms"] / args.steps, 4) for k, v in per_kernel.items()},
-        "render_set": {"ms": round(ms_render_set, 4),
+        "render_set": {"ms": round(ms_render_set, 4), "ms_p10_p50_p90": set_pct,
                        "GBps": round(render_bytes / (ms_render_set / 1e3) / 1e9, 1),
                        "pct_hbm_peak": round(100 * render_bytes / (ms_render_set / 1e3) / 1e9
                                              / HBM_PEAK_GBPS, 2),
