@@ -18,7 +18,7 @@ computed at ingest), the path whose bytes are all HBM streaming.
 Prints one JSON line. `roofline` is for the kernel with the largest share of
 the step, measured with per-kernel HIP events on the launch stream over the
 timed steps: the fused hash+render kernel against the VALU issue rate (its
-algorithmic operations: 960 per hashed 64-byte block, 5 per rotated K
+algorithmic operations: 672 per hashed 64-byte block, 5 per rotated K
 element). `roofline_render` gives the render kernel of `render_set` against
 HBM bandwidth. `cpu_baseline` times the CPU oracle on a bounded sample of the
 same workload.
@@ -39,7 +39,7 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBPS = 8000.0                 # MI355X HBM3E
 VALU_PEAK_TOPS = 256 * 64 * 2.4e9 / 1e12  # 256 CUs x 64 lanes x 2.4 GHz: one 32-bit or fp64 op
-B2S_OPS_PER_BLOCK = 960                # 10 rounds x 8 G x 12 VALU ops (add3, add, xor, alignbit)
+B3_OPS_PER_BLOCK = 672                 # BLAKE3: 7 rounds x 8 G x 12 VALU ops (add3, add, xor, alignbit)
 ROT_OPS_PER_ELEM = 5                   # widen, 2 fp64 products, 1 fp64 add/sub, narrow
 MALL_BYTES = 256 << 20                 # MI355X Infinity Cache: inputs smaller than 4x this are
 ROTATE_TARGET = 4 * MALL_BYTES         # replicated and the steps cycle through the copies
@@ -47,7 +47,8 @@ ROTATE_TARGET = 4 * MALL_BYTES         # replicated and the steps cycle through 
 # source files each timed kernel is built from: a traffic summary is only used
 # while these are unchanged
 KERNEL_SOURCES = {
-    "render_hash": ["render_hash.hip", "rotate.h", "blake2s.h", "stream_ops.h", "internal.h"],
+    "render_hash": ["render_hash.hip", "rotate.h", "blake3.h", "chunk_ops.h", "stream_ops.h",
+                    "internal.h"],
     "render": ["render.hip", "rotate.h", "stream_ops.h", "internal.h"],
 }
 
@@ -82,7 +83,7 @@ def fused_work(w, r, mask):
     hashed_blocks = sum(2 * tok * T * esize // 64 for i, T in zip(r.order, r.lengths)
                         if int(mask[i]) == 0)
     rotated = sum(tok * T for off, T in zip(r.offsets, r.lengths) if off != 0)
-    return B2S_OPS_PER_BLOCK * hashed_blocks + ROT_OPS_PER_ELEM * rotated, hashed_blocks * 64, rotated
+    return B3_OPS_PER_BLOCK * hashed_blocks + ROT_OPS_PER_ELEM * rotated, hashed_blocks * 64, rotated
 
 
 def delivered_bytes(w):

@@ -130,19 +130,15 @@ int32_t cm_workspace_size(const cm_fragset* set, size_t* bytes_out);
 /* ---------------------------------------------------------------- step 1
  * Id of Alg. 2 (content address; also the hash tiebreak of §4.3): for every
  * fragment, a 32-byte digest of its shapes, dtype and the raw bytes of
- * K^0, V^0, ..., K^{L-1}, V^{L-1} in that order. Function: per tensor a BLAKE2s-256
- * (RFC 7693) binary tree (fanout 2, depth 255, leaf 4096, inner 32) over striped
- * leaves: the tensor is cut into stripes of 256 KiB and each stripe into steps of
- * 4 KiB (the last of each may be shorter); stripe s has min(64, its 64-byte
- * blocks) leaves, and in every step leaf 64*s + k takes one 64-byte message
- * block: the 16-byte pieces k, k+64, k+128, k+192 of a full step, or block k of
- * a shorter final step; leaf j is hashed with
- * node_offset j, depth 0; parent j at level v with node_offset j, depth v,
- * children 2j and 2j+1; last_node on the last node of each level; an unpaired
- * last node is carried up unchanged. Then a sequential BLAKE2s-256 of a 64-byte
- * header (magic "CMFRAG01", u32 dtype code 0=fp32 1=bf16, u32 element bytes,
- * u32 L, u32 batch=1, u32 H, u64 T, u32 d, zero pad; little-endian) followed by
- * the 2L tensor roots.
+ * K^0, V^0, ..., K^{L-1}, V^{L-1} in that order. Function: BLAKE3-256 (unkeyed
+ * hash mode of the BLAKE3 specification). Per tensor, the root is the BLAKE3 of
+ * its bytes in a fixed order: every full 64 KiB stripe s is cut into 16 steps of
+ * 4 KiB and each step into 16-byte pieces; chunk 64*s + k of the message (1 KiB,
+ * the BLAKE3 chunk) is, for each step of the stripe in turn, its pieces k, k+64,
+ * k+128, k+192. The bytes after the last full stripe follow in their own order.
+ * Then the Id is the BLAKE3-256 of a 64-byte header (magic "CMFRAG01", u32 dtype
+ * code 0=fp32 1=bf16, u32 element bytes, u32 L, u32 batch=1, u32 H, u64 T, u32 d,
+ * zero pad; little-endian) followed by the 2L tensor roots.
  * digests_dev: device, n * 32 bytes, written in delivery order. */
 int32_t cm_fragment_hash(const cm_fragset* set, uint8_t* digests_dev,
                          void* workspace, size_t workspace_bytes, void* stream);

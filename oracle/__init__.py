@@ -7,10 +7,12 @@ nothing from it; the product path never calls it.
 """
 
 from .cmerge_oracle import (  # noqa: F401
-    LEAF_BYTES,
+    CHUNK_BYTES,
+    STRIPE_BYTES,
     Fragment,
     FragmentSet,
     bf16_bits_to_f64,
+    blake3,
     canonical_merge,
     canonical_order,
     f64_to_bf16_bits,
@@ -27,5 +29,6 @@ from .cmerge_oracle import (  # noqa: F401
     rope_inv_freq,
     rotate_pairs,
     round_to_dtype,
+    tensor_message,
     tensor_root,
 )

@@ -1,16 +1,16 @@
 """CPU oracle: CanonicalMerge render of a LatentFragmentSet, written from the paper.
 
-TEST INFRASTRUCTURE ONLY (see the package docstring). Plain Python + numpy +
-hashlib, fp64 for every floating-point step, no blocking or fusion.
+TEST INFRASTRUCTURE ONLY (see the package docstring). Plain Python + numpy,
+plus a plain C BLAKE3 (blake3_ref.c, loaded through ctypes); fp64 for every
+floating-point step, no blocking or fusion.
 
 What each function follows:
   * fragment_id / tensor_root / fragment_header: the content address Id of
     Alg. 2 (§4.5) and the hash tiebreak of §4.3 ("shapes, dtypes and raw bytes
     of every layer's K and V", order K1,V1,...,KL,VL, unshifted). The paper names
-    no hash function; the reading used here is BLAKE2s-256 (RFC 7693) in tree
-    mode over striped leaves of at most 4 KiB per tensor (see tensor_leaves),
-    then a sequential BLAKE2s over a 64-byte shape/dtype header followed by the
-    tensor roots.
+    no hash function; the reading used here is BLAKE3-256 of each tensor's
+    bytes in a fixed interleaved order (see tensor_message), then BLAKE3-256
+    of a 64-byte shape/dtype header followed by the tensor roots.
   * FragmentSet: Ingest and Merge of Alg. 2 — set union keyed by Id, Eq. (5).
   * fragment_key / mean_knorm: Eq. (3) (§4.3) and Alg. 1 — mean L2 norm of the
     routing layer's K rows over the last T* = min_j T_j positions, averaged over
@@ -31,20 +31,22 @@ What each function follows:
 
 from __future__ import annotations
 
-import hashlib
+import ctypes
+import os
 import struct
 from dataclasses import dataclass
 from typing import Dict, Iterable, List, Sequence, Tuple
 
 import numpy as np
 
-LEAF_BYTES = 4096          # tree-hash leaf size (bytes), the maximum
-BLOCK_BYTES = 64           # BLAKE2s message block
+CHUNK_BYTES = 1024         # BLAKE3 chunk
+BLOCK_BYTES = 64           # BLAKE3 message block
 PIECE_BYTES = 16           # interleave granularity inside a step
-STRIPE_LEAVES = 64         # leaves interleaved in one stripe
-STEP_BYTES = STRIPE_LEAVES * BLOCK_BYTES    # 4 KiB: one block of every leaf
-STRIPE_BYTES = STRIPE_LEAVES * LEAF_BYTES   # 256 KiB
-_DIGEST = 32               # BLAKE2s-256
+STRIPE_CHUNKS = 64         # chunks interleaved in one stripe
+STEP_BYTES = STRIPE_CHUNKS * BLOCK_BYTES    # 4 KiB: one block of every chunk
+STRIPE_STEPS = CHUNK_BYTES // BLOCK_BYTES   # 16
+STRIPE_BYTES = STRIPE_CHUNKS * CHUNK_BYTES  # 64 KiB
+_DIGEST = 32               # BLAKE3-256
 # dtype -> (header code, element bytes)
 _DTYPE_INFO = {"float32": (0, 4), "bfloat16": (1, 2)}
 _MAGIC = b"CMFRAG01"
@@ -89,73 +91,54 @@ class Fragment:
 
 # --------------------------------------------------------------------------- Id (Alg. 2)
 
-def _blake2s_node(data, node_offset: int, node_depth: int, last_node: bool) -> bytes:
-    """One node of the binary hash tree: BLAKE2s-256 with tree parameters
-    (fanout 2, unlimited depth, 4 KiB leaves, 32-byte inner digests)."""
-    return hashlib.blake2s(data, digest_size=_DIGEST, fanout=2, depth=255,
-                           leaf_size=LEAF_BYTES, node_offset=node_offset,
-                           node_depth=node_depth, inner_size=_DIGEST,
-                           last_node=last_node).digest()
+_B3_LIB = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libblake3_ref.so")
+_b3 = None
 
 
-def tensor_leaves(buf) -> List[bytes]:
-    """Leaf messages of one tensor, in leaf order.
+def _b3_lib():
+    global _b3
+    if _b3 is None:
+        if not os.path.exists(_B3_LIB):
+            raise RuntimeError(f"{_B3_LIB} is missing: build it with oracle/build_native.py "
+                               "(__graft_entry__.build() does)")
+        lib = ctypes.CDLL(_B3_LIB)
+        lib.oracle_blake3.argtypes = [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_char_p]
+        lib.oracle_blake3.restype = None
+        _b3 = lib
+    return _b3
 
-    The raw bytes (a multiple of 64) are cut into stripes of 256 KiB (the last
-    may be shorter) and each stripe into steps of 4 KiB (the last may be
-    shorter). A stripe has min(64, its 64-byte blocks) leaves; in every step each
-    leaf k takes one 64-byte message block:
-      * full 4 KiB step: the 16-byte pieces k, k+64, k+128, k+192 of the step,
-        in that order;
-      * shorter final step of m blocks: block k of the step (k < m), unchanged.
-    Leaf k's message is its blocks in step order; leaves are numbered stripe by
-    stripe: leaf index = 64 * stripe + k."""
+
+def blake3(data) -> bytes:
+    """BLAKE3-256 (unkeyed hash mode) of a byte string, computed by the plain C
+    implementation in blake3_ref.c, written from the BLAKE3 specification."""
+    raw = np.ascontiguousarray(np.frombuffer(memoryview(data).cast("B"), dtype=np.uint8))
+    out = ctypes.create_string_buffer(_DIGEST)
+    _b3_lib().oracle_blake3(raw.ctypes.data if raw.size else None, raw.size, out)
+    return out.raw
+
+
+def tensor_message(buf) -> np.ndarray:
+    """The byte string whose BLAKE3 is the tensor's root: the tensor's raw bytes
+    (a multiple of 64) in a fixed order.
+
+    Every full stripe of 64 KiB is cut into 16 steps of 4 KiB, each step into
+    256 pieces of 16 bytes; chunk 64 s + k of the message (1 KiB, the BLAKE3
+    chunk size) is, for steps 0..15 of stripe s in turn, the pieces k, k+64,
+    k+128, k+192 of that step. The bytes after the last full stripe follow
+    unchanged."""
     raw = np.frombuffer(memoryview(buf).cast("B"), dtype=np.uint8)
     n = raw.size
-    if n == 0:
-        return [b""]
     if n % BLOCK_BYTES:
         raise ValueError("tensor bytes must be a multiple of 64")
-    leaves = []
-    for s0 in range(0, n, STRIPE_BYTES):
-        stripe = raw[s0:s0 + STRIPE_BYTES]
-        n_full = stripe.size // STEP_BYTES
-        # full steps as [step][piece group j][leaf k][16 bytes]; leaf k's blocks
-        # are the pieces k + 64 j of each step, so [k][step][j] is its message
-        full = stripe[:n_full * STEP_BYTES].reshape(n_full, 4, STRIPE_LEAVES, PIECE_BYTES)
-        by_leaf = full.transpose(2, 0, 1, 3)
-        last = stripe[n_full * STEP_BYTES:].reshape(-1, BLOCK_BYTES)   # shorter final step
-        for k in range(min(STRIPE_LEAVES, stripe.size // BLOCK_BYTES)):
-            msg = by_leaf[k].tobytes() if n_full else b""
-            if k < last.shape[0]:
-                msg += last[k].tobytes()
-            leaves.append(msg)
-    return leaves
+    n_full = n // STRIPE_BYTES
+    # [stripe][step][piece group j][lane k][16 bytes] -> [stripe][k][step][j][16 bytes]
+    head = raw[:n_full * STRIPE_BYTES].reshape(n_full, STRIPE_STEPS, 4, STRIPE_CHUNKS, PIECE_BYTES)
+    return np.concatenate([head.transpose(0, 3, 1, 2, 4).reshape(-1), raw[n_full * STRIPE_BYTES:]])
 
 
 def tensor_root(buf) -> bytes:
-    """Root of the binary tree over one tensor's leaves (tensor_leaves).
-
-    Level 0: leaf k hashed with node_offset=k, node_depth=0, last_node on the
-    last leaf. Level l >= 1: node j hashes the concatenated digests of children
-    2j and 2j+1 (node_offset=j, node_depth=l, last_node on the last node of the
-    level); an unpaired last child is carried up unchanged. The single node left
-    is the root."""
-    leaves = tensor_leaves(buf)
-    nleaves = len(leaves)
-    level = [_blake2s_node(leaf, k, 0, k == nleaves - 1) for k, leaf in enumerate(leaves)]
-    depth = 0
-    while len(level) > 1:
-        depth += 1
-        m = (len(level) + 1) // 2
-        nxt = []
-        for j in range(m):
-            if 2 * j + 1 < len(level):
-                nxt.append(_blake2s_node(level[2 * j] + level[2 * j + 1], j, depth, j == m - 1))
-            else:
-                nxt.append(level[2 * j])
-        level = nxt
-    return level[0]
+    """Root of one tensor: BLAKE3-256 of tensor_message(buf)."""
+    return blake3(tensor_message(buf))
 
 
 def fragment_header(dtype: str, L: int, H: int, T: int, d: int) -> bytes:
@@ -167,7 +150,7 @@ def fragment_header(dtype: str, L: int, H: int, T: int, d: int) -> bytes:
 
 
 def fragment_id_from_roots(header: bytes, roots: Sequence[bytes]) -> bytes:
-    return hashlib.blake2s(header + b"".join(roots), digest_size=_DIGEST).digest()
+    return blake3(header + b"".join(roots))
 
 
 def fragment_id(frag: Fragment) -> bytes:

@@ -1,7 +1,7 @@
 """Build libcmerge.so (the HIP kernels + C ABI) in-tree for gfx950 with hipcc.
 
 Also builds tests/native/libcm_hostcheck.so, a CPU-side harness the tests use
-to run the library's BLAKE2s code on the host."""
+to run the library's BLAKE3 code on the host."""
 
 from __future__ import annotations
 

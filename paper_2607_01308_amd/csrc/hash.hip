@@ -1,19 +1,18 @@
 // Step 1 — content address Id of Alg. 2 (also the hash tiebreak of §4.3).
 //
-// Per tensor, a BLAKE2s-256 binary tree over striped leaves; per fragment, a
-// sequential BLAKE2s-256 of a 64-byte shape/dtype header followed by the 2L
-// tensor roots (K^0, V^0, ..., K^{L-1}, V^{L-1}). A tensor is cut into stripes
-// of 256 KiB and steps of 4 KiB; in every step each of the stripe's 64 leaves
-// takes one 64-byte block: leaf k the 16-byte pieces k, k+64, k+128, k+192 (a
-// shorter final step keeps block k whole). That layout is chosen for 64-wide
-// wavefronts: one wave takes one stripe, lane k hashes leaf k (64 dependent
-// compressions with the next blocks in flight), and each of the four 16-byte
-// loads of a step reads 1 KiB of contiguous memory across the wave. The work is
-// VALU-bound (12 VALU ops per G step, 960 per block); each upper tree level is
-// one launch over all tensors at full lane occupancy (the parents add 1/64 of
-// the leaf work).
-#include "blake2s.h"
-#include "internal.h"
+// Per tensor, BLAKE3-256 of its bytes in a fixed interleaved order; per
+// fragment, BLAKE3-256 of a 64-byte shape/dtype header followed by the 2L
+// tensor roots (K^0, V^0, ..., K^{L-1}, V^{L-1}). In every full 64 KiB stripe of
+// a tensor, chunk 64 s + k (1 KiB, the BLAKE3 chunk) is made of the 16-byte
+// pieces k, k+64, k+128, k+192 of each of the stripe's 16 steps of 4 KiB; the
+// bytes after the last full stripe keep their order. That order is chosen for
+// 64-wide wavefronts: one wave takes one stripe, lane k hashes chunk k (16
+// dependent compressions with the next blocks in flight), and each of the four
+// 16-byte loads of a step reads 1 KiB of contiguous memory across the wave. The
+// work is VALU-bound (12 VALU ops per G step, 672 per block); each upper tree
+// level is one launch over all tensors at full lane occupancy (the parents add
+// 1/16 of the chunk work).
+#include "chunk_ops.h"
 
 namespace cm {
 
@@ -25,42 +24,19 @@ constexpr int kBlock = 256;
 #endif
 constexpr int kLeafBlocksPerCu = CM_HASH_BLOCKS_PER_CU;
 
-__device__ __forceinline__ void load64(const uint8_t* p, uint32_t (&m)[16]) {
-  const CM_GLOBAL u32x4* q = global_ptr<u32x4>(p);
+// Block j of chunk `lane` of a full stripe starting at p: the 16-byte pieces
+// lane, lane+64, lane+128, lane+192 of step j.
+__device__ __forceinline__ void load_stripe_block(const uint8_t* p, int lane, int64_t j,
+                                                  uint32_t (&m)[16]) {
+  const CM_GLOBAL u32x4* q = global_ptr<u32x4>(p + (j << 12) + lane * 16);
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
-    const u32x4 v = q[k];
+    const u32x4 v = q[k * 64];
     m[4 * k + 0] = v[0];
     m[4 * k + 1] = v[1];
     m[4 * k + 2] = v[2];
     m[4 * k + 3] = v[3];
   }
-}
-
-// Block of leaf `lane` in step j of a stripe starting at p: the 16-byte pieces
-// lane, lane+64, lane+128, lane+192 of a full step; block `lane` of the final
-// short step (j == full_steps).
-__device__ __forceinline__ void load_leaf_block(const uint8_t* p, int lane, int64_t j,
-                                               int64_t full_steps, uint32_t (&m)[16]) {
-  if (j < full_steps) {
-    const CM_GLOBAL u32x4* q = global_ptr<u32x4>(p + (j << 12) + lane * 16);
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const u32x4 v = q[k * 64];
-      m[4 * k + 0] = v[0];
-      m[4 * k + 1] = v[1];
-      m[4 * k + 2] = v[2];
-      m[4 * k + 3] = v[3];
-    }
-  } else {
-    load64(p + (j << 12) + lane * 64, m);
-  }
-}
-
-__device__ __forceinline__ void store_digest(uint8_t* out, const B2sState& s) {
-  uint4* q = reinterpret_cast<uint4*>(out);
-  q[0] = make_uint4(s.h[0], s.h[1], s.h[2], s.h[3]);
-  q[1] = make_uint4(s.h[4], s.h[5], s.h[6], s.h[7]);
 }
 
 // Largest i in [0, n) with base[i] <= g (bases strictly increase).
@@ -75,7 +51,7 @@ __device__ __forceinline__ int find_fragment(const int64_t* __restrict__ base, i
 
 // base[v][i] = number of level-v nodes of fragments 0..i-1 (all 2L tensors each);
 // base[v][n] = total nodes at level v; row levels+1 holds the same prefix sums
-// of the (tensor, stripe) tasks of the leaf kernel. One workgroup, block-wide
+// of the (tensor, stripe) tasks of the chunk kernel. One workgroup, block-wide
 // inclusive scans.
 __global__ __launch_bounds__(1024) void hash_prep_kernel(const int64_t* __restrict__ table,
                                                          int32_t n, int64_t stride,
@@ -85,7 +61,7 @@ __global__ __launch_bounds__(1024) void hash_prep_kernel(const int64_t* __restri
   __shared__ int64_t sc[1024];
   const int tid = threadIdx.x;
   const int64_t bytes = tid < n ? table[(int64_t)tid * stride] * token_bytes : 0;
-  const int64_t m0 = tid < n ? leaves_of(bytes) : 0;
+  const int64_t m0 = tid < n ? chunks_of(bytes) : 0;
   for (int v = 0; v <= levels + 1; ++v) {
     const int64_t per = v <= levels ? nodes_at(m0, v) : stripes_of(bytes);
     const int64_t x = tid < n ? 2 * (int64_t)L * per : 0;
@@ -104,20 +80,21 @@ __global__ __launch_bounds__(1024) void hash_prep_kernel(const int64_t* __restri
   }
 }
 
-// One wave = one (tensor, stripe) task at a time; lane k hashes leaf k of the
-// stripe, whose blocks lie 4 KiB apart. The grid is bounded (a few workgroups
-// per CU) and strides over all tasks: a VALU-bound kernel saturates the SIMDs
-// with a couple of waves each, and the wave slots left free let an HBM-bound
-// kernel on another stream run on the same CUs.
-__global__ __launch_bounds__(kBlock) void hash_leaf_kernel(const int64_t* __restrict__ table,
-                                                           int32_t n, int64_t stride,
-                                                           int64_t token_bytes,
-                                                           const int64_t* __restrict__ base0,
-                                                           const int64_t* __restrict__ task_base,
-                                                           int64_t total_tasks,
-                                                           const uint8_t* __restrict__ select,
-                                                           uint32_t want,
-                                                           uint8_t* __restrict__ nodes) {
+// One wave = one (tensor, stripe) task at a time. A full stripe: lane k hashes
+// chunk 64 s + k, whose 16 blocks lie 4 KiB apart. The rest of a tensor: lane k
+// hashes its chunk k, 1 KiB of consecutive bytes. The grid is bounded (a few
+// workgroups per CU) and strides over all tasks: a VALU-bound kernel saturates
+// the SIMDs with a couple of waves each, and the wave slots left free let an
+// HBM-bound kernel on another stream run on the same CUs.
+__global__ __launch_bounds__(kBlock) void hash_chunk_kernel(const int64_t* __restrict__ table,
+                                                            int32_t n, int64_t stride,
+                                                            int64_t token_bytes,
+                                                            const int64_t* __restrict__ base0,
+                                                            const int64_t* __restrict__ task_base,
+                                                            int64_t total_tasks,
+                                                            const uint8_t* __restrict__ select,
+                                                            uint32_t want,
+                                                            uint8_t* __restrict__ nodes) {
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform per wave
   const int64_t waves = (int64_t)gridDim.x * (kBlock / 64);
@@ -127,29 +104,30 @@ __global__ __launch_bounds__(kBlock) void hash_leaf_kernel(const int64_t* __rest
     if (select && select[i] != want) continue;
     const int64_t bytes = table[(int64_t)i * stride] * token_bytes;
     const int64_t stripes = stripes_of(bytes);
-    const int64_t m = leaves_of(bytes);
+    const int64_t m = chunks_of(bytes);
     const int64_t local = task - task_base[i];
     const int64_t t = local / stripes;
     const int64_t sidx = local - t * stripes;
     const int64_t in_stripe = (bytes >> 6) - sidx * kStripeBlocks;
-    const int64_t blocks_here = in_stripe < kStripeBlocks ? in_stripe : kStripeBlocks;
-    if (lane >= blocks_here) continue;
-    const int64_t nb = (blocks_here - lane + kStripeLeaves - 1) / kStripeLeaves;
-    const int64_t full_steps = blocks_here / kStripeLeaves;
-    const int64_t leaf = sidx * kStripeLeaves + lane;
+    const uint64_t chunk0 = (uint64_t)sidx * kStripeChunks;
     const uint8_t* p = reinterpret_cast<const uint8_t*>(table[(int64_t)i * stride + 1 + t]) +
                        ((sidx * kStripeBlocks) << 6);
-    B2sState s;
-    b2s_init_tree(s, (uint64_t)leaf, 0);
-    b2s_node(s, (uint64_t)nb, leaf == m - 1, [&](uint64_t b, uint32_t (&w)[16]) {
-      load_leaf_block(p, lane, (int64_t)b, full_steps, w);
-    });
-    store_digest(nodes + (base0[i] + t * m + leaf) * 32, s);
+    B3Cv s;
+    if (in_stripe >= kStripeBlocks) {
+      b3_chunk(s, kB3ChunkBlocks, chunk0 + lane, false,
+               [&](int64_t b, uint32_t (&w)[16]) { load_stripe_block(p, lane, b, w); });
+    } else if (!hash_rest_chunk(s, p, in_stripe, lane, chunk0, m == 1)) {
+      continue;
+    }
+    store_cv(nodes + (base0[i] + t * m + (int64_t)chunk0 + lane) * 32, s);
   }
 }
 
-// Level v >= 1: node j of a tensor hashes children 2j, 2j+1 of level v-1;
-// an unpaired last child is carried up unchanged.
+// Level v >= 1: node j of a tensor is the BLAKE3 parent of children 2j, 2j+1
+// of level v-1 (ROOT on the tensor's top node); an unpaired last child is
+// carried up unchanged. Pairing level by level this way builds BLAKE3's
+// left-balanced tree: every complete subtree of 2^v chunks starts at a multiple
+// of 2^v and the unpaired tail joins at the level where it is a sibling.
 __global__ __launch_bounds__(kBlock) void hash_parent_kernel(
     const int64_t* __restrict__ table, int32_t n, int64_t stride, int64_t token_bytes, int32_t v,
     const int64_t* __restrict__ base_prev, const int64_t* __restrict__ base_cur,
@@ -159,7 +137,7 @@ __global__ __launch_bounds__(kBlock) void hash_parent_kernel(
   if (g >= total_cur) return;
   const int i = find_fragment(base_cur, n, g);
   if (select && select[i] != want) return;
-  const int64_t m0 = leaves_of(table[(int64_t)i * stride] * token_bytes);
+  const int64_t m0 = chunks_of(table[(int64_t)i * stride] * token_bytes);
   const int64_t m_prev = nodes_at(m0, v - 1);
   const int64_t m_cur = nodes_at(m0, v);
   const int64_t local = g - base_cur[i];
@@ -167,12 +145,13 @@ __global__ __launch_bounds__(kBlock) void hash_parent_kernel(
   const int64_t j = local - t * m_cur;
   const uint8_t* c = in + (base_prev[i] + t * m_prev + 2 * j) * 32;
   if (2 * j + 1 < m_prev) {
+    // the only node of a level that has a sibling is the tensor's root
     uint32_t m[16];
-    load64(c, m);
-    B2sState s;
-    b2s_init_tree(s, (uint64_t)j, (uint32_t)v);
-    b2s_compress(s, m, 64, true, j == m_cur - 1);
-    store_digest(out + g * 32, s);
+    load_block64(c, m);
+    B3Cv s;
+    b3_init(s);
+    b3_compress(s, m, 0, 64, kB3Parent | (m_cur == 1 ? kB3Root : 0u));
+    store_cv(out + g * 32, s);
   } else {
     const uint4* q = reinterpret_cast<const uint4*>(c);
     uint4* o = reinterpret_cast<uint4*>(out + g * 32);
@@ -181,7 +160,12 @@ __global__ __launch_bounds__(kBlock) void hash_parent_kernel(
   }
 }
 
-// Id = BLAKE2s-256(header || root(K^0) || root(V^0) || ...), one lane per fragment.
+// Id = BLAKE3-256(header || root(K^0) || root(V^0) || ...), one lane per
+// fragment. The message is L + 1 blocks: the header, then per layer the pair of
+// roots (K, V). Chunks are hashed in order; completed subtrees are merged as soon
+// as a chunk count allows (a stack of chaining values, one per set bit of the
+// chunks seen), the last chunk is merged with the stack from the top down, and
+// ROOT marks the single chunk or the last parent.
 __global__ __launch_bounds__(64) void hash_final_kernel(
     const int64_t* __restrict__ table, int32_t n, int64_t stride, int32_t L, int32_t H,
     int32_t d, uint32_t dtype_code, uint32_t esize, const int64_t* __restrict__ base_last,
@@ -191,19 +175,39 @@ __global__ __launch_bounds__(64) void hash_final_kernel(
   if (i >= n) return;
   if (select && select[i] != want) return;
   const uint64_t T = (uint64_t)table[(int64_t)i * stride];
-  uint32_t m[16] = {0x52464D43u, 0x31304741u,  // "CMFRAG01"
-                    dtype_code, esize, (uint32_t)L, 1u, (uint32_t)H,
-                    (uint32_t)T, (uint32_t)(T >> 32), (uint32_t)d,
-                    0u, 0u, 0u, 0u, 0u, 0u};
-  B2sState s;
-  b2s_init_sequential(s);
-  b2s_compress(s, m, 64, false, false);
   const uint8_t* r = roots + base_last[i] * 32;
-  for (int l = 0; l < L; ++l) {
-    load64(r + (int64_t)l * 64, m);
-    b2s_compress(s, m, (uint64_t)(l + 2) * 64, l == L - 1, false);
+  const int64_t blocks = (int64_t)L + 1;
+  const int64_t chunks = (blocks + kB3ChunkBlocks - 1) / kB3ChunkBlocks;
+  auto load = [&](int64_t g, uint32_t (&w)[16]) {
+    if (g == 0) {
+      const uint32_t h[16] = {0x52464D43u, 0x31304741u,  // "CMFRAG01"
+                              dtype_code, esize, (uint32_t)L, 1u, (uint32_t)H,
+                              (uint32_t)T, (uint32_t)(T >> 32), (uint32_t)d,
+                              0u, 0u, 0u, 0u, 0u, 0u};
+#pragma unroll
+      for (int k = 0; k < 16; ++k) w[k] = h[k];
+    } else {
+      load_block64(r + (g - 1) * 64, w);
+    }
+  };
+  B3Cv stack[40];  // chunk counts below 2^40
+  int sp = 0;
+  B3Cv cv;
+  for (int64_t c = 0; c < chunks; ++c) {
+    const int64_t g0 = c * kB3ChunkBlocks;
+    const int64_t nb = blocks - g0 < kB3ChunkBlocks ? blocks - g0 : kB3ChunkBlocks;
+    b3_chunk(cv, nb, (uint64_t)c, chunks == 1,
+             [&](int64_t b, uint32_t (&w)[16]) { load(g0 + b, w); });
+    if (c + 1 < chunks) {
+      for (int64_t total = c + 1; (total & 1) == 0; total >>= 1) b3_parent(cv, stack[--sp], cv, false);
+      stack[sp++] = cv;
+    }
   }
-  store_digest(digests + (int64_t)i * 32, s);
+  while (sp > 0) {
+    --sp;
+    b3_parent(cv, stack[sp], cv, sp == 0);
+  }
+  store_cv(digests + (int64_t)i * 32, cv);
 }
 
 }  // namespace
@@ -213,7 +217,7 @@ HashLayout hash_layout(const SetDesc& s) {
   int64_t max_m0 = 1;
   for (int i = 0; i < s.n; ++i) {
     lay.tasks += 2 * (int64_t)s.L * stripes_of(s.T(i) * token_bytes_of(s));
-    const int64_t m0 = leaves_of(s.T(i) * token_bytes_of(s));
+    const int64_t m0 = chunks_of(s.T(i) * token_bytes_of(s));
     if (m0 > max_m0) max_m0 = m0;
     lay.total0 += 2 * (int64_t)s.L * m0;
     lay.total1 += 2 * (int64_t)s.L * nodes_at(m0, 1);
@@ -251,7 +255,7 @@ hipError_t launch_hash_tree(const SetDesc& s, const HashLayout& lay, const uint8
   for (int v = 1; v <= lay.levels; ++v) {
     int64_t total = 0;
     for (int i = 0; i < s.n; ++i)
-      total += 2 * (int64_t)s.L * nodes_at(leaves_of(s.T(i) * token_bytes_of(s)), v);
+      total += 2 * (int64_t)s.L * nodes_at(chunks_of(s.T(i) * token_bytes_of(s)), v);
     ScopedTiming tm(K_HASH_PARENT, stream);
     const int64_t grid = (total + kBlock - 1) / kBlock;
     hipLaunchKernelGGL(hash_parent_kernel, dim3((uint32_t)grid), dim3(kBlock), 0, stream,
@@ -281,7 +285,7 @@ hipError_t launch_hash(const SetDesc& s, const HashLayout& lay, const uint8_t* s
     const int64_t full = (lay.tasks + (kBlock / 64) - 1) / (kBlock / 64);
     const int64_t cap = (int64_t)device_cu_count() * kLeafBlocksPerCu;
     const int64_t grid = full < cap ? full : cap;
-    hipLaunchKernelGGL(hash_leaf_kernel, dim3((uint32_t)grid), dim3(kBlock), 0, stream,
+    hipLaunchKernelGGL(hash_chunk_kernel, dim3((uint32_t)grid), dim3(kBlock), 0, stream,
                        s.table_dev, s.n, s.stride, token_bytes_of(s), base,
                        base + (int64_t)(lay.levels + 1) * nb1, lay.tasks, select, want,
                        ws + lay.off_buf0);

@@ -34,18 +34,18 @@ inline int64_t token_bytes_of(const SetDesc& s) { return (int64_t)s.H * s.row_by
 
 constexpr size_t kWsAlign = 256;
 
-// Hash-tree geometry (see cm_fragment_hash): 64-byte blocks, stripes of 4096
-// blocks (256 KiB) holding 64 leaves each.
-constexpr int64_t kStripeBlocks = 4096;
-constexpr int kStripeLeaves = 64;
+// Hash geometry (see cm_fragment_hash): 64-byte blocks, BLAKE3 chunks of 16
+// blocks, stripes of 1024 blocks (64 KiB) holding 64 interleaved chunks; the
+// blocks after the last full stripe are hashed in their own order.
+constexpr int64_t kStripeBlocks = 1024;
+constexpr int kStripeChunks = 64;
 
-// Leaves per tensor of `bytes` (a positive multiple of 64).
-__host__ __device__ __forceinline__ int64_t leaves_of(int64_t bytes) {
-  const int64_t blocks = bytes >> 6;
-  const int64_t rest = blocks % kStripeBlocks;
-  return kStripeLeaves * (blocks / kStripeBlocks) + (rest < kStripeLeaves ? rest : kStripeLeaves);
+// BLAKE3 chunks of a tensor of `bytes` (a positive multiple of 64): ceil(bytes / 1 KiB).
+__host__ __device__ __forceinline__ int64_t chunks_of(int64_t bytes) {
+  return (bytes + 1023) >> 10;
 }
 
+// (tensor, stripe) work items per tensor: full stripes plus one for the rest.
 __host__ __device__ __forceinline__ int64_t stripes_of(int64_t bytes) {
   return ((bytes >> 6) + kStripeBlocks - 1) / kStripeBlocks;
 }
@@ -60,12 +60,12 @@ inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 // Compute units of the current device (cached per device).
 int device_cu_count();
 
-// Tree-hash geometry of a set: a tensor of B bytes has B/64 blocks in stripes
-// of 4096 and m0 = 64 * full stripes + min(64, blocks of the last stripe)
-// leaves; level v has ceil(m0 / 2^v) nodes.
+// Tree-hash geometry of a set: a tensor of B bytes has m0 = ceil(B / 1 KiB)
+// BLAKE3 chunks; level v of its tree has ceil(m0 / 2^v) nodes (adjacent pairs,
+// an unpaired last node carried up, which is BLAKE3's left-balanced tree).
 struct HashLayout {
-  int32_t levels;         // parent levels above the leaves (0 if every tensor is one leaf)
-  int64_t tasks;          // (tensor, stripe) work items of the leaf kernel
+  int32_t levels;         // parent levels above the chunks (0 if every tensor is one chunk)
+  int64_t tasks;          // (tensor, stripe) work items of the chunk kernel
   int64_t total0;         // nodes at level 0 over all tensors
   int64_t total1;         // nodes at level 1 over all tensors (0 if levels == 0)
   size_t off_tables;      // int64 [levels+2][n+1]: per-level node bases, then task bases

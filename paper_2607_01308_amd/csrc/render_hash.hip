@@ -1,28 +1,30 @@
 // Steps 1 and 4-5 in one pass: the render of Eq. (1)-(2) and, for the
-// fragments whose Id is still missing, the leaf level of their hash tree (Id
-// of Alg. 2), from the same loads.
+// fragments whose Id is still missing, the chunk level of their hash (Id of
+// Alg. 2), from the same loads.
 //
-// Hashing is VALU-bound (960 VALU ops per 64-byte block) and the render is
+// Hashing is VALU-bound (672 VALU ops per 64-byte block) and the render is
 // HBM-bound; done separately they read every byte twice. Here one wave takes
-// one (slot, tensor, stripe) task. At full step j of the 256 KiB stripe every
-// lane loads the 16-byte pieces lane, lane+64, lane+128, lane+192 of the 4 KiB
-// step (four loads, each 1 KiB contiguous across the wave), compresses them as
-// one 64-byte block into its leaf (exactly the leaf layout of the tree) and
-// writes each piece to its place in the merged cache: V and offset-0 K
-// unchanged, other K rotated by R(off). A row holds row_bytes / 16 pieces and
-// 64 is a multiple of that, so all four pieces of a lane sit in the same column
-// of their rows: the lane's cos/sin pairs are fixed for the task (registers),
-// and the other half of its pairs is in lane ^ (pieces per row / 2) (one
-// cross-lane move, chosen at compile time). A step covers whole rows; unless it
-// straddles two heads its rows are consecutive in the merged cache too, so its
-// stores take the same wave-uniform base plus lane offsets as its loads. The
-// short final step of a stripe, if any, keeps whole 64-byte blocks per lane and
-// reads its angles from memory. HBM traffic is the
-// algorithmic minimum (each byte read once, written once); the kernel is bound
-// by the VALU work of the hash plus the fp64 rotation.
+// one (slot, tensor, stripe) task. At step j of a full 64 KiB stripe every lane
+// loads the 16-byte pieces lane, lane+64, lane+128, lane+192 of the 4 KiB step
+// (four loads, each 1 KiB contiguous across the wave), compresses them as block
+// j of its BLAKE3 chunk (exactly the message order of the hash) and writes each
+// piece to its place in the merged cache: V and offset-0 K unchanged, other K
+// rotated by R(off). A row holds row_bytes / 16 pieces and 64 is a multiple of
+// that, so all four pieces of a lane sit in the same column of their rows: the
+// lane's cos/sin pairs are fixed for the task (registers), and the other half of
+// its pairs is in lane ^ (pieces per row / 2) (one cross-lane move, chosen at
+// compile time). A step covers whole rows; unless it straddles two heads its
+// rows are consecutive in the merged cache too, so its stores take the same
+// wave-uniform base plus lane offsets as its loads. The rest of a tensor after
+// its last full stripe (under 64 KiB) is rendered by the same steps plus a short
+// final step whose lanes keep whole 64-byte blocks, then its chunks are hashed
+// in their own byte order from a second read (of bytes the render just pulled
+// into the cache). HBM traffic is the algorithmic minimum (each byte read once,
+// written once); the kernel is bound by the VALU work of the hash plus the fp64
+// rotation.
 #include <type_traits>
 
-#include "blake2s.h"
+#include "chunk_ops.h"
 #include "rotate.h"
 
 namespace cm {
@@ -69,14 +71,14 @@ __device__ __forceinline__ void rotate_block_tail(u32x4 (&x)[4], int c, int ppr,
   for (int k = 0; k < 4; ++k) x[k] = y[k];
 }
 
-__device__ __forceinline__ void compress_pieces(B2sState& st, const u32x4 (&x)[4], uint64_t count,
-                                                bool last, bool last_node) {
+__device__ __forceinline__ void compress_pieces(B3Cv& st, const u32x4 (&x)[4], uint64_t chunk,
+                                                uint32_t flags) {
   uint32_t w[16];
 #pragma unroll
   for (int k = 0; k < 4; ++k)
 #pragma unroll
     for (int q = 0; q < 4; ++q) w[4 * k + q] = x[k][q];
-  b2s_compress(st, w, count, last, last_node);
+  b3_compress(st, w, chunk, 64, flags);
 }
 
 // Destination of byte `rel` (0 <= rel < 4096) of a step whose first row is row
@@ -137,16 +139,17 @@ __global__ __launch_bounds__(kThreads) CM_FUSED_OCCUPANCY void render_hash_kerne
     if (rotate) piece_angles<ESIZE, STYLE>(ang, cp, ppr, cs, sn);
     const int64_t in_stripe = (bytes >> 6) - sidx * kStripeBlocks;
     const int bh = (int)(in_stripe < kStripeBlocks ? in_stripe : kStripeBlocks);
-    const int full_steps = bh / kStripeLeaves;
-    const int rem = bh - full_steps * kStripeLeaves;
-    const int nb = full_steps + (lane < rem ? 1 : 0);
+    const bool full_stripe = bh == kStripeBlocks;
+    const bool hash_steps = hashing && full_stripe;  // the lane's chunk is fed by the steps
+    const int full_steps = bh / kStripeChunks;       // 16 in a full stripe
+    const int rem = bh - full_steps * kStripeChunks; // 0 in a full stripe
     const uint8_t* src = reinterpret_cast<const uint8_t*>(table[i * stride + 1 + t]) +
                          ((sidx * kStripeBlocks) << 6);
     uint8_t* out_t = out + t * (int64_t)H * T_out * row_bytes;
-    const int64_t leaf = sidx * kStripeLeaves + lane;
-    const int64_t m = leaves_of(bytes);
-    B2sState st;
-    b2s_init_tree(st, (uint64_t)leaf, 0);
+    const uint64_t chunk0 = (uint64_t)sidx * kStripeChunks;
+    const int64_t m = chunks_of(bytes);
+    B3Cv st;
+    b3_init(st);
     // first row of the current step: head hh, row tt of that head (scalars)
     int64_t hh, tt;
     {
@@ -155,7 +158,7 @@ __global__ __launch_bounds__(kThreads) CM_FUSED_OCCUPANCY void render_hash_kerne
       tt = r0 - hh * T;
     }
     const int64_t gap = (T_out - T) << rb_shift;   // end of a head's rows -> next head
-    // One full step: prefetch the next one, hash this one into the lane's leaf,
+    // One full step: prefetch the next one, hash this one into the lane's chunk,
     // rotate it if needed, store it. WRAPS: the fragment is shorter than a step
     // (T < rows per step), so a step may span several heads.
     auto step = [&](auto wraps, const u32x4 (&x)[4], u32x4 (&nx)[4], int j) {
@@ -165,8 +168,7 @@ __global__ __launch_bounds__(kThreads) CM_FUSED_OCCUPANCY void render_hash_kerne
       const uint8_t* sb = src + ((int64_t)jn << 12);     // wave-uniform base
 #pragma unroll
       for (int k = 0; k < 4; ++k) nx[k] = ld16(sb + (uint32_t)(lane * 16 + k * 1024));
-      if (hashing) compress_pieces(st, x, (uint64_t)(j + 1) << 6, j + 1 == nb,
-                                   j + 1 == nb && leaf == m - 1);
+      if (hash_steps) compress_pieces(st, x, chunk0 + lane, b3_chunk_flags(j, full_steps, false));
       u32x4 y[4];
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
@@ -233,7 +235,6 @@ __global__ __launch_bounds__(kThreads) CM_FUSED_OCCUPANCY void render_hash_kerne
       if (lane < rem) {
 #pragma unroll
         for (int k = 0; k < 4; ++k) x[k] = ld16(sp + 16 * k);
-        if (hashing) compress_pieces(st, x, (uint64_t)nb << 6, true, leaf == m - 1);
       }
       const int cb = (int)(((lane * 64) & (row_bytes - 1)) >> 6);   // block of the row
       if (rotate) rotate_block_tail<ESIZE, STYLE, HB>(x, cb, ppr, ang);
@@ -243,10 +244,15 @@ __global__ __launch_bounds__(kThreads) CM_FUSED_OCCUPANCY void render_hash_kerne
         for (int k = 0; k < 4; ++k) st_stream(dp + 16 * k, x[k]);
       }
     }
-    if (hashing && nb > 0) {
-      uint4* q = reinterpret_cast<uint4*>(nodes + (base0[i] + t * m + leaf) * 32);
-      q[0] = make_uint4(st.h[0], st.h[1], st.h[2], st.h[3]);
-      q[1] = make_uint4(st.h[4], st.h[5], st.h[6], st.h[7]);
+    if (hashing) {
+      uint8_t* node = nodes + (base0[i] + t * m + (int64_t)chunk0 + lane) * 32;
+      if (full_stripe) {
+        store_cv(node, st);
+      } else {
+        // the rest of the tensor: chunk `lane` is 1 KiB of consecutive bytes
+        B3Cv rs;
+        if (hash_rest_chunk(rs, src, bh, lane, chunk0, m == 1)) store_cv(node, rs);
+      }
     }
   }
 }

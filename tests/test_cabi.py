@@ -68,11 +68,10 @@ def test_workspace_size_covers_hash_tree(lib):
     fs = FakeSet(lengths=(100, 3000), L=3, H=2, d=64, dtype=C.CM_BF16)
     st, ws = _ws(lib, fs)
     assert st == C.CM_OK
-    def leaves(nbytes):                      # striped leaves: 64 per full 256 KiB stripe
-        blocks = nbytes // 64
-        return 64 * (blocks // 4096) + min(64, blocks % 4096)
-    leaves = sum(2 * 3 * leaves(2 * T * 64 * 2) for T in (100, 3000))
-    assert ws >= 32 * leaves
+    def chunks(nbytes):                      # BLAKE3 chunks of 1 KiB per tensor
+        return -(-nbytes // 1024)
+    nodes = sum(2 * 3 * chunks(2 * T * 64 * 2) for T in (100, 3000))
+    assert ws >= 32 * nodes
 
 
 @pytest.mark.parametrize("mutate,code", [

@@ -76,7 +76,8 @@ def test_interleaved_rope_style():
 
 
 def test_multi_level_hash_trees():
-    # 125 and 251 leaves per tensor: odd counts carried up at several levels
+    # 500, 1004 and 8 BLAKE3 chunks per tensor (full stripes plus a rest of 52, 44
+    # and 8 chunks): odd counts carried up at several levels
     w = synth.custom("tree", dtype="bfloat16", d=128, H=2, L=2, lengths=(1000, 2008, 16))
     _, dl = gpu_deliveries(w)
     res = _run(w, dl)

@@ -1,10 +1,10 @@
-"""The library's BLAKE2s compression code, compiled for the host by the test
-harness tests/native/hostcheck.hip, against Python's hashlib (RFC 7693) with
-the tree parameters the GPU path uses; and the compiler's single-step
-fp64 -> bf16 conversion used by the render kernel, against the oracle."""
+"""The library's BLAKE3 code (csrc/blake3.h), compiled for the host by the
+test harness tests/native/hostcheck.hip, against the published BLAKE3 test
+vectors and the oracle, with the chunk counters, flags and parent nodes the GPU
+path uses; and the compiler's single-step fp64 -> bf16 conversion used by the
+render kernel, against the oracle."""
 
 import ctypes
-import hashlib
 import os
 
 import numpy as np
@@ -20,54 +20,68 @@ def hc():
     if not os.path.exists(LIB):
         pytest.fail(f"{LIB} missing: run __graft_entry__.build()")
     L = ctypes.CDLL(LIB)
-    L.hc_blake2s_tree_node.argtypes = [ctypes.c_char_p, ctypes.c_uint64, ctypes.c_uint64,
-                                       ctypes.c_uint32, ctypes.c_int, ctypes.c_char_p]
-    L.hc_blake2s_sequential.argtypes = [ctypes.c_char_p, ctypes.c_uint64, ctypes.c_char_p]
+    L.hc_blake3_chunk.argtypes = [ctypes.c_char_p, ctypes.c_uint64, ctypes.c_uint64,
+                                  ctypes.c_int, ctypes.c_char_p]
+    L.hc_blake3_parent.argtypes = [ctypes.c_char_p, ctypes.c_char_p, ctypes.c_int,
+                                   ctypes.c_char_p]
     L.hc_f64_to_bf16.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64]
     return L
 
 
-def _node(hc, data, off, depth, last):
+def _chunk(hc, data, index, root):
     out = ctypes.create_string_buffer(32)
-    assert hc.hc_blake2s_tree_node(data, len(data), off, depth, int(last), out) == 0
+    assert hc.hc_blake3_chunk(data, len(data), index, int(root), out) == 0
     return out.raw
 
 
-@pytest.mark.parametrize("length", [64, 128, 1024, 4032, 4096])
-def test_tree_node_matches_hashlib(hc, length):
-    rng = np.random.default_rng(length)
-    data = rng.integers(0, 256, size=length, dtype=np.uint8).tobytes()
-    for off, depth, last in ((0, 0, False), (5, 0, True), (2 ** 40 + 3, 7, False), (1, 200, True)):
-        want = hashlib.blake2s(data, digest_size=32, fanout=2, depth=255, leaf_size=4096,
-                               node_offset=off, node_depth=depth, inner_size=32,
-                               last_node=last).digest()
-        assert _node(hc, data, off, depth, last) == want
+def _parent(hc, left, right, root):
+    out = ctypes.create_string_buffer(32)
+    assert hc.hc_blake3_parent(left, right, int(root), out) == 0
+    return out.raw
 
 
-def test_sequential_matches_hashlib(hc):
-    rng = np.random.default_rng(9)
-    for nblocks in (1, 2, 37):
-        data = rng.integers(0, 256, size=64 * nblocks, dtype=np.uint8).tobytes()
-        out = ctypes.create_string_buffer(32)
-        assert hc.hc_blake2s_sequential(data, len(data), out) == 0
-        assert out.raw == hashlib.blake2s(data, digest_size=32).digest()
+def _library_blake3(hc, data):
+    """BLAKE3 of a message (a positive multiple of 64 bytes) built from the
+    library's chunk and parent functions the way the GPU builds it: chunks
+    paired level by level, an unpaired last node carried up, ROOT on the top."""
+    chunks = [data[k:k + 1024] for k in range(0, len(data), 1024)]
+    if len(chunks) == 1:
+        return _chunk(hc, chunks[0], 0, True)
+    level = [_chunk(hc, c, k, False) for k, c in enumerate(chunks)]
+    while len(level) > 1:
+        top = len(level) == 2
+        level = [_parent(hc, level[2 * j], level[2 * j + 1], top) if 2 * j + 1 < len(level)
+                 else level[2 * j] for j in range((len(level) + 1) // 2)]
+    return level[0]
+
+
+def test_library_blake3_matches_published_vectors(hc, golden):
+    g = golden("blake3_vectors.json")
+    checked = 0
+    for case in g["cases"]:
+        n = case["input_len"]
+        if n == 0 or n % 64:
+            continue                           # the library hashes whole 64-byte blocks
+        data = (np.arange(n, dtype=np.int64) % 251).astype(np.uint8).tobytes()
+        assert _library_blake3(hc, data).hex() == case["hash_hex"], n
+        checked += 1
+    assert checked >= 8
+
+
+@pytest.mark.parametrize("nblocks", [1, 15, 16, 17, 48, 80, 16 * 37 + 5])
+def test_library_blake3_matches_oracle(hc, nblocks):
+    rng = np.random.default_rng(nblocks)
+    data = rng.integers(0, 256, size=64 * nblocks, dtype=np.uint8).tobytes()
+    assert _library_blake3(hc, data) == oracle.blake3(data)
 
 
 def test_tensor_root_from_library_nodes(hc):
-    """Rebuild the oracle's per-tensor tree with the library's node function."""
-    from oracle import cmerge_oracle as om
+    """The oracle's tensor root rebuilt from the library's chunk and parent code
+    over the interleaved message (two full stripes and a rest)."""
     rng = np.random.default_rng(3)
-    buf = rng.integers(0, 256, size=262144 + 5 * 4096 + 1024, dtype=np.uint8).tobytes()
-    leaves = om.tensor_leaves(buf)
-    m = len(leaves)
-    level = [_node(hc, leaf, k, 0, k == m - 1) for k, leaf in enumerate(leaves)]
-    depth = 0
-    while len(level) > 1:
-        depth += 1
-        mm = (len(level) + 1) // 2
-        level = [_node(hc, level[2 * j] + level[2 * j + 1], j, depth, j == mm - 1)
-                 if 2 * j + 1 < len(level) else level[2 * j] for j in range(mm)]
-    assert level[0] == oracle.tensor_root(np.frombuffer(buf, np.uint8))
+    buf = rng.integers(0, 256, size=2 * 65536 + 5 * 1024 + 192, dtype=np.uint8)
+    msg = oracle.tensor_message(buf).tobytes()
+    assert _library_blake3(hc, msg) == oracle.tensor_root(buf)
 
 
 def test_single_step_bf16_conversion(hc):

@@ -2,12 +2,13 @@
 
 The paper fixes what the hash covers (shapes, dtypes and raw bytes of every
 layer's K and V, unshifted, in layer order) and that it is collision-resistant;
-it does not name the function. The oracle's reading is a BLAKE2s-256 tree.
-The pins below: the primitive against RFC 7693's published vector, the tree's
-node schedule against its closed form, and the coverage properties the paper
+it does not name the function. The oracle's reading is BLAKE3-256 over each
+tensor's bytes in a fixed interleaved order, then over a header and the tensor
+roots. The pins below: the BLAKE3 implementation against the published BLAKE3
+test vectors (single blocks, multi-block chunks, trees of 2 to 100 chunks), the
+message order against its closed form, and the coverage properties the paper
 states (every byte, every shape/dtype field, K/V and layer order)."""
 
-import hashlib
 import struct
 
 import numpy as np
@@ -18,90 +19,64 @@ from oracle import cmerge_oracle as om
 from helpers import copy_fragment, rand_fragment
 
 
-def test_blake2s_primitive_matches_rfc7693(golden):
-    g = golden("rfc7693_blake2s.json")
-    assert hashlib.blake2s(g["message_ascii"].encode()).hexdigest() == g["blake2s_256_hex"]
+def test_blake3_matches_published_vectors(golden):
+    g = golden("blake3_vectors.json")
+    assert len(g["cases"]) >= 16
+    for case in g["cases"]:
+        n = case["input_len"]
+        data = (np.arange(n, dtype=np.int64) % 251).astype(np.uint8).tobytes()
+        assert oracle.blake3(data).hex() == case["hash_hex"], n
+    for case in g["ascii_cases"]:
+        assert oracle.blake3(case["message_ascii"].encode()).hex() == case["hash_hex"]
 
 
-def test_tree_parameters_take_effect():
-    data = b"\x01" * 100
-    plain = hashlib.blake2s(data).digest()
-    node = om._blake2s_node(data, 0, 0, True)
-    assert node != plain
-    assert om._blake2s_node(data, 1, 0, True) != node      # node offset
-    assert om._blake2s_node(data, 0, 1, True) != node      # node depth
-    assert om._blake2s_node(data, 0, 0, False) != node     # last-node flag
+def test_blake3_accepts_any_buffer_layout():
+    rng = np.random.default_rng(5)
+    a = rng.integers(0, 256, size=3000, dtype=np.uint8)
+    want = oracle.blake3(a.tobytes())
+    assert oracle.blake3(a) == want
+    assert oracle.blake3(bytearray(a.tobytes())) == want
+    assert oracle.blake3(a.view(np.uint16)) == want
 
 
-def _expected_leaves(nbytes):
-    blocks = nbytes // 64
-    full, rest = divmod(blocks, 4096)
-    return 64 * full + min(64, rest)
-
-
-@pytest.mark.parametrize("nblocks", [1, 5, 64, 65, 130, 4096, 4096 + 1, 4096 * 2 + 70, 4096 * 3])
-def test_striped_leaves_closed_form(nblocks):
-    """Closed form of the leaf layout: in a full 4 KiB step leaf k takes the
-    16-byte pieces k, k+64, k+128, k+192; in a shorter final step it takes
-    block k whole. The leaves are a permutation of the 16-byte pieces."""
+@pytest.mark.parametrize("nblocks", [1, 5, 16, 17, 64, 1023, 1024, 1025, 1024 + 70, 2048, 3 * 1024 + 17])
+def test_message_order_closed_form(nblocks):
+    """Closed form of the message order: inside a full 64 KiB stripe s, chunk
+    64 s + k holds, for each 4 KiB step in turn, the 16-byte pieces k, k+64,
+    k+128, k+192 of the step; after the last full stripe the pieces keep their
+    order. The message is a permutation of the pieces."""
     npieces = nblocks * 4
     ids = np.arange(npieces * 4, dtype=np.uint32)           # 4 words per 16-byte piece
     buf = ids.view(np.uint8)
-    leaves = om.tensor_leaves(buf)
-    assert len(leaves) == _expected_leaves(buf.nbytes)
-    seen = []
-    for idx, leaf in enumerate(leaves):
-        assert 0 < len(leaf) <= 4096 and len(leaf) % 64 == 0
-        pieces = (np.frombuffer(leaf, np.uint32).reshape(-1, 4)[:, 0] // 4).tolist()
-        s, k = divmod(idx, 64)
-        want = []
-        stripe_pieces = min(16384, npieces - s * 16384)
-        for t0 in range(0, stripe_pieces, 256):
-            base = s * 16384 + t0
-            step = min(256, stripe_pieces - t0)
-            if step == 256:
+    msg = om.tensor_message(buf)
+    assert msg.size == buf.size
+    got = (msg.view(np.uint32).reshape(-1, 4)[:, 0] // 4).tolist()
+    want = []
+    full = npieces // 4096                                   # pieces per stripe: 4096
+    for s in range(full):
+        for k in range(64):
+            for step in range(16):
+                base = s * 4096 + step * 256
                 want += [base + k + 64 * q for q in range(4)]
-            elif 4 * k < step:
-                want += [base + 4 * k + q for q in range(4)]
-        assert pieces == want
-        seen += pieces
-    assert sorted(seen) == list(range(npieces))
+    want += list(range(full * 4096, npieces))
+    assert got == want
+    assert sorted(got) == list(range(npieces))
 
 
-@pytest.mark.parametrize("nblocks", [1, 2, 64, 65, 130, 4096 + 3, 3 * 4096])
-def test_tree_schedule_closed_form(monkeypatch, nblocks):
-    """A binary tree with m leaves and carried-up odd nodes hashes exactly m
-    leaves (offsets 0..m-1, depth 0, last flag on leaf m-1) and m-1 parents,
-    with depth = ceil(log2 m) at the root."""
-    calls = []
-    real = om._blake2s_node
-
-    def spy(data, off, depth, last):
-        calls.append((len(bytes(data)), off, depth, last))
-        return real(data, off, depth, last)
-
-    monkeypatch.setattr(om, "_blake2s_node", spy)
-    buf = np.arange(nblocks * 64, dtype=np.uint8)
-    m = _expected_leaves(buf.nbytes)
-    om.tensor_root(buf)
-    leaves = [c for c in calls if c[2] == 0]
-    parents = [c for c in calls if c[2] > 0]
-    assert [c[1] for c in leaves] == list(range(m))
-    assert [c[3] for c in leaves] == [k == m - 1 for k in range(m)]
-    assert sum(c[0] for c in leaves) == buf.nbytes
-    assert len(parents) == m - 1
-    assert all(c[0] == 64 for c in parents)
-    if m > 1:
-        assert max(c[2] for c in parents) == int(np.ceil(np.log2(m)))
-        root_call = parents[-1]
-        assert root_call[1] == 0 and root_call[3] is True
+def test_short_tensor_root_is_plain_blake3():
+    """A tensor shorter than one stripe is hashed in its own byte order."""
+    rng = np.random.default_rng(6)
+    for n in (64, 1024, 5000 - 5000 % 64, 65536 - 64):
+        buf = rng.integers(0, 256, size=n, dtype=np.uint8)
+        assert om.tensor_root(buf) == oracle.blake3(buf.tobytes())
 
 
 def test_root_changes_on_every_single_byte_flip():
     rng = np.random.default_rng(0)
-    buf = rng.integers(0, 256, size=3 * 4096 + 1024, dtype=np.uint8)
+    buf = rng.integers(0, 256, size=65536 + 3 * 4096 + 1024, dtype=np.uint8)
     base = om.tensor_root(buf)
-    positions = [0, 1, 63, 64, 4095, 4096, 8191, 8192, 12287, 12288, buf.size - 1]
+    positions = [0, 1, 15, 16, 63, 64, 1023, 1024, 4095, 4096, 65535, 65536, 69631, 69632,
+                 buf.size - 1]
     positions += list(rng.integers(0, buf.size, size=40))
     seen = {base}
     for p in positions:
@@ -121,10 +96,11 @@ def test_root_is_order_and_length_sensitive():
     assert om.tensor_root(swapped) != base
     assert om.tensor_root(np.concatenate([buf, np.zeros(4096, np.uint8)])) != base
     assert om.tensor_root(buf[:-64]) != base
-    big = rng.integers(0, 256, size=2 * 262144, dtype=np.uint8)       # two full stripes
-    sw = big.copy()
-    sw[:64], sw[64:128] = big[64:128], big[:64]                      # swap blocks of two leaves
-    assert om.tensor_root(sw) != om.tensor_root(big)
+    big = rng.integers(0, 256, size=2 * 65536 + 3072, dtype=np.uint8)  # two full stripes + rest
+    for a, b in ((0, 16), (0, 1024), (65536, 65536 + 16), (131072, 131072 + 64)):
+        sw = big.copy()
+        sw[a:a + 16], sw[b:b + 16] = big[b:b + 16], big[a:a + 16]    # swap two pieces
+        assert om.tensor_root(sw) != om.tensor_root(big)
 
 
 def test_header_layout():
