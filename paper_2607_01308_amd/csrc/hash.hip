@@ -9,9 +9,9 @@
 // 64-wide wavefronts: one wave takes one stripe, lane k hashes chunk k (16
 // dependent compressions with the next blocks in flight), and each of the four
 // 16-byte loads of a step reads 1 KiB of contiguous memory across the wave. The
-// work is VALU-bound (12 VALU ops per G step, 672 per block); each upper tree
-// level is one launch over all tensors at full lane occupancy (the parents add
-// 1/16 of the chunk work).
+// work is VALU-bound (12 VALU ops per G step, 672 per block); the tree above the
+// chunks takes one launch per three levels over all tensors at full lane
+// occupancy (the parents add 1/16 of the chunk work).
 #include "chunk_ops.h"
 
 namespace cm {
@@ -123,41 +123,75 @@ __global__ __launch_bounds__(kBlock) void hash_chunk_kernel(const int64_t* __res
   }
 }
 
-// Level v >= 1: node j of a tensor is the BLAKE3 parent of children 2j, 2j+1
-// of level v-1 (ROOT on the tensor's top node); an unpaired last child is
-// carried up unchanged. Pairing level by level this way builds BLAKE3's
+// Tree levels v0+1 .. v0+K (K <= kSubLevels) of every tensor in one launch:
+// lane g computes node g of level v0+K (numbered over all tensors) from its up to
+// 2^K children at level v0, level by level in the lane's own LDS slots. Node j
+// of a level is the BLAKE3 parent of children 2j and 2j+1 of the level below (ROOT
+// on the compression that leaves the tensor one node); an unpaired last child
+// is carried up unchanged. Pairing level by level this way builds BLAKE3's
 // left-balanced tree: every complete subtree of 2^v chunks starts at a multiple
-// of 2^v and the unpaired tail joins at the level where it is a sibling.
-__global__ __launch_bounds__(kBlock) void hash_parent_kernel(
-    const int64_t* __restrict__ table, int32_t n, int64_t stride, int64_t token_bytes, int32_t v,
-    const int64_t* __restrict__ base_prev, const int64_t* __restrict__ base_cur,
-    int64_t total_cur, const uint8_t* __restrict__ select, uint32_t want,
+// of 2^v and the unpaired tail joins at the level where it has a sibling. A lane
+// does up to 2^K - 1 dependent compressions, so a launch covers K levels at full
+// lane occupancy and the level below is read once.
+constexpr int kSubLevels = 3;
+constexpr int kSubLanes = 64;
+
+__global__ __launch_bounds__(kSubLanes) void hash_subtree_kernel(
+    const int64_t* __restrict__ table, int32_t n, int64_t stride, int64_t token_bytes, int32_t v0,
+    int32_t K, const int64_t* __restrict__ base_lo, const int64_t* __restrict__ base_hi,
+    int64_t total_hi, const uint8_t* __restrict__ select, uint32_t want,
     const uint8_t* __restrict__ in, uint8_t* __restrict__ out) {
-  const int64_t g = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-  if (g >= total_cur) return;
-  const int i = find_fragment(base_cur, n, g);
+  // word w of the lane's node p at [p * 8 + w][lane]: consecutive lanes hit
+  // consecutive banks
+  __shared__ uint32_t lds[(1 << kSubLevels) * 8][kSubLanes];
+  const int lane = threadIdx.x;
+  const int64_t g = (int64_t)blockIdx.x * kSubLanes + lane;
+  if (g >= total_hi) return;
+  const int i = find_fragment(base_hi, n, g);
   if (select && select[i] != want) return;
   const int64_t m0 = chunks_of(table[(int64_t)i * stride] * token_bytes);
-  const int64_t m_prev = nodes_at(m0, v - 1);
-  const int64_t m_cur = nodes_at(m0, v);
-  const int64_t local = g - base_cur[i];
-  const int64_t t = local / m_cur;
-  const int64_t j = local - t * m_cur;
-  const uint8_t* c = in + (base_prev[i] + t * m_prev + 2 * j) * 32;
-  if (2 * j + 1 < m_prev) {
-    // the only node of a level that has a sibling is the tensor's root
-    uint32_t m[16];
-    load_block64(c, m);
-    B3Cv s;
-    b3_init(s);
-    b3_compress(s, m, 0, 64, kB3Parent | (m_cur == 1 ? kB3Root : 0u));
-    store_cv(out + g * 32, s);
-  } else {
-    const uint4* q = reinterpret_cast<const uint4*>(c);
-    uint4* o = reinterpret_cast<uint4*>(out + g * 32);
-    o[0] = q[0];
-    o[1] = q[1];
+  const int64_t m_lo = nodes_at(m0, v0);
+  const int64_t m_hi = nodes_at(m0, v0 + K);
+  const int64_t local = g - base_hi[i];
+  const int64_t t = local / m_hi;
+  const int64_t j = local - t * m_hi;
+  const int64_t first = j << K;
+  int cur = (int)(m_lo - first < ((int64_t)1 << K) ? m_lo - first : ((int64_t)1 << K));
+  const uint8_t* c = in + (base_lo[i] + t * m_lo + first) * 32;
+  for (int q = 0; q < cur; ++q) {
+    const uint4* src = reinterpret_cast<const uint4*>(c + q * 32);
+    const uint4 a = src[0], b = src[1];
+    const uint32_t w[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+#pragma unroll
+    for (int k = 0; k < 8; ++k) lds[q * 8 + k][lane] = w[k];
   }
+  for (int lev = 1; lev <= K; ++lev) {
+    const uint32_t flags = kB3Parent | (nodes_at(m0, v0 + lev) == 1 ? kB3Root : 0u);
+    const int nn = (cur + 1) >> 1;
+    for (int p = 0; p < nn; ++p) {
+      uint32_t m[16];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) m[k] = lds[2 * p * 8 + k][lane];
+      if (2 * p + 1 < cur) {
+#pragma unroll
+        for (int k = 0; k < 8; ++k) m[8 + k] = lds[(2 * p + 1) * 8 + k][lane];
+        B3Cv cv;
+        b3_init(cv);
+        b3_compress(cv, m, 0, 64, flags);
+#pragma unroll
+        for (int k = 0; k < 8; ++k) m[k] = cv.h[k];
+      }
+#pragma unroll
+      for (int k = 0; k < 8; ++k) lds[p * 8 + k][lane] = m[k];
+    }
+    cur = nn;
+  }
+  uint32_t w[8];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) w[k] = lds[k][lane];
+  uint4* o = reinterpret_cast<uint4*>(out + g * 32);
+  o[0] = make_uint4(w[0], w[1], w[2], w[3]);
+  o[1] = make_uint4(w[4], w[5], w[6], w[7]);
 }
 
 // Id = BLAKE3-256(header || root(K^0) || root(V^0) || ...), one lane per
@@ -249,18 +283,23 @@ hipError_t launch_hash_prep(const SetDesc& s, const HashLayout& lay, uint8_t* ws
 hipError_t launch_hash_tree(const SetDesc& s, const HashLayout& lay, const uint8_t* select,
                             uint32_t want, uint8_t* digests, uint8_t* ws, hipStream_t stream) {
   int64_t* base = reinterpret_cast<int64_t*>(ws + lay.off_tables);
+  // level 0 is in buf0; each launch reads one buffer and writes the other
+  // (buf1 holds every level it receives: they are no larger than level 1)
   uint8_t* buf[2] = {ws + lay.off_buf0, ws + lay.off_buf1};
   const int64_t nb1 = s.n + 1;
   hipError_t e = hipSuccess;
-  for (int v = 1; v <= lay.levels; ++v) {
+  int launch = 0;
+  for (int v0 = 0; v0 < lay.levels; v0 += kSubLevels, ++launch) {
+    const int K = lay.levels - v0 < kSubLevels ? lay.levels - v0 : kSubLevels;
     int64_t total = 0;
     for (int i = 0; i < s.n; ++i)
-      total += 2 * (int64_t)s.L * nodes_at(chunks_of(s.T(i) * token_bytes_of(s)), v);
+      total += 2 * (int64_t)s.L * nodes_at(chunks_of(s.T(i) * token_bytes_of(s)), v0 + K);
     ScopedTiming tm(K_HASH_PARENT, stream);
-    const int64_t grid = (total + kBlock - 1) / kBlock;
-    hipLaunchKernelGGL(hash_parent_kernel, dim3((uint32_t)grid), dim3(kBlock), 0, stream,
-                       s.table_dev, s.n, s.stride, token_bytes_of(s), v, base + (v - 1) * nb1,
-                       base + v * nb1, total, select, want, buf[(v - 1) & 1], buf[v & 1]);
+    const int64_t grid = (total + kSubLanes - 1) / kSubLanes;
+    hipLaunchKernelGGL(hash_subtree_kernel, dim3((uint32_t)grid), dim3(kSubLanes), 0, stream,
+                       s.table_dev, s.n, s.stride, token_bytes_of(s), v0, K, base + v0 * nb1,
+                       base + (v0 + K) * nb1, total, select, want, buf[launch & 1],
+                       buf[(launch + 1) & 1]);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   {
@@ -269,7 +308,7 @@ hipError_t launch_hash_tree(const SetDesc& s, const HashLayout& lay, const uint8
     hipLaunchKernelGGL(hash_final_kernel, dim3((uint32_t)((s.n + 63) / 64)), dim3(64), 0,
                        stream, s.table_dev, s.n, s.stride, s.L, s.H, s.d, code,
                        (uint32_t)s.esize, base + lay.levels * nb1, select, want,
-                       buf[lay.levels & 1], digests);
+                       buf[launch & 1], digests);
   }
   return hipGetLastError();
 }
