@@ -28,6 +28,7 @@ from .cmerge_oracle import (  # noqa: F401
     rope_angles,
     rope_inv_freq,
     rotate_pairs,
+    stripe_lane_pieces,
     round_to_dtype,
     tensor_message,
     tensor_root,

@@ -24,18 +24,21 @@ constexpr int kBlock = 256;
 #endif
 constexpr int kLeafBlocksPerCu = CM_HASH_BLOCKS_PER_CU;
 
-// Block j of chunk `lane` of a full stripe starting at p: the 16-byte pieces
-// lane, lane+64, lane+128, lane+192 of step j.
-__device__ __forceinline__ void load_stripe_block(const uint8_t* p, int lane, int64_t j,
+// Block j of the lane's chunk of a full stripe: the four pieces of step j that
+// the lane takes, for rows of 2 hp pieces: f = (lane / hp) 2hp + lane % hp, its
+// partner f + hp, and the same two 2 KiB further on. a0, a1: the stripe's first
+// byte plus the offsets of pieces f and f + hp.
+__device__ __forceinline__ void load_stripe_block(const uint8_t* a0, const uint8_t* a1, int64_t j,
                                                   uint32_t (&m)[16]) {
-  const CM_GLOBAL u32x4* q = global_ptr<u32x4>(p + (j << 12) + lane * 16);
+  const u32x4 v[4] = {*global_ptr<u32x4>(a0 + (j << 12)), *global_ptr<u32x4>(a1 + (j << 12)),
+                      *global_ptr<u32x4>(a0 + (j << 12) + 2048),
+                      *global_ptr<u32x4>(a1 + (j << 12) + 2048)};
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
-    const u32x4 v = q[k * 64];
-    m[4 * k + 0] = v[0];
-    m[4 * k + 1] = v[1];
-    m[4 * k + 2] = v[2];
-    m[4 * k + 3] = v[3];
+    m[4 * k + 0] = v[k][0];
+    m[4 * k + 1] = v[k][1];
+    m[4 * k + 2] = v[k][2];
+    m[4 * k + 3] = v[k][3];
   }
 }
 
@@ -81,7 +84,8 @@ __global__ __launch_bounds__(1024) void hash_prep_kernel(const int64_t* __restri
 }
 
 // One wave = one (tensor, stripe) task at a time. A full stripe: lane k hashes
-// chunk 64 s + k, whose 16 blocks lie 4 KiB apart. The rest of a tensor: lane k
+// chunk 64 s + k, one block of four pieces from each 4 KiB step (hp: pieces per
+// half row). The rest of a tensor: lane k
 // hashes its chunk k, 1 KiB of consecutive bytes. The grid is bounded (a few
 // workgroups per CU) and strides over all tasks: a VALU-bound kernel saturates
 // the SIMDs with a couple of waves each, and the wave slots left free let an
@@ -93,9 +97,10 @@ __global__ __launch_bounds__(kBlock) void hash_chunk_kernel(const int64_t* __res
                                                             const int64_t* __restrict__ task_base,
                                                             int64_t total_tasks,
                                                             const uint8_t* __restrict__ select,
-                                                            uint32_t want,
+                                                            uint32_t want, int32_t hp,
                                                             uint8_t* __restrict__ nodes) {
   const int lane = threadIdx.x & 63;
+  const uint32_t pf = (uint32_t)((lane / hp) * 2 * hp + lane % hp) * 16;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform per wave
   const int64_t waves = (int64_t)gridDim.x * (kBlock / 64);
   for (int64_t task = (int64_t)blockIdx.x * (kBlock / 64) + wave; task < total_tasks;
@@ -114,8 +119,10 @@ __global__ __launch_bounds__(kBlock) void hash_chunk_kernel(const int64_t* __res
                        ((sidx * kStripeBlocks) << 6);
     B3Cv s;
     if (in_stripe >= kStripeBlocks) {
+      const uint8_t* a0 = p + pf;
+      const uint8_t* a1 = a0 + hp * 16;
       b3_chunk(s, kB3ChunkBlocks, chunk0 + lane, false,
-               [&](int64_t b, uint32_t (&w)[16]) { load_stripe_block(p, lane, b, w); });
+               [&](int64_t b, uint32_t (&w)[16]) { load_stripe_block(a0, a1, b, w); });
     } else if (!hash_rest_chunk(s, p, in_stripe, lane, chunk0, m == 1)) {
       continue;
     }
@@ -327,7 +334,7 @@ hipError_t launch_hash(const SetDesc& s, const HashLayout& lay, const uint8_t* s
     hipLaunchKernelGGL(hash_chunk_kernel, dim3((uint32_t)grid), dim3(kBlock), 0, stream,
                        s.table_dev, s.n, s.stride, token_bytes_of(s), base,
                        base + (int64_t)(lay.levels + 1) * nb1, lay.tasks, select, want,
-                       ws + lay.off_buf0);
+                       (int32_t)(s.row_bytes / 32), ws + lay.off_buf0);
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   return launch_hash_tree(s, lay, select, want, digests, ws, stream);

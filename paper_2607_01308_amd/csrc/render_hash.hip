@@ -4,18 +4,19 @@
 //
 // Hashing is VALU-bound (672 VALU ops per 64-byte block) and the render is
 // HBM-bound; done separately they read every byte twice. Here one wave takes
-// one (slot, tensor, stripe) task. At step j of a full 64 KiB stripe every lane
-// loads the 16-byte pieces lane, lane+64, lane+128, lane+192 of the 4 KiB step
-// (four loads, each 1 KiB contiguous across the wave), compresses them as block
-// j of its BLAKE3 chunk (exactly the message order of the hash) and writes each
-// piece to its place in the merged cache: V and offset-0 K unchanged, other K
-// rotated by R(off). A row holds row_bytes / 16 pieces and 64 is a multiple of
-// that, so all four pieces of a lane sit in the same column of their rows: the
-// lane's cos/sin pairs are fixed for the task (registers), and the other half of
-// its pairs is in lane ^ (pieces per row / 2) (one cross-lane move, chosen at
-// compile time). A step covers whole rows; unless it straddles two heads its
-// rows are consecutive in the merged cache too, so its stores take the same
-// wave-uniform base plus lane offsets as its loads. The rest of a tensor after
+// one (slot, tensor, stripe) task. A row holds 2P pieces of 16 bytes (P per
+// half). At step j of a full 64 KiB stripe lane k loads four pieces of the 4 KiB
+// step: f = (k / P) 2P + k % P, a first-half piece of a row in the step's first
+// 2 KiB, its second-half partner f + P, and the same two in the second 2 KiB
+// (each load covers whole rows' halves, 1 KiB across the wave). It compresses
+// them as block j of its BLAKE3 chunk (exactly the message order of the hash)
+// and writes each piece to its place in the merged cache: V and offset-0 K
+// unchanged, other K rotated by R(off). Both halves of each of the lane's
+// rotation pairs are in its own registers, all in one column: its cos/sin pairs
+// are fixed for the task and no lane exchange is needed. A step covers whole
+// rows; unless it straddles two heads its rows are consecutive in the merged
+// cache too, so its stores take the same wave-uniform base plus lane offsets as
+// its loads. The rest of a tensor after
 // its last full stripe (under 64 KiB) is rendered by the same steps plus a short
 // final step whose lanes keep whole 64-byte blocks, then its chunks are hashed
 // in their own byte order from a second read (of bytes the render just pulled
@@ -95,8 +96,9 @@ __device__ __forceinline__ uint8_t* dest_wrapped(uint8_t* out_t, int64_t hh, int
   return out_t + ((hh * T_out + off + rr) << rb_shift) + (rel & ((1 << rb_shift) - 1));
 }
 
-// HB: for half-split pairs, the lane distance between a piece and its partner
-// piece in full steps (16-byte pieces per row / 2); 0 for interleaved pairs.
+// HB: for half-split pairs, 16-byte pieces per half row (the short final step
+// of a tensor's rest finds partner blocks HB / 4 lanes away); 0 for interleaved
+// pairs.
 template <int ESIZE, int STYLE, int HB>
 __global__ __launch_bounds__(kThreads) CM_FUSED_OCCUPANCY void render_hash_kernel(
     const int64_t* __restrict__ table, int64_t stride, int32_t n, const int64_t* __restrict__ plan,
@@ -115,7 +117,11 @@ __global__ __launch_bounds__(kThreads) CM_FUSED_OCCUPANCY void render_hash_kerne
   const int64_t row_bytes = (int64_t)1 << rb_shift;
   const int ppr = (int)(row_bytes >> 4);           // 16-byte pieces per row: 4 .. 64
   const int rps = 4096 >> rb_shift;                // rows per full step
-  const int cp = lane & (ppr - 1);                 // column piece of this lane (full steps)
+  const int hp = ppr >> 1;                         // pieces per half row: 2 .. 32
+  const int cp = lane % hp;                        // first-half column of the lane's pairs
+  // byte offsets in a full step of the lane's pieces: f, f + P, f + 128, f + 128 + P
+  const uint32_t pf = (uint32_t)((lane / hp) * ppr + cp) * 16;
+  const uint32_t po[4] = {pf, pf + (uint32_t)hp * 16, pf + 2048, pf + (uint32_t)hp * 16 + 2048};
   const int64_t waves = (int64_t)gridDim.x * kWaves;
   for (int64_t task = (int64_t)blockIdx.x * kWaves + wave; task < total_tasks; task += waves) {
     int lo = 0, hi = n_u - 1;
@@ -135,8 +141,14 @@ __global__ __launch_bounds__(kThreads) CM_FUSED_OCCUPANCY void render_hash_kerne
     const int64_t sidx = local - t * stripes;
     const bool rotate = (t & 1) == 0 && off != 0;
     const double* ang = angles + (int64_t)s * d;
-    double cs[NA], sn[NA];
-    if (rotate) piece_angles<ESIZE, STYLE>(ang, cp, ppr, cs, sn);
+    // the lane's angles: half-split, the pairs of column cp; interleaved, the
+    // pairs inside columns cp (pieces 0, 2) and cp + P (pieces 1, 3)
+    double cs[EP], sn[EP];
+    if (rotate) {
+      piece_angles<ESIZE, STYLE>(ang, cp, ppr, cs, sn);
+      if constexpr (STYLE == CM_ROPE_INTERLEAVED)
+        piece_angles<ESIZE, STYLE>(ang, cp + hp, ppr, cs + NA, sn + NA);
+    }
     const int64_t in_stripe = (bytes >> 6) - sidx * kStripeBlocks;
     const int bh = (int)(in_stripe < kStripeBlocks ? in_stripe : kStripeBlocks);
     const bool full_stripe = bh == kStripeBlocks;
@@ -167,29 +179,32 @@ __global__ __launch_bounds__(kThreads) CM_FUSED_OCCUPANCY void render_hash_kerne
       const int jn = j + 1 < full_steps ? j + 1 : j;
       const uint8_t* sb = src + ((int64_t)jn << 12);     // wave-uniform base
 #pragma unroll
-      for (int k = 0; k < 4; ++k) nx[k] = ld16(sb + (uint32_t)(lane * 16 + k * 1024));
+      for (int k = 0; k < 4; ++k) nx[k] = ld16(sb + po[k]);
       if (hash_steps) compress_pieces(st, x, chunk0 + lane, b3_chunk_flags(j, full_steps, false));
-      u32x4 y[4];
+      u32x4 y[4] = {x[0], x[1], x[2], x[3]};
+      if (rotate) {
+        if constexpr (STYLE == CM_ROPE_HALF) {
+          rotate_pair_half<ESIZE>(y[0], y[1], cs, sn);
+          rotate_pair_half<ESIZE>(y[2], y[3], cs, sn);
+        } else {
 #pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        y[k] = x[k];
-        if (rotate) {
-          if constexpr (STYLE == CM_ROPE_HALF)
-            y[k] = rotate_piece_half<ESIZE>(x[k], lane_xor4<HB>(x[k]), cs, sn);
-          else
-            y[k] = rotate_piece_il<ESIZE>(x[k], cs, sn);
+          for (int k = 0; k < 4; ++k)
+            y[k] = rotate_piece_il<ESIZE>(x[k], cs + (k & 1) * NA, sn + (k & 1) * NA);
         }
       }
       if constexpr (!decltype(wraps)::value) {
-        // the step's rows are consecutive rows of the source and, up to one head
-        // change (branch-free: the rows from `left` on move on by `gap`), of the
-        // merged cache
+        // the step's rows are consecutive rows of the source and, unless the
+        // step crosses the end of a head (at most one step per head; the rows
+        // from `left` on then move on by `gap`), of the merged cache
         uint8_t* db = out_t + ((hh * T_out + off + tt) << rb_shift);   // wave-uniform base
         const int64_t left = T - tt;
+        if (__builtin_expect(left >= rps, 1)) {
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
-          const uint32_t rel = (uint32_t)(lane * 16 + k * 1024);
-          st_stream(db + rel + ((int64_t)(rel >> rb_shift) >= left ? gap : 0), y[k]);
+          for (int k = 0; k < 4; ++k) st_stream(db + po[k], y[k]);
+        } else {
+#pragma unroll
+          for (int k = 0; k < 4; ++k)
+            st_stream(db + po[k] + ((int64_t)(po[k] >> rb_shift) >= left ? gap : 0), y[k]);
         }
         tt += rps;
         const bool next_head = tt >= T;
@@ -198,8 +213,7 @@ __global__ __launch_bounds__(kThreads) CM_FUSED_OCCUPANCY void render_hash_kerne
       } else {
 #pragma unroll
         for (int k = 0; k < 4; ++k)
-          st_stream(dest_wrapped(out_t, hh, tt, lane * 16 + k * 1024, rb_shift, T, T_out, off),
-                    y[k]);
+          st_stream(dest_wrapped(out_t, hh, tt, (int)po[k], rb_shift, T, T_out, off), y[k]);
         tt += rps;
         while (tt >= T) {
           tt -= T;
@@ -214,7 +228,7 @@ __global__ __launch_bounds__(kThreads) CM_FUSED_OCCUPANCY void render_hash_kerne
     auto run = [&](auto wraps) {
       u32x4 bufa[4], bufb[4];
 #pragma unroll
-      for (int k = 0; k < 4; ++k) bufa[k] = ld16(src + (uint32_t)(lane * 16 + k * 1024));
+      for (int k = 0; k < 4; ++k) bufa[k] = ld16(src + po[k]);
       step(wraps, bufa, bufb, 0);
       int j = 1;
       while (j + 1 < full_steps) {

@@ -1,10 +1,12 @@
 // Device helpers of the render kernels for the RoPE re-encode of Eq. (1)-(2):
-// a 16-byte piece of a K row rotated by R(off), in fp64 with the two products
-// and the add/subtract rounded separately, then rounded once to the storage
-// dtype (round-to-nearest-even).
+// 16-byte pieces of K rows rotated by R(off) in fp64, then rounded once to the
+// storage dtype (round-to-nearest-even). Each output element is
+// fma(x, c, -(partner * s')): the partner's product is rounded to fp64, x * c
+// enters the fused multiply-add exactly. Every kernel uses these helpers, so
+// the dense, fused and paged renders agree bit for bit.
 //
 // A K row of d elements is cut into 16-byte pieces (EP = 16 / esize elements
-// each, d / EP pieces per row). Half-split pairs (j, j + d/2) put piece p of
+// each, d / EP pieces per row). Half-split pairs (j, j+d/2) put piece p of
 // the first half against piece p of the second half, P = d / (2 EP) pieces
 // apart; interleaved pairs (2j, 2j+1) stay inside one piece.
 //
@@ -42,10 +44,31 @@ __device__ __forceinline__ double piece_elem(const u32x4 v, int e) {
   }
 }
 
+// fp32 value f of an fp64 result y, nudged one ulp towards y when f sits on a
+// bf16 midpoint and y does not: rounding f to bf16 (ties to even) then gives y
+// rounded to bf16 in one step (see bf16_bits_rne).
+__device__ __forceinline__ bool on_bf16_midpoint(float f) {
+  return (__float_as_uint(f) & 0xFFFFu) == 0x8000u;
+}
+__device__ __forceinline__ float settle_bf16(float f, double y) {
+  uint32_t u = __float_as_uint(f);
+  if (on_bf16_midpoint(f)) {
+    const double back = (double)f;
+    if (y != back) u = (fabs(y) > fabs(back)) ? u + 1u : u - 1u;
+  }
+  return __uint_as_float(u);
+}
+
+// Two fp32 values as the bf16 pair of one word (round to nearest even).
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  const f32x2 v = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
+}
+
 // Round EP fp64 values into a 16-byte piece. bf16: fp32 rounding first is exact
-// unless an fp32 result sits on a bf16 midpoint (see bf16_bits_rne); that rare
-// case is tested once for the whole piece and settled element by element. The
-// fp32 -> bf16 step converts two elements per instruction.
+// unless an fp32 result sits on a bf16 midpoint; that rare case is tested once
+// for the whole piece and settled element by element. The fp32 -> bf16 step
+// converts two elements per instruction.
 template <int ESIZE>
 __device__ __forceinline__ u32x4 round_piece(const double (&y)[16 / ESIZE]) {
   constexpr int EP = 16 / ESIZE;
@@ -56,24 +79,14 @@ __device__ __forceinline__ u32x4 round_piece(const double (&y)[16 / ESIZE]) {
 #pragma unroll
     for (int e = 0; e < EP; ++e) {
       f[e] = (float)y[e];
-      mid |= (__float_as_uint(f[e]) & 0xFFFFu) == 0x8000u;
+      mid |= on_bf16_midpoint(f[e]);
     }
     if (__builtin_expect(mid, 0)) {
 #pragma unroll
-      for (int e = 0; e < EP; ++e) {
-        uint32_t u = __float_as_uint(f[e]);
-        if ((u & 0xFFFFu) == 0x8000u) {
-          const double back = (double)f[e];
-          if (y[e] != back) u = (fabs(y[e]) > fabs(back)) ? u + 1u : u - 1u;
-        }
-        f[e] = __uint_as_float(u);
-      }
+      for (int e = 0; e < EP; ++e) f[e] = settle_bf16(f[e], y[e]);
     }
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const f32x2 v = {f[2 * k], f[2 * k + 1]};
-      out[k] = __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
-    }
+    for (int k = 0; k < 4; ++k) out[k] = pack_bf16x2(f[2 * k], f[2 * k + 1]);
   } else {
 #pragma unroll
     for (int e = 0; e < EP; ++e) out[e] = __float_as_uint((float)y[e]);
@@ -81,9 +94,21 @@ __device__ __forceinline__ u32x4 round_piece(const double (&y)[16 / ESIZE]) {
   return out;
 }
 
+// The words of v, opaque to the optimiser: a value computed from them again is
+// recomputed, not kept alive from an earlier computation.
+__device__ __forceinline__ void launder(u32x4& v) {
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    uint32_t x = v[w];
+    asm volatile("" : "+v"(x));
+    v[w] = x;
+  }
+}
+
 // Rotate one 16-byte piece whose pairs are (x, partner p) with the lane's fixed
-// angles: y = x c - p s', where s' = s in the first half of the row and -s in
-// the second (x c - p (-s) = x c + p s, bit for bit).
+// angles: y = fma(x, c, -(p s')), where s' = s in the first half of the row and
+// -s in the second (p (-s) = -(p s) exactly, so both halves match
+// rotate_pair_half bit for bit).
 template <int ESIZE>
 __device__ __forceinline__ u32x4 rotate_piece_half(const u32x4 x, const u32x4 p, const double* cs,
                                                    const double* sn) {
@@ -92,8 +117,58 @@ __device__ __forceinline__ u32x4 rotate_piece_half(const u32x4 x, const u32x4 p,
   double y[EP];
 #pragma unroll
   for (int e = 0; e < EP; ++e)
-    y[e] = piece_elem<ESIZE>(x, e) * cs[e] - piece_elem<ESIZE>(p, e) * sn[e];
+    y[e] = __builtin_fma(piece_elem<ESIZE>(x, e), cs[e], -(piece_elem<ESIZE>(p, e) * sn[e]));
   return round_piece<ESIZE>(y);
+}
+
+// Rotate a first-half piece a and its second-half partner b (same column) in
+// place with the angles of that column (s not sign-flipped):
+// a' = fma(a, c, -(b s)), b' = fma(b, c, a s). Each result is rounded to fp32 as
+// soon as it is computed; in the rare case of a bf16 midpoint the piece's fp64
+// results are computed again from the inputs (same operations, same bits), so no
+// fp64 result has to stay live across the test.
+template <int ESIZE>
+__device__ __forceinline__ void rotate_pair_half(u32x4& a, u32x4& b, const double* cs,
+                                                 const double* sn) {
+#pragma clang fp contract(off)
+  constexpr int EP = 16 / ESIZE;
+  if constexpr (ESIZE == 2) {
+    float fa[EP], fb[EP];
+    bool mid = false;
+#pragma unroll
+    for (int e = 0; e < EP; ++e) {
+      const double x1 = piece_elem<ESIZE>(a, e), x2 = piece_elem<ESIZE>(b, e);
+      fa[e] = (float)__builtin_fma(x1, cs[e], -(x2 * sn[e]));
+      fb[e] = (float)__builtin_fma(x2, cs[e], x1 * sn[e]);
+      mid |= on_bf16_midpoint(fa[e]) | on_bf16_midpoint(fb[e]);
+    }
+    if (__builtin_expect(mid, 0)) {
+      u32x4 la = a, lb = b;
+      launder(la);
+      launder(lb);
+#pragma unroll
+      for (int e = 0; e < EP; ++e) {
+        const double x1 = piece_elem<ESIZE>(la, e), x2 = piece_elem<ESIZE>(lb, e);
+        fa[e] = settle_bf16(fa[e], __builtin_fma(x1, cs[e], -(x2 * sn[e])));
+        fb[e] = settle_bf16(fb[e], __builtin_fma(x2, cs[e], x1 * sn[e]));
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      a[k] = pack_bf16x2(fa[2 * k], fa[2 * k + 1]);
+      b[k] = pack_bf16x2(fb[2 * k], fb[2 * k + 1]);
+    }
+  } else {
+    u32x4 ra, rb;
+#pragma unroll
+    for (int e = 0; e < EP; ++e) {
+      const double x1 = piece_elem<ESIZE>(a, e), x2 = piece_elem<ESIZE>(b, e);
+      ra[e] = __float_as_uint((float)__builtin_fma(x1, cs[e], -(x2 * sn[e])));
+      rb[e] = __float_as_uint((float)__builtin_fma(x2, cs[e], x1 * sn[e]));
+    }
+    a = ra;
+    b = rb;
+  }
 }
 
 // Interleaved pairs (2q, 2q+1) inside the piece.
@@ -106,8 +181,8 @@ __device__ __forceinline__ u32x4 rotate_piece_il(const u32x4 x, const double* cs
 #pragma unroll
   for (int q = 0; q < EP / 2; ++q) {
     const double x1 = piece_elem<ESIZE>(x, 2 * q), x2 = piece_elem<ESIZE>(x, 2 * q + 1);
-    y[2 * q] = x1 * cs[q] - x2 * sn[q];
-    y[2 * q + 1] = x2 * cs[q] + x1 * sn[q];
+    y[2 * q] = __builtin_fma(x1, cs[q], -(x2 * sn[q]));
+    y[2 * q + 1] = __builtin_fma(x2, cs[q], x1 * sn[q]);
   }
   return round_piece<ESIZE>(y);
 }

@@ -80,8 +80,9 @@ def test_tensor_root_from_library_nodes(hc):
     over the interleaved message (two full stripes and a rest)."""
     rng = np.random.default_rng(3)
     buf = rng.integers(0, 256, size=2 * 65536 + 5 * 1024 + 192, dtype=np.uint8)
-    msg = oracle.tensor_message(buf).tobytes()
-    assert _library_blake3(hc, msg) == oracle.tensor_root(buf)
+    for row_bytes in (64, 256, 1024):
+        msg = oracle.tensor_message(buf, row_bytes).tobytes()
+        assert _library_blake3(hc, msg) == oracle.tensor_root(buf, row_bytes)
 
 
 def test_single_step_bf16_conversion(hc):
