@@ -3,12 +3,14 @@
 // Per tensor, BLAKE3-256 of its bytes in a fixed interleaved order; per
 // fragment, BLAKE3-256 of a 64-byte shape/dtype header followed by the 2L
 // tensor roots (K^0, V^0, ..., K^{L-1}, V^{L-1}). In every full 64 KiB stripe of
-// a tensor, chunk 64 s + k (1 KiB, the BLAKE3 chunk) is made of the 16-byte
-// pieces k, k+64, k+128, k+192 of each of the stripe's 16 steps of 4 KiB; the
-// bytes after the last full stripe keep their order. That order is chosen for
-// 64-wide wavefronts: one wave takes one stripe, lane k hashes chunk k (16
-// dependent compressions with the next blocks in flight), and each of the four
-// 16-byte loads of a step reads 1 KiB of contiguous memory across the wave. The
+// a tensor, chunk 64 s + k (1 KiB, the BLAKE3 chunk) takes four 16-byte pieces
+// from each of the stripe's 16 steps of 4 KiB: with P pieces per half row,
+// f = (k / P) 2P + k % P, its second-half partner f + P, and f + 128,
+// f + 128 + P. The bytes after the last full stripe keep their order. That order
+// is chosen for 64-wide wavefronts: one wave takes one stripe, lane k hashes
+// chunk k (16 dependent compressions with the next blocks in flight), each of
+// the four 16-byte loads of a step covers whole half rows (1 KiB across the
+// wave), and the fused render finds both halves of each RoPE pair in one lane. The
 // work is VALU-bound (12 VALU ops per G step, 672 per block); the tree above the
 // chunks takes one launch per three levels over all tensors at full lane
 // occupancy (the parents add 1/16 of the chunk work).
