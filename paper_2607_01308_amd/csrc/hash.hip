@@ -203,24 +203,66 @@ __global__ __launch_bounds__(kSubLanes) void hash_subtree_kernel(
   o[1] = make_uint4(w[4], w[5], w[6], w[7]);
 }
 
-// Id = BLAKE3-256(header || root(K^0) || root(V^0) || ...), one lane per
-// fragment. The message is L + 1 blocks: the header, then per layer the pair of
-// roots (K, V). Chunks are hashed in order; completed subtrees are merged as soon
-// as a chunk count allows (a stack of chaining values, one per set bit of the
-// chunks seen), the last chunk is merged with the stack from the top down, and
-// ROOT marks the single chunk or the last parent.
+// Fold cnt (>= 1) chaining values held in LDS (word w of value p at
+// [p * 8 + w][lane slot], lds_w words apart per value) into one, level by level:
+// value j of a level is the BLAKE3 parent of values 2j and 2j+1 of the level
+// below, an unpaired last value is carried up. ROOT marks the final compression
+// when root is set. All 64 lanes of the (one-wave) workgroup take part.
+__device__ __forceinline__ void fold_cvs(uint32_t* lds, int cnt, bool root, int lane) {
+  while (cnt > 1) {
+    const int nn = (cnt + 1) >> 1;
+    uint32_t m[16];
+    const bool pair = lane < nn && 2 * lane + 1 < cnt;
+    const bool copy = lane < nn && 2 * lane + 1 >= cnt;
+    if (lane < nn) {
+#pragma unroll
+      for (int k = 0; k < 8; ++k) m[k] = lds[(2 * lane) * 8 + k];
+      if (pair) {
+#pragma unroll
+        for (int k = 0; k < 8; ++k) m[8 + k] = lds[(2 * lane + 1) * 8 + k];
+      }
+    }
+    __syncthreads();
+    if (pair) {
+      B3Cv cv;
+      b3_init(cv);
+      b3_compress(cv, m, 0, 64, kB3Parent | (root && nn == 1 ? kB3Root : 0u));
+#pragma unroll
+      for (int k = 0; k < 8; ++k) lds[lane * 8 + k] = cv.h[k];
+    } else if (copy) {
+#pragma unroll
+      for (int k = 0; k < 8; ++k) lds[lane * 8 + k] = m[k];
+    }
+    __syncthreads();
+    cnt = nn;
+  }
+}
+
+// Id = BLAKE3-256(header || root(K^0) || root(V^0) || ...), one 64-lane
+// workgroup per fragment. The message is L + 1 blocks (the header, then per
+// layer the pair of roots K, V) in C = ceil((L + 1) / 16) chunks. Lane k hashes
+// chunk 64 g + k of each group g of 64 chunks; a full group is an aligned
+// complete subtree of BLAKE3's left-balanced tree and is folded into one value,
+// the last group into the value of its own subtree (carries included); then the
+// group values are folded. ROOT marks the single chunk (C = 1) or the last
+// compression.
+constexpr int kFinalGroups = 32;   // 32 x 64 chunks: L + 1 <= 32768 blocks
+
 __global__ __launch_bounds__(64) void hash_final_kernel(
     const int64_t* __restrict__ table, int32_t n, int64_t stride, int32_t L, int32_t H,
     int32_t d, uint32_t dtype_code, uint32_t esize, const int64_t* __restrict__ base_last,
     const uint8_t* __restrict__ select, uint32_t want, const uint8_t* __restrict__ roots,
     uint8_t* __restrict__ digests) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n) return;
-  if (select && select[i] != want) return;
+  __shared__ uint32_t chunk_cv[64 * 8];
+  __shared__ uint32_t group_cv[kFinalGroups * 8];
+  const int i = blockIdx.x;
+  const int lane = threadIdx.x;
+  if (select && select[i] != want) return;   // uniform over the workgroup
   const uint64_t T = (uint64_t)table[(int64_t)i * stride];
   const uint8_t* r = roots + base_last[i] * 32;
   const int64_t blocks = (int64_t)L + 1;
   const int64_t chunks = (blocks + kB3ChunkBlocks - 1) / kB3ChunkBlocks;
+  const int groups = (int)((chunks + 63) / 64);
   auto load = [&](int64_t g, uint32_t (&w)[16]) {
     if (g == 0) {
       const uint32_t h[16] = {0x52464D43u, 0x31304741u,  // "CMFRAG01"
@@ -233,24 +275,25 @@ __global__ __launch_bounds__(64) void hash_final_kernel(
       load_block64(r + (g - 1) * 64, w);
     }
   };
-  B3Cv stack[40];  // chunk counts below 2^40
-  int sp = 0;
-  B3Cv cv;
-  for (int64_t c = 0; c < chunks; ++c) {
-    const int64_t g0 = c * kB3ChunkBlocks;
-    const int64_t nb = blocks - g0 < kB3ChunkBlocks ? blocks - g0 : kB3ChunkBlocks;
-    b3_chunk(cv, nb, (uint64_t)c, chunks == 1,
-             [&](int64_t b, uint32_t (&w)[16]) { load(g0 + b, w); });
-    if (c + 1 < chunks) {
-      for (int64_t total = c + 1; (total & 1) == 0; total >>= 1) b3_parent(cv, stack[--sp], cv, false);
-      stack[sp++] = cv;
+  for (int g = 0; g < groups; ++g) {
+    const int64_t c = (int64_t)g * 64 + lane;
+    const int cnt = (int)(chunks - (int64_t)g * 64 < 64 ? chunks - (int64_t)g * 64 : 64);
+    if (c < chunks) {
+      const int64_t g0 = c * kB3ChunkBlocks;
+      const int64_t nb = blocks - g0 < kB3ChunkBlocks ? blocks - g0 : kB3ChunkBlocks;
+      B3Cv cv;
+      b3_chunk(cv, nb, (uint64_t)c, chunks == 1,
+               [&](int64_t b, uint32_t (&w)[16]) { load(g0 + b, w); });
+#pragma unroll
+      for (int k = 0; k < 8; ++k) chunk_cv[lane * 8 + k] = cv.h[k];
     }
+    __syncthreads();
+    fold_cvs(chunk_cv, cnt, groups == 1, lane);
+    if (lane < 8) group_cv[g * 8 + lane] = chunk_cv[lane];
+    __syncthreads();
   }
-  while (sp > 0) {
-    --sp;
-    b3_parent(cv, stack[sp], cv, sp == 0);
-  }
-  store_cv(digests + (int64_t)i * 32, cv);
+  fold_cvs(group_cv, groups, true, lane);
+  if (lane < 8) reinterpret_cast<uint32_t*>(digests + (int64_t)i * 32)[lane] = group_cv[lane];
 }
 
 }  // namespace
@@ -314,8 +357,7 @@ hipError_t launch_hash_tree(const SetDesc& s, const HashLayout& lay, const uint8
   {
     ScopedTiming tm(K_HASH_FINAL, stream);
     const uint32_t code = s.dtype;  // cm_dtype value doubles as the header dtype code
-    hipLaunchKernelGGL(hash_final_kernel, dim3((uint32_t)((s.n + 63) / 64)), dim3(64), 0,
-                       stream, s.table_dev, s.n, s.stride, s.L, s.H, s.d, code,
+    hipLaunchKernelGGL(hash_final_kernel, dim3((uint32_t)s.n), dim3(64), 0, stream, s.table_dev, s.n, s.stride, s.L, s.H, s.d, code,
                        (uint32_t)s.esize, base + lay.levels * nb1, select, want,
                        buf[launch & 1], digests);
   }
