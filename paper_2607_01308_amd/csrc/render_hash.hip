@@ -170,28 +170,10 @@ __global__ __launch_bounds__(kThreads) CM_FUSED_OCCUPANCY void render_hash_kerne
       tt = r0 - hh * T;
     }
     const int64_t gap = (T_out - T) << rb_shift;   // end of a head's rows -> next head
-    // One full step: prefetch the next one, hash this one into the lane's chunk,
-    // rotate it if needed, store it. WRAPS: the fragment is shorter than a step
-    // (T < rows per step), so a step may span several heads.
-    auto step = [&](auto wraps, const u32x4 (&x)[4], u32x4 (&nx)[4], int j) {
-      // the last step loads itself again: the loads stay unconditional, which
-      // keeps the count of memory operations the same on every path
-      const int jn = j + 1 < full_steps ? j + 1 : j;
-      const uint8_t* sb = src + ((int64_t)jn << 12);     // wave-uniform base
-#pragma unroll
-      for (int k = 0; k < 4; ++k) nx[k] = ld16(sb + po[k]);
-      if (hash_steps) compress_pieces(st, x, chunk0 + lane, b3_chunk_flags(j, full_steps, false));
-      u32x4 y[4] = {x[0], x[1], x[2], x[3]};
-      if (rotate) {
-        if constexpr (STYLE == CM_ROPE_HALF) {
-          rotate_pair_half<ESIZE>(y[0], y[1], cs, sn);
-          rotate_pair_half<ESIZE>(y[2], y[3], cs, sn);
-        } else {
-#pragma unroll
-          for (int k = 0; k < 4; ++k)
-            y[k] = rotate_piece_il<ESIZE>(x[k], cs + (k & 1) * NA, sn + (k & 1) * NA);
-        }
-      }
+    // Store one step's output y at the current step position (head hh, row tt),
+    // then move the position on by one step. WRAPS: the fragment is shorter than
+    // a step (T < rows per step), so a step may span several heads.
+    auto store_step = [&](auto wraps, const u32x4 (&y)[4]) {
       if constexpr (!decltype(wraps)::value) {
         // the step's rows are consecutive rows of the source and, unless the
         // step crosses the end of a head (at most one step per head; the rows
@@ -202,9 +184,10 @@ __global__ __launch_bounds__(kThreads) CM_FUSED_OCCUPANCY void render_hash_kerne
 #pragma unroll
           for (int k = 0; k < 4; ++k) st_stream(db + po[k], y[k]);
         } else {
+          uint8_t* db2 = db + gap;                                      // wave-uniform
 #pragma unroll
           for (int k = 0; k < 4; ++k)
-            st_stream(db + po[k] + ((int64_t)(po[k] >> rb_shift) >= left ? gap : 0), y[k]);
+            st_stream(((int)(po[k] >> rb_shift) >= (int)left ? db2 : db) + po[k], y[k]);
         }
         tt += rps;
         const bool next_head = tt >= T;
@@ -221,22 +204,54 @@ __global__ __launch_bounds__(kThreads) CM_FUSED_OCCUPANCY void render_hash_kerne
         }
       }
     };
-    // Software pipeline over the full steps, two buffers. The first step is
-    // peeled so that the loop is entered with the same operations in flight as
-    // on its back edge (this step's loads, the previous stores): the wait for
-    // a step's data then never covers the stores just issued.
+    // One full step j. x holds its data, loaded one step earlier. First the
+    // wave waits for that data (the only memory operations older than it were
+    // issued a step earlier too); then it stores the previous step's output,
+    // which sits in nx (PENDING: there is one), and prefetches step j + 1 into
+    // nx; then it hashes x into the lane's chunk and rotates x in place, which
+    // leaves step j's output in x. Waiting before the stores and loads are
+    // issued keeps every wait clear of memory operations issued in this step.
+    auto step = [&](auto wraps, auto pending, u32x4 (&x)[4], u32x4 (&nx)[4], int j) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) launder(x[k]);   // wait for x here, before the stores
+      if constexpr (decltype(pending)::value) store_step(wraps, nx);
+      // the last step loads itself again: the loads stay unconditional, which
+      // keeps the count of memory operations the same on every path
+      const int jn = j + 1 < full_steps ? j + 1 : j;
+      const uint8_t* sb = src + ((int64_t)jn << 12);     // wave-uniform base
+#pragma unroll
+      for (int k = 0; k < 4; ++k) nx[k] = ld16(sb + po[k]);
+      if (hash_steps) compress_pieces(st, x, chunk0 + lane, b3_chunk_flags(j, full_steps, false));
+      if (rotate) {
+        if constexpr (STYLE == CM_ROPE_HALF) {
+          rotate_pair_half<ESIZE>(x[0], x[1], cs, sn);
+          rotate_pair_half<ESIZE>(x[2], x[3], cs, sn);
+        } else {
+#pragma unroll
+          for (int k = 0; k < 4; ++k)
+            x[k] = rotate_piece_il<ESIZE>(x[k], cs + (k & 1) * NA, sn + (k & 1) * NA);
+        }
+      }
+    };
+    // Software pipeline over the full steps, two buffers; the last step's
+    // output is stored after the loop.
     auto run = [&](auto wraps) {
       u32x4 bufa[4], bufb[4];
 #pragma unroll
       for (int k = 0; k < 4; ++k) bufa[k] = ld16(src + po[k]);
-      step(wraps, bufa, bufb, 0);
+      step(wraps, std::false_type{}, bufa, bufb, 0);
       int j = 1;
       while (j + 1 < full_steps) {
-        step(wraps, bufb, bufa, j);
-        step(wraps, bufa, bufb, j + 1);
+        step(wraps, std::true_type{}, bufb, bufa, j);
+        step(wraps, std::true_type{}, bufa, bufb, j + 1);
         j += 2;
       }
-      if (j < full_steps) step(wraps, bufb, bufa, j);
+      if (j < full_steps) {
+        step(wraps, std::true_type{}, bufb, bufa, j);
+        store_step(wraps, bufb);
+      } else {
+        store_step(wraps, bufa);
+      }
     };
     if (full_steps > 0) {
       if (T >= rps) run(std::false_type{});
