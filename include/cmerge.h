@@ -21,6 +21,8 @@
  *   cm_equal_key_mask       the deliveries whose digest the order needs
  *   cm_fragment_hash_select the Id of a subset of the deliveries
  *   cm_render_merge_hash    the render plus the remaining Ids from its loads
+ *   cm_render_deliveries    steps 1-5 over a batch of deliveries in one call, with
+ *                           no host round trip
  *
  * Conventions
  *   - Every function returns int32_t: CM_OK (0) or a negative cm_status. No
@@ -253,7 +255,7 @@ int32_t cm_render_merge_devplan(const cm_fragset* set, int64_t* plan_dev, const 
                                 size_t workspace_bytes, void* stream);
 /* Steps 1 and 4-5 in one pass: the render of cm_render_merge and, for every
  * slot delivery i with select_dev[i] == 0, its Id (as cm_fragment_hash) written
- * to digests_dev[i]; the Id's leaf level is computed from the same loads that
+ * to digests_dev[i]; the Id's chunk level is computed from the same loads that
  * feed the render, so each fragment byte is read once. The digests of all
  * other deliveries are left untouched (give them select 1 and compute them
  * before, e.g. with cm_fragment_hash_select: with select = the output of
@@ -263,6 +265,29 @@ int32_t cm_render_merge_hash(const cm_fragset* set, const int64_t* plan_dev,
                              const int64_t* plan_host, const cm_rope* rope,
                              const uint8_t* select_dev, uint8_t* digests_dev, void* out_dev,
                              int64_t T_out, void* workspace, size_t workspace_bytes,
+                             void* stream);
+
+/* Steps 1-5 over a batch of deliveries (Render of Alg. 2 after Ingest of each
+ * delivery), enqueued on `stream` in one call with nothing waiting for the host:
+ * cm_fragment_knorm (keys_dev), cm_equal_key_mask (mask_dev), the Ids of the
+ * deliveries whose keys collide (cm_fragment_hash_select with mask 1), the
+ * dedupe and canonical order (plan_dev, as cm_canonical_order), then the render
+ * fused with every other Id (cm_render_merge_hash), reading the plan on the
+ * device. The merged cache of the plan's length T_out is written to the start of
+ * out_dev as [L][2][1][H][T_out][d] (each layer's K then V), so out_dev must hold
+ * that for T_out = T_cap rows: T_cap >= the sum of all delivery lengths (which
+ * bounds T_out) is required. After the stream has finished, the caller reads
+ * plan_dev: its status (CM_ENONFINITE if a score is not finite; then nothing is
+ * rendered and the digests of the non-colliding deliveries are not written), T_out,
+ * the order, offsets and the slot of each delivery.
+ * routing_layer, tail_len: as cm_fragment_knorm (tail_len = the smallest length
+ * for Eq. (3)'s T*). keys_dev: n doubles; mask_dev: n bytes; digests_dev: n * 32
+ * bytes, 16-byte aligned; plan_dev: cm_plan_elems(n) int64; all device, written by
+ * the call. Workspace: cm_workspace_size() bytes, used by each stage in turn. */
+int32_t cm_render_deliveries(const cm_fragset* set, int32_t routing_layer, int64_t tail_len,
+                             const cm_rope* rope, double* keys_dev, uint8_t* mask_dev,
+                             uint8_t* digests_dev, int64_t* plan_dev, void* out_dev,
+                             int64_t T_cap, void* workspace, size_t workspace_bytes,
                              void* stream);
 
 /* ---------------------------------------------------------------- paged render

@@ -22,6 +22,7 @@ from .binding import (  # noqa: F401
     render_merge_devplan,
     render_merge_range,
     render_merge_hash,
+    render_deliveries_async,
     timing_enable,
     timing_query,
     timing_reset,

@@ -188,6 +188,22 @@ def render_merge_hash(batch: FragmentBatch, plan_dev: torch.Tensor, plan_host: n
                                          _stream(stream, batch.device)), "cm_render_merge_hash")
 
 
+def render_deliveries_async(batch: FragmentBatch, routing_layer: int, tail_len: int,
+                            rope_base: float, style: str, keys: torch.Tensor, mask: torch.Tensor,
+                            digests: torch.Tensor, plan_dev: torch.Tensor, out: torch.Tensor,
+                            T_cap: int, workspace: torch.Tensor, stream=None) -> None:
+    """cm_render_deliveries: steps 1-5 enqueued in one call; nothing waits for the
+    host. out holds [L, 2, 1, H, T_cap, d]; the cache of the plan's T_out rows is
+    written to its first L * 2 * H * T_out * d elements."""
+    rope = C.CmRope(base=float(rope_base), style=_STYLES[style], reserved=0)
+    C.check(C.lib().cm_render_deliveries(ctypes.byref(batch.struct), routing_layer, tail_len,
+                                         ctypes.byref(rope), _ptr(keys), _ptr(mask),
+                                         _ptr(digests), _ptr(plan_dev), _ptr(out), T_cap,
+                                         _ptr(workspace),
+                                         workspace.numel() * workspace.element_size(),
+                                         _stream(stream, batch.device)), "cm_render_deliveries")
+
+
 def plan_elems(n: int) -> int:
     return int(C.lib().cm_plan_elems(n))
 

@@ -486,12 +486,55 @@ int32_t cm_render_merge_hash(const cm_fragset* set, const int64_t* plan_dev,
   const cm::RenderLayout rlay = cm::render_layout(s);
   const size_t need = cm::align_up(hlay.bytes, cm::kWsAlign) + rlay.bytes;
   if ((st = check_ws(workspace, workspace_bytes, need)) != CM_OK) return st;
-  const int64_t tasks = cm::stripe_tasks(s, plan_host, (int32_t)cm::kStripeBlocks);
-  hipError_t e = cm::launch_render_hash(s, hlay, rlay, plan_dev, (int32_t)nu, tasks, T_out,
-                                        rope->base, rope->style, select_dev, digests_dev, out_dev,
+  hipError_t e = cm::launch_render_hash(s, hlay, rlay, plan_dev, rope->base, rope->style,
+                                        select_dev, digests_dev, out_dev,
                                         static_cast<uint8_t*>(workspace),
                                         static_cast<hipStream_t>(stream));
   return e == hipSuccess ? CM_OK : fail_hip(e, "cm_render_merge_hash");
+}
+
+int32_t cm_render_deliveries(const cm_fragset* set, int32_t routing_layer, int64_t tail_len,
+                             const cm_rope* rope, double* keys_dev, uint8_t* mask_dev,
+                             uint8_t* digests_dev, int64_t* plan_dev, void* out_dev,
+                             int64_t T_cap, void* workspace, size_t workspace_bytes,
+                             void* stream) {
+  g_err.clear();
+  cm::SetDesc s;
+  int32_t st = check_set(set, &s);
+  if (st != CM_OK) return st;
+  if ((st = check_rope(rope)) != CM_OK) return st;
+  if (routing_layer < 0 || routing_layer >= s.L)
+    return fail(CM_EINVAL, "routing_layer must be in [0, L), got " + std::to_string(routing_layer));
+  const int64_t tmin = min_T(s);
+  if (tail_len < 1 || tail_len > tmin)
+    return fail(CM_EINVAL, "tail_len must be in [1, min T] = [1, " + std::to_string(tmin) + "], got " +
+                               std::to_string(tail_len));
+  if (!keys_dev || !aligned(keys_dev, 8)) return fail(CM_EINVAL, "keys_dev is NULL or misaligned");
+  if (!mask_dev) return fail(CM_EINVAL, "mask_dev is NULL");
+  if (!digests_dev || !aligned(digests_dev, 16))
+    return fail(CM_EINVAL, "digests_dev is NULL or not 16-byte aligned");
+  if (!plan_dev || !aligned(plan_dev, 8)) return fail(CM_EINVAL, "plan_dev is NULL or misaligned");
+  if (!out_dev || !aligned(out_dev, 16))
+    return fail(CM_EINVAL, "out_dev is NULL or not 16-byte aligned");
+  int64_t T_all = 0;
+  for (int i = 0; i < s.n; ++i) T_all += s.T(i);
+  if (T_cap < T_all)
+    return fail(CM_ESHAPE, "T_cap must be at least the sum of the delivery lengths (" +
+                               std::to_string(T_all) + "), got " + std::to_string(T_cap));
+  if ((st = check_ws(workspace, workspace_bytes, workspace_need(s))) != CM_OK) return st;
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  hipStream_t sm = static_cast<hipStream_t>(stream);
+  // the workspace is reused by each stage in turn: they run in order on one stream
+  hipError_t e = cm::launch_knorm(s, cm::knorm_layout(s, tail_len), routing_layer, tail_len,
+                                  keys_dev, ws, sm);
+  if (e == hipSuccess) e = cm::launch_equal_key_mask(s, keys_dev, mask_dev, sm);
+  const cm::HashLayout hlay = cm::hash_layout(s);
+  if (e == hipSuccess) e = cm::launch_hash(s, hlay, mask_dev, 1, digests_dev, ws, sm);
+  if (e == hipSuccess) e = cm::launch_order(s, keys_dev, digests_dev, true, plan_dev, sm);
+  if (e == hipSuccess)
+    e = cm::launch_render_hash(s, hlay, cm::render_layout(s), plan_dev, rope->base, rope->style,
+                               mask_dev, digests_dev, out_dev, ws, sm);
+  return e == hipSuccess ? CM_OK : fail_hip(e, "cm_render_deliveries");
 }
 
 }  // extern "C"

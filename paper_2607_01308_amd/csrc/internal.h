@@ -122,14 +122,14 @@ hipError_t launch_order(const SetDesc& s, const double* keys, const uint8_t* dig
 hipError_t launch_render_prep(const SetDesc& s, const RenderLayout& lay, const int64_t* plan_dev,
                               int32_t n_unique, double base, int32_t style, int32_t stripe_blocks,
                               const uint8_t* select, uint8_t* ws, hipStream_t stream);
-// Work items of the fused kernel: 2L * stripes of stripe_blocks per slot.
-int64_t stripe_tasks(const SetDesc& s, const int64_t* plan_host, int32_t stripe_blocks);
-// Render plus, for every slot delivery i with select[i] == 0, its Id (leaf level
-// fused into the render, then the tree). ws = hash workspace, then render's.
+// Render plus, for every slot delivery i with select[i] == 0, its Id (chunk
+// level fused into the render, then the tree). ws = hash workspace, then
+// render's. The slot count, T_out and the task count are read from the plan on
+// the device; out must hold the merged cache of the plan's T_out rows.
 hipError_t launch_render_hash(const SetDesc& s, const HashLayout& hlay, const RenderLayout& rlay,
-                              const int64_t* plan_dev, int32_t n_unique, int64_t total_tasks,
-                              int64_t T_out, double base, int32_t style, const uint8_t* select,
-                              uint8_t* digests, void* out, uint8_t* ws, hipStream_t stream);
+                              const int64_t* plan_dev, double base, int32_t style,
+                              const uint8_t* select, uint8_t* digests, void* out, uint8_t* ws,
+                              hipStream_t stream);
 // Rows [row0, T_out) of every row block are rendered into `out`, whose row
 // blocks are T_cap rows long (row0 = 0, T_cap = T_out: the whole merged cache).
 struct RenderRange {

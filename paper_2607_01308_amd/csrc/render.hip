@@ -137,7 +137,8 @@ __global__ __launch_bounds__(256) void render_unit_prep_kernel(
 // One workgroup: per-slot cos/sin(off_s * theta_j), theta_j = base^(-2j/d), in
 // fp64, in the piece-ordered layout of rotate.h. With stripe_blocks > 0 also the
 // per-slot work-unit bases of the fused hash+render (2L * stripes of that many
-// 64-byte blocks per slot, exclusive scan) and, with a select mask, hsel[i] = 0
+// 64-byte blocks per slot, exclusive scan; the total at index n as well, none if
+// the plan's status is an error) and, with a select mask, hsel[i] = 0
 // for the slot deliveries whose Id the fused kernel computes (select[i] == 0),
 // 1 for every other delivery.
 __global__ __launch_bounds__(1024) void render_prep_kernel(
@@ -181,6 +182,8 @@ __global__ __launch_bounds__(1024) void render_prep_kernel(
     __syncthreads();
   }
   if (stripe_blocks > 0) {
+    // a plan whose status is an error (a non-finite score) gets no tasks
+    if (plan[CM_PLAN_STATUS] != CM_OK || n_u < 0 || n_u > n) n_u = 0;
     const int64_t len = tid < n_u ? plan[CM_PLAN_HEADER + 2 * (int64_t)n + tid] : 0;
     int64_t x = 0;
     if (tid < n_u)
@@ -195,7 +198,10 @@ __global__ __launch_bounds__(1024) void render_prep_kernel(
       __syncthreads();
     }
     if (tid < n_u) unit_base[tid] = sc[tid] - x;
-    if (tid == (int)blockDim.x - 1) unit_base[n_u] = sc[tid];
+    if (tid == (int)blockDim.x - 1) {
+      unit_base[n_u] = sc[tid];
+      unit_base[n] = sc[tid];          // the task total, where the fused kernel reads it
+    }
     if (hsel && tid < n_u) {
       const int64_t i = plan[CM_PLAN_HEADER + tid];
       if (select[i] == 0) hsel[i] = 0;

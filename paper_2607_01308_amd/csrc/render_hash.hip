@@ -102,8 +102,8 @@ __device__ __forceinline__ uint8_t* dest_wrapped(uint8_t* out_t, int64_t hh, int
 template <int ESIZE, int STYLE, int HB>
 __global__ __launch_bounds__(kThreads) CM_FUSED_OCCUPANCY void render_hash_kernel(
     const int64_t* __restrict__ table, int64_t stride, int32_t n, const int64_t* __restrict__ plan,
-    const int64_t* __restrict__ task_base, int32_t n_u, int64_t total_tasks,
-    const double* __restrict__ angles, int32_t H, int32_t d, int64_t T_out,
+    const int64_t* __restrict__ task_base, const double* __restrict__ angles, int32_t H,
+    int32_t d,
     const uint8_t* __restrict__ select, const int64_t* __restrict__ base0,
     uint8_t* __restrict__ nodes, uint8_t* __restrict__ out) {
   constexpr int EP = 16 / ESIZE;                   // elements per 16-byte piece
@@ -123,6 +123,11 @@ __global__ __launch_bounds__(kThreads) CM_FUSED_OCCUPANCY void render_hash_kerne
   const uint32_t pf = (uint32_t)((lane / hp) * ppr + cp) * 16;
   const uint32_t po[4] = {pf, pf + (uint32_t)hp * 16, pf + 2048, pf + (uint32_t)hp * 16 + 2048};
   const int64_t waves = (int64_t)gridDim.x * kWaves;
+  // the plan and the task bases are read on the device: a plan the host has not
+  // seen is rendered as it stands (its length T_out fits the output by contract)
+  const int n_u = (int)plan[CM_PLAN_NUNIQUE];
+  const int64_t T_out = plan[CM_PLAN_TOUT];
+  const int64_t total_tasks = task_base[n];      // 0 for a plan whose status is an error
   for (int64_t task = (int64_t)blockIdx.x * kWaves + wave; task < total_tasks; task += waves) {
     int lo = 0, hi = n_u - 1;
     while (lo < hi) {
@@ -288,25 +293,15 @@ __global__ __launch_bounds__(kThreads) CM_FUSED_OCCUPANCY void render_hash_kerne
 
 }  // namespace
 
-int64_t stripe_tasks(const SetDesc& s, const int64_t* plan_host, int32_t stripe_blocks) {
-  const int64_t nu = plan_host[CM_PLAN_NUNIQUE];
-  int64_t tasks = 0;
-  for (int64_t k = 0; k < nu; ++k) {
-    const int64_t blocks = (plan_host[CM_PLAN_HEADER + 2 * (int64_t)s.n + k] * token_bytes_of(s)) >> 6;
-    tasks += 2 * (int64_t)s.L * ((blocks + stripe_blocks - 1) / stripe_blocks);
-  }
-  return tasks;
-}
-
 hipError_t launch_render_hash(const SetDesc& s, const HashLayout& hlay, const RenderLayout& rlay,
-                              const int64_t* plan_dev, int32_t n_unique, int64_t total_tasks,
-                              int64_t T_out, double base, int32_t style, const uint8_t* select,
-                              uint8_t* digests, void* out, uint8_t* ws, hipStream_t stream) {
+                              const int64_t* plan_dev, double base, int32_t style,
+                              const uint8_t* select, uint8_t* digests, void* out, uint8_t* ws,
+                              hipStream_t stream) {
   uint8_t* hws = ws;
   uint8_t* rws = ws + align_up(hlay.bytes, kWsAlign);
   hipError_t e = launch_hash_prep(s, hlay, hws, stream);
   if (e != hipSuccess) return e;
-  if ((e = launch_render_prep(s, rlay, plan_dev, n_unique, base, style, (int32_t)kStripeBlocks,
+  if ((e = launch_render_prep(s, rlay, plan_dev, s.n, base, style, (int32_t)kStripeBlocks,
                               select, rws, stream)) != hipSuccess)
     return e;
   const uint8_t* hsel = rws + rlay.off_hsel;  // 0: slot delivery whose Id is computed here
@@ -314,9 +309,9 @@ hipError_t launch_render_hash(const SetDesc& s, const HashLayout& hlay, const Re
     const int64_t* base_tab = reinterpret_cast<const int64_t*>(hws + hlay.off_tables);
     const int64_t* tasks = reinterpret_cast<const int64_t*>(rws + rlay.off_tiles);
     const double* angles = reinterpret_cast<const double*>(rws + rlay.off_angles);
-    const int64_t full = (total_tasks + kWaves - 1) / kWaves;
-    const int64_t cap = (int64_t)device_cu_count() * CM_FUSED_BLOCKS_PER_CU;
-    const dim3 grid((uint32_t)(full < cap ? full : cap));
+    // the task count is known on the device only: a persistent grid of a few
+    // workgroups per CU strides over it
+    const dim3 grid((uint32_t)(device_cu_count() * CM_FUSED_BLOCKS_PER_CU));
     ScopedTiming tm(K_RENDER_HASH, stream);
     uint8_t* nodes = hws + hlay.off_buf0;
     uint8_t* o = reinterpret_cast<uint8_t*>(out);
@@ -324,12 +319,12 @@ hipError_t launch_render_hash(const SetDesc& s, const HashLayout& hlay, const Re
       constexpr int STYLE = decltype(tag)::style, HB = decltype(tag)::hb;
       if (s.esize == 2)
         hipLaunchKernelGGL((render_hash_kernel<2, STYLE, HB>), grid, dim3(kThreads), 0, stream,
-                           s.table_dev, s.stride, s.n, plan_dev, tasks, n_unique, total_tasks,
-                           angles, s.H, s.d, T_out, hsel, base_tab, nodes, o);
+                           s.table_dev, s.stride, s.n, plan_dev, tasks, angles, s.H, s.d, hsel,
+                           base_tab, nodes, o);
       else
         hipLaunchKernelGGL((render_hash_kernel<4, STYLE, HB>), grid, dim3(kThreads), 0, stream,
-                           s.table_dev, s.stride, s.n, plan_dev, tasks, n_unique, total_tasks,
-                           angles, s.H, s.d, T_out, hsel, base_tab, nodes, o);
+                           s.table_dev, s.stride, s.n, plan_dev, tasks, angles, s.H, s.d, hsel,
+                           base_tab, nodes, o);
     };
     dispatch_style(style, s.row_bytes, go);
   }

@@ -24,7 +24,8 @@ from . import _cabi as C
 from .binding import (FragmentBatch, bag_plan, canonical_order, equal_key_mask, fragment_hash,
                       fragment_hash_select, fragment_knorm, multiset_order, plan_elems,
                       paged_render, paged_tables, paged_workspace_size, render_merge,
-                      render_merge_devplan, render_merge_hash, render_merge_range, workspace_size)
+                      render_deliveries_async, render_merge_devplan, render_merge_hash,
+                      render_merge_range, workspace_size)
 from .binding import PagedSet
 
 _WS: Dict[tuple, torch.Tensor] = {}
@@ -73,26 +74,61 @@ def _plan_to_host(plan_dev: torch.Tensor, stream) -> np.ndarray:
     return buf.numpy().copy()
 
 
-@dataclass
 class RenderResult:
-    cache: tuple                 # per layer (K, V), each [1, H, T_out, d]
-    merged: torch.Tensor         # the single [L, 2, 1, H, T_out, d] buffer behind `cache`
-    digests_dev: torch.Tensor    # [n, 32] uint8, per delivery
-    keys_dev: torch.Tensor       # [n] float64 S_i, per delivery
-    plan_host: Optional[np.ndarray]   # host copy of the plan (layout in include/cmerge.h)
-    tail_len: int
-    plan_dev: Optional[torch.Tensor] = None
+    """Result of a render: the merged cache (per layer (K, V), each [1, H, T_out, d],
+    views of one [L, 2, 1, H, T_out, d] buffer), per-delivery digests and keys,
+    and the plan (layout in include/cmerge.h).
+
+    A result of the fused pipeline is returned before the device has finished:
+    its plan travels to pinned host memory behind an event, and the first use of
+    the plan, T_out, `merged` or `cache` waits for it (a plan whose status is an
+    error raises then)."""
+
+    def __init__(self, cache=None, merged=None, digests_dev=None, keys_dev=None,
+                 plan_host: Optional[np.ndarray] = None, tail_len: int = 0,
+                 plan_dev: Optional[torch.Tensor] = None, pending=None):
+        self._cache = cache
+        self._merged = merged
+        self.digests_dev = digests_dev      # [n, 32] uint8, per delivery
+        self.keys_dev = keys_dev            # [n] float64 S_i, per delivery
+        self.plan_host = plan_host          # host copy of the plan
+        self.tail_len = tail_len
+        self.plan_dev = plan_dev
+        self._pending = pending             # (event, pinned plan copy, output buffer, shape, where)
 
     @property
     def plan(self) -> np.ndarray:
         """The plan on the host (copied from the device on first use when the
         render did not need it; a rejected plan raises)."""
         if self.plan_host is None:
-            self.plan_host = self.plan_dev.to("cpu").numpy()
-            status = int(self.plan_host[C.PLAN_STATUS])
-            if status != C.CM_OK:
-                raise C.CmError(status, "cm_render_merge_devplan", "the plan failed its device check")
+            if self._pending is not None:
+                event, pinned, _, _, where = self._pending
+                event.synchronize()
+                plan = pinned.numpy().copy()
+                _check_plan(plan, where)
+            else:
+                plan = self.plan_dev.to("cpu").numpy()
+                status = int(plan[C.PLAN_STATUS])
+                if status != C.CM_OK:
+                    raise C.CmError(status, "cm_render_merge_devplan",
+                                    "the plan failed its device check")
+            self.plan_host = plan
         return self.plan_host
+
+    @property
+    def merged(self) -> torch.Tensor:
+        if self._merged is None:
+            _, _, out, (L, H, d), _ = self._pending
+            T_out = self.T_out
+            self._merged = out[:L * 2 * H * T_out * d].view(L, 2, 1, H, T_out, d)
+        return self._merged
+
+    @property
+    def cache(self) -> tuple:
+        if self._cache is None:
+            m = self.merged
+            self._cache = tuple((m[l, 0], m[l, 1]) for l in range(m.shape[0]))
+        return self._cache
 
     @property
     def n_unique(self) -> int:
@@ -134,13 +170,17 @@ class RenderResult:
         return self.keys_dev.cpu().numpy()
 
 
+def _check_plan(plan_host: np.ndarray, where: str) -> None:
+    status = int(plan_host[C.PLAN_STATUS])
+    if status != C.CM_OK:
+        raise C.CmError(status, where, "plan status is not CM_OK "
+                        "(a score is NaN or infinite)" if status == C.CM_ENONFINITE else "")
+
+
 def _render_plan(batch: FragmentBatch, plan_dev: torch.Tensor, plan_host: np.ndarray,
                  rope_base: float, style: str, ws: torch.Tensor, stream, hash_select=None,
                  digests=None):
-    status = int(plan_host[C.PLAN_STATUS])
-    if status != C.CM_OK:
-        raise C.CmError(status, "cm_canonical_order", "plan status is not CM_OK "
-                        "(a score is NaN or infinite)" if status == C.CM_ENONFINITE else "")
+    _check_plan(plan_host, "cm_canonical_order")
     T_out = int(plan_host[C.PLAN_TOUT])
     merged = torch.empty((batch.L, 2, 1, batch.H, T_out, batch.d), dtype=batch.torch_dtype,
                          device=batch.device)
@@ -159,7 +199,15 @@ PIPELINES = ("fused", "overlap", "serial")
 def render_deliveries(deliveries: Union[FragmentBatch, Sequence], routing_layer: int,
                       rope_base: float, style: str = "half", stream=None,
                       pipeline: str = "fused") -> RenderResult:
-    """The whole path over a list of deliveries (duplicates allowed)."""
+    """The whole path over a list of deliveries (duplicates allowed).
+
+    fused (default): one library call enqueues every step (scores, the Ids of
+    deliveries whose keys collide, dedupe and order, then the render fused with
+    the remaining Ids), the plan staying on the device; the output is allocated
+    for the sum of the delivery lengths and the call returns without waiting (the
+    result waits for the plan on first use; a non-finite score raises then).
+    overlap / serial: the plan comes to the host before the render, which then
+    runs beside (overlap) or after (serial) the remaining Ids."""
     if pipeline not in PIPELINES:
         raise ValueError(f"pipeline must be one of {PIPELINES}")
     batch = deliveries if isinstance(deliveries, FragmentBatch) else FragmentBatch(deliveries)
@@ -172,6 +220,21 @@ def render_deliveries(deliveries: Union[FragmentBatch, Sequence], routing_layer:
         mask = torch.empty(batch.n, dtype=torch.uint8, device=dev)
         plan_dev = torch.empty(plan_elems(batch.n), dtype=torch.int64, device=dev)
         tail = min(batch.lengths)
+        if pipeline == "fused":
+            T_cap = int(sum(batch.lengths))
+            out = torch.empty(batch.L * 2 * batch.H * T_cap * batch.d, dtype=batch.torch_dtype,
+                              device=dev)
+            render_deliveries_async(batch, routing_layer, tail, rope_base, style, keys, mask,
+                                    digests, plan_dev, out, T_cap, ws, main)
+            # the plan follows the render to pinned host memory; nothing waits for it here
+            pinned = torch.empty(plan_dev.numel(), dtype=torch.int64, pin_memory=True)
+            pinned.copy_(plan_dev, non_blocking=True)
+            done = torch.cuda.Event()
+            done.record(main)
+            return RenderResult(digests_dev=digests, keys_dev=keys, tail_len=tail,
+                                plan_dev=plan_dev,
+                                pending=(done, pinned, out, (batch.L, batch.H, batch.d),
+                                         "cm_render_deliveries"))
         fragment_knorm(batch, routing_layer, tail, keys, ws, main)
         equal_key_mask(batch, keys, mask, main)
         fragment_hash_select(batch, mask, 1, digests, ws, main)   # the digests the order reads
@@ -184,16 +247,12 @@ def render_deliveries(deliveries: Union[FragmentBatch, Sequence], routing_layer:
             fragment_hash_select(batch, mask, 0, digests, _workspace(batch, 1), side)
             side_done = torch.cuda.Event()
             side_done.record(side)
-        elif pipeline == "serial":
+        else:
             fragment_hash_select(batch, mask, 0, digests, ws, main)
         canonical_order(batch, keys, digests, plan_dev, main)
         plan_host = _plan_to_host(plan_dev, main)
         try:
-            if pipeline == "fused":
-                merged, cache = _render_plan(batch, plan_dev, plan_host, rope_base, style, ws, main,
-                                             hash_select=mask, digests=digests)
-            else:
-                merged, cache = _render_plan(batch, plan_dev, plan_host, rope_base, style, ws, main)
+            merged, cache = _render_plan(batch, plan_dev, plan_host, rope_base, style, ws, main)
         finally:
             if side_done is not None:
                 main.wait_event(side_done)

@@ -247,6 +247,34 @@ def test_render_devplan_argument_checks(lib):
     assert call(14, rope=C.CmRope(base=0.0, style=0, reserved=0)) == C.CM_EINVAL
 
 
+def test_render_deliveries_argument_checks(lib):
+    fs = FakeSet(lengths=(5, 9))
+    _, need = _ws(lib, fs)
+    rope = C.CmRope(base=1e4, style=0, reserved=0)
+    keys, mask, dig = ctypes.c_void_p(0x10000), ctypes.c_void_p(0x20000), ctypes.c_void_p(0x30000)
+    plan, out, ws = ctypes.c_void_p(0x50000), ctypes.c_void_p(0x80000), ctypes.c_void_p(0x40000)
+
+    def call(layer=1, tail=5, T_cap=14, keys=keys, mask=mask, dig=dig, plan=plan, out=out,
+             rope=rope, ws_bytes=need):
+        return lib.cm_render_deliveries(fs.ref, layer, tail, ctypes.byref(rope), keys, mask, dig,
+                                        plan, out, T_cap, ws, ws_bytes, None)
+
+    assert call(ws_bytes=0) == C.CM_EWORKSPACE              # every other check passed
+    assert call(T_cap=100, ws_bytes=0) == C.CM_EWORKSPACE   # more room than needed is fine
+    assert call(T_cap=13) == C.CM_ESHAPE                    # below the sum of the lengths
+    assert call(layer=2) == C.CM_EINVAL
+    assert call(layer=-1) == C.CM_EINVAL
+    assert call(tail=0) == C.CM_EINVAL
+    assert call(tail=6) == C.CM_EINVAL                      # longer than the shortest delivery
+    assert call(keys=None) == C.CM_EINVAL
+    assert call(mask=None) == C.CM_EINVAL
+    assert call(dig=ctypes.c_void_p(0x30008)) == C.CM_EINVAL  # not 16-byte aligned
+    assert call(plan=None) == C.CM_EINVAL
+    assert call(out=None) == C.CM_EINVAL
+    bad = C.CmRope(base=-1.0, style=0, reserved=0)
+    assert call(rope=bad) == C.CM_EINVAL
+
+
 def test_render_range_argument_checks(lib):
     fs = FakeSet(lengths=(5, 9))
     _, need = _ws(lib, fs)

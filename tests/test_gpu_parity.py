@@ -127,9 +127,10 @@ def test_nonfinite_score_is_an_error():
     w = synth.custom("nan", dtype="bfloat16", d=128, H=2, L=2, lengths=(20, 30), routing_layer=1)
     frags, _ = gpu_deliveries(w)
     frags[1][1][0][0, 1, 25, 3] = float("nan")       # inside the routing layer's tail
-    with pytest.raises(cm.CmError) as e:
-        cm.render_deliveries(frags, w.routing_layer, w.rope_base)
-    assert e.value.status == -4
+    for pipe in cm.PIPELINES:            # fused: raised when the result is first used
+        with pytest.raises(cm.CmError) as e:
+            cm.render_deliveries(frags, w.routing_layer, w.rope_base, pipeline=pipe).T_out
+        assert e.value.status == -4
     frags2, _ = gpu_deliveries(w)
     frags2[1][1][0][0, 1, 3, 3] = float("inf")        # before the tail (T* = 20 -> rows 10..29)
     frags2[0][0][0][0, 0, 5, 7] = float("nan")        # another layer
