@@ -152,8 +152,9 @@ __global__ __launch_bounds__(kSubLanes) void hash_subtree_kernel(
     int64_t total_hi, const uint8_t* __restrict__ select, uint32_t want,
     const uint8_t* __restrict__ in, uint8_t* __restrict__ out) {
   // word w of the lane's node p at [p * 8 + w][lane]: consecutive lanes hit
-  // consecutive banks
-  __shared__ uint32_t lds[(1 << kSubLevels) * 8][kSubLanes];
+  // consecutive banks. The first level is folded straight from the children in
+  // memory, so the slots hold at most half of them.
+  __shared__ uint32_t lds[(1 << (kSubLevels - 1)) * 8][kSubLanes];
   const int lane = threadIdx.x;
   const int64_t g = (int64_t)blockIdx.x * kSubLanes + lane;
   if (g >= total_hi) return;
@@ -168,23 +169,35 @@ __global__ __launch_bounds__(kSubLanes) void hash_subtree_kernel(
   const int64_t first = j << K;
   int cur = (int)(m_lo - first < ((int64_t)1 << K) ? m_lo - first : ((int64_t)1 << K));
   const uint8_t* c = in + (base_lo[i] + t * m_lo + first) * 32;
-  for (int q = 0; q < cur; ++q) {
-    const uint4* src = reinterpret_cast<const uint4*>(c + q * 32);
-    const uint4 a = src[0], b = src[1];
-    const uint32_t w[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
-#pragma unroll
-    for (int k = 0; k < 8; ++k) lds[q * 8 + k][lane] = w[k];
-  }
   for (int lev = 1; lev <= K; ++lev) {
     const uint32_t flags = kB3Parent | (nodes_at(m0, v0 + lev) == 1 ? kB3Root : 0u);
     const int nn = (cur + 1) >> 1;
     for (int p = 0; p < nn; ++p) {
       uint32_t m[16];
+      const bool pair = 2 * p + 1 < cur;
+      if (lev == 1) {
+        // children 2p and 2p + 1 (an unpaired last child alone)
+        const uint4* q = reinterpret_cast<const uint4*>(c + (int64_t)(2 * p) * 32);
+        const int words = pair ? 4 : 2;
 #pragma unroll
-      for (int k = 0; k < 8; ++k) m[k] = lds[2 * p * 8 + k][lane];
-      if (2 * p + 1 < cur) {
+        for (int k = 0; k < 4; ++k) {
+          if (k < words) {
+            const uint4 v = q[k];
+            m[4 * k + 0] = v.x;
+            m[4 * k + 1] = v.y;
+            m[4 * k + 2] = v.z;
+            m[4 * k + 3] = v.w;
+          }
+        }
+      } else {
 #pragma unroll
-        for (int k = 0; k < 8; ++k) m[8 + k] = lds[(2 * p + 1) * 8 + k][lane];
+        for (int k = 0; k < 8; ++k) m[k] = lds[2 * p * 8 + k][lane];
+        if (pair) {
+#pragma unroll
+          for (int k = 0; k < 8; ++k) m[8 + k] = lds[(2 * p + 1) * 8 + k][lane];
+        }
+      }
+      if (pair) {
         B3Cv cv;
         b3_init(cv);
         b3_compress(cv, m, 0, 64, flags);
