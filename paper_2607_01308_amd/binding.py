@@ -20,8 +20,15 @@ def _ptr(t: torch.Tensor) -> ctypes.c_void_p:
     return ctypes.c_void_p(t.data_ptr())
 
 
-def _stream(stream, device) -> ctypes.c_void_p:
-    s = stream if stream is not None else torch.cuda.current_stream(device)
+def _stream(stream, owner) -> ctypes.c_void_p:
+    """The stream a call enqueues on (the current one if None). The owner's device
+    tables are marked as in use on it: the library's kernels read them after the
+    call returns, so the caching allocator must not hand their memory to another
+    tensor before the work enqueued there has finished, whichever stream they were
+    allocated on."""
+    s = stream if stream is not None else torch.cuda.current_stream(owner.device)
+    for t in owner.device_tables:
+        t.record_stream(s)
     return ctypes.c_void_p(s.cuda_stream)
 
 
@@ -63,6 +70,7 @@ class FragmentBatch:
         self.caches = list(caches)
         self.table_host = np.ascontiguousarray(np.array(rows, dtype=np.int64))
         self.table_dev = torch.from_numpy(self.table_host).to(self.device)
+        self.device_tables = (self.table_dev,)
         self.lengths = [int(r[0]) for r in rows]
         self.struct = C.CmFragset(
             n=len(caches), L=self.L, H=self.H, d=self.d, dtype=_DTYPES[self.torch_dtype],
@@ -91,7 +99,7 @@ def fragment_hash(batch: FragmentBatch, digests: torch.Tensor, workspace: torch.
                   stream=None) -> None:
     C.check(C.lib().cm_fragment_hash(ctypes.byref(batch.struct), _ptr(digests), _ptr(workspace),
                                      workspace.numel() * workspace.element_size(),
-                                     _stream(stream, batch.device)), "cm_fragment_hash")
+                                     _stream(stream, batch)), "cm_fragment_hash")
 
 
 def fragment_hash_select(batch: FragmentBatch, select: torch.Tensor, value: int,
@@ -99,12 +107,12 @@ def fragment_hash_select(batch: FragmentBatch, select: torch.Tensor, value: int,
     C.check(C.lib().cm_fragment_hash_select(ctypes.byref(batch.struct), _ptr(select), int(value),
                                             _ptr(digests), _ptr(workspace),
                                             workspace.numel() * workspace.element_size(),
-                                            _stream(stream, batch.device)), "cm_fragment_hash_select")
+                                            _stream(stream, batch)), "cm_fragment_hash_select")
 
 
 def equal_key_mask(batch: FragmentBatch, keys: torch.Tensor, mask: torch.Tensor, stream=None) -> None:
     C.check(C.lib().cm_equal_key_mask(ctypes.byref(batch.struct), _ptr(keys), _ptr(mask),
-                                      _stream(stream, batch.device)), "cm_equal_key_mask")
+                                      _stream(stream, batch)), "cm_equal_key_mask")
 
 
 def fragment_knorm(batch: FragmentBatch, routing_layer: int, tail_len: int, keys: torch.Tensor,
@@ -112,20 +120,20 @@ def fragment_knorm(batch: FragmentBatch, routing_layer: int, tail_len: int, keys
     C.check(C.lib().cm_fragment_knorm(ctypes.byref(batch.struct), routing_layer, tail_len,
                                       _ptr(keys), _ptr(workspace),
                                       workspace.numel() * workspace.element_size(),
-                                      _stream(stream, batch.device)), "cm_fragment_knorm")
+                                      _stream(stream, batch)), "cm_fragment_knorm")
 
 
 def canonical_order(batch: FragmentBatch, keys: torch.Tensor, digests: torch.Tensor,
                     plan: torch.Tensor, stream=None) -> None:
     C.check(C.lib().cm_canonical_order(ctypes.byref(batch.struct), _ptr(keys), _ptr(digests),
-                                       _ptr(plan), _stream(stream, batch.device)),
+                                       _ptr(plan), _stream(stream, batch)),
             "cm_canonical_order")
 
 
 def multiset_order(batch: FragmentBatch, keys: torch.Tensor, digests: torch.Tensor,
                    plan: torch.Tensor, stream=None) -> None:
     C.check(C.lib().cm_multiset_order(ctypes.byref(batch.struct), _ptr(keys), _ptr(digests),
-                                      _ptr(plan), _stream(stream, batch.device)),
+                                      _ptr(plan), _stream(stream, batch)),
             "cm_multiset_order")
 
 
@@ -148,7 +156,7 @@ def render_merge(batch: FragmentBatch, plan_dev: torch.Tensor, plan_host: np.nda
                                     plan_host.ctypes.data_as(ctypes.c_void_p), ctypes.byref(rope),
                                     _ptr(out), T_out, _ptr(workspace),
                                     workspace.numel() * workspace.element_size(),
-                                    _stream(stream, batch.device)), "cm_render_merge")
+                                    _stream(stream, batch)), "cm_render_merge")
 
 
 def render_merge_range(batch: FragmentBatch, plan_dev: torch.Tensor, plan_host: np.ndarray,
@@ -161,7 +169,7 @@ def render_merge_range(batch: FragmentBatch, plan_dev: torch.Tensor, plan_host: 
                                           ctypes.byref(rope), int(first_slot), _ptr(out), T_cap,
                                           _ptr(workspace),
                                           workspace.numel() * workspace.element_size(),
-                                          _stream(stream, batch.device)), "cm_render_merge_range")
+                                          _stream(stream, batch)), "cm_render_merge_range")
 
 
 def render_merge_devplan(batch: FragmentBatch, plan_dev: torch.Tensor, rope_base: float,
@@ -171,7 +179,7 @@ def render_merge_devplan(batch: FragmentBatch, plan_dev: torch.Tensor, rope_base
     C.check(C.lib().cm_render_merge_devplan(ctypes.byref(batch.struct), _ptr(plan_dev),
                                             ctypes.byref(rope), _ptr(out), T_out, _ptr(workspace),
                                             workspace.numel() * workspace.element_size(),
-                                            _stream(stream, batch.device)),
+                                            _stream(stream, batch)),
             "cm_render_merge_devplan")
 
 
@@ -185,7 +193,7 @@ def render_merge_hash(batch: FragmentBatch, plan_dev: torch.Tensor, plan_host: n
                                          ctypes.byref(rope), _ptr(select), _ptr(digests),
                                          _ptr(out), T_out, _ptr(workspace),
                                          workspace.numel() * workspace.element_size(),
-                                         _stream(stream, batch.device)), "cm_render_merge_hash")
+                                         _stream(stream, batch)), "cm_render_merge_hash")
 
 
 def render_deliveries_async(batch: FragmentBatch, routing_layer: int, tail_len: int,
@@ -201,7 +209,7 @@ def render_deliveries_async(batch: FragmentBatch, routing_layer: int, tail_len: 
                                          _ptr(digests), _ptr(plan_dev), _ptr(out), T_cap,
                                          _ptr(workspace),
                                          workspace.numel() * workspace.element_size(),
-                                         _stream(stream, batch.device)), "cm_render_deliveries")
+                                         _stream(stream, batch)), "cm_render_deliveries")
 
 
 def plan_elems(n: int) -> int:
@@ -250,6 +258,7 @@ class PagedSet:
         self.blocks_host = np.ascontiguousarray(np.array(blocks, dtype=np.int32))
         self.table_dev = torch.from_numpy(self.table_host).to(self.device)
         self.blocks_dev = torch.from_numpy(self.blocks_host).to(self.device)
+        self.device_tables = (self.table_dev, self.blocks_dev)
         self.struct = C.CmPagedset(
             n=len(self.lengths), L=self.L, H=self.H, d=self.d, dtype=_DTYPES[self.torch_dtype],
             block=self.B, pages=self.P, pool_dev=pool.data_ptr(),
@@ -297,4 +306,4 @@ def paged_render(pset: PagedSet, plan_dev: torch.Tensor, plan_host: np.ndarray, 
                                     plan_host.ctypes.data_as(ctypes.c_void_p), ctypes.byref(rope),
                                     _ptr(k_table), _ptr(v_table), _ptr(fresh), int(fresh.numel()),
                                     _ptr(workspace), workspace.numel() * workspace.element_size(),
-                                    _stream(stream, pset.device)), "cm_paged_render")
+                                    _stream(stream, pset)), "cm_paged_render")

@@ -3,14 +3,19 @@
 render_deliveries runs the whole path over a list of deliveries: scores
 (cm_fragment_knorm), the Id of every delivery whose score collides
 with another's (cm_equal_key_mask + cm_fragment_hash_select: only those decide
-dedupe and ties), dedupe + canonical order + offsets (cm_canonical_order), one
-device-to-host copy of the small plan so the caller can size the output, then
-the rotate-and-concatenate render. By default the render also computes the Id
-of every other delivery from the same loads (cm_render_merge_hash), so each
-byte is read once; pipeline="overlap" instead hashes them on a second stream
-next to cm_render_merge, and pipeline="serial" runs every step in order.
-LatentFragmentSet keeps the state of Alg. 2 (a set keyed by Id) and renders it
-with the ids computed at Ingest."""
+dedupe and ties), dedupe + canonical order + offsets (cm_canonical_order), then
+the rotate-and-concatenate render fused with the Ids of every other delivery
+(cm_render_merge_hash), so each byte is read once. By default one library call
+(cm_render_deliveries) enqueues all of it with the plan kept on the device and
+the output sized for the sum of the delivery lengths; pipeline="overlap" and
+pipeline="serial" bring the plan to the host before the render, which runs
+beside (overlap: cm_render_merge next to the remaining Ids on a second stream)
+or after (serial) the remaining Ids. LatentFragmentSet keeps the state of
+Alg. 2 (a set keyed by Id) and renders it with the ids computed at Ingest.
+
+Every call enqueues its work on one stream (the `stream` argument, else the
+current stream) and allocates its buffers there. Scratch memory is cached per
+(device, stream), so calls on different streams never share it."""
 
 from __future__ import annotations
 
@@ -32,15 +37,23 @@ _WS: Dict[tuple, torch.Tensor] = {}
 _SIDE: Dict[torch.device, torch.cuda.Stream] = {}
 
 
-def _workspace(batch: FragmentBatch, slot: int = 0) -> torch.Tensor:
-    """Cached workspace per (device, slot); slot 1 belongs to the side stream."""
+def _workspace(batch: FragmentBatch, stream: torch.cuda.Stream) -> torch.Tensor:
+    """Scratch for the calls enqueued on `stream`, cached per (device, stream) and
+    allocated on that stream, so that work on one stream never races with work on
+    another over it, and a buffer replaced by a larger one is only reused by
+    work ordered after what was enqueued with it."""
     need = max(workspace_size(batch), 256)
-    key = (batch.device, slot)
+    key = (batch.device, stream.cuda_stream)
     ws = _WS.get(key)
     if ws is None or ws.numel() < need:
-        ws = torch.empty(need, dtype=torch.uint8, device=batch.device)
+        with torch.cuda.stream(stream):
+            ws = torch.empty(need, dtype=torch.uint8, device=batch.device)
         _WS[key] = ws
     return ws
+
+
+def _main_stream(device: torch.device, stream) -> torch.cuda.Stream:
+    return stream if stream is not None else torch.cuda.current_stream(device)
 
 
 def _side_stream(device: torch.device) -> torch.cuda.Stream:
@@ -161,12 +174,20 @@ class RenderResult:
         b = C.PLAN_HEADER + 3 * n
         return [int(x) for x in self.plan[b:b + n]]
 
+    def _wait(self) -> None:
+        """Host wait for the work of a fused result (the copies below run on the
+        current stream, which need not be the one the result was computed on)."""
+        if self._pending is not None:
+            self._pending[0].synchronize()
+
     @property
     def digests(self) -> List[bytes]:
+        self._wait()
         return [bytes(r) for r in self.digests_dev.cpu().numpy()]
 
     @property
     def keys(self) -> np.ndarray:
+        self._wait()
         return self.keys_dev.cpu().numpy()
 
 
@@ -212,9 +233,9 @@ def render_deliveries(deliveries: Union[FragmentBatch, Sequence], routing_layer:
         raise ValueError(f"pipeline must be one of {PIPELINES}")
     batch = deliveries if isinstance(deliveries, FragmentBatch) else FragmentBatch(deliveries)
     dev = batch.device
-    main = stream if stream is not None else torch.cuda.current_stream(dev)
+    main = _main_stream(dev, stream)
     with torch.cuda.stream(main):
-        ws = _workspace(batch, 0)
+        ws = _workspace(batch, main)
         digests = torch.empty((batch.n, 32), dtype=torch.uint8, device=dev)
         keys = torch.empty(batch.n, dtype=torch.float64, device=dev)
         mask = torch.empty(batch.n, dtype=torch.uint8, device=dev)
@@ -244,7 +265,7 @@ def render_deliveries(deliveries: Union[FragmentBatch, Sequence], routing_layer:
             ready.record(main)
             side = _side_stream(dev)
             side.wait_event(ready)
-            fragment_hash_select(batch, mask, 0, digests, _workspace(batch, 1), side)
+            fragment_hash_select(batch, mask, 0, digests, _workspace(batch, side), side)
             side_done = torch.cuda.Event()
             side_done.record(side)
         else:
@@ -268,9 +289,9 @@ def render_multiset(deliveries: Union[FragmentBatch, Sequence], routing_layer: i
     foil). Digests as in render_deliveries (fused into the render)."""
     batch = deliveries if isinstance(deliveries, FragmentBatch) else FragmentBatch(deliveries)
     dev = batch.device
-    main = stream if stream is not None else torch.cuda.current_stream(dev)
+    main = _main_stream(dev, stream)
     with torch.cuda.stream(main):
-        ws = _workspace(batch, 0)
+        ws = _workspace(batch, main)
         digests = torch.empty((batch.n, 32), dtype=torch.uint8, device=dev)
         keys = torch.empty(batch.n, dtype=torch.float64, device=dev)
         mask = torch.empty(batch.n, dtype=torch.uint8, device=dev)
@@ -294,10 +315,10 @@ def bag_merge(deliveries: Union[FragmentBatch, Sequence], order: Sequence[int],
     order[k]; no scores, no Ids, no dedupe (digests and keys stay empty)."""
     batch = deliveries if isinstance(deliveries, FragmentBatch) else FragmentBatch(deliveries)
     dev = batch.device
-    main = stream if stream is not None else torch.cuda.current_stream(dev)
+    main = _main_stream(dev, stream)
     plan_host = bag_plan(batch, order)
     with torch.cuda.stream(main):
-        ws = _workspace(batch, 0)
+        ws = _workspace(batch, main)
         plan_dev = torch.from_numpy(plan_host).to(dev, non_blocking=False)
         merged, cache = _render_plan(batch, plan_dev, plan_host, rope_base, style, ws, main)
     empty = torch.empty(0, dtype=torch.uint8, device=dev)
@@ -309,10 +330,13 @@ def bag_merge(deliveries: Union[FragmentBatch, Sequence], order: Sequence[int],
 def fragment_ids(caches: Sequence, stream=None) -> List[bytes]:
     """Id of Alg. 2 for each cache (one batched launch)."""
     batch = FragmentBatch(caches)
-    ws = _workspace(batch)
-    digests = torch.empty((batch.n, 32), dtype=torch.uint8, device=batch.device)
-    fragment_hash(batch, digests, ws, stream)
-    return [bytes(r) for r in digests.cpu().numpy()]
+    main = _main_stream(batch.device, stream)
+    with torch.cuda.stream(main):
+        ws = _workspace(batch, main)
+        digests = torch.empty((batch.n, 32), dtype=torch.uint8, device=batch.device)
+        fragment_hash(batch, digests, ws, main)
+        host = digests.cpu().numpy()       # a copy on `main`, ordered after the hash
+    return [bytes(r) for r in host]
 
 
 class LatentFragmentSet:
@@ -364,18 +388,21 @@ class LatentFragmentSet:
             raise ValueError("cannot render an empty set")
         batch, digests = self._description()
         dev = batch.device
-        ws = _workspace(batch)
-        keys = torch.empty(batch.n, dtype=torch.float64, device=dev)
-        plan_dev = torch.empty(plan_elems(batch.n), dtype=torch.int64, device=dev)
-        tail = min(batch.lengths)
-        fragment_knorm(batch, routing_layer, tail, keys, ws, stream)
-        canonical_order(batch, keys, digests, plan_dev, stream)
-        # the members are distinct, so T_out is the sum of their lengths and the
-        # plan can stay on the device (checked there before the render)
-        T_out = int(sum(batch.lengths))
-        merged = torch.empty((batch.L, 2, 1, batch.H, T_out, batch.d), dtype=batch.torch_dtype,
-                             device=dev)
-        render_merge_devplan(batch, plan_dev, rope_base, style, merged, T_out, ws, stream)
+        main = _main_stream(dev, stream)
+        with torch.cuda.stream(main):
+            ws = _workspace(batch, main)
+            digests.record_stream(main)      # the set may drop this array while main still reads it
+            keys = torch.empty(batch.n, dtype=torch.float64, device=dev)
+            plan_dev = torch.empty(plan_elems(batch.n), dtype=torch.int64, device=dev)
+            tail = min(batch.lengths)
+            fragment_knorm(batch, routing_layer, tail, keys, ws, main)
+            canonical_order(batch, keys, digests, plan_dev, main)
+            # the members are distinct, so T_out is the sum of their lengths and the
+            # plan can stay on the device (checked there before the render)
+            T_out = int(sum(batch.lengths))
+            merged = torch.empty((batch.L, 2, 1, batch.H, T_out, batch.d),
+                                 dtype=batch.torch_dtype, device=dev)
+            render_merge_devplan(batch, plan_dev, rope_base, style, merged, T_out, ws, main)
         cache = tuple((merged[l, 0], merged[l, 1]) for l in range(batch.L))
         plan_host = None
         return RenderResult(cache=cache, merged=merged, digests_dev=digests, keys_dev=keys,
@@ -419,26 +446,31 @@ class MergedCache:
         batch, digests = self.fset._description()
         ids = list(self.fset._items.keys())
         dev = batch.device
-        ws = _workspace(batch)
-        keys = torch.empty(batch.n, dtype=torch.float64, device=dev)
-        plan_dev = torch.empty(plan_elems(batch.n), dtype=torch.int64, device=dev)
-        fragment_knorm(batch, self.routing_layer, min(batch.lengths), keys, ws, stream)
-        canonical_order(batch, keys, digests, plan_dev, stream)
-        plan = _plan_to_host(plan_dev, stream)
+        main = _main_stream(dev, stream)
+        with torch.cuda.stream(main):
+            ws = _workspace(batch, main)
+            digests.record_stream(main)
+            keys = torch.empty(batch.n, dtype=torch.float64, device=dev)
+            plan_dev = torch.empty(plan_elems(batch.n), dtype=torch.int64, device=dev)
+            fragment_knorm(batch, self.routing_layer, min(batch.lengths), keys, ws, main)
+            canonical_order(batch, keys, digests, plan_dev, main)
+            plan = _plan_to_host(plan_dev, main)
         n, n_u, T_out = int(plan[C.PLAN_N]), int(plan[C.PLAN_NUNIQUE]), int(plan[C.PLAN_TOUT])
         slot_ids = [ids[int(plan[C.PLAN_HEADER + s])] for s in range(n_u)]
         if self.buffer is None or T_out > self.T_cap:
             T_cap = max(T_out, self.capacity, int(self.T_cap * self.growth))
-            self.buffer = torch.empty((batch.L, 2, 1, batch.H, T_cap, batch.d),
-                                      dtype=batch.torch_dtype, device=dev)
+            with torch.cuda.stream(main):
+                self.buffer = torch.empty((batch.L, 2, 1, batch.H, T_cap, batch.d),
+                                          dtype=batch.torch_dtype, device=dev)
             first = 0
         else:
             first = 0
             while first < min(n_u, len(self.slot_ids)) and slot_ids[first] == self.slot_ids[first]:
                 first += 1
         if first < n_u:
+            self.buffer.record_stream(main)
             render_merge_range(batch, plan_dev, plan, self.rope_base, self.style, first,
-                               self.buffer, self.T_cap, ws, stream)
+                               self.buffer, self.T_cap, ws, main)
         self.last_first_slot = first
         self.last_rows = T_out - (int(plan[C.PLAN_HEADER + n + first]) if first < n_u else T_out)
         self.slot_ids, self.T_out = slot_ids, T_out

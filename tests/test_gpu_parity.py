@@ -384,3 +384,31 @@ def test_devplan_render_equals_host_checked_render_and_rejects_bad_plans():
     cm.render_merge_devplan(batch, plan, w.rope_base, "half", out, ref.T_out - 1, ws)
     torch.cuda.synchronize()
     assert int(plan[0]) == -2 and bool((out == 3).all())
+
+
+def test_results_on_two_streams_and_read_late():
+    """Fused calls on two caller streams, each result read only after later calls
+    were enqueued: every call keeps its own scratch and buffers, so each result
+    equals the same render made alone (and the oracle's plan)."""
+    w1 = synth.custom("streams-a", dtype="bfloat16", d=128, H=2, L=2, lengths=(300, 517, 128),
+                      deliveries=(0, 1, 2, 1), routing_layer=1)
+    w2 = synth.custom("streams-b", dtype="bfloat16", d=128, H=2, L=3, lengths=(200, 90),
+                      seed=11, routing_layer=2)
+    f1, dl1 = gpu_deliveries(w1)
+    f2, dl2 = gpu_deliveries(w2)
+    ref1 = _run(w1, dl1)
+    ref2 = _run(w2, dl2)
+    check_render(ref1, dl1, w1.dtype, w1.routing_layer, w1.rope_base)
+    check_render(ref2, dl2, w2.dtype, w2.routing_layer, w2.rope_base)
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    torch.cuda.synchronize()
+    pending = []
+    for rep in range(3):
+        log(f"[streams] round {rep}")
+        pending.append((ref1, cm.render_deliveries(dl1, w1.routing_layer, w1.rope_base, stream=sa)))
+        pending.append((ref2, cm.render_deliveries(dl2, w2.routing_layer, w2.rope_base, stream=sb)))
+    for ref, res in reversed(pending):
+        assert res.T_out == ref.T_out
+        assert np.array_equal(res.plan, ref.plan)
+        assert res.digests == ref.digests
+        assert torch.equal(res.merged, ref.merged)
