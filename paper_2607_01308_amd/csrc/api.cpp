@@ -531,9 +531,11 @@ int32_t cm_render_deliveries(const cm_fragset* set, int32_t routing_layer, int64
   const cm::HashLayout hlay = cm::hash_layout(s);
   if (e == hipSuccess) e = cm::launch_hash(s, hlay, mask_dev, 1, digests_dev, ws, sm);
   if (e == hipSuccess) e = cm::launch_order(s, keys_dev, digests_dev, true, plan_dev, sm);
+  // the node-base tables written for the first Ids are still in the workspace
+  // (the order and render tables live elsewhere in it), so the fused pass reuses them
   if (e == hipSuccess)
     e = cm::launch_render_hash(s, hlay, cm::render_layout(s), plan_dev, rope->base, rope->style,
-                               mask_dev, digests_dev, out_dev, ws, sm);
+                               mask_dev, digests_dev, out_dev, ws, sm, true);
   return e == hipSuccess ? CM_OK : fail_hip(e, "cm_render_deliveries");
 }
 

@@ -13,7 +13,8 @@
 // wave), and the fused render finds both halves of each RoPE pair in one lane. The
 // work is VALU-bound (12 VALU ops per G step, 672 per block); the tree above the
 // chunks takes one launch per three levels over all tensors at full lane
-// occupancy (the parents add 1/16 of the chunk work).
+// occupancy (the parents add 1/16 of the chunk work) until at most nine levels
+// remain, then one launch folds the top of every tensor's tree.
 #include "chunk_ops.h"
 
 namespace cm {
@@ -133,42 +134,18 @@ __global__ __launch_bounds__(kBlock) void hash_chunk_kernel(const int64_t* __res
   }
 }
 
-// Tree levels v0+1 .. v0+K (K <= kSubLevels) of every tensor in one launch:
-// lane g computes node g of level v0+K (numbered over all tensors) from its up to
-// 2^K children at level v0, level by level in the lane's own LDS slots. Node j
-// of a level is the BLAKE3 parent of children 2j and 2j+1 of the level below (ROOT
-// on the compression that leaves the tensor one node); an unpaired last child
-// is carried up unchanged. Pairing level by level this way builds BLAKE3's
-// left-balanced tree: every complete subtree of 2^v chunks starts at a multiple
-// of 2^v and the unpaired tail joins at the level where it has a sibling. A lane
-// does up to 2^K - 1 dependent compressions, so a launch covers K levels at full
-// lane occupancy and the level below is read once.
 constexpr int kSubLevels = 3;
 constexpr int kSubLanes = 64;
 
-__global__ __launch_bounds__(kSubLanes) void hash_subtree_kernel(
-    const int64_t* __restrict__ table, int32_t n, int64_t stride, int64_t token_bytes, int32_t v0,
-    int32_t K, const int64_t* __restrict__ base_lo, const int64_t* __restrict__ base_hi,
-    int64_t total_hi, const uint8_t* __restrict__ select, uint32_t want,
-    const uint8_t* __restrict__ in, uint8_t* __restrict__ out) {
-  // word w of the lane's node p at [p * 8 + w][lane]: consecutive lanes hit
-  // consecutive banks. The first level is folded straight from the children in
-  // memory, so the slots hold at most half of them.
-  __shared__ uint32_t lds[(1 << (kSubLevels - 1)) * 8][kSubLanes];
-  const int lane = threadIdx.x;
-  const int64_t g = (int64_t)blockIdx.x * kSubLanes + lane;
-  if (g >= total_hi) return;
-  const int i = find_fragment(base_hi, n, g);
-  if (select && select[i] != want) return;
-  const int64_t m0 = chunks_of(table[(int64_t)i * stride] * token_bytes);
-  const int64_t m_lo = nodes_at(m0, v0);
-  const int64_t m_hi = nodes_at(m0, v0 + K);
-  const int64_t local = g - base_hi[i];
-  const int64_t t = local / m_hi;
-  const int64_t j = local - t * m_hi;
-  const int64_t first = j << K;
-  int cur = (int)(m_lo - first < ((int64_t)1 << K) ? m_lo - first : ((int64_t)1 << K));
-  const uint8_t* c = in + (base_lo[i] + t * m_lo + first) * 32;
+// Fold one lane's cur (1 .. 2^K) consecutive level-v0 nodes at c (32 bytes each)
+// into their level-(v0 + K) node, level by level in the lane's own LDS slots
+// (word w of the lane's node p at [p * 8 + w][lane]: consecutive lanes hit
+// consecutive banks). The first level is folded straight from the children in
+// memory, so the slots hold at most half of them. m0: the tensor's chunk count,
+// which places ROOT on the compression that leaves the tensor one node.
+__device__ __forceinline__ void fold_children(const uint8_t* c, int cur, int64_t m0, int v0, int K,
+                                              uint32_t (*lds)[kSubLanes], int lane,
+                                              uint32_t (&w)[8]) {
   for (int lev = 1; lev <= K; ++lev) {
     const uint32_t flags = kB3Parent | (nodes_at(m0, v0 + lev) == 1 ? kB3Root : 0u);
     const int nn = (cur + 1) >> 1;
@@ -209,9 +186,41 @@ __global__ __launch_bounds__(kSubLanes) void hash_subtree_kernel(
     }
     cur = nn;
   }
-  uint32_t w[8];
 #pragma unroll
   for (int k = 0; k < 8; ++k) w[k] = lds[k][lane];
+}
+
+// Tree levels v0+1 .. v0+K (K <= kSubLevels) of every tensor in one launch:
+// lane g computes node g of level v0+K (numbered over all tensors) from its up to
+// 2^K children at level v0, level by level in the lane's own LDS slots. Node j
+// of a level is the BLAKE3 parent of children 2j and 2j+1 of the level below (ROOT
+// on the compression that leaves the tensor one node); an unpaired last child
+// is carried up unchanged. Pairing level by level this way builds BLAKE3's
+// left-balanced tree: every complete subtree of 2^v chunks starts at a multiple
+// of 2^v and the unpaired tail joins at the level where it has a sibling. A lane
+// does up to 2^K - 1 dependent compressions, so a launch covers K levels at full
+// lane occupancy and the level below is read once.
+__global__ __launch_bounds__(kSubLanes) void hash_subtree_kernel(
+    const int64_t* __restrict__ table, int32_t n, int64_t stride, int64_t token_bytes, int32_t v0,
+    int32_t K, const int64_t* __restrict__ base_lo, const int64_t* __restrict__ base_hi,
+    int64_t total_hi, const uint8_t* __restrict__ select, uint32_t want,
+    const uint8_t* __restrict__ in, uint8_t* __restrict__ out) {
+  __shared__ uint32_t lds[(1 << (kSubLevels - 1)) * 8][kSubLanes];
+  const int lane = threadIdx.x;
+  const int64_t g = (int64_t)blockIdx.x * kSubLanes + lane;
+  if (g >= total_hi) return;
+  const int i = find_fragment(base_hi, n, g);
+  if (select && select[i] != want) return;
+  const int64_t m0 = chunks_of(table[(int64_t)i * stride] * token_bytes);
+  const int64_t m_lo = nodes_at(m0, v0);
+  const int64_t m_hi = nodes_at(m0, v0 + K);
+  const int64_t local = g - base_hi[i];
+  const int64_t t = local / m_hi;
+  const int64_t j = local - t * m_hi;
+  const int64_t first = j << K;
+  const int cur = (int)(m_lo - first < ((int64_t)1 << K) ? m_lo - first : ((int64_t)1 << K));
+  uint32_t w[8];
+  fold_children(in + (base_lo[i] + t * m_lo + first) * 32, cur, m0, v0, K, lds, lane, w);
   uint4* o = reinterpret_cast<uint4*>(out + g * 32);
   o[0] = make_uint4(w[0], w[1], w[2], w[3]);
   o[1] = make_uint4(w[4], w[5], w[6], w[7]);
@@ -250,6 +259,40 @@ __device__ __forceinline__ void fold_cvs(uint32_t* lds, int cnt, bool root, int 
     __syncthreads();
     cnt = nn;
   }
+}
+
+// The top of every tensor's tree in one launch, one 64-lane workgroup per
+// (tensor t, fragment i): its at most 64 x 8 nodes of level v0 are folded,
+// eight consecutive ones per lane (an aligned complete subtree, or the tail of
+// the level with its carries), then the lane values level by level across the
+// workgroup; the root goes to node base_top[i] + t of the top level.
+constexpr int kTailLevels = kSubLevels + 6;   // 2^3 nodes per lane x 64 lanes
+
+__global__ __launch_bounds__(kSubLanes) void hash_tail_kernel(
+    const int64_t* __restrict__ table, int64_t stride, int64_t token_bytes, int32_t v0,
+    const int64_t* __restrict__ base_lo, const int64_t* __restrict__ base_top,
+    const uint8_t* __restrict__ select, uint32_t want, const uint8_t* __restrict__ in,
+    uint8_t* __restrict__ out) {
+  __shared__ uint32_t lds[(1 << (kSubLevels - 1)) * 8][kSubLanes];
+  __shared__ uint32_t vals[kSubLanes * 8];
+  const int t = blockIdx.x;
+  const int i = blockIdx.y;
+  const int lane = threadIdx.x;
+  if (select && select[i] != want) return;   // uniform over the workgroup
+  const int64_t m0 = chunks_of(table[(int64_t)i * stride] * token_bytes);
+  const int64_t m = nodes_at(m0, v0);                  // <= 2^kTailLevels (checked by the host)
+  const int cnt = (int)nodes_at(m, kSubLevels);        // lane values, <= 64
+  if (lane < cnt) {
+    const int64_t first = (int64_t)lane << kSubLevels;
+    const int cur = (int)(m - first < (1 << kSubLevels) ? m - first : (1 << kSubLevels));
+    uint32_t w[8];
+    fold_children(in + (base_lo[i] + t * m + first) * 32, cur, m0, v0, kSubLevels, lds, lane, w);
+#pragma unroll
+    for (int k = 0; k < 8; ++k) vals[lane * 8 + k] = w[k];
+  }
+  __syncthreads();
+  fold_cvs(vals, cnt, true, lane);
+  if (lane < 8) reinterpret_cast<uint32_t*>(out + (base_top[i] + t) * 32)[lane] = vals[lane];
 }
 
 // Id = BLAKE3-256(header || root(K^0) || root(V^0) || ...), one 64-lane
@@ -355,8 +398,11 @@ hipError_t launch_hash_tree(const SetDesc& s, const HashLayout& lay, const uint8
   const int64_t nb1 = s.n + 1;
   hipError_t e = hipSuccess;
   int launch = 0;
-  for (int v0 = 0; v0 < lay.levels; v0 += kSubLevels, ++launch) {
-    const int K = lay.levels - v0 < kSubLevels ? lay.levels - v0 : kSubLevels;
+  int v0 = 0;
+  // three levels per launch over all tensors while more than kTailLevels remain
+  // (every tensor then has at most 2^kTailLevels nodes), then the rest at once
+  for (; lay.levels - v0 > kTailLevels; v0 += kSubLevels, ++launch) {
+    const int K = kSubLevels;
     int64_t total = 0;
     for (int i = 0; i < s.n; ++i)
       total += 2 * (int64_t)s.L * nodes_at(chunks_of(s.T(i) * token_bytes_of(s)), v0 + K);
@@ -367,6 +413,15 @@ hipError_t launch_hash_tree(const SetDesc& s, const HashLayout& lay, const uint8
                        base + (v0 + K) * nb1, total, select, want, buf[launch & 1],
                        buf[(launch + 1) & 1]);
     if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  if (v0 < lay.levels) {
+    ScopedTiming tm(K_HASH_PARENT, stream);
+    hipLaunchKernelGGL(hash_tail_kernel, dim3((uint32_t)(2 * s.L), (uint32_t)s.n), dim3(kSubLanes),
+                       0, stream, s.table_dev, s.stride, token_bytes_of(s), v0, base + v0 * nb1,
+                       base + lay.levels * nb1, select, want, buf[launch & 1],
+                       buf[(launch + 1) & 1]);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    ++launch;
   }
   {
     ScopedTiming tm(K_HASH_FINAL, stream);

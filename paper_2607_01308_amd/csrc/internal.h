@@ -126,10 +126,12 @@ hipError_t launch_render_prep(const SetDesc& s, const RenderLayout& lay, const i
 // level fused into the render, then the tree). ws = hash workspace, then
 // render's. The slot count, T_out and the task count are read from the plan on
 // the device; out must hold the merged cache of the plan's T_out rows.
+// tables_ready: the hash workspace already holds this set's node-base tables
+// (written by launch_hash_prep earlier on the same stream).
 hipError_t launch_render_hash(const SetDesc& s, const HashLayout& hlay, const RenderLayout& rlay,
                               const int64_t* plan_dev, double base, int32_t style,
                               const uint8_t* select, uint8_t* digests, void* out, uint8_t* ws,
-                              hipStream_t stream);
+                              hipStream_t stream, bool tables_ready = false);
 // Rows [row0, T_out) of every row block are rendered into `out`, whose row
 // blocks are T_cap rows long (row0 = 0, T_cap = T_out: the whole merged cache).
 struct RenderRange {
