@@ -262,10 +262,12 @@ __device__ __forceinline__ void fold_cvs(uint32_t* lds, int cnt, bool root, int 
 }
 
 // The top of every tensor's tree in one launch, one 64-lane workgroup per
-// (tensor t, fragment i): its at most 64 x 8 nodes of level v0 are folded,
-// eight consecutive ones per lane (an aligned complete subtree, or the tail of
-// the level with its carries), then the lane values level by level across the
-// workgroup; the root goes to node base_top[i] + t of the top level.
+// (tensor t, fragment i): its m <= 64 x 8 nodes of level v0 are folded in runs
+// of r consecutive ones per lane (r the smallest power of two with m <= 64 r:
+// an aligned complete subtree, or the tail of the level with its carries), then
+// the lane values level by level across the workgroup, so the chain of
+// dependent compressions is about log2(m) long; the root goes to node
+// base_top[i] + t of the top level.
 constexpr int kTailLevels = kSubLevels + 6;   // 2^3 nodes per lane x 64 lanes
 
 __global__ __launch_bounds__(kSubLanes) void hash_tail_kernel(
@@ -281,12 +283,22 @@ __global__ __launch_bounds__(kSubLanes) void hash_tail_kernel(
   if (select && select[i] != want) return;   // uniform over the workgroup
   const int64_t m0 = chunks_of(table[(int64_t)i * stride] * token_bytes);
   const int64_t m = nodes_at(m0, v0);                  // <= 2^kTailLevels (checked by the host)
-  const int cnt = (int)nodes_at(m, kSubLevels);        // lane values, <= 64
+  int K = 0;                                           // r = 2^K nodes per lane
+  while (K < kSubLevels && m > ((int64_t)kSubLanes << K)) ++K;
+  const int cnt = (int)nodes_at(m, K);                 // lane values, <= 64
   if (lane < cnt) {
-    const int64_t first = (int64_t)lane << kSubLevels;
-    const int cur = (int)(m - first < (1 << kSubLevels) ? m - first : (1 << kSubLevels));
+    const int64_t first = (int64_t)lane << K;
+    const uint8_t* c = in + (base_lo[i] + t * m + first) * 32;
     uint32_t w[8];
-    fold_children(in + (base_lo[i] + t * m + first) * 32, cur, m0, v0, kSubLevels, lds, lane, w);
+    if (K == 0) {
+      const uint4* q = reinterpret_cast<const uint4*>(c);
+      const uint4 a = q[0], b = q[1];
+      w[0] = a.x; w[1] = a.y; w[2] = a.z; w[3] = a.w;
+      w[4] = b.x; w[5] = b.y; w[6] = b.z; w[7] = b.w;
+    } else {
+      const int cur = (int)(m - first < ((int64_t)1 << K) ? m - first : ((int64_t)1 << K));
+      fold_children(c, cur, m0, v0, K, lds, lane, w);
+    }
 #pragma unroll
     for (int k = 0; k < 8; ++k) vals[lane * 8 + k] = w[k];
   }
