@@ -378,7 +378,10 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16" if w.dtype == "bfloat16" else "f32",
+        # the arithmetic of the path: BLAKE3 in 32-bit integers, scores and the
+        # rotation in fp64; the cache elements it moves are element_dtype
+        "dtype": "u32+f64",
+        "element_dtype": "bf16" if w.dtype == "bfloat16" else "f32",
         "data": "synthetic",
         "config": {"workload": w.name, "deliveries": w.n_deliveries, "distinct": w.n_distinct,
                    "merged_tokens": w.merged_tokens, "layers": w.L, "kv_heads": w.H,
