@@ -228,7 +228,9 @@ def render_deliveries(deliveries: Union[FragmentBatch, Sequence], routing_layer:
     for the sum of the delivery lengths and the call returns without waiting (the
     result waits for the plan on first use; a non-finite score raises then).
     overlap / serial: the plan comes to the host before the render, which then
-    runs beside (overlap) or after (serial) the remaining Ids."""
+    runs beside (overlap) or after (serial) the remaining Ids, and the output is
+    exactly the merged cache: the choice when re-deliveries make the sum of the
+    delivery lengths much larger than the merged cache."""
     if pipeline not in PIPELINES:
         raise ValueError(f"pipeline must be one of {PIPELINES}")
     batch = deliveries if isinstance(deliveries, FragmentBatch) else FragmentBatch(deliveries)
