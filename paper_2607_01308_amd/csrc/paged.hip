@@ -91,22 +91,34 @@ __global__ __launch_bounds__(64) void paged_render_kernel(
     const bool rotate = kv == 0 && offs[s0] != 0;
     double cs[NA], sn[NA];
     if (rotate) piece_angles<ESIZE, STYLE>(angles + (int64_t)s0 * d, cp, ppr, cs, sn);
-    for (int k = 0; k < pieces; ++k) {
-      const int64_t b = lane * 16 + 1024 * (int64_t)k;   // byte of the page's [B][row] block
-      const int64_t row_in = b >> rb_shift;
-      const int64_t q = d1.y + row_in;                   // row counted from page A's start
-      const int64_t page = q < B ? d0.w : d1.x;
-      const bool valid = row_in < d1.z;
-      u32x4 x = {0u, 0u, 0u, 0u};
-      if (valid) x = ld16(src_pool + page * page_bytes + ((q & (B - 1)) << rb_shift) + (b & row_mask));
-      u32x4 y = x;
-      if constexpr (STYLE == CM_ROPE_HALF) {
-        const u32x4 p = lane_xor4<HB>(x);            // every lane takes part
-        if (rotate) y = rotate_piece_half<ESIZE>(x, p, cs, sn);
-      } else {
-        if (rotate) y = rotate_piece_il<ESIZE>(x, cs, sn);
+    // kBatch pieces at a time: all their loads are issued before the first store
+    constexpr int kBatch = 4;
+    for (int k0 = 0; k0 < pieces; k0 += kBatch) {
+      u32x4 x[kBatch];
+      bool valid[kBatch];
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {
+        const int64_t b = lane * 16 + 1024 * (int64_t)(k0 + u);   // byte of the page's [B][row] block
+        const int64_t row_in = b >> rb_shift;
+        const int64_t q = d1.y + row_in;                 // row counted from page A's start
+        const int64_t page = q < B ? d0.w : d1.x;
+        valid[u] = k0 + u < pieces && row_in < d1.z;
+        x[u] = u32x4{0u, 0u, 0u, 0u};
+        if (valid[u])
+          x[u] = ld16(src_pool + page * page_bytes + ((q & (B - 1)) << rb_shift) + (b & row_mask));
       }
-      if (valid) st_stream(dst + b, y);
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {
+        if (k0 + u >= pieces) break;                    // uniform over the wave
+        u32x4 y = x[u];
+        if constexpr (STYLE == CM_ROPE_HALF) {
+          const u32x4 p = lane_xor4<HB>(x[u]);           // every lane takes part
+          if (rotate) y = rotate_piece_half<ESIZE>(x[u], p, cs, sn);
+        } else {
+          if (rotate) y = rotate_piece_il<ESIZE>(x[u], cs, sn);
+        }
+        if (valid[u]) st_stream(dst + lane * 16 + 1024 * (int64_t)(k0 + u), y);
+      }
     }
     return;
   }
