@@ -46,7 +46,9 @@ __device__ __forceinline__ double piece_elem(const u32x4 v, int e) {
 
 // fp32 value f of an fp64 result y, nudged one ulp towards y when f sits on a
 // bf16 midpoint and y does not: rounding f to bf16 (ties to even) then gives y
-// rounded to bf16 in one step (see bf16_bits_rne).
+// rounded to bf16 in one step: every bf16 value and midpoint is an fp32
+// value, so otherwise y and its fp32 rounding lie on the same side of every
+// midpoint.
 __device__ __forceinline__ bool on_bf16_midpoint(float f) {
   return (__float_as_uint(f) & 0xFFFFu) == 0x8000u;
 }
