@@ -530,12 +530,17 @@ int32_t cm_render_deliveries(const cm_fragset* set, int32_t routing_layer, int64
   if (e == hipSuccess) e = cm::launch_equal_key_mask(s, keys_dev, mask_dev, sm);
   const cm::HashLayout hlay = cm::hash_layout(s);
   if (e == hipSuccess) e = cm::launch_hash(s, hlay, mask_dev, 1, digests_dev, ws, sm);
-  if (e == hipSuccess) e = cm::launch_order(s, keys_dev, digests_dev, true, plan_dev, sm);
-  // the node-base tables written for the first Ids are still in the workspace
-  // (the order and render tables live elsewhere in it), so the fused pass reuses them
+  // the order kernel also builds the render's per-slot tables; the node-base
+  // tables written for the first Ids are still in the workspace (the render's
+  // tables live after them), so the fused pass reuses both
+  const cm::RenderLayout rlay = cm::render_layout(s);
   if (e == hipSuccess)
-    e = cm::launch_render_hash(s, hlay, cm::render_layout(s), plan_dev, rope->base, rope->style,
-                               mask_dev, digests_dev, out_dev, ws, sm, true);
+    e = cm::launch_order_render_prep(s, keys_dev, digests_dev, plan_dev, rlay, rope->base,
+                                     rope->style, (int32_t)cm::kStripeBlocks, mask_dev,
+                                     ws + cm::align_up(hlay.bytes, cm::kWsAlign), sm);
+  if (e == hipSuccess)
+    e = cm::launch_render_hash(s, hlay, rlay, plan_dev, rope->base, rope->style, mask_dev,
+                               digests_dev, out_dev, ws, sm, true, true);
   return e == hipSuccess ? CM_OK : fail_hip(e, "cm_render_deliveries");
 }
 

@@ -117,6 +117,12 @@ hipError_t launch_knorm(const SetDesc& s, const KnormLayout& lay, int32_t layer,
 // dedupe = false: every delivery gets a slot (naive multiset order).
 hipError_t launch_order(const SetDesc& s, const double* keys, const uint8_t* digests,
                         bool dedupe, int64_t* plan, hipStream_t stream);
+// Order (with dedupe) and, in the same launch, the per-slot render tables of
+// launch_render_prep (rws: the render's part of the workspace).
+hipError_t launch_order_render_prep(const SetDesc& s, const double* keys, const uint8_t* digests,
+                                    int64_t* plan, const RenderLayout& rlay, double base,
+                                    int32_t style, int32_t stripe_blocks, const uint8_t* select,
+                                    uint8_t* rws, hipStream_t stream);
 // Per-slot angle tables; with stripe_blocks > 0 also the per-slot task bases of
 // 2L * stripes of that many 64-byte blocks (and hsel when select is given).
 hipError_t launch_render_prep(const SetDesc& s, const RenderLayout& lay, const int64_t* plan_dev,
@@ -127,11 +133,13 @@ hipError_t launch_render_prep(const SetDesc& s, const RenderLayout& lay, const i
 // render's. The slot count, T_out and the task count are read from the plan on
 // the device; out must hold the merged cache of the plan's T_out rows.
 // tables_ready: the hash workspace already holds this set's node-base tables
-// (written by launch_hash_prep earlier on the same stream).
+// (written by launch_hash_prep earlier on the same stream); prep_ready: the
+// render's per-slot tables too (launch_order_render_prep).
 hipError_t launch_render_hash(const SetDesc& s, const HashLayout& hlay, const RenderLayout& rlay,
                               const int64_t* plan_dev, double base, int32_t style,
                               const uint8_t* select, uint8_t* digests, void* out, uint8_t* ws,
-                              hipStream_t stream, bool tables_ready = false);
+                              hipStream_t stream, bool tables_ready = false,
+                              bool prep_ready = false);
 // Rows [row0, T_out) of every row block are rendered into `out`, whose row
 // blocks are T_cap rows long (row0 = 0, T_cap = T_out: the whole merged cache).
 struct RenderRange {

@@ -18,7 +18,7 @@
 // digest of a delivery is read only when another delivery has the same key.
 // That lets the digests of every other delivery be computed concurrently with
 // the render (equal_key_mask marks the ones needed first).
-#include "internal.h"
+#include "render_tables.h"
 
 namespace cm {
 
@@ -44,11 +44,11 @@ __device__ __forceinline__ int cmp_digest(const uint32_t (&a)[8], const uint32_t
   return 0;
 }
 
-__global__ __launch_bounds__(1024) void order_kernel(const int64_t* __restrict__ table,
-                                                     int64_t stride, int32_t n,
-                                                     const double* __restrict__ keys,
-                                                     const uint8_t* __restrict__ digests,
-                                                     int32_t dedupe, int64_t* __restrict__ plan) {
+// The plan, by one workgroup of at least n threads (see the top of this file).
+__device__ __forceinline__ void order_body(const int64_t* __restrict__ table, int64_t stride,
+                                           int32_t n, const double* __restrict__ keys,
+                                           const uint8_t* __restrict__ digests, int32_t dedupe,
+                                           int64_t* __restrict__ plan) {
   __shared__ double s_key[1024];
   __shared__ int64_t s_len[1024];     // by delivery, then by slot
   __shared__ int32_t s_first[1024];   // first delivery with the same digest
@@ -141,6 +141,29 @@ __global__ __launch_bounds__(1024) void order_kernel(const int64_t* __restrict__
   }
 }
 
+__global__ __launch_bounds__(1024) void order_kernel(const int64_t* __restrict__ table,
+                                                     int64_t stride, int32_t n,
+                                                     const double* __restrict__ keys,
+                                                     const uint8_t* __restrict__ digests,
+                                                     int32_t dedupe, int64_t* __restrict__ plan) {
+  order_body(table, stride, n, keys, digests, dedupe, plan);
+}
+
+// The plan, then (same workgroup, after a barrier that makes the plan visible to
+// every thread) the render's per-slot tables: one launch where the path would
+// otherwise take two.
+__global__ __launch_bounds__(1024) void order_render_prep_kernel(
+    const int64_t* __restrict__ table, int64_t stride, int32_t n, const double* __restrict__ keys,
+    const uint8_t* __restrict__ digests, int64_t* __restrict__ plan, int32_t d, int32_t ep,
+    int32_t style, double base, int32_t stripe_blocks, int64_t tensor_pairs, int64_t token_bytes,
+    const uint8_t* __restrict__ select, uint8_t* __restrict__ hsel,
+    int64_t* __restrict__ unit_base, double* __restrict__ angles) {
+  order_body(table, stride, n, keys, digests, 1, plan);
+  __syncthreads();
+  render_tables(plan, n, d, ep, style, base, stripe_blocks, tensor_pairs, token_bytes, select,
+                hsel, unit_base, angles, table, stride, 0, nullptr, nullptr);
+}
+
 // mask[i] = 1 if another delivery has a bitwise-equal key (only those digests
 // decide dedupe and ties), else 0.
 __global__ __launch_bounds__(1024) void equal_key_mask_kernel(const int64_t* __restrict__ table,
@@ -181,6 +204,22 @@ hipError_t launch_order(const SetDesc& s, const double* keys, const uint8_t* dig
   ScopedTiming tm(K_ORDER, stream);
   hipLaunchKernelGGL(order_kernel, dim3(1), dim3(threads), 0, stream, s.table_dev, s.stride,
                      s.n, keys, digests, dedupe ? 1 : 0, plan);
+  return hipGetLastError();
+}
+
+hipError_t launch_order_render_prep(const SetDesc& s, const double* keys, const uint8_t* digests,
+                                    int64_t* plan, const RenderLayout& rlay, double base,
+                                    int32_t style, int32_t stripe_blocks, const uint8_t* select,
+                                    uint8_t* rws, hipStream_t stream) {
+  ScopedTiming tm(K_ORDER, stream);
+  int threads = 64;
+  while (threads < s.n) threads <<= 1;
+  hipLaunchKernelGGL(order_render_prep_kernel, dim3(1), dim3(threads), 0, stream, s.table_dev,
+                     s.stride, s.n, keys, digests, plan, s.d, 16 / s.esize, style, base,
+                     stripe_blocks, (int64_t)s.L, token_bytes_of(s), select,
+                     select ? rws + rlay.off_hsel : nullptr,
+                     reinterpret_cast<int64_t*>(rws + rlay.off_tiles),
+                     reinterpret_cast<double*>(rws + rlay.off_angles));
   return hipGetLastError();
 }
 

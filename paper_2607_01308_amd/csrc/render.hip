@@ -14,7 +14,7 @@
 // slot in its row block. A unit crossing a slot boundary resolves the slot per
 // lane. K at a non-zero offset is rotated with the partner piece fetched from
 // the lane P pieces away.
-#include "rotate.h"
+#include "render_tables.h"
 
 namespace cm {
 
@@ -134,13 +134,6 @@ __global__ __launch_bounds__(256) void render_unit_prep_kernel(
   }
 }
 
-// One workgroup: per-slot cos/sin(off_s * theta_j), theta_j = base^(-2j/d), in
-// fp64, in the piece-ordered layout of rotate.h. With stripe_blocks > 0 also the
-// per-slot work-unit bases of the fused hash+render (2L * stripes of that many
-// 64-byte blocks per slot, exclusive scan; the total at index n as well, none if
-// the plan's status is an error) and, with a select mask, hsel[i] = 0
-// for the slot deliveries whose Id the fused kernel computes (select[i] == 0),
-// 1 for every other delivery.
 __global__ __launch_bounds__(1024) void render_prep_kernel(
     const int64_t* __restrict__ plan, int32_t n, int32_t d, int32_t ep, int32_t style,
     double base, int32_t stripe_blocks, int64_t tensor_pairs, int64_t token_bytes,
@@ -148,77 +141,8 @@ __global__ __launch_bounds__(1024) void render_prep_kernel(
     int64_t* __restrict__ unit_base, double* __restrict__ angles,
     const int64_t* __restrict__ table, int64_t stride, int64_t T_out, int32_t* plan_ok,
     int64_t* plan_status) {
-  __shared__ int64_t sc[1024];
-  const int tid = threadIdx.x;
-  int n_u = (int)plan[CM_PLAN_NUNIQUE];
-  if (plan_ok) {
-    // A plan the host has not seen: status, n, n_unique, T_out, every slot's
-    // delivery and length, and the offsets as exclusive prefix sums. The block
-    // holds at least n threads, one per slot.
-    const bool head = plan[CM_PLAN_STATUS] == CM_OK && plan[CM_PLAN_N] == n && n_u >= 1 &&
-                      n_u <= n && plan[CM_PLAN_TOUT] == T_out;
-    bool ok = true;
-    int64_t len = 0;
-    if (head && tid < n_u) {
-      const int64_t src = plan[CM_PLAN_HEADER + tid];
-      len = plan[CM_PLAN_HEADER + 2 * (int64_t)n + tid];
-      ok = src >= 0 && src < n && len >= 1 && len == table[src * stride];
-    }
-    sc[tid] = ok ? len : 0;
-    __syncthreads();
-    for (int o = 1; o < (int)blockDim.x; o <<= 1) {
-      const int64_t t = tid >= o ? sc[tid - o] : 0;
-      __syncthreads();
-      sc[tid] += t;
-      __syncthreads();
-    }
-    if (head && tid < n_u) ok = ok && plan[CM_PLAN_HEADER + n + tid] == sc[tid] - len;
-    const bool all = __syncthreads_and(ok) && head && sc[blockDim.x - 1] == T_out;
-    if (tid == 0) {
-      *plan_ok = all ? 1 : 0;
-      if (!all) *plan_status = CM_ESHAPE;
-    }
-    if (!all) return;
-    __syncthreads();
-  }
-  if (stripe_blocks > 0) {
-    // a plan whose status is an error (a non-finite score) gets no tasks
-    if (plan[CM_PLAN_STATUS] != CM_OK || n_u < 0 || n_u > n) n_u = 0;
-    const int64_t len = tid < n_u ? plan[CM_PLAN_HEADER + 2 * (int64_t)n + tid] : 0;
-    int64_t x = 0;
-    if (tid < n_u)
-      x = 2 * tensor_pairs * ((((len * token_bytes) >> 6) + stripe_blocks - 1) / stripe_blocks);
-    sc[tid] = x;
-    if (hsel && tid < n) hsel[tid] = 1;
-    __syncthreads();
-    for (int o = 1; o < (int)blockDim.x; o <<= 1) {
-      const int64_t t = tid >= o ? sc[tid - o] : 0;
-      __syncthreads();
-      sc[tid] += t;
-      __syncthreads();
-    }
-    if (tid < n_u) unit_base[tid] = sc[tid] - x;
-    if (tid == (int)blockDim.x - 1) {
-      unit_base[n_u] = sc[tid];
-      unit_base[n] = sc[tid];          // the task total, where the fused kernel reads it
-    }
-    if (hsel && tid < n_u) {
-      const int64_t i = plan[CM_PLAN_HEADER + tid];
-      if (select[i] == 0) hsel[i] = 0;
-    }
-  }
-  const int halfd = d >> 1;
-  const int ppr = d / ep;                    // pieces per row
-  for (int idx = tid; idx < n_u * halfd; idx += blockDim.x) {
-    const int s = idx / halfd;
-    const int j = idx - s * halfd;
-    const double theta = pow(base, -(double)(2 * j) / (double)d);
-    const double phi = (double)plan[CM_PLAN_HEADER + n + s] * theta;
-    const int k = style == CM_ROPE_HALF ? angle_slot_half(j / ep, j % ep, ppr >> 1)
-                                        : angle_slot_il(j / (ep >> 1), j % (ep >> 1), ppr);
-    angles[2 * ((int64_t)s * halfd + k)] = cos(phi);
-    angles[2 * ((int64_t)s * halfd + k) + 1] = sin(phi);
-  }
+  render_tables(plan, n, d, ep, style, base, stripe_blocks, tensor_pairs, token_bytes, select, hsel,
+                unit_base, angles, table, stride, T_out, plan_ok, plan_status);
 }
 
 }  // namespace

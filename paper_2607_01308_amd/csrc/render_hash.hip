@@ -296,13 +296,14 @@ __global__ __launch_bounds__(kThreads) CM_FUSED_OCCUPANCY void render_hash_kerne
 hipError_t launch_render_hash(const SetDesc& s, const HashLayout& hlay, const RenderLayout& rlay,
                               const int64_t* plan_dev, double base, int32_t style,
                               const uint8_t* select, uint8_t* digests, void* out, uint8_t* ws,
-                              hipStream_t stream, bool tables_ready) {
+                              hipStream_t stream, bool tables_ready, bool prep_ready) {
   uint8_t* hws = ws;
   uint8_t* rws = ws + align_up(hlay.bytes, kWsAlign);
   hipError_t e = hipSuccess;
   if (!tables_ready && (e = launch_hash_prep(s, hlay, hws, stream)) != hipSuccess) return e;
-  if ((e = launch_render_prep(s, rlay, plan_dev, s.n, base, style, (int32_t)kStripeBlocks,
-                              select, rws, stream)) != hipSuccess)
+  if (!prep_ready && (e = launch_render_prep(s, rlay, plan_dev, s.n, base, style,
+                                             (int32_t)kStripeBlocks, select, rws, stream)) !=
+                         hipSuccess)
     return e;
   const uint8_t* hsel = rws + rlay.off_hsel;  // 0: slot delivery whose Id is computed here
   {
