@@ -527,9 +527,11 @@ int32_t cm_render_deliveries(const cm_fragset* set, int32_t routing_layer, int64
   // the workspace is reused by each stage in turn: they run in order on one stream
   hipError_t e = cm::launch_knorm(s, cm::knorm_layout(s, tail_len), routing_layer, tail_len,
                                   keys_dev, ws, sm);
-  if (e == hipSuccess) e = cm::launch_equal_key_mask(s, keys_dev, mask_dev, sm);
   const cm::HashLayout hlay = cm::hash_layout(s);
-  if (e == hipSuccess) e = cm::launch_hash(s, hlay, mask_dev, 1, digests_dev, ws, sm);
+  // the key mask and the hash trees' node tables in one launch (the tables depend
+  // only on the lengths); the knorm scratch they overwrite is no longer needed
+  if (e == hipSuccess) e = cm::launch_mask_hash_prep(s, hlay, keys_dev, mask_dev, ws, sm);
+  if (e == hipSuccess) e = cm::launch_hash(s, hlay, mask_dev, 1, digests_dev, ws, sm, true);
   // the order kernel also builds the render's per-slot tables; the node-base
   // tables written for the first Ids are still in the workspace (the render's
   // tables live after them), so the fused pass reuses both

@@ -16,6 +16,7 @@
 // occupancy (the parents add 1/16 of the chunk work) until at most nine levels
 // remain, then one launch folds the top of every tensor's tree.
 #include "chunk_ops.h"
+#include "key_mask.h"
 
 namespace cm {
 
@@ -62,11 +63,9 @@ __device__ __forceinline__ int find_fragment(const int64_t* __restrict__ base, i
 // base[v][n] = total nodes at level v; row levels+1 holds the same prefix sums
 // of the (tensor, stripe) tasks of the chunk kernel. One workgroup, block-wide
 // inclusive scans.
-__global__ __launch_bounds__(1024) void hash_prep_kernel(const int64_t* __restrict__ table,
-                                                         int32_t n, int64_t stride,
-                                                         int64_t token_bytes, int32_t L,
-                                                         int32_t levels,
-                                                         int64_t* __restrict__ base) {
+__device__ __forceinline__ void hash_tables(const int64_t* __restrict__ table, int32_t n,
+                                            int64_t stride, int64_t token_bytes, int32_t L,
+                                            int32_t levels, int64_t* __restrict__ base) {
   __shared__ int64_t sc[1024];
   const int tid = threadIdx.x;
   const int64_t bytes = tid < n ? table[(int64_t)tid * stride] * token_bytes : 0;
@@ -87,6 +86,24 @@ __global__ __launch_bounds__(1024) void hash_prep_kernel(const int64_t* __restri
     if (tid == (int)blockDim.x - 1) row[n] = sc[tid];
     __syncthreads();
   }
+}
+
+__global__ __launch_bounds__(1024) void hash_prep_kernel(const int64_t* __restrict__ table,
+                                                         int32_t n, int64_t stride,
+                                                         int64_t token_bytes, int32_t L,
+                                                         int32_t levels,
+                                                         int64_t* __restrict__ base) {
+  hash_tables(table, n, stride, token_bytes, L, levels, base);
+}
+
+// The key mask and the node-base tables in one launch (the tables depend only
+// on the lengths; the two parts share nothing but the workgroup).
+__global__ __launch_bounds__(1024) void mask_hash_prep_kernel(
+    const int64_t* __restrict__ table, int32_t n, int64_t stride, int64_t token_bytes, int32_t L,
+    int32_t levels, const double* __restrict__ keys, uint8_t* __restrict__ mask,
+    int64_t* __restrict__ base) {
+  equal_key_mask_body(n, keys, mask);
+  hash_tables(table, n, stride, token_bytes, L, levels, base);
 }
 
 // One wave = one (tensor, stripe) task at a time. A full stripe: lane k hashes
@@ -445,10 +462,22 @@ hipError_t launch_hash_tree(const SetDesc& s, const HashLayout& lay, const uint8
   return hipGetLastError();
 }
 
+hipError_t launch_mask_hash_prep(const SetDesc& s, const HashLayout& lay, const double* keys,
+                                 uint8_t* mask, uint8_t* ws, hipStream_t stream) {
+  ScopedTiming tm(K_KEY_MASK, stream);
+  int threads = 64;
+  while (threads < s.n) threads <<= 1;
+  hipLaunchKernelGGL(mask_hash_prep_kernel, dim3(1), dim3(threads), 0, stream, s.table_dev, s.n,
+                     s.stride, token_bytes_of(s), s.L, lay.levels, keys, mask,
+                     reinterpret_cast<int64_t*>(ws + lay.off_tables));
+  return hipGetLastError();
+}
+
 hipError_t launch_hash(const SetDesc& s, const HashLayout& lay, const uint8_t* select,
-                       uint32_t want, uint8_t* digests, uint8_t* ws, hipStream_t stream) {
-  hipError_t e = launch_hash_prep(s, lay, ws, stream);
-  if (e != hipSuccess) return e;
+                       uint32_t want, uint8_t* digests, uint8_t* ws, hipStream_t stream,
+                       bool tables_ready) {
+  hipError_t e = hipSuccess;
+  if (!tables_ready && (e = launch_hash_prep(s, lay, ws, stream)) != hipSuccess) return e;
   {
     int64_t* base = reinterpret_cast<int64_t*>(ws + lay.off_tables);
     const int64_t nb1 = s.n + 1;

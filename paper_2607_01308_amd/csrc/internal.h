@@ -102,8 +102,13 @@ int64_t render_units(const SetDesc& s, int64_t T_out);
 // Launchers (enqueue on `stream`, return the first HIP error).
 // select == nullptr hashes every fragment; otherwise only fragments i with
 // select[i] == want (the other digests are left untouched).
+// tables_ready: the node-base tables are already in ws (launch_mask_hash_prep).
 hipError_t launch_hash(const SetDesc& s, const HashLayout& lay, const uint8_t* select,
-                       uint32_t want, uint8_t* digests, uint8_t* ws, hipStream_t stream);
+                       uint32_t want, uint8_t* digests, uint8_t* ws, hipStream_t stream,
+                       bool tables_ready = false);
+// launch_equal_key_mask and launch_hash_prep in one launch.
+hipError_t launch_mask_hash_prep(const SetDesc& s, const HashLayout& lay, const double* keys,
+                                 uint8_t* mask, uint8_t* ws, hipStream_t stream);
 // The stages of launch_hash: node-base tables, then (after the leaves) the
 // parent levels and the final Id.
 hipError_t launch_hash_prep(const SetDesc& s, const HashLayout& lay, uint8_t* ws,

@@ -18,6 +18,7 @@
 // digest of a delivery is read only when another delivery has the same key.
 // That lets the digests of every other delivery be computed concurrently with
 // the render (equal_key_mask marks the ones needed first).
+#include "key_mask.h"
 #include "render_tables.h"
 
 namespace cm {
@@ -164,25 +165,11 @@ __global__ __launch_bounds__(1024) void order_render_prep_kernel(
                 hsel, unit_base, angles, table, stride, 0, nullptr, nullptr);
 }
 
-// mask[i] = 1 if another delivery has a bitwise-equal key (only those digests
-// decide dedupe and ties), else 0.
 __global__ __launch_bounds__(1024) void equal_key_mask_kernel(const int64_t* __restrict__ table,
                                                               int64_t stride, int32_t n,
                                                               const double* __restrict__ keys,
                                                               uint8_t* __restrict__ mask) {
-  __shared__ double s_key[1024];
-  const int tid = threadIdx.x;
-  double key = 0.0;
-  if (tid < n) {
-    key = keys[tid];
-    s_key[tid] = key;
-  }
-  __syncthreads();
-  if (tid < n) {
-    bool shared = false;
-    for (int j = 0; j < n; ++j) shared |= (j != tid && s_key[j] == key);
-    mask[tid] = shared ? 1 : 0;
-  }
+  equal_key_mask_body(n, keys, mask);
 }
 
 }  // namespace
