@@ -65,11 +65,9 @@ __device__ __forceinline__ int find_fragment(const int64_t* __restrict__ base, i
 // inclusive scans.
 __device__ __forceinline__ void hash_tables(const int64_t* __restrict__ table, int32_t n,
                                             int64_t stride, int64_t token_bytes, int32_t L,
-                                            int32_t levels, int64_t* __restrict__ base,
-                                            int32_t* __restrict__ count) {
+                                            int32_t levels, int64_t* __restrict__ base) {
   __shared__ int64_t sc[1024];
   const int tid = threadIdx.x;
-  if (tid < n) count[tid] = 0;
   const int64_t bytes = tid < n ? table[(int64_t)tid * stride] * token_bytes : 0;
   const int64_t m0 = tid < n ? chunks_of(bytes) : 0;
   for (int v = 0; v <= levels + 1; ++v) {
@@ -94,9 +92,8 @@ __global__ __launch_bounds__(1024) void hash_prep_kernel(const int64_t* __restri
                                                          int32_t n, int64_t stride,
                                                          int64_t token_bytes, int32_t L,
                                                          int32_t levels,
-                                                         int64_t* __restrict__ base,
-                                                         int32_t* __restrict__ count) {
-  hash_tables(table, n, stride, token_bytes, L, levels, base, count);
+                                                         int64_t* __restrict__ base) {
+  hash_tables(table, n, stride, token_bytes, L, levels, base);
 }
 
 // The key mask and the node-base tables in one launch (the tables depend only
@@ -104,9 +101,9 @@ __global__ __launch_bounds__(1024) void hash_prep_kernel(const int64_t* __restri
 __global__ __launch_bounds__(1024) void mask_hash_prep_kernel(
     const int64_t* __restrict__ table, int32_t n, int64_t stride, int64_t token_bytes, int32_t L,
     int32_t levels, const double* __restrict__ keys, uint8_t* __restrict__ mask,
-    int64_t* __restrict__ base, int32_t* __restrict__ count) {
+    int64_t* __restrict__ base) {
   equal_key_mask_body(n, keys, mask);
-  hash_tables(table, n, stride, token_bytes, L, levels, base, count);
+  hash_tables(table, n, stride, token_bytes, L, levels, base);
 }
 
 // One wave = one (tensor, stripe) task at a time. A full stripe: lane k hashes
@@ -281,24 +278,74 @@ __device__ __forceinline__ void fold_cvs(uint32_t* lds, int cnt, bool root, int 
   }
 }
 
-// Id = BLAKE3-256(header || root(K^0) || root(V^0) || ...) of fragment i, by one
-// 64-lane workgroup. The message is L + 1 blocks (the header, then per layer the
-// pair of roots K, V) in C = ceil((L + 1) / 16) chunks. Lane k hashes chunk
-// 64 g + k of each group g of 64 chunks; a full group is an aligned complete
-// subtree of BLAKE3's left-balanced tree and is folded into one value, the last
-// group into the value of its own subtree (carries included); then the group
-// values are folded. ROOT marks the single chunk (C = 1) or the last
+// The top of every tensor's tree in one launch, one 64-lane workgroup per
+// (tensor t, fragment i): its m <= 64 x 8 nodes of level v0 are folded in runs
+// of r consecutive ones per lane (r the smallest power of two with m <= 64 r:
+// an aligned complete subtree, or the tail of the level with its carries), then
+// the lane values level by level across the workgroup, so the chain of
+// dependent compressions is about log2(m) long; the root goes to node
+// base_top[i] + t of the top level.
+constexpr int kTailLevels = kSubLevels + 6;   // 2^3 nodes per lane x 64 lanes
+
+__global__ __launch_bounds__(kSubLanes) void hash_tail_kernel(
+    const int64_t* __restrict__ table, int64_t stride, int64_t token_bytes, int32_t v0,
+    const int64_t* __restrict__ base_lo, const int64_t* __restrict__ base_top,
+    const uint8_t* __restrict__ select, uint32_t want, const uint8_t* __restrict__ in,
+    uint8_t* __restrict__ out) {
+  __shared__ uint32_t lds[(1 << (kSubLevels - 1)) * 8][kSubLanes];
+  __shared__ uint32_t vals[kSubLanes * 8];
+  const int t = blockIdx.x;
+  const int i = blockIdx.y;
+  const int lane = threadIdx.x;
+  if (select && select[i] != want) return;   // uniform over the workgroup
+  const int64_t m0 = chunks_of(table[(int64_t)i * stride] * token_bytes);
+  const int64_t m = nodes_at(m0, v0);                  // <= 2^kTailLevels (checked by the host)
+  int K = 0;                                           // r = 2^K nodes per lane
+  while (K < kSubLevels && m > ((int64_t)kSubLanes << K)) ++K;
+  const int cnt = (int)nodes_at(m, K);                 // lane values, <= 64
+  if (lane < cnt) {
+    const int64_t first = (int64_t)lane << K;
+    const uint8_t* c = in + (base_lo[i] + t * m + first) * 32;
+    uint32_t w[8];
+    if (K == 0) {
+      const uint4* q = reinterpret_cast<const uint4*>(c);
+      const uint4 a = q[0], b = q[1];
+      w[0] = a.x; w[1] = a.y; w[2] = a.z; w[3] = a.w;
+      w[4] = b.x; w[5] = b.y; w[6] = b.z; w[7] = b.w;
+    } else {
+      const int cur = (int)(m - first < ((int64_t)1 << K) ? m - first : ((int64_t)1 << K));
+      fold_children(c, cur, m0, v0, K, lds, lane, w);
+    }
+#pragma unroll
+    for (int k = 0; k < 8; ++k) vals[lane * 8 + k] = w[k];
+  }
+  __syncthreads();
+  fold_cvs(vals, cnt, true, lane);
+  if (lane < 8) reinterpret_cast<uint32_t*>(out + (base_top[i] + t) * 32)[lane] = vals[lane];
+}
+
+// Id = BLAKE3-256(header || root(K^0) || root(V^0) || ...), one 64-lane
+// workgroup per fragment. The message is L + 1 blocks (the header, then per
+// layer the pair of roots K, V) in C = ceil((L + 1) / 16) chunks. Lane k hashes
+// chunk 64 g + k of each group g of 64 chunks; a full group is an aligned
+// complete subtree of BLAKE3's left-balanced tree and is folded into one value,
+// the last group into the value of its own subtree (carries included); then the
+// group values are folded. ROOT marks the single chunk (C = 1) or the last
 // compression.
 constexpr int kFinalGroups = 32;   // 32 x 64 chunks: L + 1 <= 32768 blocks
 
-__device__ __forceinline__ void fragment_id(int i, const int64_t* __restrict__ table,
-                                            int64_t stride, int32_t L, int32_t H, int32_t d,
-                                            uint32_t dtype_code, uint32_t esize,
-                                            const uint8_t* __restrict__ r,
-                                            uint8_t* __restrict__ digests, int lane) {
+__global__ __launch_bounds__(64) void hash_final_kernel(
+    const int64_t* __restrict__ table, int32_t n, int64_t stride, int32_t L, int32_t H,
+    int32_t d, uint32_t dtype_code, uint32_t esize, const int64_t* __restrict__ base_last,
+    const uint8_t* __restrict__ select, uint32_t want, const uint8_t* __restrict__ roots,
+    uint8_t* __restrict__ digests) {
   __shared__ uint32_t chunk_cv[64 * 8];
   __shared__ uint32_t group_cv[kFinalGroups * 8];
+  const int i = blockIdx.x;
+  const int lane = threadIdx.x;
+  if (select && select[i] != want) return;   // uniform over the workgroup
   const uint64_t T = (uint64_t)table[(int64_t)i * stride];
+  const uint8_t* r = roots + base_last[i] * 32;
   const int64_t blocks = (int64_t)L + 1;
   const int64_t chunks = (blocks + kB3ChunkBlocks - 1) / kB3ChunkBlocks;
   const int groups = (int)((chunks + 63) / 64);
@@ -335,79 +382,6 @@ __device__ __forceinline__ void fragment_id(int i, const int64_t* __restrict__ t
   if (lane < 8) reinterpret_cast<uint32_t*>(digests + (int64_t)i * 32)[lane] = group_cv[lane];
 }
 
-// The top of every tensor's tree in one launch, one 64-lane workgroup per
-// (tensor t, fragment i): its m <= 64 x 8 nodes of level v0 are folded in runs
-// of r consecutive ones per lane (r the smallest power of two with m <= 64 r:
-// an aligned complete subtree, or the tail of the level with its carries), then
-// the lane values level by level across the workgroup, so the chain of
-// dependent compressions is about log2(m) long; the root goes to node
-// base_top[i] + t of the top level. The workgroup that completes a fragment's
-// 2L roots (count[i], published with device-scope fences) then computes its Id
-// and sets the count back to zero for the next tree.
-constexpr int kTailLevels = kSubLevels + 6;   // 2^3 nodes per lane x 64 lanes
-
-__global__ __launch_bounds__(kSubLanes) void hash_tail_kernel(
-    const int64_t* __restrict__ table, int64_t stride, int64_t token_bytes, int32_t v0,
-    const int64_t* __restrict__ base_lo, const int64_t* __restrict__ base_top,
-    const uint8_t* __restrict__ select, uint32_t want, const uint8_t* __restrict__ in,
-    uint8_t* __restrict__ out, int32_t L, int32_t H, int32_t d, uint32_t dtype_code,
-    uint32_t esize, int32_t* __restrict__ count, uint8_t* __restrict__ digests) {
-  __shared__ uint32_t lds[(1 << (kSubLevels - 1)) * 8][kSubLanes];
-  __shared__ uint32_t vals[kSubLanes * 8];
-  __shared__ int last;
-  const int t = blockIdx.x;
-  const int i = blockIdx.y;
-  const int lane = threadIdx.x;
-  if (select && select[i] != want) return;   // uniform over the workgroup
-  const int64_t m0 = chunks_of(table[(int64_t)i * stride] * token_bytes);
-  const int64_t m = nodes_at(m0, v0);                  // <= 2^kTailLevels (checked by the host)
-  int K = 0;                                           // r = 2^K nodes per lane
-  while (K < kSubLevels && m > ((int64_t)kSubLanes << K)) ++K;
-  const int cnt = (int)nodes_at(m, K);                 // lane values, <= 64
-  if (lane < cnt) {
-    const int64_t first = (int64_t)lane << K;
-    const uint8_t* c = in + (base_lo[i] + t * m + first) * 32;
-    uint32_t w[8];
-    if (K == 0) {
-      const uint4* q = reinterpret_cast<const uint4*>(c);
-      const uint4 a = q[0], b = q[1];
-      w[0] = a.x; w[1] = a.y; w[2] = a.z; w[3] = a.w;
-      w[4] = b.x; w[5] = b.y; w[6] = b.z; w[7] = b.w;
-    } else {
-      const int cur = (int)(m - first < ((int64_t)1 << K) ? m - first : ((int64_t)1 << K));
-      fold_children(c, cur, m0, v0, K, lds, lane, w);
-    }
-#pragma unroll
-    for (int k = 0; k < 8; ++k) vals[lane * 8 + k] = w[k];
-  }
-  __syncthreads();
-  fold_cvs(vals, cnt, true, lane);
-  if (lane < 8) reinterpret_cast<uint32_t*>(out + (base_top[i] + t) * 32)[lane] = vals[lane];
-  // publish the root (release), then count it; the last of the fragment's 2L
-  // workgroups sees every root after an acquire fence
-  __threadfence();
-  __syncthreads();
-  if (lane == 0) last = atomicAdd(&count[i], 1) == 2 * L - 1 ? 1 : 0;
-  __syncthreads();
-  if (!last) return;                          // uniform over the workgroup
-  __threadfence();
-  fragment_id(i, table, stride, L, H, d, dtype_code, esize, out + base_top[i] * 32, digests, lane);
-  if (lane == 0) count[i] = 0;
-}
-
-// The Id of every (selected) fragment when the trees need no tail launch (every
-// tensor is a single chunk): one workgroup per fragment.
-__global__ __launch_bounds__(64) void hash_final_kernel(
-    const int64_t* __restrict__ table, int32_t n, int64_t stride, int32_t L, int32_t H,
-    int32_t d, uint32_t dtype_code, uint32_t esize, const int64_t* __restrict__ base_last,
-    const uint8_t* __restrict__ select, uint32_t want, const uint8_t* __restrict__ roots,
-    uint8_t* __restrict__ digests) {
-  const int i = blockIdx.x;
-  if (select && select[i] != want) return;   // uniform over the workgroup
-  fragment_id(i, table, stride, L, H, d, dtype_code, esize, roots + base_last[i] * 32, digests,
-              threadIdx.x);
-}
-
 }  // namespace
 
 HashLayout hash_layout(const SetDesc& s) {
@@ -429,8 +403,6 @@ HashLayout hash_layout(const SetDesc& s) {
   off = align_up(off + 32 * (size_t)lay.total0, kWsAlign);
   lay.off_buf1 = off;
   off = align_up(off + 32 * (size_t)lay.total1, kWsAlign);
-  lay.off_count = off;
-  off = align_up(off + sizeof(int32_t) * (size_t)s.n, kWsAlign);
   lay.bytes = off;
   return lay;
 }
@@ -442,8 +414,7 @@ hipError_t launch_hash_prep(const SetDesc& s, const HashLayout& lay, uint8_t* ws
   while (threads < s.n) threads <<= 1;
   hipLaunchKernelGGL(hash_prep_kernel, dim3(1), dim3(threads), 0, stream, s.table_dev, s.n,
                      s.stride, token_bytes_of(s), s.L, lay.levels,
-                     reinterpret_cast<int64_t*>(ws + lay.off_tables),
-                     reinterpret_cast<int32_t*>(ws + lay.off_count));
+                     reinterpret_cast<int64_t*>(ws + lay.off_tables));
   return hipGetLastError();
 }
 
@@ -472,22 +443,22 @@ hipError_t launch_hash_tree(const SetDesc& s, const HashLayout& lay, const uint8
                        buf[(launch + 1) & 1]);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
-  const uint32_t code = s.dtype;  // cm_dtype value doubles as the header dtype code
   if (v0 < lay.levels) {
-    // the top levels, and each fragment's Id by the workgroup that completes it
     ScopedTiming tm(K_HASH_PARENT, stream);
     hipLaunchKernelGGL(hash_tail_kernel, dim3((uint32_t)(2 * s.L), (uint32_t)s.n), dim3(kSubLanes),
                        0, stream, s.table_dev, s.stride, token_bytes_of(s), v0, base + v0 * nb1,
                        base + lay.levels * nb1, select, want, buf[launch & 1],
-                       buf[(launch + 1) & 1], s.L, s.H, s.d, code, (uint32_t)s.esize,
-                       reinterpret_cast<int32_t*>(ws + lay.off_count), digests);
-    return hipGetLastError();
+                       buf[(launch + 1) & 1]);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    ++launch;
   }
-  // every tensor is one chunk: its chunk value is its root
-  ScopedTiming tm(K_HASH_FINAL, stream);
-  hipLaunchKernelGGL(hash_final_kernel, dim3((uint32_t)s.n), dim3(64), 0, stream, s.table_dev,
-                     s.n, s.stride, s.L, s.H, s.d, code, (uint32_t)s.esize,
-                     base + lay.levels * nb1, select, want, buf[launch & 1], digests);
+  {
+    ScopedTiming tm(K_HASH_FINAL, stream);
+    const uint32_t code = s.dtype;  // cm_dtype value doubles as the header dtype code
+    hipLaunchKernelGGL(hash_final_kernel, dim3((uint32_t)s.n), dim3(64), 0, stream, s.table_dev, s.n, s.stride, s.L, s.H, s.d, code,
+                       (uint32_t)s.esize, base + lay.levels * nb1, select, want,
+                       buf[launch & 1], digests);
+  }
   return hipGetLastError();
 }
 
@@ -498,8 +469,7 @@ hipError_t launch_mask_hash_prep(const SetDesc& s, const HashLayout& lay, const 
   while (threads < s.n) threads <<= 1;
   hipLaunchKernelGGL(mask_hash_prep_kernel, dim3(1), dim3(threads), 0, stream, s.table_dev, s.n,
                      s.stride, token_bytes_of(s), s.L, lay.levels, keys, mask,
-                     reinterpret_cast<int64_t*>(ws + lay.off_tables),
-                     reinterpret_cast<int32_t*>(ws + lay.off_count));
+                     reinterpret_cast<int64_t*>(ws + lay.off_tables));
   return hipGetLastError();
 }
 

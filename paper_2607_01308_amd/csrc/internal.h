@@ -71,8 +71,6 @@ struct HashLayout {
   size_t off_tables;      // int64 [levels+2][n+1]: per-level node bases, then task bases
   size_t off_buf0;        // level-0 (and even levels) node digests
   size_t off_buf1;        // odd levels
-  size_t off_count;       // int32 [n]: tensors of each fragment whose root is done (the
-                          // tree's last launch); zero between launches
   size_t bytes;           // total workspace bytes
 };
 HashLayout hash_layout(const SetDesc& s);

@@ -189,10 +189,8 @@ def test_timing_api_counts_launches():
         cm.render_deliveries(dl, w.routing_layer, w.rope_base, pipeline="fused")
         cm.render_deliveries(dl, w.routing_layer, w.rope_base, pipeline="serial")
         torch.cuda.synchronize()
-        # (hash_final runs only for sets whose tensors are single chunks; otherwise the
-        # Ids are computed inside the tree's last launch, timed as hash_parent)
-        for k in ("hash_leaf", "hash_parent", "knorm_rows", "order", "key_mask", "render_prep",
-                  "render", "render_hash"):
+        for k in ("hash_leaf", "hash_parent", "hash_final", "knorm_rows", "order", "key_mask",
+                  "render_prep", "render", "render_hash"):
             ms, n = cm.timing_query(k)
             assert n >= 1 and ms > 0.0, k
     finally:
@@ -318,10 +316,10 @@ PIPE_SHAPES = [
     dict(dtype="bfloat16", d=256, H=2, L=2, lengths=(520, 61, 3)),       # partner 16 lanes away
     dict(dtype="float32", d=32, H=3, L=2, lengths=(300, 17)),            # partner 4 lanes away
     dict(dtype="float32", d=128, H=2, L=2, lengths=(140, 1025)),         # partner 16 lanes away
-    # every tensor one chunk (no parent levels: the Id kernel runs on its own),
-    # with a re-delivery whose Id is computed before the order
+    # every tensor one chunk (no parent levels), with a re-delivery whose Id is
+    # computed before the order
     dict(dtype="float32", d=16, H=2, L=2, lengths=(5, 3, 8), deliveries=(0, 1, 2, 1)),
-    # a tree of one parent level (the tail launch alone, Ids inside it)
+    # a tree of one parent level (the tail launch alone)
     dict(dtype="bfloat16", d=64, H=1, L=3, lengths=(9, 16, 2), deliveries=(2, 0, 1, 0)),
 ]
 
