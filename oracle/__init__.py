@@ -8,7 +8,6 @@ nothing from it; the product path never calls it.
 
 from .cmerge_oracle import (  # noqa: F401
     CHUNK_BYTES,
-    STRIPE_BYTES,
     Fragment,
     FragmentSet,
     bf16_bits_to_f64,
@@ -28,8 +27,6 @@ from .cmerge_oracle import (  # noqa: F401
     rope_angles,
     rope_inv_freq,
     rotate_pairs,
-    stripe_lane_pieces,
     round_to_dtype,
-    tensor_message,
     tensor_root,
 )

@@ -8,10 +8,9 @@ What each function follows:
   * fragment_id / tensor_root / fragment_header: the content address Id of
     Alg. 2 (§4.5) and the hash tiebreak of §4.3 ("shapes, dtypes and raw bytes
     of every layer's K and V", order K1,V1,...,KL,VL, unshifted). The paper names
-    no hash function; the reading used here is BLAKE3-256 of each tensor's
-    bytes in a fixed interleaved order that depends on the row size (see
-    tensor_message), then BLAKE3-256 of a 64-byte shape/dtype header followed
-    by the tensor roots.
+    no hash function; the reading used here is BLAKE3-256 of each tensor's raw
+    bytes in memory order (its root), then BLAKE3-256 of a 64-byte shape/dtype
+    header followed by the roots of K1, V1, ..., KL, VL.
   * FragmentSet: Ingest and Merge of Alg. 2 — set union keyed by Id, Eq. (5).
   * fragment_key / mean_knorm: Eq. (3) (§4.3) and Alg. 1 — mean L2 norm of the
     routing layer's K rows over the last T* = min_j T_j positions, averaged over
@@ -41,12 +40,6 @@ from typing import Dict, Iterable, List, Sequence, Tuple
 import numpy as np
 
 CHUNK_BYTES = 1024         # BLAKE3 chunk
-BLOCK_BYTES = 64           # BLAKE3 message block
-PIECE_BYTES = 16           # interleave granularity inside a step
-STRIPE_CHUNKS = 64         # chunks interleaved in one stripe
-STEP_BYTES = STRIPE_CHUNKS * BLOCK_BYTES    # 4 KiB: one block of every chunk
-STRIPE_STEPS = CHUNK_BYTES // BLOCK_BYTES   # 16
-STRIPE_BYTES = STRIPE_CHUNKS * CHUNK_BYTES  # 64 KiB
 _DIGEST = 32               # BLAKE3-256
 # dtype -> (header code, element bytes)
 _DTYPE_INFO = {"float32": (0, 4), "bfloat16": (1, 2)}
@@ -118,48 +111,11 @@ def blake3(data) -> bytes:
     return out.raw
 
 
-def stripe_lane_pieces(row_bytes: int) -> np.ndarray:
-    """Pieces of a 4 KiB step (256 pieces of 16 bytes, row-major rows of
-    row_bytes) that lane k of a stripe takes, [64, 4].
-
-    A row holds 2P pieces, P = row_bytes / 32 in each half. Lane k takes
-    piece f = (k // P) * 2P + k % P of the step's first 2 KiB (a piece of a
-    row's first half), then its partner f + P in the same row's second half,
-    then the same two pieces of the second 2 KiB: f + 128, f + 128 + P."""
-    P = row_bytes // 32
-    if row_bytes % 32 or not 1 <= P <= 64 or 4096 % row_bytes:
-        raise ValueError("row bytes must be a power of two in [64, 4096]")
-    k = np.arange(STRIPE_CHUNKS)
-    f = (k // P) * 2 * P + k % P
-    return np.stack([f, f + P, f + 128, f + 128 + P], axis=1)
-
-
-def tensor_message(buf, row_bytes: int) -> np.ndarray:
-    """The byte string whose BLAKE3 is the tensor's root: the tensor's raw bytes
-    (a multiple of 64) in a fixed order.
-
-    Every full stripe of 64 KiB is cut into 16 steps of 4 KiB, each step into
-    256 pieces of 16 bytes; chunk 64 s + k of the message (1 KiB, the BLAKE3
-    chunk) is, for steps 0..15 of stripe s in turn, the four pieces that
-    stripe_lane_pieces(row_bytes) assigns to lane k. The bytes after the last
-    full stripe follow unchanged."""
-    raw = np.frombuffer(memoryview(buf).cast("B"), dtype=np.uint8)
-    n = raw.size
-    if n % BLOCK_BYTES:
-        raise ValueError("tensor bytes must be a multiple of 64")
-    lanes = stripe_lane_pieces(row_bytes)
-    n_full = n // STRIPE_BYTES
-    # [stripe][step][piece][16 bytes] -> [stripe][step][lane][4 pieces][16 bytes]
-    steps = raw[:n_full * STRIPE_BYTES].reshape(n_full, STRIPE_STEPS, STEP_BYTES // PIECE_BYTES,
-                                               PIECE_BYTES)
-    picked = steps[:, :, lanes, :]
-    # chunk k of a stripe: lane k's blocks in step order
-    return np.concatenate([picked.transpose(0, 2, 1, 3, 4).reshape(-1), raw[n_full * STRIPE_BYTES:]])
-
-
-def tensor_root(buf, row_bytes: int) -> bytes:
-    """Root of one tensor with rows of row_bytes: BLAKE3-256 of tensor_message."""
-    return blake3(tensor_message(buf, row_bytes))
+def tensor_root(buf) -> bytes:
+    """Root of one tensor: BLAKE3-256 of its raw bytes in memory order (a
+    [1, H, T, d] row-major tensor: head by head, row by row, element by element,
+    each element's bytes little-endian as stored)."""
+    return blake3(np.ascontiguousarray(np.frombuffer(memoryview(buf).cast("B"), dtype=np.uint8)))
 
 
 def fragment_header(dtype: str, L: int, H: int, T: int, d: int) -> bytes:
@@ -175,12 +131,12 @@ def fragment_id_from_roots(header: bytes, roots: Sequence[bytes]) -> bytes:
 
 
 def fragment_id(frag: Fragment) -> bytes:
-    """Id(C) of Alg. 2: hash of the header and the roots of K1, V1, ..., KL, VL."""
-    row_bytes = frag.d * _DTYPE_INFO[frag.dtype][1]
+    """Id(C) of Alg. 2: BLAKE3-256(header || root(K1) || root(V1) || ... ||
+    root(KL) || root(VL)), each root the BLAKE3-256 of the tensor's bytes."""
     roots = []
     for K, V in frag.layers:
-        roots.append(tensor_root(np.ascontiguousarray(K), row_bytes))
-        roots.append(tensor_root(np.ascontiguousarray(V), row_bytes))
+        roots.append(tensor_root(np.ascontiguousarray(K)))
+        roots.append(tensor_root(np.ascontiguousarray(V)))
     return fragment_id_from_roots(fragment_header(frag.dtype, frag.L, frag.H, frag.T, frag.d), roots)
 
 

@@ -40,11 +40,10 @@ def oracle_ids(deliveries: Sequence, dtype: str) -> List[bytes]:
     for cache in deliveries:
         L = len(cache)
         _, H, T, d = cache[0][0].shape
-        esize = 2 if dtype == "bfloat16" else 4
         roots = []
         for K, V in cache:
             for x in (K, V):
-                roots.append(om.tensor_root(synth.tensor_to_numpy(x), d * esize))
+                roots.append(om.tensor_root(synth.tensor_to_numpy(x)))
         ids.append(om.fragment_id_from_roots(om.fragment_header(dtype, L, H, T, d), roots))
     return ids
 

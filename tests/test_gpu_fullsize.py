@@ -42,8 +42,7 @@ def _oracle_id(cache, dtype):
     """Oracle Id of one delivery, one tensor at a time on the host."""
     L = len(cache)
     _, H, T, d = cache[0][0].shape
-    row_bytes = d * (2 if dtype == "bfloat16" else 4)
-    roots = [om.tensor_root(synth.tensor_to_numpy(x), row_bytes) for K, V in cache for x in (K, V)]
+    roots = [om.tensor_root(synth.tensor_to_numpy(x)) for K, V in cache for x in (K, V)]
     return om.fragment_id_from_roots(om.fragment_header(dtype, L, H, T, d), roots)
 
 
