@@ -133,13 +133,9 @@ int32_t cm_workspace_size(const cm_fragset* set, size_t* bytes_out);
  * Id of Alg. 2 (content address; also the hash tiebreak of §4.3): for every
  * fragment, a 32-byte digest of its shapes, dtype and the raw bytes of
  * K^0, V^0, ..., K^{L-1}, V^{L-1} in that order. Function: BLAKE3-256 (unkeyed
- * hash mode of the BLAKE3 specification). Per tensor, the root is the BLAKE3 of
- * its bytes in a fixed order: every full 64 KiB stripe s is cut into 16 steps of
- * 4 KiB and each step into 256 pieces of 16 bytes; with P = d * element_bytes / 32
- * pieces per half row, chunk 64*s + k of the message (1 KiB, the BLAKE3 chunk)
- * is, for each step of the stripe in turn, its pieces f = (k / P) * 2P + k % P,
- * f + P, f + 128 and f + 128 + P. The bytes after the last full stripe follow
- * in their own order.
+ * hash mode of the BLAKE3 specification). Per tensor, the root is the BLAKE3-256
+ * of its raw bytes in memory order (the [1, H, T, d] row-major bytes: what any
+ * BLAKE3 implementation gives for the buffer).
  * Then the Id is the BLAKE3-256 of a 64-byte header (magic "CMFRAG01", u32 dtype
  * code 0=fp32 1=bf16, u32 element bytes, u32 L, u32 batch=1, u32 H, u64 T, u32 d,
  * zero pad; little-endian) followed by the 2L tensor roots.

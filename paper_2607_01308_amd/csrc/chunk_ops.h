@@ -1,6 +1,5 @@
 // Device helpers of the hash kernels (hash.hip, render_hash.hip): 64-byte block
-// loads, chaining-value stores, and the chunks of a tensor's rest (the bytes
-// after its last full 64 KiB stripe), which are hashed in their own order.
+// loads, chaining-value stores, and the BLAKE3 chunk of one lane of a stripe.
 #pragma once
 
 #include "blake3.h"
@@ -26,17 +25,19 @@ __device__ __forceinline__ void store_cv(uint8_t* out, const B3Cv& s) {
   q[1] = make_uint4(s.h[4], s.h[5], s.h[6], s.h[7]);
 }
 
-// Chunk `lane` of a tensor's rest: `rest` points at the rest's first byte,
-// rest_blocks (< 1024) 64-byte blocks follow; chunk k is blocks [16k, 16k+16)
+// Chunk `lane` of a stripe: `stripe` points at the stripe's first byte,
+// stripe_blocks (<= 1024) 64-byte blocks follow; chunk k is blocks [16k, 16k+16)
 // (the last may be shorter) and has BLAKE3 chunk index chunk0 + k. root: the
 // tensor is this one chunk. Returns false (s untouched) for a lane past the
 // last chunk.
-__device__ __forceinline__ bool hash_rest_chunk(B3Cv& s, const uint8_t* rest, int64_t rest_blocks,
-                                                int lane, uint64_t chunk0, bool root) {
+__device__ __forceinline__ bool hash_lane_chunk(B3Cv& s, const uint8_t* stripe,
+                                                int64_t stripe_blocks, int lane, uint64_t chunk0,
+                                                bool root) {
   const int64_t first = (int64_t)lane * kB3ChunkBlocks;
-  if (first >= rest_blocks) return false;
-  const int64_t nb = rest_blocks - first < kB3ChunkBlocks ? rest_blocks - first : kB3ChunkBlocks;
-  const uint8_t* p = rest + first * 64;
+  if (first >= stripe_blocks) return false;
+  const int64_t nb =
+      stripe_blocks - first < kB3ChunkBlocks ? stripe_blocks - first : kB3ChunkBlocks;
+  const uint8_t* p = stripe + first * 64;
   b3_chunk(s, nb, chunk0 + (uint64_t)lane, root,
            [&](int64_t b, uint32_t (&w)[16]) { load_block64(p + b * 64, w); });
   return true;

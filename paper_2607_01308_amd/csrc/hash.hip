@@ -1,20 +1,16 @@
 // Step 1 — content address Id of Alg. 2 (also the hash tiebreak of §4.3).
 //
-// Per tensor, BLAKE3-256 of its bytes in a fixed interleaved order; per
-// fragment, BLAKE3-256 of a 64-byte shape/dtype header followed by the 2L
-// tensor roots (K^0, V^0, ..., K^{L-1}, V^{L-1}). In every full 64 KiB stripe of
-// a tensor, chunk 64 s + k (1 KiB, the BLAKE3 chunk) takes four 16-byte pieces
-// from each of the stripe's 16 steps of 4 KiB: with P pieces per half row,
-// f = (k / P) 2P + k % P, its second-half partner f + P, and f + 128,
-// f + 128 + P. The bytes after the last full stripe keep their order. That order
-// is chosen for 64-wide wavefronts: one wave takes one stripe, lane k hashes
-// chunk k (16 dependent compressions with the next blocks in flight), each of
-// the four 16-byte loads of a step covers whole half rows (1 KiB across the
-// wave), and the fused render finds both halves of each RoPE pair in one lane. The
-// work is VALU-bound (12 VALU ops per G step, 672 per block); the tree above the
-// chunks takes one launch per three levels over all tensors at full lane
-// occupancy (the parents add 1/16 of the chunk work) until at most nine levels
-// remain, then one launch folds the top of every tensor's tree.
+// Per tensor, BLAKE3-256 of its raw bytes in memory order; per fragment,
+// BLAKE3-256 of a 64-byte shape/dtype header followed by the 2L tensor roots
+// (K^0, V^0, ..., K^{L-1}, V^{L-1}). One wave takes one stripe of 64
+// consecutive BLAKE3 chunks (64 KiB) and lane k hashes chunk k of it: 16
+// dependent compressions, each 64-byte block loaded as four 16-byte pieces (the
+// lanes' loads are 1 KiB apart, so each lane reads whole 64-byte halves of
+// cache lines and the other half one block later), two blocks ahead of the
+// compression. The work is VALU-bound (12 VALU ops per G step, 672 per block);
+// the tree above the chunks takes one launch per three levels over all tensors
+// at full lane occupancy (the parents add 1/16 of the chunk work) until at most
+// nine levels remain, then one launch folds the top of every tensor's tree.
 #include "chunk_ops.h"
 #include "key_mask.h"
 
@@ -30,24 +26,6 @@ constexpr int kBlock = 256;
 #define CM_HASH_BLOCKS_PER_CU 4
 #endif
 constexpr int kLeafBlocksPerCu = CM_HASH_BLOCKS_PER_CU;
-
-// Block j of the lane's chunk of a full stripe: the four pieces of step j that
-// the lane takes, for rows of 2 hp pieces: f = (lane / hp) 2hp + lane % hp, its
-// partner f + hp, and the same two 2 KiB further on. a0, a1: the stripe's first
-// byte plus the offsets of pieces f and f + hp.
-__device__ __forceinline__ void load_stripe_block(const uint8_t* a0, const uint8_t* a1, int64_t j,
-                                                  uint32_t (&m)[16]) {
-  const u32x4 v[4] = {*global_ptr<u32x4>(a0 + (j << 12)), *global_ptr<u32x4>(a1 + (j << 12)),
-                      *global_ptr<u32x4>(a0 + (j << 12) + 2048),
-                      *global_ptr<u32x4>(a1 + (j << 12) + 2048)};
-#pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    m[4 * k + 0] = v[k][0];
-    m[4 * k + 1] = v[k][1];
-    m[4 * k + 2] = v[k][2];
-    m[4 * k + 3] = v[k][3];
-  }
-}
 
 // Largest i in [0, n) with base[i] <= g (bases strictly increase).
 __device__ __forceinline__ int find_fragment(const int64_t* __restrict__ base, int n, int64_t g) {
@@ -106,11 +84,10 @@ __global__ __launch_bounds__(1024) void mask_hash_prep_kernel(
   hash_tables(table, n, stride, token_bytes, L, levels, base);
 }
 
-// One wave = one (tensor, stripe) task at a time. A full stripe: lane k hashes
-// chunk 64 s + k, one block of four pieces from each 4 KiB step (hp: pieces per
-// half row). The rest of a tensor: lane k
-// hashes its chunk k, 1 KiB of consecutive bytes. The grid is bounded (a few
-// workgroups per CU) and strides over all tasks.
+// One wave = one (tensor, stripe) task at a time: lane k hashes chunk k of the
+// stripe, 1 KiB of consecutive bytes (the tensor's last chunk may be shorter,
+// lanes past it idle). The grid is bounded (a few workgroups per CU) and strides
+// over all tasks.
 __global__ __launch_bounds__(kBlock) void hash_chunk_kernel(const int64_t* __restrict__ table,
                                                             int32_t n, int64_t stride,
                                                             int64_t token_bytes,
@@ -118,10 +95,9 @@ __global__ __launch_bounds__(kBlock) void hash_chunk_kernel(const int64_t* __res
                                                             const int64_t* __restrict__ task_base,
                                                             int64_t total_tasks,
                                                             const uint8_t* __restrict__ select,
-                                                            uint32_t want, int32_t hp,
+                                                            uint32_t want,
                                                             uint8_t* __restrict__ nodes) {
   const int lane = threadIdx.x & 63;
-  const uint32_t pf = (uint32_t)((lane / hp) * 2 * hp + lane % hp) * 16;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform per wave
   const int64_t waves = (int64_t)gridDim.x * (kBlock / 64);
   for (int64_t task = (int64_t)blockIdx.x * (kBlock / 64) + wave; task < total_tasks;
@@ -139,14 +115,9 @@ __global__ __launch_bounds__(kBlock) void hash_chunk_kernel(const int64_t* __res
     const uint8_t* p = reinterpret_cast<const uint8_t*>(table[(int64_t)i * stride + 1 + t]) +
                        ((sidx * kStripeBlocks) << 6);
     B3Cv s;
-    if (in_stripe >= kStripeBlocks) {
-      const uint8_t* a0 = p + pf;
-      const uint8_t* a1 = a0 + hp * 16;
-      b3_chunk(s, kB3ChunkBlocks, chunk0 + lane, false,
-               [&](int64_t b, uint32_t (&w)[16]) { load_stripe_block(a0, a1, b, w); });
-    } else if (!hash_rest_chunk(s, p, in_stripe, lane, chunk0, m == 1)) {
+    if (!hash_lane_chunk(s, p, in_stripe < kStripeBlocks ? in_stripe : kStripeBlocks, lane,
+                         chunk0, m == 1))
       continue;
-    }
     store_cv(nodes + (base0[i] + t * m + (int64_t)chunk0 + lane) * 32, s);
   }
 }
@@ -488,7 +459,7 @@ hipError_t launch_hash(const SetDesc& s, const HashLayout& lay, const uint8_t* s
     hipLaunchKernelGGL(hash_chunk_kernel, dim3((uint32_t)grid), dim3(kBlock), 0, stream,
                        s.table_dev, s.n, s.stride, token_bytes_of(s), base,
                        base + (int64_t)(lay.levels + 1) * nb1, lay.tasks, select, want,
-                       (int32_t)(s.row_bytes / 32), ws + lay.off_buf0);
+                       ws + lay.off_buf0);
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   return launch_hash_tree(s, lay, select, want, digests, ws, stream);

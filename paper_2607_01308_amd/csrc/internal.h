@@ -35,8 +35,9 @@ inline int64_t token_bytes_of(const SetDesc& s) { return (int64_t)s.H * s.row_by
 constexpr size_t kWsAlign = 256;
 
 // Hash geometry (see cm_fragment_hash): 64-byte blocks, BLAKE3 chunks of 16
-// blocks, stripes of 1024 blocks (64 KiB) holding 64 interleaved chunks; the
-// blocks after the last full stripe are hashed in their own order.
+// blocks (1 KiB of consecutive tensor bytes), and the work unit of the hash
+// kernels: a stripe of 1024 blocks (64 KiB), i.e. 64 consecutive chunks, one per
+// lane of a wave; a tensor's last stripe may be shorter.
 constexpr int64_t kStripeBlocks = 1024;
 constexpr int kStripeChunks = 64;
 
@@ -88,7 +89,8 @@ size_t knorm_max_bytes(const SetDesc& s);  // over every legal tail_len
 
 struct RenderLayout {
   size_t off_tiles;       // int64 [n+1] work-unit bases per slot (fused hash+render tasks)
-  size_t off_angles;      // double [n][d/2][2] cos, sin per slot (piece-ordered, rotate.h)
+  size_t off_angles;      // double [n][d/2][2] cos, sin per slot (rotate.h: piece-ordered for
+                          // the unit and paged renders, pair order for the fused kernel)
   size_t off_hsel;        // uint8 [n]: 0 = slot delivery hashed by the fused kernel
   size_t off_src_base;    // int64 [n][2LH]: per slot and row block, the source base of row 0
   size_t off_unit_slot;   // int32 [render units]: slot of each unit of a row block

@@ -4,28 +4,28 @@
 //
 // Hashing is VALU-bound (672 VALU ops per 64-byte block) and the render is
 // HBM-bound; done separately they read every byte twice. Here one wave takes
-// one (slot, tensor, stripe) task. A row holds 2P pieces of 16 bytes (P per
-// half). At step j of a full 64 KiB stripe lane k loads four pieces of the 4 KiB
-// step: f = (k / P) 2P + k % P, a first-half piece of a row in the step's first
-// 2 KiB, its second-half partner f + P, and the same two in the second 2 KiB
-// (each load covers whole rows' halves, 1 KiB across the wave). It compresses
-// them as block j of its BLAKE3 chunk (exactly the message order of the hash)
-// and writes each piece to its place in the merged cache: V and offset-0 K
-// unchanged, other K rotated by R(off). Both halves of each of the lane's
-// rotation pairs are in its own registers, all in one column: its cos/sin pairs
-// are fixed for the task and no lane exchange is needed. A step covers whole
-// rows; unless it straddles two heads its rows are consecutive in the merged
-// cache too, so its stores take the same wave-uniform base plus lane offsets as
-// its loads. The rest of a tensor after
-// its last full stripe (under 64 KiB) is rendered by the same steps plus a short
-// final step whose lanes keep whole 64-byte blocks, then its chunks are hashed
-// in their own byte order from a second read (of bytes the render just pulled
-// into the cache). HBM traffic is the algorithmic minimum (each byte read once,
-// written once); the kernel is bound by the VALU work of the hash plus the fp64
-// rotation.
+// one (slot, tensor, stripe) task: a stripe is 64 consecutive BLAKE3 chunks of
+// the tensor (64 KiB) and lane k owns chunk k, 1 KiB of consecutive bytes,
+// i.e. whole rows of the tensor (a row is 64 B .. 1 KiB). Step k loads blocks
+// 2k and 2k + 1 of every lane's chunk (128 bytes per lane, a whole cache line,
+// lanes 1 KiB apart), one step ahead of their use; the lane compresses them
+// into its chunk's chaining value and the pair is written to the lane's rows of
+// the merged cache: V and offset-0 K unchanged, other K rotated by R(off) in
+// fp64. A half-split pair (j, j + d/2) has its halves half a row apart: in a
+// 128-byte row both are in one step, in a 256-byte row the first-half step is
+// kept in registers until its partner arrives, in longer rows it is re-read
+// from the cache one step before it is needed. The angles depend only on the
+// slot and the column, so every lane of a step uses the same (cos, sin) pairs,
+// read from the slot's table as wave-uniform values. The output goes through
+// the LDS so that each store instruction writes whole 128-byte lines of eight
+// chunks; each lane follows its own rows into the merged cache (a chunk may
+// cross the end of a head). HBM traffic is the algorithmic minimum (each byte
+// read once, written once); the kernel is bound by the VALU work of the hash
+// plus the fp64 rotation.
 #include <type_traits>
 
 #include "chunk_ops.h"
+#include "fused_geometry.h"
 #include "rotate.h"
 
 namespace cm {
@@ -34,264 +34,352 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
-// Persistent grid of CUs x CM_FUSED_BLOCKS_PER_CU blocks; the register budget
-// is capped so that CM_FUSED_WAVES_PER_EU waves fit on each SIMD (3 waves:
-// 168 VGPRs, enough for the hash state, two 4 KiB step buffers and the angles),
-// i.e. three blocks per CU at a time. Many more blocks than fit keep the end of
-// the launch short: a block that starts late has few tasks (measured on the
-// 4B-large whole path, blocks per CU -> kernel time: 4 -> 16.3-16.7 ms,
-// 16 -> 15.6-15.7, 32 -> 15.4-15.5, 64 -> 15.5, one task per wave -> 16.3).
+// Persistent grid of up to CUs x CM_FUSED_BLOCKS_PER_CU blocks (fewer when the
+// set has fewer tasks); the register budget is capped so that
+// CM_FUSED_WAVES_PER_EU waves fit on each SIMD (2 waves: 256 VGPRs, enough for
+// three pairs of blocks, the hash state and the fp64 rotation without spills).
+// Many more blocks than fit keep the end of the launch short: a block that
+// starts late has few tasks.
 #ifndef CM_FUSED_BLOCKS_PER_CU
 #define CM_FUSED_BLOCKS_PER_CU 32
 #endif
 #ifndef CM_FUSED_WAVES_PER_EU
-#define CM_FUSED_WAVES_PER_EU 3
+#define CM_FUSED_WAVES_PER_EU 2
 #endif
 #define CM_FUSED_OCCUPANCY __attribute__((amdgpu_waves_per_eu(CM_FUSED_WAVES_PER_EU)))
 
-// Short final step: lane owns block c of its row as 4 pieces with consecutive
-// columns c*4 .. c*4+3 of a row of ppr pieces; ang = the slot's (cos, sin)
-// table. Half-split: a row holds HB / 2 blocks and the partner block sits HB / 4
-// lanes away (HB = 2: the row is this one block, pieces 0-1 pair with 2-3).
-// Reached by every lane of the wave (cross-lane exchange).
-template <int ESIZE, int STYLE, int HB>
-__device__ __forceinline__ void rotate_block_tail(u32x4 (&x)[4], int c, int ppr,
-                                                  const double* __restrict__ ang) {
-  constexpr int EP = 16 / ESIZE;
-  constexpr int NA = STYLE == CM_ROPE_HALF ? EP : EP / 2;
-  u32x4 y[4];
+template <int V>
+using IC = std::integral_constant<int, V>;
+
+// Loads and stores of the fused kernel are ordinary (cached) accesses: a lane
+// reads and writes whole 128-byte lines over two consecutive instructions of
+// the same step, which the caches merge (the nontemporal hints suit only
+// wave-contiguous accesses; here they made every 16-byte piece a transfer of
+// its own).
+__device__ __forceinline__ void load_block(u32x4 (&x)[4], const uint8_t* p) {
 #pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    double cs[NA], sn[NA];
-    piece_angles<ESIZE, STYLE>(ang, c * 4 + k, ppr, cs, sn);
-    if constexpr (STYLE == CM_ROPE_INTERLEAVED) {
-      y[k] = rotate_piece_il<ESIZE>(x[k], cs, sn);
-    } else if constexpr (HB == 2) {
-      y[k] = rotate_piece_half<ESIZE>(x[k], x[k ^ 2], cs, sn);
-    } else {
-      y[k] = rotate_piece_half<ESIZE>(x[k], lane_xor4<HB / 4>(x[k]), cs, sn);
-    }
-  }
-#pragma unroll
-  for (int k = 0; k < 4; ++k) x[k] = y[k];
+  for (int q = 0; q < 4; ++q) x[q] = *global_ptr<u32x4>(p + 16 * q);
 }
 
-__device__ __forceinline__ void compress_pieces(B3Cv& st, const u32x4 (&x)[4], uint64_t chunk,
-                                                uint32_t flags) {
+__device__ __forceinline__ void store16(uint8_t* p, u32x4 v) { *(CM_GLOBAL u32x4*)p = v; }
+
+__device__ __forceinline__ void compress_block(B3Cv& st, const u32x4 (&x)[4], uint64_t chunk,
+                                               uint32_t flags) {
   uint32_t w[16];
 #pragma unroll
-  for (int k = 0; k < 4; ++k)
+  for (int q = 0; q < 4; ++q)
 #pragma unroll
-    for (int q = 0; q < 4; ++q) w[4 * k + q] = x[k][q];
+    for (int k = 0; k < 4; ++k) w[4 * q + k] = x[q][k];
   b3_compress(st, w, chunk, 64, flags);
 }
 
-// Destination of byte `rel` (0 <= rel < 4096) of a step whose first row is row
-// tt of head hh of the fragment: rows past the head's end continue in the next
-// head of the merged cache (only reached when a step straddles heads).
-__device__ __forceinline__ uint8_t* dest_wrapped(uint8_t* out_t, int64_t hh, int64_t tt, int rel,
-                                                 int rb_shift, int64_t T, int64_t T_out,
-                                                 int64_t off) {
-  int64_t rr = tt + (rel >> rb_shift);
-  while (rr >= T) {
-    rr -= T;
-    ++hh;
+// N consecutive (cos, sin) pairs j0 .. j0 + N - 1 of a slot's pair-ordered
+// table (entry j = cos, sin of off * theta_j). j0 is the same on every lane,
+// so the pairs are read by scalar loads (through the constant address space:
+// the table is not written while the kernel runs) into scalar registers, which
+// the fp64 multiply and FMA take as operands. The table address is made opaque
+// first, so that the loads stay where they are used (loop-invariant loads of
+// every angle of the slot hoisted out of the step loop would not fit the
+// scalar registers).
+#define CM_CONST __attribute__((address_space(4)))
+template <int N>
+__device__ __forceinline__ void pair_angles(const double* __restrict__ table, int j0, double* cs,
+                                            double* sn) {
+  const double* a = table;
+  asm volatile("" : "+s"(a));
+  const CM_CONST double* ang = (const CM_CONST double*)a;
+#pragma unroll
+  for (int e = 0; e < N; ++e) {
+    cs[e] = ang[2 * (j0 + e)];
+    sn[e] = ang[2 * (j0 + e) + 1];
   }
-  return out_t + ((hh * T_out + off + rr) << rb_shift) + (rel & ((1 << rb_shift) - 1));
 }
 
-// HB: for half-split pairs, 16-byte pieces per half row (the short final step
-// of a tensor's rest finds partner blocks HB / 4 lanes away); 0 for interleaved
-// pairs.
-template <int ESIZE, int STYLE, int HB>
+// Stage slot of 16-byte piece q (0 .. 7: two blocks of four pieces) of lane l's
+// pair of blocks in a wave's LDS buffer: the xor spreads the writes of any
+// eight consecutive lanes, and the reads of the eight lanes that store one
+// chunk's 128 bytes, over distinct LDS banks.
+__device__ __forceinline__ int stage_slot(int q, int l) { return q * 64 + (l ^ q); }
+
+// ESIZE: element bytes; STYLE: pairing; RB: row bytes (64 .. 1024).
+template <int ESIZE, int STYLE, int RB>
 __global__ __launch_bounds__(kThreads) CM_FUSED_OCCUPANCY void render_hash_kernel(
     const int64_t* __restrict__ table, int64_t stride, int32_t n, const int64_t* __restrict__ plan,
     const int64_t* __restrict__ task_base, const double* __restrict__ angles, int32_t H,
-    int32_t d,
-    const uint8_t* __restrict__ select, const int64_t* __restrict__ base0,
+    int32_t d, const uint8_t* __restrict__ select, const int64_t* __restrict__ base0,
     uint8_t* __restrict__ nodes, uint8_t* __restrict__ out) {
-  constexpr int EP = 16 / ESIZE;                   // elements per 16-byte piece
-  constexpr int NA = STYLE == CM_ROPE_HALF ? EP : EP / 2;  // angle pairs per lane
+  constexpr int EP = 16 / ESIZE;              // elements per 16-byte piece
+  constexpr int BPR = RB / 64;                // blocks per row: 1 .. 16
+  constexpr int HBK = BPR / 2;                // blocks per half row (0: a row is one block)
+  constexpr int PPR = BPR >= 2 ? BPR / 2 : 1; // steps (pairs of blocks) per row
+  constexpr int HP = BPR >= 4 ? BPR / 4 : 0;  // steps per half row when halves span steps
+  constexpr int RB_SHIFT = __builtin_ctz(RB);
+  constexpr bool HALF = STYLE == CM_ROPE_HALF;
+  // a half-split pair whose halves are in different steps: the first-half pair
+  // of blocks is kept in registers for rows of 256 bytes (one step back) and
+  // re-read from the cache for longer rows
+  constexpr bool KEEP = HP == 1;
   // the wave index is the same on every lane: say so, so that everything derived
   // from the task (slot, lengths, offsets, step positions, branches) stays in
   // scalar registers
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
-  const int rb_shift = __builtin_ctz((unsigned)(d * ESIZE));   // log2 of the row bytes
-  const int64_t row_bytes = (int64_t)1 << rb_shift;
-  const int ppr = (int)(row_bytes >> 4);           // 16-byte pieces per row: 4 .. 64
-  const int rps = 4096 >> rb_shift;                // rows per full step
-  const int hp = ppr >> 1;                         // pieces per half row: 2 .. 32
-  const int cp = lane % hp;                        // first-half column of the lane's pairs
-  // byte offsets in a full step of the lane's pieces: f, f + P, f + 128, f + 128 + P
-  const uint32_t pf = (uint32_t)((lane / hp) * ppr + cp) * 16;
-  const uint32_t po[4] = {pf, pf + (uint32_t)hp * 16, pf + 2048, pf + (uint32_t)hp * 16 + 2048};
   const int64_t waves = (int64_t)gridDim.x * kWaves;
+  // Per wave, an 8 KiB buffer through which a pair of blocks of every lane's
+  // chunk is handed to the eight lanes that store that chunk's 128 bytes, and
+  // the merged-cache address of each lane's two blocks.
+  __shared__ u32x4 stage_lds[kWaves][512];
+  __shared__ uint8_t* dst_lds[kWaves][2][64];
+  u32x4* stage = stage_lds[wave];
+  uint8_t* (*dsts)[64] = dst_lds[wave];
+  const int ps = lane & 7;                         // piece (of 8) this lane stores
+  const int cs0 = lane >> 3;                       // chunk (of 8) this lane stores
   // the plan and the task bases are read on the device: a plan the host has not
   // seen is rendered as it stands (its length T_out fits the output by contract)
   const int n_u = (int)plan[CM_PLAN_NUNIQUE];
   const int64_t T_out = plan[CM_PLAN_TOUT];
   const int64_t total_tasks = task_base[n];      // 0 for a plan whose status is an error
   for (int64_t task = (int64_t)blockIdx.x * kWaves + wave; task < total_tasks; task += waves) {
-    int lo = 0, hi = n_u - 1;
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if (task_base[mid] <= task) lo = mid; else hi = mid - 1;
-    }
-    const int s = lo;
+    const int s = fused_slot(task_base, n_u, task);
     const int64_t i = plan[CM_PLAN_HEADER + s];
     const int64_t off = plan[CM_PLAN_HEADER + n + s];
     const int64_t T = plan[CM_PLAN_HEADER + 2 * (int64_t)n + s];
     const bool hashing = select[i] == 0;
-    const int64_t bytes = (int64_t)H * T * row_bytes;
+    const int64_t bytes = (int64_t)H * T * RB;
     const int64_t stripes = stripes_of(bytes);
     const int64_t local = task - task_base[s];
     const int64_t t = local / stripes;             // tensor: 2l + kv
     const int64_t sidx = local - t * stripes;
     const bool rotate = (t & 1) == 0 && off != 0;
     const double* ang = angles + (int64_t)s * d;
-    // the lane's angles: half-split, the pairs of column cp; interleaved, the
-    // pairs inside columns cp (pieces 0, 2) and cp + P (pieces 1, 3)
-    double cs[EP], sn[EP];
-    if (rotate) {
-      piece_angles<ESIZE, STYLE>(ang, cp, ppr, cs, sn);
-      if constexpr (STYLE == CM_ROPE_INTERLEAVED)
-        piece_angles<ESIZE, STYLE>(ang, cp + hp, ppr, cs + NA, sn + NA);
-    }
-    const int64_t in_stripe = (bytes >> 6) - sidx * kStripeBlocks;
-    const int bh = (int)(in_stripe < kStripeBlocks ? in_stripe : kStripeBlocks);
-    const bool full_stripe = bh == kStripeBlocks;
-    const bool hash_steps = hashing && full_stripe;  // the lane's chunk is fed by the steps
-    const int full_steps = bh / kStripeChunks;       // 16 in a full stripe
-    const int rem = bh - full_steps * kStripeChunks; // 0 in a full stripe
-    const uint8_t* src = reinterpret_cast<const uint8_t*>(table[i * stride + 1 + t]) +
-                         ((sidx * kStripeBlocks) << 6);
-    uint8_t* out_t = out + t * (int64_t)H * T_out * row_bytes;
-    const uint64_t chunk0 = (uint64_t)sidx * kStripeChunks;
     const int64_t m = chunks_of(bytes);
+    const int64_t in_stripe = (bytes >> 6) - sidx * kStripeBlocks;
+    const bool full = in_stripe >= kStripeBlocks;
+    const uint64_t chunk = (uint64_t)sidx * kStripeChunks + lane;
+    const FusedLane fl = fused_lane(bytes, sidx, lane, RB_SHIFT, T, T_out, off);
+    const int nb = fl.nb;                          // blocks of the lane's chunk
+    const uint8_t* src = reinterpret_cast<const uint8_t*>(table[i * stride + 1 + t]) + fl.src;
+    uint8_t* dst = out + t * (int64_t)H * T_out * RB + fl.dst;
+    int64_t left = fl.left;
+    const int64_t gap = (T_out - T) << RB_SHIFT;   // end of a head's rows -> next head
+    auto next_row = [&]() { fused_next_row(dst, left, T, gap, RB); };
     B3Cv st;
     b3_init(st);
-    // first row of the current step: head hh, row tt of that head (scalars)
-    int64_t hh, tt;
-    {
-      const int64_t r0 = ((sidx * kStripeBlocks) << 6) >> rb_shift;
-      hh = r0 / T;
-      tt = r0 - hh * T;
-    }
-    const int64_t gap = (T_out - T) << rb_shift;   // end of a head's rows -> next head
-    // Store one step's output y at the current step position (head hh, row tt),
-    // then move the position on by one step. WRAPS: the fragment is shorter than
-    // a step (T < rows per step), so a step may span several heads.
-    auto store_step = [&](auto wraps, const u32x4 (&y)[4]) {
-      if constexpr (!decltype(wraps)::value) {
-        // the step's rows are consecutive rows of the source and, unless the
-        // step crosses the end of a head (at most one step per head; the rows
-        // from `left` on then move on by `gap`), of the merged cache
-        uint8_t* db = out_t + ((hh * T_out + off + tt) << rb_shift);   // wave-uniform base
-        const int64_t left = T - tt;
-        if (__builtin_expect(left >= rps, 1)) {
+    const uint32_t root = m == 1 ? kB3Root : 0u;
+    auto flags = [&](int b, int last) {
+      return (b == 0 ? kB3ChunkStart : 0u) | (b == last ? (kB3ChunkEnd | root) : 0u);
+    };
+
+    // Rotation in place of block x, block bi of its row (pos of its first
+    // piece: bi * 64 bytes), for the pairings a block holds by itself: both
+    // halves of a 64-byte row, or interleaved pairs.
+    auto rotate_own = [&](u32x4 (&x)[4], int bi) {
+      if constexpr (HALF) {
+        // the row is this one block: pieces 0, 1 pair with pieces 2, 3
 #pragma unroll
-          for (int k = 0; k < 4; ++k) st_stream(db + po[k], y[k]);
-        } else {
-          uint8_t* db2 = db + gap;                                      // wave-uniform
-#pragma unroll
-          for (int k = 0; k < 4; ++k)
-            st_stream(((int)(po[k] >> rb_shift) >= (int)left ? db2 : db) + po[k], y[k]);
+        for (int q = 0; q < 2; ++q) {
+          double cs[EP], sn[EP];
+          pair_angles<EP>(ang, q * EP, cs, sn);
+          rotate_pair_half<ESIZE>(x[q], x[q + 2], cs, sn);
         }
-        tt += rps;
-        const bool next_head = tt >= T;
-        tt = next_head ? tt - T : tt;
-        hh += next_head ? 1 : 0;
       } else {
 #pragma unroll
-        for (int k = 0; k < 4; ++k)
-          st_stream(dest_wrapped(out_t, hh, tt, (int)po[k], rb_shift, T, T_out, off), y[k]);
-        tt += rps;
-        while (tt >= T) {
-          tt -= T;
-          ++hh;
+        for (int q = 0; q < 4; ++q) {
+          double cs[EP / 2], sn[EP / 2];
+          pair_angles<EP / 2>(ang, (bi * 64 + 16 * q) / ESIZE / 2, cs, sn);
+          x[q] = rotate_piece_il<ESIZE>(x[q], cs, sn);
         }
       }
     };
-    // One full step j. x holds its data, loaded one step earlier. First the
-    // wave waits for that data (the only memory operations older than it were
-    // issued a step earlier too); then it stores the previous step's output,
-    // which sits in nx (PENDING: there is one), and prefetches step j + 1 into
-    // nx; then it hashes x into the lane's chunk and rotates x in place, which
-    // leaves step j's output in x. Waiting before the stores and loads are
-    // issued keeps every wait clear of memory operations issued in this step.
-    auto step = [&](auto wraps, auto pending, u32x4 (&x)[4], u32x4 (&nx)[4], int j) {
+    // Rotation in place of first-half block a (block bi of its row) and its
+    // second-half partner b.
+    auto rotate_halves = [&](u32x4 (&a)[4], u32x4 (&b)[4], int bi) {
 #pragma unroll
-      for (int k = 0; k < 4; ++k) launder(x[k]);   // wait for x here, before the stores
-      if constexpr (decltype(pending)::value) store_step(wraps, nx);
-      // the last step loads itself again: the loads stay unconditional, which
-      // keeps the count of memory operations the same on every path
-      const int jn = j + 1 < full_steps ? j + 1 : j;
-      const uint8_t* sb = src + ((int64_t)jn << 12);     // wave-uniform base
+      for (int q = 0; q < 4; ++q) {
+        double cs[EP], sn[EP];
+        pair_angles<EP>(ang, bi * (4 * EP) + q * EP, cs, sn);
+        rotate_pair_half<ESIZE>(a[q], b[q], cs, sn);
+      }
+    };
+    // Two blocks of every lane (x0 to d0, x1 to d1) through the LDS: lane l
+    // stores piece l % 8 of chunk 8 j + l / 8 (j = 0 .. 7), so each store
+    // instruction writes eight runs of 128 contiguous bytes.
+    auto put2 = [&](const u32x4 (&x0)[4], const u32x4 (&x1)[4], uint8_t* d0, uint8_t* d1) {
+      dsts[0][lane] = d0;
+      dsts[1][lane] = d1;
 #pragma unroll
-      for (int k = 0; k < 4; ++k) nx[k] = ld16(sb + po[k]);
-      if (hash_steps) compress_pieces(st, x, chunk0 + lane, b3_chunk_flags(j, full_steps, false));
-      if (rotate) {
-        if constexpr (STYLE == CM_ROPE_HALF) {
-          rotate_pair_half<ESIZE>(x[0], x[1], cs, sn);
-          rotate_pair_half<ESIZE>(x[2], x[3], cs, sn);
-        } else {
+      for (int q = 0; q < 4; ++q) {
+        stage[stage_slot(q, lane)] = x0[q];
+        stage[stage_slot(q + 4, lane)] = x1[q];
+      }
+      __builtin_amdgcn_wave_barrier();   // the wave's LDS writes come before its reads
 #pragma unroll
-          for (int k = 0; k < 4; ++k)
-            x[k] = rotate_piece_il<ESIZE>(x[k], cs + (k & 1) * NA, sn + (k & 1) * NA);
+      for (int j = 0; j < 8; ++j) {
+        const int c = 8 * j + cs0;
+        store16(dsts[ps >> 2][c] + (ps & 3) * 16, stage[stage_slot(ps, c)]);
+      }
+      __builtin_amdgcn_wave_barrier();   // and before the next put's writes
+    };
+
+    // Output of step k (blocks 2k, 2k + 1 of every lane's chunk, in y; yp:
+    // with half-split pairs spanning steps, the step half a row earlier, the
+    // first halves of y's pairs): rotated in place if ROTC, stored, then the
+    // lanes move on to the next row after a row's last step. A first-half step
+    // of such a row is output with its partner.
+    auto emit = [&](auto rotc, int k, u32x4 (&y0)[4], u32x4 (&y1)[4], u32x4 (&yp0)[4],
+                    u32x4 (&yp1)[4]) {
+      constexpr bool ROT = decltype(rotc)::value;
+      const int pp = k % PPR;                     // step of the row
+      if constexpr (BPR == 1) {
+        // two rows of one block
+        if (ROT) { rotate_own(y0, 0); rotate_own(y1, 0); }
+        uint8_t* d0 = dst;
+        next_row();
+        put2(y0, y1, d0, dst);
+        next_row();
+        return;
+      } else if constexpr (BPR == 2) {
+        // one row: halves in y0, y1
+        if (ROT) {
+          if (HALF) rotate_halves(y0, y1, 0);
+          else { rotate_own(y0, 0); rotate_own(y1, 1); }
         }
+        put2(y0, y1, dst, dst + 64);
+        next_row();
+        return;
+      } else {
+        if (ROT && HALF) {
+          if (pp < HP) return;                    // output with its partner
+          const int pb = 2 * (pp - HP);           // row block of yp0
+          rotate_halves(yp0, y0, pb);
+          rotate_halves(yp1, y1, pb + 1);
+          put2(yp0, yp1, dst + pb * 64, dst + pb * 64 + 64);
+        } else if (ROT) {
+          rotate_own(y0, 2 * pp);
+          rotate_own(y1, 2 * pp + 1);
+        }
+        put2(y0, y1, dst + 2 * pp * 64, dst + 2 * pp * 64 + 64);
+        if (pp == PPR - 1) next_row();
       }
     };
-    // Software pipeline over the full steps, two buffers; the last step's
-    // output is stored after the loop.
-    auto run = [&](auto wraps) {
-      u32x4 bufa[4], bufb[4];
+
+    // The steps of a full stripe (every lane owns 16 blocks): step k waits for
+    // blocks 2k, 2k + 1 (x, loaded one step earlier); outputs step k - 1 (prev);
+    // loads step k + 1 into nx (the last step loads itself again, so every
+    // step issues the same loads), and, when re-reading, the partner pair of
+    // step k into pn; then compresses its two blocks. The phases are kept apart
+    // so that the fp64 rotation and the compression never hold registers at the
+    // same time; every memory operation older than a step's wait was issued a
+    // step earlier.
+    auto full_stripe = [&](auto hashc, auto rotc) {
+      constexpr bool HASH = decltype(hashc)::value;
+      constexpr bool ROT = decltype(rotc)::value;
+      constexpr bool SPLIT = ROT && HALF && HP > 0;      // halves in different steps
+      u32x4 xa0[4], xa1[4], xb0[4], xb1[4], k0[4], k1[4];
+      auto load2 = [&](u32x4 (&y0)[4], u32x4 (&y1)[4], int b) {
+        load_block(y0, src + b * 64);
+        load_block(y1, src + b * 64 + 64);
+      };
+      auto step = [&](int k, u32x4 (&x0)[4], u32x4 (&x1)[4], u32x4 (&p0)[4], u32x4 (&p1)[4]) {
 #pragma unroll
-      for (int k = 0; k < 4; ++k) bufa[k] = ld16(src + po[k]);
-      step(wraps, std::false_type{}, bufa, bufb, 0);
-      int j = 1;
-      while (j + 1 < full_steps) {
-        step(wraps, std::true_type{}, bufb, bufa, j);
-        step(wraps, std::true_type{}, bufa, bufb, j + 1);
-        j += 2;
+        for (int q = 0; q < 4; ++q) {
+          launder(x0[q]);
+          launder(x1[q]);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        if (k > 0) {
+          // step k - 1 sits in p (the other buffer); its partner in k
+          if constexpr (SPLIT && KEEP) {
+            if (((k - 1) % PPR) < HP) {
+#pragma unroll
+              for (int q = 0; q < 4; ++q) {
+                k0[q] = p0[q];
+                k1[q] = p1[q];
+              }
+            } else {
+              emit(rotc, k - 1, p0, p1, k0, k1);
+            }
+          } else {
+            emit(rotc, k - 1, p0, p1, k0, k1);
+          }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        load2(p0, p1, (k + 1 < 8 ? k + 1 : k) * 2);
+        if constexpr (SPLIT && !KEEP) {
+          // the partner pair of step k, needed when step k is output
+          if ((k % PPR) >= HP) load2(k0, k1, 2 * (k - HP));
+        }
+        if constexpr (HASH) {
+          compress_block(st, x0, chunk, flags(2 * k, kB3ChunkBlocks - 1));
+          compress_block(st, x1, chunk, flags(2 * k + 1, kB3ChunkBlocks - 1));
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      };
+      load2(xa0, xa1, 0);
+#pragma nounroll
+      for (int k = 0; k < 8; k += 2) {
+        step(k, xa0, xa1, xb0, xb1);
+        step(k + 1, xb0, xb1, xa0, xa1);
       }
-      if (j < full_steps) {
-        step(wraps, std::true_type{}, bufb, bufa, j);
-        store_step(wraps, bufb);
-      } else {
-        store_step(wraps, bufa);
+      emit(rotc, 7, xb0, xb1, k0, k1);              // step 7's output
+    };
+
+    // The last stripe of a tensor (a lane may own fewer than 16 blocks, or
+    // none): a block at a time, its partner re-read when it is needed, each lane
+    // storing its own blocks; at most one stripe per tensor, so it is kept
+    // short in registers.
+    auto partial = [&](auto rotc) {
+      constexpr bool ROT = decltype(rotc)::value;
+      u32x4 x[4], par[4];
+      for (int b = 0; b < nb; ++b) {
+        const int pos = b & (BPR - 1);
+        load_block(x, src + b * 64);
+        if (ROT && HALF && BPR > 1 && pos >= HBK) load_block(par, src + (b - HBK) * 64);
+        if (hashing) compress_block(st, x, chunk, flags(b, nb - 1));
+        bool out = true;
+        if (ROT) {
+          if (HALF && BPR > 1) {
+            if (pos >= HBK) rotate_halves(par, x, pos - HBK);
+            else out = false;                     // stored with its partner
+          } else {
+            rotate_own(x, pos);
+          }
+        }
+        if (out) {
+          if (ROT && HALF && BPR > 1) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) store16(dst + (pos - HBK) * 64 + 16 * q, par[q]);
+          }
+#pragma unroll
+          for (int q = 0; q < 4; ++q) store16(dst + pos * 64 + 16 * q, x[q]);
+        }
+        if (pos == BPR - 1) next_row();
       }
     };
-    if (full_steps > 0) {
-      if (T >= rps) run(std::false_type{});
-      else run(std::true_type{});
+
+    if (!full) {
+      if (rotate) partial(std::true_type{});
+      else partial(std::false_type{});
+    } else if (hashing) {
+      if (rotate) full_stripe(std::true_type{}, std::true_type{});
+      else full_stripe(std::true_type{}, std::false_type{});
+    } else {
+      if (rotate) full_stripe(std::false_type{}, std::true_type{});
+      else full_stripe(std::false_type{}, std::false_type{});
     }
-    if (rem > 0) {
-      // short final step: lane < rem owns block `lane` whole (4 consecutive pieces)
-      const uint8_t* sp = src + ((int64_t)full_steps << 12) + lane * 64;
-      u32x4 x[4] = {};
-      if (lane < rem) {
-#pragma unroll
-        for (int k = 0; k < 4; ++k) x[k] = ld16(sp + 16 * k);
-      }
-      const int cb = (int)(((lane * 64) & (row_bytes - 1)) >> 6);   // block of the row
-      if (rotate) rotate_block_tail<ESIZE, STYLE, HB>(x, cb, ppr, ang);
-      if (lane < rem) {
-        uint8_t* dp = dest_wrapped(out_t, hh, tt, lane * 64, rb_shift, T, T_out, off);
-#pragma unroll
-        for (int k = 0; k < 4; ++k) st_stream(dp + 16 * k, x[k]);
-      }
-    }
-    if (hashing) {
-      uint8_t* node = nodes + (base0[i] + t * m + (int64_t)chunk0 + lane) * 32;
-      if (full_stripe) {
-        store_cv(node, st);
-      } else {
-        // the rest of the tensor: chunk `lane` is 1 KiB of consecutive bytes
-        B3Cv rs;
-        if (hash_rest_chunk(rs, src, bh, lane, chunk0, m == 1)) store_cv(node, rs);
-      }
-    }
+    if (hashing && nb > 0) store_cv(nodes + (base0[i] + t * m + (int64_t)chunk) * 32, st);
+  }
+}
+
+// Calls go(IC<RB>) for the row size of the set.
+template <class Go>
+__host__ inline void dispatch_row(int64_t row_bytes, Go&& go) {
+  switch ((int)row_bytes) {
+    case 64: return go(IC<64>{});
+    case 128: return go(IC<128>{});
+    case 256: return go(IC<256>{});
+    case 512: return go(IC<512>{});
+    default: return go(IC<1024>{});
   }
 }
 
@@ -314,24 +402,30 @@ hipError_t launch_render_hash(const SetDesc& s, const HashLayout& hlay, const Re
     const int64_t* base_tab = reinterpret_cast<const int64_t*>(hws + hlay.off_tables);
     const int64_t* tasks = reinterpret_cast<const int64_t*>(rws + rlay.off_tiles);
     const double* angles = reinterpret_cast<const double*>(rws + rlay.off_angles);
-    // the task count is known on the device only: a persistent grid of a few
-    // workgroups per CU strides over it
-    const dim3 grid((uint32_t)(device_cu_count() * CM_FUSED_BLOCKS_PER_CU));
+    // the task count is known on the device only; the tasks of every delivery
+    // (hlay.tasks) bound it. A persistent grid of a few workgroups per CU, or
+    // fewer when there are fewer tasks, strides over it.
+    const int64_t cap = (int64_t)device_cu_count() * CM_FUSED_BLOCKS_PER_CU;
+    const int64_t want = (hlay.tasks + kWaves - 1) / kWaves;
+    const dim3 grid((uint32_t)(want < cap ? (want > 0 ? want : 1) : cap));
     ScopedTiming tm(K_RENDER_HASH, stream);
     uint8_t* nodes = hws + hlay.off_buf0;
     uint8_t* o = reinterpret_cast<uint8_t*>(out);
-    auto go = [&](auto tag) {
-      constexpr int STYLE = decltype(tag)::style, HB = decltype(tag)::hb;
-      if (s.esize == 2)
-        hipLaunchKernelGGL((render_hash_kernel<2, STYLE, HB>), grid, dim3(kThreads), 0, stream,
-                           s.table_dev, s.stride, s.n, plan_dev, tasks, angles, s.H, s.d, hsel,
-                           base_tab, nodes, o);
-      else
-        hipLaunchKernelGGL((render_hash_kernel<4, STYLE, HB>), grid, dim3(kThreads), 0, stream,
-                           s.table_dev, s.stride, s.n, plan_dev, tasks, angles, s.H, s.d, hsel,
-                           base_tab, nodes, o);
+    auto go = [&](auto rbc) {
+      constexpr int RB = decltype(rbc)::value;
+      auto launch = [&](auto kern) {
+        hipLaunchKernelGGL(kern, grid, dim3(kThreads), 0, stream, s.table_dev, s.stride, s.n,
+                           plan_dev, tasks, angles, s.H, s.d, hsel, base_tab, nodes, o);
+      };
+      if (s.esize == 2) {
+        if (style == CM_ROPE_HALF) launch(render_hash_kernel<2, CM_ROPE_HALF, RB>);
+        else launch(render_hash_kernel<2, CM_ROPE_INTERLEAVED, RB>);
+      } else {
+        if (style == CM_ROPE_HALF) launch(render_hash_kernel<4, CM_ROPE_HALF, RB>);
+        else launch(render_hash_kernel<4, CM_ROPE_INTERLEAVED, RB>);
+      }
     };
-    dispatch_style(style, s.row_bytes, go);
+    dispatch_row(s.row_bytes, go);
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   return launch_hash_tree(s, hlay, hsel, 0, digests, hws, stream);

@@ -8,7 +8,9 @@
 namespace cm {
 
 // One workgroup: per-slot cos/sin(off_s * theta_j), theta_j = base^(-2j/d), in
-// fp64, in the piece-ordered layout of rotate.h. With stripe_blocks > 0 also the
+// fp64: in the piece-ordered layout of rotate.h for the unit render
+// (stripe_blocks == 0), in pair order (entry j holds pair j) for the fused
+// hash+render, whose lanes read them wave-uniformly. With stripe_blocks > 0 also the
 // per-slot work-unit bases of the fused hash+render (2L * stripes of that many
 // 64-byte blocks per slot, exclusive scan; the total at index n as well, none if
 // the plan's status is an error) and, with a select mask, hsel[i] = 0
@@ -87,8 +89,9 @@ __device__ __forceinline__ void render_tables(
     const int j = idx - s * halfd;
     const double theta = pow(base, -(double)(2 * j) / (double)d);
     const double phi = (double)plan[CM_PLAN_HEADER + n + s] * theta;
-    const int k = style == CM_ROPE_HALF ? angle_slot_half(j / ep, j % ep, ppr >> 1)
-                                        : angle_slot_il(j / (ep >> 1), j % (ep >> 1), ppr);
+    const int k = stripe_blocks > 0 ? j
+                  : style == CM_ROPE_HALF ? angle_slot_half(j / ep, j % ep, ppr >> 1)
+                                          : angle_slot_il(j / (ep >> 1), j % (ep >> 1), ppr);
     angles[2 * ((int64_t)s * halfd + k)] = cos(phi);
     angles[2 * ((int64_t)s * halfd + k) + 1] = sin(phi);
   }

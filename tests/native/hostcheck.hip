@@ -1,13 +1,17 @@
 // Host-side harness for CPU tests: runs the library's BLAKE3 compression code
 // (paper_2607_01308_amd/csrc/blake3.h, the same source the GPU kernels use) on
 // the CPU, so chunk counters, flags and parent nodes can be compared with the
-// published BLAKE3 test vectors and the oracle without a GPU. Also exposes the
-// compiler's single-step fp64 -> bf16 conversion that the render kernel uses.
-// Test support only.
+// published BLAKE3 test vectors and the oracle without a GPU; exposes the
+// compiler's single-step fp64 -> bf16 conversion that the render kernel uses;
+// and walks the fused kernel's address map (fused_geometry.h, the same source
+// the kernel uses) over every task and lane of a launch. Test support only.
 #include <stdint.h>
 #include <string.h>
 
+#include <vector>
+
 #include "blake3.h"
+#include "fused_geometry.h"
 
 namespace {
 void store(const cm::B3Cv& s, uint8_t* out) { memcpy(out, s.h, 32); }
@@ -41,6 +45,59 @@ void hc_f64_to_bf16(const double* x, uint16_t* y, int64_t n) {
     const __bf16 b = (__bf16)x[i];
     memcpy(&y[i], &b, 2);
   }
+}
+
+// Every (slot, tensor stripe, lane) of a fused launch over n_u slots of
+// lengths T[s] at offsets off[s] (one tensor; every tensor of a slot has the
+// same geometry): checks that each lane reads whole 64-byte blocks and whole
+// rows inside its tensor, that the source rows of all lanes partition the
+// tensor, that each row lands at merged row h * T_out + off + t (the row's
+// head h and position t), and that the merged rows [0, H * T_out) are written
+// exactly once. Returns the number of violations (0: the map is right).
+int64_t hc_fused_check(int32_t n_u, const int64_t* T, const int64_t* off, int32_t H, int32_t rb,
+                       int64_t T_out) {
+  const int rb_shift = __builtin_ctz((unsigned)rb);
+  std::vector<uint8_t> seen((size_t)H * (size_t)T_out, 0);
+  int64_t bad = 0;
+  for (int s = 0; s < n_u; ++s) {
+    const int64_t bytes = (int64_t)H * T[s] * rb;
+    const int64_t stripes = ((bytes >> 6) + 1023) / 1024;
+    const int64_t gap = (T_out - T[s]) << rb_shift;
+    int64_t covered = 0;
+    for (int64_t sidx = 0; sidx < stripes; ++sidx) {
+      for (int lane = 0; lane < 64; ++lane) {
+        const cm::FusedLane f = cm::fused_lane(bytes, sidx, lane, rb_shift, T[s], T_out, off[s]);
+        if (f.nb < 0 || f.nb > 16) { ++bad; continue; }
+        if (f.nb == 0) {
+          if (f.src < bytes) ++bad;              // a lane inside the tensor must own blocks
+          continue;
+        }
+        if (f.src != (sidx * 64 + lane) * 1024 || f.src + f.nb * 64 > bytes) ++bad;
+        if ((f.nb * 64) % rb != 0) ++bad;        // whole rows only
+        if (f.left < 1 || f.left > T[s]) ++bad;
+        int64_t dst = f.dst, left = f.left;
+        const int64_t rows = (int64_t)f.nb * 64 / rb;
+        for (int64_t k = 0; k < rows; ++k) {
+          const int64_t r = (f.src >> rb_shift) + k;      // source row (all heads in order)
+          const int64_t h = r / T[s], t = r % T[s];
+          const int64_t want = (h * T_out + off[s] + t) << rb_shift;
+          if (dst != want || dst < 0 || dst + rb > ((int64_t)H * T_out) << rb_shift) {
+            ++bad;
+          } else {
+            uint8_t& c = seen[(size_t)(dst >> rb_shift)];
+            if (c) ++bad;
+            c = 1;
+          }
+          cm::fused_next_row(dst, left, T[s], gap, rb);
+          ++covered;
+        }
+      }
+    }
+    if (covered != (int64_t)H * T[s]) ++bad;      // the source rows partition the tensor
+  }
+  for (uint8_t c : seen)
+    if (!c) ++bad;
+  return bad;
 }
 
 }  // extern "C"
