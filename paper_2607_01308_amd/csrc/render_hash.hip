@@ -95,11 +95,13 @@ __device__ __forceinline__ void pair_angles(const double* __restrict__ table, in
   }
 }
 
-// Stage slot of 16-byte piece q (0 .. 7: two blocks of four pieces) of lane l's
-// pair of blocks in a wave's LDS buffer: the xor spreads the writes of any
-// eight consecutive lanes, and the reads of the eight lanes that store one
-// chunk's 128 bytes, over distinct LDS banks.
-__device__ __forceinline__ int stage_slot(int q, int l) { return q * 64 + (l ^ q); }
+// A wave's LDS staging area: lane l's pair of blocks (eight 16-byte pieces)
+// at byte l * 144 + q * 16. The 16 bytes of padding per lane put the pieces q
+// of any eight consecutive lanes, and the eight pieces of one lane (read by
+// eight consecutive lanes), on distinct LDS banks; each side addresses them
+// from one register plus immediate offsets.
+constexpr int kStageLane = 144;
+constexpr int kStageBytes = 64 * kStageLane;
 
 // ESIZE: element bytes; STYLE: pairing; RB: row bytes (64 .. 1024).
 template <int ESIZE, int STYLE, int RB>
@@ -125,15 +127,17 @@ __global__ __launch_bounds__(kThreads) CM_FUSED_OCCUPANCY void render_hash_kerne
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   const int64_t waves = (int64_t)gridDim.x * kWaves;
-  // Per wave, an 8 KiB buffer through which a pair of blocks of every lane's
+  // Per wave, a staging area through which a pair of blocks of every lane's
   // chunk is handed to the eight lanes that store that chunk's 128 bytes, and
-  // the merged-cache address of each lane's two blocks.
-  __shared__ u32x4 stage_lds[kWaves][512];
+  // the merged-cache address of each lane's two blocks. Lane l stores piece
+  // l % 8 of chunk 8 j + l / 8 (j = 0 .. 7).
+  __shared__ __attribute__((aligned(16))) uint8_t stage_lds[kWaves][kStageBytes];
   __shared__ uint8_t* dst_lds[kWaves][2][64];
-  u32x4* stage = stage_lds[wave];
-  uint8_t* (*dsts)[64] = dst_lds[wave];
-  const int ps = lane & 7;                         // piece (of 8) this lane stores
-  const int cs0 = lane >> 3;                       // chunk (of 8) this lane stores
+  uint8_t* stage_w = stage_lds[wave] + lane * kStageLane;              // this lane's pieces
+  uint8_t* stage_r = stage_lds[wave] + (lane >> 3) * kStageLane + (lane & 7) * 16;
+  uint8_t** dst_w = &dst_lds[wave][0][lane];
+  uint8_t** dst_r = &dst_lds[wave][(lane & 7) >> 2][lane >> 3];
+  const int pq = lane & 3;                         // piece of its block this lane stores
   // the plan and the task bases are read on the device: a plan the host has not
   // seen is rendered as it stands (its length T_out fits the output by contract)
   const int n_u = (int)plan[CM_PLAN_NUNIQUE];
@@ -201,23 +205,21 @@ __global__ __launch_bounds__(kThreads) CM_FUSED_OCCUPANCY void render_hash_kerne
         rotate_pair_half<ESIZE>(a[q], b[q], cs, sn);
       }
     };
-    // Two blocks of every lane (x0 to d0, x1 to d1) through the LDS: lane l
-    // stores piece l % 8 of chunk 8 j + l / 8 (j = 0 .. 7), so each store
-    // instruction writes eight runs of 128 contiguous bytes.
+    // Two blocks of every lane (x0 to d0, x1 to d1) through the LDS, so that
+    // each store instruction writes eight runs of 128 contiguous bytes.
     auto put2 = [&](const u32x4 (&x0)[4], const u32x4 (&x1)[4], uint8_t* d0, uint8_t* d1) {
-      dsts[0][lane] = d0;
-      dsts[1][lane] = d1;
+      dst_w[0] = d0;
+      dst_w[64] = d1;
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        stage[stage_slot(q, lane)] = x0[q];
-        stage[stage_slot(q + 4, lane)] = x1[q];
+        *reinterpret_cast<u32x4*>(stage_w + q * 16) = x0[q];
+        *reinterpret_cast<u32x4*>(stage_w + 64 + q * 16) = x1[q];
       }
       __builtin_amdgcn_wave_barrier();   // the wave's LDS writes come before its reads
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int c = 8 * j + cs0;
-        store16(dsts[ps >> 2][c] + (ps & 3) * 16, stage[stage_slot(ps, c)]);
-      }
+      for (int j = 0; j < 8; ++j)
+        store16(dst_r[8 * j] + pq * 16,
+                *reinterpret_cast<const u32x4*>(stage_r + j * 8 * kStageLane));
       __builtin_amdgcn_wave_barrier();   // and before the next put's writes
     };
 

@@ -61,6 +61,13 @@ __device__ __forceinline__ float settle_bf16(float f, double y) {
   return __uint_as_float(u);
 }
 
+// Lanes of the wave whose fp32 value f sits on a bf16 midpoint: the rare
+// settling below is one wave-uniform branch, taken when any lane needs it
+// (settle_bf16 leaves every other value unchanged).
+__device__ __forceinline__ uint64_t midpoint_lanes(float f) {
+  return __builtin_amdgcn_ballot_w64(on_bf16_midpoint(f));
+}
+
 // Two fp32 values as the bf16 pair of one word (round to nearest even).
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   const f32x2 v = {lo, hi};
@@ -77,13 +84,13 @@ __device__ __forceinline__ u32x4 round_piece(const double (&y)[16 / ESIZE]) {
   u32x4 out;
   if constexpr (ESIZE == 2) {
     float f[EP];
-    bool mid = false;
+    uint64_t mid = 0;
 #pragma unroll
     for (int e = 0; e < EP; ++e) {
       f[e] = (float)y[e];
-      mid |= on_bf16_midpoint(f[e]);
+      mid |= midpoint_lanes(f[e]);
     }
-    if (__builtin_expect(mid, 0)) {
+    if (__builtin_expect(mid != 0, 0)) {
 #pragma unroll
       for (int e = 0; e < EP; ++e) f[e] = settle_bf16(f[e], y[e]);
     }
@@ -136,15 +143,15 @@ __device__ __forceinline__ void rotate_pair_half(u32x4& a, u32x4& b, const doubl
   constexpr int EP = 16 / ESIZE;
   if constexpr (ESIZE == 2) {
     float fa[EP], fb[EP];
-    bool mid = false;
+    uint64_t mid = 0;
 #pragma unroll
     for (int e = 0; e < EP; ++e) {
       const double x1 = piece_elem<ESIZE>(a, e), x2 = piece_elem<ESIZE>(b, e);
       fa[e] = (float)__builtin_fma(x1, cs[e], -(x2 * sn[e]));
       fb[e] = (float)__builtin_fma(x2, cs[e], x1 * sn[e]);
-      mid |= on_bf16_midpoint(fa[e]) | on_bf16_midpoint(fb[e]);
+      mid |= midpoint_lanes(fa[e]) | midpoint_lanes(fb[e]);
     }
-    if (__builtin_expect(mid, 0)) {
+    if (__builtin_expect(mid != 0, 0)) {
       u32x4 la = a, lb = b;
       launder(la);
       launder(lb);
@@ -173,20 +180,49 @@ __device__ __forceinline__ void rotate_pair_half(u32x4& a, u32x4& b, const doubl
   }
 }
 
-// Interleaved pairs (2q, 2q+1) inside the piece.
+// Interleaved pairs (2q, 2q+1) inside the piece. bf16: each result is rounded
+// to fp32 as soon as it is computed, and in the rare case of a bf16 midpoint
+// the piece's fp64 results are computed again from the inputs (as in
+// rotate_pair_half), so no fp64 result stays live across the test.
 template <int ESIZE>
 __device__ __forceinline__ u32x4 rotate_piece_il(const u32x4 x, const double* cs,
                                                  const double* sn) {
 #pragma clang fp contract(off)
   constexpr int EP = 16 / ESIZE;
-  double y[EP];
+  if constexpr (ESIZE == 2) {
+    float f[EP];
+    uint64_t mid = 0;
 #pragma unroll
-  for (int q = 0; q < EP / 2; ++q) {
-    const double x1 = piece_elem<ESIZE>(x, 2 * q), x2 = piece_elem<ESIZE>(x, 2 * q + 1);
-    y[2 * q] = __builtin_fma(x1, cs[q], -(x2 * sn[q]));
-    y[2 * q + 1] = __builtin_fma(x2, cs[q], x1 * sn[q]);
+    for (int q = 0; q < EP / 2; ++q) {
+      const double x1 = piece_elem<ESIZE>(x, 2 * q), x2 = piece_elem<ESIZE>(x, 2 * q + 1);
+      f[2 * q] = (float)__builtin_fma(x1, cs[q], -(x2 * sn[q]));
+      f[2 * q + 1] = (float)__builtin_fma(x2, cs[q], x1 * sn[q]);
+      mid |= midpoint_lanes(f[2 * q]) | midpoint_lanes(f[2 * q + 1]);
+    }
+    if (__builtin_expect(mid != 0, 0)) {
+      u32x4 lx = x;
+      launder(lx);
+#pragma unroll
+      for (int q = 0; q < EP / 2; ++q) {
+        const double x1 = piece_elem<ESIZE>(lx, 2 * q), x2 = piece_elem<ESIZE>(lx, 2 * q + 1);
+        f[2 * q] = settle_bf16(f[2 * q], __builtin_fma(x1, cs[q], -(x2 * sn[q])));
+        f[2 * q + 1] = settle_bf16(f[2 * q + 1], __builtin_fma(x2, cs[q], x1 * sn[q]));
+      }
+    }
+    u32x4 out;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) out[k] = pack_bf16x2(f[2 * k], f[2 * k + 1]);
+    return out;
+  } else {
+    double y[EP];
+#pragma unroll
+    for (int q = 0; q < EP / 2; ++q) {
+      const double x1 = piece_elem<ESIZE>(x, 2 * q), x2 = piece_elem<ESIZE>(x, 2 * q + 1);
+      y[2 * q] = __builtin_fma(x1, cs[q], -(x2 * sn[q]));
+      y[2 * q + 1] = __builtin_fma(x2, cs[q], x1 * sn[q]);
+    }
+    return round_piece<ESIZE>(y);
   }
-  return round_piece<ESIZE>(y);
 }
 
 // Word of the lane HB away (lane ^ HB) in the wave, without LDS traffic where
