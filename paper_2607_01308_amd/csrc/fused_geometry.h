@@ -11,6 +11,7 @@
 // [off, off + T) of row block h.
 #pragma once
 
+#include <hip/hip_runtime.h>
 #include <stdint.h>
 
 namespace cm {

@@ -71,6 +71,24 @@ __device__ __forceinline__ void order_body(const int64_t* __restrict__ table, in
     s_len[tid] = len;
   }
   const int bad = __syncthreads_or(live && !isfinite(key));
+  if (bad) {
+    // a non-finite score leaves the order undefined: the plan says so and
+    // holds no slots (nothing is rendered from it)
+    if (tid < n) {
+      const int64_t nn = n;
+      plan[CM_PLAN_HEADER + tid] = -1;
+      plan[CM_PLAN_HEADER + nn + tid] = -1;
+      plan[CM_PLAN_HEADER + 2 * nn + tid] = -1;
+      plan[CM_PLAN_HEADER + 3 * nn + tid] = -1;
+    }
+    if (tid == 0) {
+      plan[CM_PLAN_STATUS] = CM_ENONFINITE;
+      plan[CM_PLAN_N] = n;
+      plan[CM_PLAN_NUNIQUE] = 0;
+      plan[CM_PLAN_TOUT] = 0;
+    }
+    return;
+  }
   if (live) {
     bool shared = false;
     for (int j = 0; j < n; ++j) shared |= (j != tid && s_key[j] == key);
@@ -135,7 +153,7 @@ __device__ __forceinline__ void order_body(const int64_t* __restrict__ table, in
     plan[CM_PLAN_HEADER + 3 * nn + tid] = s_rank[s_first[tid]];
   }
   if (tid == n_unique - 1) {
-    plan[CM_PLAN_STATUS] = bad ? CM_ENONFINITE : CM_OK;
+    plan[CM_PLAN_STATUS] = CM_OK;
     plan[CM_PLAN_N] = n;
     plan[CM_PLAN_NUNIQUE] = n_unique;
     plan[CM_PLAN_TOUT] = off + s_slot_len[tid];

@@ -14,18 +14,15 @@
 // slot in its row block. A unit crossing a slot boundary resolves the slot per
 // lane. K at a non-zero offset is rotated with the partner piece fetched from
 // the lane P pieces away.
+#include "render_geometry.h"
 #include "render_tables.h"
 
 namespace cm {
 
 namespace {
 
-#ifndef CM_RENDER_UNIT_PIECES
-#define CM_RENDER_UNIT_PIECES 4
-#endif
-constexpr int kUnitPieces = CM_RENDER_UNIT_PIECES;   // 16-byte pieces per lane
-constexpr int kUnitBytes = 1024 * kUnitPieces;
-constexpr int32_t kUnitCrosses = 1 << 16;            // unit_slot flag: slot boundary inside
+constexpr int kUnitPieces = kRenderUnitPieces;       // 16-byte pieces per lane
+constexpr int kUnitBytes = kRenderUnitBytes;
 
 template <int ESIZE, int STYLE, int HB>
 __global__ __launch_bounds__(64) void render_unit_kernel(
@@ -85,12 +82,8 @@ __global__ __launch_bounds__(64) void render_unit_kernel(
   } else {
     // the unit crosses a slot boundary: slot per lane and piece
 #pragma unroll
-    for (int k = 0; k < kUnitPieces; ++k) {
-      const int64_t r = (lb + 1024 * k) >> rb_shift;
-      int s = s0;
-      while (s + 1 < n_u && offs[s + 1] <= r) ++s;
-      piece(k, s, nullptr, nullptr);
-    }
+    for (int k = 0; k < kUnitPieces; ++k)
+      piece(k, unit_piece_slot(offs, n_u, us, (lb + 1024 * k) >> rb_shift), nullptr, nullptr);
   }
 }
 
@@ -111,26 +104,15 @@ __global__ __launch_bounds__(256) void render_unit_prep_kernel(
   const int n_u = (int)plan[CM_PLAN_NUNIQUE];
   const int64_t* offs = plan + CM_PLAN_HEADER + n;
   const int64_t T_out = plan[CM_PLAN_TOUT];
-  for (int64_t x = tid; x < units; x += nthreads) {
-    const int64_t b0 = (row0 << rb_shift) + x * kUnitBytes;
-    const int64_t r0 = b0 >> rb_shift;
-    int64_t r1 = (b0 + kUnitBytes - 1) >> rb_shift;
-    r1 = r1 < T_out ? r1 : T_out - 1;
-    int lo = 0, hi = n_u - 1;
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if (offs[mid] <= r0) lo = mid; else hi = mid - 1;
-    }
-    const bool crosses = lo + 1 < n_u && offs[lo + 1] <= r1;
-    unit_slot[x] = lo | (crosses ? kUnitCrosses : 0);
-  }
+  for (int64_t x = tid; x < units; x += nthreads)
+    unit_slot[x] = unit_slot_code(offs, n_u, T_out, rb_shift, row0, x);
   for (int64_t e = tid; e < (int64_t)n_u * n_lkh; e += nthreads) {
     const int s = (int)(e / n_lkh);
     const int lkh = (int)(e - (int64_t)s * n_lkh);
     const int64_t i = plan[CM_PLAN_HEADER + s];
     const int64_t T = plan[CM_PLAN_HEADER + 2 * (int64_t)n + s];
     const int64_t base = table[i * stride + 1 + lkh / H];
-    src_base[e] = base + (((int64_t)(lkh % H) * T - offs[s]) << rb_shift);
+    src_base[e] = base + unit_src_offset(lkh % H, T, offs[s], rb_shift, 0);
   }
 }
 

@@ -51,7 +51,8 @@ __device__ __forceinline__ void render_tables(
     const bool all = __syncthreads_and(ok) && head && sc[blockDim.x - 1] == T_out;
     if (tid == 0) {
       *plan_ok = all ? 1 : 0;
-      if (!all) *plan_status = CM_ESHAPE;
+      // a plan that already reports an error (a non-finite score) keeps it
+      if (!all && plan[CM_PLAN_STATUS] == CM_OK) *plan_status = CM_ESHAPE;
     }
     if (!all) return;
     __syncthreads();

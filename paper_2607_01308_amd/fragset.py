@@ -94,8 +94,10 @@ class RenderResult:
 
     A result of the fused pipeline is returned before the device has finished:
     its plan travels to pinned host memory behind an event, and the first use of
-    the plan, T_out, `merged` or `cache` waits for it (a plan whose status is an
-    error raises then)."""
+    the plan, T_out, `merged` or `cache` waits for it. A render whose plan was
+    checked on the device (LatentFragmentSet.render) brings the plan to the host
+    on the first use of `merged` or `cache`. Either way a plan whose status is an
+    error raises then, so a cache that was not rendered is never handed out."""
 
     def __init__(self, cache=None, merged=None, digests_dev=None, keys_dev=None,
                  plan_host: Optional[np.ndarray] = None, tail_len: int = 0,
@@ -122,6 +124,9 @@ class RenderResult:
             else:
                 plan = self.plan_dev.to("cpu").numpy()
                 status = int(plan[C.PLAN_STATUS])
+                if status == C.CM_ENONFINITE:
+                    raise C.CmError(status, "cm_canonical_order",
+                                    "a score is NaN or infinite; nothing was rendered")
                 if status != C.CM_OK:
                     raise C.CmError(status, "cm_render_merge_devplan",
                                     "the plan failed its device check")
@@ -134,6 +139,8 @@ class RenderResult:
             _, _, out, (L, H, d), _ = self._pending
             T_out = self.T_out
             self._merged = out[:L * 2 * H * T_out * d].view(L, 2, 1, H, T_out, d)
+        elif self.plan_host is None:
+            self.plan          # a plan checked on the device: raises if it was rejected
         return self._merged
 
     @property
@@ -141,6 +148,8 @@ class RenderResult:
         if self._cache is None:
             m = self.merged
             self._cache = tuple((m[l, 0], m[l, 1]) for l in range(m.shape[0]))
+        elif self.plan_host is None:
+            self.plan
         return self._cache
 
     @property
@@ -457,6 +466,7 @@ class MergedCache:
             fragment_knorm(batch, self.routing_layer, min(batch.lengths), keys, ws, main)
             canonical_order(batch, keys, digests, plan_dev, main)
             plan = _plan_to_host(plan_dev, main)
+        _check_plan(plan, "cm_canonical_order")     # before the plan is used or the buffer grows
         n, n_u, T_out = int(plan[C.PLAN_N]), int(plan[C.PLAN_NUNIQUE]), int(plan[C.PLAN_TOUT])
         slot_ids = [ids[int(plan[C.PLAN_HEADER + s])] for s in range(n_u)]
         if self.buffer is None or T_out > self.T_cap:

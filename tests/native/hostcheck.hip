@@ -3,8 +3,9 @@
 // the CPU, so chunk counters, flags and parent nodes can be compared with the
 // published BLAKE3 test vectors and the oracle without a GPU; exposes the
 // compiler's single-step fp64 -> bf16 conversion that the render kernel uses;
-// and walks the fused kernel's address map (fused_geometry.h, the same source
-// the kernel uses) over every task and lane of a launch. Test support only.
+// and walks the address maps of the fused kernel (fused_geometry.h) and of the
+// unit render (render_geometry.h), the same sources the kernels use, over every
+// task, unit, lane and piece of a launch. Test support only.
 #include <stdint.h>
 #include <string.h>
 
@@ -12,6 +13,7 @@
 
 #include "blake3.h"
 #include "fused_geometry.h"
+#include "render_geometry.h"
 
 namespace {
 void store(const cm::B3Cv& s, uint8_t* out) { memcpy(out, s.h, 32); }
@@ -97,6 +99,43 @@ int64_t hc_fused_check(int32_t n_u, const int64_t* T, const int64_t* off, int32_
   }
   for (uint8_t c : seen)
     if (!c) ++bad;
+  return bad;
+}
+
+// Every (unit, lane, piece) of a unit-render launch over rows [row0, T_out) of
+// n_u slots of lengths T[s] at offsets off[s]: each piece's slot must hold its
+// row, its source byte must lie inside that slot's tensor for every head, and
+// the pieces must cover rows [row0, T_out) of a row block exactly once.
+// Returns the number of violations.
+int64_t hc_unit_check(int32_t n_u, const int64_t* T, const int64_t* off, int32_t H, int32_t rb,
+                      int64_t row0, int64_t T_out) {
+  const int rb_shift = __builtin_ctz((unsigned)rb);
+  const int64_t end = T_out << rb_shift;
+  const int64_t units = ((T_out - row0) * rb + cm::kRenderUnitBytes - 1) / cm::kRenderUnitBytes;
+  std::vector<uint8_t> seen((size_t)(end >> 4), 0);
+  int64_t bad = 0;
+  for (int64_t x = 0; x < units; ++x) {
+    const int32_t code = cm::unit_slot_code(off, n_u, T_out, rb_shift, row0, x);
+    for (int lane = 0; lane < 64; ++lane) {
+      for (int k = 0; k < cm::kRenderUnitPieces; ++k) {
+        const int64_t b = (row0 << rb_shift) + x * cm::kRenderUnitBytes + lane * 16 + 1024 * k;
+        if (b >= end) continue;                   // past the merged rows: not loaded or stored
+        const int64_t r = b >> rb_shift;
+        const int s = cm::unit_piece_slot(off, n_u, code, r);
+        if (s < 0 || s >= n_u || r < off[s] || r >= off[s] + T[s]) { ++bad; continue; }
+        for (int64_t h = 0; h < H; ++h) {
+          const int64_t o = cm::unit_src_offset(h, T[s], off[s], rb_shift, b);
+          const int64_t want = ((h * T[s] + r - off[s]) << rb_shift) + (b & (rb - 1));
+          if (o != want || o < 0 || o + 16 > ((int64_t)H * T[s]) << rb_shift) ++bad;
+        }
+        uint8_t& c = seen[(size_t)(b >> 4)];
+        if (c) ++bad;
+        c = 1;
+      }
+    }
+  }
+  for (int64_t p = 0; p < (int64_t)seen.size(); ++p)
+    if (seen[(size_t)p] != (p >= ((row0 << rb_shift) >> 4) ? 1 : 0)) ++bad;
   return bad;
 }
 

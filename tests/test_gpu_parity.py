@@ -138,6 +138,50 @@ def test_nonfinite_score_is_an_error():
     check_render(res, frags2, w.dtype, w.routing_layer, w.rope_base)
 
 
+def test_nonfinite_score_in_a_set_render_and_incremental_cache():
+    """A NaN in the routing layer's tail of a set member: the set render and the
+    incremental cache report CM_ENONFINITE (-4) and hand out no cache; the
+    order kernel writes an empty plan for it; a later valid set renders."""
+    w = synth.custom("nan-set", dtype="bfloat16", d=128, H=2, L=2, lengths=(20, 30, 24),
+                     routing_layer=1)
+    frags, _ = gpu_deliveries(w)
+    fs = cm.LatentFragmentSet()
+    fs.ingest_many(frags)
+    mc = cm.MergedCache(fs, w.routing_layer, w.rope_base)
+    mc.update()
+    cap, before = mc.T_cap, [x.clone() for kv in mc.cache for x in kv]
+    bad = [tuple((K.clone(), V.clone()) for K, V in f) for f in frags]
+    bad[2][1][0][0, 0, 23, 5] = float("nan")      # routing layer, last row (inside T* = 20)
+    fs_bad = cm.LatentFragmentSet()
+    fs_bad.ingest_many(bad)
+    res = fs_bad.render(w.routing_layer, w.rope_base)
+    with pytest.raises(cm.CmError) as e:
+        res.cache
+    assert e.value.status == -4
+    with pytest.raises(cm.CmError) as e:
+        res.merged
+    assert e.value.status == -4
+    plan = res.plan_dev.cpu().numpy()
+    n = len(bad)
+    assert plan[0] == -4 and plan[2] == 0 and plan[3] == 0
+    assert (plan[4:4 + 4 * n] == -1).all()
+    # the incremental cache of a set that gains the bad fragment is left as it was
+    fs.ingest(bad[2])                              # a new Id (different bytes)
+    with pytest.raises(cm.CmError) as e:
+        mc.update()
+    assert e.value.status == -4
+    assert mc.T_cap == cap
+    after = [x for kv in mc.cache for x in kv]
+    assert all(torch.equal(a, b) for a, b in zip(before, after))
+    # a valid set still renders, as the deliveries' render (checked against the oracle)
+    ok = cm.LatentFragmentSet()
+    ok.ingest_many(frags)
+    a = ok.render(w.routing_layer, w.rope_base)
+    b = cm.render_deliveries(frags, w.routing_layer, w.rope_base)
+    check_render(b, frags, w.dtype, w.routing_layer, w.rope_base)
+    assert torch.equal(a.merged, b.merged)
+
+
 def test_render_equals_one_long_sequence():
     """Fragments keyed at local positions (rotation done here by complex
     multiplication in fp64) render into one long sequence's keys (§4.2)."""
@@ -354,7 +398,8 @@ def test_fused_interleaved_style(dtype):
 def test_devplan_render_equals_host_checked_render_and_rejects_bad_plans():
     """cm_render_merge_devplan renders the device plan exactly like
     cm_render_merge; a plan that fails the device check moves no byte and
-    reports CM_ESHAPE in its status entry."""
+    reports CM_ESHAPE in its status entry, unless its status already reports an
+    error (a non-finite score, CM_ENONFINITE), which it keeps."""
     w = synth.custom("devplan", dtype="bfloat16", d=128, H=2, L=2, lengths=(300, 129, 77),
                      routing_layer=1)
     _, dl = gpu_deliveries(w)
@@ -380,7 +425,7 @@ def test_devplan_render_equals_host_checked_render_and_rejects_bad_plans():
         out = torch.full_like(ref.merged, 3)
         cm.render_merge_devplan(batch, plan, w.rope_base, "half", out, ref.T_out, ws)
         torch.cuda.synchronize()
-        assert int(plan[0]) == -2, what
+        assert int(plan[0]) == (-4 if what == "status" else -2), what
         assert bool((out == 3).all()), what
     plan = torch.from_numpy(ref.plan.copy()).to("cuda")
     shape = list(ref.merged.shape)
