@@ -41,15 +41,17 @@ HBM_PEAK_GBPS = 8000.0                 # MI355X HBM3E
 VALU_PEAK_TOPS = 256 * 64 * 2.4e9 / 1e12  # 256 CUs x 64 lanes x 2.4 GHz: one 32-bit or fp64 op
 B3_OPS_PER_BLOCK = 672                 # BLAKE3: 7 rounds x 8 G x 12 VALU ops (add3, add, xor, alignbit)
 ROT_OPS_PER_ELEM = 4                   # widen, fp64 product, fp64 FMA, narrow
+OTHER_WORKLOADS = ("qwen3-4b-n4", "qwen3-1.7b-n5", "qwen3-1.7b-n2", "tiny")
 MALL_BYTES = 256 << 20                 # MI355X Infinity Cache: inputs smaller than 4x this are
 ROTATE_TARGET = 4 * MALL_BYTES         # replicated and the steps cycle through the copies
 
 # source files each timed kernel is built from: a traffic summary is only used
 # while these are unchanged
 KERNEL_SOURCES = {
-    "render_hash": ["render_hash.hip", "rotate.h", "blake3.h", "chunk_ops.h", "stream_ops.h",
-                    "internal.h"],
-    "render": ["render.hip", "rotate.h", "stream_ops.h", "internal.h"],
+    "render_hash": ["render_hash.hip", "fused_geometry.h", "rotate.h", "blake3.h", "chunk_ops.h",
+                    "stream_ops.h", "internal.h"],
+    "render": ["render.hip", "render_geometry.h", "render_tables.h", "rotate.h", "stream_ops.h",
+               "internal.h"],
 }
 
 
@@ -97,25 +99,180 @@ def percentiles(ms):
     return [round(v[min(len(v) - 1, int(q * len(v)))], 4) for q in (0.1, 0.5, 0.9)]
 
 
+def _cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def _oracle_path(sample, w, workers):
+    """The oracle's functions over the sample: the Id of every fragment (one
+    tensor root per task), the keys, the order and offsets, then the render of
+    every (layer, slot) (K rotated and rounded, V copied) into the layer's
+    merged arrays; tasks run on `workers` threads (numpy and the C BLAKE3 run
+    outside the interpreter lock)."""
+    import concurrent.futures as cf
+
+    import numpy as np
+    from oracle import cmerge_oracle as om
+
+    with cf.ThreadPoolExecutor(workers) as ex:
+        roots = list(ex.map(lambda t: om.tensor_root(np.ascontiguousarray(sample[t[0]].layers[t[1]][t[2]])),
+                            [(i, l, kv) for i in range(len(sample)) for l in range(w.L)
+                             for kv in (0, 1)]))
+        ids = []
+        for i, f in enumerate(sample):
+            ids.append(om.fragment_id_from_roots(om.fragment_header(f.dtype, f.L, f.H, f.T, f.d),
+                                                 roots[2 * w.L * i:2 * w.L * (i + 1)]))
+        tail = min(f.T for f in sample)
+        keys = [om.fragment_key(f, w.routing_layer, tail) for f in sample]
+        order = om.canonical_order(keys, ids)
+        offs = om.offsets_of([sample[i].T for i in order])
+        T_out = sum(f.T for f in sample)
+        out = [(np.empty((1, w.H, T_out, w.d), sample[0].layers[0][0].dtype),
+                np.empty((1, w.H, T_out, w.d), sample[0].layers[0][0].dtype)) for _ in range(w.L)]
+
+        def unit(t):
+            l, k = t
+            f, off = sample[order[k]], offs[k]
+            K, V = f.layers[l]
+            if off == 0:
+                out[l][0][:, :, :f.T] = K
+            else:
+                c, sn = om.rope_angles(off, w.d, w.rope_base)
+                out[l][0][:, :, off:off + f.T] = om.round_to_dtype(
+                    om.rotate_pairs(om.to_f64(K, f.dtype), c, sn), f.dtype)
+            out[l][1][:, :, off:off + f.T] = V
+
+        list(ex.map(unit, [(l, k) for l in range(w.L) for k in range(len(order))]))
+    return out
+
+
 def cpu_baseline(w, frags):
-    """The oracle, unchanged, over the five shortest distinct fragments."""
+    """The oracle, unchanged, over the five shortest distinct fragments of the
+    workload, on the cores the process may use (a thread pool over (layer,
+    fragment) tasks, at most 16 threads: a GPU host's share per GPU) and on one
+    thread."""
     import oracle
     import synth
     idx = sorted(range(w.n_distinct), key=lambda i: w.lengths[i])[:5]
     sample = [oracle.Fragment(*synth.to_numpy_cache(frags[i])) for i in idx]
-    t0 = time.perf_counter()
-    oracle.render_deliveries(sample, w.routing_layer, w.rope_base)
-    dt = time.perf_counter() - t0
     nbytes = 2 * sum(w.fragment_bytes(i) for i in idx)
+    allowed = len(os.sched_getaffinity(0))
+    cores = min(allowed, 16)
+    t0 = time.perf_counter()
+    _oracle_path(sample, w, cores)
+    dt_all = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    _oracle_path(sample, w, 1)
+    dt_one = time.perf_counter() - t0
     return {
-        "value": round(nbytes / dt / 1e9, 4),
+        "value": round(nbytes / dt_all / 1e9, 4),
         "unit": "GB/s",
-        "cores": 1,
+        "cores": cores,
         "kind": "oracle",
-        "sample": f"full path (hash, score, order, render) over the 5 shortest distinct fragments "
-                  f"(T={[w.lengths[i] for i in idx]}, {nbytes / 1e9:.2f} GB read+write), "
-                  f"{dt:.1f} s, single-threaded numpy + the oracle's C BLAKE3",
+        "value_all": round(nbytes / dt_all / 1e9, 4),
+        "value_1thread": round(nbytes / dt_one / 1e9, 4),
+        "cores_allowed": allowed,
+        "model": _cpu_model(),
+        "sample_bytes": nbytes,
+        "sample": f"full path (Id of every fragment, score, order, render) over the 5 shortest "
+                  f"distinct fragments (T={[w.lengths[i] for i in idx]}, {nbytes / 1e9:.2f} GB "
+                  f"read+write): {dt_all:.1f} s on {cores} threads (tensor roots and (layer, "
+                  f"slot) renders as tasks), {dt_one:.1f} s on one; numpy + the oracle's C BLAKE3",
     }
+
+
+def time_steps(step_fn, steps, warmup):
+    """Mean ms per step (host clock around `steps` steps bracketed by device
+    synchronisation), p10/p50/p90 of per-step HIP event times, and the library's
+    per-kernel totals over the timed steps."""
+    import torch
+    import paper_2607_01308_amd as cm
+
+    for _ in range(warmup):
+        r = step_fn(0)
+        del r
+    torch.cuda.synchronize()
+    cm.timing_reset()
+    cm.timing_enable(True)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev[0].record()
+    for i in range(steps):
+        r = step_fn(i)
+        ev[i + 1].record()
+        del r
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    cm.timing_enable(False)
+    pct = percentiles([ev[i].elapsed_time(ev[i + 1]) for i in range(steps)])
+    kernels = {}
+    for k in cm.KERNELS:
+        ms, n = cm.timing_query(k)
+        if n:
+            kernels[k] = {"total_ms": ms, "launches": n, "avg_ms": ms / n}
+    cm.timing_reset()
+    return (t1 - t0) / steps * 1e3, pct, kernels
+
+
+def replicas(w, deliveries):
+    """Copies of a workload's deliveries so that successive steps read different
+    inputs: a workload under four times the Infinity Cache would otherwise be
+    served from it."""
+    n_copies = max(1, min(32, -(-ROTATE_TARGET // w.delivery_bytes)))
+    return [deliveries] + [[tuple((K.clone(), V.clone()) for K, V in c) for c in deliveries]
+                           for _ in range(n_copies - 1)]
+
+
+def other_workload(name, seed, steps, warmup, dev):
+    """Whole path (steps 1-5) and render of the ingested set (steps 2-5) of one
+    more workload."""
+    import torch
+    import synth
+    import paper_2607_01308_amd as cm
+
+    w = synth.workload(name, seed)
+    frags = synth.make_fragments(w, device=dev)
+    copies = replicas(w, synth.make_deliveries(w, frags))
+    batches = [cm.FragmentBatch(c) for c in copies]
+    n = len(batches)
+    ms, pct, kern = time_steps(
+        lambda i: cm.render_deliveries(batches[i % n], w.routing_layer, w.rope_base), steps, warmup)
+    sets = []
+    for c in copies:
+        sets.append(cm.LatentFragmentSet())
+        sets[-1].ingest_many(c)
+    ms_set, pct_set, kern_set = time_steps(
+        lambda i: sets[i % n].render(w.routing_layer, w.rope_base), steps, warmup)
+    b = w.render_bytes
+    out = {
+        "render_bytes": b, "deliveries": w.n_deliveries, "distinct": w.n_distinct,
+        "merged_tokens": w.merged_tokens, "input_copies": n,
+        "whole_path": {"ms": round(ms, 4), "ms_p10_p50_p90": pct,
+                       "GBps": round(b / (ms / 1e3) / 1e9, 1),
+                       "pct_hbm_peak": round(100 * b / (ms / 1e3) / 1e9 / HBM_PEAK_GBPS, 2),
+                       "merges_per_s": round(1e3 / ms, 1),
+                       "launches_per_step": round(sum(v["launches"] for v in kern.values()) / steps, 1),
+                       "kernels_ms": {k: round(v["total_ms"] / steps, 4) for k, v in kern.items()}},
+        "render_set": {"ms": round(ms_set, 4), "ms_p10_p50_p90": pct_set,
+                       "GBps": round(b / (ms_set / 1e3) / 1e9, 1),
+                       "pct_hbm_peak": round(100 * b / (ms_set / 1e3) / 1e9 / HBM_PEAK_GBPS, 2),
+                       "merges_per_s": round(1e3 / ms_set, 1),
+                       "launches_per_step": round(sum(v["launches"] for v in kern_set.values())
+                                                  / steps, 1),
+                       "kernels_ms": {k: round(v["total_ms"] / steps, 4)
+                                      for k, v in kern_set.items()}},
+    }
+    del sets, batches, copies, frags
+    torch.cuda.empty_cache()
+    return out
 
 
 def main():
@@ -126,6 +283,8 @@ def main():
     ap.add_argument("--workload", default="qwen3-4b-large")
     ap.add_argument("--seed", type=int, default=42)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-other-workloads", action="store_true",
+                    help="skip the whole-path and set-render figures of the four smaller workloads")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first run a plain streaming kernel (torch.neg over 2 GiB of bf16), whose "
                          "known read/write bytes scale rocprofv3's FETCH_SIZE/WRITE_SIZE counters")
@@ -158,47 +317,15 @@ def main():
     batch = cm.FragmentBatch(deliveries)
     # a workload that would sit in the Infinity Cache is replicated, each step
     # taking the next copy, so every step reads its inputs from HBM
-    n_copies = max(1, min(32, -(-ROTATE_TARGET // w.delivery_bytes)))
-    copies = [deliveries] + [[tuple((K.clone(), V.clone()) for K, V in c) for c in deliveries]
-                             for _ in range(n_copies - 1)]
+    copies = replicas(w, deliveries)
+    n_copies = len(copies)
     batches = [batch] + [cm.FragmentBatch(c) for c in copies[1:]]
     torch.cuda.synchronize()
-    k_step = [0]
 
-    def step():
-        b = batches[k_step[0] % n_copies]
-        k_step[0] += 1
-        return cm.render_deliveries(b, w.routing_layer, w.rope_base)
-
-    for _ in range(args.warmup):
-        r = step()
-        del r
-    torch.cuda.synchronize()
-    print("[bench] warmup done", file=sys.stderr, flush=True)
-
-    def events(n):
-        return [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
-
-    cm.timing_reset()
-    cm.timing_enable(True)
-    ev = events(args.steps)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    ev[0].record()
-    for i in range(args.steps):
-        r = step()
-        ev[i + 1].record()
-        del r
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    step_pct = percentiles([ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps)])
-    cm.timing_enable(False)
-    per_kernel = {}
-    for k in cm.KERNELS:
-        ms, n = cm.timing_query(k)
-        if n:
-            per_kernel[k] = {"total_ms": ms, "launches": n, "avg_ms": ms / n}
-    cm.timing_reset()
+    ms_step, step_pct, per_kernel = time_steps(
+        lambda i: cm.render_deliveries(batches[i % n_copies], w.routing_layer, w.rope_base),
+        args.steps, args.warmup)
+    print("[bench] whole path timed", file=sys.stderr, flush=True)
 
     # steps 2-5 on the ingested set (ids already computed at Ingest, Alg. 2)
     sets = []
@@ -206,28 +333,8 @@ def main():
         sets.append(cm.LatentFragmentSet())
         sets[-1].ingest_many(c)
     S = sets[0]
-    for i in range(2):
-        sets[i % n_copies].render(w.routing_layer, w.rope_base)
-    torch.cuda.synchronize()
-    cm.timing_reset()
-    cm.timing_enable(True)
-    ev = events(args.steps)
-    t2 = time.perf_counter()
-    ev[0].record()
-    for i in range(args.steps):
-        r = sets[i % n_copies].render(w.routing_layer, w.rope_base)
-        ev[i + 1].record()
-        del r
-    torch.cuda.synchronize()
-    t3 = time.perf_counter()
-    set_pct = percentiles([ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps)])
-    cm.timing_enable(False)
-    set_kernels = {}
-    for k in cm.KERNELS:
-        ms, n = cm.timing_query(k)
-        if n:
-            set_kernels[k] = {"total_ms": ms, "launches": n}
-    cm.timing_reset()
+    ms_render_set, set_pct, set_kernels = time_steps(
+        lambda i: sets[i % n_copies].render(w.routing_layer, w.rope_base), args.steps, 2)
 
     # the paper's baselines over the same render: the naive multiset re-render
     # (§5.9, every delivery its own operand) and BagMerge in delivery order (§4.2)
@@ -331,8 +438,6 @@ def main():
     del pool, pset, pr
     torch.cuda.empty_cache()
 
-    ms_step = (t1 - t0) / args.steps * 1e3
-    ms_render_set = (t3 - t2) / args.steps * 1e3
     render_bytes = w.render_bytes
     value = render_bytes / (ms_step / 1e3) / 1e9
 
@@ -418,6 +523,16 @@ def main():
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(w, frags)
+    if not args.no_other_workloads:
+        del frags, deliveries, batch, batches, copies, sets, S, distinct
+        torch.cuda.empty_cache()
+        out["workloads"] = {}
+        for name in OTHER_WORKLOADS:
+            if name == w.name:
+                continue
+            print(f"[bench] workload {name}", file=sys.stderr, flush=True)
+            out["workloads"][name] = other_workload(name, args.seed, max(args.steps, 20),
+                                                    args.warmup, dev)
     print(json.dumps(out), flush=True)
 
 
