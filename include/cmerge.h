@@ -286,6 +286,25 @@ int32_t cm_render_deliveries(const cm_fragset* set, int32_t routing_layer, int64
                              int64_t T_cap, void* workspace, size_t workspace_bytes,
                              void* stream);
 
+/* cm_render_deliveries for callers that cannot allocate device memory or
+ * cannot hand over a workspace: code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc. Same arguments, outputs and errors as
+ * cm_render_deliveries, without the workspace: the scratch is a fixed array of
+ * CM_NOALLOC_SCRATCH_BYTES inside the library, one per GPU, created when the
+ * library's code object is loaded on that GPU and held until the process ends.
+ * The call allocates nothing (no hipMalloc, no library allocation); its first
+ * call on a device looks up that device's copy of the array. A set whose
+ * workspace (cm_workspace_size) exceeds CM_NOALLOC_SCRATCH_BYTES is rejected
+ * with CM_EWORKSPACE before anything is enqueued. Every call on one GPU shares
+ * its array, and no stage reads scratch it has not written in the same call:
+ * calls on one GPU must be ordered (one stream, or synchronised); two calls that
+ * overlap on one GPU race and give undefined results. */
+#define CM_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+int32_t cm_render_deliveries_noalloc(const cm_fragset* set, int32_t routing_layer,
+                                     int64_t tail_len, const cm_rope* rope, double* keys_dev,
+                                     uint8_t* mask_dev, uint8_t* digests_dev, int64_t* plan_dev,
+                                     void* out_dev, int64_t T_cap, void* stream);
+
 /* ---------------------------------------------------------------- paged render
  * Paged KV storage (the merge as a permutation of already-allocated blocks plus
  * the RoPE rotation, §4.5): one page pool holds, for every layer and K/V, P pages

@@ -22,6 +22,7 @@ CM_BF16 = 1
 CM_ROPE_HALF = 0
 CM_ROPE_INTERLEAVED = 1
 CM_MAX_FRAGMENTS = 1024
+NOALLOC_SCRATCH_BYTES = 64 << 20     # CM_NOALLOC_SCRATCH_BYTES
 
 PLAN_STATUS, PLAN_N, PLAN_NUNIQUE, PLAN_TOUT, PLAN_HEADER = 0, 1, 2, 3, 4
 
@@ -31,7 +32,7 @@ EXPORTS = (
     "cm_fragment_hash", "cm_fragment_hash_select", "cm_fragment_knorm", "cm_equal_key_mask",
     "cm_canonical_order", "cm_multiset_order", "cm_bag_plan", "cm_render_merge",
     "cm_render_merge_devplan", "cm_render_merge_range", "cm_render_merge_hash",
-    "cm_render_deliveries",
+    "cm_render_deliveries", "cm_render_deliveries_noalloc",
     "cm_paged_workspace_size", "cm_paged_tables", "cm_paged_render",
     "cm_timing_enable", "cm_timing_reset", "cm_timing_query",
 )
@@ -113,6 +114,8 @@ def lib() -> ctypes.CDLL:
                                            P]),
             "cm_render_deliveries": (I32, [FS, I32, I64, ctypes.POINTER(CmRope), P, P, P, P, P,
                                            I64, P, SZ, P]),
+            "cm_render_deliveries_noalloc": (I32, [FS, I32, I64, ctypes.POINTER(CmRope), P, P, P,
+                                                   P, P, I64, P]),
             "cm_paged_workspace_size": (I32, [PS, ctypes.POINTER(SZ)]),
             "cm_paged_tables": (I32, [PS, P, P, I64, P, P, P, ctypes.POINTER(I64)]),
             "cm_paged_render": (I32, [PS, P, P, ctypes.POINTER(CmRope), P, P, P, I64, P, SZ, P]),

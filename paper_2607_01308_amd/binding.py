@@ -212,6 +212,21 @@ def render_deliveries_async(batch: FragmentBatch, routing_layer: int, tail_len: 
                                          _stream(stream, batch)), "cm_render_deliveries")
 
 
+def render_deliveries_noalloc(batch: FragmentBatch, routing_layer: int, tail_len: int,
+                              rope_base: float, style: str, keys: torch.Tensor,
+                              mask: torch.Tensor, digests: torch.Tensor, plan_dev: torch.Tensor,
+                              out: torch.Tensor, T_cap: int, stream=None) -> None:
+    """cm_render_deliveries_noalloc: as render_deliveries_async with the library's
+    fixed per-GPU scratch in place of a workspace (nothing is allocated; calls on
+    one GPU must be ordered)."""
+    rope = C.CmRope(base=float(rope_base), style=_STYLES[style], reserved=0)
+    C.check(C.lib().cm_render_deliveries_noalloc(ctypes.byref(batch.struct), routing_layer,
+                                                 tail_len, ctypes.byref(rope), _ptr(keys),
+                                                 _ptr(mask), _ptr(digests), _ptr(plan_dev),
+                                                 _ptr(out), T_cap, _stream(stream, batch)),
+            "cm_render_deliveries_noalloc")
+
+
 def plan_elems(n: int) -> int:
     return int(C.lib().cm_plan_elems(n))
 

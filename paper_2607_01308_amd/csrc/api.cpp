@@ -85,6 +85,38 @@ int32_t check_ws(void* ws, size_t ws_bytes, size_t need) {
   return CM_OK;
 }
 
+// Scratch of cm_render_deliveries_noalloc: one copy per GPU, created with the
+// library's code object on that device and held until the process ends. On the
+// host `scratch` names a stand-in, not device memory, so host code never passes
+// it to a kernel: device_scratch() looks up the current device's own address
+// once (hipGetSymbolAddress) and every launch takes that.
+constexpr size_t kScratchBytes = (size_t)CM_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+int32_t device_scratch(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail_hip(e, "cm_render_deliveries_noalloc: hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(CM_EINVAL, "cm_render_deliveries_noalloc: device index " + std::to_string(dev) +
+                               " is beyond the library's table of " + std::to_string(kMaxDevices));
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return fail_hip(e, "cm_render_deliveries_noalloc: hipGetSymbolAddress");
+    if (!p || !aligned(p, cm::kWsAlign))
+      return fail(CM_EHIP, "cm_render_deliveries_noalloc: scratch address is NULL or misaligned");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return CM_OK;
+}
+
 // Every call fits in this many bytes; the fused render+hash needs the hash
 // workspace followed by the render workspace.
 size_t workspace_need(const cm::SetDesc& s) {
@@ -493,11 +525,18 @@ int32_t cm_render_merge_hash(const cm_fragset* set, const int64_t* plan_dev,
   return e == hipSuccess ? CM_OK : fail_hip(e, "cm_render_merge_hash");
 }
 
-int32_t cm_render_deliveries(const cm_fragset* set, int32_t routing_layer, int64_t tail_len,
-                             const cm_rope* rope, double* keys_dev, uint8_t* mask_dev,
-                             uint8_t* digests_dev, int64_t* plan_dev, void* out_dev,
-                             int64_t T_cap, void* workspace, size_t workspace_bytes,
-                             void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Steps 1-5 of cm_render_deliveries after its argument checks. The workspace is
+// the caller's (workspace_bytes its size) or, with fixed_scratch, this device's
+// copy of `scratch`, once the set's need is known to fit it.
+int32_t render_deliveries_common(const cm_fragset* set, int32_t routing_layer, int64_t tail_len,
+                                 const cm_rope* rope, double* keys_dev, uint8_t* mask_dev,
+                                 uint8_t* digests_dev, int64_t* plan_dev, void* out_dev,
+                                 int64_t T_cap, void* workspace, size_t workspace_bytes,
+                                 bool fixed_scratch, void* stream, const char* where) {
   g_err.clear();
   cm::SetDesc s;
   int32_t st = check_set(set, &s);
@@ -521,7 +560,18 @@ int32_t cm_render_deliveries(const cm_fragset* set, int32_t routing_layer, int64
   if (T_cap < T_all)
     return fail(CM_ESHAPE, "T_cap must be at least the sum of the delivery lengths (" +
                                std::to_string(T_all) + "), got " + std::to_string(T_cap));
-  if ((st = check_ws(workspace, workspace_bytes, workspace_need(s))) != CM_OK) return st;
+  const size_t need = workspace_need(s);
+  if (fixed_scratch) {
+    if (need > kScratchBytes)
+      return fail(CM_EWORKSPACE, std::string(where) + ": this set needs " + std::to_string(need) +
+                                     " bytes of scratch, more than the fixed " +
+                                     std::to_string(kScratchBytes) +
+                                     " (CM_NOALLOC_SCRATCH_BYTES); call cm_render_deliveries "
+                                     "with a workspace instead");
+    if ((st = device_scratch(&workspace)) != CM_OK) return st;
+  } else if ((st = check_ws(workspace, workspace_bytes, need)) != CM_OK) {
+    return st;
+  }
   uint8_t* ws = static_cast<uint8_t*>(workspace);
   hipStream_t sm = static_cast<hipStream_t>(stream);
   // the workspace is reused by each stage in turn: they run in order on one stream
@@ -543,7 +593,30 @@ int32_t cm_render_deliveries(const cm_fragset* set, int32_t routing_layer, int64
   if (e == hipSuccess)
     e = cm::launch_render_hash(s, hlay, rlay, plan_dev, rope->base, rope->style, mask_dev,
                                digests_dev, out_dev, ws, sm, true, true);
-  return e == hipSuccess ? CM_OK : fail_hip(e, "cm_render_deliveries");
+  return e == hipSuccess ? CM_OK : fail_hip(e, where);
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t cm_render_deliveries(const cm_fragset* set, int32_t routing_layer, int64_t tail_len,
+                             const cm_rope* rope, double* keys_dev, uint8_t* mask_dev,
+                             uint8_t* digests_dev, int64_t* plan_dev, void* out_dev,
+                             int64_t T_cap, void* workspace, size_t workspace_bytes,
+                             void* stream) {
+  return render_deliveries_common(set, routing_layer, tail_len, rope, keys_dev, mask_dev,
+                                  digests_dev, plan_dev, out_dev, T_cap, workspace,
+                                  workspace_bytes, false, stream, "cm_render_deliveries");
+}
+
+int32_t cm_render_deliveries_noalloc(const cm_fragset* set, int32_t routing_layer,
+                                     int64_t tail_len, const cm_rope* rope, double* keys_dev,
+                                     uint8_t* mask_dev, uint8_t* digests_dev, int64_t* plan_dev,
+                                     void* out_dev, int64_t T_cap, void* stream) {
+  return render_deliveries_common(set, routing_layer, tail_len, rope, keys_dev, mask_dev,
+                                  digests_dev, plan_dev, out_dev, T_cap, nullptr, 0, true, stream,
+                                  "cm_render_deliveries_noalloc");
 }
 
 }  // extern "C"

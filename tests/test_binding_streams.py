@@ -99,6 +99,8 @@ CALLS = {
                                                                 1, T, s),
     "render_deliveries_async": lambda b, s: binding.render_deliveries_async(
         b, 0, 1, 1e4, "half", T, T, T, T, T, 1, T, s),
+    "render_deliveries_noalloc": lambda b, s: binding.render_deliveries_noalloc(
+        b, 0, 1, 1e4, "half", T, T, T, T, T, 1, s),
 }
 
 

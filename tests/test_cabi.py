@@ -275,6 +275,36 @@ def test_render_deliveries_argument_checks(lib):
     assert call(rope=bad) == C.CM_EINVAL
 
 
+def test_render_deliveries_noalloc_argument_checks(lib):
+    """The entry point without a workspace runs the same checks, and a set whose
+    workspace exceeds the fixed scratch is refused before the library touches
+    the GPU (no device is needed to reach that answer)."""
+    rope = C.CmRope(base=1e4, style=0, reserved=0)
+    keys, mask, dig = ctypes.c_void_p(0x10000), ctypes.c_void_p(0x20000), ctypes.c_void_p(0x30000)
+    plan, out = ctypes.c_void_p(0x50000), ctypes.c_void_p(0x80000)
+
+    def call(fs, layer=1, tail=5, T_cap=None, keys=keys, dig=dig, out=out):
+        T_cap = int(fs.table[:, 0].sum()) if T_cap is None else T_cap
+        return lib.cm_render_deliveries_noalloc(fs.ref, layer, tail, ctypes.byref(rope), keys,
+                                                mask, dig, plan, out, T_cap, None)
+
+    small = FakeSet(lengths=(5, 9))
+    assert call(small, T_cap=13) == C.CM_ESHAPE
+    assert call(small, layer=2) == C.CM_EINVAL
+    assert call(small, tail=6) == C.CM_EINVAL
+    assert call(small, keys=None) == C.CM_EINVAL
+    assert call(small, dig=ctypes.c_void_p(0x30008)) == C.CM_EINVAL
+    assert call(small, out=None) == C.CM_EINVAL
+    # 4 bf16 fragments of 4 layers x K, V x 8 heads x 30,000 rows x 128: about
+    # 2 GB, whose 32-byte digest per 1 KiB chunk alone exceeds the fixed scratch
+    big = FakeSet(lengths=(30000,) * 4, L=4, H=8, d=128, dtype=C.CM_BF16, align=1 << 24)
+    st, need = _ws(lib, big)
+    assert st == C.CM_OK and need > C.NOALLOC_SCRATCH_BYTES
+    assert call(big) == C.CM_EWORKSPACE
+    msg = lib.cm_last_error().decode()
+    assert "CM_NOALLOC_SCRATCH_BYTES" in msg and str(need) in msg
+
+
 def test_render_range_argument_checks(lib):
     fs = FakeSet(lengths=(5, 9))
     _, need = _ws(lib, fs)
