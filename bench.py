@@ -188,10 +188,12 @@ def cpu_baseline(w, frags):
     }
 
 
-def time_steps(step_fn, steps, warmup):
+def time_steps(step_fn, steps, warmup, kernel_timing=True):
     """Mean ms per step (host clock around `steps` steps bracketed by device
     synchronisation), p10/p50/p90 of per-step HIP event times, and the library's
-    per-kernel totals over the timed steps."""
+    per-kernel totals over the timed steps (kernel_timing; the library then
+    records an event pair around every launch, which costs a few microseconds
+    per launch: negligible for the large workload, not for the small ones)."""
     import torch
     import paper_2607_01308_amd as cm
 
@@ -200,7 +202,7 @@ def time_steps(step_fn, steps, warmup):
         del r
     torch.cuda.synchronize()
     cm.timing_reset()
-    cm.timing_enable(True)
+    cm.timing_enable(kernel_timing)
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -243,14 +245,19 @@ def other_workload(name, seed, steps, warmup, dev):
     copies = replicas(w, synth.make_deliveries(w, frags))
     batches = [cm.FragmentBatch(c) for c in copies]
     n = len(batches)
-    ms, pct, kern = time_steps(
-        lambda i: cm.render_deliveries(batches[i % n], w.routing_layer, w.rope_base), steps, warmup)
     sets = []
     for c in copies:
         sets.append(cm.LatentFragmentSet())
         sets[-1].ingest_many(c)
-    ms_set, pct_set, kern_set = time_steps(
-        lambda i: sets[i % n].render(w.routing_layer, w.rope_base), steps, warmup)
+    whole = lambda i: cm.render_deliveries(batches[i % n], w.routing_layer, w.rope_base)
+    render = lambda i: sets[i % n].render(w.routing_layer, w.rope_base)
+    # the step times without per-launch events, then the same steps again for the
+    # per-kernel breakdown (event-timed, so each kernel's figure includes its
+    # launch latency)
+    ms, pct, _ = time_steps(whole, steps, warmup, kernel_timing=False)
+    ms_set, pct_set, _ = time_steps(render, steps, warmup, kernel_timing=False)
+    _, _, kern = time_steps(whole, steps, 0)
+    _, _, kern_set = time_steps(render, steps, 0)
     b = w.render_bytes
     out = {
         "render_bytes": b, "deliveries": w.n_deliveries, "distinct": w.n_distinct,
@@ -531,7 +538,9 @@ def main():
             if name == w.name:
                 continue
             print(f"[bench] workload {name}", file=sys.stderr, flush=True)
-            out["workloads"][name] = other_workload(name, args.seed, max(args.steps, 20),
+            # many short steps: a step of tens of microseconds needs hundreds for a
+            # mean that the first step's host latency does not move
+            out["workloads"][name] = other_workload(name, args.seed, max(args.steps, 200),
                                                     args.warmup, dev)
     print(json.dumps(out), flush=True)
 

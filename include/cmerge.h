@@ -13,6 +13,7 @@
  *                           both concatenated along the sequence axis
  *   cm_render_merge_devplan the same with the plan left on the device
  *   cm_render_merge_range   the slots from a given rank on (incremental render)
+ *   cm_render_set           steps 2-5 for a set with known Ids, in one call
  *   cm_paged_tables / cm_paged_render  the same render over paged storage
  * the paper's baselines over the same render:
  *   cm_multiset_order       the naive re-render order of §5.9 (no dedupe)
@@ -249,6 +250,21 @@ int32_t cm_render_merge_range(const cm_fragset* set, const int64_t* plan_dev,
 int32_t cm_render_merge_devplan(const cm_fragset* set, int64_t* plan_dev, const cm_rope* rope,
                                 void* out_dev, int64_t T_out, void* workspace,
                                 size_t workspace_bytes, void* stream);
+/* Render of Alg. 2 for a set whose members are distinct and whose Ids are
+ * known (computed at Ingest): steps 2-5 in one call with nothing waiting for the
+ * host. cm_fragment_knorm (keys_dev), cm_canonical_order (plan_dev) and the
+ * render of cm_render_merge_devplan, with the order and the render's tables
+ * built in one launch. digests_dev: n * 32 bytes, device, 16-byte aligned, the
+ * members' Ids; routing_layer, tail_len as cm_fragment_knorm. T_out must be the
+ * sum of all member lengths (CM_ESHAPE otherwise): out_dev holds
+ * [L][2][1][H][T_out][d]. After the stream has finished the caller reads
+ * plan_dev's status: CM_ENONFINITE (a score is not finite) or CM_ESHAPE (two
+ * members have the same Id, so the plan's T_out is shorter) mean nothing was
+ * rendered. Workspace: cm_workspace_size() bytes. */
+int32_t cm_render_set(const cm_fragset* set, const uint8_t* digests_dev, int32_t routing_layer,
+                      int64_t tail_len, const cm_rope* rope, double* keys_dev, int64_t* plan_dev,
+                      void* out_dev, int64_t T_out, void* workspace, size_t workspace_bytes,
+                      void* stream);
 /* Steps 1 and 4-5 in one pass: the render of cm_render_merge and, for every
  * slot delivery i with select_dev[i] == 0, its Id (as cm_fragment_hash) written
  * to digests_dev[i]; the Id's chunk level is computed from the same loads that

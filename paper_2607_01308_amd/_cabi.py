@@ -31,7 +31,7 @@ EXPORTS = (
     "cm_version", "cm_last_error", "cm_status_string", "cm_plan_elems", "cm_workspace_size",
     "cm_fragment_hash", "cm_fragment_hash_select", "cm_fragment_knorm", "cm_equal_key_mask",
     "cm_canonical_order", "cm_multiset_order", "cm_bag_plan", "cm_render_merge",
-    "cm_render_merge_devplan", "cm_render_merge_range", "cm_render_merge_hash",
+    "cm_render_merge_devplan", "cm_render_merge_range", "cm_render_merge_hash", "cm_render_set",
     "cm_render_deliveries", "cm_render_deliveries_noalloc",
     "cm_paged_workspace_size", "cm_paged_tables", "cm_paged_render",
     "cm_timing_enable", "cm_timing_reset", "cm_timing_query",
@@ -112,6 +112,8 @@ def lib() -> ctypes.CDLL:
                                             P]),
             "cm_render_merge_hash": (I32, [FS, P, P, ctypes.POINTER(CmRope), P, P, P, I64, P, SZ,
                                            P]),
+            "cm_render_set": (I32, [FS, P, I32, I64, ctypes.POINTER(CmRope), P, P, P, I64, P, SZ,
+                                    P]),
             "cm_render_deliveries": (I32, [FS, I32, I64, ctypes.POINTER(CmRope), P, P, P, P, P,
                                            I64, P, SZ, P]),
             "cm_render_deliveries_noalloc": (I32, [FS, I32, I64, ctypes.POINTER(CmRope), P, P, P,

@@ -212,6 +212,19 @@ def render_deliveries_async(batch: FragmentBatch, routing_layer: int, tail_len: 
                                          _stream(stream, batch)), "cm_render_deliveries")
 
 
+def render_set(batch: FragmentBatch, digests: torch.Tensor, routing_layer: int, tail_len: int,
+               rope_base: float, style: str, keys: torch.Tensor, plan_dev: torch.Tensor,
+               out: torch.Tensor, T_out: int, workspace: torch.Tensor, stream=None) -> None:
+    """cm_render_set: steps 2-5 for a set of distinct fragments whose Ids are
+    known, in one call; the plan's status tells whether it was rendered."""
+    rope = C.CmRope(base=float(rope_base), style=_STYLES[style], reserved=0)
+    C.check(C.lib().cm_render_set(ctypes.byref(batch.struct), _ptr(digests), routing_layer,
+                                  tail_len, ctypes.byref(rope), _ptr(keys), _ptr(plan_dev),
+                                  _ptr(out), T_out, _ptr(workspace),
+                                  workspace.numel() * workspace.element_size(),
+                                  _stream(stream, batch)), "cm_render_set")
+
+
 def render_deliveries_noalloc(batch: FragmentBatch, routing_layer: int, tail_len: int,
                               rope_base: float, style: str, keys: torch.Tensor,
                               mask: torch.Tensor, digests: torch.Tensor, plan_dev: torch.Tensor,

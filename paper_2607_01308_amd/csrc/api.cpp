@@ -117,14 +117,17 @@ int32_t device_scratch(void** out) {
   return CM_OK;
 }
 
-// Every call fits in this many bytes; the fused render+hash needs the hash
-// workspace followed by the render workspace.
-size_t workspace_need(const cm::SetDesc& s) {
-  const size_t hb = cm::align_up(cm::hash_layout(s).bytes, cm::kWsAlign);
-  const size_t rb = cm::render_layout(s).bytes;
-  size_t need = hb + rb;
+// Every call fits in this many bytes: the render's tables follow the hash
+// workspace (fused render+hash) or the score partials (set render, which keeps
+// them until the order kernel has folded them).
+size_t render_ws_offset(const cm::SetDesc& s) {
+  const size_t hb = cm::hash_layout(s).bytes;
   const size_t kn = cm::knorm_max_bytes(s);
-  return kn > need ? kn : need;
+  return cm::align_up(hb > kn ? hb : kn, cm::kWsAlign);
+}
+
+size_t workspace_need(const cm::SetDesc& s) {
+  return render_ws_offset(s) + cm::render_layout(s).bytes;
 }
 
 int64_t min_T(const cm::SetDesc& s) {
@@ -499,6 +502,47 @@ int32_t cm_render_merge_devplan(const cm_fragset* set, int64_t* plan_dev, const 
   return e == hipSuccess ? CM_OK : fail_hip(e, "cm_render_merge_devplan");
 }
 
+int32_t cm_render_set(const cm_fragset* set, const uint8_t* digests_dev, int32_t routing_layer,
+                      int64_t tail_len, const cm_rope* rope, double* keys_dev, int64_t* plan_dev,
+                      void* out_dev, int64_t T_out, void* workspace, size_t workspace_bytes,
+                      void* stream) {
+  g_err.clear();
+  cm::SetDesc s;
+  int32_t st = check_set(set, &s);
+  if (st != CM_OK) return st;
+  if ((st = check_rope(rope)) != CM_OK) return st;
+  if (routing_layer < 0 || routing_layer >= s.L)
+    return fail(CM_EINVAL, "routing_layer must be in [0, L), got " + std::to_string(routing_layer));
+  const int64_t tmin = min_T(s);
+  if (tail_len < 1 || tail_len > tmin)
+    return fail(CM_EINVAL, "tail_len must be in [1, min T] = [1, " + std::to_string(tmin) + "], got " +
+                               std::to_string(tail_len));
+  if (!digests_dev || !aligned(digests_dev, 16))
+    return fail(CM_EINVAL, "digests_dev is NULL or not 16-byte aligned");
+  if (!keys_dev || !aligned(keys_dev, 8)) return fail(CM_EINVAL, "keys_dev is NULL or misaligned");
+  if (!plan_dev || !aligned(plan_dev, 8)) return fail(CM_EINVAL, "plan_dev is NULL or misaligned");
+  if (!out_dev || !aligned(out_dev, 16))
+    return fail(CM_EINVAL, "out_dev is NULL or not 16-byte aligned");
+  int64_t T_all = 0;
+  for (int i = 0; i < s.n; ++i) T_all += s.T(i);
+  if (T_out != T_all)
+    return fail(CM_ESHAPE, "T_out must be the sum of the member lengths (" + std::to_string(T_all) +
+                               "), got " + std::to_string(T_out));
+  if (cm::render_units(s, T_out) >= ((int64_t)1 << 31))
+    return fail(CM_ESHAPE, "merged cache too long for one launch");
+  if ((st = check_ws(workspace, workspace_bytes, workspace_need(s))) != CM_OK) return st;
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  hipStream_t sm = static_cast<hipStream_t>(stream);
+  // score partials at the start of the workspace, the render's tables after them
+  cm::KnormPartials kp{};
+  hipError_t e = cm::launch_knorm_partial(s, cm::knorm_layout(s, tail_len), routing_layer,
+                                          tail_len, keys_dev, ws, sm, cm::kKnormFoldMax, &kp);
+  if (e == hipSuccess)
+    e = cm::launch_render_set(s, cm::render_layout(s), kp, keys_dev, digests_dev, plan_dev, T_out,
+                              rope->base, rope->style, out_dev, ws + render_ws_offset(s), sm);
+  return e == hipSuccess ? CM_OK : fail_hip(e, "cm_render_set");
+}
+
 int32_t cm_render_merge_hash(const cm_fragset* set, const int64_t* plan_dev,
                              const int64_t* plan_host, const cm_rope* rope,
                              const uint8_t* select_dev, uint8_t* digests_dev, void* out_dev,
@@ -575,12 +619,14 @@ int32_t render_deliveries_common(const cm_fragset* set, int32_t routing_layer, i
   uint8_t* ws = static_cast<uint8_t*>(workspace);
   hipStream_t sm = static_cast<hipStream_t>(stream);
   // the workspace is reused by each stage in turn: they run in order on one stream
-  hipError_t e = cm::launch_knorm(s, cm::knorm_layout(s, tail_len), routing_layer, tail_len,
-                                  keys_dev, ws, sm);
+  cm::KnormPartials kp{};
+  hipError_t e = cm::launch_knorm_partial(s, cm::knorm_layout(s, tail_len), routing_layer,
+                                          tail_len, keys_dev, ws, sm, cm::kKnormFoldMax, &kp);
   const cm::HashLayout hlay = cm::hash_layout(s);
-  // the key mask and the hash trees' node tables in one launch (the tables depend
-  // only on the lengths); the knorm scratch they overwrite is no longer needed
-  if (e == hipSuccess) e = cm::launch_mask_hash_prep(s, hlay, keys_dev, mask_dev, ws, sm);
+  // the last score levels, the key mask and the hash trees' node tables in one
+  // launch (the tables depend only on the lengths); it reads the score partials
+  // before it writes over them
+  if (e == hipSuccess) e = cm::launch_mask_hash_prep(s, hlay, kp, keys_dev, mask_dev, ws, sm);
   if (e == hipSuccess) e = cm::launch_hash(s, hlay, mask_dev, 1, digests_dev, ws, sm, true);
   // the order kernel also builds the render's per-slot tables; the node-base
   // tables written for the first Ids are still in the workspace (the render's

@@ -13,6 +13,7 @@
 // nine levels remain, then one launch folds the top of every tensor's tree.
 #include "chunk_ops.h"
 #include "key_mask.h"
+#include "knorm_fold.h"
 
 namespace cm {
 
@@ -43,9 +44,11 @@ __device__ __forceinline__ int find_fragment(const int64_t* __restrict__ base, i
 // inclusive scans.
 __device__ __forceinline__ void hash_tables(const int64_t* __restrict__ table, int32_t n,
                                             int64_t stride, int64_t token_bytes, int32_t L,
-                                            int32_t levels, int64_t* __restrict__ base) {
+                                            int32_t levels, int64_t* __restrict__ base,
+                                            int32_t* __restrict__ arrived) {
   __shared__ int64_t sc[1024];
   const int tid = threadIdx.x;
+  if (tid < n) arrived[tid] = 0;
   const int64_t bytes = tid < n ? table[(int64_t)tid * stride] * token_bytes : 0;
   const int64_t m0 = tid < n ? chunks_of(bytes) : 0;
   for (int v = 0; v <= levels + 1; ++v) {
@@ -70,18 +73,22 @@ __global__ __launch_bounds__(1024) void hash_prep_kernel(const int64_t* __restri
                                                          int32_t n, int64_t stride,
                                                          int64_t token_bytes, int32_t L,
                                                          int32_t levels,
-                                                         int64_t* __restrict__ base) {
-  hash_tables(table, n, stride, token_bytes, L, levels, base);
+                                                         int64_t* __restrict__ base,
+                                                         int32_t* __restrict__ arrived) {
+  hash_tables(table, n, stride, token_bytes, L, levels, base, arrived);
 }
 
-// The key mask and the node-base tables in one launch (the tables depend only
-// on the lengths; the two parts share nothing but the workgroup).
+// The last levels of the scores (count > 1), the key mask and the node-base
+// tables in one launch (the tables depend only on the lengths). The score
+// partials may share workspace with the tables: the fold reads all of them
+// into LDS before a table entry is written.
 __global__ __launch_bounds__(1024) void mask_hash_prep_kernel(
     const int64_t* __restrict__ table, int32_t n, int64_t stride, int64_t token_bytes, int32_t L,
-    int32_t levels, const double* __restrict__ keys, uint8_t* __restrict__ mask,
-    int64_t* __restrict__ base) {
+    int32_t levels, const double* parts, int64_t count, double* keys,
+    uint8_t* __restrict__ mask, int64_t* base, int32_t* __restrict__ arrived) {
+  if (count > 1) knorm_fold(parts, n, count, keys);
   equal_key_mask_body(n, keys, mask);
-  hash_tables(table, n, stride, token_bytes, L, levels, base);
+  hash_tables(table, n, stride, token_bytes, L, levels, base, arrived);
 }
 
 // One wave = one (tensor, stripe) task at a time: lane k hashes chunk k of the
@@ -249,6 +256,62 @@ __device__ __forceinline__ void fold_cvs(uint32_t* lds, int cnt, bool root, int 
   }
 }
 
+// Id = BLAKE3-256(header || root(K^0) || root(V^0) || ...) of fragment i by
+// one 64-lane workgroup. The message is L + 1 blocks (the header, then per
+// layer the pair of roots K, V) in C = ceil((L + 1) / 16) chunks. Lane k hashes
+// chunk 64 g + k of each group g of 64 chunks; a full group is an aligned
+// complete subtree of BLAKE3's left-balanced tree and is folded into one value,
+// the last group into the value of its own subtree (carries included); then the
+// group values are folded. ROOT marks the single chunk (C = 1) or the last
+// compression.
+constexpr int kFinalGroups = 32;   // 32 x 64 chunks: L + 1 <= 32768 blocks
+
+struct IdShape {
+  int32_t L, H, d;
+  uint32_t dtype_code, esize;
+};
+
+__device__ __forceinline__ void fragment_id(uint64_t T, const IdShape& sh,
+                                            const uint8_t* __restrict__ r,
+                                            uint8_t* __restrict__ digest, int lane) {
+  __shared__ uint32_t chunk_cv[64 * 8];
+  __shared__ uint32_t group_cv[kFinalGroups * 8];
+  const int64_t blocks = (int64_t)sh.L + 1;
+  const int64_t chunks = (blocks + kB3ChunkBlocks - 1) / kB3ChunkBlocks;
+  const int groups = (int)((chunks + 63) / 64);
+  auto load = [&](int64_t g, uint32_t (&w)[16]) {
+    if (g == 0) {
+      const uint32_t h[16] = {0x52464D43u, 0x31304741u,  // "CMFRAG01"
+                              sh.dtype_code, sh.esize, (uint32_t)sh.L, 1u, (uint32_t)sh.H,
+                              (uint32_t)T, (uint32_t)(T >> 32), (uint32_t)sh.d,
+                              0u, 0u, 0u, 0u, 0u, 0u};
+#pragma unroll
+      for (int k = 0; k < 16; ++k) w[k] = h[k];
+    } else {
+      load_block64(r + (g - 1) * 64, w);
+    }
+  };
+  for (int g = 0; g < groups; ++g) {
+    const int64_t c = (int64_t)g * 64 + lane;
+    const int cnt = (int)(chunks - (int64_t)g * 64 < 64 ? chunks - (int64_t)g * 64 : 64);
+    if (c < chunks) {
+      const int64_t g0 = c * kB3ChunkBlocks;
+      const int64_t nb = blocks - g0 < kB3ChunkBlocks ? blocks - g0 : kB3ChunkBlocks;
+      B3Cv cv;
+      b3_chunk(cv, nb, (uint64_t)c, chunks == 1,
+               [&](int64_t b, uint32_t (&w)[16]) { load(g0 + b, w); });
+#pragma unroll
+      for (int k = 0; k < 8; ++k) chunk_cv[lane * 8 + k] = cv.h[k];
+    }
+    __syncthreads();
+    fold_cvs(chunk_cv, cnt, groups == 1, lane);
+    if (lane < 8) group_cv[g * 8 + lane] = chunk_cv[lane];
+    __syncthreads();
+  }
+  fold_cvs(group_cv, groups, true, lane);
+  if (lane < 8) reinterpret_cast<uint32_t*>(digest)[lane] = group_cv[lane];
+}
+
 // The top of every tensor's tree in one launch, one 64-lane workgroup per
 // (tensor t, fragment i): its m <= 64 x 8 nodes of level v0 are folded in runs
 // of r consecutive ones per lane (r the smallest power of two with m <= 64 r:
@@ -258,13 +321,20 @@ __device__ __forceinline__ void fold_cvs(uint32_t* lds, int cnt, bool root, int 
 // base_top[i] + t of the top level.
 constexpr int kTailLevels = kSubLevels + 6;   // 2^3 nodes per lane x 64 lanes
 
+//
+// The workgroup that writes the last of fragment i's 2L roots then computes its
+// Id (fragment_id): each workgroup makes its root visible device-wide and
+// counts itself in arrived[i] (zeroed by the node-table kernel of the same
+// call); the one that sees 2L - 1 arrivals before its own reads every root
+// (after an acquire fence) and resets the counter for a later pass.
 __global__ __launch_bounds__(kSubLanes) void hash_tail_kernel(
     const int64_t* __restrict__ table, int64_t stride, int64_t token_bytes, int32_t v0,
     const int64_t* __restrict__ base_lo, const int64_t* __restrict__ base_top,
     const uint8_t* __restrict__ select, uint32_t want, const uint8_t* __restrict__ in,
-    uint8_t* __restrict__ out) {
+    uint8_t* out, IdShape sh, int32_t* __restrict__ arrived, uint8_t* __restrict__ digests) {
   __shared__ uint32_t lds[(1 << (kSubLevels - 1)) * 8][kSubLanes];
   __shared__ uint32_t vals[kSubLanes * 8];
+  __shared__ int32_t seen;
   const int t = blockIdx.x;
   const int i = blockIdx.y;
   const int lane = threadIdx.x;
@@ -293,64 +363,27 @@ __global__ __launch_bounds__(kSubLanes) void hash_tail_kernel(
   __syncthreads();
   fold_cvs(vals, cnt, true, lane);
   if (lane < 8) reinterpret_cast<uint32_t*>(out + (base_top[i] + t) * 32)[lane] = vals[lane];
+  __threadfence();                       // release this root to the other workgroups
+  __syncthreads();
+  if (lane == 0) seen = atomicAdd(&arrived[i], 1);
+  __syncthreads();
+  if (seen != 2 * sh.L - 1) return;      // uniform over the workgroup
+  __threadfence();                       // acquire the other workgroups' roots
+  fragment_id((uint64_t)table[(int64_t)i * stride], sh, out + base_top[i] * 32,
+              digests + (int64_t)i * 32, lane);
+  if (lane == 0) arrived[i] = 0;
 }
 
-// Id = BLAKE3-256(header || root(K^0) || root(V^0) || ...), one 64-lane
-// workgroup per fragment. The message is L + 1 blocks (the header, then per
-// layer the pair of roots K, V) in C = ceil((L + 1) / 16) chunks. Lane k hashes
-// chunk 64 g + k of each group g of 64 chunks; a full group is an aligned
-// complete subtree of BLAKE3's left-balanced tree and is folded into one value,
-// the last group into the value of its own subtree (carries included); then the
-// group values are folded. ROOT marks the single chunk (C = 1) or the last
-// compression.
-constexpr int kFinalGroups = 32;   // 32 x 64 chunks: L + 1 <= 32768 blocks
-
+// The Id alone (every tensor of the set is a single chunk, so there is no tail
+// launch to compute it), one workgroup per fragment.
 __global__ __launch_bounds__(64) void hash_final_kernel(
-    const int64_t* __restrict__ table, int32_t n, int64_t stride, int32_t L, int32_t H,
-    int32_t d, uint32_t dtype_code, uint32_t esize, const int64_t* __restrict__ base_last,
-    const uint8_t* __restrict__ select, uint32_t want, const uint8_t* __restrict__ roots,
-    uint8_t* __restrict__ digests) {
-  __shared__ uint32_t chunk_cv[64 * 8];
-  __shared__ uint32_t group_cv[kFinalGroups * 8];
+    const int64_t* __restrict__ table, int64_t stride, IdShape sh,
+    const int64_t* __restrict__ base_last, const uint8_t* __restrict__ select, uint32_t want,
+    const uint8_t* __restrict__ roots, uint8_t* __restrict__ digests) {
   const int i = blockIdx.x;
-  const int lane = threadIdx.x;
   if (select && select[i] != want) return;   // uniform over the workgroup
-  const uint64_t T = (uint64_t)table[(int64_t)i * stride];
-  const uint8_t* r = roots + base_last[i] * 32;
-  const int64_t blocks = (int64_t)L + 1;
-  const int64_t chunks = (blocks + kB3ChunkBlocks - 1) / kB3ChunkBlocks;
-  const int groups = (int)((chunks + 63) / 64);
-  auto load = [&](int64_t g, uint32_t (&w)[16]) {
-    if (g == 0) {
-      const uint32_t h[16] = {0x52464D43u, 0x31304741u,  // "CMFRAG01"
-                              dtype_code, esize, (uint32_t)L, 1u, (uint32_t)H,
-                              (uint32_t)T, (uint32_t)(T >> 32), (uint32_t)d,
-                              0u, 0u, 0u, 0u, 0u, 0u};
-#pragma unroll
-      for (int k = 0; k < 16; ++k) w[k] = h[k];
-    } else {
-      load_block64(r + (g - 1) * 64, w);
-    }
-  };
-  for (int g = 0; g < groups; ++g) {
-    const int64_t c = (int64_t)g * 64 + lane;
-    const int cnt = (int)(chunks - (int64_t)g * 64 < 64 ? chunks - (int64_t)g * 64 : 64);
-    if (c < chunks) {
-      const int64_t g0 = c * kB3ChunkBlocks;
-      const int64_t nb = blocks - g0 < kB3ChunkBlocks ? blocks - g0 : kB3ChunkBlocks;
-      B3Cv cv;
-      b3_chunk(cv, nb, (uint64_t)c, chunks == 1,
-               [&](int64_t b, uint32_t (&w)[16]) { load(g0 + b, w); });
-#pragma unroll
-      for (int k = 0; k < 8; ++k) chunk_cv[lane * 8 + k] = cv.h[k];
-    }
-    __syncthreads();
-    fold_cvs(chunk_cv, cnt, groups == 1, lane);
-    if (lane < 8) group_cv[g * 8 + lane] = chunk_cv[lane];
-    __syncthreads();
-  }
-  fold_cvs(group_cv, groups, true, lane);
-  if (lane < 8) reinterpret_cast<uint32_t*>(digests + (int64_t)i * 32)[lane] = group_cv[lane];
+  fragment_id((uint64_t)table[(int64_t)i * stride], sh, roots + base_last[i] * 32,
+              digests + (int64_t)i * 32, threadIdx.x);
 }
 
 }  // namespace
@@ -370,6 +403,8 @@ HashLayout hash_layout(const SetDesc& s) {
   size_t off = 0;
   lay.off_tables = off;
   off = align_up(off + sizeof(int64_t) * (size_t)(lay.levels + 2) * (size_t)(s.n + 1), kWsAlign);
+  lay.off_arrived = off;
+  off = align_up(off + sizeof(int32_t) * (size_t)s.n, kWsAlign);
   lay.off_buf0 = off;
   off = align_up(off + 32 * (size_t)lay.total0, kWsAlign);
   lay.off_buf1 = off;
@@ -385,7 +420,8 @@ hipError_t launch_hash_prep(const SetDesc& s, const HashLayout& lay, uint8_t* ws
   while (threads < s.n) threads <<= 1;
   hipLaunchKernelGGL(hash_prep_kernel, dim3(1), dim3(threads), 0, stream, s.table_dev, s.n,
                      s.stride, token_bytes_of(s), s.L, lay.levels,
-                     reinterpret_cast<int64_t*>(ws + lay.off_tables));
+                     reinterpret_cast<int64_t*>(ws + lay.off_tables),
+                     reinterpret_cast<int32_t*>(ws + lay.off_arrived));
   return hipGetLastError();
 }
 
@@ -414,33 +450,36 @@ hipError_t launch_hash_tree(const SetDesc& s, const HashLayout& lay, const uint8
                        buf[(launch + 1) & 1]);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
+  // the cm_dtype value doubles as the header's dtype code
+  const IdShape sh{s.L, s.H, s.d, (uint32_t)s.dtype, (uint32_t)s.esize};
+  int32_t* arrived = reinterpret_cast<int32_t*>(ws + lay.off_arrived);
   if (v0 < lay.levels) {
+    // the top levels of every tensor, and each fragment's Id in the workgroup
+    // that finishes its last root
     ScopedTiming tm(K_HASH_PARENT, stream);
     hipLaunchKernelGGL(hash_tail_kernel, dim3((uint32_t)(2 * s.L), (uint32_t)s.n), dim3(kSubLanes),
                        0, stream, s.table_dev, s.stride, token_bytes_of(s), v0, base + v0 * nb1,
                        base + lay.levels * nb1, select, want, buf[launch & 1],
-                       buf[(launch + 1) & 1]);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    ++launch;
+                       buf[(launch + 1) & 1], sh, arrived, digests);
+    return hipGetLastError();
   }
-  {
-    ScopedTiming tm(K_HASH_FINAL, stream);
-    const uint32_t code = s.dtype;  // cm_dtype value doubles as the header dtype code
-    hipLaunchKernelGGL(hash_final_kernel, dim3((uint32_t)s.n), dim3(64), 0, stream, s.table_dev, s.n, s.stride, s.L, s.H, s.d, code,
-                       (uint32_t)s.esize, base + lay.levels * nb1, select, want,
-                       buf[launch & 1], digests);
-  }
+  ScopedTiming tm(K_HASH_FINAL, stream);
+  hipLaunchKernelGGL(hash_final_kernel, dim3((uint32_t)s.n), dim3(64), 0, stream, s.table_dev,
+                     s.stride, sh, base + lay.levels * nb1, select, want, buf[launch & 1],
+                     digests);
   return hipGetLastError();
 }
 
-hipError_t launch_mask_hash_prep(const SetDesc& s, const HashLayout& lay, const double* keys,
-                                 uint8_t* mask, uint8_t* ws, hipStream_t stream) {
+hipError_t launch_mask_hash_prep(const SetDesc& s, const HashLayout& lay, const KnormPartials& kp,
+                                 double* keys, uint8_t* mask, uint8_t* ws, hipStream_t stream) {
   ScopedTiming tm(K_KEY_MASK, stream);
-  int threads = 64;
+  // the fold spreads over the workgroup; the scans want at least n threads
+  int threads = kp.count > 1 ? 1024 : 64;
   while (threads < s.n) threads <<= 1;
   hipLaunchKernelGGL(mask_hash_prep_kernel, dim3(1), dim3(threads), 0, stream, s.table_dev, s.n,
-                     s.stride, token_bytes_of(s), s.L, lay.levels, keys, mask,
-                     reinterpret_cast<int64_t*>(ws + lay.off_tables));
+                     s.stride, token_bytes_of(s), s.L, lay.levels, kp.parts, kp.count, keys, mask,
+                     reinterpret_cast<int64_t*>(ws + lay.off_tables),
+                     reinterpret_cast<int32_t*>(ws + lay.off_arrived));
   return hipGetLastError();
 }
 

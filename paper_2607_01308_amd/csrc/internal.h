@@ -58,6 +58,14 @@ __host__ __device__ __forceinline__ int64_t nodes_at(int64_t m0, int v) {
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
+// Threads of a one-workgroup table kernel: at least n (one per delivery), and
+// about one per 16 table entries of `work`, a power of two in [64, 1024].
+inline int table_threads(int32_t n, int64_t work) {
+  int t = 64;
+  while (t < 1024 && (t < n || (int64_t)t * 16 < work)) t <<= 1;
+  return t;
+}
+
 // Compute units of the current device (cached per device).
 int device_cu_count();
 
@@ -70,6 +78,7 @@ struct HashLayout {
   int64_t total0;         // nodes at level 0 over all tensors
   int64_t total1;         // nodes at level 1 over all tensors (0 if levels == 0)
   size_t off_tables;      // int64 [levels+2][n+1]: per-level node bases, then task bases
+  size_t off_arrived;     // int32 [n]: roots written per fragment (the tail kernel's Id step)
   size_t off_buf0;        // level-0 (and even levels) node digests
   size_t off_buf1;        // odd levels
   size_t bytes;           // total workspace bytes
@@ -86,6 +95,13 @@ struct KnormLayout {
 };
 KnormLayout knorm_layout(const SetDesc& s, int64_t tail_len);
 size_t knorm_max_bytes(const SetDesc& s);  // over every legal tail_len
+// Partial sums of the score tree that a one-workgroup kernel finishes
+// (knorm_fold.h): at most this many over the whole set.
+constexpr int64_t kKnormFoldMax = 4096;
+struct KnormPartials {
+  const double* parts;    // count per fragment, fragment-major (keys itself if count == 1)
+  int64_t count;
+};
 
 struct RenderLayout {
   size_t off_tiles;       // int64 [n+1] work-unit bases per slot (fused hash+render tasks)
@@ -108,9 +124,10 @@ int64_t render_units(const SetDesc& s, int64_t T_out);
 hipError_t launch_hash(const SetDesc& s, const HashLayout& lay, const uint8_t* select,
                        uint32_t want, uint8_t* digests, uint8_t* ws, hipStream_t stream,
                        bool tables_ready = false);
-// launch_equal_key_mask and launch_hash_prep in one launch.
-hipError_t launch_mask_hash_prep(const SetDesc& s, const HashLayout& lay, const double* keys,
-                                 uint8_t* mask, uint8_t* ws, hipStream_t stream);
+// launch_equal_key_mask and launch_hash_prep in one launch, after folding the
+// score partials into keys (kp.count > 1).
+hipError_t launch_mask_hash_prep(const SetDesc& s, const HashLayout& lay, const KnormPartials& kp,
+                                 double* keys, uint8_t* mask, uint8_t* ws, hipStream_t stream);
 // The stages of launch_hash: node-base tables, then (after the leaves) the
 // parent levels and the final Id.
 hipError_t launch_hash_prep(const SetDesc& s, const HashLayout& lay, uint8_t* ws,
@@ -121,6 +138,12 @@ hipError_t launch_equal_key_mask(const SetDesc& s, const double* keys, uint8_t* 
                                  hipStream_t stream);
 hipError_t launch_knorm(const SetDesc& s, const KnormLayout& lay, int32_t layer, int64_t tail_len,
                         double* keys, uint8_t* ws, hipStream_t stream);
+// The score kernels up to the last fold_max (or fewer) partial sums of the set,
+// which a later one-workgroup kernel folds (knorm_fold); with count == 1 the
+// keys are already written.
+hipError_t launch_knorm_partial(const SetDesc& s, const KnormLayout& lay, int32_t layer,
+                                int64_t tail_len, double* keys, uint8_t* ws, hipStream_t stream,
+                                int64_t fold_max, KnormPartials* out);
 // dedupe = false: every delivery gets a slot (naive multiset order).
 hipError_t launch_order(const SetDesc& s, const double* keys, const uint8_t* digests,
                         bool dedupe, int64_t* plan, hipStream_t stream);
@@ -130,6 +153,15 @@ hipError_t launch_order_render_prep(const SetDesc& s, const double* keys, const 
                                     int64_t* plan, const RenderLayout& rlay, double base,
                                     int32_t style, int32_t stripe_blocks, const uint8_t* select,
                                     uint8_t* rws, hipStream_t stream);
+// Render of a set of distinct fragments, steps 2-5 after the score partials:
+// one workgroup folds the scores (kp.count > 1), orders, and builds the unit
+// render's tables for T_out rows; a plan whose T_out differs (the set held
+// byte-identical members) gets CM_ESHAPE in its status, and neither it nor a
+// plan with a non-finite score is rendered. Then the unit render.
+hipError_t launch_render_set(const SetDesc& s, const RenderLayout& lay, const KnormPartials& kp,
+                             double* keys, const uint8_t* digests, int64_t* plan, int64_t T_out,
+                             double base, int32_t style, void* out, uint8_t* rws,
+                             hipStream_t stream);
 // Per-slot angle tables; with stripe_blocks > 0 also the per-slot task bases of
 // 2L * stripes of that many 64-byte blocks (and hsel when select is given).
 hipError_t launch_render_prep(const SetDesc& s, const RenderLayout& lay, const int64_t* plan_dev,
@@ -158,6 +190,10 @@ struct RenderRange {
 hipError_t launch_render(const SetDesc& s, const RenderLayout& lay, const int64_t* plan_dev,
                          const RenderRange& rr, double base, int32_t style, bool check_on_device,
                          void* out, uint8_t* ws, hipStream_t stream);
+// The unit render alone, its tables (angles, unit slots, source bases) already in ws.
+hipError_t launch_render_units(const SetDesc& s, const RenderLayout& lay,
+                               const int64_t* plan_dev, const RenderRange& rr, int32_t style,
+                               void* out, uint8_t* ws, hipStream_t stream);
 
 // Validated paged set (see cm_pagedset): s describes the fragments with a table
 // of 2 int64 per fragment {T, first page index}.

@@ -10,8 +10,9 @@
 // of the row tree in registers and an xor-butterfly over those lanes forms the
 // upper levels (fp addition is commutative, so both partners hold the same
 // node). An aligned block of up to 256 row norms is one subtree, reduced in LDS;
-// further levels run as small tree launches. Reads only the H*T*d*e tail bytes
-// of one layer per fragment.
+// further levels run as small tree launches, the last few of them, where a
+// one-workgroup kernel follows, inside that kernel (knorm_fold.h). Reads only
+// the H*T*d*e tail bytes of one layer per fragment.
 #include "internal.h"
 
 namespace cm {
@@ -55,6 +56,8 @@ __device__ __forceinline__ double lds_tree(double* sh, int count) {
   return sh[0];
 }
 
+constexpr int kInFlight = 16;   // row loads in flight per thread
+
 // grid (count0, n), 256 threads: block b of fragment i sums rows
 // [b*rpb, (b+1)*rpb) of the padded (h, r) row space.
 template <int ESIZE>
@@ -74,19 +77,38 @@ __global__ __launch_bounds__(256) void knorm_rows_kernel(const int64_t* __restri
   const int rpp = 256 / lpr;       // rows per pass
   const int tid = threadIdx.x;
   const int q = tid & (lpr - 1);
-  for (int p0 = 0; p0 < rpb; p0 += rpp) {
-    const int fl = p0 + tid / lpr;
-    const int64_t f = blk * rpb + fl;
-    const bool valid = fl < rpb && f < rows;
-    double acc = 0.0;
-    if (valid) {
-      const int64_t h = f / tail;
-      const int64_t r = f - h * tail;
-      const uint8_t* src = K + (h * T + (T - tail + r)) * row_bytes + q * 16;
-      acc = row_chunk_sumsq<ESIZE>(*global_ptr<u32x4>(src));
+  // kInFlight passes at a time: their loads are all issued before the first is
+  // used, so the block waits for memory once per group instead of once per pass
+  // row f = h * tail + r of the (h, r) space: one division for the thread's
+  // first row, then steps of rpp rows
+  const int64_t f0 = blk * rpb + tid / lpr;
+  int64_t h = f0 / tail;
+  int64_t r = f0 - h * tail;
+  for (int p0 = 0; p0 < rpb; p0 += rpp * kInFlight) {
+    u32x4 v[kInFlight];
+    bool valid[kInFlight];
+#pragma unroll
+    for (int g = 0; g < kInFlight; ++g) {
+      const int fl = p0 + g * rpp + tid / lpr;
+      const int64_t f = blk * rpb + fl;
+      valid[g] = fl < rpb && f < rows;
+      v[g] = u32x4{0u, 0u, 0u, 0u};
+      if (valid[g])
+        v[g] = *global_ptr<u32x4>(K + (h * T + (T - tail + r)) * row_bytes + q * 16);
+      r += rpp;
+      if (r >= tail) {               // a division only for tails shorter than a pass
+        const int64_t k = r < 2 * tail ? 1 : r / tail;
+        h += k;
+        r -= k * tail;
+      }
     }
-    for (int o = 1; o < lpr; o <<= 1) acc = acc + __shfl_xor(acc, o, 64);
-    if (fl < rpb && q == 0) sh[fl] = valid ? sqrt(acc) : 0.0;
+#pragma unroll
+    for (int g = 0; g < kInFlight; ++g) {
+      const int fl = p0 + g * rpp + tid / lpr;
+      double acc = valid[g] ? row_chunk_sumsq<ESIZE>(v[g]) : 0.0;
+      for (int o = 1; o < lpr; o <<= 1) acc = acc + __shfl_xor(acc, o, 64);
+      if (fl < rpb && q == 0) sh[fl] = valid[g] ? sqrt(acc) : 0.0;
+    }
   }
   __syncthreads();
   const double s = lds_tree(sh, rpb);
@@ -136,39 +158,50 @@ size_t knorm_max_bytes(const SetDesc& s) {
   return knorm_layout(s, tmin).bytes;  // grows with tail_len, which is at most min T
 }
 
-hipError_t launch_knorm(const SetDesc& s, const KnormLayout& lay, int32_t layer, int64_t tail_len,
-                        double* keys, uint8_t* ws, hipStream_t stream) {
+hipError_t launch_knorm_partial(const SetDesc& s, const KnormLayout& lay, int32_t layer,
+                                int64_t tail_len, double* keys, uint8_t* ws, hipStream_t stream,
+                                int64_t fold_max, KnormPartials* out) {
   double* bufs[2] = {reinterpret_cast<double*>(ws + lay.off_a),
                      reinterpret_cast<double*>(ws + lay.off_b)};
   {
     ScopedTiming tm(K_KNORM_ROWS, stream);
-    double* out = lay.count0 == 1 ? keys : bufs[0];
+    double* o = lay.count0 == 1 ? keys : bufs[0];
     const dim3 grid((uint32_t)lay.count0, (uint32_t)s.n);
     if (s.esize == 2)
       hipLaunchKernelGGL(knorm_rows_kernel<2>, grid, dim3(256), 0, stream, s.table_dev,
                          s.stride, layer, tail_len, s.d, lay.rows, lay.rows_per_block,
-                         lay.count0, out);
+                         lay.count0, o);
     else
       hipLaunchKernelGGL(knorm_rows_kernel<4>, grid, dim3(256), 0, stream, s.table_dev,
                          s.stride, layer, tail_len, s.d, lay.rows, lay.rows_per_block,
-                         lay.count0, out);
+                         lay.count0, o);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   int64_t c = lay.count0;
   int cur = 0;
-  while (c > 1) {
-    const int64_t g = c < 256 ? c : 256;
+  while (c > 1 && (int64_t)s.n * c > fold_max) {
+    // one launch takes up to 8 levels; the last one folds no further than needed
+    int64_t g = c < 256 ? c : 256;
+    while (g > 2 && (int64_t)s.n * (c / (g >> 1)) <= fold_max) g >>= 1;
     const int64_t cout = c / g;
-    double* out = cout == 1 ? keys : bufs[cur ^ 1];
+    double* o = cout == 1 ? keys : bufs[cur ^ 1];
     ScopedTiming tm(K_KNORM_TREE, stream);
     hipLaunchKernelGGL(knorm_tree_kernel, dim3((uint32_t)cout, (uint32_t)s.n), dim3((uint32_t)g),
-                       0, stream, bufs[cur], c, out, cout);
+                       0, stream, bufs[cur], c, o, cout);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     cur ^= 1;
     c = cout;
   }
+  out->parts = c == 1 ? keys : bufs[cur];
+  out->count = c;
   return hipSuccess;
+}
+
+hipError_t launch_knorm(const SetDesc& s, const KnormLayout& lay, int32_t layer, int64_t tail_len,
+                        double* keys, uint8_t* ws, hipStream_t stream) {
+  KnormPartials kp;
+  return launch_knorm_partial(s, lay, layer, tail_len, keys, ws, stream, 1, &kp);
 }
 
 }  // namespace cm

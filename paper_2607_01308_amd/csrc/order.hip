@@ -19,6 +19,7 @@
 // That lets the digests of every other delivery be computed concurrently with
 // the render (equal_key_mask marks the ones needed first).
 #include "key_mask.h"
+#include "knorm_fold.h"
 #include "render_tables.h"
 
 namespace cm {
@@ -183,6 +184,33 @@ __global__ __launch_bounds__(1024) void order_render_prep_kernel(
                 hsel, unit_base, angles, table, stride, 0, nullptr, nullptr);
 }
 
+// Steps 2-5 of a set render before the render itself: the last levels of the
+// scores (count > 1), the plan, then the unit render's tables for T_out rows.
+// The members of a set are distinct, so the plan's T_out is the sum of all
+// lengths; a plan whose T_out differs (byte-identical members were absorbed)
+// gets CM_ESHAPE, and it, like a plan with a non-finite score, is not rendered.
+__global__ __launch_bounds__(1024) void order_set_prep_kernel(
+    const int64_t* __restrict__ table, int64_t stride, int32_t n,
+    const double* __restrict__ parts, int64_t count, double* __restrict__ keys,
+    const uint8_t* __restrict__ digests, int64_t* __restrict__ plan, int64_t T_out, int32_t d,
+    int32_t ep, int32_t style, double base, double* __restrict__ angles,
+    int64_t* __restrict__ unit_base, int32_t H, int32_t n_lkh, int32_t rb_shift, int64_t units,
+    int32_t* __restrict__ unit_slot, int64_t* __restrict__ src_base) {
+  if (count > 1) knorm_fold(parts, n, count, keys);
+  order_body(table, stride, n, keys, digests, 1, plan);
+  __syncthreads();
+  bool ok = plan[CM_PLAN_STATUS] == CM_OK;
+  if (ok && plan[CM_PLAN_TOUT] != T_out) {
+    ok = false;
+    if (threadIdx.x == 0) plan[CM_PLAN_STATUS] = CM_ESHAPE;
+  }
+  if (ok)
+    render_tables(plan, n, d, ep, style, base, 0, 0, 0, nullptr, nullptr, unit_base, angles,
+                  table, stride, T_out, nullptr, nullptr);
+  unit_tables(table, stride, plan, n, H, n_lkh, rb_shift, 0, T_out, units, ok, unit_slot,
+              src_base);
+}
+
 __global__ __launch_bounds__(1024) void equal_key_mask_kernel(const int64_t* __restrict__ table,
                                                               int64_t stride, int32_t n,
                                                               const double* __restrict__ keys,
@@ -226,6 +254,27 @@ hipError_t launch_order_render_prep(const SetDesc& s, const double* keys, const 
                      reinterpret_cast<int64_t*>(rws + rlay.off_tiles),
                      reinterpret_cast<double*>(rws + rlay.off_angles));
   return hipGetLastError();
+}
+
+hipError_t launch_render_set(const SetDesc& s, const RenderLayout& lay, const KnormPartials& kp,
+                             double* keys, const uint8_t* digests, int64_t* plan, int64_t T_out,
+                             double base, int32_t style, void* out, uint8_t* rws,
+                             hipStream_t stream) {
+  const int64_t units = render_units(s, T_out);
+  const int threads = table_threads(s.n, units + (int64_t)s.n * 2 * s.L * s.H);
+  {
+    ScopedTiming tm(K_ORDER, stream);
+    hipLaunchKernelGGL(order_set_prep_kernel, dim3(1), dim3(threads), 0, stream, s.table_dev,
+                       s.stride, s.n, kp.parts, kp.count, keys, digests, plan, T_out, s.d,
+                       16 / s.esize, style, base, reinterpret_cast<double*>(rws + lay.off_angles),
+                       reinterpret_cast<int64_t*>(rws + lay.off_tiles), s.H, 2 * s.L * s.H,
+                       (int32_t)__builtin_ctzll((unsigned long long)s.row_bytes), units,
+                       reinterpret_cast<int32_t*>(rws + lay.off_unit_slot),
+                       reinterpret_cast<int64_t*>(rws + lay.off_src_base));
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return launch_render_units(s, lay, plan, RenderRange{0, T_out, T_out}, style, out, rws, stream);
 }
 
 }  // namespace cm

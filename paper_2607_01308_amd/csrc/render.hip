@@ -11,8 +11,8 @@
 // pieces of a lane in one column). The lookups are precomputed by a prep pass so
 // that a wave's data load waits on two scalar loads only: the slot of its unit
 // (every row block has the same row -> slot map) and the source base of that
-// slot in its row block. A unit crossing a slot boundary resolves the slot per
-// lane. K at a non-zero offset is rotated with the partner piece fetched from
+// slot in its row block (render_tables.h). A unit crossing a slot boundary
+// resolves the slot per lane. K at a non-zero offset is rotated with the partner piece fetched from
 // the lane P pieces away.
 #include "render_geometry.h"
 #include "render_tables.h"
@@ -87,33 +87,18 @@ __global__ __launch_bounds__(64) void render_unit_kernel(
   }
 }
 
-// The lookups of the unit render: unit_slot[x] = slot of the first row of unit
-// x (| kUnitCrosses if a later row of the unit lies in another slot), and
-// src_base[s][lkh] = address that row r of slot s in row block lkh is read from
-// when offset by r * row_bytes: fragment tensor base + (h * T_s - off_s) rows.
-__global__ __launch_bounds__(256) void render_unit_prep_kernel(
-    const int64_t* __restrict__ table, int64_t stride, const int64_t* __restrict__ plan,
-    int32_t n, int32_t H, int32_t n_lkh, int32_t rb_shift, int64_t row0, int64_t units,
-    const int32_t* __restrict__ plan_ok, int32_t* unit_slot, int64_t* src_base) {
-  const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t nthreads = (int64_t)gridDim.x * blockDim.x;
-  if (plan_ok && *plan_ok == 0) {                      // rejected plan: every unit is skipped
-    for (int64_t x = tid; x < units; x += nthreads) unit_slot[x] = -1;
-    return;
-  }
-  const int n_u = (int)plan[CM_PLAN_NUNIQUE];
-  const int64_t* offs = plan + CM_PLAN_HEADER + n;
-  const int64_t T_out = plan[CM_PLAN_TOUT];
-  for (int64_t x = tid; x < units; x += nthreads)
-    unit_slot[x] = unit_slot_code(offs, n_u, T_out, rb_shift, row0, x);
-  for (int64_t e = tid; e < (int64_t)n_u * n_lkh; e += nthreads) {
-    const int s = (int)(e / n_lkh);
-    const int lkh = (int)(e - (int64_t)s * n_lkh);
-    const int64_t i = plan[CM_PLAN_HEADER + s];
-    const int64_t T = plan[CM_PLAN_HEADER + 2 * (int64_t)n + s];
-    const int64_t base = table[i * stride + 1 + lkh / H];
-    src_base[e] = base + unit_src_offset(lkh % H, T, offs[s], rb_shift, 0);
-  }
+// The plan check (check_on_device), the angle tables and the unit render's
+// lookups in one workgroup.
+__global__ __launch_bounds__(1024) void render_prep_units_kernel(
+    const int64_t* __restrict__ plan, int32_t n, int32_t d, int32_t ep, int32_t style,
+    double base, int64_t* __restrict__ unit_base, double* __restrict__ angles,
+    const int64_t* __restrict__ table, int64_t stride, int64_t T_out, int32_t* plan_ok,
+    int64_t* plan_status, int32_t H, int32_t n_lkh, int32_t rb_shift, int64_t row0,
+    int64_t units, int32_t* __restrict__ unit_slot, int64_t* __restrict__ src_base) {
+  const bool ok = render_tables(plan, n, d, ep, style, base, 0, 0, 0, nullptr, nullptr, unit_base,
+                                angles, table, stride, T_out, plan_ok, plan_status);
+  unit_tables(table, stride, plan, n, H, n_lkh, rb_shift, row0, ok ? plan[CM_PLAN_TOUT] : 0, units,
+              ok, unit_slot, src_base);
 }
 
 __global__ __launch_bounds__(1024) void render_prep_kernel(
@@ -165,36 +150,14 @@ hipError_t launch_render_prep(const SetDesc& s, const RenderLayout& lay, const i
   return hipGetLastError();
 }
 
-hipError_t launch_render(const SetDesc& s, const RenderLayout& lay, const int64_t* plan_dev,
-                         const RenderRange& rr, double base, int32_t style, bool check_on_device,
-                         void* out, uint8_t* ws, hipStream_t stream) {
-  int32_t* plan_ok = check_on_device ? reinterpret_cast<int32_t*>(ws + lay.off_flag) : nullptr;
-  {
-    ScopedTiming tm(K_RENDER_PREP, stream);
-    int threads = 64;
-    while (threads < s.n) threads <<= 1;
-    hipLaunchKernelGGL(render_prep_kernel, dim3(1), dim3(threads), 0, stream, plan_dev, s.n, s.d,
-                       16 / s.esize, style, base, 0, (int64_t)s.L, token_bytes_of(s), nullptr,
-                       nullptr, reinterpret_cast<int64_t*>(ws + lay.off_tiles),
-                       reinterpret_cast<double*>(ws + lay.off_angles), s.table_dev, s.stride,
-                       rr.T_out, plan_ok, const_cast<int64_t*>(plan_dev));
-  }
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+hipError_t launch_render_units(const SetDesc& s, const RenderLayout& lay,
+                               const int64_t* plan_dev, const RenderRange& rr, int32_t style,
+                               void* out, uint8_t* ws, hipStream_t stream) {
   const int64_t units = render_units(s, rr.T_out - rr.row0);
+  if (units <= 0) return hipSuccess;
   const int32_t n_lkh = 2 * s.L * s.H;
-  const int rb_shift = __builtin_ctzll((unsigned long long)s.row_bytes);
-  int32_t* unit_slot = reinterpret_cast<int32_t*>(ws + lay.off_unit_slot);
-  int64_t* src_base = reinterpret_cast<int64_t*>(ws + lay.off_src_base);
-  {
-    ScopedTiming tm(K_RENDER_PREP, stream);
-    const int64_t work = units > (int64_t)s.n * n_lkh ? units : (int64_t)s.n * n_lkh;
-    const int64_t blocks = (work + 255) / 256;
-    hipLaunchKernelGGL(render_unit_prep_kernel, dim3((uint32_t)(blocks < 1024 ? blocks : 1024)),
-                       dim3(256), 0, stream, s.table_dev, s.stride, plan_dev, s.n, s.H, n_lkh,
-                       rb_shift, rr.row0, units, plan_ok, unit_slot, src_base);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-  }
+  const int32_t* unit_slot = reinterpret_cast<const int32_t*>(ws + lay.off_unit_slot);
+  const int64_t* src_base = reinterpret_cast<const int64_t*>(ws + lay.off_src_base);
   const double* angles = reinterpret_cast<const double*>(ws + lay.off_angles);
   const dim3 grid((uint32_t)units, (uint32_t)n_lkh);
   uint8_t* o = reinterpret_cast<uint8_t*>(out);
@@ -210,6 +173,28 @@ hipError_t launch_render(const SetDesc& s, const RenderLayout& lay, const int64_
   };
   dispatch_style(style, s.row_bytes, go);
   return hipGetLastError();
+}
+
+hipError_t launch_render(const SetDesc& s, const RenderLayout& lay, const int64_t* plan_dev,
+                         const RenderRange& rr, double base, int32_t style, bool check_on_device,
+                         void* out, uint8_t* ws, hipStream_t stream) {
+  int32_t* plan_ok = check_on_device ? reinterpret_cast<int32_t*>(ws + lay.off_flag) : nullptr;
+  const int64_t units = render_units(s, rr.T_out - rr.row0);
+  {
+    ScopedTiming tm(K_RENDER_PREP, stream);
+    const int threads = table_threads(s.n, units + (int64_t)s.n * 2 * s.L * s.H);
+    hipLaunchKernelGGL(render_prep_units_kernel, dim3(1), dim3(threads), 0, stream, plan_dev, s.n,
+                       s.d, 16 / s.esize, style, base,
+                       reinterpret_cast<int64_t*>(ws + lay.off_tiles),
+                       reinterpret_cast<double*>(ws + lay.off_angles), s.table_dev, s.stride,
+                       rr.T_out, plan_ok, const_cast<int64_t*>(plan_dev), s.H, 2 * s.L * s.H,
+                       (int32_t)__builtin_ctzll((unsigned long long)s.row_bytes), rr.row0,
+                       units, reinterpret_cast<int32_t*>(ws + lay.off_unit_slot),
+                       reinterpret_cast<int64_t*>(ws + lay.off_src_base));
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return launch_render_units(s, lay, plan_dev, rr, style, out, ws, stream);
 }
 
 }  // namespace cm

@@ -1,8 +1,9 @@
 // Per-slot tables of the render, built by one workgroup once the plan exists
-// (shared by the render's own prep kernel and the order kernel of the one-call
-// path, which builds them right after the plan, in the same workgroup).
+// (shared by the render's own prep kernel and the order kernels of the one-call
+// paths, which build them right after the plan, in the same workgroup).
 #pragma once
 
+#include "render_geometry.h"
 #include "rotate.h"
 
 namespace cm {
@@ -15,8 +16,9 @@ namespace cm {
 // 64-byte blocks per slot, exclusive scan; the total at index n as well, none if
 // the plan's status is an error) and, with a select mask, hsel[i] = 0
 // for the slot deliveries whose Id the fused kernel computes (select[i] == 0),
-// 1 for every other delivery.
-__device__ __forceinline__ void render_tables(
+// 1 for every other delivery. Returns false (the same in every thread) for a
+// plan that fails the device check; nothing else is written then.
+__device__ __forceinline__ bool render_tables(
     const int64_t* __restrict__ plan, int32_t n, int32_t d, int32_t ep, int32_t style,
     double base, int32_t stripe_blocks, int64_t tensor_pairs, int64_t token_bytes,
     const uint8_t* __restrict__ select, uint8_t* __restrict__ hsel,
@@ -54,7 +56,7 @@ __device__ __forceinline__ void render_tables(
       // a plan that already reports an error (a non-finite score) keeps it
       if (!all && plan[CM_PLAN_STATUS] == CM_OK) *plan_status = CM_ESHAPE;
     }
-    if (!all) return;
+    if (!all) return false;
     __syncthreads();
   }
   if (stripe_blocks > 0) {
@@ -95,6 +97,46 @@ __device__ __forceinline__ void render_tables(
                                           : angle_slot_il(j / (ep >> 1), j % (ep >> 1), ppr);
     angles[2 * ((int64_t)s * halfd + k)] = cos(phi);
     angles[2 * ((int64_t)s * halfd + k) + 1] = sin(phi);
+  }
+  return true;
+}
+
+// The lookups of the unit render (render.hip) for rows [row0, T_out) of a plan,
+// by one workgroup: unit_slot[x] = slot of the first row of unit x (|
+// kUnitCrosses if a later row of the unit lies in another slot), src_base[s][lkh]
+// = the address that row r of slot s in row block lkh = (l * 2 + kv) * H + h is
+// read from when offset by r * row_bytes. ok == false (a plan that is not
+// rendered): every unit gets -1, which the render skips. The slots' delivery,
+// length and offset are staged in LDS first.
+__device__ __forceinline__ void unit_tables(const int64_t* __restrict__ table, int64_t stride,
+                                            const int64_t* __restrict__ plan, int32_t n,
+                                            int32_t H, int32_t n_lkh, int32_t rb_shift,
+                                            int64_t row0, int64_t T_out, int64_t units, bool ok,
+                                            int32_t* __restrict__ unit_slot,
+                                            int64_t* __restrict__ src_base) {
+  __shared__ int64_t u_off[1024];
+  __shared__ int64_t u_len[1024];
+  __shared__ int64_t u_src[1024];
+  const int tid = threadIdx.x;
+  const int nt = blockDim.x;
+  if (!ok) {
+    for (int64_t x = tid; x < units; x += nt) unit_slot[x] = -1;
+    return;
+  }
+  const int n_u = (int)plan[CM_PLAN_NUNIQUE];
+  for (int s = tid; s < n_u; s += nt) {
+    u_src[s] = plan[CM_PLAN_HEADER + s];
+    u_off[s] = plan[CM_PLAN_HEADER + n + s];
+    u_len[s] = plan[CM_PLAN_HEADER + 2 * (int64_t)n + s];
+  }
+  __syncthreads();
+  for (int64_t x = tid; x < units; x += nt)
+    unit_slot[x] = unit_slot_code(u_off, n_u, T_out, rb_shift, row0, x);
+  for (int64_t e = tid; e < (int64_t)n_u * n_lkh; e += nt) {
+    const int s = (int)(e / n_lkh);
+    const int lkh = (int)(e - (int64_t)s * n_lkh);
+    const int64_t base = table[u_src[s] * stride + 1 + lkh / H];
+    src_base[e] = base + unit_src_offset(lkh % H, u_len[s], u_off[s], rb_shift, 0);
   }
 }
 

@@ -30,7 +30,7 @@ from .binding import (FragmentBatch, bag_plan, canonical_order, equal_key_mask, 
                       fragment_hash_select, fragment_knorm, multiset_order, plan_elems,
                       paged_render, paged_tables, paged_workspace_size, render_merge,
                       render_deliveries_async, render_merge_devplan, render_merge_hash,
-                      render_merge_range, workspace_size)
+                      render_merge_range, render_set, workspace_size)
 from .binding import PagedSet
 
 _WS: Dict[tuple, torch.Tensor] = {}
@@ -219,8 +219,7 @@ def _render_plan(batch: FragmentBatch, plan_dev: torch.Tensor, plan_host: np.nda
     else:
         render_merge_hash(batch, plan_dev, plan_host, rope_base, style, hash_select, digests,
                           merged, T_out, ws, stream)
-    cache = tuple((merged[l, 0], merged[l, 1]) for l in range(batch.L))
-    return merged, cache
+    return merged
 
 
 PIPELINES = ("fused", "overlap", "serial")
@@ -284,11 +283,11 @@ def render_deliveries(deliveries: Union[FragmentBatch, Sequence], routing_layer:
         canonical_order(batch, keys, digests, plan_dev, main)
         plan_host = _plan_to_host(plan_dev, main)
         try:
-            merged, cache = _render_plan(batch, plan_dev, plan_host, rope_base, style, ws, main)
+            merged = _render_plan(batch, plan_dev, plan_host, rope_base, style, ws, main)
         finally:
             if side_done is not None:
                 main.wait_event(side_done)
-    return RenderResult(cache=cache, merged=merged, digests_dev=digests, keys_dev=keys,
+    return RenderResult(merged=merged, digests_dev=digests, keys_dev=keys,
                         plan_host=plan_host, tail_len=tail, plan_dev=plan_dev)
 
 
@@ -313,9 +312,9 @@ def render_multiset(deliveries: Union[FragmentBatch, Sequence], routing_layer: i
         fragment_hash_select(batch, mask, 1, digests, ws, main)   # the digests the order reads
         multiset_order(batch, keys, digests, plan_dev, main)
         plan_host = _plan_to_host(plan_dev, main)
-        merged, cache = _render_plan(batch, plan_dev, plan_host, rope_base, style, ws, main,
+        merged = _render_plan(batch, plan_dev, plan_host, rope_base, style, ws, main,
                                      hash_select=mask, digests=digests)
-    return RenderResult(cache=cache, merged=merged, digests_dev=digests, keys_dev=keys,
+    return RenderResult(merged=merged, digests_dev=digests, keys_dev=keys,
                         plan_host=plan_host, tail_len=tail, plan_dev=plan_dev)
 
 
@@ -331,9 +330,9 @@ def bag_merge(deliveries: Union[FragmentBatch, Sequence], order: Sequence[int],
     with torch.cuda.stream(main):
         ws = _workspace(batch, main)
         plan_dev = torch.from_numpy(plan_host).to(dev, non_blocking=False)
-        merged, cache = _render_plan(batch, plan_dev, plan_host, rope_base, style, ws, main)
+        merged = _render_plan(batch, plan_dev, plan_host, rope_base, style, ws, main)
     empty = torch.empty(0, dtype=torch.uint8, device=dev)
-    return RenderResult(cache=cache, merged=merged, digests_dev=empty,
+    return RenderResult(merged=merged, digests_dev=empty,
                         keys_dev=torch.empty(0, dtype=torch.float64, device=dev),
                         plan_host=plan_host, tail_len=0, plan_dev=plan_dev)
 
@@ -406,18 +405,17 @@ class LatentFragmentSet:
             keys = torch.empty(batch.n, dtype=torch.float64, device=dev)
             plan_dev = torch.empty(plan_elems(batch.n), dtype=torch.int64, device=dev)
             tail = min(batch.lengths)
-            fragment_knorm(batch, routing_layer, tail, keys, ws, main)
-            canonical_order(batch, keys, digests, plan_dev, main)
             # the members are distinct, so T_out is the sum of their lengths and the
-            # plan can stay on the device (checked there before the render)
+            # plan stays on the device: scores, order and render in one call
             T_out = int(sum(batch.lengths))
             merged = torch.empty((batch.L, 2, 1, batch.H, T_out, batch.d),
                                  dtype=batch.torch_dtype, device=dev)
-            render_merge_devplan(batch, plan_dev, rope_base, style, merged, T_out, ws, main)
-        cache = tuple((merged[l, 0], merged[l, 1]) for l in range(batch.L))
-        plan_host = None
-        return RenderResult(cache=cache, merged=merged, digests_dev=digests, keys_dev=keys,
-                            plan_host=plan_host, tail_len=tail, plan_dev=plan_dev)
+            render_set(batch, digests, routing_layer, tail, rope_base, style, keys, plan_dev,
+                       merged, T_out, ws, main)
+        # the per-layer views are made on first use of `cache` (tens of microseconds
+        # of host time for a deep model, which would otherwise pace a render loop)
+        return RenderResult(merged=merged, digests_dev=digests, keys_dev=keys, plan_host=None,
+                            tail_len=tail, plan_dev=plan_dev)
 
 
 class MergedCache:

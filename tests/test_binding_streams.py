@@ -101,6 +101,7 @@ CALLS = {
         b, 0, 1, 1e4, "half", T, T, T, T, T, 1, T, s),
     "render_deliveries_noalloc": lambda b, s: binding.render_deliveries_noalloc(
         b, 0, 1, 1e4, "half", T, T, T, T, T, 1, s),
+    "render_set": lambda b, s: binding.render_set(b, T, 0, 1, 1e4, "half", T, T, T, 1, T, s),
 }
 
 

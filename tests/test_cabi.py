@@ -275,6 +275,29 @@ def test_render_deliveries_argument_checks(lib):
     assert call(rope=bad) == C.CM_EINVAL
 
 
+def test_render_set_argument_checks(lib):
+    fs = FakeSet(lengths=(5, 9))
+    _, need = _ws(lib, fs)
+    rope = C.CmRope(base=1e4, style=0, reserved=0)
+    dig, keys, plan = ctypes.c_void_p(0x30000), ctypes.c_void_p(0x10000), ctypes.c_void_p(0x50000)
+    out, ws = ctypes.c_void_p(0x80000), ctypes.c_void_p(0x40000)
+
+    def call(layer=1, tail=5, T_out=14, dig=dig, keys=keys, plan=plan, out=out, ws_bytes=need):
+        return lib.cm_render_set(fs.ref, dig, layer, tail, ctypes.byref(rope), keys, plan, out,
+                                 T_out, ws, ws_bytes, None)
+
+    assert call(ws_bytes=0) == C.CM_EWORKSPACE             # every other check passed
+    assert call(T_out=13) == C.CM_ESHAPE                   # must be the sum of the lengths
+    assert call(T_out=15) == C.CM_ESHAPE
+    assert call(layer=2) == C.CM_EINVAL
+    assert call(tail=6) == C.CM_EINVAL
+    assert call(dig=None) == C.CM_EINVAL
+    assert call(dig=ctypes.c_void_p(0x30008)) == C.CM_EINVAL
+    assert call(keys=None) == C.CM_EINVAL
+    assert call(plan=None) == C.CM_EINVAL
+    assert call(out=ctypes.c_void_p(0x80008)) == C.CM_EINVAL
+
+
 def test_render_deliveries_noalloc_argument_checks(lib):
     """The entry point without a workspace runs the same checks, and a set whose
     workspace exceeds the fixed scratch is refused before the library touches

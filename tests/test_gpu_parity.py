@@ -224,6 +224,56 @@ def test_latent_fragment_set_matches_delivery_render():
     assert set(U.ids()) == set(oracle_ids([frags[i] for i in range(3)], w.dtype))
 
 
+def test_long_tail_scores_fold_in_the_order_kernels():
+    """Scores whose row tree leaves more partial sums than one workgroup folds
+    (3 fragments x 2048 partials): one tree launch, then the fold inside the
+    order kernel (set render) or the key-mask kernel (whole path). Keys equal the
+    oracle's bit for bit; the set render equals the serial pipeline, whose
+    scores take the full tree of launches."""
+    w = synth.custom("long-tail", dtype="bfloat16", d=64, H=8, L=1,
+                     lengths=(40000, 40003, 40001), routing_layer=0)
+    frags, dl = gpu_deliveries(w)
+    tail = min(w.lengths)
+    want = oracle_keys(dl, w.dtype, 0, tail)
+    S = cm.LatentFragmentSet()
+    S.ingest_many(dl)
+    a = S.render(w.routing_layer, w.rope_base)
+    b = cm.render_deliveries(dl, w.routing_layer, w.rope_base, pipeline="serial")
+    c = cm.render_deliveries(dl, w.routing_layer, w.rope_base, pipeline="fused")
+    torch.cuda.synchronize()
+    assert torch.equal(a.merged, b.merged) and torch.equal(c.merged, b.merged)
+    assert list(b.keys_dev.cpu().numpy()) == want
+    assert list(c.keys_dev.cpu().numpy()) == want
+    # the set's keys follow its members' order (by Id), not the deliveries'
+    ids = oracle_ids(dl, w.dtype)
+    by_id = dict(zip(ids, want))
+    assert list(a.keys_dev.cpu().numpy()) == [by_id[bytes(x)] for x in a.digests_dev.cpu().numpy()]
+
+
+def test_render_set_rejects_members_with_one_id():
+    """cm_render_set on a table that lists one fragment twice: the dedupe
+    absorbs the copy, the plan's T_out falls short of the caller's, the plan
+    says CM_ESHAPE and nothing is rendered."""
+    w = synth.custom("set-dup", dtype="bfloat16", d=128, H=2, L=2, lengths=(40, 24),
+                     deliveries=(0, 1, 0), routing_layer=1)
+    _, dl = gpu_deliveries(w)
+    batch = cm.FragmentBatch(dl)
+    ws = torch.empty(max(cm.workspace_size(batch), 256), dtype=torch.uint8, device="cuda")
+    digests = torch.empty((batch.n, 32), dtype=torch.uint8, device="cuda")
+    cm.fragment_hash(batch, digests, ws)
+    keys = torch.empty(batch.n, dtype=torch.float64, device="cuda")
+    plan = torch.full((cm.plan_elems(batch.n),), 7, dtype=torch.int64, device="cuda")
+    T_out = int(sum(batch.lengths))
+    out = torch.zeros((batch.L, 2, 1, batch.H, T_out, batch.d), dtype=batch.torch_dtype,
+                      device="cuda")
+    cm.render_set(batch, digests, w.routing_layer, min(batch.lengths), w.rope_base, "half", keys,
+                  plan, out, T_out, ws)
+    torch.cuda.synchronize()
+    p = plan.cpu().numpy()
+    assert p[0] == -2 and p[2] == 2 and p[3] == 64
+    assert not bool(out.any())
+
+
 def test_timing_api_counts_launches():
     w = synth.custom("timing", lengths=(64, 32))
     _, dl = gpu_deliveries(w)
@@ -233,7 +283,9 @@ def test_timing_api_counts_launches():
         cm.render_deliveries(dl, w.routing_layer, w.rope_base, pipeline="fused")
         cm.render_deliveries(dl, w.routing_layer, w.rope_base, pipeline="serial")
         torch.cuda.synchronize()
-        for k in ("hash_leaf", "hash_parent", "hash_final", "knorm_rows", "order", "key_mask",
+        # (the fragments' Ids come from the tree's top launch: hash_final runs
+        # only for sets whose tensors are single chunks)
+        for k in ("hash_leaf", "hash_parent", "knorm_rows", "order", "key_mask",
                   "render_prep", "render", "render_hash"):
             ms, n = cm.timing_query(k)
             assert n >= 1 and ms > 0.0, k
