@@ -14,7 +14,7 @@
  *   cm_render_merge_devplan the same with the plan left on the device
  *   cm_render_merge_range   the slots from a given rank on (incremental render)
  *   cm_render_set           steps 2-5 for a set with known Ids, in one call
- *   cm_paged_tables / cm_paged_render  the same render over paged storage
+ *   cm_paged_order / cm_paged_tables / cm_paged_render  steps 1-5 over paged storage
  * the paper's baselines over the same render:
  *   cm_multiset_order       the naive re-render order of §5.9 (no dedupe)
  *   cm_bag_plan             BagMerge with a caller-supplied order (§4.2)
@@ -348,6 +348,18 @@ typedef struct {
   const int32_t* blocks_dev;
   int64_t n_blocks;
 } cm_pagedset;
+
+/* Steps 1-3 on fragments that live only in the pool: cm_fragment_knorm's keys
+ * (keys_dev, n doubles), the Id of every fragment (digests_dev, n * 32 bytes,
+ * 16-byte aligned; the same content address as the dense form's: each tensor is
+ * hashed in the byte order of its [1, H, T, d] layout, Alg. 2 Id), then
+ * cm_canonical_order's dedupe, order and offsets (plan_dev, cm_plan_elems(n)
+ * int64), all on the device with nothing waiting for the host. The plan then
+ * drives cm_paged_tables and cm_paged_render. routing_layer, tail_len as
+ * cm_fragment_knorm. Workspace: cm_paged_workspace_size() bytes. */
+int32_t cm_paged_order(const cm_pagedset* set, int32_t routing_layer, int64_t tail_len,
+                       double* keys_dev, uint8_t* digests_dev, int64_t* plan_dev, void* workspace,
+                       size_t workspace_bytes, void* stream);
 
 /* Block tables of the merged cache for a plan over the paged fragments (any plan
  * of this file's layout whose slots index the paged set's fragments, e.g. from

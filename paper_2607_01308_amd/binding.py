@@ -306,6 +306,16 @@ def paged_workspace_size(pset: PagedSet) -> int:
     return int(out.value)
 
 
+def paged_order(pset: PagedSet, routing_layer: int, tail_len: int, keys: torch.Tensor,
+                digests: torch.Tensor, plan_dev: torch.Tensor, workspace: torch.Tensor,
+                stream=None) -> None:
+    """cm_paged_order: scores, Ids and the plan of fragments that live in the pool."""
+    C.check(C.lib().cm_paged_order(ctypes.byref(pset.struct), routing_layer, tail_len,
+                                   _ptr(keys), _ptr(digests), _ptr(plan_dev), _ptr(workspace),
+                                   workspace.numel() * workspace.element_size(),
+                                   _stream(stream, pset)), "cm_paged_order")
+
+
 def paged_tables(pset: PagedSet, plan_host: np.ndarray, free_pages):
     """Block tables of the merged cache (host): K table, V table, fresh codes 2j + kv."""
     plan_host = np.ascontiguousarray(plan_host, dtype=np.int64)

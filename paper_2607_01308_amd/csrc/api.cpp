@@ -726,12 +726,23 @@ int32_t check_pagedset(const cm_pagedset* set, cm::PagedDesc* out) {
 
 // Workspace of the paged render: angles, then 32 bytes per fresh page (at most
 // two per merged block of B rows, T_out at most the sum of the lengths).
-size_t paged_ws(const cm::PagedDesc& p) {
+size_t paged_render_ws(const cm::PagedDesc& p) {
   int64_t T_all = 0;
   for (int i = 0; i < p.s.n; ++i) T_all += p.s.T(i);
   const int64_t blocks = (T_all + p.block - 1) / p.block;
   return cm::align_up(sizeof(double) * (size_t)p.s.n * p.s.d, cm::kWsAlign) +
          cm::align_up(32 * 2 * (size_t)blocks, cm::kWsAlign);
+}
+
+// Every paged call fits: the render's, or the scores' and Ids' of
+// cm_paged_order (which run one after the other over the same bytes).
+size_t paged_ws(const cm::PagedDesc& p) {
+  size_t need = paged_render_ws(p);
+  const size_t kn = cm::knorm_max_bytes(p.s);
+  const size_t hb = cm::hash_layout(p.s).bytes;
+  if (kn > need) need = kn;
+  if (hb > need) need = hb;
+  return need;
 }
 
 // Plan checks against the fragments' lengths (slots, lengths, prefix offsets).
@@ -768,6 +779,34 @@ int32_t cm_paged_workspace_size(const cm_pagedset* set, size_t* bytes_out) {
   if (!bytes_out) return fail(CM_EINVAL, "bytes_out is NULL");
   *bytes_out = paged_ws(p);
   return CM_OK;
+}
+
+int32_t cm_paged_order(const cm_pagedset* set, int32_t routing_layer, int64_t tail_len,
+                       double* keys_dev, uint8_t* digests_dev, int64_t* plan_dev, void* workspace,
+                       size_t workspace_bytes, void* stream) {
+  g_err.clear();
+  cm::PagedDesc p;
+  int32_t st = check_pagedset(set, &p);
+  if (st != CM_OK) return st;
+  const cm::SetDesc& s = p.s;
+  if (routing_layer < 0 || routing_layer >= s.L)
+    return fail(CM_EINVAL, "routing_layer must be in [0, L), got " + std::to_string(routing_layer));
+  const int64_t tmin = min_T(s);
+  if (tail_len < 1 || tail_len > tmin)
+    return fail(CM_EINVAL, "tail_len must be in [1, min T] = [1, " + std::to_string(tmin) + "], got " +
+                               std::to_string(tail_len));
+  if (!keys_dev || !aligned(keys_dev, 8)) return fail(CM_EINVAL, "keys_dev is NULL or misaligned");
+  if (!digests_dev || !aligned(digests_dev, 16))
+    return fail(CM_EINVAL, "digests_dev is NULL or not 16-byte aligned");
+  if (!plan_dev || !aligned(plan_dev, 8)) return fail(CM_EINVAL, "plan_dev is NULL or misaligned");
+  if ((st = check_ws(workspace, workspace_bytes, paged_ws(p))) != CM_OK) return st;
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  hipStream_t sm = static_cast<hipStream_t>(stream);
+  hipError_t e = cm::launch_knorm_paged(p, cm::knorm_layout(s, tail_len), routing_layer, tail_len,
+                                        keys_dev, ws, sm);
+  if (e == hipSuccess) e = cm::launch_hash_paged(p, cm::hash_layout(s), digests_dev, ws, sm);
+  if (e == hipSuccess) e = cm::launch_order(s, keys_dev, digests_dev, true, plan_dev, sm);
+  return e == hipSuccess ? CM_OK : fail_hip(e, "cm_paged_order");
 }
 
 int32_t cm_paged_tables(const cm_pagedset* set, const int64_t* plan_host, const int32_t* free_host,
@@ -847,7 +886,7 @@ int32_t cm_paged_render(const cm_pagedset* set, const int64_t* plan_dev, const i
   if (n_fresh < 0 || n_fresh > 2 * nbo) return fail(CM_EINVAL, "n_fresh out of range");
   if (n_fresh > 0 && (!fresh_dev || !k_table_dev || !v_table_dev))
     return fail(CM_EINVAL, "fresh_dev / tables are NULL");
-  if ((st = check_ws(workspace, workspace_bytes, paged_ws(p))) != CM_OK) return st;
+  if ((st = check_ws(workspace, workspace_bytes, paged_render_ws(p))) != CM_OK) return st;
   hipError_t e = cm::launch_paged_render(p, plan_dev, (int32_t)nu, rope->base, rope->style,
                                          k_table_dev, v_table_dev, fresh_dev, n_fresh,
                                          static_cast<uint8_t*>(workspace),

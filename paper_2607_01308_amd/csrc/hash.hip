@@ -129,6 +129,65 @@ __global__ __launch_bounds__(kBlock) void hash_chunk_kernel(const int64_t* __res
   }
 }
 
+// The chunk kernel for fragments in a paged pool ([L][2][P][H][B][d]; the
+// fragment's row t in row t % B of page blocks[first + t / B]). The Id is the
+// same content address as for the dense form, so each tensor's bytes are hashed
+// in the order of its dense [1, H, T, d] layout: lane k of a stripe walks chunk
+// k's blocks row by row through the pages (a 64-byte block never straddles a
+// row, rows being 64-byte multiples).
+__global__ __launch_bounds__(kBlock) void paged_hash_chunk_kernel(
+    const uint8_t* __restrict__ pool, int64_t P, int32_t H, int32_t b_shift, int32_t rb_shift,
+    const int64_t* __restrict__ table, const int32_t* __restrict__ blocks, int32_t n,
+    int64_t token_bytes, const int64_t* __restrict__ base0, const int64_t* __restrict__ task_base,
+    int64_t total_tasks, uint8_t* __restrict__ nodes) {
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform per wave
+  const int64_t waves = (int64_t)gridDim.x * (kBlock / 64);
+  const int64_t rb = (int64_t)1 << rb_shift;
+  const int64_t bmask = ((int64_t)1 << b_shift) - 1;
+  for (int64_t task = (int64_t)blockIdx.x * (kBlock / 64) + wave; task < total_tasks;
+       task += waves) {
+    const int i = find_fragment(task_base, n, task);
+    const int64_t T = table[2 * (int64_t)i];
+    const int64_t first = table[2 * (int64_t)i + 1];
+    const int64_t bytes = T * token_bytes;
+    const int64_t stripes = stripes_of(bytes);
+    const int64_t m = chunks_of(bytes);
+    const int64_t local = task - task_base[i];
+    const int64_t t = local / stripes;                 // tensor 2l + kv
+    const int64_t sidx = local - t * stripes;
+    const int64_t in_stripe = (bytes >> 6) - sidx * kStripeBlocks;
+    const int64_t stripe_blocks = in_stripe < kStripeBlocks ? in_stripe : kStripeBlocks;
+    const int64_t b0 = (int64_t)lane * kB3ChunkBlocks;
+    if (b0 >= stripe_blocks) continue;                 // lane past the tensor's last chunk
+    const int64_t nb = stripe_blocks - b0 < kB3ChunkBlocks ? stripe_blocks - b0 : kB3ChunkBlocks;
+    const int64_t c = sidx * kStripeChunks + lane;     // chunk index in the tensor
+    // dense byte 1024 c = head h, row tr, column col
+    const int64_t o = c << 10;
+    int64_t h = o / (T << rb_shift);
+    const int64_t r = o - h * (T << rb_shift);
+    int64_t tr = r >> rb_shift;
+    int64_t col = r & (rb - 1);
+    // b3_chunk asks for the chunk's blocks in order, one call each
+    auto load = [&](int64_t, uint32_t (&w)[16]) {
+      const int64_t page = blocks[first + (tr >> b_shift)];
+      const int64_t row = ((((t * P + page) * H + h) << b_shift) + (tr & bmask));
+      load_block64(pool + (row << rb_shift) + col, w);
+      col += 64;
+      if (col == rb) {
+        col = 0;
+        if (++tr == T) {
+          tr = 0;
+          ++h;
+        }
+      }
+    };
+    B3Cv st;
+    b3_chunk(st, nb, (uint64_t)c, m == 1, load);
+    store_cv(nodes + (base0[i] + t * m + c) * 32, st);
+  }
+}
+
 constexpr int kSubLevels = 3;
 constexpr int kSubLanes = 64;
 
@@ -502,6 +561,28 @@ hipError_t launch_hash(const SetDesc& s, const HashLayout& lay, const uint8_t* s
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   return launch_hash_tree(s, lay, select, want, digests, ws, stream);
+}
+
+hipError_t launch_hash_paged(const PagedDesc& p, const HashLayout& lay, uint8_t* digests,
+                             uint8_t* ws, hipStream_t stream) {
+  const SetDesc& s = p.s;
+  hipError_t e = launch_hash_prep(s, lay, ws, stream);
+  if (e != hipSuccess) return e;
+  {
+    int64_t* base = reinterpret_cast<int64_t*>(ws + lay.off_tables);
+    const int64_t nb1 = s.n + 1;
+    ScopedTiming tm(K_HASH_LEAF, stream);
+    const int64_t full = (lay.tasks + (kBlock / 64) - 1) / (kBlock / 64);
+    const int64_t cap = (int64_t)device_cu_count() * kLeafBlocksPerCu;
+    const int64_t grid = full < cap ? full : cap;
+    hipLaunchKernelGGL(paged_hash_chunk_kernel, dim3((uint32_t)grid), dim3(kBlock), 0, stream,
+                       static_cast<const uint8_t*>(p.pool), p.pages, s.H, p.b_shift,
+                       (int32_t)__builtin_ctzll((unsigned long long)s.row_bytes), s.table_dev,
+                       p.blocks_dev, s.n, token_bytes_of(s), base,
+                       base + (int64_t)(lay.levels + 1) * nb1, lay.tasks, ws + lay.off_buf0);
+  }
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  return launch_hash_tree(s, lay, nullptr, 0, digests, ws, stream);
 }
 
 }  // namespace cm

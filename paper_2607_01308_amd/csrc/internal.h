@@ -204,6 +204,13 @@ struct PagedDesc {
   void* pool;
   const int32_t* blocks_dev;
 };
+// Steps 1-2 on paged fragments: scores (full tree) and the Id of every fragment
+// (the same content address as the dense form's: each tensor hashed in the
+// byte order of its dense layout).
+hipError_t launch_knorm_paged(const PagedDesc& p, const KnormLayout& lay, int32_t layer,
+                              int64_t tail_len, double* keys, uint8_t* ws, hipStream_t stream);
+hipError_t launch_hash_paged(const PagedDesc& p, const HashLayout& lay, uint8_t* digests,
+                             uint8_t* ws, hipStream_t stream);
 hipError_t launch_paged_render(const PagedDesc& p, const int64_t* plan_dev, int32_t n_unique,
                                double base, int32_t style, const int32_t* k_table,
                                const int32_t* v_table, const int32_t* fresh, int64_t n_fresh,

@@ -58,21 +58,51 @@ __device__ __forceinline__ double lds_tree(double* sh, int count) {
 
 constexpr int kInFlight = 16;   // row loads in flight per thread
 
+// Where row t of head h of fragment i's routing-layer K lives: a dense
+// [1, H, T, d] tensor named by the fragment table, or a page of a paged pool
+// ([L][2][P][H][B][d], the fragment's row t in row t % B of its page t / B).
+struct DenseRows {
+  const int64_t* table;
+  int64_t stride;
+  int32_t layer;
+  __device__ __forceinline__ int64_t length(int i) const { return table[(int64_t)i * stride]; }
+  __device__ __forceinline__ const uint8_t* row(int i, int64_t T, int64_t h, int64_t t,
+                                                int rb_shift) const {
+    return reinterpret_cast<const uint8_t*>(table[(int64_t)i * stride + 1 + 2 * layer]) +
+           ((h * T + t) << rb_shift);
+  }
+};
+
+struct PagedRows {
+  const uint8_t* pool;
+  const int64_t* table;    // {T_i, first page index}
+  const int32_t* blocks;
+  int64_t P;
+  int32_t H, b_shift, layer;
+  __device__ __forceinline__ int64_t length(int i) const { return table[2 * (int64_t)i]; }
+  __device__ __forceinline__ const uint8_t* row(int i, int64_t, int64_t h, int64_t t,
+                                                int rb_shift) const {
+    const int64_t page = blocks[table[2 * (int64_t)i + 1] + (t >> b_shift)];
+    const int64_t r = ((((int64_t)2 * layer * P + page) * H + h) << b_shift) +
+                      (t & (((int64_t)1 << b_shift) - 1));
+    return pool + (r << rb_shift);
+  }
+};
+
 // grid (count0, n), 256 threads: block b of fragment i sums rows
 // [b*rpb, (b+1)*rpb) of the padded (h, r) row space.
-template <int ESIZE>
-__global__ __launch_bounds__(256) void knorm_rows_kernel(const int64_t* __restrict__ table,
-                                                         int64_t stride, int32_t layer,
-                                                         int64_t tail, int32_t d, int64_t rows,
-                                                         int32_t rpb, int64_t count0,
+template <int ESIZE, class Rows>
+__global__ __launch_bounds__(256) void knorm_rows_kernel(Rows src, int64_t tail, int32_t d,
+                                                         int64_t rows, int32_t rpb,
+                                                         int64_t count0,
                                                          double* __restrict__ out) {
 #pragma clang fp contract(off)
   __shared__ double sh[256];
   const int i = blockIdx.y;
   const int64_t blk = blockIdx.x;
-  const int64_t T = table[(int64_t)i * stride];
-  const uint8_t* K = reinterpret_cast<const uint8_t*>(table[(int64_t)i * stride + 1 + 2 * layer]);
+  const int64_t T = src.length(i);
   const int row_bytes = d * ESIZE;
+  const int rb_shift = __builtin_ctz((unsigned)row_bytes);
   const int lpr = row_bytes >> 4;  // lanes per row: a power of two in [4, 64]
   const int rpp = 256 / lpr;       // rows per pass
   const int tid = threadIdx.x;
@@ -93,8 +123,7 @@ __global__ __launch_bounds__(256) void knorm_rows_kernel(const int64_t* __restri
       const int64_t f = blk * rpb + fl;
       valid[g] = fl < rpb && f < rows;
       v[g] = u32x4{0u, 0u, 0u, 0u};
-      if (valid[g])
-        v[g] = *global_ptr<u32x4>(K + (h * T + (T - tail + r)) * row_bytes + q * 16);
+      if (valid[g]) v[g] = *global_ptr<u32x4>(src.row(i, T, h, T - tail + r, rb_shift) + q * 16);
       r += rpp;
       if (r >= tail) {               // a division only for tails shorter than a pass
         const int64_t k = r < 2 * tail ? 1 : r / tail;
@@ -158,9 +187,13 @@ size_t knorm_max_bytes(const SetDesc& s) {
   return knorm_layout(s, tmin).bytes;  // grows with tail_len, which is at most min T
 }
 
-hipError_t launch_knorm_partial(const SetDesc& s, const KnormLayout& lay, int32_t layer,
-                                int64_t tail_len, double* keys, uint8_t* ws, hipStream_t stream,
-                                int64_t fold_max, KnormPartials* out) {
+namespace {
+
+// knorm_rows over `src`, then tree launches down to fold_max partial sums.
+template <class Rows>
+hipError_t knorm_launches(const SetDesc& s, const KnormLayout& lay, Rows src, int64_t tail_len,
+                          double* keys, uint8_t* ws, hipStream_t stream, int64_t fold_max,
+                          KnormPartials* out) {
   double* bufs[2] = {reinterpret_cast<double*>(ws + lay.off_a),
                      reinterpret_cast<double*>(ws + lay.off_b)};
   {
@@ -168,13 +201,11 @@ hipError_t launch_knorm_partial(const SetDesc& s, const KnormLayout& lay, int32_
     double* o = lay.count0 == 1 ? keys : bufs[0];
     const dim3 grid((uint32_t)lay.count0, (uint32_t)s.n);
     if (s.esize == 2)
-      hipLaunchKernelGGL(knorm_rows_kernel<2>, grid, dim3(256), 0, stream, s.table_dev,
-                         s.stride, layer, tail_len, s.d, lay.rows, lay.rows_per_block,
-                         lay.count0, o);
+      hipLaunchKernelGGL((knorm_rows_kernel<2, Rows>), grid, dim3(256), 0, stream, src, tail_len,
+                         s.d, lay.rows, lay.rows_per_block, lay.count0, o);
     else
-      hipLaunchKernelGGL(knorm_rows_kernel<4>, grid, dim3(256), 0, stream, s.table_dev,
-                         s.stride, layer, tail_len, s.d, lay.rows, lay.rows_per_block,
-                         lay.count0, o);
+      hipLaunchKernelGGL((knorm_rows_kernel<4, Rows>), grid, dim3(256), 0, stream, src, tail_len,
+                         s.d, lay.rows, lay.rows_per_block, lay.count0, o);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -196,6 +227,23 @@ hipError_t launch_knorm_partial(const SetDesc& s, const KnormLayout& lay, int32_
   out->parts = c == 1 ? keys : bufs[cur];
   out->count = c;
   return hipSuccess;
+}
+
+}  // namespace
+
+hipError_t launch_knorm_partial(const SetDesc& s, const KnormLayout& lay, int32_t layer,
+                                int64_t tail_len, double* keys, uint8_t* ws, hipStream_t stream,
+                                int64_t fold_max, KnormPartials* out) {
+  return knorm_launches(s, lay, DenseRows{s.table_dev, s.stride, layer}, tail_len, keys, ws,
+                        stream, fold_max, out);
+}
+
+hipError_t launch_knorm_paged(const PagedDesc& p, const KnormLayout& lay, int32_t layer,
+                              int64_t tail_len, double* keys, uint8_t* ws, hipStream_t stream) {
+  KnormPartials kp;
+  const PagedRows src{static_cast<const uint8_t*>(p.pool), p.s.table_dev, p.blocks_dev, p.pages,
+                      p.s.H, p.b_shift, layer};
+  return knorm_launches(p.s, lay, src, tail_len, keys, ws, stream, 1, &kp);
 }
 
 hipError_t launch_knorm(const SetDesc& s, const KnormLayout& lay, int32_t layer, int64_t tail_len,

@@ -30,7 +30,7 @@ from .binding import (FragmentBatch, bag_plan, canonical_order, equal_key_mask, 
                       fragment_hash_select, fragment_knorm, multiset_order, plan_elems,
                       paged_render, paged_tables, paged_workspace_size, render_merge,
                       render_deliveries_async, render_merge_devplan, render_merge_hash,
-                      render_merge_range, render_set, workspace_size)
+                      render_merge_range, render_set, workspace_size, paged_order)
 from .binding import PagedSet
 
 _WS: Dict[tuple, torch.Tensor] = {}
@@ -493,6 +493,9 @@ class PagedRender:
     v_table: np.ndarray          # the same for V
     fresh: np.ndarray            # pages written by the render, as codes 2j + kv
     T_out: int
+    plan: Optional[np.ndarray] = None              # render_paged_set: the plan it computed
+    digests_dev: Optional[torch.Tensor] = None     # render_paged_set: [n, 32] Ids
+    keys_dev: Optional[torch.Tensor] = None        # render_paged_set: [n] scores S_i
 
     @property
     def reused_pages(self) -> int:
@@ -517,3 +520,28 @@ def render_paged(pset: PagedSet, plan_host: np.ndarray, free_pages, rope_base: f
         paged_render(pset, plan_dev, plan_host, rope_base, style, kd, vd, fd, ws, main)
     return PagedRender(k_table=kt, v_table=vt, fresh=fresh,
                        T_out=int(plan_host[C.PLAN_TOUT]))
+
+
+def render_paged_set(pset: PagedSet, routing_layer: int, rope_base: float, free_pages,
+                     style: str = "half", stream=None) -> PagedRender:
+    """Steps 1-5 on fragments that live only in the pool (§4.5): scores, the Id
+    of every fragment (the content address of its dense form), dedupe, order and
+    offsets on the device (cm_paged_order), the plan to the host for the block
+    tables, then the render of the pages that no fragment page can stand for.
+    No dense copy of any fragment is made."""
+    dev = pset.device
+    main = stream if stream is not None else torch.cuda.current_stream(dev)
+    with torch.cuda.stream(main):
+        ws = torch.empty(max(paged_workspace_size(pset), 256), dtype=torch.uint8, device=dev)
+        keys = torch.empty(pset.n, dtype=torch.float64, device=dev)
+        digests = torch.empty((pset.n, 32), dtype=torch.uint8, device=dev)
+        plan_dev = torch.empty(plan_elems(pset.n), dtype=torch.int64, device=dev)
+        paged_order(pset, routing_layer, min(pset.lengths), keys, digests, plan_dev, ws, main)
+        plan_host = _plan_to_host(plan_dev, main)
+        _check_plan(plan_host, "cm_paged_order")
+        kt, vt, fresh = paged_tables(pset, plan_host, free_pages)
+        kd, vd = torch.from_numpy(kt).to(dev), torch.from_numpy(vt).to(dev)
+        fd = torch.from_numpy(fresh).to(dev)
+        paged_render(pset, plan_dev, plan_host, rope_base, style, kd, vd, fd, ws, main)
+    return PagedRender(k_table=kt, v_table=vt, fresh=fresh, T_out=int(plan_host[C.PLAN_TOUT]),
+                       plan=plan_host, digests_dev=digests, keys_dev=keys)

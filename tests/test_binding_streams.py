@@ -110,7 +110,7 @@ def test_every_enqueuing_call_is_covered():
     render is checked separately below)."""
     takes_stream = {name for name, f in inspect.getmembers(binding, inspect.isfunction)
                     if "stream" in inspect.signature(f).parameters and not name.startswith("_")}
-    assert takes_stream == set(CALLS) | {"paged_render"}
+    assert takes_stream == set(CALLS) | {"paged_render", "paged_order"}
 
 
 @pytest.mark.parametrize("name", sorted(CALLS))
@@ -130,6 +130,14 @@ def test_paged_render_marks_both_tables(fake_lib):
     binding.paged_render(pset, T, PLAN, 1e4, "half", T, T, T, T, s)
     assert [t.streams for t in pset.device_tables] == [[s], [s]]
     assert fake_lib.calls[-1][1].value == 33
+
+
+def test_paged_order_marks_both_tables(fake_lib):
+    pset = _owner(2)
+    s = FakeStream(44)
+    binding.paged_order(pset, 0, 1, T, T, T, T, s)
+    assert [t.streams for t in pset.device_tables] == [[s], [s]]
+    assert fake_lib.calls[-1][1].value == 44
 
 
 def test_scratch_is_cached_per_stream(monkeypatch):

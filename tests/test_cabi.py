@@ -440,3 +440,26 @@ def test_paged_tables_rejects(lib):
     fp.blocks[0] = fp.P                                                 # page outside the pool
     st, *_ = _paged_tables(lib, fp, plan)
     assert st == C.CM_EINVAL
+
+
+def test_paged_order_argument_checks(lib):
+    fp = FakePaged((30, 50))
+    need = ctypes.c_size_t(0)
+    assert lib.cm_paged_workspace_size(fp.ref, ctypes.byref(need)) == C.CM_OK
+    # the workspace covers the paged hash's node tables and digests too
+    assert need.value >= 32 * 2 * 2 * sum(-(-T * 2 * 64 * 2 // 1024) for T in (30, 50))
+    keys, dig, plan = ctypes.c_void_p(0x30000), ctypes.c_void_p(0x40000), ctypes.c_void_p(0x50000)
+    ws = ctypes.c_void_p(0x60000)
+
+    def call(layer=1, tail=30, keys=keys, dig=dig, plan=plan, ws_bytes=need.value):
+        return lib.cm_paged_order(fp.ref, layer, tail, keys, dig, plan, ws, ws_bytes, None)
+
+    assert call(ws_bytes=0) == C.CM_EWORKSPACE             # every other check passed
+    assert call(layer=2) == C.CM_EINVAL
+    assert call(tail=31) == C.CM_EINVAL                    # longer than the shortest fragment
+    assert call(tail=0) == C.CM_EINVAL
+    assert call(keys=None) == C.CM_EINVAL
+    assert call(dig=ctypes.c_void_p(0x40008)) == C.CM_EINVAL
+    assert call(plan=None) == C.CM_EINVAL
+    fp.blocks[0] = fp.P                                     # a page id outside the pool
+    assert call() == C.CM_EINVAL

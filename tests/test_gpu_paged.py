@@ -2,7 +2,9 @@
 merged cache read back through its K and V block tables equals the dense render
 of the same fragments bit for bit (the dense render is checked against the
 oracle elsewhere; one case here is checked against the oracle directly), reused
-pages are the fragments' own, and no page outside the fresh list changes."""
+pages are the fragments' own, and no page outside the fresh list changes. Steps
+1-5 on fragments that live only in the pool (cm_paged_order, then the paged
+render) are checked against the oracle: Ids, scores, plan and merged cache."""
 
 import numpy as np
 import pytest
@@ -10,7 +12,8 @@ import torch
 
 import synth
 import paper_2607_01308_amd as cm
-from gpu_util import check_render, log
+from gpu_util import (check_render, k_close, k_stats, log, oracle_ids, oracle_keys,
+                      oracle_layers, oracle_plan)
 
 pytestmark = pytest.mark.gpu
 
@@ -78,3 +81,64 @@ def test_paged_render_against_oracle():
     paged[:, 0], paged[:, 1] = K, V
     dense.merged.copy_(paged)                 # the cache views now show the paged result
     check_render(dense, dl, w.dtype, w.routing_layer, w.rope_base)
+
+
+SET_CASES = [
+    # duplicate delivery and an equal-score pair (shared K), ragged lengths
+    dict(dtype="bfloat16", d=128, B=16, H=2, L=3, lengths=(300, 517, 45, 300),
+         deliveries=(0, 1, 2, 3, 1), shared_k=((0, 3),)),
+    dict(dtype="float32", d=64, B=16, H=3, L=2, lengths=(70, 33, 129, 2),
+         deliveries=(2, 0, 1, 3, 2, 2)),
+    dict(dtype="bfloat16", d=32, B=32, H=2, L=2, lengths=(99, 64, 1, 200)),     # 64-byte rows, T=1
+    dict(dtype="bfloat16", d=256, B=8, H=4, L=2, lengths=(1030, 77, 513)),     # 512-byte rows
+    dict(dtype="float32", d=256, B=16, H=1, L=2, lengths=(257, 4096)),         # 1 KiB rows, 16 KiB pages
+]
+
+
+@pytest.mark.parametrize("case", SET_CASES,
+                         ids=[f"{c['dtype']}-d{c['d']}-B{c['B']}" for c in SET_CASES])
+def test_paged_set_steps_1_to_5_against_oracle(case):
+    """render_paged_set on a pool holding every delivery (copies on pages of
+    their own): the Ids are the dense form's content addresses, the scores and
+    the plan are the oracle's, and the merged cache read back through the block
+    tables is the oracle's render. The fragments' dense tensors serve only to
+    fill the pool and to compute the oracle's answer; they are dropped before
+    the paged path runs."""
+    w = synth.custom("paged-set", dtype=case["dtype"], d=case["d"], H=case["H"], L=case["L"],
+                     lengths=case["lengths"], deliveries=case.get("deliveries"),
+                     shared_k=case.get("shared_k", ()), routing_layer=1, rope_base=1e4)
+    dl = synth.make_deliveries(w, synth.make_fragments(w, device="cuda"))
+    tail = min(w.lengths)
+    ids = oracle_ids(dl, w.dtype)
+    keys = oracle_keys(dl, w.dtype, w.routing_layer, tail)
+    plan = oracle_plan(dl, ids, keys)
+    ref = oracle_layers(dl, w.dtype, plan["order"], w.rope_base, range(w.L))
+    # room for every merged block of K and V to be fresh
+    spare = 2 * (sum(w.lengths) // case["B"] + len(w.lengths) + 1)
+    pool, lengths, page_lists, free = synth.make_paged(dl, case["B"], spare_pages=spare, seed=5)
+    del dl
+    torch.cuda.synchronize()
+    log(f"[paged-set] {case}")
+    pr = cm.render_paged_set(cm.PagedSet(pool, lengths, page_lists), w.routing_layer, w.rope_base,
+                             free)
+    torch.cuda.synchronize()
+    assert [bytes(x) for x in pr.digests_dev.cpu().numpy()] == ids
+    assert list(pr.keys_dev.cpu().numpy()) == keys
+    n = len(ids)
+    p = pr.plan
+    assert p[2] == plan["n_unique"] and p[3] == plan["T_out"] == pr.T_out
+    assert list(p[4:4 + plan["n_unique"]]) == plan["order"]
+    assert list(p[4 + n:4 + n + plan["n_unique"]]) == plan["offsets"]
+    assert list(p[4 + 3 * n:4 + 4 * n]) == plan["slot_of_delivery"]
+    K = synth.gather_paged(pool, pr.k_table, pr.T_out)[:, 0]
+    V = synth.gather_paged(pool, pr.v_table, pr.T_out)[:, 1]
+    worst = 0
+    for l in range(w.L):
+        gK, gV = synth.tensor_to_numpy(K[l]), synth.tensor_to_numpy(V[l])
+        rK, rV = ref[l]
+        assert np.array_equal(gV, rV), f"V of layer {l} differs"
+        ok, _ = k_close(gK, rK, w.dtype)
+        worst = max(worst, k_stats(gK, rK, w.dtype)[0])
+        assert ok, f"K of layer {l} outside tolerance"
+    log(f"  paged set: {n} deliveries, {plan['n_unique']} slots, T_out {pr.T_out}, "
+        f"K largest distance {worst} ulp")
