@@ -302,6 +302,7 @@ def main():
               "single-GPU path and no multi-GPU figure is produced", file=sys.stderr)
         sys.exit(2)
 
+    import numpy as np
     import torch
     import synth
     import paper_2607_01308_amd as cm
@@ -434,6 +435,28 @@ def main():
     cm.timing_enable(False)
     k_ms, k_n = cm.timing_query("paged")
     cm.timing_reset()
+    # steps 1-5 on the pool alone: scores, Ids (a second read of every fragment
+    # byte: the paged hash is not fused into the paged render) and order on the
+    # device, the plan to the host, block tables, render of the fresh pages
+    for _ in range(2):
+        ps = cm.render_paged_set(pset, w.routing_layer, w.rope_base, free)
+    torch.cuda.synchronize()
+    cm.timing_reset()
+    cm.timing_enable(True)
+    tp = time.perf_counter()
+    for _ in range(args.steps):
+        ps = cm.render_paged_set(pset, w.routing_layer, w.rope_base, free)
+    torch.cuda.synchronize()
+    ms_paged_set = (time.perf_counter() - tp) / args.steps * 1e3
+    cm.timing_enable(False)
+    paged_set_kernels = {}
+    for k in cm.KERNELS:
+        kms, kn = cm.timing_query(k)
+        if kn:
+            paged_set_kernels[k] = round(kms / args.steps, 4)
+    cm.timing_reset()
+    paged_set_equal = bool(np.array_equal(ps.plan, set_plan))
+    del ps
     page_bytes = w.L * w.H * B * w.d * (2 if w.dtype == "bfloat16" else 4)
     paged_bytes = 2 * len(pr.fresh) * page_bytes
     paged = {"ms": round(ms_paged, 4), "kernel_ms": round(k_ms / max(k_n, 1), 4),
@@ -441,7 +464,11 @@ def main():
              "pages_reused": pr.reused_pages, "bytes": paged_bytes,
              "bytes_vs_dense": round(paged_bytes / w.render_bytes, 4),
              "kernel_GBps": round(paged_bytes / (k_ms / max(k_n, 1) / 1e3) / 1e9, 1),
-             "what": "block tables (host) + table upload + paged render kernel per step"}
+             "what": "block tables (host) + table upload + paged render kernel per step",
+             "set_steps_1_to_5": {"ms": round(ms_paged_set, 4), "kernels_ms": paged_set_kernels,
+                                  "plan_equals_dense_set_plan": paged_set_equal,
+                                  "what": "cm_paged_order (scores, Ids, order) + plan to host + "
+                                          "block tables + paged render, fragments only in the pool"}}
     del pool, pset, pr
     torch.cuda.empty_cache()
 

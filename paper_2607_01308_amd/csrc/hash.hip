@@ -532,8 +532,10 @@ hipError_t launch_hash_tree(const SetDesc& s, const HashLayout& lay, const uint8
 hipError_t launch_mask_hash_prep(const SetDesc& s, const HashLayout& lay, const KnormPartials& kp,
                                  double* keys, uint8_t* mask, uint8_t* ws, hipStream_t stream) {
   ScopedTiming tm(K_KEY_MASK, stream);
-  // the fold spreads over the workgroup; the scans want at least n threads
-  int threads = kp.count > 1 ? 1024 : 64;
+  // at least n threads (the scans over fragments); the node tables' scans cost a
+  // barrier per step, so no more threads than that (the fold's few thousand
+  // additions do not need them)
+  int threads = 64;
   while (threads < s.n) threads <<= 1;
   hipLaunchKernelGGL(mask_hash_prep_kernel, dim3(1), dim3(threads), 0, stream, s.table_dev, s.n,
                      s.stride, token_bytes_of(s), s.L, lay.levels, kp.parts, kp.count, keys, mask,

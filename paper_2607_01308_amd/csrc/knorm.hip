@@ -9,7 +9,7 @@
 // lanes (one 16-byte load each): the lane's own elements form the bottom levels
 // of the row tree in registers and an xor-butterfly over those lanes forms the
 // upper levels (fp addition is commutative, so both partners hold the same
-// node). An aligned block of up to 256 row norms is one subtree, reduced in LDS;
+// node). An aligned block of up to 64 row norms is one subtree, reduced in LDS;
 // further levels run as small tree launches, the last few of them, where a
 // one-workgroup kernel follows, inside that kernel (knorm_fold.h). Reads only
 // the H*T*d*e tail bytes of one layer per fragment.
@@ -170,7 +170,9 @@ KnormLayout knorm_layout(const SetDesc& s, int64_t tail_len) {
   KnormLayout lay{};
   lay.rows = (int64_t)s.H * tail_len;
   lay.padded = next_pow2(lay.rows);
-  lay.rows_per_block = (int32_t)(lay.padded < 256 ? lay.padded : 256);
+  // 64 rows (one subtree) per workgroup: enough workgroups to keep the loads of a
+  // short tail in flight across the chip
+  lay.rows_per_block = (int32_t)(lay.padded < 64 ? lay.padded : 64);
   lay.count0 = lay.padded / lay.rows_per_block;
   const size_t a = sizeof(double) * (size_t)s.n * (size_t)lay.count0;
   const size_t b = sizeof(double) * (size_t)s.n * (size_t)((lay.count0 + 255) / 256);
