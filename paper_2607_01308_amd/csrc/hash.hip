@@ -379,13 +379,20 @@ __device__ __forceinline__ void fragment_id(uint64_t T, const IdShape& sh,
 // dependent compressions is about log2(m) long; the root goes to node
 // base_top[i] + t of the top level.
 constexpr int kTailLevels = kSubLevels + 6;   // 2^3 nodes per lane x 64 lanes
+// Largest tail grid (2L x n workgroups) whose last workgroups compute the Ids
+// (Tiny 8, Qwen3-1.7B N=2 112; measured at 2304 on the Qwen3-4B large set, the
+// fences cost about 0.1 ms more than the Id launch).
+constexpr int64_t kFuseIdMaxGroups = 256;
 
 //
-// The workgroup that writes the last of fragment i's 2L roots then computes its
-// Id (fragment_id): each workgroup makes its root visible device-wide and
-// counts itself in arrived[i] (zeroed by the node-table kernel of the same
-// call); the one that sees 2L - 1 arrivals before its own reads every root
-// (after an acquire fence) and resets the counter for a later pass.
+// With `arrived` (small sets): the workgroup that writes the last of fragment
+// i's 2L roots then computes its Id (fragment_id), which saves the Id launch.
+// Each workgroup makes its root visible device-wide and counts itself in
+// arrived[i] (zeroed by the node-table kernel of the same call); the one that
+// sees 2L - 1 arrivals before its own reads every root (after an acquire fence)
+// and resets the counter for a later pass. The release fence writes back the
+// XCD's L2, which across thousands of workgroups costs more than the launch it
+// saves, so large sets take the separate Id kernel.
 __global__ __launch_bounds__(kSubLanes) void hash_tail_kernel(
     const int64_t* __restrict__ table, int64_t stride, int64_t token_bytes, int32_t v0,
     const int64_t* __restrict__ base_lo, const int64_t* __restrict__ base_top,
@@ -422,6 +429,7 @@ __global__ __launch_bounds__(kSubLanes) void hash_tail_kernel(
   __syncthreads();
   fold_cvs(vals, cnt, true, lane);
   if (lane < 8) reinterpret_cast<uint32_t*>(out + (base_top[i] + t) * 32)[lane] = vals[lane];
+  if (!arrived) return;                  // the Ids come from hash_final_kernel
   __threadfence();                       // release this root to the other workgroups
   __syncthreads();
   if (lane == 0) seen = atomicAdd(&arrived[i], 1);
@@ -513,14 +521,18 @@ hipError_t launch_hash_tree(const SetDesc& s, const HashLayout& lay, const uint8
   const IdShape sh{s.L, s.H, s.d, (uint32_t)s.dtype, (uint32_t)s.esize};
   int32_t* arrived = reinterpret_cast<int32_t*>(ws + lay.off_arrived);
   if (v0 < lay.levels) {
-    // the top levels of every tensor, and each fragment's Id in the workgroup
-    // that finishes its last root
-    ScopedTiming tm(K_HASH_PARENT, stream);
-    hipLaunchKernelGGL(hash_tail_kernel, dim3((uint32_t)(2 * s.L), (uint32_t)s.n), dim3(kSubLanes),
-                       0, stream, s.table_dev, s.stride, token_bytes_of(s), v0, base + v0 * nb1,
-                       base + lay.levels * nb1, select, want, buf[launch & 1],
-                       buf[(launch + 1) & 1], sh, arrived, digests);
-    return hipGetLastError();
+    // the top levels of every tensor; for a small set also each fragment's Id, in
+    // the workgroup that finishes its last root
+    const bool fuse_id = (int64_t)2 * s.L * s.n <= kFuseIdMaxGroups;
+    {
+      ScopedTiming tm(K_HASH_PARENT, stream);
+      hipLaunchKernelGGL(hash_tail_kernel, dim3((uint32_t)(2 * s.L), (uint32_t)s.n),
+                         dim3(kSubLanes), 0, stream, s.table_dev, s.stride, token_bytes_of(s), v0,
+                         base + v0 * nb1, base + lay.levels * nb1, select, want, buf[launch & 1],
+                         buf[(launch + 1) & 1], sh, fuse_id ? arrived : nullptr, digests);
+    }
+    if ((e = hipGetLastError()) != hipSuccess || fuse_id) return e;
+    ++launch;
   }
   ScopedTiming tm(K_HASH_FINAL, stream);
   hipLaunchKernelGGL(hash_final_kernel, dim3((uint32_t)s.n), dim3(64), 0, stream, s.table_dev,

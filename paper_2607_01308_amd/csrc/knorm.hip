@@ -9,7 +9,7 @@
 // lanes (one 16-byte load each): the lane's own elements form the bottom levels
 // of the row tree in registers and an xor-butterfly over those lanes forms the
 // upper levels (fp addition is commutative, so both partners hold the same
-// node). An aligned block of up to 64 row norms is one subtree, reduced in LDS;
+// node). An aligned block of up to 256 row norms is one subtree, reduced in LDS;
 // further levels run as small tree launches, the last few of them, where a
 // one-workgroup kernel follows, inside that kernel (knorm_fold.h). Reads only
 // the H*T*d*e tail bytes of one layer per fragment.
@@ -170,9 +170,12 @@ KnormLayout knorm_layout(const SetDesc& s, int64_t tail_len) {
   KnormLayout lay{};
   lay.rows = (int64_t)s.H * tail_len;
   lay.padded = next_pow2(lay.rows);
-  // 64 rows (one subtree) per workgroup: enough workgroups to keep the loads of a
-  // short tail in flight across the chip
-  lay.rows_per_block = (int32_t)(lay.padded < 64 ? lay.padded : 64);
+  // one subtree of 256 rows per workgroup, or of fewer (down to 64) when that
+  // leaves too few workgroups to keep the loads of a short tail in flight (2048:
+  // eight per CU)
+  int64_t rpb = lay.padded < 256 ? lay.padded : 256;
+  while (rpb > 64 && (int64_t)s.n * (lay.padded / rpb) < 2048) rpb >>= 1;
+  lay.rows_per_block = (int32_t)rpb;
   lay.count0 = lay.padded / lay.rows_per_block;
   const size_t a = sizeof(double) * (size_t)s.n * (size_t)lay.count0;
   const size_t b = sizeof(double) * (size_t)s.n * (size_t)((lay.count0 + 255) / 256);
