@@ -183,6 +183,17 @@ class RenderResult:
         b = C.PLAN_HEADER + 3 * n
         return [int(x) for x in self.plan[b:b + n]]
 
+    def compact(self) -> "RenderResult":
+        """Move the merged cache into a buffer of exactly T_out rows and release
+        the larger one. A fused result's output buffer holds the sum of all
+        delivery lengths (the bound the device has before the dedupe), so with
+        many re-deliveries most of it is unused; this costs one copy of the
+        merged cache on the current stream. Other results are already exact."""
+        if self._pending is not None:
+            merged = self.merged.clone()
+            self._merged, self._cache, self._pending = merged, None, None
+        return self
+
     def _wait(self) -> None:
         """Host wait for the work of a fused result (the copies below run on the
         current stream, which need not be the one the result was computed on)."""

@@ -274,6 +274,44 @@ def test_render_set_rejects_members_with_one_id():
     assert not bool(out.any())
 
 
+@pytest.mark.parametrize("dtype,d,style", [("bfloat16", 128, "interleaved"),
+                                           ("float32", 64, "half"),
+                                           ("float32", 256, "interleaved"),
+                                           ("bfloat16", 32, "half")])
+def test_set_render_styles_and_row_sizes(dtype, d, style):
+    """cm_render_set (scores, order and unit tables in one launch, then the
+    unit render) for each pairing and several row sizes: the same cache as the
+    deliveries' render, which is checked against the oracle."""
+    w = synth.custom("set-style", dtype=dtype, d=d, H=3, L=2, lengths=(130, 61, 200, 7),
+                     deliveries=(2, 0, 1, 3, 0), routing_layer=1, rope_base=1e4)
+    _, dl = gpu_deliveries(w)
+    S = cm.LatentFragmentSet()
+    S.ingest_many(dl)
+    a = S.render(w.routing_layer, w.rope_base, style=style)
+    b = cm.render_deliveries(dl, w.routing_layer, w.rope_base, style=style, pipeline="serial")
+    torch.cuda.synchronize()
+    check_render(b, dl, w.dtype, w.routing_layer, w.rope_base, style=style)
+    assert a.T_out == b.T_out and torch.equal(a.merged, b.merged)
+
+
+def test_compact_releases_the_fused_buffer():
+    """A fused result over re-deliveries holds an output buffer sized for every
+    delivery; compact() moves the merged cache into one of exactly T_out rows,
+    with the same bytes, and drops the larger buffer."""
+    w = synth.custom("compact", dtype="bfloat16", d=128, H=2, L=2, lengths=(64, 40),
+                     deliveries=(0, 1, 0, 0, 1), routing_layer=1)
+    _, dl = gpu_deliveries(w)
+    res = cm.render_deliveries(dl, w.routing_layer, w.rope_base, pipeline="fused")
+    before = res.merged.clone()
+    big = res.merged.untyped_storage().nbytes()
+    res.compact()
+    torch.cuda.synchronize()
+    assert torch.equal(res.merged, before) and res.T_out == 104
+    assert res.merged.untyped_storage().nbytes() == before.numel() * before.element_size() < big
+    assert all(torch.equal(k, res.merged[l, 0]) for l, (k, _) in enumerate(res.cache))
+    check_render(res, dl, w.dtype, w.routing_layer, w.rope_base)
+
+
 def test_timing_api_counts_launches():
     w = synth.custom("timing", lengths=(64, 32))
     _, dl = gpu_deliveries(w)
