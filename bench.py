@@ -435,9 +435,11 @@ def main():
     cm.timing_enable(False)
     k_ms, k_n = cm.timing_query("paged")
     cm.timing_reset()
-    # steps 1-5 on the pool alone: scores, Ids (a second read of every fragment
-    # byte: the paged hash is not fused into the paged render) and order on the
-    # device, the plan to the host, block tables, render of the fresh pages
+    # steps 1-5 on the pool alone: scores, the colliding deliveries' Ids and the
+    # order on the device, the plan to the host, block tables, then the render of
+    # the fresh pages with the other Ids hashed beside it on a second stream (a
+    # second read of every fragment byte: the paged hash is not fused into the
+    # paged render)
     for _ in range(2):
         ps = cm.render_paged_set(pset, w.routing_layer, w.rope_base, free)
     torch.cuda.synchronize()
@@ -467,8 +469,10 @@ def main():
              "what": "block tables (host) + table upload + paged render kernel per step",
              "set_steps_1_to_5": {"ms": round(ms_paged_set, 4), "kernels_ms": paged_set_kernels,
                                   "plan_equals_dense_set_plan": paged_set_equal,
-                                  "what": "cm_paged_order (scores, Ids, order) + plan to host + "
-                                          "block tables + paged render, fragments only in the pool"}}
+                                  "what": "cm_paged_order (scores, colliding Ids, order) + plan to "
+                                          "host + block tables + paged render beside "
+                                          "cm_paged_hash_select (other Ids), fragments only in the "
+                                          "pool"}}
     del pool, pset, pr
     torch.cuda.empty_cache()
 

@@ -14,7 +14,8 @@
  *   cm_render_merge_devplan the same with the plan left on the device
  *   cm_render_merge_range   the slots from a given rank on (incremental render)
  *   cm_render_set           steps 2-5 for a set with known Ids, in one call
- *   cm_paged_order / cm_paged_tables / cm_paged_render  steps 1-5 over paged storage
+ *   cm_paged_order / cm_paged_hash_select / cm_paged_tables / cm_paged_render
+ *                           steps 1-5 over paged storage
  * the paper's baselines over the same render:
  *   cm_multiset_order       the naive re-render order of §5.9 (no dedupe)
  *   cm_bag_plan             BagMerge with a caller-supplied order (§4.2)
@@ -349,17 +350,32 @@ typedef struct {
   int64_t n_blocks;
 } cm_pagedset;
 
-/* Steps 1-3 on fragments that live only in the pool: cm_fragment_knorm's keys
- * (keys_dev, n doubles), the Id of every fragment (digests_dev, n * 32 bytes,
+/* Steps 1-3 on fragments that live only in the pool, enqueued with nothing
+ * waiting for the host: cm_fragment_knorm's keys (keys_dev, n doubles), the mask
+ * of cm_equal_key_mask (mask_dev, n bytes: 1 for a delivery whose key equals
+ * another's), the Ids of the deliveries with mask 1 (digests_dev, n * 32 bytes,
  * 16-byte aligned; the same content address as the dense form's: each tensor is
  * hashed in the byte order of its [1, H, T, d] layout, Alg. 2 Id), then
  * cm_canonical_order's dedupe, order and offsets (plan_dev, cm_plan_elems(n)
- * int64), all on the device with nothing waiting for the host. The plan then
- * drives cm_paged_tables and cm_paged_render. routing_layer, tail_len as
+ * int64), which read only those digests. The Ids of the deliveries with mask 0
+ * are not written: compute them with cm_paged_hash_select(mask_dev, 0), e.g.
+ * on another stream beside cm_paged_render. routing_layer, tail_len as
  * cm_fragment_knorm. Workspace: cm_paged_workspace_size() bytes. */
 int32_t cm_paged_order(const cm_pagedset* set, int32_t routing_layer, int64_t tail_len,
-                       double* keys_dev, uint8_t* digests_dev, int64_t* plan_dev, void* workspace,
-                       size_t workspace_bytes, void* stream);
+                       double* keys_dev, uint8_t* mask_dev, uint8_t* digests_dev,
+                       int64_t* plan_dev, void* workspace, size_t workspace_bytes, void* stream);
+
+/* The Id of every paged fragment i with select_dev[i] == select_value (as
+ * cm_fragment_hash_select; the other digests are left untouched).
+ * workgroups_per_cu: the chunk kernel's persistent grid per compute unit, 0 for
+ * the default (4); fewer leave room for a kernel running beside it on another
+ * stream, such as the paged render. It reads the pool and writes only
+ * digests_dev and its workspace, so it may run concurrently with
+ * cm_paged_render over the same set (which writes only fresh pages) if the two
+ * have separate workspaces. Workspace: cm_paged_workspace_size() bytes. */
+int32_t cm_paged_hash_select(const cm_pagedset* set, const uint8_t* select_dev,
+                             int32_t select_value, uint8_t* digests_dev, int32_t workgroups_per_cu,
+                             void* workspace, size_t workspace_bytes, void* stream);
 
 /* Block tables of the merged cache for a plan over the paged fragments (any plan
  * of this file's layout whose slots index the paged set's fragments, e.g. from

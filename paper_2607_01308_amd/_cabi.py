@@ -33,7 +33,8 @@ EXPORTS = (
     "cm_canonical_order", "cm_multiset_order", "cm_bag_plan", "cm_render_merge",
     "cm_render_merge_devplan", "cm_render_merge_range", "cm_render_merge_hash", "cm_render_set",
     "cm_render_deliveries", "cm_render_deliveries_noalloc",
-    "cm_paged_workspace_size", "cm_paged_order", "cm_paged_tables", "cm_paged_render",
+    "cm_paged_workspace_size", "cm_paged_order", "cm_paged_hash_select", "cm_paged_tables",
+    "cm_paged_render",
     "cm_timing_enable", "cm_timing_reset", "cm_timing_query",
 )
 
@@ -119,7 +120,8 @@ def lib() -> ctypes.CDLL:
             "cm_render_deliveries_noalloc": (I32, [FS, I32, I64, ctypes.POINTER(CmRope), P, P, P,
                                                    P, P, I64, P]),
             "cm_paged_workspace_size": (I32, [PS, ctypes.POINTER(SZ)]),
-            "cm_paged_order": (I32, [PS, I32, I64, P, P, P, P, SZ, P]),
+            "cm_paged_order": (I32, [PS, I32, I64, P, P, P, P, P, SZ, P]),
+            "cm_paged_hash_select": (I32, [PS, P, I32, P, I32, P, SZ, P]),
             "cm_paged_tables": (I32, [PS, P, P, I64, P, P, P, ctypes.POINTER(I64)]),
             "cm_paged_render": (I32, [PS, P, P, ctypes.POINTER(CmRope), P, P, P, I64, P, SZ, P]),
             "cm_timing_enable": (I32, [I32]),

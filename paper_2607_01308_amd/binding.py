@@ -307,13 +307,23 @@ def paged_workspace_size(pset: PagedSet) -> int:
 
 
 def paged_order(pset: PagedSet, routing_layer: int, tail_len: int, keys: torch.Tensor,
-                digests: torch.Tensor, plan_dev: torch.Tensor, workspace: torch.Tensor,
-                stream=None) -> None:
-    """cm_paged_order: scores, Ids and the plan of fragments that live in the pool."""
+                mask: torch.Tensor, digests: torch.Tensor, plan_dev: torch.Tensor,
+                workspace: torch.Tensor, stream=None) -> None:
+    """cm_paged_order: scores, the equal-key mask, the Ids the order reads and the
+    plan of fragments that live in the pool."""
     C.check(C.lib().cm_paged_order(ctypes.byref(pset.struct), routing_layer, tail_len,
-                                   _ptr(keys), _ptr(digests), _ptr(plan_dev), _ptr(workspace),
-                                   workspace.numel() * workspace.element_size(),
+                                   _ptr(keys), _ptr(mask), _ptr(digests), _ptr(plan_dev),
+                                   _ptr(workspace), workspace.numel() * workspace.element_size(),
                                    _stream(stream, pset)), "cm_paged_order")
+
+
+def paged_hash_select(pset: PagedSet, select: torch.Tensor, value: int, digests: torch.Tensor,
+                      workspace: torch.Tensor, workgroups_per_cu: int = 0, stream=None) -> None:
+    """cm_paged_hash_select: the Ids of the paged fragments i with select[i] == value."""
+    C.check(C.lib().cm_paged_hash_select(ctypes.byref(pset.struct), _ptr(select), value,
+                                         _ptr(digests), workgroups_per_cu, _ptr(workspace),
+                                         workspace.numel() * workspace.element_size(),
+                                         _stream(stream, pset)), "cm_paged_hash_select")
 
 
 def paged_tables(pset: PagedSet, plan_host: np.ndarray, free_pages):

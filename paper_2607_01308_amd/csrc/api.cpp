@@ -782,8 +782,8 @@ int32_t cm_paged_workspace_size(const cm_pagedset* set, size_t* bytes_out) {
 }
 
 int32_t cm_paged_order(const cm_pagedset* set, int32_t routing_layer, int64_t tail_len,
-                       double* keys_dev, uint8_t* digests_dev, int64_t* plan_dev, void* workspace,
-                       size_t workspace_bytes, void* stream) {
+                       double* keys_dev, uint8_t* mask_dev, uint8_t* digests_dev,
+                       int64_t* plan_dev, void* workspace, size_t workspace_bytes, void* stream) {
   g_err.clear();
   cm::PagedDesc p;
   int32_t st = check_pagedset(set, &p);
@@ -796,17 +796,44 @@ int32_t cm_paged_order(const cm_pagedset* set, int32_t routing_layer, int64_t ta
     return fail(CM_EINVAL, "tail_len must be in [1, min T] = [1, " + std::to_string(tmin) + "], got " +
                                std::to_string(tail_len));
   if (!keys_dev || !aligned(keys_dev, 8)) return fail(CM_EINVAL, "keys_dev is NULL or misaligned");
+  if (!mask_dev) return fail(CM_EINVAL, "mask_dev is NULL");
   if (!digests_dev || !aligned(digests_dev, 16))
     return fail(CM_EINVAL, "digests_dev is NULL or not 16-byte aligned");
   if (!plan_dev || !aligned(plan_dev, 8)) return fail(CM_EINVAL, "plan_dev is NULL or misaligned");
   if ((st = check_ws(workspace, workspace_bytes, paged_ws(p))) != CM_OK) return st;
   uint8_t* ws = static_cast<uint8_t*>(workspace);
   hipStream_t sm = static_cast<hipStream_t>(stream);
+  // scores, the deliveries whose digest the order reads (a key equal to
+  // another's), their Ids, the order; the other Ids are left to
+  // cm_paged_hash_select, which can run beside the render
   hipError_t e = cm::launch_knorm_paged(p, cm::knorm_layout(s, tail_len), routing_layer, tail_len,
                                         keys_dev, ws, sm);
-  if (e == hipSuccess) e = cm::launch_hash_paged(p, cm::hash_layout(s), digests_dev, ws, sm);
+  if (e == hipSuccess) e = cm::launch_equal_key_mask(s, keys_dev, mask_dev, sm);
+  if (e == hipSuccess)
+    e = cm::launch_hash_paged(p, cm::hash_layout(s), mask_dev, 1, digests_dev, ws, sm);
   if (e == hipSuccess) e = cm::launch_order(s, keys_dev, digests_dev, true, plan_dev, sm);
   return e == hipSuccess ? CM_OK : fail_hip(e, "cm_paged_order");
+}
+
+int32_t cm_paged_hash_select(const cm_pagedset* set, const uint8_t* select_dev,
+                             int32_t select_value, uint8_t* digests_dev, int32_t workgroups_per_cu,
+                             void* workspace, size_t workspace_bytes, void* stream) {
+  g_err.clear();
+  cm::PagedDesc p;
+  int32_t st = check_pagedset(set, &p);
+  if (st != CM_OK) return st;
+  if (!digests_dev || !aligned(digests_dev, 16))
+    return fail(CM_EINVAL, "digests_dev is NULL or not 16-byte aligned");
+  if (select_value < 0 || select_value > 255)
+    return fail(CM_EINVAL, "select_value must be in [0, 255]");
+  if (workgroups_per_cu < 0 || workgroups_per_cu > 64)
+    return fail(CM_EINVAL, "workgroups_per_cu must be in [0, 64]");
+  const cm::HashLayout lay = cm::hash_layout(p.s);
+  if ((st = check_ws(workspace, workspace_bytes, lay.bytes)) != CM_OK) return st;
+  hipError_t e = cm::launch_hash_paged(p, lay, select_dev, (uint32_t)select_value, digests_dev,
+                                       static_cast<uint8_t*>(workspace),
+                                       static_cast<hipStream_t>(stream), workgroups_per_cu);
+  return e == hipSuccess ? CM_OK : fail_hip(e, "cm_paged_hash_select");
 }
 
 int32_t cm_paged_tables(const cm_pagedset* set, const int64_t* plan_host, const int32_t* free_host,

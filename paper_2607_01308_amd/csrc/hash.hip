@@ -139,7 +139,8 @@ __global__ __launch_bounds__(kBlock) void paged_hash_chunk_kernel(
     const uint8_t* __restrict__ pool, int64_t P, int32_t H, int32_t b_shift, int32_t rb_shift,
     const int64_t* __restrict__ table, const int32_t* __restrict__ blocks, int32_t n,
     int64_t token_bytes, const int64_t* __restrict__ base0, const int64_t* __restrict__ task_base,
-    int64_t total_tasks, uint8_t* __restrict__ nodes) {
+    int64_t total_tasks, const uint8_t* __restrict__ select, uint32_t want,
+    uint8_t* __restrict__ nodes) {
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform per wave
   const int64_t waves = (int64_t)gridDim.x * (kBlock / 64);
@@ -148,6 +149,7 @@ __global__ __launch_bounds__(kBlock) void paged_hash_chunk_kernel(
   for (int64_t task = (int64_t)blockIdx.x * (kBlock / 64) + wave; task < total_tasks;
        task += waves) {
     const int i = find_fragment(task_base, n, task);
+    if (select && select[i] != want) continue;
     const int64_t T = table[2 * (int64_t)i];
     const int64_t first = table[2 * (int64_t)i + 1];
     const int64_t bytes = T * token_bytes;
@@ -577,8 +579,9 @@ hipError_t launch_hash(const SetDesc& s, const HashLayout& lay, const uint8_t* s
   return launch_hash_tree(s, lay, select, want, digests, ws, stream);
 }
 
-hipError_t launch_hash_paged(const PagedDesc& p, const HashLayout& lay, uint8_t* digests,
-                             uint8_t* ws, hipStream_t stream) {
+hipError_t launch_hash_paged(const PagedDesc& p, const HashLayout& lay, const uint8_t* select,
+                             uint32_t want, uint8_t* digests, uint8_t* ws, hipStream_t stream,
+                             int blocks_per_cu) {
   const SetDesc& s = p.s;
   hipError_t e = launch_hash_prep(s, lay, ws, stream);
   if (e != hipSuccess) return e;
@@ -587,16 +590,18 @@ hipError_t launch_hash_paged(const PagedDesc& p, const HashLayout& lay, uint8_t*
     const int64_t nb1 = s.n + 1;
     ScopedTiming tm(K_HASH_LEAF, stream);
     const int64_t full = (lay.tasks + (kBlock / 64) - 1) / (kBlock / 64);
-    const int64_t cap = (int64_t)device_cu_count() * kLeafBlocksPerCu;
+    const int64_t cap =
+        (int64_t)device_cu_count() * (blocks_per_cu > 0 ? blocks_per_cu : kLeafBlocksPerCu);
     const int64_t grid = full < cap ? full : cap;
     hipLaunchKernelGGL(paged_hash_chunk_kernel, dim3((uint32_t)grid), dim3(kBlock), 0, stream,
                        static_cast<const uint8_t*>(p.pool), p.pages, s.H, p.b_shift,
                        (int32_t)__builtin_ctzll((unsigned long long)s.row_bytes), s.table_dev,
                        p.blocks_dev, s.n, token_bytes_of(s), base,
-                       base + (int64_t)(lay.levels + 1) * nb1, lay.tasks, ws + lay.off_buf0);
+                       base + (int64_t)(lay.levels + 1) * nb1, lay.tasks, select, want,
+                       ws + lay.off_buf0);
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  return launch_hash_tree(s, lay, nullptr, 0, digests, ws, stream);
+  return launch_hash_tree(s, lay, select, want, digests, ws, stream);
 }
 
 }  // namespace cm

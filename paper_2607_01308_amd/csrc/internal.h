@@ -209,8 +209,11 @@ struct PagedDesc {
 // byte order of its dense layout).
 hipError_t launch_knorm_paged(const PagedDesc& p, const KnormLayout& lay, int32_t layer,
                               int64_t tail_len, double* keys, uint8_t* ws, hipStream_t stream);
-hipError_t launch_hash_paged(const PagedDesc& p, const HashLayout& lay, uint8_t* digests,
-                             uint8_t* ws, hipStream_t stream);
+// select as launch_hash; blocks_per_cu > 0 caps the chunk kernel's persistent
+// grid (fewer workgroups leave room for a kernel running beside it).
+hipError_t launch_hash_paged(const PagedDesc& p, const HashLayout& lay, const uint8_t* select,
+                             uint32_t want, uint8_t* digests, uint8_t* ws, hipStream_t stream,
+                             int blocks_per_cu = 0);
 hipError_t launch_paged_render(const PagedDesc& p, const int64_t* plan_dev, int32_t n_unique,
                                double base, int32_t style, const int32_t* k_table,
                                const int32_t* v_table, const int32_t* fresh, int64_t n_fresh,

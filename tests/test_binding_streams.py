@@ -110,7 +110,7 @@ def test_every_enqueuing_call_is_covered():
     render is checked separately below)."""
     takes_stream = {name for name, f in inspect.getmembers(binding, inspect.isfunction)
                     if "stream" in inspect.signature(f).parameters and not name.startswith("_")}
-    assert takes_stream == set(CALLS) | {"paged_render", "paged_order"}
+    assert takes_stream == set(CALLS) | {"paged_render", "paged_order", "paged_hash_select"}
 
 
 @pytest.mark.parametrize("name", sorted(CALLS))
@@ -135,9 +135,13 @@ def test_paged_render_marks_both_tables(fake_lib):
 def test_paged_order_marks_both_tables(fake_lib):
     pset = _owner(2)
     s = FakeStream(44)
-    binding.paged_order(pset, 0, 1, T, T, T, T, s)
+    binding.paged_order(pset, 0, 1, T, T, T, T, T, s)
     assert [t.streams for t in pset.device_tables] == [[s], [s]]
     assert fake_lib.calls[-1][1].value == 44
+    s2 = FakeStream(45)
+    binding.paged_hash_select(pset, T, 0, T, T, 2, s2)
+    assert [t.streams for t in pset.device_tables] == [[s, s2], [s, s2]]
+    assert fake_lib.calls[-1][1].value == 45
 
 
 def test_scratch_is_cached_per_stream(monkeypatch):

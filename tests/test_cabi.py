@@ -451,8 +451,10 @@ def test_paged_order_argument_checks(lib):
     keys, dig, plan = ctypes.c_void_p(0x30000), ctypes.c_void_p(0x40000), ctypes.c_void_p(0x50000)
     ws = ctypes.c_void_p(0x60000)
 
-    def call(layer=1, tail=30, keys=keys, dig=dig, plan=plan, ws_bytes=need.value):
-        return lib.cm_paged_order(fp.ref, layer, tail, keys, dig, plan, ws, ws_bytes, None)
+    mask = ctypes.c_void_p(0x70000)
+
+    def call(layer=1, tail=30, keys=keys, mask=mask, dig=dig, plan=plan, ws_bytes=need.value):
+        return lib.cm_paged_order(fp.ref, layer, tail, keys, mask, dig, plan, ws, ws_bytes, None)
 
     assert call(ws_bytes=0) == C.CM_EWORKSPACE             # every other check passed
     assert call(layer=2) == C.CM_EINVAL
@@ -461,5 +463,11 @@ def test_paged_order_argument_checks(lib):
     assert call(keys=None) == C.CM_EINVAL
     assert call(dig=ctypes.c_void_p(0x40008)) == C.CM_EINVAL
     assert call(plan=None) == C.CM_EINVAL
+    assert call(mask=None) == C.CM_EINVAL
+    h = lib.cm_paged_hash_select
+    assert h(fp.ref, mask, 0, dig, 0, ws, 0, None) == C.CM_EWORKSPACE   # every other check passed
+    assert h(fp.ref, mask, 0, ctypes.c_void_p(0x40008), 0, ws, need.value, None) == C.CM_EINVAL
+    assert h(fp.ref, mask, 256, dig, 0, ws, need.value, None) == C.CM_EINVAL
+    assert h(fp.ref, mask, 0, dig, 65, ws, need.value, None) == C.CM_EINVAL
     fp.blocks[0] = fp.P                                     # a page id outside the pool
     assert call() == C.CM_EINVAL
