@@ -158,6 +158,7 @@ def cpu_baseline(w, frags):
     workload, on the cores the process may use (a thread pool over (layer,
     fragment) tasks, at most 16 threads: a GPU host's share per GPU) and on one
     thread."""
+    import numpy as np
     import oracle
     import synth
     idx = sorted(range(w.n_distinct), key=lambda i: w.lengths[i])[:5]
@@ -180,6 +181,8 @@ def cpu_baseline(w, frags):
         "value_1thread": round(nbytes / dt_one / 1e9, 4),
         "cores_allowed": allowed,
         "model": _cpu_model(),
+        "numpy": np.__version__,
+        "python": sys.version.split()[0],
         "sample_bytes": nbytes,
         "sample": f"full path (Id of every fragment, score, order, render) over the 5 shortest "
                   f"distinct fragments (T={[w.lengths[i] for i in idx]}, {nbytes / 1e9:.2f} GB "
