@@ -10,7 +10,11 @@
 // compression. The work is VALU-bound (12 VALU ops per G step, 672 per block);
 // the tree above the chunks takes one launch per three levels over all tensors
 // at full lane occupancy (the parents add 1/16 of the chunk work) until at most
-// nine levels remain, then one launch folds the top of every tensor's tree.
+// nine levels remain, then one launch folds the top of every tensor's tree (and,
+// for a small set, computes each fragment's Id in its last workgroup; otherwise
+// one more launch does). Fragments stored in a page pool are hashed by a chunk
+// kernel that walks each chunk's blocks through the page list in the order of
+// the dense layout, so the Id does not depend on the storage.
 #include "chunk_ops.h"
 #include "key_mask.h"
 #include "knorm_fold.h"

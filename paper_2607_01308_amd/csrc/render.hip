@@ -12,8 +12,8 @@
 // that a wave's data load waits on two scalar loads only: the slot of its unit
 // (every row block has the same row -> slot map) and the source base of that
 // slot in its row block (render_tables.h). A unit crossing a slot boundary
-// resolves the slot per lane. K at a non-zero offset is rotated with the partner piece fetched from
-// the lane P pieces away.
+// resolves the slot per lane. K at a non-zero offset is rotated with the
+// partner piece fetched from the lane P pieces away.
 #include "render_geometry.h"
 #include "render_tables.h"
 
