@@ -440,27 +440,37 @@ def main():
     cm.timing_reset()
     # steps 1-5 on the pool alone: scores, the colliding deliveries' Ids and the
     # order on the device, the plan to the host, block tables, then the render of
-    # the fresh pages with the other Ids hashed beside it on a second stream (a
-    # second read of every fragment byte: the paged hash is not fused into the
-    # paged render)
-    for _ in range(2):
-        ps = cm.render_paged_set(pset, w.routing_layer, w.rope_base, free)
-    torch.cuda.synchronize()
-    cm.timing_reset()
-    cm.timing_enable(True)
-    tp = time.perf_counter()
-    for _ in range(args.steps):
-        ps = cm.render_paged_set(pset, w.routing_layer, w.rope_base, free)
-    torch.cuda.synchronize()
-    ms_paged_set = (time.perf_counter() - tp) / args.steps * 1e3
-    cm.timing_enable(False)
-    paged_set_kernels = {}
-    for k in cm.KERNELS:
-        kms, kn = cm.timing_query(k)
-        if kn:
-            paged_set_kernels[k] = round(kms / args.steps, 4)
-    cm.timing_reset()
+    # the merged rows no fragment page holds with the other Ids from the same
+    # loads (fused, cm_paged_render_hash); and, beside it, the earlier two-kernel
+    # form: the paged render with the other Ids hashed beside it on a second
+    # stream (every fragment byte read twice)
+    def paged_set_steps(fused):
+        for _ in range(2):
+            ps = cm.render_paged_set(pset, w.routing_layer, w.rope_base, free, fused=fused)
+        torch.cuda.synchronize()
+        cm.timing_reset()
+        cm.timing_enable(True)
+        tp = time.perf_counter()
+        for _ in range(args.steps):
+            ps = cm.render_paged_set(pset, w.routing_layer, w.rope_base, free, fused=fused)
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - tp) / args.steps * 1e3
+        cm.timing_enable(False)
+        kernels = {}
+        for k in cm.KERNELS:
+            kms, kn = cm.timing_query(k)
+            if kn:
+                kernels[k] = round(kms / args.steps, 4)
+        cm.timing_reset()
+        return ms, kernels, ps
+
+    ms_paged_set, paged_set_kernels, ps = paged_set_steps(True)
     paged_set_equal = bool(np.array_equal(ps.plan, set_plan))
+    fused_ids = ps.digests_dev.cpu().numpy()
+    del ps
+    ms_paged_two, paged_two_kernels, ps = paged_set_steps(False)
+    paged_two_equal = bool(np.array_equal(ps.plan, set_plan)) and bool(
+        np.array_equal(ps.digests_dev.cpu().numpy(), fused_ids))
     del ps
     page_bytes = w.L * w.H * B * w.d * (2 if w.dtype == "bfloat16" else 4)
     paged_bytes = 2 * len(pr.fresh) * page_bytes
@@ -473,9 +483,14 @@ def main():
              "set_steps_1_to_5": {"ms": round(ms_paged_set, 4), "kernels_ms": paged_set_kernels,
                                   "plan_equals_dense_set_plan": paged_set_equal,
                                   "what": "cm_paged_order (scores, colliding Ids, order) + plan to "
-                                          "host + block tables + paged render beside "
-                                          "cm_paged_hash_select (other Ids), fragments only in the "
-                                          "pool"}}
+                                          "host + block tables + cm_paged_render_hash (render and "
+                                          "the other Ids from one read), fragments only in the "
+                                          "pool"},
+             "set_steps_1_to_5_two_kernels": {
+                 "ms": round(ms_paged_two, 4), "kernels_ms": paged_two_kernels,
+                 "plan_and_ids_equal_fused": paged_two_equal,
+                 "what": "as set_steps_1_to_5 with cm_paged_render and cm_paged_hash_select on "
+                         "a second stream in place of the fused kernel"}}
     del pool, pset, pr
     torch.cuda.empty_cache()
 

@@ -14,8 +14,8 @@
  *   cm_render_merge_devplan the same with the plan left on the device
  *   cm_render_merge_range   the slots from a given rank on (incremental render)
  *   cm_render_set           steps 2-5 for a set with known Ids, in one call
- *   cm_paged_order / cm_paged_hash_select / cm_paged_tables / cm_paged_render
- *                           steps 1-5 over paged storage
+ *   cm_paged_order / cm_paged_hash_select / cm_paged_tables / cm_paged_render /
+ *   cm_paged_render_hash    steps 1-5 over paged storage
  * the paper's baselines over the same render:
  *   cm_multiset_order       the naive re-render order of §5.9 (no dedupe)
  *   cm_bag_plan             BagMerge with a caller-supplied order (§4.2)
@@ -405,6 +405,30 @@ int32_t cm_paged_render(const cm_pagedset* set, const int64_t* plan_dev, const i
                         const cm_rope* rope, const int32_t* k_table_dev,
                         const int32_t* v_table_dev, const int32_t* fresh_dev, int64_t n_fresh,
                         void* workspace, size_t workspace_bytes, void* stream);
+/* Steps 1 and 4-5 in one pass over paged storage (§4.5; Alg. 2 Id; Eq. (1)-(2)),
+ * the paged counterpart of cm_render_merge_hash: every row of the plan's merged
+ * cache whose page in the block tables is not the page it is read from is
+ * written there (K of a slot at offset s rotated by R(s), V copied), rows in a
+ * reused fragment page stay in place, rows past T_out in the last page are left
+ * untouched; from the same loads, the Id of every slot delivery i with
+ * select_dev[i] == 0 is written to digests_dev (the others are left untouched;
+ * with the mask of cm_paged_order, the deliveries whose Id it did not compute).
+ * The result equals cm_paged_render with the same tables plus
+ * cm_paged_hash_select(select_dev, 0), with each byte read once.
+ * k_table_host / v_table_host: the block tables (ceil(T_out / B) page ids each,
+ * e.g. from cm_paged_tables), checked on the host: every entry a page of the
+ * pool, a fragment page only where cm_paged_tables would reuse it, no other
+ * page twice (CM_EINVAL otherwise); k_table_dev / v_table_dev: their device
+ * copies, read by the kernel. select_dev: device, n bytes; digests_dev: n * 32
+ * bytes, 16-byte aligned. plan_dev / plan_host as in cm_render_merge.
+ * P * H * B must not exceed 2^32 - 1 (CM_ESHAPE; the kernel names a pool row
+ * with 32 bits). Workspace: cm_paged_workspace_size() bytes. */
+int32_t cm_paged_render_hash(const cm_pagedset* set, const int64_t* plan_dev,
+                             const int64_t* plan_host, const cm_rope* rope,
+                             const int32_t* k_table_host, const int32_t* v_table_host,
+                             const int32_t* k_table_dev, const int32_t* v_table_dev,
+                             const uint8_t* select_dev, uint8_t* digests_dev, void* workspace,
+                             size_t workspace_bytes, void* stream);
 int32_t cm_paged_workspace_size(const cm_pagedset* set, size_t* bytes_out);
 
 /* ---------------------------------------------------------------- timing
@@ -414,7 +438,7 @@ int32_t cm_paged_workspace_size(const cm_pagedset* set, size_t* bytes_out);
  * to the per-kernel totals and returns the total milliseconds and launch count
  * for one kernel name ("hash_prep", "hash_leaf", "hash_parent", "hash_final",
  * "knorm_rows", "knorm_tree", "order", "key_mask", "render_prep", "render",
- * "render_hash"). */
+ * "render_hash", "paged", "paged_hash_render"). */
 int32_t cm_timing_enable(int32_t on);
 int32_t cm_timing_reset(void);
 int32_t cm_timing_query(const char* kernel, double* total_ms, int64_t* launches);

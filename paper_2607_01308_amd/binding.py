@@ -261,7 +261,8 @@ def timing_query(kernel: str):
 
 
 KERNELS = ("hash_prep", "hash_leaf", "hash_parent", "hash_final", "knorm_rows", "knorm_tree",
-           "order", "key_mask", "render_prep", "render", "render_hash", "paged")
+           "order", "key_mask", "render_prep", "render", "render_hash", "paged",
+           "paged_hash_render")
 
 
 class PagedSet:
@@ -324,6 +325,29 @@ def paged_hash_select(pset: PagedSet, select: torch.Tensor, value: int, digests:
                                          _ptr(digests), workgroups_per_cu, _ptr(workspace),
                                          workspace.numel() * workspace.element_size(),
                                          _stream(stream, pset)), "cm_paged_hash_select")
+
+
+def paged_render_hash(pset: PagedSet, plan_dev: torch.Tensor, plan_host: np.ndarray,
+                      rope_base: float, style: str, k_table_host: np.ndarray,
+                      v_table_host: np.ndarray, k_table: torch.Tensor, v_table: torch.Tensor,
+                      select: torch.Tensor, digests: torch.Tensor, workspace: torch.Tensor,
+                      stream=None) -> None:
+    """cm_paged_render_hash: the merged cache into the pages of the block tables
+    (host arrays for the check, device copies for the kernel) and, from the same
+    loads, the Ids of the slot deliveries i with select[i] == 0."""
+    plan_host = np.ascontiguousarray(plan_host, dtype=np.int64)
+    kh = np.ascontiguousarray(k_table_host, dtype=np.int32)
+    vh = np.ascontiguousarray(v_table_host, dtype=np.int32)
+    rope = C.CmRope(base=float(rope_base), style=_STYLES[style], reserved=0)
+    C.check(C.lib().cm_paged_render_hash(ctypes.byref(pset.struct), _ptr(plan_dev),
+                                         plan_host.ctypes.data_as(ctypes.c_void_p),
+                                         ctypes.byref(rope),
+                                         kh.ctypes.data_as(ctypes.c_void_p),
+                                         vh.ctypes.data_as(ctypes.c_void_p), _ptr(k_table),
+                                         _ptr(v_table), _ptr(select), _ptr(digests),
+                                         _ptr(workspace),
+                                         workspace.numel() * workspace.element_size(),
+                                         _stream(stream, pset)), "cm_paged_render_hash")
 
 
 def paged_tables(pset: PagedSet, plan_host: np.ndarray, free_pages):

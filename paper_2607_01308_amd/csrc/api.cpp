@@ -139,7 +139,8 @@ int64_t min_T(const cm::SetDesc& s) {
 // ------------------------------------------------------------------ timing registry
 const char* const kKernelNames[cm::K_COUNT] = {
     "hash_prep", "hash_leaf", "hash_parent", "hash_final", "knorm_rows", "knorm_tree",
-    "order",     "key_mask",  "render_prep", "render",     "render_hash", "paged"};
+    "order",     "key_mask",  "render_prep", "render",     "render_hash", "paged",
+    "paged_hash_render"};
 std::atomic<bool> g_timing{false};
 std::mutex g_tmu;
 struct Pending {
@@ -734,14 +735,22 @@ size_t paged_render_ws(const cm::PagedDesc& p) {
          cm::align_up(32 * 2 * (size_t)blocks, cm::kWsAlign);
 }
 
-// Every paged call fits: the render's, or the scores' and Ids' of
-// cm_paged_order (which run one after the other over the same bytes).
+// Workspace of the paged hash + render: the hash layout, then the render's.
+size_t paged_fused_ws(const cm::PagedDesc& p) {
+  return cm::align_up(cm::hash_layout(p.s).bytes, cm::kWsAlign) + cm::render_layout(p.s).bytes;
+}
+
+// Every paged call fits: the render's, the fused hash + render's, or the
+// scores' and Ids' of cm_paged_order (which run one after the other over the
+// same bytes).
 size_t paged_ws(const cm::PagedDesc& p) {
   size_t need = paged_render_ws(p);
   const size_t kn = cm::knorm_max_bytes(p.s);
   const size_t hb = cm::hash_layout(p.s).bytes;
+  const size_t fu = paged_fused_ws(p);
   if (kn > need) need = kn;
   if (hb > need) need = hb;
+  if (fu > need) need = fu;
   return need;
 }
 
@@ -764,6 +773,60 @@ int32_t check_plan_host(const cm::SetDesc& s, const int64_t* plan_host, int64_t*
   }
   if (plan_host[CM_PLAN_TOUT] != off) return fail(CM_ESHAPE, "plan T_out is not the sum of lengths");
   *nu_out = nu;
+  return CM_OK;
+}
+
+// Merged block j of a plan's cache (rows [jB, min(jB + B, T_out))) can keep a
+// fragment page, with no copy, when all its rows come from one slot and start at
+// a page boundary of that slot's fragment: that page (-1 if none), and whether
+// the slot is at offset 0 (K pages only then: R(0) = I). s: the slot holding
+// row jB, advanced from the previous block's.
+struct Reuse {
+  int32_t page;
+  bool k_too;
+};
+Reuse reusable_page(const cm_pagedset* set, const int64_t* plan_host, int64_t nu, int64_t j,
+                    int64_t* s) {
+  const int64_t n = set->n, B = set->block;
+  const int64_t T_out = plan_host[CM_PLAN_TOUT];
+  const int64_t r0 = j * B, e = std::min(r0 + B, T_out);
+  while (*s + 1 < nu && plan_host[CM_PLAN_HEADER + n + *s + 1] <= r0) ++*s;
+  const int64_t i = plan_host[CM_PLAN_HEADER + *s];
+  const int64_t off = plan_host[CM_PLAN_HEADER + n + *s];
+  const int64_t T = plan_host[CM_PLAN_HEADER + 2 * n + *s];
+  const bool whole_page = e <= off + T && (r0 - off) % B == 0;
+  Reuse r;
+  r.page = whole_page ? set->blocks_host[set->table_host[2 * i + 1] + (r0 - off) / B] : -1;
+  r.k_too = off == 0;
+  return r;
+}
+
+// Block tables given by the caller for a render that writes every row whose
+// merged page is not the page it is read from: every entry a page of the pool;
+// a fragment page only where reusable_page allows it (then it is that page);
+// every other page used once.
+int32_t check_block_tables(const cm_pagedset* set, const int64_t* plan_host, int64_t nu,
+                           const int32_t* k_table_host, const int32_t* v_table_host) {
+  if (!k_table_host || !v_table_host) return fail(CM_EINVAL, "k_table_host / v_table_host NULL");
+  std::vector<uint8_t> used((size_t)set->pages, 0);
+  for (int64_t k = 0; k < set->n_blocks; ++k) used[(size_t)set->blocks_host[k]] = 1;
+  const int64_t nbo = (plan_host[CM_PLAN_TOUT] + set->block - 1) / set->block;
+  int64_t s = 0;
+  for (int64_t j = 0; j < nbo; ++j) {
+    const Reuse r = reusable_page(set, plan_host, nu, j, &s);
+    for (int kv = 0; kv < 2; ++kv) {
+      const int32_t q = (kv ? v_table_host : k_table_host)[j];
+      const std::string where = std::string(kv ? "v" : "k") + "_table[" + std::to_string(j) + "]";
+      if (q < 0 || q >= set->pages) return fail(CM_EINVAL, where + " is outside the pool");
+      if (used[(size_t)q] == 1) {
+        if (q != r.page || (kv == 0 && !r.k_too))
+          return fail(CM_EINVAL, where + " is a fragment page that this block cannot reuse");
+      } else {
+        if (used[(size_t)q] == 2) return fail(CM_EINVAL, where + " repeats a page");
+        used[(size_t)q] = 2;
+      }
+    }
+  }
   return CM_OK;
 }
 
@@ -858,24 +921,17 @@ int32_t cm_paged_tables(const cm_pagedset* set, const int64_t* plan_host, const 
                                  " is outside the pool, repeated or holds a fragment page");
     used[(size_t)q] = 2;
   }
-  const int64_t n = p.s.n, B = p.block;
+  const int64_t B = p.block;
   const int64_t T_out = plan_host[CM_PLAN_TOUT];
   const int64_t nbo = (T_out + B - 1) / B;
   int64_t taken = 0, count = 0;
   int64_t s = 0;                                   // slot holding row j * B
   for (int64_t j = 0; j < nbo; ++j) {
-    const int64_t r0 = j * B, e = std::min(r0 + B, T_out);
-    while (s + 1 < nu && plan_host[CM_PLAN_HEADER + n + s + 1] <= r0) ++s;
-    const int64_t i = plan_host[CM_PLAN_HEADER + s];
-    const int64_t off = plan_host[CM_PLAN_HEADER + n + s];
-    const int64_t T = plan_host[CM_PLAN_HEADER + 2 * n + s];
-    const bool whole_page = e <= off + T && (r0 - off) % B == 0;
-    const int32_t page = whole_page ? set->blocks_host[set->table_host[2 * i + 1] + (r0 - off) / B]
-                                    : -1;
+    const Reuse r = reusable_page(set, plan_host, nu, j, &s);
     for (int kv = 0; kv < 2; ++kv) {
       int32_t* tab = kv ? v_table_host : k_table_host;
-      if (whole_page && (kv == 1 || off == 0)) {
-        tab[j] = page;
+      if (r.page >= 0 && (kv == 1 || r.k_too)) {
+        tab[j] = r.page;
       } else {
         tab[j] = taken < n_free ? free_host[taken] : -1;
         ++taken;
@@ -919,6 +975,38 @@ int32_t cm_paged_render(const cm_pagedset* set, const int64_t* plan_dev, const i
                                          static_cast<uint8_t*>(workspace),
                                          static_cast<hipStream_t>(stream));
   return e == hipSuccess ? CM_OK : fail_hip(e, "cm_paged_render");
+}
+
+int32_t cm_paged_render_hash(const cm_pagedset* set, const int64_t* plan_dev,
+                             const int64_t* plan_host, const cm_rope* rope,
+                             const int32_t* k_table_host, const int32_t* v_table_host,
+                             const int32_t* k_table_dev, const int32_t* v_table_dev,
+                             const uint8_t* select_dev, uint8_t* digests_dev, void* workspace,
+                             size_t workspace_bytes, void* stream) {
+  g_err.clear();
+  cm::PagedDesc p;
+  int32_t st = check_pagedset(set, &p);
+  if (st != CM_OK) return st;
+  if ((uint64_t)set->pages * (uint64_t)set->H * (uint64_t)set->block > 0xFFFFFFFFull)
+    return fail(CM_ESHAPE, "pages * H * block must be below 2^32 for the fused paged render");
+  if ((st = check_rope(rope)) != CM_OK) return st;
+  int64_t nu = 0;
+  if ((st = check_plan_host(p.s, plan_host, &nu)) != CM_OK) return st;
+  if (!plan_dev || !aligned(plan_dev, 8)) return fail(CM_EINVAL, "plan_dev is NULL or misaligned");
+  if ((st = check_block_tables(set, plan_host, nu, k_table_host, v_table_host)) != CM_OK) return st;
+  if (!k_table_dev || !v_table_dev || !aligned(k_table_dev, 4) || !aligned(v_table_dev, 4))
+    return fail(CM_EINVAL, "k_table_dev / v_table_dev NULL or misaligned");
+  if (!select_dev) return fail(CM_EINVAL, "select_dev is NULL");
+  if (!digests_dev || !aligned(digests_dev, 16))
+    return fail(CM_EINVAL, "digests_dev is NULL or not 16-byte aligned");
+  if ((st = check_ws(workspace, workspace_bytes, paged_fused_ws(p))) != CM_OK) return st;
+  const cm::HashLayout hlay = cm::hash_layout(p.s);
+  const cm::RenderLayout rlay = cm::render_layout(p.s);
+  hipError_t e = cm::launch_paged_render_hash(p, hlay, rlay, plan_dev, rope->base, rope->style,
+                                              select_dev, k_table_dev, v_table_dev, digests_dev,
+                                              static_cast<uint8_t*>(workspace),
+                                              static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? CM_OK : fail_hip(e, "cm_paged_render_hash");
 }
 
 int32_t cm_timing_enable(int32_t on) {

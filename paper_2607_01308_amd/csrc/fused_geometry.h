@@ -72,4 +72,61 @@ __host__ __device__ __forceinline__ void fused_next_row(P& dst, int64_t& left, i
   left = wrap ? T : left;
 }
 
+
+// Paged storage: a pool [L][2][P][H][B][RB] of pages of B rows of every head,
+// fragment row tr of head h in row tr % B of page blocks[first + tr / B]. The
+// paged fused kernel names a pool row by its index in the (layer, K/V) slice of
+// the pool, (page * H + h) * B + row (the caller keeps P * H * B below 2^32 - 1),
+// so that a row is 4 bytes of a wave's LDS table.
+constexpr uint32_t kPagedSkipRow = 0xFFFFFFFFu;   // a row that is not written
+
+struct ChunkRow {
+  int64_t h;    // head
+  int64_t tr;   // row of that head, in [0, T)
+};
+
+// Head and row of the first row of lane `lane`'s chunk in stripe sidx of a
+// tensor of H * T rows of 2^rb_shift bytes (the chunk's row 0; it exists when
+// the lane's chunk holds at least one block).
+__host__ __device__ __forceinline__ ChunkRow fused_chunk_row(int64_t sidx, int lane, int rb_shift,
+                                                             int64_t T) {
+  const int64_t rpc = (int64_t)1024 >> rb_shift;
+  const int64_t r0 = sidx * 64 * rpc;
+  const int64_t h0 = r0 / T;
+  const int64_t rel = r0 - h0 * T + (int64_t)lane * rpc;
+  int64_t dh;
+  if (T > 64 * rpc) dh = rel >= T ? 1 : 0;           // rel < 2T
+  else dh = (int64_t)((uint32_t)rel / (uint32_t)T);  // rel < 2048
+  ChunkRow c;
+  c.h = h0 + dh;
+  c.tr = rel - dh * T;
+  return c;
+}
+
+__host__ __device__ __forceinline__ void fused_chunk_next(ChunkRow& c, int64_t T) {
+  if (++c.tr == T) {
+    c.tr = 0;
+    ++c.h;
+  }
+}
+
+// Pool rows of row c of a slot at merged offset `off` whose fragment's page
+// list starts at blocks[first]: where it is read (*src) and where the merged
+// cache holds it (*dst: row off + tr of head h, in page tab[(off + tr) / B] of
+// the merged K or V block table), or kPagedSkipRow for a row whose merged page
+// is the page it is read from (a reused page: its bytes are already in place)
+// or not a page of the pool.
+__host__ __device__ __forceinline__ void paged_row_pair(const int32_t* blocks, int64_t first,
+                                                        const int32_t* tab, int64_t P, int64_t H,
+                                                        int b_shift, int64_t off, ChunkRow c,
+                                                        uint32_t* src, uint32_t* dst) {
+  const int64_t bmask = ((int64_t)1 << b_shift) - 1;
+  const int64_t page = blocks[first + (c.tr >> b_shift)];
+  *src = (uint32_t)(((page * H + c.h) << b_shift) + (c.tr & bmask));
+  const int64_t m = off + c.tr;
+  const int64_t out = tab[m >> b_shift];
+  *dst = (out == page || out < 0 || out >= P) ? kPagedSkipRow
+                                              : (uint32_t)(((out * H + c.h) << b_shift) + (m & bmask));
+}
+
 }  // namespace cm

@@ -214,6 +214,16 @@ hipError_t launch_knorm_paged(const PagedDesc& p, const KnormLayout& lay, int32_
 hipError_t launch_hash_paged(const PagedDesc& p, const HashLayout& lay, const uint8_t* select,
                              uint32_t want, uint8_t* digests, uint8_t* ws, hipStream_t stream,
                              int blocks_per_cu = 0);
+// Steps 1 and 4-5 in one pass over paged storage: the render of the fragment
+// rows into the pages of the merged K and V block tables (rows whose merged
+// page is the page they are read from are left in place) and, for the slot
+// deliveries with select[i] == 0, their Ids (hsel as launch_render_hash).
+// Workspace: the hash layout, then the render layout (launch_render_hash's).
+hipError_t launch_paged_render_hash(const PagedDesc& p, const HashLayout& hlay,
+                                    const RenderLayout& rlay, const int64_t* plan_dev, double base,
+                                    int32_t style, const uint8_t* select, const int32_t* k_table,
+                                    const int32_t* v_table, uint8_t* digests, uint8_t* ws,
+                                    hipStream_t stream);
 hipError_t launch_paged_render(const PagedDesc& p, const int64_t* plan_dev, int32_t n_unique,
                                double base, int32_t style, const int32_t* k_table,
                                const int32_t* v_table, const int32_t* fresh, int64_t n_fresh,
@@ -246,6 +256,7 @@ enum KernelId {
   K_RENDER,
   K_RENDER_HASH,
   K_PAGED,
+  K_PAGED_HASH_RENDER,
   K_COUNT
 };
 

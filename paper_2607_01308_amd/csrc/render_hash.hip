@@ -103,19 +103,117 @@ __device__ __forceinline__ void pair_angles(const double* __restrict__ table, in
 constexpr int kStageLane = 144;
 constexpr int kStageBytes = 64 * kStageLane;
 
-// ESIZE: element bytes; STYLE: pairing; RB: row bytes (64 .. 1024).
-template <int ESIZE, int STYLE, int RB>
-__global__ __launch_bounds__(kThreads) CM_FUSED_OCCUPANCY void render_hash_kernel(
-    const int64_t* __restrict__ table, int64_t stride, int32_t n, const int64_t* __restrict__ plan,
+// Where a task's lanes read and write. A task's address state gives s(b), the
+// address of block b of the lane's chunk; d(pos), that of block pos of the
+// lane's current output row (nullptr: the row is not written); next_row().
+//
+// Dense: fragment tensors are contiguous [H][T][row] and the merged cache is
+// [2L][H][T_out][row]; a lane's chunk is 1 KiB of consecutive bytes and it
+// walks its rows into the merged cache.
+template <int RB>
+struct DenseTask {
+  static constexpr bool kSkips = false;
+  const uint8_t* src;     // the lane's chunk
+  uint8_t* dst;           // the lane's current row in the merged cache
+  int64_t left, T, gap;
+  __device__ __forceinline__ const uint8_t* s(int b) const { return src + b * 64; }
+  __device__ __forceinline__ uint8_t* d(int pos) const { return dst + pos * 64; }
+  __device__ __forceinline__ void next_row() { fused_next_row(dst, left, T, gap, RB); }
+};
+
+struct DenseAddr {
+  const int64_t* table;   // per fragment: a row of `stride` int64, tensor pointers from entry 1
+  int64_t stride;
+  uint8_t* out;
+  template <int RB>
+  __device__ __forceinline__ DenseTask<RB> task(int64_t i, int64_t t, int64_t sidx, int64_t off,
+                                                int64_t T, int64_t T_out, int32_t H,
+                                                int64_t bytes, int lane, int) const {
+    constexpr int RB_SHIFT = __builtin_ctz(RB);
+    const FusedLane fl = fused_lane(bytes, sidx, lane, RB_SHIFT, T, T_out, off);
+    DenseTask<RB> a;
+    a.src = reinterpret_cast<const uint8_t*>(table[i * stride + 1 + t]) + fl.src;
+    a.dst = out + t * (int64_t)H * T_out * RB + fl.dst;
+    a.left = fl.left;
+    a.T = T;
+    a.gap = (T_out - T) << RB_SHIFT;   // end of a head's rows -> next head
+    return a;
+  }
+};
+
+// Paged: fragments and the merged cache on pages of a pool (fused_geometry.h).
+// At the start of a task each lane resolves the RPC rows of its chunk, where
+// each is read and where it goes, into its column of the wave's LDS table
+// (entry j * 64 + lane: source row j; (RPC + j) * 64 + lane: destination).
+template <int RB>
+struct PagedTask {
+  static constexpr bool kSkips = true;
+  static constexpr int RPC = 1024 / RB;
+  static constexpr int BPR = RB / 64;
+  static constexpr int RB_SHIFT = __builtin_ctz(RB);
+  uint8_t* slice;          // the tensor's (layer, K/V) slice of the pool
+  const uint32_t* rows;    // the lane's column of the wave's table
+  int j;                   // the lane's current output row (the same on every lane)
+  __device__ __forceinline__ const uint8_t* s(int b) const {
+    return slice + ((uint64_t)rows[(b / BPR) * 64] << RB_SHIFT) + (b % BPR) * 64;
+  }
+  __device__ __forceinline__ uint8_t* d(int pos) const {
+    const uint32_t r = rows[(RPC + j) * 64];
+    return r == kPagedSkipRow ? nullptr : slice + ((uint64_t)r << RB_SHIFT) + pos * 64;
+  }
+  __device__ __forceinline__ void next_row() { ++j; }
+};
+
+struct PagedAddr {
+  uint8_t* pool;
+  int64_t P;                 // pages
+  int32_t b_shift;           // log2 of the rows per page
+  const int64_t* table;      // per fragment {T, first}: its page ids start at blocks[first]
+  const int32_t* blocks;
+  const int32_t* k_table;    // merged block -> page, K and V
+  const int32_t* v_table;
+  uint32_t* lds;             // the block's tables: [waves][2 * RPC][64]
+  template <int RB>
+  __device__ __forceinline__ PagedTask<RB> task(int64_t i, int64_t t, int64_t sidx, int64_t off,
+                                                int64_t T, int64_t, int32_t H, int64_t,
+                                                int lane, int wave) const {
+    constexpr int RPC = PagedTask<RB>::RPC;
+    constexpr int RB_SHIFT = PagedTask<RB>::RB_SHIFT;
+    PagedTask<RB> a;
+    a.slice = pool + ((t * P * H) << (b_shift + RB_SHIFT));
+    uint32_t* col = lds + (int64_t)wave * (2 * RPC * 64) + lane;
+    a.rows = col;
+    a.j = 0;
+    const int64_t first = table[2 * i + 1];
+    const int32_t* tab = (t & 1) ? v_table : k_table;
+    const int64_t q0 = (sidx * 64 + lane) * RPC;   // the chunk's first row in the tensor
+    const int64_t rows = (int64_t)H * T;
+    ChunkRow c = fused_chunk_row(sidx, lane, RB_SHIFT, T);
+#pragma unroll
+    for (int r = 0; r < RPC; ++r) {
+      uint32_t sr = 0, dr = kPagedSkipRow;
+      if (q0 + r < rows) paged_row_pair(blocks, first, tab, P, H, b_shift, off, c, &sr, &dr);
+      col[r * 64] = sr;
+      col[(RPC + r) * 64] = dr;
+      fused_chunk_next(c, T);
+    }
+    return a;
+  }
+};
+
+// ESIZE: element bytes; STYLE: pairing; RB: row bytes (64 .. 1024); Addr: the
+// storage of the fragments and of the merged cache.
+template <int ESIZE, int STYLE, int RB, class Addr>
+__device__ __forceinline__ void render_hash_body(
+    const Addr& addr, int32_t n, const int64_t* __restrict__ plan,
     const int64_t* __restrict__ task_base, const double* __restrict__ angles, int32_t H,
     int32_t d, const uint8_t* __restrict__ select, const int64_t* __restrict__ base0,
-    uint8_t* __restrict__ nodes, uint8_t* __restrict__ out) {
+    uint8_t* __restrict__ nodes) {
   constexpr int EP = 16 / ESIZE;              // elements per 16-byte piece
   constexpr int BPR = RB / 64;                // blocks per row: 1 .. 16
   constexpr int HBK = BPR / 2;                // blocks per half row (0: a row is one block)
   constexpr int PPR = BPR >= 2 ? BPR / 2 : 1; // steps (pairs of blocks) per row
   constexpr int HP = BPR >= 4 ? BPR / 4 : 0;  // steps per half row when halves span steps
-  constexpr int RB_SHIFT = __builtin_ctz(RB);
   constexpr bool HALF = STYLE == CM_ROPE_HALF;
   // a half-split pair whose halves are in different steps: the first-half pair
   // of blocks is kept in registers for rows of 256 bytes (one step back) and
@@ -160,13 +258,10 @@ __global__ __launch_bounds__(kThreads) CM_FUSED_OCCUPANCY void render_hash_kerne
     const int64_t in_stripe = (bytes >> 6) - sidx * kStripeBlocks;
     const bool full = in_stripe >= kStripeBlocks;
     const uint64_t chunk = (uint64_t)sidx * kStripeChunks + lane;
-    const FusedLane fl = fused_lane(bytes, sidx, lane, RB_SHIFT, T, T_out, off);
-    const int nb = fl.nb;                          // blocks of the lane's chunk
-    const uint8_t* src = reinterpret_cast<const uint8_t*>(table[i * stride + 1 + t]) + fl.src;
-    uint8_t* dst = out + t * (int64_t)H * T_out * RB + fl.dst;
-    int64_t left = fl.left;
-    const int64_t gap = (T_out - T) << RB_SHIFT;   // end of a head's rows -> next head
-    auto next_row = [&]() { fused_next_row(dst, left, T, gap, RB); };
+    const int64_t blocks_left = (bytes >> 6) - (int64_t)chunk * 16;
+    const int nb = blocks_left < 0 ? 0 : (blocks_left > 16 ? 16 : (int)blocks_left);
+    auto A = addr.template task<RB>(i, t, sidx, off, T, T_out, H, bytes, lane, wave);
+    constexpr bool SKIPS = decltype(A)::kSkips;   // rows that are not written
     B3Cv st;
     b3_init(st);
     const uint32_t root = m == 1 ? kB3Root : 0u;
@@ -217,9 +312,15 @@ __global__ __launch_bounds__(kThreads) CM_FUSED_OCCUPANCY void render_hash_kerne
       }
       __builtin_amdgcn_wave_barrier();   // the wave's LDS writes come before its reads
 #pragma unroll
-      for (int j = 0; j < 8; ++j)
-        store16(dst_r[8 * j] + pq * 16,
-                *reinterpret_cast<const u32x4*>(stage_r + j * 8 * kStageLane));
+      for (int j = 0; j < 8; ++j) {
+        uint8_t* p = dst_r[8 * j];
+        const u32x4 v = *reinterpret_cast<const u32x4*>(stage_r + j * 8 * kStageLane);
+        if constexpr (SKIPS) {
+          if (p != nullptr) store16(p + pq * 16, v);
+        } else {
+          store16(p + pq * 16, v);
+        }
+      }
       __builtin_amdgcn_wave_barrier();   // and before the next put's writes
     };
 
@@ -235,10 +336,10 @@ __global__ __launch_bounds__(kThreads) CM_FUSED_OCCUPANCY void render_hash_kerne
       if constexpr (BPR == 1) {
         // two rows of one block
         if (ROT) { rotate_own(y0, 0); rotate_own(y1, 0); }
-        uint8_t* d0 = dst;
-        next_row();
-        put2(y0, y1, d0, dst);
-        next_row();
+        uint8_t* d0 = A.d(0);
+        A.next_row();
+        put2(y0, y1, d0, A.d(0));
+        A.next_row();
         return;
       } else if constexpr (BPR == 2) {
         // one row: halves in y0, y1
@@ -246,8 +347,8 @@ __global__ __launch_bounds__(kThreads) CM_FUSED_OCCUPANCY void render_hash_kerne
           if (HALF) rotate_halves(y0, y1, 0);
           else { rotate_own(y0, 0); rotate_own(y1, 1); }
         }
-        put2(y0, y1, dst, dst + 64);
-        next_row();
+        put2(y0, y1, A.d(0), A.d(1));
+        A.next_row();
         return;
       } else {
         if (ROT && HALF) {
@@ -255,13 +356,13 @@ __global__ __launch_bounds__(kThreads) CM_FUSED_OCCUPANCY void render_hash_kerne
           const int pb = 2 * (pp - HP);           // row block of yp0
           rotate_halves(yp0, y0, pb);
           rotate_halves(yp1, y1, pb + 1);
-          put2(yp0, yp1, dst + pb * 64, dst + pb * 64 + 64);
+          put2(yp0, yp1, A.d(pb), A.d(pb + 1));
         } else if (ROT) {
           rotate_own(y0, 2 * pp);
           rotate_own(y1, 2 * pp + 1);
         }
-        put2(y0, y1, dst + 2 * pp * 64, dst + 2 * pp * 64 + 64);
-        if (pp == PPR - 1) next_row();
+        put2(y0, y1, A.d(2 * pp), A.d(2 * pp + 1));
+        if (pp == PPR - 1) A.next_row();
       }
     };
 
@@ -279,8 +380,15 @@ __global__ __launch_bounds__(kThreads) CM_FUSED_OCCUPANCY void render_hash_kerne
       constexpr bool SPLIT = ROT && HALF && HP > 0;      // halves in different steps
       u32x4 xa0[4], xa1[4], xb0[4], xb1[4], k0[4], k1[4];
       auto load2 = [&](u32x4 (&y0)[4], u32x4 (&y1)[4], int b) {
-        load_block(y0, src + b * 64);
-        load_block(y1, src + b * 64 + 64);
+        if constexpr (SKIPS && BPR == 1) {
+          // two rows, each a block
+          load_block(y0, A.s(b));
+          load_block(y1, A.s(b + 1));
+        } else {
+          const uint8_t* p = A.s(b);
+          load_block(y0, p);
+          load_block(y1, p + 64);
+        }
       };
       auto step = [&](int k, u32x4 (&x0)[4], u32x4 (&x1)[4], u32x4 (&p0)[4], u32x4 (&p1)[4]) {
 #pragma unroll
@@ -335,8 +443,8 @@ __global__ __launch_bounds__(kThreads) CM_FUSED_OCCUPANCY void render_hash_kerne
       u32x4 x[4], par[4];
       for (int b = 0; b < nb; ++b) {
         const int pos = b & (BPR - 1);
-        load_block(x, src + b * 64);
-        if (ROT && HALF && BPR > 1 && pos >= HBK) load_block(par, src + (b - HBK) * 64);
+        load_block(x, A.s(b));
+        if (ROT && HALF && BPR > 1 && pos >= HBK) load_block(par, A.s(b - HBK));
         if (hashing) compress_block(st, x, chunk, flags(b, nb - 1));
         bool out = true;
         if (ROT) {
@@ -347,15 +455,17 @@ __global__ __launch_bounds__(kThreads) CM_FUSED_OCCUPANCY void render_hash_kerne
             rotate_own(x, pos);
           }
         }
-        if (out) {
+        if (out && (!SKIPS || A.d(0) != nullptr)) {
           if (ROT && HALF && BPR > 1) {
+            uint8_t* dp = A.d(pos - HBK);
 #pragma unroll
-            for (int q = 0; q < 4; ++q) store16(dst + (pos - HBK) * 64 + 16 * q, par[q]);
+            for (int q = 0; q < 4; ++q) store16(dp + 16 * q, par[q]);
           }
+          uint8_t* dx = A.d(pos);
 #pragma unroll
-          for (int q = 0; q < 4; ++q) store16(dst + pos * 64 + 16 * q, x[q]);
+          for (int q = 0; q < 4; ++q) store16(dx + 16 * q, x[q]);
         }
-        if (pos == BPR - 1) next_row();
+        if (pos == BPR - 1) A.next_row();
       }
     };
 
@@ -371,6 +481,32 @@ __global__ __launch_bounds__(kThreads) CM_FUSED_OCCUPANCY void render_hash_kerne
     }
     if (hashing && nb > 0) store_cv(nodes + (base0[i] + t * m + (int64_t)chunk) * 32, st);
   }
+}
+
+template <int ESIZE, int STYLE, int RB>
+__global__ __launch_bounds__(kThreads) CM_FUSED_OCCUPANCY void render_hash_kernel(
+    const int64_t* __restrict__ table, int64_t stride, int32_t n, const int64_t* __restrict__ plan,
+    const int64_t* __restrict__ task_base, const double* __restrict__ angles, int32_t H,
+    int32_t d, const uint8_t* __restrict__ select, const int64_t* __restrict__ base0,
+    uint8_t* __restrict__ nodes, uint8_t* __restrict__ out) {
+  render_hash_body<ESIZE, STYLE, RB>(DenseAddr{table, stride, out}, n, plan, task_base, angles, H,
+                                     d, select, base0, nodes);
+}
+
+// The pool is read (fragment pages) and written (the merged cache's fresh
+// pages) through the same pointer.
+template <int ESIZE, int STYLE, int RB>
+__global__ __launch_bounds__(kThreads) CM_FUSED_OCCUPANCY void paged_hash_render_kernel(
+    uint8_t* pool, int64_t P, int32_t b_shift, const int64_t* __restrict__ table,
+    const int32_t* __restrict__ blocks, const int32_t* __restrict__ k_table,
+    const int32_t* __restrict__ v_table, int32_t n, const int64_t* __restrict__ plan,
+    const int64_t* __restrict__ task_base, const double* __restrict__ angles, int32_t H,
+    int32_t d, const uint8_t* __restrict__ select, const int64_t* __restrict__ base0,
+    uint8_t* __restrict__ nodes) {
+  __shared__ uint32_t rows_lds[kWaves * 2 * (1024 / RB) * 64];
+  render_hash_body<ESIZE, STYLE, RB>(
+      PagedAddr{pool, P, b_shift, table, blocks, k_table, v_table, rows_lds}, n, plan, task_base,
+      angles, H, d, select, base0, nodes);
 }
 
 // Calls go(IC<RB>) for the row size of the set.
@@ -425,6 +561,51 @@ hipError_t launch_render_hash(const SetDesc& s, const HashLayout& hlay, const Re
       } else {
         if (style == CM_ROPE_HALF) launch(render_hash_kernel<4, CM_ROPE_HALF, RB>);
         else launch(render_hash_kernel<4, CM_ROPE_INTERLEAVED, RB>);
+      }
+    };
+    dispatch_row(s.row_bytes, go);
+  }
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  return launch_hash_tree(s, hlay, hsel, 0, digests, hws, stream);
+}
+
+hipError_t launch_paged_render_hash(const PagedDesc& p, const HashLayout& hlay,
+                                    const RenderLayout& rlay, const int64_t* plan_dev, double base,
+                                    int32_t style, const uint8_t* select, const int32_t* k_table,
+                                    const int32_t* v_table, uint8_t* digests, uint8_t* ws,
+                                    hipStream_t stream) {
+  const SetDesc& s = p.s;
+  uint8_t* hws = ws;
+  uint8_t* rws = ws + align_up(hlay.bytes, kWsAlign);
+  hipError_t e = launch_hash_prep(s, hlay, hws, stream);
+  if (e != hipSuccess) return e;
+  if ((e = launch_render_prep(s, rlay, plan_dev, s.n, base, style, (int32_t)kStripeBlocks, select,
+                              rws, stream)) != hipSuccess)
+    return e;
+  const uint8_t* hsel = rws + rlay.off_hsel;  // 0: slot delivery whose Id is computed here
+  {
+    const int64_t* base_tab = reinterpret_cast<const int64_t*>(hws + hlay.off_tables);
+    const int64_t* tasks = reinterpret_cast<const int64_t*>(rws + rlay.off_tiles);
+    const double* angles = reinterpret_cast<const double*>(rws + rlay.off_angles);
+    const int64_t cap = (int64_t)device_cu_count() * CM_FUSED_BLOCKS_PER_CU;
+    const int64_t want = (hlay.tasks + kWaves - 1) / kWaves;
+    const dim3 grid((uint32_t)(want < cap ? (want > 0 ? want : 1) : cap));
+    ScopedTiming tm(K_PAGED_HASH_RENDER, stream);
+    uint8_t* nodes = hws + hlay.off_buf0;
+    uint8_t* pool = static_cast<uint8_t*>(p.pool);
+    auto go = [&](auto rbc) {
+      constexpr int RB = decltype(rbc)::value;
+      auto launch = [&](auto kern) {
+        hipLaunchKernelGGL(kern, grid, dim3(kThreads), 0, stream, pool, p.pages, p.b_shift,
+                           s.table_dev, p.blocks_dev, k_table, v_table, s.n, plan_dev, tasks,
+                           angles, s.H, s.d, hsel, base_tab, nodes);
+      };
+      if (s.esize == 2) {
+        if (style == CM_ROPE_HALF) launch(paged_hash_render_kernel<2, CM_ROPE_HALF, RB>);
+        else launch(paged_hash_render_kernel<2, CM_ROPE_INTERLEAVED, RB>);
+      } else {
+        if (style == CM_ROPE_HALF) launch(paged_hash_render_kernel<4, CM_ROPE_HALF, RB>);
+        else launch(paged_hash_render_kernel<4, CM_ROPE_INTERLEAVED, RB>);
       }
     };
     dispatch_row(s.row_bytes, go);

@@ -31,7 +31,7 @@ from .binding import (FragmentBatch, bag_plan, canonical_order, equal_key_mask, 
                       paged_render, paged_tables, paged_workspace_size, render_merge,
                       render_deliveries_async, render_merge_devplan, render_merge_hash,
                       render_merge_range, render_set, workspace_size, paged_order,
-                      paged_hash_select)
+                      paged_hash_select, paged_render_hash)
 from .binding import PagedSet
 
 _WS: Dict[tuple, torch.Tensor] = {}
@@ -534,20 +534,29 @@ def render_paged(pset: PagedSet, plan_host: np.ndarray, free_pages, rope_base: f
                        T_out=int(plan_host[C.PLAN_TOUT]))
 
 
+def paged_fused_fits(pset: PagedSet) -> bool:
+    """Whether cm_paged_render_hash takes this pool: it names a pool row of one
+    (layer, K/V) slice with 32 bits, so P * H * B must not exceed 2^32 - 1."""
+    return pset.P * pset.H * pset.B <= 0xFFFFFFFF
+
+
 def render_paged_set(pset: PagedSet, routing_layer: int, rope_base: float, free_pages,
-                     style: str = "half", stream=None,
+                     style: str = "half", stream=None, fused: Optional[bool] = None,
                      hash_workgroups_per_cu: int = 1) -> PagedRender:
     """Steps 1-5 on fragments that live only in the pool (§4.5): scores, the Ids
     the order reads (deliveries whose key equals another's), dedupe, order and
     offsets on the device (cm_paged_order), the plan to the host for the block
-    tables, then the render of the pages that no fragment page can stand for,
-    with the remaining Ids (the content address of each fragment's dense form)
-    hashed beside it on a second stream: the hash is VALU work and the render
-    memory traffic, so the two overlap (one hash workgroup per CU leaves the
-    render the most room: measured 25.4 ms on the Qwen3-4B large set, against
-    26.6 ms with the default four and 30.8 ms with the hash before the render).
-    No dense copy of any fragment is made; the result's digests wait for both
-    streams."""
+    tables, then the render of every merged row that no fragment page holds
+    already and, from the same loads, the remaining Ids (the content address of
+    each fragment's dense form): cm_paged_render_hash, the paged counterpart of
+    the dense path's fused kernel. fused=False (the default for a pool too large
+    for that kernel's 32-bit row index) renders with cm_paged_render instead and
+    hashes the remaining Ids beside it on a second stream with
+    hash_workgroups_per_cu chunk workgroups per CU, each byte then read twice.
+    No dense copy of any fragment is made; the result's digests wait for all of
+    its work."""
+    if fused is None:
+        fused = paged_fused_fits(pset)
     dev = pset.device
     main = stream if stream is not None else torch.cuda.current_stream(dev)
     with torch.cuda.stream(main):
@@ -558,25 +567,33 @@ def render_paged_set(pset: PagedSet, routing_layer: int, rope_base: float, free_
         digests = torch.empty((pset.n, 32), dtype=torch.uint8, device=dev)
         plan_dev = torch.empty(plan_elems(pset.n), dtype=torch.int64, device=dev)
         paged_order(pset, routing_layer, min(pset.lengths), keys, mask, digests, plan_dev, ws, main)
-        ready = torch.cuda.Event()
-        ready.record(main)
-        side = _side_stream(dev)
-        side.wait_event(ready)
-        with torch.cuda.stream(side):
-            ws_side = torch.empty(need, dtype=torch.uint8, device=dev)
-        paged_hash_select(pset, mask, 0, digests, ws_side, hash_workgroups_per_cu, side)
-        for t in (mask, digests, ws_side):
-            t.record_stream(side)
-        side_done = torch.cuda.Event()
-        side_done.record(side)
-        plan_host = _plan_to_host(plan_dev, main)
-        try:
+        if fused:
+            plan_host = _plan_to_host(plan_dev, main)
             _check_plan(plan_host, "cm_paged_order")
             kt, vt, fresh = paged_tables(pset, plan_host, free_pages)
             kd, vd = torch.from_numpy(kt).to(dev), torch.from_numpy(vt).to(dev)
-            fd = torch.from_numpy(fresh).to(dev)
-            paged_render(pset, plan_dev, plan_host, rope_base, style, kd, vd, fd, ws, main)
-        finally:
-            main.wait_event(side_done)       # the digests are complete once main is
+            paged_render_hash(pset, plan_dev, plan_host, rope_base, style, kt, vt, kd, vd, mask,
+                              digests, ws, main)
+        else:
+            ready = torch.cuda.Event()
+            ready.record(main)
+            side = _side_stream(dev)
+            side.wait_event(ready)
+            with torch.cuda.stream(side):
+                ws_side = torch.empty(need, dtype=torch.uint8, device=dev)
+            paged_hash_select(pset, mask, 0, digests, ws_side, hash_workgroups_per_cu, side)
+            for t in (mask, digests, ws_side):
+                t.record_stream(side)
+            side_done = torch.cuda.Event()
+            side_done.record(side)
+            plan_host = _plan_to_host(plan_dev, main)
+            try:
+                _check_plan(plan_host, "cm_paged_order")
+                kt, vt, fresh = paged_tables(pset, plan_host, free_pages)
+                kd, vd = torch.from_numpy(kt).to(dev), torch.from_numpy(vt).to(dev)
+                fd = torch.from_numpy(fresh).to(dev)
+                paged_render(pset, plan_dev, plan_host, rope_base, style, kd, vd, fd, ws, main)
+            finally:
+                main.wait_event(side_done)       # the digests are complete once main is
     return PagedRender(k_table=kt, v_table=vt, fresh=fresh, T_out=int(plan_host[C.PLAN_TOUT]),
                        plan=plan_host, digests_dev=digests, keys_dev=keys)

@@ -3,9 +3,10 @@
 // the CPU, so chunk counters, flags and parent nodes can be compared with the
 // published BLAKE3 test vectors and the oracle without a GPU; exposes the
 // compiler's single-step fp64 -> bf16 conversion that the render kernel uses;
-// and walks the address maps of the fused kernel (fused_geometry.h) and of the
-// unit render (render_geometry.h), the same sources the kernels use, over every
-// task, unit, lane and piece of a launch. Test support only.
+// and walks the address maps of the fused kernel on dense and on paged storage
+// (fused_geometry.h) and of the unit render (render_geometry.h), the same
+// sources the kernels use, over every task, unit, lane, row and piece of a
+// launch. Test support only.
 #include <stdint.h>
 #include <string.h>
 
@@ -136,6 +137,77 @@ int64_t hc_unit_check(int32_t n_u, const int64_t* T, const int64_t* off, int32_t
   }
   for (int64_t p = 0; p < (int64_t)seen.size(); ++p)
     if (seen[(size_t)p] != (p >= ((row0 << rb_shift) >> 4) ? 1 : 0)) ++bad;
+  return bad;
+}
+
+// Every (slot, tensor stripe, lane, chunk row) of a paged fused launch
+// (paged_hash_render_kernel) over n_u slots of lengths T[s] at offsets off[s],
+// slot s's fragment on pages blocks[first[s] ..], into the merged K (kv = 0) or
+// V (kv = 1) block table tab of a pool of P pages of B = 2^b_shift rows: each
+// row the lane reads must be row tr of head h of its chunk's rows (in dense
+// order) at its fragment page; each row it writes must go to merged row off + tr
+// of head h in the page tab[(off + tr) / B], a page that holds no fragment row;
+// a row it skips must sit in the very page it is read from; and every merged
+// row [0, T_out) of every head must be written or skipped exactly once, and no
+// pool row written twice. Returns the number of violations.
+int64_t hc_paged_fused_check(int32_t n_u, const int64_t* T, const int64_t* off,
+                             const int64_t* first, const int32_t* blocks, int64_t n_blocks,
+                             int32_t H, int32_t rb, int32_t b_shift, int64_t P,
+                             const int32_t* tab, int64_t T_out) {
+  const int rb_shift = __builtin_ctz((unsigned)rb);
+  const int64_t B = (int64_t)1 << b_shift;
+  const int64_t rpc = 1024 / rb;
+  std::vector<uint8_t> frag_page((size_t)P, 0), seen((size_t)H * (size_t)T_out, 0);
+  std::vector<uint8_t> written((size_t)(P * H * B), 0);
+  for (int64_t k = 0; k < n_blocks; ++k) frag_page[(size_t)blocks[k]] = 1;
+  int64_t bad = 0;
+  for (int s = 0; s < n_u; ++s) {
+    const int64_t bytes = (int64_t)H * T[s] * rb;
+    const int64_t stripes = ((bytes >> 6) + 1023) / 1024;
+    for (int64_t sidx = 0; sidx < stripes; ++sidx) {
+      for (int lane = 0; lane < 64; ++lane) {
+        const int64_t chunk = sidx * 64 + lane;
+        const int64_t left = (bytes >> 6) - chunk * 16;
+        const int64_t nb = left < 0 ? 0 : (left > 16 ? 16 : left);
+        if (nb == 0) continue;
+        const int64_t rows = nb * 64 / rb;        // the chunk's rows the kernel reads
+        const int64_t q0 = chunk * rpc;
+        cm::ChunkRow c = cm::fused_chunk_row(sidx, lane, rb_shift, T[s]);
+        for (int64_t j = 0; j < rpc; ++j) {
+          const int64_t q = q0 + j;
+          if (j < rows) {
+            // the kernel builds the entry only for rows inside the tensor
+            if (q >= (int64_t)H * T[s]) { ++bad; break; }
+            if (c.h != q / T[s] || c.tr != q % T[s]) { ++bad; break; }
+            uint32_t src = 0, dst = 0;
+            cm::paged_row_pair(blocks, first[s], tab, P, H, b_shift, off[s], c, &src, &dst);
+            const int64_t page = blocks[first[s] + c.tr / B];
+            if (src != (uint32_t)((page * H + c.h) * B + c.tr % B)) ++bad;
+            const int64_t m = off[s] + c.tr;
+            const int64_t out = tab[m / B];
+            if (dst == cm::kPagedSkipRow) {
+              if (out != page) ++bad;               // only a row already in place is skipped
+            } else {
+              if (out < 0 || out >= P || frag_page[(size_t)out]) ++bad;
+              if (dst != (uint32_t)((out * H + c.h) * B + m % B)) {
+                ++bad;
+              } else {
+                uint8_t& w = written[dst];
+                if (w) ++bad;
+                w = 1;
+              }
+            }
+            uint8_t& z = seen[(size_t)(c.h * T_out + m)];
+            if (z) ++bad;
+            z = 1;
+          }
+          cm::fused_chunk_next(c, T[s]);
+        }
+      }
+    }
+  }
+  for (uint8_t z : seen)
+    if (!z) ++bad;
   return bad;
 }
 

@@ -110,7 +110,8 @@ def test_every_enqueuing_call_is_covered():
     render is checked separately below)."""
     takes_stream = {name for name, f in inspect.getmembers(binding, inspect.isfunction)
                     if "stream" in inspect.signature(f).parameters and not name.startswith("_")}
-    assert takes_stream == set(CALLS) | {"paged_render", "paged_order", "paged_hash_select"}
+    assert takes_stream == set(CALLS) | {"paged_render", "paged_order", "paged_hash_select",
+                                         "paged_render_hash"}
 
 
 @pytest.mark.parametrize("name", sorted(CALLS))
@@ -130,6 +131,16 @@ def test_paged_render_marks_both_tables(fake_lib):
     binding.paged_render(pset, T, PLAN, 1e4, "half", T, T, T, T, s)
     assert [t.streams for t in pset.device_tables] == [[s], [s]]
     assert fake_lib.calls[-1][1].value == 33
+
+
+def test_paged_render_hash_marks_both_tables(fake_lib):
+    pset = _owner(2)
+    s = FakeStream(34)
+    tab = np.zeros(3, dtype=np.int32)
+    binding.paged_render_hash(pset, T, PLAN, 1e4, "half", tab, tab, T, T, T, T, T, s)
+    assert [t.streams for t in pset.device_tables] == [[s], [s]]
+    assert fake_lib.calls[-1][0] == "cm_paged_render_hash"
+    assert fake_lib.calls[-1][1].value == 34
 
 
 def test_paged_order_marks_both_tables(fake_lib):

@@ -471,3 +471,55 @@ def test_paged_order_argument_checks(lib):
     assert h(fp.ref, mask, 0, dig, 65, ws, need.value, None) == C.CM_EINVAL
     fp.blocks[0] = fp.P                                     # a page id outside the pool
     assert call() == C.CM_EINVAL
+
+
+def test_paged_render_hash_argument_checks(lib):
+    """cm_paged_render_hash checks the block tables on the host before anything
+    is enqueued: the tables of cm_paged_tables pass (the call then stops at the
+    missing workspace, its last check); a fragment page where no whole page of
+    that fragment lines up, a K page kept at a non-zero offset, a page used
+    twice or outside the pool, and a pool too large for 32-bit row indices are
+    refused."""
+    lengths, order = (32, 48, 16), [1, 0, 2]                 # every slot page-aligned
+    fp = FakePaged(lengths, spare=64)
+    plan = _plan(3, order, [lengths[i] for i in order])
+    st, kt, vt, _ = _paged_tables(lib, fp, plan)
+    assert st == C.CM_OK
+    rope = C.CmRope(base=1e4, style=0, reserved=0)
+    need = ctypes.c_size_t(0)
+    assert lib.cm_paged_workspace_size(fp.ref, ctypes.byref(need)) == C.CM_OK
+    sel, dig = ctypes.c_void_p(0x70000), ctypes.c_void_p(0x40000)
+
+    def call(k=kt, v=vt, fp=fp, ws_bytes=0, sel=sel, dig=dig, p=plan):
+        k = np.ascontiguousarray(k, dtype=np.int32)
+        v = np.ascontiguousarray(v, dtype=np.int32)
+        return lib.cm_paged_render_hash(fp.ref, ctypes.c_void_p(0x50000),
+                                        p.ctypes.data_as(ctypes.c_void_p), ctypes.byref(rope),
+                                        k.ctypes.data_as(ctypes.c_void_p),
+                                        v.ctypes.data_as(ctypes.c_void_p),
+                                        ctypes.c_void_p(0x80000), ctypes.c_void_p(0x90000), sel,
+                                        dig, ctypes.c_void_p(0x60000), ws_bytes, None)
+
+    assert call() == C.CM_EWORKSPACE                      # every other check passed
+    assert call(ws_bytes=need.value - 1) == C.CM_EWORKSPACE
+    # slot 0 (fragment 1) sits at offset 0: its K pages are kept, and V pages of
+    # every slot; the V page of block 0 stands in K's place at block 3 (slot 1,
+    # offset 48): a fragment page this block cannot keep
+    assert kt[0] == fp.pages[1][0] and vt[3] == fp.pages[0][0]
+    k = kt.copy(); k[3] = vt[3]
+    assert call(k=k) == C.CM_EINVAL
+    assert "cannot reuse" in lib.cm_last_error().decode()
+    v = vt.copy(); v[0] = fp.pages[2][0]                  # another fragment's page
+    assert call(v=v) == C.CM_EINVAL
+    fresh_k = [j for j in range(len(kt)) if kt[j] in set(fp.free.tolist())]
+    k = kt.copy(); k[fresh_k[1]] = k[fresh_k[0]]          # one fresh page twice
+    assert call(k=k) == C.CM_EINVAL
+    assert "repeats" in lib.cm_last_error().decode()
+    k = kt.copy(); k[fresh_k[0]] = fp.P                   # outside the pool
+    assert call(k=k) == C.CM_EINVAL
+    assert call(sel=None) == C.CM_EINVAL
+    assert call(dig=ctypes.c_void_p(0x40008)) == C.CM_EINVAL
+    assert call(p=_plan(3, order, [48, 33, 16])) == C.CM_ESHAPE
+    fp.s.pages = 1 << 27                                  # P * H * B = 2^32
+    assert call() == C.CM_ESHAPE
+    assert "2^32" in lib.cm_last_error().decode()

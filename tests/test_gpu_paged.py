@@ -2,9 +2,12 @@
 merged cache read back through its K and V block tables equals the dense render
 of the same fragments bit for bit (the dense render is checked against the
 oracle elsewhere; one case here is checked against the oracle directly), reused
-pages are the fragments' own, and no page outside the fresh list changes. Steps
-1-5 on fragments that live only in the pool (cm_paged_order, then the paged
-render) are checked against the oracle: Ids, scores, plan and merged cache."""
+pages are the fragments' own, and no page outside the fresh list changes. The
+fused paged render + hash (cm_paged_render_hash) leaves the pool exactly as the
+paged render does and writes the dense form's Ids. Steps 1-5 on fragments that
+live only in the pool (cm_paged_order, then the fused kernel or the paged render
+beside the paged hash) are checked against the oracle: Ids, scores, plan and
+merged cache."""
 
 import numpy as np
 import pytest
@@ -65,6 +68,47 @@ def test_paged_render_equals_dense_render(case, style):
         assert pr.reused_pages == len(pr.v_table) + dense.lengths[0] // case["B"]
 
 
+@pytest.mark.parametrize("case", CASES, ids=[f"{c['dtype']}-d{c['d']}-B{c['B']}" for c in CASES])
+@pytest.mark.parametrize("style", ["half", "interleaved"])
+def test_paged_render_hash_equals_render_plus_hash(case, style):
+    """cm_paged_render_hash with the tables of cm_paged_tables leaves the pool
+    byte for byte as cm_paged_render does (fresh pages written, every other
+    page, reused ones included, untouched) and writes the Ids of the slot
+    deliveries selected with 0, equal to the dense path's, leaving the others'
+    digests as they were."""
+    w = synth.custom("paged-fused", dtype=case["dtype"], d=case["d"], H=2, L=3,
+                     lengths=case["lengths"], routing_layer=1, rope_base=1e4)
+    dl = synth.make_deliveries(w, synth.make_fragments(w, device="cuda"))
+    dense = cm.render_deliveries(dl, w.routing_layer, w.rope_base, style=style)
+    torch.cuda.synchronize()
+    ids = dense.digests_dev.cpu().numpy().copy()
+    pool, lengths, page_lists, free = synth.make_paged(dl, case["B"], spare_pages=64, seed=3)
+    before = pool.clone()
+    pset = cm.PagedSet(pool, lengths, page_lists)
+    log(f"[paged-fused] {case} style={style}")
+    pr = cm.render_paged(pset, dense.plan, free, w.rope_base, style=style)
+    torch.cuda.synchronize()
+    ref = pool.clone()
+    pool.copy_(before)
+    n = len(lengths)
+    select = torch.tensor([k % 2 for k in range(n)], dtype=torch.uint8, device="cuda")
+    digests = torch.full((n, 32), 0xAB, dtype=torch.uint8, device="cuda")
+    ws = torch.empty(cm.paged_workspace_size(pset), dtype=torch.uint8, device="cuda")
+    plan_dev = torch.from_numpy(dense.plan).cuda()
+    kd = torch.from_numpy(pr.k_table).cuda()
+    vd = torch.from_numpy(pr.v_table).cuda()
+    cm.paged_render_hash(pset, plan_dev, dense.plan, w.rope_base, style, pr.k_table, pr.v_table,
+                         kd, vd, select, digests, ws)
+    torch.cuda.synchronize()
+    assert torch.equal(pool, ref)
+    got = digests.cpu().numpy()
+    for k in range(n):
+        if k % 2 == 0:
+            assert bytes(got[k]) == bytes(ids[k]), f"Id of delivery {k}"
+        else:
+            assert (got[k] == 0xAB).all(), f"digest {k} was not selected and must stay"
+
+
 def test_paged_render_against_oracle():
     w = synth.custom("paged-oracle", dtype="bfloat16", d=128, H=2, L=2, lengths=(48, 77, 16),
                      routing_layer=1)
@@ -95,15 +139,17 @@ SET_CASES = [
 ]
 
 
+@pytest.mark.parametrize("fused", [True, False], ids=["fused", "overlapped"])
 @pytest.mark.parametrize("case", SET_CASES,
                          ids=[f"{c['dtype']}-d{c['d']}-B{c['B']}" for c in SET_CASES])
-def test_paged_set_steps_1_to_5_against_oracle(case):
+def test_paged_set_steps_1_to_5_against_oracle(case, fused):
     """render_paged_set on a pool holding every delivery (copies on pages of
     their own): the Ids are the dense form's content addresses, the scores and
     the plan are the oracle's, and the merged cache read back through the block
-    tables is the oracle's render. The fragments' dense tensors serve only to
-    fill the pool and to compute the oracle's answer; they are dropped before
-    the paged path runs."""
+    tables is the oracle's render; with the render and the remaining Ids in one
+    kernel (cm_paged_render_hash) and with the paged render and the paged hash
+    beside it. The fragments' dense tensors serve only to fill the pool and to
+    compute the oracle's answer; they are dropped before the paged path runs."""
     w = synth.custom("paged-set", dtype=case["dtype"], d=case["d"], H=case["H"], L=case["L"],
                      lengths=case["lengths"], deliveries=case.get("deliveries"),
                      shared_k=case.get("shared_k", ()), routing_layer=1, rope_base=1e4)
@@ -118,9 +164,9 @@ def test_paged_set_steps_1_to_5_against_oracle(case):
     pool, lengths, page_lists, free = synth.make_paged(dl, case["B"], spare_pages=spare, seed=5)
     del dl
     torch.cuda.synchronize()
-    log(f"[paged-set] {case}")
+    log(f"[paged-set] {case} fused={fused}")
     pr = cm.render_paged_set(cm.PagedSet(pool, lengths, page_lists), w.routing_layer, w.rope_base,
-                             free)
+                             free, fused=fused)
     torch.cuda.synchronize()
     assert [bytes(x) for x in pr.digests_dev.cpu().numpy()] == ids
     assert list(pr.keys_dev.cpu().numpy()) == keys
