@@ -16,6 +16,8 @@
  *   cm_render_set           steps 2-5 for a set with known Ids, in one call
  *   cm_paged_order / cm_paged_hash_select / cm_paged_tables / cm_paged_render /
  *   cm_paged_render_hash    steps 1-5 over paged storage
+ *   cm_paged_deliveries     steps 1-5 over paged storage in one call, with no host
+ *                           round trip
  * the paper's baselines over the same render:
  *   cm_multiset_order       the naive re-render order of §5.9 (no dedupe)
  *   cm_bag_plan             BagMerge with a caller-supplied order (§4.2)
@@ -429,6 +431,29 @@ int32_t cm_paged_render_hash(const cm_pagedset* set, const int64_t* plan_dev,
                              const int32_t* k_table_dev, const int32_t* v_table_dev,
                              const uint8_t* select_dev, uint8_t* digests_dev, void* workspace,
                              size_t workspace_bytes, void* stream);
+/* Steps 1-5 over paged storage in one call with nothing waiting for the host
+ * (Render of Alg. 2 over deliveries that live only in the pool, §4.5): the steps
+ * of cm_paged_order (keys_dev, mask_dev, the colliding deliveries' digests,
+ * plan_dev), the merged K and V block tables built on the device by
+ * cm_paged_tables' rule from the free pages in list order (k_table_dev,
+ * v_table_dev; *n_fresh_dev = the free pages taken), then cm_paged_render_hash
+ * with them and mask_dev (every other Id). After the stream has finished the
+ * caller reads plan_dev (status, T_out, order, offsets, slots) and the first
+ * ceil(T_out / B) entries of each table. A plan status of CM_ENONFINITE (a score
+ * is not finite) or CM_EINVAL (the free list is shorter than the render needs;
+ * *n_fresh_dev then holds the number needed) means nothing was rendered and the
+ * non-colliding Ids were not written.
+ * free_host / free_dev: n_free page ids (host, checked: pages of the pool,
+ * distinct, no fragment page; and its device copy). k_table_dev, v_table_dev:
+ * device, ceil(sum of the lengths / B) int32 each; n_fresh_dev: device, one
+ * int64. Other arguments as cm_paged_order and cm_paged_render_hash (the same
+ * P * H * B limit). Workspace: cm_paged_workspace_size() bytes. */
+int32_t cm_paged_deliveries(const cm_pagedset* set, int32_t routing_layer, int64_t tail_len,
+                            const cm_rope* rope, const int32_t* free_host,
+                            const int32_t* free_dev, int64_t n_free, double* keys_dev,
+                            uint8_t* mask_dev, uint8_t* digests_dev, int64_t* plan_dev,
+                            int32_t* k_table_dev, int32_t* v_table_dev, int64_t* n_fresh_dev,
+                            void* workspace, size_t workspace_bytes, void* stream);
 int32_t cm_paged_workspace_size(const cm_pagedset* set, size_t* bytes_out);
 
 /* ---------------------------------------------------------------- timing

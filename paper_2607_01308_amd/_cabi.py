@@ -34,7 +34,7 @@ EXPORTS = (
     "cm_render_merge_devplan", "cm_render_merge_range", "cm_render_merge_hash", "cm_render_set",
     "cm_render_deliveries", "cm_render_deliveries_noalloc",
     "cm_paged_workspace_size", "cm_paged_order", "cm_paged_hash_select", "cm_paged_tables",
-    "cm_paged_render", "cm_paged_render_hash",
+    "cm_paged_render", "cm_paged_render_hash", "cm_paged_deliveries",
     "cm_timing_enable", "cm_timing_reset", "cm_timing_query",
 )
 
@@ -126,6 +126,8 @@ def lib() -> ctypes.CDLL:
             "cm_paged_render": (I32, [PS, P, P, ctypes.POINTER(CmRope), P, P, P, I64, P, SZ, P]),
             "cm_paged_render_hash": (I32, [PS, P, P, ctypes.POINTER(CmRope), P, P, P, P, P, P, P,
                                            SZ, P]),
+            "cm_paged_deliveries": (I32, [PS, I32, I64, ctypes.POINTER(CmRope), P, P, I64, P, P,
+                                          P, P, P, P, P, P, SZ, P]),
             "cm_timing_enable": (I32, [I32]),
             "cm_timing_reset": (I32, []),
             "cm_timing_query": (I32, [ctypes.c_char_p, ctypes.POINTER(ctypes.c_double),

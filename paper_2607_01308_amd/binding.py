@@ -318,6 +318,26 @@ def paged_order(pset: PagedSet, routing_layer: int, tail_len: int, keys: torch.T
                                    _stream(stream, pset)), "cm_paged_order")
 
 
+def paged_deliveries(pset: PagedSet, routing_layer: int, tail_len: int, rope_base: float,
+                     style: str, free_host: np.ndarray, free_dev: torch.Tensor,
+                     keys: torch.Tensor, mask: torch.Tensor, digests: torch.Tensor,
+                     plan_dev: torch.Tensor, k_table: torch.Tensor, v_table: torch.Tensor,
+                     n_fresh: torch.Tensor, workspace: torch.Tensor, stream=None) -> None:
+    """cm_paged_deliveries: steps 1-5 over the pool in one call (scores, the
+    colliding Ids, the plan, the block tables on the device, the render with the
+    other Ids), nothing waiting for the host. free_host and free_dev: the same
+    free page ids (host, for the check; device, for the tables)."""
+    fh = np.ascontiguousarray(free_host, dtype=np.int32)
+    rope = C.CmRope(base=float(rope_base), style=_STYLES[style], reserved=0)
+    C.check(C.lib().cm_paged_deliveries(ctypes.byref(pset.struct), routing_layer, tail_len,
+                                        ctypes.byref(rope), fh.ctypes.data_as(ctypes.c_void_p),
+                                        _ptr(free_dev), int(fh.size), _ptr(keys), _ptr(mask),
+                                        _ptr(digests), _ptr(plan_dev), _ptr(k_table),
+                                        _ptr(v_table), _ptr(n_fresh), _ptr(workspace),
+                                        workspace.numel() * workspace.element_size(),
+                                        _stream(stream, pset)), "cm_paged_deliveries")
+
+
 def paged_hash_select(pset: PagedSet, select: torch.Tensor, value: int, digests: torch.Tensor,
                       workspace: torch.Tensor, workgroups_per_cu: int = 0, stream=None) -> None:
     """cm_paged_hash_select: the Ids of the paged fragments i with select[i] == value."""

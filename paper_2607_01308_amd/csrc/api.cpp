@@ -844,13 +844,15 @@ int32_t cm_paged_workspace_size(const cm_pagedset* set, size_t* bytes_out) {
   return CM_OK;
 }
 
-int32_t cm_paged_order(const cm_pagedset* set, int32_t routing_layer, int64_t tail_len,
-                       double* keys_dev, uint8_t* mask_dev, uint8_t* digests_dev,
-                       int64_t* plan_dev, void* workspace, size_t workspace_bytes, void* stream) {
-  g_err.clear();
-  cm::PagedDesc p;
-  int32_t st = check_pagedset(set, &p);
-  if (st != CM_OK) return st;
+}  // extern "C"
+
+namespace {
+
+// Argument checks of steps 1-3 on a paged set (cm_paged_order and
+// cm_paged_deliveries).
+int32_t check_paged_order_args(const cm::PagedDesc& p, int32_t routing_layer, int64_t tail_len,
+                               const double* keys_dev, const uint8_t* mask_dev,
+                               const uint8_t* digests_dev, const int64_t* plan_dev) {
   const cm::SetDesc& s = p.s;
   if (routing_layer < 0 || routing_layer >= s.L)
     return fail(CM_EINVAL, "routing_layer must be in [0, L), got " + std::to_string(routing_layer));
@@ -863,19 +865,103 @@ int32_t cm_paged_order(const cm_pagedset* set, int32_t routing_layer, int64_t ta
   if (!digests_dev || !aligned(digests_dev, 16))
     return fail(CM_EINVAL, "digests_dev is NULL or not 16-byte aligned");
   if (!plan_dev || !aligned(plan_dev, 8)) return fail(CM_EINVAL, "plan_dev is NULL or misaligned");
-  if ((st = check_ws(workspace, workspace_bytes, paged_ws(p))) != CM_OK) return st;
-  uint8_t* ws = static_cast<uint8_t*>(workspace);
-  hipStream_t sm = static_cast<hipStream_t>(stream);
-  // scores, the deliveries whose digest the order reads (a key equal to
-  // another's), their Ids, the order; the other Ids are left to
-  // cm_paged_hash_select, which can run beside the render
+  return CM_OK;
+}
+
+// Steps 1-3 on a paged set: scores, the deliveries whose digest the order reads
+// (a key equal to another's), their Ids, the order. The other Ids are left to
+// the caller (cm_paged_hash_select beside the render, or the fused render).
+hipError_t enqueue_paged_order(const cm::PagedDesc& p, int32_t routing_layer, int64_t tail_len,
+                               double* keys_dev, uint8_t* mask_dev, uint8_t* digests_dev,
+                               int64_t* plan_dev, uint8_t* ws, hipStream_t sm) {
+  const cm::SetDesc& s = p.s;
   hipError_t e = cm::launch_knorm_paged(p, cm::knorm_layout(s, tail_len), routing_layer, tail_len,
                                         keys_dev, ws, sm);
   if (e == hipSuccess) e = cm::launch_equal_key_mask(s, keys_dev, mask_dev, sm);
   if (e == hipSuccess)
     e = cm::launch_hash_paged(p, cm::hash_layout(s), mask_dev, 1, digests_dev, ws, sm);
   if (e == hipSuccess) e = cm::launch_order(s, keys_dev, digests_dev, true, plan_dev, sm);
+  return e;
+}
+
+// A free-page list: pages of the pool, distinct, holding no fragment row.
+int32_t check_free_pages(const cm_pagedset* set, const int32_t* free_host, int64_t n_free) {
+  if (n_free < 0 || (n_free > 0 && !free_host)) return fail(CM_EINVAL, "free_host is NULL");
+  std::vector<uint8_t> used((size_t)set->pages, 0);
+  for (int64_t k = 0; k < set->n_blocks; ++k) used[(size_t)set->blocks_host[k]] = 1;
+  for (int64_t k = 0; k < n_free; ++k) {
+    const int32_t q = free_host[k];
+    if (q < 0 || q >= set->pages || used[(size_t)q])
+      return fail(CM_EINVAL, "free page " + std::to_string(k) +
+                                 " is outside the pool, repeated or holds a fragment page");
+    used[(size_t)q] = 2;
+  }
+  return CM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t cm_paged_order(const cm_pagedset* set, int32_t routing_layer, int64_t tail_len,
+                       double* keys_dev, uint8_t* mask_dev, uint8_t* digests_dev,
+                       int64_t* plan_dev, void* workspace, size_t workspace_bytes, void* stream) {
+  g_err.clear();
+  cm::PagedDesc p;
+  int32_t st = check_pagedset(set, &p);
+  if (st != CM_OK) return st;
+  if ((st = check_paged_order_args(p, routing_layer, tail_len, keys_dev, mask_dev, digests_dev,
+                                   plan_dev)) != CM_OK)
+    return st;
+  if ((st = check_ws(workspace, workspace_bytes, paged_ws(p))) != CM_OK) return st;
+  hipError_t e = enqueue_paged_order(p, routing_layer, tail_len, keys_dev, mask_dev, digests_dev,
+                                     plan_dev, static_cast<uint8_t*>(workspace),
+                                     static_cast<hipStream_t>(stream));
   return e == hipSuccess ? CM_OK : fail_hip(e, "cm_paged_order");
+}
+
+int32_t cm_paged_deliveries(const cm_pagedset* set, int32_t routing_layer, int64_t tail_len,
+                            const cm_rope* rope, const int32_t* free_host,
+                            const int32_t* free_dev, int64_t n_free, double* keys_dev,
+                            uint8_t* mask_dev, uint8_t* digests_dev, int64_t* plan_dev,
+                            int32_t* k_table_dev, int32_t* v_table_dev, int64_t* n_fresh_dev,
+                            void* workspace, size_t workspace_bytes, void* stream) {
+  g_err.clear();
+  cm::PagedDesc p;
+  int32_t st = check_pagedset(set, &p);
+  if (st != CM_OK) return st;
+  if ((uint64_t)set->pages * (uint64_t)set->H * (uint64_t)set->block > 0xFFFFFFFFull)
+    return fail(CM_ESHAPE, "pages * H * block must be below 2^32 for the fused paged render");
+  if ((st = check_rope(rope)) != CM_OK) return st;
+  if ((st = check_paged_order_args(p, routing_layer, tail_len, keys_dev, mask_dev, digests_dev,
+                                   plan_dev)) != CM_OK)
+    return st;
+  if ((st = check_free_pages(set, free_host, n_free)) != CM_OK) return st;
+  if (n_free > 0 && (!free_dev || !aligned(free_dev, 4)))
+    return fail(CM_EINVAL, "free_dev is NULL or misaligned");
+  if (!k_table_dev || !v_table_dev || !aligned(k_table_dev, 4) || !aligned(v_table_dev, 4))
+    return fail(CM_EINVAL, "k_table_dev / v_table_dev NULL or misaligned");
+  if (!n_fresh_dev || !aligned(n_fresh_dev, 8))
+    return fail(CM_EINVAL, "n_fresh_dev is NULL or misaligned");
+  if ((st = check_ws(workspace, workspace_bytes, paged_ws(p))) != CM_OK) return st;
+  int64_t T_all = 0;
+  for (int i = 0; i < p.s.n; ++i) T_all += p.s.T(i);
+  const int64_t nbo_cap = (T_all + p.block - 1) / p.block;
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  hipStream_t sm = static_cast<hipStream_t>(stream);
+  // steps 1-3 (the colliding deliveries' Ids), the block tables, then the
+  // render with every other Id from its loads, in workspace that each step
+  // takes over from the one before
+  hipError_t e = enqueue_paged_order(p, routing_layer, tail_len, keys_dev, mask_dev, digests_dev,
+                                     plan_dev, ws, sm);
+  if (e == hipSuccess)
+    e = cm::launch_paged_tables(p, plan_dev, free_dev, n_free, nbo_cap, k_table_dev, v_table_dev,
+                                n_fresh_dev, sm);
+  if (e == hipSuccess)
+    e = cm::launch_paged_render_hash(p, cm::hash_layout(p.s), cm::render_layout(p.s), plan_dev,
+                                     rope->base, rope->style, mask_dev, k_table_dev, v_table_dev,
+                                     digests_dev, ws, sm);
+  return e == hipSuccess ? CM_OK : fail_hip(e, "cm_paged_deliveries");
 }
 
 int32_t cm_paged_hash_select(const cm_pagedset* set, const uint8_t* select_dev,
@@ -910,17 +996,7 @@ int32_t cm_paged_tables(const cm_pagedset* set, const int64_t* plan_host, const 
   if ((st = check_plan_host(p.s, plan_host, &nu)) != CM_OK) return st;
   if (!k_table_host || !v_table_host || !fresh_host || !n_fresh)
     return fail(CM_EINVAL, "output pointer is NULL");
-  if (n_free < 0 || (n_free > 0 && !free_host)) return fail(CM_EINVAL, "free_host is NULL");
-  // free pages: inside the pool, distinct, used by no fragment
-  std::vector<uint8_t> used((size_t)p.pages, 0);
-  for (int64_t k = 0; k < set->n_blocks; ++k) used[(size_t)set->blocks_host[k]] = 1;
-  for (int64_t k = 0; k < n_free; ++k) {
-    const int32_t q = free_host[k];
-    if (q < 0 || q >= p.pages || used[(size_t)q])
-      return fail(CM_EINVAL, "free page " + std::to_string(k) +
-                                 " is outside the pool, repeated or holds a fragment page");
-    used[(size_t)q] = 2;
-  }
+  if ((st = check_free_pages(set, free_host, n_free)) != CM_OK) return st;
   const int64_t B = p.block;
   const int64_t T_out = plan_host[CM_PLAN_TOUT];
   const int64_t nbo = (T_out + B - 1) / B;

@@ -224,6 +224,11 @@ hipError_t launch_paged_render_hash(const PagedDesc& p, const HashLayout& hlay,
                                     int32_t style, const uint8_t* select, const int32_t* k_table,
                                     const int32_t* v_table, uint8_t* digests, uint8_t* ws,
                                     hipStream_t stream);
+// Merged K and V block tables of the plan on the device (cm_paged_tables' rule;
+// paged.hip). nbo_cap: the tables' capacity in blocks.
+hipError_t launch_paged_tables(const PagedDesc& p, int64_t* plan_dev, const int32_t* free_dev,
+                               int64_t n_free, int64_t nbo_cap, int32_t* k_table,
+                               int32_t* v_table, int64_t* n_fresh, hipStream_t stream);
 hipError_t launch_paged_render(const PagedDesc& p, const int64_t* plan_dev, int32_t n_unique,
                                double base, int32_t style, const int32_t* k_table,
                                const int32_t* v_table, const int32_t* fresh, int64_t n_fresh,

@@ -159,7 +159,118 @@ __global__ __launch_bounds__(64) void paged_render_kernel(
   }
 }
 
+// Block tables of a plan's merged cache, built on the device by one workgroup
+// with the rule of cm_paged_tables: merged block j (rows [jB, min(jB + B,
+// T_out))) keeps the page of its slot's fragment when all its rows come from
+// that slot and start at one of the fragment's page boundaries (V), and the
+// slot is at offset 0 (K: R(0) = I); every other block takes the next page of
+// `free` in block order, K before V. Each thread takes a run of consecutive
+// blocks: a count, a scan of the counts, then the assignment. A free list too
+// short for the plan leaves the tables unwritten and the plan's status
+// CM_EINVAL (n_fresh: the pages needed), so nothing is rendered; a plan whose
+// status is already an error is left as it is (n_fresh: 0).
+__global__ __launch_bounds__(1024) void paged_tables_kernel(
+    int64_t* __restrict__ plan, int32_t n, const int64_t* __restrict__ table,
+    const int32_t* __restrict__ blocks, int32_t b_shift, const int32_t* __restrict__ free_pages,
+    int64_t n_free, int64_t nbo_cap, int32_t* __restrict__ k_table,
+    int32_t* __restrict__ v_table, int64_t* __restrict__ n_fresh) {
+  __shared__ int64_t s_off[CM_MAX_FRAGMENTS];
+  __shared__ int64_t s_len[CM_MAX_FRAGMENTS];
+  __shared__ int64_t s_first[CM_MAX_FRAGMENTS];
+  __shared__ int64_t scan[1024];
+  const int tid = threadIdx.x, nt = blockDim.x;
+  if (plan[CM_PLAN_STATUS] != CM_OK) {
+    if (tid == 0) *n_fresh = 0;
+    return;
+  }
+  const int n_u = (int)plan[CM_PLAN_NUNIQUE];
+  const int64_t T_out = plan[CM_PLAN_TOUT];
+  const int64_t B = (int64_t)1 << b_shift;
+  const int64_t nbo = (T_out + B - 1) >> b_shift;
+  if (n_u < 1 || n_u > n || nbo > nbo_cap) {     // not a plan of this set (checked on the
+    if (tid == 0) {                              // host for every other entry point)
+      *n_fresh = 0;
+      plan[CM_PLAN_STATUS] = CM_ESHAPE;
+    }
+    return;
+  }
+  for (int s = tid; s < n_u; s += nt) {
+    s_off[s] = plan[CM_PLAN_HEADER + n + s];
+    s_len[s] = plan[CM_PLAN_HEADER + 2 * (int64_t)n + s];
+    s_first[s] = table[2 * plan[CM_PLAN_HEADER + s] + 1];
+  }
+  __syncthreads();
+  const int64_t per = (nbo + nt - 1) / nt;
+  const int64_t j0 = (int64_t)tid * per < nbo ? (int64_t)tid * per : nbo;
+  const int64_t j1 = j0 + per < nbo ? j0 + per : nbo;
+  // slot holding row j0 * B (offsets increase over the slots)
+  int s0 = 0;
+  {
+    int hi = n_u - 1;
+    while (s0 < hi) {
+      const int mid = (s0 + hi + 1) >> 1;
+      if (s_off[mid] <= j0 * B) s0 = mid; else hi = mid - 1;
+    }
+  }
+  // block j: the fragment page it may keep (-1: none) and whether K may keep it
+  auto reuse = [&](int64_t j, int& s, int32_t& page, bool& k_too) {
+    const int64_t r0 = j * B;
+    while (s + 1 < n_u && s_off[s + 1] <= r0) ++s;
+    const int64_t e = r0 + B < T_out ? r0 + B : T_out;
+    const int64_t t0 = r0 - s_off[s];
+    const bool whole = e <= s_off[s] + s_len[s] && (t0 & (B - 1)) == 0;
+    page = whole ? blocks[s_first[s] + (t0 >> b_shift)] : -1;
+    k_too = s_off[s] == 0;
+  };
+  int64_t cnt = 0;
+  {
+    int s = s0;
+    for (int64_t j = j0; j < j1; ++j) {
+      int32_t page;
+      bool k_too;
+      reuse(j, s, page, k_too);
+      cnt += (page >= 0 ? 0 : 1) + ((page >= 0 && k_too) ? 0 : 1);
+    }
+  }
+  scan[tid] = cnt;
+  __syncthreads();
+  for (int o = 1; o < nt; o <<= 1) {
+    const int64_t t = tid >= o ? scan[tid - o] : 0;
+    __syncthreads();
+    scan[tid] += t;
+    __syncthreads();
+  }
+  const int64_t total = scan[nt - 1];
+  if (total > n_free) {
+    if (tid == 0) {
+      *n_fresh = total;
+      plan[CM_PLAN_STATUS] = CM_EINVAL;
+    }
+    return;
+  }
+  int64_t next = scan[tid] - cnt;
+  int s = s0;
+  for (int64_t j = j0; j < j1; ++j) {
+    int32_t page;
+    bool k_too;
+    reuse(j, s, page, k_too);
+    k_table[j] = (page >= 0 && k_too) ? page : free_pages[next++];
+    v_table[j] = page >= 0 ? page : free_pages[next++];
+  }
+  if (tid == 0) *n_fresh = total;
+}
+
 }  // namespace
+
+hipError_t launch_paged_tables(const PagedDesc& p, int64_t* plan_dev, const int32_t* free_dev,
+                               int64_t n_free, int64_t nbo_cap, int32_t* k_table,
+                               int32_t* v_table, int64_t* n_fresh, hipStream_t stream) {
+  ScopedTiming tm(K_RENDER_PREP, stream);
+  hipLaunchKernelGGL(paged_tables_kernel, dim3(1), dim3(1024), 0, stream, plan_dev, p.s.n,
+                     p.s.table_dev, p.blocks_dev, p.b_shift, free_dev, n_free, nbo_cap, k_table,
+                     v_table, n_fresh);
+  return hipGetLastError();
+}
 
 hipError_t launch_paged_render(const PagedDesc& p, const int64_t* plan_dev, int32_t n_unique,
                                double base, int32_t style, const int32_t* k_table,

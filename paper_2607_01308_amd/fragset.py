@@ -19,7 +19,6 @@ current stream) and allocates its buffers there. Scratch memory is cached per
 
 from __future__ import annotations
 
-from dataclasses import dataclass
 from typing import Dict, List, Optional, Sequence, Union
 
 import numpy as np
@@ -31,7 +30,7 @@ from .binding import (FragmentBatch, bag_plan, canonical_order, equal_key_mask, 
                       paged_render, paged_tables, paged_workspace_size, render_merge,
                       render_deliveries_async, render_merge_devplan, render_merge_hash,
                       render_merge_range, render_set, workspace_size, paged_order,
-                      paged_hash_select, paged_render_hash)
+                      paged_hash_select, paged_render_hash, paged_deliveries)
 from .binding import PagedSet
 
 _WS: Dict[tuple, torch.Tensor] = {}
@@ -499,15 +498,72 @@ class MergedCache:
         return self.cache
 
 
-@dataclass
 class PagedRender:
-    k_table: np.ndarray          # page id of each merged block of K (B rows)
-    v_table: np.ndarray          # the same for V
-    fresh: np.ndarray            # pages written by the render, as codes 2j + kv
-    T_out: int
-    plan: Optional[np.ndarray] = None              # render_paged_set: the plan it computed
-    digests_dev: Optional[torch.Tensor] = None     # render_paged_set: [n, 32] Ids
-    keys_dev: Optional[torch.Tensor] = None        # render_paged_set: [n] scores S_i
+    """Block tables of a paged render (page id of each merged block of B rows,
+    K and V; the fresh pages written, as codes 2j + kv, K first, by page id;
+    T_out) and, for render_paged_set, the plan, Ids and scores it computed. A
+    render enqueued with nothing waiting for the host (render_paged_set's fused
+    path) fills the host fields on their first use, which waits for its copies;
+    a plan it rejected (a score that is not finite, a free list too short)
+    raises there."""
+
+    def __init__(self, k_table=None, v_table=None, fresh=None, T_out=None, plan=None,
+                 digests_dev=None, keys_dev=None, pending=None):
+        self._k_table, self._v_table, self._fresh = k_table, v_table, fresh
+        self._T_out, self._plan = T_out, plan
+        self.digests_dev = digests_dev      # render_paged_set: [n, 32] Ids
+        self.keys_dev = keys_dev            # render_paged_set: [n] scores S_i
+        self._pending = pending             # (event, pinned copy, plan length, capacity, B,
+                                            #  fragment pages)
+
+    def _finish(self) -> None:
+        if self._pending is None:
+            return
+        event, pinned, pe, cap, B, frag_pages = self._pending
+        event.synchronize()
+        buf = pinned.numpy()
+        plan = buf[:pe].copy()
+        if int(plan[C.PLAN_STATUS]) == C.CM_EINVAL:
+            raise C.CmError(C.CM_EINVAL, "cm_paged_deliveries",
+                            f"the free list is shorter than the render needs ({int(buf[pe])} "
+                            "pages); nothing was rendered")
+        _check_plan(plan, "cm_paged_deliveries")
+        T_out = int(plan[C.PLAN_TOUT])
+        nbo = (T_out + B - 1) // B
+        tabs = buf[pe + 1:].view(np.int32)
+        kt, vt = tabs[:nbo].copy(), tabs[cap:cap + nbo].copy()
+        # every page that is not a fragment page came from the free list
+        kf = np.nonzero(~np.isin(kt, frag_pages))[0]
+        vf = np.nonzero(~np.isin(vt, frag_pages))[0]
+        fresh = np.concatenate([2 * kf[np.argsort(kt[kf], kind="stable")],
+                                2 * vf[np.argsort(vt[vf], kind="stable")] + 1]).astype(np.int32)
+        self._k_table, self._v_table, self._fresh = kt, vt, fresh
+        self._T_out, self._plan, self._pending = T_out, plan, None
+
+    @property
+    def k_table(self) -> np.ndarray:
+        self._finish()
+        return self._k_table
+
+    @property
+    def v_table(self) -> np.ndarray:
+        self._finish()
+        return self._v_table
+
+    @property
+    def fresh(self) -> np.ndarray:
+        self._finish()
+        return self._fresh
+
+    @property
+    def T_out(self) -> int:
+        self._finish()
+        return self._T_out
+
+    @property
+    def plan(self) -> Optional[np.ndarray]:
+        self._finish()
+        return self._plan
 
     @property
     def reused_pages(self) -> int:
@@ -543,16 +599,20 @@ def paged_fused_fits(pset: PagedSet) -> bool:
 def render_paged_set(pset: PagedSet, routing_layer: int, rope_base: float, free_pages,
                      style: str = "half", stream=None, fused: Optional[bool] = None,
                      hash_workgroups_per_cu: int = 1) -> PagedRender:
-    """Steps 1-5 on fragments that live only in the pool (§4.5): scores, the Ids
-    the order reads (deliveries whose key equals another's), dedupe, order and
-    offsets on the device (cm_paged_order), the plan to the host for the block
-    tables, then the render of every merged row that no fragment page holds
-    already and, from the same loads, the remaining Ids (the content address of
-    each fragment's dense form): cm_paged_render_hash, the paged counterpart of
-    the dense path's fused kernel. fused=False (the default for a pool too large
-    for that kernel's 32-bit row index) renders with cm_paged_render instead and
-    hashes the remaining Ids beside it on a second stream with
-    hash_workgroups_per_cu chunk workgroups per CU, each byte then read twice.
+    """Steps 1-5 on fragments that live only in the pool (§4.5).
+
+    fused (the default when the pool fits its 32-bit row index): one call,
+    cm_paged_deliveries, with nothing waiting for the host: scores, the Ids the
+    order reads (deliveries whose key equals another's), dedupe, order and
+    offsets, the merged block tables built on the device from free_pages, then
+    the render of every merged row that no fragment page holds already with the
+    remaining Ids (the content address of each fragment's dense form) from the
+    same loads. The plan and tables reach the host on first use of the result.
+
+    fused=False: cm_paged_order, the plan to the host, the block tables there,
+    cm_paged_render, and the remaining Ids beside it on a second stream with
+    hash_workgroups_per_cu chunk workgroups per CU (each byte read twice).
+
     No dense copy of any fragment is made; the result's digests wait for all of
     its work."""
     if fused is None:
@@ -565,35 +625,46 @@ def render_paged_set(pset: PagedSet, routing_layer: int, rope_base: float, free_
         keys = torch.empty(pset.n, dtype=torch.float64, device=dev)
         mask = torch.empty(pset.n, dtype=torch.uint8, device=dev)
         digests = torch.empty((pset.n, 32), dtype=torch.uint8, device=dev)
-        plan_dev = torch.empty(plan_elems(pset.n), dtype=torch.int64, device=dev)
-        paged_order(pset, routing_layer, min(pset.lengths), keys, mask, digests, plan_dev, ws, main)
+        pe = plan_elems(pset.n)
         if fused:
-            plan_host = _plan_to_host(plan_dev, main)
+            # plan, pages taken and both tables in one buffer, copied back once
+            cap = (sum(pset.lengths) + pset.B - 1) // pset.B
+            out = torch.empty(pe + 1 + cap, dtype=torch.int64, device=dev)
+            tabs = out[pe + 1:].view(torch.int32)
+            free_host = np.ascontiguousarray(np.asarray(free_pages, dtype=np.int32))
+            staged = torch.empty(max(free_host.size, 1), dtype=torch.int32, pin_memory=True)
+            staged[:free_host.size].copy_(torch.from_numpy(free_host))
+            free_dev = staged.to(dev, non_blocking=True)
+            paged_deliveries(pset, routing_layer, min(pset.lengths), rope_base, style, free_host,
+                             free_dev, keys, mask, digests, out[:pe], tabs[:cap],
+                             tabs[cap:2 * cap], out[pe:pe + 1], ws, main)
+            pinned = torch.empty(out.numel(), dtype=torch.int64, pin_memory=True)
+            pinned.copy_(out, non_blocking=True)
+            done = torch.cuda.Event()
+            done.record(main)
+            return PagedRender(digests_dev=digests, keys_dev=keys,
+                               pending=(done, pinned, pe, cap, pset.B, pset.blocks_host))
+        plan_dev = torch.empty(pe, dtype=torch.int64, device=dev)
+        paged_order(pset, routing_layer, min(pset.lengths), keys, mask, digests, plan_dev, ws, main)
+        ready = torch.cuda.Event()
+        ready.record(main)
+        side = _side_stream(dev)
+        side.wait_event(ready)
+        with torch.cuda.stream(side):
+            ws_side = torch.empty(need, dtype=torch.uint8, device=dev)
+        paged_hash_select(pset, mask, 0, digests, ws_side, hash_workgroups_per_cu, side)
+        for t in (mask, digests, ws_side):
+            t.record_stream(side)
+        side_done = torch.cuda.Event()
+        side_done.record(side)
+        plan_host = _plan_to_host(plan_dev, main)
+        try:
             _check_plan(plan_host, "cm_paged_order")
             kt, vt, fresh = paged_tables(pset, plan_host, free_pages)
             kd, vd = torch.from_numpy(kt).to(dev), torch.from_numpy(vt).to(dev)
-            paged_render_hash(pset, plan_dev, plan_host, rope_base, style, kt, vt, kd, vd, mask,
-                              digests, ws, main)
-        else:
-            ready = torch.cuda.Event()
-            ready.record(main)
-            side = _side_stream(dev)
-            side.wait_event(ready)
-            with torch.cuda.stream(side):
-                ws_side = torch.empty(need, dtype=torch.uint8, device=dev)
-            paged_hash_select(pset, mask, 0, digests, ws_side, hash_workgroups_per_cu, side)
-            for t in (mask, digests, ws_side):
-                t.record_stream(side)
-            side_done = torch.cuda.Event()
-            side_done.record(side)
-            plan_host = _plan_to_host(plan_dev, main)
-            try:
-                _check_plan(plan_host, "cm_paged_order")
-                kt, vt, fresh = paged_tables(pset, plan_host, free_pages)
-                kd, vd = torch.from_numpy(kt).to(dev), torch.from_numpy(vt).to(dev)
-                fd = torch.from_numpy(fresh).to(dev)
-                paged_render(pset, plan_dev, plan_host, rope_base, style, kd, vd, fd, ws, main)
-            finally:
-                main.wait_event(side_done)       # the digests are complete once main is
+            fd = torch.from_numpy(fresh).to(dev)
+            paged_render(pset, plan_dev, plan_host, rope_base, style, kd, vd, fd, ws, main)
+        finally:
+            main.wait_event(side_done)       # the digests are complete once main is
     return PagedRender(k_table=kt, v_table=vt, fresh=fresh, T_out=int(plan_host[C.PLAN_TOUT]),
                        plan=plan_host, digests_dev=digests, keys_dev=keys)

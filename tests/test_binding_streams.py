@@ -111,7 +111,7 @@ def test_every_enqueuing_call_is_covered():
     takes_stream = {name for name, f in inspect.getmembers(binding, inspect.isfunction)
                     if "stream" in inspect.signature(f).parameters and not name.startswith("_")}
     assert takes_stream == set(CALLS) | {"paged_render", "paged_order", "paged_hash_select",
-                                         "paged_render_hash"}
+                                         "paged_render_hash", "paged_deliveries"}
 
 
 @pytest.mark.parametrize("name", sorted(CALLS))
@@ -141,6 +141,16 @@ def test_paged_render_hash_marks_both_tables(fake_lib):
     assert [t.streams for t in pset.device_tables] == [[s], [s]]
     assert fake_lib.calls[-1][0] == "cm_paged_render_hash"
     assert fake_lib.calls[-1][1].value == 34
+
+
+def test_paged_deliveries_marks_both_tables(fake_lib):
+    pset = _owner(2)
+    s = FakeStream(35)
+    free = np.zeros(4, dtype=np.int32)
+    binding.paged_deliveries(pset, 0, 1, 1e4, "half", free, T, T, T, T, T, T, T, T, T, s)
+    assert [t.streams for t in pset.device_tables] == [[s], [s]]
+    assert fake_lib.calls[-1][0] == "cm_paged_deliveries"
+    assert fake_lib.calls[-1][1].value == 35
 
 
 def test_paged_order_marks_both_tables(fake_lib):

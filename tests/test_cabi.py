@@ -523,3 +523,38 @@ def test_paged_render_hash_argument_checks(lib):
     fp.s.pages = 1 << 27                                  # P * H * B = 2^32
     assert call() == C.CM_ESHAPE
     assert "2^32" in lib.cm_last_error().decode()
+
+
+def test_paged_deliveries_argument_checks(lib):
+    """cm_paged_deliveries runs cm_paged_order's checks, the fused render's pool
+    limit and a check of the free list (pages of the pool, distinct, no fragment
+    page) before anything is enqueued; with every argument right it stops at
+    the missing workspace, its last check."""
+    fp = FakePaged((30, 50), spare=64)
+    rope = C.CmRope(base=1e4, style=0, reserved=0)
+    need = ctypes.c_size_t(0)
+    assert lib.cm_paged_workspace_size(fp.ref, ctypes.byref(need)) == C.CM_OK
+    D = ctypes.c_void_p
+
+    def call(free=fp.free, layer=1, tail=30, kt=D(0x90000), nf=D(0xA0000), fdev=D(0xB0000),
+             ws_bytes=0, fp=fp):
+        free = np.ascontiguousarray(free, dtype=np.int32)
+        return lib.cm_paged_deliveries(fp.ref, layer, tail, ctypes.byref(rope),
+                                       free.ctypes.data_as(ctypes.c_void_p), fdev,
+                                       int(free.size), D(0x30000), D(0x70000), D(0x40000),
+                                       D(0x50000), kt, D(0x98000), nf, D(0x60000), ws_bytes,
+                                       None)
+
+    assert call() == C.CM_EWORKSPACE                      # every other check passed
+    assert call(ws_bytes=need.value - 1) == C.CM_EWORKSPACE
+    assert call(free=fp.free[:0], fdev=None) == C.CM_EWORKSPACE   # an empty list is allowed
+    assert call(free=[fp.pages[1][0]]) == C.CM_EINVAL     # a fragment's page
+    assert call(free=[fp.free[0], fp.free[0]]) == C.CM_EINVAL
+    assert call(free=[fp.P]) == C.CM_EINVAL               # outside the pool
+    assert call(fdev=None) == C.CM_EINVAL
+    assert call(kt=None) == C.CM_EINVAL
+    assert call(nf=D(0xA0004)) == C.CM_EINVAL             # misaligned
+    assert call(layer=2) == C.CM_EINVAL
+    assert call(tail=31) == C.CM_EINVAL
+    fp.s.pages = 1 << 27                                  # P * H * B = 2^32
+    assert call() == C.CM_ESHAPE

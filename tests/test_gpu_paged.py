@@ -15,6 +15,7 @@ import torch
 
 import synth
 import paper_2607_01308_amd as cm
+from paper_2607_01308_amd import _cabi as C
 from gpu_util import (check_render, k_close, k_stats, log, oracle_ids, oracle_keys,
                       oracle_layers, oracle_plan)
 
@@ -165,9 +166,13 @@ def test_paged_set_steps_1_to_5_against_oracle(case, fused):
     del dl
     torch.cuda.synchronize()
     log(f"[paged-set] {case} fused={fused}")
-    pr = cm.render_paged_set(cm.PagedSet(pool, lengths, page_lists), w.routing_layer, w.rope_base,
-                             free, fused=fused)
+    pset = cm.PagedSet(pool, lengths, page_lists)
+    pr = cm.render_paged_set(pset, w.routing_layer, w.rope_base, free, fused=fused)
     torch.cuda.synchronize()
+    # the tables (built on the device by the one-call path) follow cm_paged_tables' rule
+    kt, vt, fresh = cm.paged_tables(pset, pr.plan, free)
+    assert np.array_equal(pr.k_table, kt) and np.array_equal(pr.v_table, vt)
+    assert np.array_equal(pr.fresh, fresh)
     assert [bytes(x) for x in pr.digests_dev.cpu().numpy()] == ids
     assert list(pr.keys_dev.cpu().numpy()) == keys
     n = len(ids)
@@ -188,3 +193,27 @@ def test_paged_set_steps_1_to_5_against_oracle(case, fused):
         assert ok, f"K of layer {l} outside tolerance"
     log(f"  paged set: {n} deliveries, {plan['n_unique']} slots, T_out {pr.T_out}, "
         f"K largest distance {worst} ulp")
+
+
+def test_paged_deliveries_with_too_few_free_pages():
+    """The one-call paged path builds its block tables on the device; a free list
+    shorter than the render needs is reported through the plan (CM_EINVAL, with
+    the number of pages needed) when the result is read, and no page of the pool
+    is written."""
+    w = synth.custom("paged-short", dtype="bfloat16", d=128, H=2, L=2, lengths=(300, 517, 45),
+                     routing_layer=1, rope_base=1e4)
+    dl = synth.make_deliveries(w, synth.make_fragments(w, device="cuda"))
+    pool, lengths, page_lists, free = synth.make_paged(dl, 16, spare_pages=64, seed=2)
+    del dl
+    before = pool.clone()
+    pset = cm.PagedSet(pool, lengths, page_lists)
+    log("[paged-short]")
+    pr = cm.render_paged_set(pset, w.routing_layer, w.rope_base, free[:5], fused=True)
+    torch.cuda.synchronize()
+    with pytest.raises(cm.CmError) as e:
+        pr.k_table
+    assert e.value.status == C.CM_EINVAL and "free list" in str(e.value)
+    assert torch.equal(pool, before)
+    # with room for every merged block it renders
+    pr = cm.render_paged_set(pset, w.routing_layer, w.rope_base, free, fused=True)
+    assert pr.T_out == sum(lengths) and len(pr.fresh) > 5
