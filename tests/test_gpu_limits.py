@@ -4,7 +4,8 @@
   fragments of 1 to 48 tokens (so T* = 1), 324 re-deliveries drawn at random
   and 40 pairs with equal K (ties broken by the digest); every layer is
   compared with the oracle, and the serial pipeline and the render of the
-  ingested set equal the fused one.
+  ingested set equal the fused one. The same deliveries on pages of 8 tokens,
+  through the one-call paged path, equal the dense render.
 * A tensor past 2 GiB: one layer of 8 heads x 1.2M tokens (2.46 GB for each of
   K and V) next to a 3-token fragment that sorts first, so the long one is
   rotated at offset 3. Keys, Ids, order, and the first, middle and last rows
@@ -71,6 +72,35 @@ def test_max_fragments_per_call():
     from_set = S.render(w.routing_layer, w.rope_base)
     torch.cuda.synchronize()
     assert torch.equal(serial.merged, res.merged) and torch.equal(from_set.merged, res.merged)
+
+
+def test_max_fragments_on_pages():
+    """The same 1024 deliveries stored only on 1 KiB pages (8 tokens each),
+    through the one-call paged path: 700 slots and about 2,100 merged blocks for
+    the device-built block tables. Ids, scores and plan equal the dense path's
+    (checked against the oracle above), the tables follow cm_paged_tables' rule,
+    and the merged cache read back through them equals the dense render."""
+    w = _max_fragments_workload()
+    dl = synth.make_deliveries(w, synth.make_fragments(w, device="cuda"))
+    res = cm.render_deliveries(dl, w.routing_layer, w.rope_base)
+    torch.cuda.synchronize()
+    B = 8
+    spare = 2 * (sum(w.lengths) // B + len(w.lengths) + 1)
+    pool, lengths, page_lists, free = synth.make_paged(dl, B, spare_pages=spare, seed=7)
+    del dl
+    pset = cm.PagedSet(pool, lengths, page_lists)
+    log(f"[limits-paged] {w.n_deliveries} deliveries on pages of {B} tokens")
+    pr = cm.render_paged_set(pset, w.routing_layer, w.rope_base, free, fused=True)
+    torch.cuda.synchronize()
+    assert np.array_equal(pr.plan, res.plan)
+    assert torch.equal(pr.digests_dev, res.digests_dev)
+    assert torch.equal(pr.keys_dev, res.keys_dev)
+    kt, vt, fresh = cm.paged_tables(pset, pr.plan, free)
+    assert np.array_equal(pr.k_table, kt) and np.array_equal(pr.v_table, vt)
+    assert np.array_equal(pr.fresh, fresh)
+    K = synth.gather_paged(pool, pr.k_table, pr.T_out)[:, 0]
+    V = synth.gather_paged(pool, pr.v_table, pr.T_out)[:, 1]
+    assert torch.equal(K, res.merged[:, 0]) and torch.equal(V, res.merged[:, 1])
 
 
 def test_tensor_larger_than_2gib():

@@ -137,12 +137,16 @@ SET_CASES = [
     dict(dtype="bfloat16", d=32, B=32, H=2, L=2, lengths=(99, 64, 1, 200)),     # 64-byte rows, T=1
     dict(dtype="bfloat16", d=256, B=8, H=4, L=2, lengths=(1030, 77, 513)),     # 512-byte rows
     dict(dtype="float32", d=256, B=16, H=1, L=2, lengths=(257, 4096)),         # 1 KiB rows, 16 KiB pages
+    dict(dtype="bfloat16", d=128, B=16, H=2, L=2, lengths=(1,)),               # one token: all pages kept
+    dict(dtype="float32", d=32, B=32, H=1, L=2, lengths=(3,),
+         deliveries=(0, 0, 0)),                                               # one fragment, three times
 ]
 
 
 @pytest.mark.parametrize("fused", [True, False], ids=["fused", "overlapped"])
 @pytest.mark.parametrize("case", SET_CASES,
-                         ids=[f"{c['dtype']}-d{c['d']}-B{c['B']}" for c in SET_CASES])
+                         ids=[f"{c['dtype']}-d{c['d']}-B{c['B']}-n{len(c.get('deliveries', c['lengths']))}"
+                              for c in SET_CASES])
 def test_paged_set_steps_1_to_5_against_oracle(case, fused):
     """render_paged_set on a pool holding every delivery (copies on pages of
     their own): the Ids are the dense form's content addresses, the scores and
