@@ -368,8 +368,9 @@ __device__ __forceinline__ void render_hash_body(
 
     // The steps of a full stripe (every lane owns 16 blocks): step k waits for
     // blocks 2k, 2k + 1 (x, loaded one step earlier); outputs step k - 1 (prev);
-    // loads step k + 1 into nx (the last step loads itself again, so every
-    // step issues the same loads), and, when re-reading, the partner pair of
+    // loads step k + 1 into nx (the last step loads 128 bytes of the slot's
+    // angle table instead, lines that stay cached, so that every step issues
+    // the same loads), and, when re-reading, the partner pair of
     // step k into pn; then compresses its two blocks. The phases are kept apart
     // so that the fp64 rotation and the compression never hold registers at the
     // same time; every memory operation older than a step's wait was issued a
@@ -414,7 +415,15 @@ __device__ __forceinline__ void render_hash_body(
           }
         }
         __builtin_amdgcn_sched_barrier(0);
-        load2(p0, p1, (k + 1 < 8 ? k + 1 : k) * 2);
+        if (k + 1 < 8) {
+          load2(p0, p1, (k + 1) * 2);
+        } else {
+          // the same loads from a line every wave keeps cached: the slot's
+          // angle table (at least 128 bytes: d >= 16)
+          const uint8_t* hot = reinterpret_cast<const uint8_t*>(ang);
+          load_block(p0, hot);
+          load_block(p1, hot + 64);
+        }
         if constexpr (SPLIT && !KEEP) {
           // the partner pair of step k, needed when step k is output
           if ((k % PPR) >= HP) load2(k0, k1, 2 * (k - HP));
