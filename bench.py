@@ -261,6 +261,18 @@ def other_workload(name, seed, steps, warmup, dev):
     ms_set, pct_set, _ = time_steps(render, steps, warmup, kernel_timing=False)
     _, _, kern = time_steps(whole, steps, 0)
     _, _, kern_set = time_steps(render, steps, 0)
+    # the whole path captured into a HIP graph per input copy, replayed: one
+    # launch per step instead of one per kernel
+    graphs = [cm.RenderGraph(bt, w.routing_layer, w.rope_base) for bt in batches]
+    replay = lambda i: graphs[i % n].replay()
+    ms_g, pct_g, _ = time_steps(replay, steps, warmup, kernel_timing=False)
+    rg, re_ = graphs[0].replay(), whole(0)
+    graph_equal = bool(torch.equal(rg.merged, re_.merged) and torch.equal(rg.digests_dev,
+                                                                          re_.digests_dev))
+    del rg, re_
+    for g in graphs:
+        g.close()
+    del graphs
     b = w.render_bytes
     out = {
         "render_bytes": b, "deliveries": w.n_deliveries, "distinct": w.n_distinct,
@@ -271,6 +283,12 @@ def other_workload(name, seed, steps, warmup, dev):
                        "merges_per_s": round(1e3 / ms, 1),
                        "launches_per_step": round(sum(v["launches"] for v in kern.values()) / steps, 1),
                        "kernels_ms": {k: round(v["total_ms"] / steps, 4) for k, v in kern.items()}},
+        "whole_path_graph": {"ms": round(ms_g, 4), "ms_p10_p50_p90": pct_g,
+                             "GBps": round(b / (ms_g / 1e3) / 1e9, 1),
+                             "pct_hbm_peak": round(100 * b / (ms_g / 1e3) / 1e9 / HBM_PEAK_GBPS, 2),
+                             "merges_per_s": round(1e3 / ms_g, 1), "equals_eager": graph_equal,
+                             "what": "the whole path captured into a HIP graph per input copy "
+                                     "(RenderGraph), replayed: one launch per step"},
         "render_set": {"ms": round(ms_set, 4), "ms_p10_p50_p90": pct_set,
                        "GBps": round(b / (ms_set / 1e3) / 1e9, 1),
                        "pct_hbm_peak": round(100 * b / (ms_set / 1e3) / 1e9 / HBM_PEAK_GBPS, 2),

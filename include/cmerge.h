@@ -27,6 +27,8 @@
  *   cm_render_merge_hash    the render plus the remaining Ids from its loads
  *   cm_render_deliveries    steps 1-5 over a batch of deliveries in one call, with
  *                           no host round trip
+ *   cm_render_deliveries_graph / cm_graph_launch / cm_graph_destroy
+ *                           the same call captured into a HIP graph and replayed
  *
  * Conventions
  *   - Every function returns int32_t: CM_OK (0) or a negative cm_status. No
@@ -323,6 +325,29 @@ int32_t cm_render_deliveries_noalloc(const cm_fragset* set, int32_t routing_laye
                                      int64_t tail_len, const cm_rope* rope, double* keys_dev,
                                      uint8_t* mask_dev, uint8_t* digests_dev, int64_t* plan_dev,
                                      void* out_dev, int64_t T_cap, void* stream);
+
+/* cm_render_deliveries captured into a HIP graph, for callers that repeat the
+ * same merge shape (Render of Alg. 2 after Ingest; steps 1-5) and are bound by
+ * kernel launches (small sets): cm_graph_launch then enqueues every kernel of
+ * the call with one launch. The graph holds the call's arguments: the set's
+ * device table and fragment tensors, keys_dev, mask_dev, digests_dev, plan_dev,
+ * out_dev and the workspace must stay allocated, at the same addresses, until
+ * cm_graph_destroy, and each launch reads the fragment tensors as they are then
+ * (write new contents of the same shapes into them between launches). The
+ * arguments are checked as in cm_render_deliveries (the host tables are read
+ * once, here); nothing is enqueued by this call. Launches that overlap (or that
+ * overlap other calls using the same buffers) race. *graph_out: an opaque
+ * handle, NULL on error. */
+typedef struct cm_graph cm_graph;
+int32_t cm_render_deliveries_graph(const cm_fragset* set, int32_t routing_layer, int64_t tail_len,
+                                   const cm_rope* rope, double* keys_dev, uint8_t* mask_dev,
+                                   uint8_t* digests_dev, int64_t* plan_dev, void* out_dev,
+                                   int64_t T_cap, void* workspace, size_t workspace_bytes,
+                                   cm_graph** graph_out);
+/* Enqueue the captured kernels on `stream`. CM_EINVAL for a NULL graph. */
+int32_t cm_graph_launch(cm_graph* graph, void* stream);
+/* Free a graph (NULL is allowed). Launches already enqueued still run. */
+int32_t cm_graph_destroy(cm_graph* graph);
 
 /* ---------------------------------------------------------------- paged render
  * Paged KV storage (the merge as a permutation of already-allocated blocks plus

@@ -32,7 +32,8 @@ EXPORTS = (
     "cm_fragment_hash", "cm_fragment_hash_select", "cm_fragment_knorm", "cm_equal_key_mask",
     "cm_canonical_order", "cm_multiset_order", "cm_bag_plan", "cm_render_merge",
     "cm_render_merge_devplan", "cm_render_merge_range", "cm_render_merge_hash", "cm_render_set",
-    "cm_render_deliveries", "cm_render_deliveries_noalloc",
+    "cm_render_deliveries", "cm_render_deliveries_noalloc", "cm_render_deliveries_graph",
+    "cm_graph_launch", "cm_graph_destroy",
     "cm_paged_workspace_size", "cm_paged_order", "cm_paged_hash_select", "cm_paged_tables",
     "cm_paged_render", "cm_paged_render_hash", "cm_paged_deliveries",
     "cm_timing_enable", "cm_timing_reset", "cm_timing_query",
@@ -119,6 +120,10 @@ def lib() -> ctypes.CDLL:
                                            I64, P, SZ, P]),
             "cm_render_deliveries_noalloc": (I32, [FS, I32, I64, ctypes.POINTER(CmRope), P, P, P,
                                                    P, P, I64, P]),
+            "cm_render_deliveries_graph": (I32, [FS, I32, I64, ctypes.POINTER(CmRope), P, P, P, P,
+                                                 P, I64, P, SZ, ctypes.POINTER(P)]),
+            "cm_graph_launch": (I32, [P, P]),
+            "cm_graph_destroy": (I32, [P]),
             "cm_paged_workspace_size": (I32, [PS, ctypes.POINTER(SZ)]),
             "cm_paged_order": (I32, [PS, I32, I64, P, P, P, P, P, SZ, P]),
             "cm_paged_hash_select": (I32, [PS, P, I32, P, I32, P, SZ, P]),

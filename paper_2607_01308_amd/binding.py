@@ -212,6 +212,39 @@ def render_deliveries_async(batch: FragmentBatch, routing_layer: int, tail_len: 
                                          _stream(stream, batch)), "cm_render_deliveries")
 
 
+def render_deliveries_graph(batch: FragmentBatch, routing_layer: int, tail_len: int,
+                            rope_base: float, style: str, keys: torch.Tensor, mask: torch.Tensor,
+                            digests: torch.Tensor, plan_dev: torch.Tensor, out: torch.Tensor,
+                            T_cap: int, workspace: torch.Tensor) -> ctypes.c_void_p:
+    """cm_render_deliveries_graph: the call of render_deliveries_async captured
+    into a HIP graph over these buffers (nothing is enqueued); returns the
+    handle for graph_launch / graph_destroy."""
+    rope = C.CmRope(base=float(rope_base), style=_STYLES[style], reserved=0)
+    handle = ctypes.c_void_p(0)
+    C.check(C.lib().cm_render_deliveries_graph(ctypes.byref(batch.struct), routing_layer,
+                                               tail_len, ctypes.byref(rope), _ptr(keys),
+                                               _ptr(mask), _ptr(digests), _ptr(plan_dev),
+                                               _ptr(out), T_cap, _ptr(workspace),
+                                               workspace.numel() * workspace.element_size(),
+                                               ctypes.byref(handle)),
+            "cm_render_deliveries_graph")
+    return handle
+
+
+def graph_launch(handle: ctypes.c_void_p, owner, stream=None) -> None:
+    """cm_graph_launch: every kernel of the captured call, one launch on `stream`
+    (owner: the batch whose device tables the kernels read, marked as in use
+    there)."""
+    if not handle:
+        raise ValueError("graph handle is NULL")
+    C.check(C.lib().cm_graph_launch(handle, _stream(stream, owner)), "cm_graph_launch")
+
+
+def graph_destroy(handle: ctypes.c_void_p) -> None:
+    """cm_graph_destroy."""
+    C.check(C.lib().cm_graph_destroy(handle), "cm_graph_destroy")
+
+
 def render_set(batch: FragmentBatch, digests: torch.Tensor, routing_layer: int, tail_len: int,
                rope_base: float, style: str, keys: torch.Tensor, plan_dev: torch.Tensor,
                out: torch.Tensor, T_out: int, workspace: torch.Tensor, stream=None) -> None:

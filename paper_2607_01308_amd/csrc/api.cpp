@@ -142,6 +142,8 @@ const char* const kKernelNames[cm::K_COUNT] = {
     "order",     "key_mask",  "render_prep", "render",     "render_hash", "paged",
     "paged_hash_render"};
 std::atomic<bool> g_timing{false};
+// set while this thread captures a call into a graph: no timing events then
+thread_local bool t_capturing = false;
 std::mutex g_tmu;
 struct Pending {
   int id;
@@ -206,7 +208,7 @@ int device_cu_count() {
 }
 
 ScopedTiming::ScopedTiming(int kernel_id, hipStream_t stream) : id_(kernel_id), stream_(stream) {
-  if (!g_timing.load(std::memory_order_relaxed)) return;
+  if (t_capturing || !g_timing.load(std::memory_order_relaxed)) return;
   start_ = take_event();
   if (start_ && hipEventRecord(start_, stream_) != hipSuccess) start_ = nullptr;
 }
@@ -581,7 +583,8 @@ int32_t render_deliveries_common(const cm_fragset* set, int32_t routing_layer, i
                                  const cm_rope* rope, double* keys_dev, uint8_t* mask_dev,
                                  uint8_t* digests_dev, int64_t* plan_dev, void* out_dev,
                                  int64_t T_cap, void* workspace, size_t workspace_bytes,
-                                 bool fixed_scratch, void* stream, const char* where) {
+                                 bool fixed_scratch, void* stream, const char* where,
+                                 bool check_only = false) {
   g_err.clear();
   cm::SetDesc s;
   int32_t st = check_set(set, &s);
@@ -617,6 +620,7 @@ int32_t render_deliveries_common(const cm_fragset* set, int32_t routing_layer, i
   } else if ((st = check_ws(workspace, workspace_bytes, need)) != CM_OK) {
     return st;
   }
+  if (check_only) return CM_OK;
   uint8_t* ws = static_cast<uint8_t*>(workspace);
   hipStream_t sm = static_cast<hipStream_t>(stream);
   // the workspace is reused by each stage in turn: they run in order on one stream
@@ -664,6 +668,82 @@ int32_t cm_render_deliveries_noalloc(const cm_fragset* set, int32_t routing_laye
   return render_deliveries_common(set, routing_layer, tail_len, rope, keys_dev, mask_dev,
                                   digests_dev, plan_dev, out_dev, T_cap, nullptr, 0, true, stream,
                                   "cm_render_deliveries_noalloc");
+}
+
+}  // extern "C"
+
+struct cm_graph {
+  hipGraph_t graph;
+  hipGraphExec_t exec;
+};
+
+extern "C" {
+
+int32_t cm_render_deliveries_graph(const cm_fragset* set, int32_t routing_layer, int64_t tail_len,
+                                   const cm_rope* rope, double* keys_dev, uint8_t* mask_dev,
+                                   uint8_t* digests_dev, int64_t* plan_dev, void* out_dev,
+                                   int64_t T_cap, void* workspace, size_t workspace_bytes,
+                                   cm_graph** graph_out) {
+  g_err.clear();
+  if (!graph_out) return fail(CM_EINVAL, "graph_out is NULL");
+  *graph_out = nullptr;
+  // the arguments first, on the host
+  int32_t st = render_deliveries_common(set, routing_layer, tail_len, rope, keys_dev, mask_dev,
+                                        digests_dev, plan_dev, out_dev, T_cap, workspace,
+                                        workspace_bytes, false, nullptr,
+                                        "cm_render_deliveries_graph", true);
+  if (st != CM_OK) return st;
+  // capture on a stream of this call's own (the caller's may be the null
+  // stream, which cannot be captured); nothing runs until the graph is launched
+  hipStream_t cs = nullptr;
+  hipError_t e = hipStreamCreateWithFlags(&cs, hipStreamNonBlocking);
+  if (e != hipSuccess) return fail_hip(e, "cm_render_deliveries_graph");
+  e = hipStreamBeginCapture(cs, hipStreamCaptureModeThreadLocal);
+  if (e != hipSuccess) {
+    (void)hipStreamDestroy(cs);
+    return fail_hip(e, "cm_render_deliveries_graph");
+  }
+  t_capturing = true;
+  st = render_deliveries_common(set, routing_layer, tail_len, rope, keys_dev, mask_dev,
+                                digests_dev, plan_dev, out_dev, T_cap, workspace, workspace_bytes,
+                                false, cs, "cm_render_deliveries_graph");
+  t_capturing = false;
+  const std::string err = g_err;       // a failed launch's message, if any
+  hipGraph_t g = nullptr;
+  e = hipStreamEndCapture(cs, &g);
+  (void)hipStreamDestroy(cs);
+  if (st != CM_OK) {
+    if (g) (void)hipGraphDestroy(g);
+    g_err = err;
+    return st;
+  }
+  if (e != hipSuccess) return fail_hip(e, "cm_render_deliveries_graph");
+  if (!g) return fail(CM_EHIP, "cm_render_deliveries_graph: the capture gave no graph");
+  hipGraphExec_t x = nullptr;
+  e = hipGraphInstantiate(&x, g, nullptr, nullptr, 0);
+  if (e != hipSuccess) {
+    (void)hipGraphDestroy(g);
+    return fail_hip(e, "cm_render_deliveries_graph");
+  }
+  *graph_out = new cm_graph{g, x};
+  return CM_OK;
+}
+
+int32_t cm_graph_launch(cm_graph* graph, void* stream) {
+  g_err.clear();
+  if (!graph) return fail(CM_EINVAL, "graph is NULL");
+  const hipError_t e = hipGraphLaunch(graph->exec, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? CM_OK : fail_hip(e, "cm_graph_launch");
+}
+
+int32_t cm_graph_destroy(cm_graph* graph) {
+  g_err.clear();
+  if (!graph) return CM_OK;
+  hipError_t e = hipGraphExecDestroy(graph->exec);
+  const hipError_t e2 = hipGraphDestroy(graph->graph);
+  delete graph;
+  if (e == hipSuccess) e = e2;
+  return e == hipSuccess ? CM_OK : fail_hip(e, "cm_graph_destroy");
 }
 
 }  // extern "C"

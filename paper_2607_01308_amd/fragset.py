@@ -30,7 +30,8 @@ from .binding import (FragmentBatch, bag_plan, canonical_order, equal_key_mask, 
                       paged_render, paged_tables, paged_workspace_size, render_merge,
                       render_deliveries_async, render_merge_devplan, render_merge_hash,
                       render_merge_range, render_set, workspace_size, paged_order,
-                      paged_hash_select, paged_render_hash, paged_deliveries)
+                      paged_hash_select, paged_render_hash, paged_deliveries,
+                      render_deliveries_graph, graph_launch, graph_destroy)
 from .binding import PagedSet
 
 _WS: Dict[tuple, torch.Tensor] = {}
@@ -496,6 +497,65 @@ class MergedCache:
         self.last_rows = T_out - (int(plan[C.PLAN_HEADER + n + first]) if first < n_u else T_out)
         self.slot_ids, self.T_out = slot_ids, T_out
         return self.cache
+
+
+class RenderGraph:
+    """Steps 1-5 of one batch of deliveries captured into a HIP graph
+    (cm_render_deliveries_graph) over buffers this object owns: replay()
+    enqueues every kernel of the whole path with one launch, for callers that
+    merge sets of the same shape again and again and are bound by kernel
+    launches (small sets run the path's kernels in tens of microseconds). Each
+    replay reads the fragment tensors as they are then: write new contents into
+    the same tensors in place to merge new data. The result of a replay is
+    valid until the next replay, which writes the same buffers."""
+
+    def __init__(self, deliveries: Union[FragmentBatch, Sequence], routing_layer: int,
+                 rope_base: float, style: str = "half"):
+        self.batch = (deliveries if isinstance(deliveries, FragmentBatch)
+                      else FragmentBatch(deliveries))
+        b = self.batch
+        dev = b.device
+        self.ws = torch.empty(max(workspace_size(b), 256), dtype=torch.uint8, device=dev)
+        self.digests = torch.empty((b.n, 32), dtype=torch.uint8, device=dev)
+        self.keys = torch.empty(b.n, dtype=torch.float64, device=dev)
+        self.mask = torch.empty(b.n, dtype=torch.uint8, device=dev)
+        self.plan_dev = torch.empty(plan_elems(b.n), dtype=torch.int64, device=dev)
+        self.tail = min(b.lengths)
+        self.T_cap = int(sum(b.lengths))
+        self.out = torch.empty(b.L * 2 * b.H * self.T_cap * b.d, dtype=b.torch_dtype, device=dev)
+        self._handle = None
+        torch.cuda.synchronize(dev)           # the buffers exist before the graph refers to them
+        self._handle = render_deliveries_graph(b, routing_layer, self.tail, rope_base, style,
+                                               self.keys, self.mask, self.digests,
+                                               self.plan_dev, self.out, self.T_cap, self.ws)
+
+    def replay(self, stream=None) -> RenderResult:
+        if self._handle is None:
+            raise RuntimeError("the graph was closed")
+        b = self.batch
+        main = _main_stream(b.device, stream)
+        with torch.cuda.stream(main):
+            graph_launch(self._handle, b, main)
+            pinned = torch.empty(self.plan_dev.numel(), dtype=torch.int64, pin_memory=True)
+            pinned.copy_(self.plan_dev, non_blocking=True)
+            done = torch.cuda.Event()
+            done.record(main)
+        return RenderResult(digests_dev=self.digests, keys_dev=self.keys, tail_len=self.tail,
+                            plan_dev=self.plan_dev,
+                            pending=(done, pinned, self.out, (b.L, b.H, b.d),
+                                     "cm_render_deliveries_graph"))
+
+    def close(self) -> None:
+        """Free the graph (its buffers go with this object)."""
+        if self._handle is not None:
+            handle, self._handle = self._handle, None
+            graph_destroy(handle)
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
 
 
 class PagedRender:

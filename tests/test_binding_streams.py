@@ -111,7 +111,7 @@ def test_every_enqueuing_call_is_covered():
     takes_stream = {name for name, f in inspect.getmembers(binding, inspect.isfunction)
                     if "stream" in inspect.signature(f).parameters and not name.startswith("_")}
     assert takes_stream == set(CALLS) | {"paged_render", "paged_order", "paged_hash_select",
-                                         "paged_render_hash", "paged_deliveries"}
+                                         "paged_render_hash", "paged_deliveries", "graph_launch"}
 
 
 @pytest.mark.parametrize("name", sorted(CALLS))
@@ -151,6 +151,17 @@ def test_paged_deliveries_marks_both_tables(fake_lib):
     assert [t.streams for t in pset.device_tables] == [[s], [s]]
     assert fake_lib.calls[-1][0] == "cm_paged_deliveries"
     assert fake_lib.calls[-1][1].value == 35
+
+
+def test_graph_launch_marks_the_batch_tables(fake_lib):
+    """A graph's kernels read the batch's device table at every launch."""
+    batch = _owner(1)
+    s = FakeStream(36)
+    binding.graph_launch(ctypes.c_void_p(0x1234), batch, s)
+    assert batch.device_tables[0].streams == [s]
+    assert fake_lib.calls[-1][0] == "cm_graph_launch" and fake_lib.calls[-1][1].value == 36
+    with pytest.raises(ValueError):
+        binding.graph_launch(ctypes.c_void_p(0), batch, s)
 
 
 def test_paged_order_marks_both_tables(fake_lib):

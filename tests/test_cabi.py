@@ -558,3 +558,31 @@ def test_paged_deliveries_argument_checks(lib):
     assert call(tail=31) == C.CM_EINVAL
     fp.s.pages = 1 << 27                                  # P * H * B = 2^32
     assert call() == C.CM_ESHAPE
+
+
+def test_render_deliveries_graph_argument_checks(lib):
+    """cm_render_deliveries_graph checks its arguments on the host, as
+    cm_render_deliveries does, before it creates anything (no device is needed
+    to reach these answers); the graph calls take NULL as documented."""
+    rope = C.CmRope(base=1e4, style=0, reserved=0)
+    fs = FakeSet(lengths=(5, 9))
+    _, need = _ws(lib, fs)
+    D = ctypes.c_void_p
+
+    def call(layer=1, tail=5, T_cap=14, ws_bytes=need, out=D(0x80000), g=True):
+        handle = ctypes.c_void_p(0x77)
+        st = lib.cm_render_deliveries_graph(fs.ref, layer, tail, ctypes.byref(rope), D(0x10000),
+                                            D(0x20000), D(0x30000), D(0x50000), out, T_cap,
+                                            D(0x60000), ws_bytes,
+                                            ctypes.byref(handle) if g else None)
+        return st, handle.value
+
+    st, h = call(layer=2)
+    assert st == C.CM_EINVAL and h is None                # the handle is cleared on error
+    assert call(tail=6)[0] == C.CM_EINVAL
+    assert call(T_cap=13)[0] == C.CM_ESHAPE
+    assert call(ws_bytes=need - 1)[0] == C.CM_EWORKSPACE
+    assert call(out=None)[0] == C.CM_EINVAL
+    assert call(g=False)[0] == C.CM_EINVAL
+    assert lib.cm_graph_destroy(None) == C.CM_OK
+    assert lib.cm_graph_launch(None, None) == C.CM_EINVAL
