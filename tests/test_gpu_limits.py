@@ -6,6 +6,8 @@
   compared with the oracle, and the serial pipeline and the render of the
   ingested set equal the fused one. The same deliveries on pages of 8 tokens,
   through the one-call paged path, equal the dense render.
+* A page pool whose slices pass 4 GiB, with pages on both sides: the paged
+  paths equal the dense render.
 * A tensor past 2 GiB: one layer of 8 heads x 1.2M tokens (2.46 GB for each of
   K and V) next to a 3-token fragment that sorts first, so the long one is
   rotated at offset 3. Keys, Ids, order, and the first, middle and last rows
@@ -101,6 +103,34 @@ def test_max_fragments_on_pages():
     K = synth.gather_paged(pool, pr.k_table, pr.T_out)[:, 0]
     V = synth.gather_paged(pool, pr.v_table, pr.T_out)[:, 1]
     assert torch.equal(K, res.merged[:, 0]) and torch.equal(V, res.merged[:, 1])
+
+
+def test_paged_pool_past_4gib():
+    """A pool whose (layer, K/V) slice holds 4.6 GB (140,000 pages of 16 bf16
+    rows of 8 heads x 128), so fragment and fresh pages sit past 4 GiB: the
+    one-call paged path (32-bit pool rows, 64-bit byte offsets) and the
+    two-stream form equal the dense render."""
+    w = synth.custom("big-pool", dtype="bfloat16", d=128, H=8, L=1, lengths=(3000, 1000, 7),
+                     routing_layer=0, seed=11)
+    dl = synth.make_deliveries(w, synth.make_fragments(w, device="cuda"))
+    res = cm.render_deliveries(dl, w.routing_layer, w.rope_base)
+    torch.cuda.synchronize()
+    need = sum((T + 15) // 16 for T in w.lengths)
+    P = 140_000
+    pool, lengths, page_lists, free = synth.make_paged(dl, 16, spare_pages=P - need, seed=3)
+    assert pool.shape[2] == P and pool[0, 0].numel() * pool.element_size() > 4 * 2**30
+    assert max(max(p) for p in page_lists) >= 2**32 // (8 * 16 * 128 * 2)   # past 4 GiB
+    log(f"[limits-pool] {pool.numel() * pool.element_size() / 1e9:.1f} GB pool")
+    pset = cm.PagedSet(pool, lengths, page_lists)
+    for fused in (True, False):
+        pr = cm.render_paged_set(pset, w.routing_layer, w.rope_base, free[::-1], fused=fused)
+        torch.cuda.synchronize()
+        assert np.array_equal(pr.plan, res.plan)
+        assert torch.equal(pr.digests_dev, res.digests_dev)
+        assert max(pr.k_table.max(), pr.v_table.max()) >= 2**32 // (8 * 16 * 128 * 2)
+        K = synth.gather_paged(pool, pr.k_table, pr.T_out)[:, 0]
+        V = synth.gather_paged(pool, pr.v_table, pr.T_out)[:, 1]
+        assert torch.equal(K, res.merged[:, 0]) and torch.equal(V, res.merged[:, 1])
 
 
 def test_tensor_larger_than_2gib():
