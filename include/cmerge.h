@@ -27,6 +27,9 @@
  *   cm_render_merge_hash    the render plus the remaining Ids from its loads
  *   cm_render_deliveries    steps 1-5 over a batch of deliveries in one call, with
  *                           no host round trip
+ *   cm_render_deliveries_noalloc
+ *                           the same with no workspace argument, for callers that
+ *                           cannot allocate
  *   cm_render_deliveries_graph / cm_graph_launch / cm_graph_destroy
  *                           the same call captured into a HIP graph and replayed
  *
