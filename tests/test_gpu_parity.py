@@ -552,3 +552,32 @@ def test_results_on_two_streams_and_read_late():
         assert np.array_equal(res.plan, ref.plan)
         assert res.digests == ref.digests
         assert torch.equal(res.merged, ref.merged)
+
+
+def test_eight_streams_of_independent_merges():
+    """Eight different sets merged at once, one per caller stream, three rounds
+    issued before any result is read: each result equals that set's render made
+    alone, which the oracle checks for two of them."""
+    ws, dls, refs = [], [], []
+    for k in range(8):
+        w = synth.custom(f"streams8-{k}", dtype=["bfloat16", "float32"][k % 2], d=64 * (1 + k % 2),
+                         H=1 + k % 3, L=2, lengths=(17 + 31 * k, 40 + 7 * k, 3 + k),
+                         deliveries=(0, 1, 2, k % 3), routing_layer=k % 2, seed=40 + k)
+        _, dl = gpu_deliveries(w)
+        ws.append(w)
+        dls.append(dl)
+        refs.append(_run(w, dl))
+    for k in (0, 5):
+        check_render(refs[k], dls[k], ws[k].dtype, ws[k].routing_layer, ws[k].rope_base)
+    streams = [torch.cuda.Stream() for _ in range(8)]
+    torch.cuda.synchronize()
+    pending = []
+    for rep in range(3):
+        for k, st in enumerate(streams):
+            pending.append((refs[k], cm.render_deliveries(dls[k], ws[k].routing_layer,
+                                                          ws[k].rope_base, stream=st)))
+    log(f"[streams8] {len(pending)} merges issued")
+    for ref, res in pending:
+        assert np.array_equal(res.plan, ref.plan)
+        assert res.digests == ref.digests
+        assert torch.equal(res.merged, ref.merged)
