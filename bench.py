@@ -569,6 +569,15 @@ def main():
             "traffic": _traffic("render_hash", w.name),
             "ops_per_launch": ops, "hashed_bytes": hashed_bytes, "rotated_elements": rotated,
             "avg_ms": round(avg * 1e3, 4), "hbm_GBps": round(render_bytes / avg / 1e9, 1)}
+        # the fused paged kernel does the same work (same plan, same deliveries
+        # hashed, same elements rotated) on the pool
+        pms = paged.get("set_steps_1_to_5", {}).get("kernels_ms", {}).get("paged_hash_render")
+        if pms:
+            achp = ops / (pms / 1e3) / 1e12
+            paged["set_steps_1_to_5"]["roofline"] = {
+                "kernel": "paged_hash_render", "bound": "alu", "achieved": round(achp, 3),
+                "peak": round(VALU_PEAK_TOPS, 3), "unit": "Tops/s",
+                "frac": round(achp / VALU_PEAK_TOPS, 4), "ops_per_launch": ops, "avg_ms": pms}
     if "render" in set_kernels:
         pk = set_kernels["render"]
         avg = pk["total_ms"] / pk["launches"] / 1e3
