@@ -15,6 +15,7 @@
 // one more launch does). Fragments stored in a page pool are hashed by a chunk
 // kernel that walks each chunk's blocks through the page list in the order of
 // the dense layout, so the Id does not depend on the storage.
+#include "blake3_quad.h"
 #include "chunk_ops.h"
 #include "key_mask.h"
 #include "knorm_fold.h"
@@ -44,8 +45,9 @@ __device__ __forceinline__ int find_fragment(const int64_t* __restrict__ base, i
 
 // base[v][i] = number of level-v nodes of fragments 0..i-1 (all 2L tensors each);
 // base[v][n] = total nodes at level v; row levels+1 holds the same prefix sums
-// of the (tensor, stripe) tasks of the chunk kernel. One workgroup, block-wide
-// inclusive scans.
+// of the (tensor, stripe) tasks of the chunk kernel. One workgroup. A one-wave
+// workgroup (n <= 64) gives each row a lane that walks the fragments in order,
+// all rows at once; a wider one runs a block-wide inclusive scan per row.
 __device__ __forceinline__ void hash_tables(const int64_t* __restrict__ table, int32_t n,
                                             int64_t stride, int64_t token_bytes, int32_t L,
                                             int32_t levels, int64_t* __restrict__ base,
@@ -53,6 +55,22 @@ __device__ __forceinline__ void hash_tables(const int64_t* __restrict__ table, i
   __shared__ int64_t sc[1024];
   const int tid = threadIdx.x;
   if (tid < n) arrived[tid] = 0;
+  if (blockDim.x == 64) {
+    if (tid < n) sc[tid] = table[(int64_t)tid * stride] * token_bytes;
+    __syncthreads();
+    for (int v = tid; v <= levels + 1; v += 64) {
+      int64_t* row = base + (int64_t)v * (n + 1);
+      int64_t acc = 0;
+      for (int i = 0; i < n; ++i) {
+        const int64_t bytes = sc[i];
+        row[i] = acc;
+        acc += 2 * (int64_t)L * (v <= levels ? nodes_at(chunks_of(bytes), v) : stripes_of(bytes));
+      }
+      row[n] = acc;
+    }
+    __syncthreads();
+    return;
+  }
   const int64_t bytes = tid < n ? table[(int64_t)tid * stride] * token_bytes : 0;
   const int64_t m0 = tid < n ? chunks_of(bytes) : 0;
   for (int v = 0; v <= levels + 1; ++v) {
@@ -290,10 +308,40 @@ __global__ __launch_bounds__(kSubLanes) void hash_subtree_kernel(
 // [p * 8 + w][lane slot], lds_w words apart per value) into one, level by level:
 // value j of a level is the BLAKE3 parent of values 2j and 2j+1 of the level
 // below, an unpaired last value is carried up. ROOT marks the final compression
-// when root is set. All 64 lanes of the (one-wave) workgroup take part.
+// when root is set. All 64 lanes of the (one-wave) workgroup take part. A level
+// of at most 16 values is made by quads (b3_compress_quad: value j by lanes
+// 4j .. 4j + 3), which shortens the chain of dependent compressions about 2x;
+// a wider level takes one lane per value.
 __device__ __forceinline__ void fold_cvs(uint32_t* lds, int cnt, bool root, int lane) {
+  const int Q = lane >> 2;
+  const int q = lane & 3;
   while (cnt > 1) {
     const int nn = (cnt + 1) >> 1;
+    const uint32_t flags = kB3Parent | (root && nn == 1 ? kB3Root : 0u);
+    if (nn <= 16) {
+      uint32_t m[16];
+      uint32_t lo = 0, hi = 0;
+      const bool pair = Q < nn && 2 * Q + 1 < cnt;   // uniform over the quad
+      if (pair) {
+#pragma unroll
+        for (int k = 0; k < 16; ++k) m[k] = lds[(2 * Q) * 8 + k];
+      } else if (Q < nn) {
+        lo = lds[(2 * Q) * 8 + q];
+        hi = lds[(2 * Q) * 8 + 4 + q];
+      }
+      __syncthreads();
+      if (pair) {
+        b3_init_quad(lo, hi, (q & 1) != 0, (q & 2) != 0);
+        b3_compress_quad(lo, hi, m, 0, 64, flags, (q & 1) != 0, (q & 2) != 0);
+      }
+      if (Q < nn) {
+        lds[Q * 8 + q] = lo;
+        lds[Q * 8 + 4 + q] = hi;
+      }
+      __syncthreads();
+      cnt = nn;
+      continue;
+    }
     uint32_t m[16];
     const bool pair = lane < nn && 2 * lane + 1 < cnt;
     const bool copy = lane < nn && 2 * lane + 1 >= cnt;
@@ -309,7 +357,7 @@ __device__ __forceinline__ void fold_cvs(uint32_t* lds, int cnt, bool root, int 
     if (pair) {
       B3Cv cv;
       b3_init(cv);
-      b3_compress(cv, m, 0, 64, kB3Parent | (root && nn == 1 ? kB3Root : 0u));
+      b3_compress(cv, m, 0, 64, flags);
 #pragma unroll
       for (int k = 0; k < 8; ++k) lds[lane * 8 + k] = cv.h[k];
     } else if (copy) {
@@ -356,6 +404,25 @@ __device__ __forceinline__ void fragment_id(uint64_t T, const IdShape& sh,
       load_block64(r + (g - 1) * 64, w);
     }
   };
+  if (chunks <= 16) {
+    // up to 255 layers: quad j hashes chunk j (b3_chunk_quad), a chain of at
+    // most 16 compressions of about half the latency of one lane's
+    const int Q = lane >> 2;
+    const int q = lane & 3;
+    if (Q < chunks) {
+      const int64_t g0 = (int64_t)Q * kB3ChunkBlocks;
+      const int64_t nb = blocks - g0 < kB3ChunkBlocks ? blocks - g0 : kB3ChunkBlocks;
+      uint32_t lo, hi;
+      b3_chunk_quad(lo, hi, nb, (uint64_t)Q, chunks == 1, (q & 1) != 0, (q & 2) != 0,
+                    [&](int64_t b, uint32_t (&w)[16]) { load(g0 + b, w); });
+      chunk_cv[Q * 8 + q] = lo;
+      chunk_cv[Q * 8 + 4 + q] = hi;
+    }
+    __syncthreads();
+    fold_cvs(chunk_cv, (int)chunks, true, lane);
+    if (lane < 8) reinterpret_cast<uint32_t*>(digest)[lane] = chunk_cv[lane];
+    return;
+  }
   for (int g = 0; g < groups; ++g) {
     const int64_t c = (int64_t)g * 64 + lane;
     const int cnt = (int)(chunks - (int64_t)g * 64 < 64 ? chunks - (int64_t)g * 64 : 64);

@@ -84,6 +84,20 @@ def test_multi_level_hash_trees():
     assert res.digests == oracle_ids(dl, w.dtype)
 
 
+@pytest.mark.parametrize("L", [15, 16, 255, 256, 1100])
+def test_fragment_id_message_lengths(L):
+    # The Id hashes L + 1 blocks: one chunk up to L = 15, at most 16 chunks (one
+    # quad of lanes per chunk) up to L = 255, one lane per chunk past that, and
+    # groups of 64 chunks past L = 1023. Tensors of one chunk, so the Ids come
+    # from the Id kernel alone.
+    w = synth.custom(f"id-L{L}", dtype="float32", d=16, H=1, L=L, lengths=(3, 5, 3),
+                     deliveries=(0, 1, 2, 0), routing_layer=L // 2)
+    _, dl = gpu_deliveries(w)
+    res = _run(w, dl)
+    check_render(res, dl, w.dtype, w.routing_layer, w.rope_base)
+    assert res.n_unique == 3
+
+
 def test_single_fragment_and_all_duplicates():
     w = synth.custom("one", dtype="bfloat16", d=128, H=2, L=2, lengths=(77,), deliveries=(0, 0, 0, 0))
     frags, dl = gpu_deliveries(w)
