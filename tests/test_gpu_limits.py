@@ -8,6 +8,10 @@
   through the one-call paged path, equal the dense render.
 * A page pool whose slices pass 4 GiB, with pages on both sides: the paged
   paths equal the dense render.
+* The most layers a fragment can have (2 L H <= 65535: L = 32767 at H = 1):
+  the Id's message is 32768 blocks, 2048 chunks folded in the Id kernel's 32
+  groups of 64; digests, keys and order against the oracle, and the first,
+  middle and last layers.
 * A tensor past 2 GiB: one layer of 8 heads x 1.2M tokens (2.46 GB for each of
   K and V) next to a 3-token fragment that sorts first, so the long one is
   rotated at offset 3. Keys, Ids, order, and the first, middle and last rows
@@ -131,6 +135,18 @@ def test_paged_pool_past_4gib():
         K = synth.gather_paged(pool, pr.k_table, pr.T_out)[:, 0]
         V = synth.gather_paged(pool, pr.v_table, pr.T_out)[:, 1]
         assert torch.equal(K, res.merged[:, 0]) and torch.equal(V, res.merged[:, 1])
+
+
+def test_most_layers_per_fragment():
+    w = synth.custom("max-L", dtype="float32", d=16, H=1, L=32767, lengths=(2, 3),
+                     deliveries=(0, 1, 0), routing_layer=32766)
+    frags = synth.make_fragments(w, device="cuda")
+    dl = synth.make_deliveries(w, frags)
+    log(f"[limits] L={w.L}: {w.n_deliveries} deliveries of {2 * w.L} tensors")
+    res = cm.render_deliveries(dl, w.routing_layer, w.rope_base)
+    torch.cuda.synchronize()
+    check_render(res, dl, w.dtype, w.routing_layer, w.rope_base, layers=[0, 1, 16383, 32766])
+    assert res.n_unique == 2 and res.T_out == 5
 
 
 def test_tensor_larger_than_2gib():
