@@ -245,8 +245,12 @@ hipError_t launch_order_render_prep(const SetDesc& s, const double* keys, const 
                                     int32_t style, int32_t stripe_blocks, const uint8_t* select,
                                     uint8_t* rws, hipStream_t stream) {
   ScopedTiming tm(K_ORDER, stream);
+  // at least n threads (one per delivery), and enough for about two angle
+  // pairs each (fp64 pow, cos and sin per pair: 31 pairs per thread of 64 took
+  // 43 us on a 32-delivery set)
   int threads = 64;
-  while (threads < s.n) threads <<= 1;
+  while (threads < 1024 && (threads < s.n || (int64_t)threads * 2 < (int64_t)s.n * (s.d / 2)))
+    threads <<= 1;
   hipLaunchKernelGGL(order_render_prep_kernel, dim3(1), dim3(threads), 0, stream, s.table_dev,
                      s.stride, s.n, keys, digests, plan, s.d, 16 / s.esize, style, base,
                      stripe_blocks, (int64_t)s.L, token_bytes_of(s), select,

@@ -87,10 +87,17 @@ __device__ __forceinline__ bool render_tables(
   }
   const int halfd = d >> 1;
   const int ppr = d / ep;                    // pieces per row
+  // theta_j is computed once per column a thread visits (with a block of at
+  // least d / 2 threads, a thread keeps one column for every slot)
+  int tj = -1;
+  double theta = 0.0;
   for (int idx = tid; idx < n_u * halfd; idx += blockDim.x) {
     const int s = idx / halfd;
     const int j = idx - s * halfd;
-    const double theta = pow(base, -(double)(2 * j) / (double)d);
+    if (j != tj) {
+      theta = pow(base, -(double)(2 * j) / (double)d);
+      tj = j;
+    }
     const double phi = (double)plan[CM_PLAN_HEADER + n + s] * theta;
     const int k = stripe_blocks > 0 ? j
                   : style == CM_ROPE_HALF ? angle_slot_half(j / ep, j % ep, ppr >> 1)
