@@ -48,8 +48,8 @@ ROTATE_TARGET = 4 * MALL_BYTES         # replicated and the steps cycle through 
 # source files each timed kernel is built from: a traffic summary is only used
 # while these are unchanged
 KERNEL_SOURCES = {
-    "render_hash": ["render_hash.hip", "fused_geometry.h", "rotate.h", "blake3.h", "chunk_ops.h",
-                    "stream_ops.h", "internal.h"],
+    "render_hash": ["render_hash.hip", "fused_geometry.h", "rotate.h", "blake3.h", "blake3_quad.h",
+                    "chunk_ops.h", "stream_ops.h", "internal.h"],
     "render": ["render.hip", "render_geometry.h", "render_tables.h", "rotate.h", "stream_ops.h",
                "internal.h"],
 }

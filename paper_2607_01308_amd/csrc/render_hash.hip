@@ -24,6 +24,7 @@
 // plus the fp64 rotation.
 #include <type_traits>
 
+#include "blake3_quad.h"
 #include "chunk_ops.h"
 #include "fused_geometry.h"
 #include "rotate.h"
@@ -119,14 +120,22 @@ struct DenseTask {
   uint8_t* dst;           // the lane's current row in the merged cache
   int64_t left, T, gap;
   __device__ __forceinline__ const uint8_t* s(int b) const { return src + b * 64; }
+  // block b of the chunk dl lanes away (the same stripe)
+  __device__ __forceinline__ const uint8_t* s_lane(int b, int dl) const {
+    return src + ((int64_t)dl << 10) + b * 64;
+  }
   __device__ __forceinline__ uint8_t* d(int pos) const { return dst + pos * 64; }
   __device__ __forceinline__ void next_row() { fused_next_row(dst, left, T, gap, RB); }
 };
 
+// QP: stripes of at most 16 chunks are hashed by quads of lanes (the variant
+// for sets whose tensors are all shorter than one stripe).
+template <bool QP>
 struct DenseAddr {
   const int64_t* table;   // per fragment: a row of `stride` int64, tensor pointers from entry 1
   int64_t stride;
   uint8_t* out;
+  static constexpr bool kQuadPartial = QP;
   template <int RB>
   __device__ __forceinline__ DenseTask<RB> task(int64_t i, int64_t t, int64_t sidx, int64_t off,
                                                 int64_t T, int64_t T_out, int32_t H,
@@ -175,6 +184,7 @@ struct PagedAddr {
   const int32_t* k_table;    // merged block -> page, K and V
   const int32_t* v_table;
   uint32_t* lds;             // the block's tables: [waves][2 * RPC][64]
+  static constexpr bool kQuadPartial = false;
   template <int RB>
   __device__ __forceinline__ PagedTask<RB> task(int64_t i, int64_t t, int64_t sidx, int64_t off,
                                                 int64_t T, int64_t, int32_t H, int64_t,
@@ -202,6 +212,29 @@ struct PagedAddr {
     return a;
   }
 };
+
+// The chaining values of a stripe of at most 16 chunks of a dense tensor, by
+// quads of lanes: lanes 4Q .. 4Q + 3 hash chunk Q (b3_chunk_quad), a chain of
+// about half the latency of one lane's. On a small set such stripes are all the
+// work and few waves run. stripe: the stripe's first byte; blocks: the tensor's
+// 64-byte blocks; cvs: the stripe's first chaining value. Out of line: inlined,
+// it makes the 256-byte-row kernel spill.
+__device__ __attribute__((noinline)) void quad_hash_stripe(const uint8_t* stripe, int64_t blocks,
+                                                           int64_t sidx, bool root, uint8_t* cvs,
+                                                           int lane) {
+  const int Q = lane >> 2;
+  const int64_t left = blocks - (sidx * kStripeChunks + Q) * 16;
+  const int nb = left <= 0 ? 0 : (left > 16 ? 16 : (int)left);
+  if (nb == 0) return;                                 // uniform over the quad
+  const uint8_t* c = stripe + ((int64_t)Q << 10);
+  uint32_t lo, hi;
+  b3_chunk_quad(lo, hi, nb, (uint64_t)(sidx * kStripeChunks + Q), root, (lane & 1) != 0,
+                (lane & 2) != 0,
+                [&](int64_t b, uint32_t (&w)[16]) { load_block64(c + b * 64, w); });
+  uint32_t* o = reinterpret_cast<uint32_t*>(cvs + (int64_t)Q * 32);
+  o[lane & 3] = lo;
+  o[4 + (lane & 3)] = hi;
+}
 
 // ESIZE: element bytes; STYLE: pairing; RB: row bytes (64 .. 1024); Addr: the
 // storage of the fragments and of the merged cache.
@@ -259,6 +292,11 @@ __device__ __forceinline__ void render_hash_body(
     const int64_t m = chunks_of(bytes);
     const int64_t in_stripe = (bytes >> 6) - sidx * kStripeBlocks;
     const bool full = in_stripe >= kStripeBlocks;
+    // a last stripe of at most 16 chunks is hashed by quads of lanes in the
+    // kernel variant for sets of short tensors (kept out of the other variants:
+    // the extra code changes their registers and costs the full-stripe loop)
+    constexpr bool kQuadPartial = Addr::kQuadPartial;
+    const bool quad_hash = kQuadPartial && hashing && !full && in_stripe <= 16 * 16;
     const uint64_t chunk = (uint64_t)sidx * kStripeChunks + lane;
     const int64_t blocks_left = (bytes >> 6) - (int64_t)chunk * 16;
     const int nb = blocks_left < 0 ? 0 : (blocks_left > 16 ? 16 : (int)blocks_left);
@@ -456,7 +494,7 @@ __device__ __forceinline__ void render_hash_body(
         const int pos = b & (BPR - 1);
         load_block(x, A.s(b));
         if (ROT && HALF && BPR > 1 && pos >= HBK) load_block(par, A.s(b - HBK));
-        if (hashing) compress_block(st, x, chunk, flags(b, nb - 1));
+        if (hashing && !quad_hash) compress_block(st, x, chunk, flags(b, nb - 1));
         bool out = true;
         if (ROT) {
           if (HALF && BPR > 1) {
@@ -483,6 +521,11 @@ __device__ __forceinline__ void render_hash_body(
     if (!full) {
       if (rotate) partial(std::true_type{});
       else partial(std::false_type{});
+      if constexpr (kQuadPartial) {
+        if (quad_hash)
+          quad_hash_stripe(A.s_lane(0, -lane), bytes >> 6, sidx, m == 1,
+                           nodes + (base0[i] + t * m + (int64_t)sidx * kStripeChunks) * 32, lane);
+      }
     } else if (hashing) {
       if (rotate) full_stripe(std::true_type{}, std::true_type{});
       else full_stripe(std::true_type{}, std::false_type{});
@@ -490,18 +533,19 @@ __device__ __forceinline__ void render_hash_body(
       if (rotate) full_stripe(std::false_type{}, std::true_type{});
       else full_stripe(std::false_type{}, std::false_type{});
     }
-    if (hashing && nb > 0) store_cv(nodes + (base0[i] + t * m + (int64_t)chunk) * 32, st);
+    if (hashing && !quad_hash && nb > 0)
+      store_cv(nodes + (base0[i] + t * m + (int64_t)chunk) * 32, st);
   }
 }
 
-template <int ESIZE, int STYLE, int RB>
+template <int ESIZE, int STYLE, int RB, bool QP = false>
 __global__ __launch_bounds__(kThreads) CM_FUSED_OCCUPANCY void render_hash_kernel(
     const int64_t* __restrict__ table, int64_t stride, int32_t n, const int64_t* __restrict__ plan,
     const int64_t* __restrict__ task_base, const double* __restrict__ angles, int32_t H,
     int32_t d, const uint8_t* __restrict__ select, const int64_t* __restrict__ base0,
     uint8_t* __restrict__ nodes, uint8_t* __restrict__ out) {
-  render_hash_body<ESIZE, STYLE, RB>(DenseAddr{table, stride, out}, n, plan, task_base, angles, H,
-                                     d, select, base0, nodes);
+  render_hash_body<ESIZE, STYLE, RB>(DenseAddr<QP>{table, stride, out}, n, plan, task_base,
+                                     angles, H, d, select, base0, nodes);
 }
 
 // The pool is read (fragment pages) and written (the merged cache's fresh
@@ -560,19 +604,34 @@ hipError_t launch_render_hash(const SetDesc& s, const HashLayout& hlay, const Re
     ScopedTiming tm(K_RENDER_HASH, stream);
     uint8_t* nodes = hws + hlay.off_buf0;
     uint8_t* o = reinterpret_cast<uint8_t*>(out);
+    bool short_tensors = true;
+    for (int i = 0; i < s.n && short_tensors; ++i)
+      short_tensors = s.T(i) * token_bytes_of(s) < kStripeBlocks * 64;
     auto go = [&](auto rbc) {
       constexpr int RB = decltype(rbc)::value;
       auto launch = [&](auto kern) {
         hipLaunchKernelGGL(kern, grid, dim3(kThreads), 0, stream, s.table_dev, s.stride, s.n,
                            plan_dev, tasks, angles, s.H, s.d, hsel, base_tab, nodes, o);
       };
-      if (s.esize == 2) {
-        if (style == CM_ROPE_HALF) launch(render_hash_kernel<2, CM_ROPE_HALF, RB>);
-        else launch(render_hash_kernel<2, CM_ROPE_INTERLEAVED, RB>);
-      } else {
-        if (style == CM_ROPE_HALF) launch(render_hash_kernel<4, CM_ROPE_HALF, RB>);
-        else launch(render_hash_kernel<4, CM_ROPE_INTERLEAVED, RB>);
+      auto pick = [&](auto qpc) {
+        constexpr bool QP = decltype(qpc)::value;
+        if (s.esize == 2) {
+          if (style == CM_ROPE_HALF) launch(render_hash_kernel<2, CM_ROPE_HALF, RB, QP>);
+          else launch(render_hash_kernel<2, CM_ROPE_INTERLEAVED, RB, QP>);
+        } else {
+          if (style == CM_ROPE_HALF) launch(render_hash_kernel<4, CM_ROPE_HALF, RB, QP>);
+          else launch(render_hash_kernel<4, CM_ROPE_INTERLEAVED, RB, QP>);
+        }
+      };
+      // every tensor shorter than one stripe (rows up to 256 bytes): every task
+      // is a tensor's only, partial stripe, hashed by quads of lanes
+      if constexpr (RB <= 256) {
+        if (short_tensors) {
+          pick(std::true_type{});
+          return;
+        }
       }
+      pick(std::false_type{});
     };
     dispatch_row(s.row_bytes, go);
   }
