@@ -131,12 +131,19 @@ __global__ __launch_bounds__(256) void knorm_rows_kernel(Rows src, int64_t tail,
         r -= k * tail;
       }
     }
+    // each level of the butterfly over all kInFlight rows before the next, so
+    // their cross-lane moves overlap instead of forming one long chain
+    double acc[kInFlight];
+#pragma unroll
+    for (int g = 0; g < kInFlight; ++g) acc[g] = valid[g] ? row_chunk_sumsq<ESIZE>(v[g]) : 0.0;
+    for (int o = 1; o < lpr; o <<= 1) {
+#pragma unroll
+      for (int g = 0; g < kInFlight; ++g) acc[g] = acc[g] + __shfl_xor(acc[g], o, 64);
+    }
 #pragma unroll
     for (int g = 0; g < kInFlight; ++g) {
       const int fl = p0 + g * rpp + tid / lpr;
-      double acc = valid[g] ? row_chunk_sumsq<ESIZE>(v[g]) : 0.0;
-      for (int o = 1; o < lpr; o <<= 1) acc = acc + __shfl_xor(acc, o, 64);
-      if (fl < rpb && q == 0) sh[fl] = valid[g] ? sqrt(acc) : 0.0;
+      if (fl < rpb && q == 0) sh[fl] = valid[g] ? sqrt(acc[g]) : 0.0;
     }
   }
   __syncthreads();
