@@ -20,7 +20,22 @@ __device__ __forceinline__ void knorm_fold(const double* __restrict__ parts, int
   const int tid = threadIdx.x;
   const int nt = blockDim.x;
   int w = (int)count;
-  for (int e = tid; e < n * w; e += nt) fa[e] = parts[e];
+  // eight loads in flight per thread before their LDS stores (one workgroup of
+  // as few as 64 threads copies up to 4096 partial sums)
+  const int total = n * w;
+  for (int e0 = tid; e0 < total; e0 += 8 * nt) {
+    double v[8];
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+      const int e = e0 + r * nt;
+      v[r] = e < total ? parts[e] : 0.0;
+    }
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+      const int e = e0 + r * nt;
+      if (e < total) fa[e] = v[r];
+    }
+  }
   __syncthreads();
   double* src = fa;
   double* dst = fb;
