@@ -84,6 +84,24 @@ def test_multi_level_hash_trees():
     assert res.digests == oracle_ids(dl, w.dtype)
 
 
+@pytest.mark.parametrize("style", ["half", "interleaved"])
+@pytest.mark.parametrize("dtype,d,lengths", [
+    # 512 bytes per token: 32 tokens are 16 chunks (hashed by quads), 33 are 17
+    # (one lane per chunk), 127 just under one stripe; every tensor shorter than
+    # a stripe selects the short-tensor variant of the fused kernel
+    ("bfloat16", 128, (32, 33, 127, 1)),
+    ("float32", 64, (1, 16, 17, 63)),
+    # one tensor of exactly one stripe: the other variant, same short stripes
+    ("bfloat16", 128, (32, 128, 5)),
+])
+def test_short_tensor_stripes(dtype, d, lengths, style):
+    w = synth.custom("short", dtype=dtype, d=d, H=2, L=2, lengths=lengths, routing_layer=1,
+                     deliveries=tuple(range(len(lengths))) + (0,))
+    _, dl = gpu_deliveries(w)
+    res = _run(w, dl, style=style)
+    check_render(res, dl, w.dtype, w.routing_layer, w.rope_base, style=style)
+
+
 @pytest.mark.parametrize("L", [15, 16, 255, 256, 1100])
 def test_fragment_id_message_lengths(L):
     # The Id hashes L + 1 blocks: one chunk up to L = 15, at most 16 chunks (one
