@@ -45,9 +45,9 @@ __device__ __forceinline__ int find_fragment(const int64_t* __restrict__ base, i
 
 // base[v][i] = number of level-v nodes of fragments 0..i-1 (all 2L tensors each);
 // base[v][n] = total nodes at level v; row levels+1 holds the same prefix sums
-// of the (tensor, stripe) tasks of the chunk kernel. One workgroup. A one-wave
-// workgroup (n <= 64) gives each row a lane that walks the fragments in order,
-// all rows at once; a wider one runs a block-wide inclusive scan per row.
+// of the (tensor, stripe) tasks of the chunk kernel. One workgroup. For n <= 64
+// each row gets a thread that walks the fragments in order, all rows at once;
+// more fragments take a block-wide inclusive scan per row.
 __device__ __forceinline__ void hash_tables(const int64_t* __restrict__ table, int32_t n,
                                             int64_t stride, int64_t token_bytes, int32_t L,
                                             int32_t levels, int64_t* __restrict__ base,
@@ -55,10 +55,10 @@ __device__ __forceinline__ void hash_tables(const int64_t* __restrict__ table, i
   __shared__ int64_t sc[1024];
   const int tid = threadIdx.x;
   if (tid < n) arrived[tid] = 0;
-  if (blockDim.x == 64) {
+  if (n <= 64) {
     if (tid < n) sc[tid] = table[(int64_t)tid * stride] * token_bytes;
     __syncthreads();
-    for (int v = tid; v <= levels + 1; v += 64) {
+    for (int v = tid; v <= levels + 1; v += (int)blockDim.x) {
       int64_t* row = base + (int64_t)v * (n + 1);
       int64_t acc = 0;
       for (int i = 0; i < n; ++i) {
@@ -106,9 +106,9 @@ __global__ __launch_bounds__(1024) void hash_prep_kernel(const int64_t* __restri
 // into LDS before a table entry is written.
 __global__ __launch_bounds__(1024) void mask_hash_prep_kernel(
     const int64_t* __restrict__ table, int32_t n, int64_t stride, int64_t token_bytes, int32_t L,
-    int32_t levels, const double* parts, int64_t count, double* keys,
-    uint8_t* __restrict__ mask, int64_t* base, int32_t* __restrict__ arrived) {
-  if (count > 1) knorm_fold(parts, n, count, keys);
+    int32_t levels, const double* parts, int64_t count, KnormDirect kd, int32_t H, int32_t d,
+    double* keys, uint8_t* __restrict__ mask, int64_t* base, int32_t* __restrict__ arrived) {
+  knorm_finish(table, stride, n, H, d, kd, parts, count, keys);
   equal_key_mask_body(n, keys, mask);
   hash_tables(table, n, stride, token_bytes, L, levels, base, arrived);
 }
@@ -622,8 +622,10 @@ hipError_t launch_mask_hash_prep(const SetDesc& s, const HashLayout& lay, const 
   // additions do not need them)
   int threads = 64;
   while (threads < s.n) threads <<= 1;
+  if (kp.direct.layer >= 0) threads = 1024;   // the score rows too
   hipLaunchKernelGGL(mask_hash_prep_kernel, dim3(1), dim3(threads), 0, stream, s.table_dev, s.n,
-                     s.stride, token_bytes_of(s), s.L, lay.levels, kp.parts, kp.count, keys, mask,
+                     s.stride, token_bytes_of(s), s.L, lay.levels, kp.parts, kp.count, kp.direct,
+                     s.H, s.d, keys, mask,
                      reinterpret_cast<int64_t*>(ws + lay.off_tables),
                      reinterpret_cast<int32_t*>(ws + lay.off_arrived));
   return hipGetLastError();

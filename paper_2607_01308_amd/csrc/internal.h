@@ -98,10 +98,23 @@ size_t knorm_max_bytes(const SetDesc& s);  // over every legal tail_len
 // Partial sums of the score tree that a one-workgroup kernel finishes
 // (knorm_fold.h): at most this many over the whole set.
 constexpr int64_t kKnormFoldMax = 4096;
+// A set small enough to score inside the one-workgroup kernel that needs the
+// keys (no score launch): layer >= 0 names the routing layer.
+struct KnormDirect {
+  int32_t layer;          // -1: the scores come from the knorm launches
+  int32_t esize;
+  int64_t tail;           // T*
+  int64_t padded;         // leaves per fragment: next power of two >= H * T*
+};
+
 struct KnormPartials {
   const double* parts;    // count per fragment, fragment-major (keys itself if count == 1)
   int64_t count;
+  KnormDirect direct{-1, 0, 0, 0};
 };
+// Largest score tree computed inside the consumer instead of launched: leaves
+// (n * padded) and 16-byte row pieces (at most four passes of 1024 threads).
+constexpr int64_t kKnormDirectPieces = 4096;
 
 struct RenderLayout {
   size_t off_tiles;       // int64 [n+1] work-unit bases per slot (fused hash+render tasks)

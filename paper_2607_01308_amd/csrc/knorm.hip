@@ -14,34 +14,11 @@
 // one-workgroup kernel follows, inside that kernel (knorm_fold.h). Reads only
 // the H*T*d*e tail bytes of one layer per fragment.
 #include "internal.h"
+#include "knorm_fold.h"
 
 namespace cm {
 
 namespace {
-
-template <int ESIZE>
-__device__ __forceinline__ double row_chunk_sumsq(const u32x4 v) {
-  const uint32_t w[4] = {v[0], v[1], v[2], v[3]};
-  if constexpr (ESIZE == 2) {
-    double e[8];
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const double lo = (double)__uint_as_float(w[k] << 16);
-      const double hi = (double)__uint_as_float(w[k] & 0xFFFF0000u);
-      e[2 * k] = lo * lo;
-      e[2 * k + 1] = hi * hi;
-    }
-    return ((e[0] + e[1]) + (e[2] + e[3])) + ((e[4] + e[5]) + (e[6] + e[7]));
-  } else {
-    double e[4];
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const double x = (double)__uint_as_float(w[k]);
-      e[k] = x * x;
-    }
-    return (e[0] + e[1]) + (e[2] + e[3]);
-  }
-}
 
 // In-place level-wise adjacent-pair tree over sh[0..count), count a power of two.
 __device__ __forceinline__ double lds_tree(double* sh, int count) {
@@ -246,6 +223,15 @@ hipError_t knorm_launches(const SetDesc& s, const KnormLayout& lay, Rows src, in
 hipError_t launch_knorm_partial(const SetDesc& s, const KnormLayout& lay, int32_t layer,
                                 int64_t tail_len, double* keys, uint8_t* ws, hipStream_t stream,
                                 int64_t fold_max, KnormPartials* out) {
+  // a small set (Tiny: 64 rows) is scored inside the consumer: no launch
+  const int64_t leaves = (int64_t)s.n * lay.padded;
+  if (fold_max >= kKnormFoldMax && leaves <= kKnormFoldMax &&
+      leaves * (s.row_bytes / 16) <= kKnormDirectPieces) {
+    out->parts = nullptr;
+    out->count = lay.padded;
+    out->direct = KnormDirect{layer, s.esize, tail_len, lay.padded};
+    return hipSuccess;
+  }
   return knorm_launches(s, lay, DenseRows{s.table_dev, s.stride, layer}, tail_len, keys, ws,
                         stream, fold_max, out);
 }

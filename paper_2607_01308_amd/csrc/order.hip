@@ -191,12 +191,12 @@ __global__ __launch_bounds__(1024) void order_render_prep_kernel(
 // gets CM_ESHAPE, and it, like a plan with a non-finite score, is not rendered.
 __global__ __launch_bounds__(1024) void order_set_prep_kernel(
     const int64_t* __restrict__ table, int64_t stride, int32_t n,
-    const double* __restrict__ parts, int64_t count, double* __restrict__ keys,
+    const double* __restrict__ parts, int64_t count, KnormDirect kd, double* __restrict__ keys,
     const uint8_t* __restrict__ digests, int64_t* __restrict__ plan, int64_t T_out, int32_t d,
     int32_t ep, int32_t style, double base, double* __restrict__ angles,
     int64_t* __restrict__ unit_base, int32_t H, int32_t n_lkh, int32_t rb_shift, int64_t units,
     int32_t* __restrict__ unit_slot, int64_t* __restrict__ src_base) {
-  if (count > 1) knorm_fold(parts, n, count, keys);
+  knorm_finish(table, stride, n, H, d, kd, parts, count, keys);
   order_body(table, stride, n, keys, digests, 1, plan);
   __syncthreads();
   bool ok = plan[CM_PLAN_STATUS] == CM_OK;
@@ -265,11 +265,13 @@ hipError_t launch_render_set(const SetDesc& s, const RenderLayout& lay, const Kn
                              double base, int32_t style, void* out, uint8_t* rws,
                              hipStream_t stream) {
   const int64_t units = render_units(s, T_out);
-  const int threads = table_threads(s.n, units + (int64_t)s.n * 2 * s.L * s.H);
+  // the score rows too when the set is scored here
+  const int threads = kp.direct.layer >= 0 ? 1024
+                                           : table_threads(s.n, units + (int64_t)s.n * 2 * s.L * s.H);
   {
     ScopedTiming tm(K_ORDER, stream);
     hipLaunchKernelGGL(order_set_prep_kernel, dim3(1), dim3(threads), 0, stream, s.table_dev,
-                       s.stride, s.n, kp.parts, kp.count, keys, digests, plan, T_out, s.d,
+                       s.stride, s.n, kp.parts, kp.count, kp.direct, keys, digests, plan, T_out, s.d,
                        16 / s.esize, style, base, reinterpret_cast<double*>(rws + lay.off_angles),
                        reinterpret_cast<int64_t*>(rws + lay.off_tiles), s.H, 2 * s.L * s.H,
                        (int32_t)__builtin_ctzll((unsigned long long)s.row_bytes), units,
